@@ -1,0 +1,213 @@
+"""GreedyLore per-step method, fp64, step by step in the paper's order.
+
+TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
+
+Notation (per layer matrix, Algorithm 4 / Appendix D): the caller's matrix is
+m x n; the method works on the oriented form with d = min(m, n) rows and
+D = max(m, n) columns, transposing the gradient when m > n and transposing the
+reconstructed gradient back before the optimizer.  Worker i holds the error
+buffer E^(i) (d x D, zero at start); all workers share U (d x d, identity at
+start) and the weights X (m x n, zero at start in the synthetic workloads).
+
+One step t, following Algorithm 4 with Approx-Top-r (Algorithm 2):
+  1. M^(i) = G^(i) (or G^(i)^T) + E^(i)                      [Alg. 3/4, EF]
+  2. refresh iff t mod tau == 0                               [eq-SVD-P1]
+  3. refresh:  Mbar = mean_i M^(i); U, Sigma = SVD(Mbar); J = {0..r-1}
+     else:     v_j ~ N(0, I_D); lambda_j^(i) = u_j^T M^(i) v_j;
+               lambdabar = mean_i lambda^(i); J = argtop_r(lambdabar^2)
+               ('exact' scores ||u_j^T Mbar||^2 instead, eq-semi-lazy-svd-2)
+  4. P = U[:, J]                                              [eq-semi-lazy-svd-3]
+  5. Q^(i) = P^T M^(i)                                        [eq 8zhb2we09]
+  6. E^(i) = M^(i) - P Q^(i)                                  [eq-ef, Alg. 4]
+  7. Rbar = mean_i Q^(i)                                      [All-Reduce]
+  8. Ghat = P Rbar, transposed back iff m > n                 [Alg. 4]
+  9. optimizer on X with Ghat                                 [eq-msgd / eq-adam]
+With refresh="full" (Algorithm 3) a refresh step instead sets E^(i) = 0 and
+Ghat = Mbar (the uncompressed average).
+
+Readings where the paper is loose (each listed in the design notes):
+  * the residual of Algorithm 3 is written P R^T, dimensionally impossible;
+    Algorithm 4's P R^(i) is used;
+  * Algorithm 4 prints the transpose-back on the m <= n branch; the transpose
+    is undone iff the gradient was transposed (m > n), as its text says;
+  * argtop_r breaks exact ties toward the smaller index; J is kept ascending;
+  * "T iterations" means t = 0..T-1; t = 0 is a refresh;
+  * MSGD is the EMA form with the (1 - beta) factor; Adam has no bias
+    correction and adds eps after the square root.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from .philox import gaussian_vectors
+from .svd import left_svd
+
+# ----------------------------------------------------------------------------
+# building blocks (each pinned in tests/test_oracle_method.py)
+# ----------------------------------------------------------------------------
+
+
+def compress(p, g):
+    """C(G) = P P^T G (eq 2nasdn)."""
+    return p @ (p.T @ g)
+
+
+def argtop_r(score, r):
+    """Indices of the r largest scores (descending; exact ties toward the
+    smaller index), returned in ascending index order (eq-semi-lazy-svd-2)."""
+    score = np.asarray(score, dtype=np.float64)
+    idx = np.arange(score.size)
+    order = np.lexsort((idx, -score))
+    return np.sort(order[: min(r, score.size)])
+
+
+def exact_scores(u, mbar):
+    """||u_j^T Mbar||^2 for every column u_j of U (eq-semi-lazy-svd-2)."""
+    z = u.T @ mbar
+    return np.einsum("ij,ij->i", z, z)
+
+
+def approx_lambdas(u, ms, v):
+    """lambda_j^(i) = u_j^T M^(i) v_j per worker (Algorithm 2), and their mean
+    over workers (eq:lambda-bar).  ms: N x d x D; v: d x D (row j is v_j)."""
+    lam = np.empty((ms.shape[0], u.shape[1]))
+    for i in range(ms.shape[0]):
+        z = u.T @ ms[i]
+        lam[i] = np.einsum("jb,jb->j", z, v)
+    return lam, lam.mean(axis=0)
+
+
+def msgd_update(x, b, ghat, lr, beta):
+    """M_t = beta M_{t-1} + (1 - beta) G_t;  X_{t+1} = X_t - gamma M_t (eq-msgd)."""
+    b = beta * b + (1.0 - beta) * ghat
+    return x - lr * b, b
+
+
+def adam_update(x, m1, m2, ghat, lr, beta1, beta2, eps):
+    """eq-adam: no bias correction; eps added after the square root."""
+    m1 = beta1 * m1 + (1.0 - beta1) * ghat
+    m2 = beta2 * m2 + (1.0 - beta2) * ghat * ghat
+    return x - lr * m1 / (np.sqrt(m2) + eps), m1, m2
+
+
+# ----------------------------------------------------------------------------
+# the per-step driver
+# ----------------------------------------------------------------------------
+
+
+@dataclass
+class MatrixState:
+    m: int
+    n: int
+    e: np.ndarray            # N x d x D (oriented)
+    u: np.ndarray            # d x d
+    x: np.ndarray            # m x n
+    s1: np.ndarray           # MSGD buffer / Adam first moment, m x n
+    s2: np.ndarray | None    # Adam second moment, m x n
+    sigma: np.ndarray | None = None
+
+    @property
+    def right(self) -> bool:
+        return self.m > self.n
+
+
+@dataclass
+class Oracle:
+    shapes: tuple
+    workers: int
+    rank: int
+    tau: int
+    opt: str = "msgd"
+    lr: float = 0.01
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    seed: int = 0
+    refresh: str = "compressed"   # "compressed" (Alg. 4) | "full" (Alg. 3)
+    select: str = "approx"        # "approx" (Alg. 2) | "exact" (eq-semi-lazy-svd-2)
+    svd_tol: float | None = None
+    states: list = field(default_factory=list)
+    t_next: int = 0
+
+    def __post_init__(self):
+        self.states = []
+        for (m, n) in self.shapes:
+            d, D = min(m, n), max(m, n)
+            self.states.append(MatrixState(
+                m=m, n=n,
+                e=np.zeros((self.workers, d, D)),
+                u=np.eye(d),
+                x=np.zeros((m, n)),
+                s1=np.zeros((m, n)),
+                s2=np.zeros((m, n)) if self.opt == "adam" else None,
+            ))
+
+    @classmethod
+    def from_workload(cls, wl, **kw):
+        return cls(shapes=wl.shapes, workers=wl.workers, rank=wl.rank, tau=wl.tau,
+                   opt=wl.opt, lr=wl.lr, beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps,
+                   seed=wl.seed, **kw)
+
+    def step(self, grads, t: int):
+        """One step on every matrix.  grads[l] is N x m x n (any float dtype).
+        Returns one dict of intermediate values per matrix."""
+        if t != self.t_next:
+            raise ValueError(f"steps run in order: expected t={self.t_next}, got {t}")
+        self.t_next += 1
+        return [self._step_one(l, st, np.asarray(g, dtype=np.float64), t)
+                for l, (st, g) in enumerate(zip(self.states, grads))]
+
+    def _step_one(self, l, st: MatrixState, g, t):
+        n_w = self.workers
+        d, D = min(st.m, st.n), max(st.m, st.n)
+        r = min(self.rank, d)
+        gc = np.transpose(g, (0, 2, 1)) if st.right else g        # N x d x D
+        ms = gc + st.e                                            # step 1
+        is_refresh = (t % self.tau) == 0                          # step 2
+        out = {"refresh": is_refresh, "t": t}
+        mbar = ms.sum(axis=0) / n_w
+        out["mbar"] = mbar
+        if is_refresh:                                            # step 3
+            u, sigma, sweeps = left_svd(mbar, tol=self.svd_tol)
+            st.u = u
+            st.sigma = sigma
+            jsel = np.arange(r)
+            out.update(sigma=sigma, sweeps=sweeps)
+        else:
+            if self.select == "approx":
+                v = gaussian_vectors(self.seed, t, l, np.arange(d), D).astype(np.float64)
+                lam_i, lam = approx_lambdas(st.u, ms, v)
+                score = lam * lam
+                out.update(lam=lam, lam_workers=lam_i)
+            else:
+                score = exact_scores(st.u, mbar)
+            jsel = argtop_r(score, r)
+            out["score"] = score
+        p = st.u[:, jsel]                                         # step 4
+        q = np.einsum("ak,iab->ikb", p, ms)                       # step 5
+        rbar = q.sum(axis=0) / n_w                                # step 7
+        if is_refresh and self.refresh == "full":
+            st.e = np.zeros_like(ms)                              # Alg. 3 reset
+            ghat = mbar
+        else:
+            st.e = ms - np.einsum("ak,ikb->iab", p, q)            # step 6
+            ghat = p @ rbar                                       # step 8
+        ghat_mn = ghat.T if st.right else ghat
+        if self.opt == "msgd":                                    # step 9
+            st.x, st.s1 = msgd_update(st.x, st.s1, ghat_mn, self.lr, self.beta1)
+        else:
+            st.x, st.s1, st.s2 = adam_update(st.x, st.s1, st.s2, ghat_mn, self.lr,
+                                             self.beta1, self.beta2, self.eps)
+        out.update(J=jsel, P=p, Q=q, Rbar=rbar, ghat=ghat_mn,
+                   E=st.e.copy(), U=st.u, X=st.x.copy(), s1=st.s1.copy(),
+                   s2=None if st.s2 is None else st.s2.copy())
+        return out
+
+
+def oriented_to_mn(a, m, n):
+    """Map an oriented d x D (or N x d x D) array back to the m x n layout."""
+    if m > n:
+        return np.swapaxes(a, -1, -2)
+    return a
