@@ -1,0 +1,178 @@
+/*
+ * greedylore.h -- C ABI of the MI355X (gfx950) GreedyLore compression step.
+ *
+ * The method is GreedyLore (arXiv 2507.08784): greedy low-rank compression of
+ * the gradients of N data-parallel workers with error feedback and a
+ * semi-lazy SVD subspace.  One call of glr_step performs, for every layer
+ * matrix X in R^{m x n} (problem (1), Section I):
+ *
+ *   error feedback       M^(i) = G^(i) + E^(i)                (Section IV-A, eq-ef)
+ *   worker mean          Mbar  = (1/N) sum_i M^(i)           (All-Reduce of Alg. 3/4)
+ *   subspace             t mod tau == 0: U = complete left singular basis of
+ *                        Mbar, P = first r columns (eq-SVD-P1);
+ *                        otherwise P = r columns of U chosen by Approx-Top-r
+ *                        (Algorithm 2, eq:lambda-bar, eq-semi-lazy-svd-3)
+ *   projection           Q^(i) = P^T M^(i)                    (eq 8zhb2we09)
+ *   residual             E^(i) = M^(i) - P Q^(i)              (Algorithm 4)
+ *   average              Rbar  = (1/N) sum_i Q^(i)           (All-Reduce)
+ *   reconstruction       Ghat  = P Rbar                       (Algorithm 4)
+ *   optimizer            MSGD (eq-msgd) or Adam (eq-adam) on X with Ghat.
+ *
+ * Orientation (Algorithm 4, Appendix D): d = min(m, n), D = max(m, n).  When
+ * m > n the method works on the transposed gradient (right projection); no
+ * buffer is physically transposed: every m x n buffer stays in the caller's
+ * row-major layout.
+ *
+ * The N workers are simulated on one GPU: G holds all N gradients of a
+ * matrix, and the All-Reduce averages are device-side means in a fixed worker
+ * order (deterministic: no floating-point atomics).
+ *
+ * Memory ownership.  The caller owns every device buffer: the weights X, the
+ * gradients G, the state blob and the workspace.  The library never allocates
+ * device memory and never frees caller memory; the handle holds host metadata
+ * only.  Device pointers must be 256-byte aligned and must not alias.
+ *
+ * Streams.  `stream` arguments are hipStream_t values passed as void*; NULL is
+ * the default stream.  glr_step enqueues its kernels on the stream; it blocks
+ * the host only on refresh steps, where it reads the convergence flag of the
+ * Jacobi sweeps (one 4-byte read per sweep).
+ *
+ * Errors.  Every function returns a glr_status and never throws or aborts
+ * across the ABI.  Argument and shape errors are detected before anything is
+ * enqueued and leave the state untouched.  A HIP error returns GLR_ERR_DEVICE
+ * (text via glr_last_error).  Device-side conditions (non-finite gradient
+ * with GLR_CHECK_FINITE, refresh not converged within max_sweeps) are latched
+ * in a status word in the state blob and reported by glr_sync_status.
+ *
+ * Threading.  A handle is not thread-safe; one glr_step may be in flight per
+ * handle; kernels of different handles may share a stream.
+ */
+#ifndef GREEDYLORE_H
+#define GREEDYLORE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GLR_OK = 0,
+  GLR_ERR_INVALID_ARG = 1,      /* null / misaligned pointer, bad enum, bad hyper-parameter */
+  GLR_ERR_SHAPE = 2,            /* non-positive or too large dimensions */
+  GLR_ERR_BUFFER_TOO_SMALL = 3, /* state or workspace smaller than glr_workspace_bytes says */
+  GLR_ERR_STATE = 4,            /* t out of order, or a handle whose state is suspect */
+  GLR_ERR_DEVICE = 5,           /* a HIP call failed */
+  GLR_ERR_NONFINITE = 6,        /* a gradient held NaN/Inf (only with GLR_CHECK_FINITE) */
+  GLR_ERR_NOT_CONVERGED = 7     /* a refresh reached max_sweeps before tol */
+} glr_status;
+
+typedef enum { GLR_MSGD = 0, GLR_ADAM = 1 } glr_opt;
+
+/* Refresh-step semantics.  COMPRESSED follows Algorithm 4 ("the complete
+ * procedure"): refresh steps compress like every other step.  FULL follows
+ * Algorithm 3: at a refresh step Ghat = Mbar (uncompressed) and E^(i) = 0. */
+typedef enum { GLR_REFRESH_COMPRESSED = 0, GLR_REFRESH_FULL = 1 } glr_refresh;
+
+/* Non-refresh selection.  APPROX is Approx-Top-r (Algorithm 2): scores
+ * lambdabar_j^2 with lambdabar_j = u_j^T Mbar v_j and v_j ~ N(0, I_D).
+ * EXACT scores ||u_j^T Mbar||^2 (eq-semi-lazy-svd-2). */
+typedef enum { GLR_SELECT_APPROX = 0, GLR_SELECT_EXACT = 1 } glr_select;
+
+#define GLR_CHECK_FINITE 0x1u  /* scan G for NaN/Inf during the worker mean */
+#define GLR_COLD_START   0x2u  /* start every refresh from U = I instead of the previous U */
+
+typedef struct {
+  int64_t m, n;                /* layer matrix shape, caller's row-major layout */
+} glr_shape;
+
+typedef struct {
+  int32_t num_mats;            /* number of layer matrices, >= 1 */
+  const glr_shape* shapes;     /* host array of num_mats shapes; copied by glr_create */
+  int32_t num_workers;         /* N >= 1 simulated workers */
+  int32_t rank;                /* r >= 1; r >= min(m, n) keeps every direction (E = 0) */
+  int32_t tau;                 /* refresh period >= 1: refresh iff t mod tau == 0 */
+  int32_t opt;                 /* glr_opt */
+  float lr;                    /* gamma > 0 */
+  float beta1;                 /* MSGD momentum beta / Adam beta1, in [0, 1) */
+  float beta2;                 /* Adam beta2 in [0, 1) (ignored for MSGD) */
+  float eps;                   /* Adam epsilon > 0 (ignored for MSGD) */
+  int32_t refresh;             /* glr_refresh */
+  int32_t select;              /* glr_select */
+  uint64_t seed;               /* Philox4x32-10 key of the random vectors v_j */
+  int32_t max_sweeps;          /* bound on Jacobi sweeps per refresh, >= 1 */
+  float tol;                   /* Jacobi stop: max |w_p.w_q| / (|w_p||w_q|) <= tol, in (0, 1) */
+  uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START */
+} glr_config;
+
+/* Byte offsets into the state blob for one matrix (all 256-byte aligned). */
+typedef struct {
+  int64_t m, n, d, D;
+  int32_t right;               /* 1 iff m > n (the method works on G^T) */
+  int32_t r;                   /* effective rank min(rank, d) */
+  uint64_t off_E;              /* N x m x n fp32: error buffers E^(i), worker-major */
+  uint64_t off_Ebar;           /* m x n fp32: mean over workers of E^(i) */
+  uint64_t off_U;              /* d x d fp32: row j holds u_j, the j-th column of U */
+  uint64_t off_sigma;          /* d fp32: singular values of Mbar at the last refresh, descending */
+  uint64_t off_J;              /* r int32: selected columns of U, ascending */
+  uint64_t off_score;          /* d fp32: last selection scores (lambdabar^2 or ||u_j^T Mbar||^2) */
+  uint64_t off_S1;             /* m x n fp32: MSGD buffer M, or Adam first moment M */
+  uint64_t off_S2;             /* m x n fp32: Adam second moment V (0 for MSGD: absent) */
+  uint64_t off_Rbar;           /* r x D fp32: mean over workers of Q^(i) = P^T M^(i) (oriented) */
+  uint64_t off_info;           /* 16 int32: [0] sweeps of the last refresh, [1] converged flag */
+} glr_mat_layout;
+
+typedef struct glr_handle glr_handle;
+
+/* Checks a configuration; pure host, no device call. */
+glr_status glr_validate_config(const glr_config* cfg);
+
+/* Bytes of caller-owned device memory a configuration needs; pure host.
+ * state_bytes: persistent across steps (error buffers, U, optimizer state).
+ * ws_bytes: scratch reused by every step. */
+glr_status glr_workspace_bytes(const glr_config* cfg, size_t* state_bytes, size_t* ws_bytes);
+
+/* Layout of matrix `mat` inside the state blob; pure host. */
+glr_status glr_state_layout(const glr_config* cfg, int32_t mat, glr_mat_layout* out);
+
+/* Creates a handle over caller-owned device buffers d_state (state_bytes) and
+ * d_ws (ws_bytes) on the current HIP device, and enqueues on `stream` the
+ * initial state of Algorithm 3: E^(i) = 0, optimizer state 0, U = I.
+ * The first step to run is t = 0.  *out receives the handle. */
+glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes,
+                      void* d_ws, size_t ws_bytes, void* stream, glr_handle** out);
+
+/* Runs step t on every matrix.  X: host array of num_mats device pointers to
+ * the m x n fp32 weights, updated in place.  G: host array of num_mats device
+ * pointers, each to N contiguous m x n fp32 gradients (worker-major), read
+ * only.  t must be the handle's next step (0, 1, 2, ...). */
+glr_status glr_step(glr_handle* h, float* const* X, const float* const* G,
+                    int64_t t, void* stream);
+
+/* Waits for `stream`, reads and clears the device status word.  Returns
+ * GLR_ERR_NONFINITE (and marks the state suspect) or GLR_ERR_NOT_CONVERGED
+ * (informational; the handle stays usable) or GLR_OK. */
+glr_status glr_sync_status(glr_handle* h, void* stream);
+
+/* Declares the caller-owned state valid again after the caller wrote it
+ * (resume from a saved blob, or a hand-off) and sets the next step to t. */
+glr_status glr_resume(glr_handle* h, int64_t next_t);
+
+/* Next step the handle expects. */
+glr_status glr_next_step(const glr_handle* h, int64_t* next_t);
+
+/* Frees the handle (host memory only). */
+glr_status glr_destroy(glr_handle* h);
+
+const char* glr_status_string(glr_status s);
+
+/* Text of the last error on this handle ("" if none); NULL handle gives the
+ * last error of a failed glr_create on this thread. */
+const char* glr_last_error(const glr_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GREEDYLORE_H */

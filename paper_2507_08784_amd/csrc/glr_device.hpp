@@ -1,0 +1,349 @@
+// Device building blocks for the gfx950 GreedyLore kernels: MFMA wrappers,
+// an LDS-staged fp32 MFMA tile engine with pluggable operand loaders,
+// Philox4x32-10 + Box-Muller, and an LDS bitonic sort.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace glr {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;   // every tiled kernel runs 4 wave64s
+
+// streaming (non-temporal) 16-byte load
+__device__ __forceinline__ float4 load_nt4(const float* p) {
+  const f32x4v v = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// v_mfma_f32_32x32x2_f32:  A 32x2, B 2x32, C 32x32.
+//   A[i][k] from lane i + 32k; B[k][j] from lane j + 32k;
+//   C[i][j] in lane j + 32*((i/4)%2), register (i%4) + 4*(i/8).
+__device__ __forceinline__ f32x16 mfma32(float a, float b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ int mfma32_row(int v, int lane) {
+  return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+// v_mfma_f64_16x16x4_f64:  A 16x4, B 4x16, C 16x16 (fp64).
+//   A[i][k] from lane i + 16k; B[k][j] from lane j + 16k;
+//   C[i][j] in lane j + 16*(i%4), register i/4.
+__device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// Operand loaders.  A loader stages a BK x R slice of one GEMM operand into
+// LDS in k-major order, s[k * P + r], where r runs over the operand's M (for
+// A) or N (for B) dimension.  fetch() issues the global loads into registers,
+// put() writes them to LDS, so that the next slice loads while the current
+// one feeds the MFMAs.
+// ---------------------------------------------------------------------------
+
+// Element (r, k) at base[row(r) * ld + k] (+ base2[...] when fused): the
+// operand is contiguous along k.  Optional row gather through `rows`.
+template <int R, int BK, bool FUSED, bool GATHER>
+struct LoadK {
+  static constexpr int KQ = BK / 4;                 // float4s per row slice
+  static constexpr int NV = (R * KQ + kThreads - 1) / kThreads;
+  const float* base;
+  const float* base2;
+  int64_t ld;
+  int nrows, K;
+  bool vec;
+  int64_t roff[NV];
+  int rl[NV], kq[NV];
+  float4 v[NV];
+
+  __device__ LoadK(const float* b, const float* b2, int64_t ld_, int row0, int nrows_, int K_,
+                   const int* rows) : base(b), base2(b2), ld(ld_), nrows(nrows_), K(K_) {
+    vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & 15) == 0) &&
+          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & 15) == 0));
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int idx = threadIdx.x + kThreads * i;
+      rl[i] = idx / KQ;
+      kq[i] = idx % KQ;
+      int gr = row0 + rl[i];
+      bool ok = (rl[i] < R) && (gr < nrows);
+      if (!ok) { roff[i] = -1; continue; }
+      int64_t pr = GATHER ? (int64_t)rows[gr] : (int64_t)gr;
+      roff[i] = pr * ld;
+    }
+  }
+  __device__ __forceinline__ float ld1(int64_t off) const {
+    float x = base[off];
+    if (FUSED) x += base2[off];
+    return x;
+  }
+  __device__ __forceinline__ void fetch(int k0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int k = k0 + 4 * kq[i];
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (roff[i] >= 0) {
+        int64_t off = roff[i] + k;
+        if (vec && k + 3 < K) {
+          x = *reinterpret_cast<const float4*>(base + off);
+          if (FUSED) {
+            float4 y = *reinterpret_cast<const float4*>(base2 + off);
+            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+          }
+        } else {
+          if (k + 0 < K) x.x = ld1(off + 0);
+          if (k + 1 < K) x.y = ld1(off + 1);
+          if (k + 2 < K) x.z = ld1(off + 2);
+          if (k + 3 < K) x.w = ld1(off + 3);
+        }
+      }
+      v[i] = x;
+    }
+  }
+  template <int P>
+  __device__ __forceinline__ void put(float* s) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (rl[i] >= R) continue;
+      int k = 4 * kq[i];
+      s[(k + 0) * P + rl[i]] = v[i].x;
+      s[(k + 1) * P + rl[i]] = v[i].y;
+      s[(k + 2) * P + rl[i]] = v[i].z;
+      s[(k + 3) * P + rl[i]] = v[i].w;
+    }
+  }
+};
+
+// Element (r, k) at base[k * ld + r] (+ base2): contiguous along r.
+template <int R, int BK, bool FUSED>
+struct LoadR {
+  static constexpr int RQ = R / 4;
+  static constexpr int NV = (BK * RQ + kThreads - 1) / kThreads;
+  const float* base;
+  const float* base2;
+  int64_t ld;
+  int r0, nr, K;
+  bool vec;
+  int kl[NV], rq[NV];
+  float4 v[NV];
+
+  __device__ LoadR(const float* b, const float* b2, int64_t ld_, int r0_, int nr_, int K_)
+      : base(b), base2(b2), ld(ld_), r0(r0_), nr(nr_), K(K_) {
+    vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & 15) == 0) &&
+          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & 15) == 0));
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int idx = threadIdx.x + kThreads * i;
+      kl[i] = idx / RQ;
+      rq[i] = idx % RQ;
+    }
+  }
+  __device__ __forceinline__ float ld1(int64_t off) const {
+    float x = base[off];
+    if (FUSED) x += base2[off];
+    return x;
+  }
+  __device__ __forceinline__ void fetch(int k0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      int k = k0 + kl[i];
+      int r = r0 + 4 * rq[i];
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (kl[i] < BK && k < K) {
+        int64_t off = (int64_t)k * ld + r;
+        if (vec && r + 3 < nr) {
+          x = *reinterpret_cast<const float4*>(base + off);
+          if (FUSED) {
+            float4 y = *reinterpret_cast<const float4*>(base2 + off);
+            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+          }
+        } else {
+          if (r + 0 < nr) x.x = ld1(off + 0);
+          if (r + 1 < nr) x.y = ld1(off + 1);
+          if (r + 2 < nr) x.z = ld1(off + 2);
+          if (r + 3 < nr) x.w = ld1(off + 3);
+        }
+      }
+      v[i] = x;
+    }
+  }
+  template <int P>
+  __device__ __forceinline__ void put(float* s) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (kl[i] >= BK) continue;
+      *reinterpret_cast<float4*>(s + kl[i] * P + 4 * rq[i]) = v[i];
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// MFMA tile engine: C[BM x BN] = A[BM x K] B[K x BN] in fp32 with
+// v_mfma_f32_32x32x2_f32.  4 waves in a WM x WN grid; each wave owns a
+// (BM/WM) x (BN/WN) sub-tile of TM x TN MFMA blocks.  LDS holds one k-major
+// slice per operand; the next slice is prefetched into registers while the
+// current one feeds the MFMAs.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN>
+struct MfmaTile {
+  static constexpr int BK = 32;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int PA = BM + 4, PB = BN + 4;
+  static constexpr int SA = BK * PA, SB = BK * PB;
+  static constexpr int LDS_FLOATS = SA + SB;
+  static_assert(WM * WN == 4, "4 waves");
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "32x32 blocks");
+
+  f32x16 acc[TM][TN];
+  int wm, wn, lane;
+
+  __device__ MfmaTile() {
+    lane = lane_id();
+    wm = wave_id() / WN;
+    wn = wave_id() % WN;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  }
+
+  // tile-relative row / column of accumulator element (tm, tn, v)
+  __device__ __forceinline__ int row(int tm, int v) const {
+    return wm * WTM + tm * 32 + mfma32_row(v, lane);
+  }
+  __device__ __forceinline__ int col(int tn) const { return wn * WTN + tn * 32 + (lane & 31); }
+
+  __device__ __forceinline__ void compute(const float* As, const float* Bs) {
+    const int kh = lane >> 5, l32 = lane & 31;
+#pragma unroll
+    for (int kk = 0; kk < BK / 2; ++kk) {
+      float a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = As[(2 * kk + kh) * PA + wm * WTM + i * 32 + l32];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) b[j] = Bs[(2 * kk + kh) * PB + wn * WTN + j * 32 + l32];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+  }
+
+  template <class LA, class LB>
+  __device__ void run(LA& la, LB& lb, int K, float* smem) {
+    float* As = smem;
+    float* Bs = smem + SA;
+    const int nk = (K + BK - 1) / BK;
+    if (nk == 0) return;
+    la.fetch(0);
+    lb.fetch(0);
+    la.template put<PA>(As);
+    lb.template put<PB>(Bs);
+    __syncthreads();
+    for (int kb = 0; kb < nk; ++kb) {
+      const bool more = kb + 1 < nk;
+      if (more) {
+        la.fetch((kb + 1) * BK);
+        lb.fetch((kb + 1) * BK);
+      }
+      compute(As, Bs);
+      __syncthreads();
+      if (more) {
+        la.template put<PA>(As);
+        lb.template put<PB>(Bs);
+        __syncthreads();
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11) and Box-Muller normals.
+// Element b of v_j (matrix l, step t) comes from counter (b/4, j, l, t) under
+// key (seed lo, seed hi); words (x0,x1) give b = 4c, 4c+1 and (x2,x3) give
+// 4c+2, 4c+3; u(x) = (x >> 9) 2^-23 + 2^-24.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void philox4x32_10(uint32_t& c0, uint32_t& c1, uint32_t& c2, uint32_t& c3,
+                                              uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    const uint32_t a = c0, b = c2;
+    const uint32_t hi_a = __umulhi(0xD2511F53u, a), lo_a = 0xD2511F53u * a;
+    const uint32_t hi_b = __umulhi(0xCD9E8D57u, b), lo_b = 0xCD9E8D57u * b;
+    c0 = hi_b ^ c1 ^ k0;
+    c1 = lo_b;
+    c2 = hi_a ^ c3 ^ k1;
+    c3 = lo_a;
+  }
+}
+
+__device__ __forceinline__ float uniform01(uint32_t x) {
+  return (float)(x >> 9) * 0x1p-23f + 0x1p-24f;
+}
+
+__device__ __forceinline__ void box_muller(uint32_t xa, uint32_t xb, float& z0, float& z1) {
+  const float rho = sqrtf(-2.0f * logf(uniform01(xa)));
+  float s, c;
+  sincospif(2.0f * uniform01(xb), &s, &c);
+  z0 = rho * c;
+  z1 = rho * s;
+}
+
+// the four normals v_j[4c .. 4c+3]
+__device__ __forceinline__ void normals4(uint32_t c, uint32_t j, uint32_t mat, uint32_t t,
+                                         uint32_t k0, uint32_t k1, float z[4]) {
+  uint32_t x0 = c, x1 = j, x2 = mat, x3 = t;
+  philox4x32_10(x0, x1, x2, x3, k0, k1);
+  box_muller(x0, x1, z[0], z[1]);
+  box_muller(x2, x3, z[2], z[3]);
+}
+
+// ---------------------------------------------------------------------------
+// reductions and sorting
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// order-preserving map of a float to uint32 (ascending)
+__device__ __forceinline__ uint32_t float_order(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ascending bitonic sort of n (power of two) 64-bit keys in LDS, whole block
+__device__ inline void bitonic_sort(uint64_t* s, int n) {
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t a = s[i], b = s[ixj];
+          const bool up = (i & k) == 0;
+          if ((a > b) == up) { s[i] = b; s[ixj] = a; }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+}  // namespace glr

@@ -1,0 +1,65 @@
+// Internal interface between the host runtime and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace glr {
+
+constexpr int kJB = 16;   // rows per Jacobi block; a pair holds 2 * kJB rows
+constexpr int kJP = 32;
+
+// Per-refresh control words of the block Jacobi (device memory).
+struct JacCtl {
+  uint32_t converged;
+  uint32_t sweeps;
+  uint32_t sweep_max_bits;   // float bits of the largest pair off-norm this sweep
+  uint32_t pad[13];
+};
+
+// One matrix of the current step, as the kernels see it.
+struct MatView {
+  int64_t m, n, d, D;
+  bool right;                // m > n
+  int r;                     // effective rank
+  int N;                     // workers
+  int mat;                   // matrix index (RNG counter)
+  // state
+  float* E;      float* Ebar;  float* Ut;   float* sigma;  int* J;
+  float* score;  float* S1;    float* S2;   float* Rbar;   int* info;
+  uint32_t* status;
+  // caller buffers
+  float* X;      const float* G;
+  // workspace
+  float* Mbar;   float* Q;     float* lam_part;
+  float* W;      float* Utw;   double* gram_part; float* Vrot; int* skip;
+  JacCtl* ctl;   float* sigma_w; int* perm;
+};
+
+struct OptParams {
+  int opt;                   // 0 MSGD, 1 Adam
+  float lr, beta1, beta2, eps;
+};
+
+// launchers (return the first launch error)
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_eye(float* Ut, int64_t d, hipStream_t s);
+hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s);
+hipError_t launch_sel_scores(const MatView& v, bool approx, uint64_t seed, int64_t t, hipStream_t s);
+hipError_t launch_topr(const MatView& v, hipStream_t s);
+hipError_t launch_iota_J(const MatView& v, hipStream_t s);
+hipError_t launch_proj(const MatView& v, hipStream_t s);
+hipError_t launch_rbar(const MatView& v, hipStream_t s);
+hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s);
+hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s);
+
+// block one-sided Jacobi
+int jac_blocks(int64_t d);
+int jac_seats(int64_t d);
+int jac_slices(int64_t d, int64_t D);
+hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
+hipError_t launch_jac_round(const MatView& v, int round, float tol, hipStream_t s);
+hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
+hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
+
+}  // namespace glr

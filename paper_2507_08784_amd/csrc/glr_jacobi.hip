@@ -1,0 +1,450 @@
+// Refresh step: complete left singular basis U of Mbar (d x D) by block
+// one-sided (Hestenes) Jacobi on the rows of W = U^T Mo.
+//
+// Rows are grouped in blocks of kJB; a round of the round-robin tournament
+// pairs the blocks two by two, and each pair (2 kJB rows) is orthogonalised
+// as a whole:
+//   gram   : the pair Gram W_p W_p^T in fp64 (fp64 MFMA, column slices in
+//            parallel, partial sums per slice)
+//   solve  : cyclic two-sided Jacobi on the 2kJB x 2kJB Gram in LDS (fp64);
+//            its eigenvectors V give the rotation
+//   apply  : rows of [W | U^T] <- V^T rows (fp32 MFMA, in place)
+// A sweep is one tournament (every pair of blocks meets once).  The sweep
+// stops when every pair met in a sweep has  max |w_p.w_q| / (|w_p| |w_q|)
+// <= tol.  The final singular values are the row norms of W, sorted
+// descending (ties keep the lower row first); U^T rows follow the sort.
+#include "glr_device.hpp"
+#include "glr_internal.hpp"
+
+namespace glr {
+
+int jac_blocks(int64_t d) { return (int)((d + kJB - 1) / kJB); }
+int jac_seats(int64_t d) {
+  int nb = jac_blocks(d);
+  return nb + (nb & 1) < 2 ? 2 : nb + (nb & 1);
+}
+// column slices per pair for the Gram, so that pairs x slices fills the chip
+int jac_slices(int64_t d, int64_t D) {
+  int pairs = jac_seats(d) / 2;
+  int64_t s = (512 + pairs - 1) / pairs;
+  int64_t maxs = (D + 255) / 256;
+  if (s > maxs) s = maxs;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+// blocks met by `pair` in `round` of the circle-method tournament on `seats`
+__device__ __forceinline__ void pair_blocks(int round, int pair, int seats, int& bi, int& bj) {
+  const int last = seats - 1;
+  if (pair == 0) {
+    bi = round;
+    bj = last;
+  } else {
+    bi = (round + pair) % last;
+    bj = (round - pair + last) % last;
+  }
+}
+
+__device__ __forceinline__ int64_t pair_row(int lr, int bi, int bj) {
+  return lr < kJB ? (int64_t)bi * kJB + lr : (int64_t)bj * kJB + (lr - kJB);
+}
+
+// ---------------------------------------------------------------------------
+// initialisation: cold (W = Mo, Utw = I) or warm (Utw = Ut, W = Ut Mo)
+// ---------------------------------------------------------------------------
+__global__ void k_jac_copy_cold(const float* __restrict__ Mbar, float* __restrict__ W, int64_t d,
+                                int64_t D, int right) {
+  // W[a][b] = Mo[a][b]: a straight copy (left) or a transpose (right)
+  __shared__ float tile[32][33];
+  const int64_t a0 = (int64_t)blockIdx.y * 32, b0 = (int64_t)blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
+  if (!right) {
+    for (int k = ty; k < 32; k += 8) {
+      int64_t a = a0 + k, b = b0 + tx;
+      if (a < d && b < D) W[a * D + b] = Mbar[a * D + b];
+    }
+    return;
+  }
+  // Mbar is D x d (row b, column a)
+  for (int k = ty; k < 32; k += 8) {
+    int64_t b = b0 + k, a = a0 + tx;
+    tile[k][tx] = (b < D && a < d) ? Mbar[b * d + a] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    int64_t a = a0 + k, b = b0 + tx;
+    if (a < d && b < D) W[a * D + b] = tile[tx][k];
+  }
+}
+
+__global__ void k_copy(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ void k_ctl_reset(JacCtl* ctl) {
+  if (threadIdx.x == 0) {
+    ctl->converged = 0;
+    ctl->sweeps = 0;
+    ctl->sweep_max_bits = 0;
+  }
+}
+
+// W (d x D) = Ut (d x d) Mo (d x D), MFMA tiles 128 x 128
+template <bool RIGHT>
+__global__ void __launch_bounds__(256)
+k_jac_warm(const float* __restrict__ Mbar, const float* __restrict__ Ut, float* __restrict__ W,
+           int64_t d, int64_t D) {
+  using T = MfmaTile<128, 128, 2, 2>;
+  __shared__ __align__(16) float smem[T::LDS_FLOATS];
+  const int n0 = blockIdx.x * 128;  // b
+  const int m0 = blockIdx.y * 128;  // j
+  T tile;
+  LoadK<128, 32, false, false> la(Ut, nullptr, d, m0, (int)d, (int)d, nullptr);
+  if (RIGHT) {
+    LoadK<128, 32, false, false> lb(Mbar, nullptr, d, n0, (int)D, (int)d, nullptr);
+    tile.run(la, lb, (int)d, smem);
+  } else {
+    LoadR<128, 32, false> lb(Mbar, nullptr, D, n0, (int)D, (int)d);
+    tile.run(la, lb, (int)d, smem);
+  }
+#pragma unroll
+  for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < T::TN; ++tn) {
+      const int b = n0 + tile.col(tn);
+      if (b >= D) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int j = m0 + tile.row(tm, v);
+        if (j < d) W[(int64_t)j * D + b] = tile.acc[tm][tn][v];
+      }
+    }
+}
+
+static inline int grid1(int64_t n) {
+  int64_t g = (n + 1023) / 1024;
+  if (g < 1) g = 1;
+  if (g > 8192) g = 8192;
+  return (int)g;
+}
+
+hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s) {
+  hipLaunchKernelGGL(k_ctl_reset, dim3(1), dim3(64), 0, s, v.ctl);
+  if (warm) {
+    hipLaunchKernelGGL(k_copy, dim3(grid1(v.d * v.d)), dim3(256), 0, s, v.Ut, v.Utw, v.d * v.d);
+    dim3 grid((unsigned)((v.D + 127) / 128), (unsigned)((v.d + 127) / 128));
+    if (v.right)
+      hipLaunchKernelGGL(k_jac_warm<true>, grid, dim3(256), 0, s, v.Mbar, v.Ut, v.W, v.d, v.D);
+    else
+      hipLaunchKernelGGL(k_jac_warm<false>, grid, dim3(256), 0, s, v.Mbar, v.Ut, v.W, v.d, v.D);
+  } else {
+    hipError_t e = launch_eye(v.Utw, v.d, s);
+    if (e != hipSuccess) return e;
+    dim3 grid((unsigned)((v.D + 31) / 32), (unsigned)((v.d + 31) / 32));
+    hipLaunchKernelGGL(k_jac_copy_cold, grid, dim3(256), 0, s, v.Mbar, v.W, v.d, v.D, v.right ? 1 : 0);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// one round
+// ---------------------------------------------------------------------------
+// partial pair Gram over one column slice: part[pair][slice][32][32] (fp64)
+__global__ void __launch_bounds__(256)
+k_jac_gram(const float* __restrict__ W, int64_t d, int64_t D, const JacCtl* __restrict__ ctl,
+           int round, int seats, int nb, int slice_cols, double* __restrict__ part) {
+  if (ctl->converged) return;
+  const int pair = blockIdx.x, slice = blockIdx.y, nslices = gridDim.y;
+  int bi, bj;
+  pair_blocks(round, pair, seats, bi, bj);
+  if (bi >= nb && bj >= nb) return;
+  __shared__ float S[64][kJP + 1];
+  const int lane = lane_id(), w = wave_id();
+  const int I = w >> 1, Jb = w & 1;
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  const int64_t c_begin = (int64_t)slice * slice_cols;
+  const int64_t c_end = c_begin + slice_cols < D ? c_begin + slice_cols : D;
+  // loader mapping: lane = column within the 64-column chunk, 8 rows per thread
+  const int cl = threadIdx.x & 63, rb = threadIdx.x >> 6;
+  const float* wrow[8];
+  bool rok[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int64_t grow = pair_row(rb + 4 * i, bi, bj);
+    rok[i] = grow < d;
+    wrow[i] = W + (rok[i] ? grow : 0) * D;
+  }
+  for (int64_t c0 = c_begin; c0 < c_end; c0 += 64) {
+    const int64_t c = c0 + cl;
+    const bool cok = c < c_end;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) S[cl][rb + 4 * i] = (rok[i] && cok) ? wrow[i][c] : 0.f;
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      const int k = 4 * ks + (lane >> 4);
+      const double a = (double)S[k][16 * I + (lane & 15)];
+      const double b = (double)S[k][16 * Jb + (lane & 15)];
+      acc = mfma64(a, b, acc);
+    }
+    __syncthreads();
+  }
+  double* out = part + ((int64_t)pair * nslices + slice) * (kJP * kJP);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int i = 16 * I + 4 * v + (lane >> 4);
+    const int j = 16 * Jb + (lane & 15);
+    out[i * kJP + j] = acc[v];
+  }
+}
+
+// rotation of the pair: eigenvectors of its Gram by cyclic Jacobi (fp64, LDS)
+__global__ void __launch_bounds__(64)
+k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ ctl, int round,
+            int seats, int nb, float tol, float* __restrict__ Vout, int* __restrict__ skip) {
+  if (ctl->converged) return;
+  const int pair = blockIdx.x;
+  int bi, bj;
+  pair_blocks(round, pair, seats, bi, bj);
+  if (bi >= nb && bj >= nb) return;
+  __shared__ double G[kJP][kJP + 1];
+  __shared__ double V[kJP][kJP + 1];
+  __shared__ int pp[kJP / 2], qq[kJP / 2];
+  __shared__ double cs[kJP / 2], sn[kJP / 2];
+  __shared__ double red[64];
+  const int lane = threadIdx.x;
+  const double* src = part + (int64_t)pair * nslices * (kJP * kJP);
+  for (int e = lane; e < kJP * kJP; e += 64) {
+    double s = 0.0;
+    for (int k = 0; k < nslices; ++k) s += src[(int64_t)k * kJP * kJP + e];
+    G[e / kJP][e % kJP] = s;
+    V[e / kJP][e % kJP] = (e / kJP == e % kJP) ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  // largest relative off-diagonal entry before the rotation
+  double mx = 0.0;
+  for (int e = lane; e < kJP * kJP; e += 64) {
+    const int p = e / kJP, q = e % kJP;
+    if (p < q) {
+      const double den = G[p][p] * G[q][q];
+      if (den > 0.0) mx = fmax(mx, fabs(G[p][q]) / sqrt(den));
+    }
+  }
+  red[lane] = mx;
+  __syncthreads();
+  for (int o = 32; o > 0; o >>= 1) {
+    if (lane < o) red[lane] = fmax(red[lane], red[lane + o]);
+    __syncthreads();
+  }
+  const double off0 = red[0];
+  if (lane == 0) atomicMax(&ctl->sweep_max_bits, __float_as_uint((float)off0));
+  if (off0 <= (double)tol) {
+    if (lane == 0) skip[pair] = 1;
+    return;
+  }
+  for (int sweep = 0; sweep < 12; ++sweep) {
+    for (int rd = 0; rd < kJP - 1; ++rd) {
+      if (lane < kJP / 2) {
+        int p, q;
+        const int last = kJP - 1;
+        if (lane == 0) { p = rd; q = last; }
+        else { p = (rd + lane) % last; q = (rd - lane + last) % last; }
+        if (p > q) { int t = p; p = q; q = t; }
+        const double gpq = G[p][q], gpp = G[p][p], gqq = G[q][q];
+        double c = 1.0, s = 0.0;
+        if (gpq != 0.0 && fabs(gpq) > 1e-16 * sqrt(gpp * gqq)) {
+          const double zeta = (gqq - gpp) / (2.0 * gpq);
+          const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + hypot(1.0, zeta));
+          c = 1.0 / sqrt(1.0 + t * t);
+          s = c * t;
+        }
+        pp[lane] = p; qq[lane] = q; cs[lane] = c; sn[lane] = s;
+      }
+      __syncthreads();
+      for (int idx = lane; idx < (kJP / 2) * kJP; idx += 64) {
+        const int k = idx / kJP, x = idx % kJP;
+        const int p = pp[k], q = qq[k];
+        const double c = cs[k], s = sn[k];
+        const double gp = G[p][x], gq = G[q][x];
+        G[p][x] = c * gp - s * gq;
+        G[q][x] = s * gp + c * gq;
+      }
+      __syncthreads();
+      for (int idx = lane; idx < (kJP / 2) * kJP; idx += 64) {
+        const int k = idx / kJP, x = idx % kJP;
+        const int p = pp[k], q = qq[k];
+        const double c = cs[k], s = sn[k];
+        const double gp = G[x][p], gq = G[x][q];
+        G[x][p] = c * gp - s * gq;
+        G[x][q] = s * gp + c * gq;
+        const double vp = V[x][p], vq = V[x][q];
+        V[x][p] = c * vp - s * vq;
+        V[x][q] = s * vp + c * vq;
+      }
+      __syncthreads();
+    }
+    double m2 = 0.0;
+    for (int e = lane; e < kJP * kJP; e += 64) {
+      const int p = e / kJP, q = e % kJP;
+      if (p < q) {
+        const double den = G[p][p] * G[q][q];
+        if (den > 0.0) m2 = fmax(m2, fabs(G[p][q]) / sqrt(den));
+      }
+    }
+    red[lane] = m2;
+    __syncthreads();
+    for (int o = 32; o > 0; o >>= 1) {
+      if (lane < o) red[lane] = fmax(red[lane], red[lane + o]);
+      __syncthreads();
+    }
+    const double done = red[0];
+    __syncthreads();
+    if (done <= 1e-15) break;
+  }
+  float* vo = Vout + (int64_t)pair * kJP * kJP;
+  for (int e = lane; e < kJP * kJP; e += 64) vo[e] = (float)V[e / kJP][e % kJP];
+  if (lane == 0) skip[pair] = 0;
+}
+
+// rows of the pair in [W | Utw] <- V^T rows; chunk of 512 columns per block
+constexpr int JAC_CHUNK = 512;
+
+__global__ void __launch_bounds__(256)
+k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D,
+            const float* __restrict__ Vin, const int* __restrict__ skip,
+            const JacCtl* __restrict__ ctl, int round, int seats, int nb) {
+  if (ctl->converged) return;
+  const int pair = blockIdx.x;
+  if (skip[pair]) return;
+  int bi, bj;
+  pair_blocks(round, pair, seats, bi, bj);
+  if (bi >= nb && bj >= nb) return;
+  const int lane = lane_id(), w = wave_id();
+  const int l32 = lane & 31, kh = lane >> 5;
+  const float* V = Vin + (int64_t)pair * kJP * kJP;
+  // A[i][k] = V^T[i][k] = V[k][i]
+  float a[kJP / 2];
+#pragma unroll
+  for (int kk = 0; kk < kJP / 2; ++kk) a[kk] = V[(2 * kk + kh) * kJP + l32];
+  int64_t brow[kJP / 2];
+#pragma unroll
+  for (int kk = 0; kk < kJP / 2; ++kk) brow[kk] = pair_row(2 * kk + kh, bi, bj);
+  int64_t orow[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) orow[v] = pair_row(mfma32_row(v, lane), bi, bj);
+  const int64_t Dt = D + d;
+  const int64_t c0 = (int64_t)blockIdx.y * JAC_CHUNK;
+  for (int it = 0; it < JAC_CHUNK / 128; ++it) {
+    const int64_t cb = c0 + it * 128 + w * 32;
+    if (cb >= Dt) break;
+    const int64_t c = cb + l32;
+    const bool cok = c < Dt;
+    float* base;
+    int64_t ld, cc;
+    if (c < D) { base = W; ld = D; cc = c; }
+    else { base = Utw; ld = d; cc = c - D; }
+    float b[kJP / 2];
+#pragma unroll
+    for (int kk = 0; kk < kJP / 2; ++kk)
+      b[kk] = (cok && brow[kk] < d) ? base[brow[kk] * ld + cc] : 0.f;
+    f32x16 acc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < kJP / 2; ++kk) acc = mfma32(a[kk], b[kk], acc);
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (cok && orow[v] < d) base[orow[v] * ld + cc] = acc[v];
+  }
+}
+
+hipError_t launch_jac_round(const MatView& v, int round, float tol, hipStream_t s) {
+  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
+  const int nsl = jac_slices(v.d, v.D);
+  const int slice_cols = (int)(((v.D + nsl - 1) / nsl + 63) / 64 * 64);
+  hipLaunchKernelGGL(k_jac_gram, dim3(pairs, nsl), dim3(256), 0, s, v.W, v.d, v.D, v.ctl, round,
+                     seats, nb, slice_cols, v.gram_part);
+  hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(64), 0, s, v.gram_part, nsl, v.ctl, round,
+                     seats, nb, tol, v.Vrot, v.skip);
+  const int64_t Dt = v.D + v.d;
+  hipLaunchKernelGGL(k_jac_apply, dim3(pairs, (unsigned)((Dt + JAC_CHUNK - 1) / JAC_CHUNK)),
+                     dim3(256), 0, s, v.W, v.Utw, v.d, v.D, v.Vrot, v.skip, v.ctl, round, seats, nb);
+  return hipGetLastError();
+}
+
+__global__ void k_jac_check(JacCtl* ctl, float tol) {
+  if (threadIdx.x != 0 || ctl->converged) return;
+  ctl->sweeps += 1;
+  if (__uint_as_float(ctl->sweep_max_bits) <= tol) ctl->converged = 1;
+  ctl->sweep_max_bits = 0;
+}
+
+hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s) {
+  hipLaunchKernelGGL(k_jac_check, dim3(1), dim3(64), 0, s, v.ctl, tol);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// finish: sigma_j = ||W_j|| (fp64 sum), sort descending, permute U^T rows
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+k_rownorm(const float* __restrict__ W, int64_t D, float* __restrict__ sig) {
+  const int64_t j = blockIdx.x;
+  const float* row = W + j * D;
+  double s = 0.0;
+  for (int64_t b = threadIdx.x; b < D; b += blockDim.x) {
+    const double x = row[b];
+    s += x * x;
+  }
+  __shared__ double red[4];
+  s = wave_sum(s);
+  if (lane_id() == 0) red[wave_id()] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) sig[j] = (float)sqrt(red[0] + red[1] + red[2] + red[3]);
+}
+
+__global__ void __launch_bounds__(1024)
+k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ perm) {
+  extern __shared__ __align__(16) unsigned char dyn[];
+  uint64_t* keys = reinterpret_cast<uint64_t*>(dyn);
+  for (int i = threadIdx.x; i < n_pad; i += blockDim.x) {
+    if (i < d) keys[i] = ((uint64_t)(~float_order(sig[i])) << 32) | (uint32_t)i;
+    else keys[i] = ~0ull;
+  }
+  __syncthreads();
+  bitonic_sort(keys, n_pad);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) perm[i] = (int)(keys[i] & 0xFFFFFFFFu);
+}
+
+__global__ void k_permute(const float* __restrict__ Utw, const float* __restrict__ sig_w,
+                          const int* __restrict__ perm, int64_t d, float* __restrict__ Ut,
+                          float* __restrict__ sigma, int* __restrict__ J, int r,
+                          const JacCtl* __restrict__ ctl, int* __restrict__ info,
+                          uint32_t* __restrict__ status, int max_sweeps) {
+  const int64_t k = blockIdx.x;
+  const int64_t src = perm[k];
+  for (int64_t a = threadIdx.x; a < d; a += blockDim.x) Ut[k * d + a] = Utw[src * d + a];
+  if (threadIdx.x == 0) {
+    sigma[k] = sig_w[src];
+    if (k < r) J[k] = (int)k;
+    if (k == 0) {
+      info[0] = (int)ctl->sweeps;
+      info[1] = (int)ctl->converged;
+      if (!ctl->converged) atomicOr(status, 2u);
+    }
+  }
+}
+
+hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s) {
+  hipLaunchKernelGGL(k_rownorm, dim3((unsigned)v.d), dim3(256), 0, s, v.W, v.D, v.sigma_w);
+  int n_pad = 2;
+  while (n_pad < v.d) n_pad <<= 1;
+  hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d,
+                     n_pad, v.perm);
+  hipLaunchKernelGGL(k_permute, dim3((unsigned)v.d), dim3(256), 0, s, v.Utw, v.sigma_w, v.perm, v.d,
+                     v.Ut, v.sigma, v.J, v.r, v.ctl, v.info, v.status, max_sweeps);
+  return hipGetLastError();
+}
+
+}  // namespace glr

@@ -1,0 +1,435 @@
+// Host runtime behind the C ABI in include/greedylore.h: configuration
+// checks, the state / workspace layout, and the launch sequence of one step.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/greedylore.h"
+#include "glr_internal.hpp"
+
+using namespace glr;
+
+namespace {
+
+constexpr uint64_t kAlign = 256;
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+constexpr int64_t kMaxSortDim = 8192;   // LDS sort of d keys
+constexpr int kMaxRank = 1024;
+constexpr int kMaxWorkers = 4096;
+constexpr uint64_t kHeaderBytes = 256;  // device status word + padding
+
+inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+thread_local std::string g_create_error;
+
+struct WsLayout {
+  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_V, off_skip, off_ctl, off_sigw,
+      off_perm, bytes;
+};
+
+struct Dims {
+  int64_t m, n, d, D;
+  int r;
+  bool right;
+};
+
+Dims dims_of(const glr_config* c, int mat) {
+  Dims x;
+  x.m = c->shapes[mat].m;
+  x.n = c->shapes[mat].n;
+  x.d = x.m < x.n ? x.m : x.n;
+  x.D = x.m < x.n ? x.n : x.m;
+  x.r = (int)((int64_t)c->rank < x.d ? (int64_t)c->rank : x.d);
+  x.right = x.m > x.n;
+  return x;
+}
+
+std::string fmt(const char* f, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, f);
+  vsnprintf(buf, sizeof buf, f, ap);
+  va_end(ap);
+  return buf;
+}
+
+glr_status check_config(const glr_config* c, std::string* why) {
+  auto bad = [&](glr_status s, const std::string& m) {
+    if (why) *why = m;
+    return s;
+  };
+  if (!c) return bad(GLR_ERR_INVALID_ARG, "config is NULL");
+  if (c->num_mats < 1) return bad(GLR_ERR_INVALID_ARG, "num_mats must be >= 1");
+  if (!c->shapes) return bad(GLR_ERR_INVALID_ARG, "shapes is NULL");
+  if (c->num_workers < 1 || c->num_workers > kMaxWorkers)
+    return bad(GLR_ERR_INVALID_ARG, fmt("num_workers must be in [1, %d]", kMaxWorkers));
+  if (c->rank < 1) return bad(GLR_ERR_INVALID_ARG, "rank must be >= 1");
+  if (c->tau < 1) return bad(GLR_ERR_INVALID_ARG, "tau must be >= 1");
+  if (c->opt != GLR_MSGD && c->opt != GLR_ADAM) return bad(GLR_ERR_INVALID_ARG, "unknown optimizer");
+  if (!(std::isfinite(c->lr) && c->lr > 0.f)) return bad(GLR_ERR_INVALID_ARG, "lr must be finite and > 0");
+  if (!(c->beta1 >= 0.f && c->beta1 < 1.f)) return bad(GLR_ERR_INVALID_ARG, "beta1 must be in [0, 1)");
+  if (c->opt == GLR_ADAM) {
+    if (!(c->beta2 >= 0.f && c->beta2 < 1.f)) return bad(GLR_ERR_INVALID_ARG, "beta2 must be in [0, 1)");
+    if (!(std::isfinite(c->eps) && c->eps > 0.f)) return bad(GLR_ERR_INVALID_ARG, "eps must be finite and > 0");
+  }
+  if (c->refresh != GLR_REFRESH_COMPRESSED && c->refresh != GLR_REFRESH_FULL)
+    return bad(GLR_ERR_INVALID_ARG, "unknown refresh mode");
+  if (c->select != GLR_SELECT_APPROX && c->select != GLR_SELECT_EXACT)
+    return bad(GLR_ERR_INVALID_ARG, "unknown select mode");
+  if (c->max_sweeps < 1) return bad(GLR_ERR_INVALID_ARG, "max_sweeps must be >= 1");
+  if (!(c->tol > 0.f && c->tol < 1.f)) return bad(GLR_ERR_INVALID_ARG, "tol must be in (0, 1)");
+  if (c->flags & ~(GLR_CHECK_FINITE | GLR_COLD_START)) return bad(GLR_ERR_INVALID_ARG, "unknown flag bits");
+  for (int i = 0; i < c->num_mats; ++i) {
+    const int64_t m = c->shapes[i].m, n = c->shapes[i].n;
+    if (m < 1 || n < 1) return bad(GLR_ERR_SHAPE, fmt("matrix %d: shape %lldx%lld must be positive", i, (long long)m, (long long)n));
+    if (m > kMaxDim || n > kMaxDim) return bad(GLR_ERR_SHAPE, fmt("matrix %d: dimension above 2^30", i));
+    const Dims x = dims_of(c, i);
+    if (x.d > kMaxSortDim)
+      return bad(GLR_ERR_SHAPE, fmt("matrix %d: min(m, n) = %lld exceeds %lld", i, (long long)x.d, (long long)kMaxSortDim));
+    if (x.r > kMaxRank) return bad(GLR_ERR_SHAPE, fmt("matrix %d: effective rank above %d", i, kMaxRank));
+    if ((int64_t)c->num_workers * m * n > ((int64_t)1 << 40))
+      return bad(GLR_ERR_SHAPE, fmt("matrix %d: N*m*n too large", i));
+  }
+  return GLR_OK;
+}
+
+void mat_layout(const glr_config* c, int mat, uint64_t base, glr_mat_layout* L, uint64_t* end) {
+  const Dims x = dims_of(c, mat);
+  const uint64_t N = (uint64_t)c->num_workers, mn = (uint64_t)(x.m * x.n);
+  uint64_t o = base;
+  auto take = [&](uint64_t bytes) {
+    uint64_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L->m = x.m; L->n = x.n; L->d = x.d; L->D = x.D;
+  L->right = x.right ? 1 : 0;
+  L->r = x.r;
+  L->off_E = take(N * mn * 4);
+  L->off_Ebar = take(mn * 4);
+  L->off_U = take((uint64_t)(x.d * x.d) * 4);
+  L->off_sigma = take((uint64_t)x.d * 4);
+  L->off_J = take((uint64_t)x.r * 4);
+  L->off_score = take((uint64_t)x.d * 4);
+  L->off_S1 = take(mn * 4);
+  L->off_S2 = c->opt == GLR_ADAM ? take(mn * 4) : 0;
+  L->off_Rbar = take((uint64_t)x.r * (uint64_t)x.D * 4);
+  L->off_info = take(16 * 4);
+  *end = o;
+}
+
+uint64_t state_bytes_of(const glr_config* c) {
+  uint64_t o = kHeaderBytes;
+  for (int i = 0; i < c->num_mats; ++i) {
+    glr_mat_layout L;
+    mat_layout(c, i, o, &L, &o);
+  }
+  return o;
+}
+
+WsLayout ws_layout(const glr_config* c) {
+  uint64_t mx_mn = 0, mx_Q = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
+  for (int i = 0; i < c->num_mats; ++i) {
+    const Dims x = dims_of(c, i);
+    const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
+    const uint64_t sl = (uint64_t)jac_slices(x.d, x.D);
+    auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
+    mx(mx_mn, (uint64_t)(x.m * x.n));
+    mx(mx_Q, (uint64_t)c->num_workers * (uint64_t)x.r * (uint64_t)x.D);
+    mx(mx_lam, (uint64_t)((x.D + 127) / 128) * (uint64_t)x.d);
+    mx(mx_dD, (uint64_t)(x.d * x.D));
+    mx(mx_dd, (uint64_t)(x.d * x.d));
+    mx(mx_gram, pairs * sl * kJP * kJP);
+    mx(mx_pairs, pairs);
+    mx(mx_d, (uint64_t)x.d);
+  }
+  WsLayout w;
+  uint64_t o = 0;
+  auto take = [&](uint64_t bytes) {
+    uint64_t at = o;
+    o = align_up(o + (bytes ? bytes : 4));
+    return at;
+  };
+  w.off_Mbar = take(mx_mn * 4);
+  w.off_Q = take(mx_Q * 4);
+  w.off_lam = take(mx_lam * 4);
+  w.off_W = take(mx_dD * 4);
+  w.off_Utw = take(mx_dd * 4);
+  w.off_gram = take(mx_gram * 8);
+  w.off_V = take(mx_pairs * kJP * kJP * 4);
+  w.off_skip = take(mx_pairs * 4);
+  w.off_ctl = take(sizeof(JacCtl));
+  w.off_sigw = take(mx_d * 4);
+  w.off_perm = take(mx_d * 4);
+  w.bytes = o;
+  return w;
+}
+
+bool aligned(const void* p) { return ((uintptr_t)p % kAlign) == 0; }
+
+}  // namespace
+
+struct glr_handle {
+  glr_config cfg;
+  std::vector<glr_shape> shapes;
+  std::vector<glr_mat_layout> lay;
+  WsLayout ws;
+  char* state = nullptr;
+  char* work = nullptr;
+  int device = 0;
+  int64_t next_t = 0;
+  bool suspect = false;
+  std::string err;
+};
+
+namespace {
+
+glr_status fail(glr_handle* h, glr_status s, const std::string& m) {
+  if (h) h->err = m; else g_create_error = m;
+  return s;
+}
+
+glr_status hip_fail(glr_handle* h, hipError_t e, const char* where) {
+  if (h) h->suspect = true;
+  return fail(h, GLR_ERR_DEVICE, fmt("%s: %s", where, hipGetErrorString(e)));
+}
+
+MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
+  const glr_mat_layout& L = h->lay[mat];
+  MatView v;
+  v.m = L.m; v.n = L.n; v.d = L.d; v.D = L.D;
+  v.right = L.right != 0;
+  v.r = L.r;
+  v.N = h->cfg.num_workers;
+  v.mat = mat;
+  char* s = h->state;
+  v.E = (float*)(s + L.off_E);
+  v.Ebar = (float*)(s + L.off_Ebar);
+  v.Ut = (float*)(s + L.off_U);
+  v.sigma = (float*)(s + L.off_sigma);
+  v.J = (int*)(s + L.off_J);
+  v.score = (float*)(s + L.off_score);
+  v.S1 = (float*)(s + L.off_S1);
+  v.S2 = L.off_S2 ? (float*)(s + L.off_S2) : nullptr;
+  v.Rbar = (float*)(s + L.off_Rbar);
+  v.info = (int*)(s + L.off_info);
+  v.status = (uint32_t*)s;
+  v.X = X;
+  v.G = G;
+  char* w = h->work;
+  v.Mbar = (float*)(w + h->ws.off_Mbar);
+  v.Q = (float*)(w + h->ws.off_Q);
+  v.lam_part = (float*)(w + h->ws.off_lam);
+  v.W = (float*)(w + h->ws.off_W);
+  v.Utw = (float*)(w + h->ws.off_Utw);
+  v.gram_part = (double*)(w + h->ws.off_gram);
+  v.Vrot = (float*)(w + h->ws.off_V);
+  v.skip = (int*)(w + h->ws.off_skip);
+  v.ctl = (JacCtl*)(w + h->ws.off_ctl);
+  v.sigma_w = (float*)(w + h->ws.off_sigw);
+  v.perm = (int*)(w + h->ws.off_perm);
+  return v;
+}
+
+#define GLR_HIP(h, call)                                 \
+  do {                                                   \
+    hipError_t e_ = (call);                              \
+    if (e_ != hipSuccess) return hip_fail(h, e_, #call); \
+  } while (0)
+
+// Semi-Lazy SVD refresh: complete U of Mbar by block one-sided Jacobi
+glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
+  GLR_HIP(h, launch_jac_init(v, warm, s));
+  const int rounds = jac_seats(v.d) - 1;
+  for (int sw = 0; sw < c.max_sweeps; ++sw) {
+    for (int rd = 0; rd < rounds; ++rd) GLR_HIP(h, launch_jac_round(v, rd, c.tol, s));
+    GLR_HIP(h, launch_jac_check(v, c.tol, s));
+    uint32_t conv = 0;
+    GLR_HIP(h, hipMemcpyAsync(&conv, &v.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
+    GLR_HIP(h, hipStreamSynchronize(s));
+    if (conv) break;
+  }
+  GLR_HIP(h, launch_jac_finish(v, c.max_sweeps, s));
+  return GLR_OK;
+}
+
+glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  MatView v = view_of(h, mat, X, G);
+  const bool refresh = (t % c.tau) == 0;
+  OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
+  GLR_HIP(h, launch_ef_mean(v, (c.flags & GLR_CHECK_FINITE) != 0, s));
+  if (refresh) {
+    glr_status st = refresh_svd(h, v, t, s);
+    if (st != GLR_OK) return st;
+  } else if (v.r < v.d) {
+    GLR_HIP(h, launch_sel_scores(v, c.select == GLR_SELECT_APPROX, c.seed, t, s));
+    GLR_HIP(h, launch_topr(v, s));
+  }
+  GLR_HIP(h, launch_proj(v, s));
+  GLR_HIP(h, launch_rbar(v, s));
+  if (refresh && c.refresh == GLR_REFRESH_FULL)
+    GLR_HIP(h, launch_full_refresh(v, op, s));
+  else
+    GLR_HIP(h, launch_resid_opt(v, op, s));
+  return GLR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+glr_status glr_validate_config(const glr_config* cfg) {
+  std::string why;
+  glr_status s = check_config(cfg, &why);
+  if (s != GLR_OK) g_create_error = why;
+  return s;
+}
+
+glr_status glr_workspace_bytes(const glr_config* cfg, size_t* state_bytes, size_t* ws_bytes) {
+  std::string why;
+  glr_status s = check_config(cfg, &why);
+  if (s != GLR_OK) { g_create_error = why; return s; }
+  if (!state_bytes || !ws_bytes) { g_create_error = "output pointer is NULL"; return GLR_ERR_INVALID_ARG; }
+  *state_bytes = (size_t)state_bytes_of(cfg);
+  *ws_bytes = (size_t)ws_layout(cfg).bytes;
+  return GLR_OK;
+}
+
+glr_status glr_state_layout(const glr_config* cfg, int32_t mat, glr_mat_layout* out) {
+  std::string why;
+  glr_status s = check_config(cfg, &why);
+  if (s != GLR_OK) { g_create_error = why; return s; }
+  if (!out) { g_create_error = "output pointer is NULL"; return GLR_ERR_INVALID_ARG; }
+  if (mat < 0 || mat >= cfg->num_mats) { g_create_error = "matrix index out of range"; return GLR_ERR_INVALID_ARG; }
+  uint64_t o = kHeaderBytes;
+  for (int i = 0; i <= mat; ++i) mat_layout(cfg, i, o, out, &o);
+  return GLR_OK;
+}
+
+glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, void* d_ws,
+                      size_t ws_bytes, void* stream, glr_handle** out) {
+  std::string why;
+  glr_status s = check_config(cfg, &why);
+  if (s != GLR_OK) return fail(nullptr, s, why);
+  if (!out) return fail(nullptr, GLR_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!d_state || !d_ws) return fail(nullptr, GLR_ERR_INVALID_ARG, "state or workspace pointer is NULL");
+  if (!aligned(d_state) || !aligned(d_ws))
+    return fail(nullptr, GLR_ERR_INVALID_ARG, "state and workspace must be 256-byte aligned");
+  const uint64_t need_s = state_bytes_of(cfg);
+  const WsLayout wl = ws_layout(cfg);
+  if (state_bytes < need_s || ws_bytes < wl.bytes)
+    return fail(nullptr, GLR_ERR_BUFFER_TOO_SMALL,
+                fmt("need %llu state bytes and %llu workspace bytes", (unsigned long long)need_s,
+                    (unsigned long long)wl.bytes));
+  glr_handle* h = new (std::nothrow) glr_handle();
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "out of host memory");
+  h->cfg = *cfg;
+  h->shapes.assign(cfg->shapes, cfg->shapes + cfg->num_mats);
+  h->cfg.shapes = h->shapes.data();
+  h->ws = wl;
+  h->state = (char*)d_state;
+  h->work = (char*)d_ws;
+  uint64_t o = kHeaderBytes;
+  h->lay.resize(cfg->num_mats);
+  for (int i = 0; i < cfg->num_mats; ++i) mat_layout(&h->cfg, i, o, &h->lay[i], &o);
+  hipError_t e = hipGetDevice(&h->device);
+  hipStream_t st = (hipStream_t)stream;
+  if (e == hipSuccess) e = launch_fill_zero(d_state, (size_t)need_s, st);
+  for (int i = 0; e == hipSuccess && i < cfg->num_mats; ++i)
+    e = launch_eye((float*)(h->state + h->lay[i].off_U), h->lay[i].d, st);
+  if (e == hipSuccess) e = launch_fill_zero(d_ws, (size_t)wl.bytes, st);
+  if (e != hipSuccess) {
+    std::string m = fmt("glr_create: %s", hipGetErrorString(e));
+    delete h;
+    return fail(nullptr, GLR_ERR_DEVICE, m);
+  }
+  *out = h;
+  return GLR_OK;
+}
+
+glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64_t t, void* stream) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (h->suspect) return fail(h, GLR_ERR_STATE, "state is suspect after an earlier error; call glr_resume");
+  if (t != h->next_t)
+    return fail(h, GLR_ERR_STATE, fmt("steps run in order: expected t=%lld, got %lld", (long long)h->next_t, (long long)t));
+  if (!X || !G) return fail(h, GLR_ERR_INVALID_ARG, "X or G is NULL");
+  for (int i = 0; i < h->cfg.num_mats; ++i) {
+    if (!X[i] || !G[i]) return fail(h, GLR_ERR_INVALID_ARG, fmt("matrix %d: NULL buffer", i));
+    if (!aligned(X[i]) || !aligned(G[i]))
+      return fail(h, GLR_ERR_INVALID_ARG, fmt("matrix %d: buffers must be 256-byte aligned", i));
+  }
+  hipStream_t s = (hipStream_t)stream;
+  for (int i = 0; i < h->cfg.num_mats; ++i) {
+    glr_status st = step_one(h, i, X[i], G[i], t, s);
+    if (st != GLR_OK) return st;
+  }
+  h->next_t = t + 1;
+  return GLR_OK;
+}
+
+glr_status glr_sync_status(glr_handle* h, void* stream) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t word = 0;
+  GLR_HIP(h, hipStreamSynchronize(s));
+  GLR_HIP(h, hipMemcpy(&word, h->state, sizeof word, hipMemcpyDeviceToHost));
+  if (word) {
+    GLR_HIP(h, launch_fill_zero(h->state, 4, s));
+    GLR_HIP(h, hipStreamSynchronize(s));
+  }
+  if (word & 1u) {
+    h->suspect = true;
+    return fail(h, GLR_ERR_NONFINITE, "a gradient held NaN or Inf");
+  }
+  if (word & 2u) return fail(h, GLR_ERR_NOT_CONVERGED, "a refresh reached max_sweeps before tol");
+  return GLR_OK;
+}
+
+glr_status glr_resume(glr_handle* h, int64_t next_t) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (next_t < 0) return fail(h, GLR_ERR_INVALID_ARG, "next_t must be >= 0");
+  h->next_t = next_t;
+  h->suspect = false;
+  h->err.clear();
+  return GLR_OK;
+}
+
+glr_status glr_next_step(const glr_handle* h, int64_t* next_t) {
+  if (!h || !next_t) return GLR_ERR_INVALID_ARG;
+  *next_t = h->next_t;
+  return GLR_OK;
+}
+
+glr_status glr_destroy(glr_handle* h) {
+  delete h;
+  return GLR_OK;
+}
+
+const char* glr_status_string(glr_status s) {
+  switch (s) {
+    case GLR_OK: return "ok";
+    case GLR_ERR_INVALID_ARG: return "invalid argument";
+    case GLR_ERR_SHAPE: return "invalid shape";
+    case GLR_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case GLR_ERR_STATE: return "invalid state";
+    case GLR_ERR_DEVICE: return "device error";
+    case GLR_ERR_NONFINITE: return "non-finite gradient";
+    case GLR_ERR_NOT_CONVERGED: return "refresh not converged";
+  }
+  return "unknown status";
+}
+
+const char* glr_last_error(const glr_handle* h) {
+  return h ? h->err.c_str() : g_create_error.c_str();
+}
+
+}  // extern "C"

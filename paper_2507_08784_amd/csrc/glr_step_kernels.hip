@@ -1,0 +1,512 @@
+// Per-step kernels of the GreedyLore compression path on gfx950:
+//   worker mean with error feedback, Approx-Top-r scores (MFMA GEMM with a
+//   fused Philox/Box-Muller epilogue), top-r selection, projection,
+//   fused residual + worker mean + reconstruction + optimizer.
+#include "glr_device.hpp"
+#include "glr_internal.hpp"
+
+namespace glr {
+
+// ---------------------------------------------------------------------------
+// small utilities
+// ---------------------------------------------------------------------------
+__global__ void k_fill_zero(uint32_t* p, size_t nwords) {
+  size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (; i < nwords; i += stride) p[i] = 0u;
+}
+
+__global__ void k_eye(float* Ut, int64_t d) {
+  int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < d * d; i += stride) Ut[i] = (i / d == i % d) ? 1.0f : 0.0f;
+}
+
+static inline int grid_for(int64_t n, int per_thread = 1) {
+  int64_t g = (n + (int64_t)kThreads * per_thread - 1) / ((int64_t)kThreads * per_thread);
+  if (g < 1) g = 1;
+  if (g > 2048 * 8) g = 2048 * 8;
+  return (int)g;
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  size_t words = bytes / 4;
+  if (!words) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_zero, dim3(grid_for((int64_t)words, 4)), dim3(kThreads), 0, s,
+                     (uint32_t*)p, words);
+  return hipGetLastError();
+}
+
+hipError_t launch_eye(float* Ut, int64_t d, hipStream_t s) {
+  hipLaunchKernelGGL(k_eye, dim3(grid_for(d * d, 4)), dim3(kThreads), 0, s, Ut, d);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// S1 + S2: Mbar = Ebar + (1/N) sum_i G^(i)   (m x n layout; Ebar is the mean
+// of the workers' error buffers left by the previous step)
+// ---------------------------------------------------------------------------
+__global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__ Ebar,
+                          float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status,
+                          int check) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  bool bad = false;
+  if ((mn & 3) == 0) {
+    const int64_t q = mn >> 2;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < q; i += stride) {
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int w = 0; w < N; ++w) {
+        float4 g = load_nt4(G + (int64_t)w * mn + 4 * i);
+        if (check) bad |= !(isfinite(g.x) && isfinite(g.y) && isfinite(g.z) && isfinite(g.w));
+        acc.x += g.x; acc.y += g.y; acc.z += g.z; acc.w += g.w;
+      }
+      float4 e = reinterpret_cast<const float4*>(Ebar)[i];
+      float4 o;
+      o.x = e.x + acc.x / (float)N;
+      o.y = e.y + acc.y / (float)N;
+      o.z = e.z + acc.z / (float)N;
+      o.w = e.w + acc.w / (float)N;
+      reinterpret_cast<float4*>(Mbar)[i] = o;
+    }
+  } else {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
+      float acc = 0.f;
+      for (int w = 0; w < N; ++w) {
+        float g = G[(int64_t)w * mn + i];
+        if (check) bad |= !isfinite(g);
+        acc += g;
+      }
+      Mbar[i] = Ebar[i] + acc / (float)N;
+    }
+  }
+  if (check && bad) atomicOr(status, 1u);
+}
+
+hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
+  const int64_t mn = v.m * v.n;
+  hipLaunchKernelGGL(k_ef_mean, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.G, v.Ebar, v.Mbar,
+                     mn, v.N, v.status, check_finite ? 1 : 0);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// S3b: selection scores.  C[b][j] = sum_a Mo[a][b] Ut[j][a]  (C = Mo^T U,
+// D x d), never stored: the epilogue folds each column j with v_j (approx:
+// lambdabar_j = u_j^T Mbar v_j) or with itself (exact: ||u_j^T Mbar||^2) and
+// writes one partial per 128-row tile: part[tile][j].
+// ---------------------------------------------------------------------------
+constexpr int SEL_BM = 128, SEL_BN = 128;
+
+template <bool RIGHT, bool APPROX>
+__global__ void __launch_bounds__(256)
+k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d, int64_t D,
+             float* __restrict__ part, uint32_t mat, uint32_t tstep, uint32_t key0, uint32_t key1) {
+  using T = MfmaTile<SEL_BM, SEL_BN, 2, 2>;
+  __shared__ __align__(16) float smem[T::LDS_FLOATS];
+  __shared__ float red[2][SEL_BN];
+  const int m0 = blockIdx.y * SEL_BM;   // rows: b in [0, D)
+  const int n0 = blockIdx.x * SEL_BN;   // cols: j in [0, d)
+  T tile;
+  LoadK<SEL_BN, 32, false, false> lb(Ut, nullptr, d, n0, (int)d, (int)d, nullptr);
+  if (RIGHT) {
+    // Mo[a][b] = Mbar[b][a] : A[b][a] contiguous along a
+    LoadK<SEL_BM, 32, false, false> la(Mbar, nullptr, d, m0, (int)D, (int)d, nullptr);
+    tile.run(la, lb, (int)d, smem);
+  } else {
+    // Mo[a][b] = Mbar[a][b] : A[b][a] contiguous along b
+    LoadR<SEL_BM, 32, false> la(Mbar, nullptr, D, m0, (int)D, (int)d);
+    tile.run(la, lb, (int)d, smem);
+  }
+  const int lane = lane_id();
+#pragma unroll
+  for (int tn = 0; tn < T::TN; ++tn) {
+    const int j = n0 + tile.col(tn);
+    float acc = 0.f;
+    if (j < d) {
+#pragma unroll
+      for (int tm = 0; tm < T::TM; ++tm) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int b0 = m0 + tile.row(tm, 4 * g);   // multiple of 4
+          if (b0 >= D) continue;
+          if (APPROX) {
+            float z[4];
+            normals4((uint32_t)(b0 >> 2), (uint32_t)j, mat, tstep, key0, key1, z);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (b0 + e < D) acc += tile.acc[tm][tn][4 * g + e] * z[e];
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float c = tile.acc[tm][tn][4 * g + e];
+              acc += c * c;
+            }
+          }
+        }
+      }
+    }
+    acc += __shfl_xor(acc, 32, 64);
+    if (lane < 32) red[tile.wm][tile.wn * T::WTN + tn * 32 + lane] = acc;
+  }
+  __syncthreads();
+  if (threadIdx.x < SEL_BN) {
+    const int j = n0 + threadIdx.x;
+    if (j < d) part[(int64_t)blockIdx.y * d + j] = red[0][threadIdx.x] + red[1][threadIdx.x];
+  }
+}
+
+// lambdabar / scores from the tile partials, summed in a fixed order
+__global__ void k_sel_finish(const float* __restrict__ part, int ntiles, int64_t d, int approx,
+                             float* __restrict__ score) {
+  int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (j >= d) return;
+  float s = 0.f;
+  for (int t = 0; t < ntiles; ++t) s += part[(int64_t)t * d + j];
+  score[j] = approx ? s * s : s;
+}
+
+hipError_t launch_sel_scores(const MatView& v, bool approx, uint64_t seed, int64_t t, hipStream_t s) {
+  dim3 grid((unsigned)((v.d + SEL_BN - 1) / SEL_BN), (unsigned)((v.D + SEL_BM - 1) / SEL_BM));
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+  const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
+#define GLR_SEL(R, A)                                                                          \
+  hipLaunchKernelGGL((k_sel_scores<R, A>), grid, dim3(kThreads), 0, s, v.Mbar, v.Ut, v.d, v.D, \
+                     v.lam_part, (uint32_t)v.mat, tt, k0, k1)
+  if (v.right) { if (approx) GLR_SEL(true, true); else GLR_SEL(true, false); }
+  else         { if (approx) GLR_SEL(false, true); else GLR_SEL(false, false); }
+#undef GLR_SEL
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_sel_finish, dim3(grid_for(v.d)), dim3(kThreads), 0, s, v.lam_part,
+                     (int)grid.y, v.d, approx ? 1 : 0, v.score);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// argtop_r: descending score, ties to the smaller index; J ascending.
+// One block of 1024 threads; n_pad (power of two) 64-bit keys in LDS.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(1024)
+k_topr(const float* __restrict__ score, int d, int r, int n_pad, int* __restrict__ J) {
+  extern __shared__ __align__(16) unsigned char dyn[];
+  uint64_t* keys = reinterpret_cast<uint64_t*>(dyn);
+  for (int i = threadIdx.x; i < n_pad; i += blockDim.x) {
+    if (i < d) {
+      const uint32_t hi = ~float_order(score[i]);   // descending score
+      keys[i] = ((uint64_t)hi << 32) | (uint32_t)i; // ties: smaller index first
+    } else {
+      keys[i] = ~0ull;
+    }
+  }
+  __syncthreads();
+  bitonic_sort(keys, n_pad);
+  // winners' indices to registers, then reuse the buffer for flags and a scan
+  constexpr int MAXW = 8;   // r <= d <= 8192 = 8 * 1024
+  int win[MAXW];
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q) {
+    const int k = threadIdx.x + q * (int)blockDim.x;
+    win[q] = k < r ? (int)(keys[k] & 0xFFFFFFFFu) : -1;
+  }
+  __syncthreads();
+  int* sel = reinterpret_cast<int*>(dyn);
+  int* scan = sel + n_pad;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) sel[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < MAXW; ++q)
+    if (win[q] >= 0) sel[win[q]] = 1;
+  __syncthreads();
+  const int per = (d + blockDim.x - 1) / blockDim.x;
+  const int lo = threadIdx.x * per;
+  int cnt = 0;
+  for (int i = lo; i < lo + per && i < d; ++i) cnt += sel[i];
+  scan[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int off = 1; off < (int)blockDim.x; off <<= 1) {
+    const int x = (threadIdx.x >= (unsigned)off) ? scan[threadIdx.x - off] : 0;
+    __syncthreads();
+    scan[threadIdx.x] += x;
+    __syncthreads();
+  }
+  int pos = scan[threadIdx.x] - cnt;
+  for (int i = lo; i < lo + per && i < d; ++i)
+    if (sel[i]) J[pos++] = i;
+}
+
+__global__ void k_iota(int* J, int r) {
+  for (int i = threadIdx.x; i < r; i += blockDim.x) J[i] = i;
+}
+
+static int next_pow2(int64_t x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+hipError_t launch_topr(const MatView& v, hipStream_t s) {
+  const int n_pad = next_pow2(v.d < 2 ? 2 : v.d);
+  size_t lds = (size_t)n_pad * 8;
+  if (lds < (size_t)(n_pad + 1024) * 4) lds = (size_t)(n_pad + 1024) * 4;
+  hipLaunchKernelGGL(k_topr, dim3(1), dim3(1024), lds, s, v.score, (int)v.d, v.r, n_pad, v.J);
+  return hipGetLastError();
+}
+
+hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
+  hipLaunchKernelGGL(k_iota, dim3(1), dim3(256), 0, s, v.J, v.r);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// S4: Q^(i) = P^T M^(i), r x D per worker (both orientations), with
+// P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN, bool RIGHT>
+__global__ void __launch_bounds__(256)
+k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
+       const int* __restrict__ J, float* __restrict__ Q, int64_t d, int64_t D, int r) {
+  using T = MfmaTile<BM, BN, WM, WN>;
+  __shared__ __align__(16) float smem[T::LDS_FLOATS];
+  const int n0 = blockIdx.x * BN;   // b
+  const int m0 = blockIdx.y * BM;   // k (rank index)
+  const int w = blockIdx.z;
+  const int64_t dD = d * D;
+  const float* Gi = G + (int64_t)w * dD;
+  const float* Ei = E + (int64_t)w * dD;
+  T tile;
+  LoadK<BM, 32, false, true> la(Ut, nullptr, d, m0, r, (int)d, J);
+  if (RIGHT) {
+    // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
+    LoadK<BN, 32, true, false> lb(Gi, Ei, d, n0, (int)D, (int)d, nullptr);
+    tile.run(la, lb, (int)d, smem);
+  } else {
+    LoadR<BN, 32, true> lb(Gi, Ei, D, n0, (int)D, (int)d);
+    tile.run(la, lb, (int)d, smem);
+  }
+  float* Qi = Q + (int64_t)w * r * D;
+#pragma unroll
+  for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < T::TN; ++tn) {
+      const int b = n0 + tile.col(tn);
+      if (b >= D) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int k = m0 + tile.row(tm, v);
+        if (k < r) Qi[(int64_t)k * D + b] = tile.acc[tm][tn][v];
+      }
+    }
+}
+
+hipError_t launch_proj(const MatView& v, hipStream_t s) {
+  const int r = v.r;
+  dim3 grid;
+  grid.z = v.N;
+#define GLR_PROJ(BM, BN, WM, WN)                                                                  \
+  do {                                                                                            \
+    grid.x = (unsigned)((v.D + BN - 1) / BN);                                                     \
+    grid.y = (unsigned)((r + BM - 1) / BM);                                                       \
+    if (v.right)                                                                                  \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true>), grid, dim3(kThreads), 0, s, v.G, v.E,    \
+                         v.Ut, v.J, v.Q, v.d, v.D, r);                                            \
+    else                                                                                          \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false>), grid, dim3(kThreads), 0, s, v.G, v.E,   \
+                         v.Ut, v.J, v.Q, v.d, v.D, r);                                            \
+  } while (0)
+  if (r <= 32) GLR_PROJ(32, 128, 1, 4);
+  else if (r <= 64) GLR_PROJ(64, 128, 1, 4);
+  else GLR_PROJ(128, 128, 2, 2);
+#undef GLR_PROJ
+  return hipGetLastError();
+}
+
+// S6: Rbar = (1/N) sum_i Q^(i), fixed worker order
+__global__ void k_rbar(const float* __restrict__ Q, int N, int64_t rD, float* __restrict__ Rbar) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < rD; i += stride) {
+    float acc = 0.f;
+    for (int w = 0; w < N; ++w) acc += Q[(int64_t)w * rD + i];
+    Rbar[i] = acc / (float)N;
+  }
+}
+
+hipError_t launch_rbar(const MatView& v, hipStream_t s) {
+  const int64_t rD = (int64_t)v.r * v.D;
+  hipLaunchKernelGGL(k_rbar, dim3(grid_for(rD)), dim3(kThreads), 0, s, v.Q, v.N, rD, v.Rbar);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// S5 + S7 + S8 fused, one pass over the m x n tile:
+//   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
+//   E^(i) <- G^(i) + E^(i) - C^(i);  Ebar = (1/N) sum_i E^(i)
+//   Ghat  = (1/N) sum_i C^(i)  (= P Rbar);  optimizer on X with Ghat.
+// Each wave owns 32 rows x 64 columns; a block stacks 4 waves (128 x 64).
+// ---------------------------------------------------------------------------
+constexpr int RO_ROWS = 128, RO_COLS = 64, RO_TN = 2;
+constexpr int RO_MAX_R = 1024;
+
+template <int OPT, bool RIGHT>
+__global__ void __launch_bounds__(256)
+k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
+            const float* __restrict__ Q, const float* __restrict__ Ut, const int* __restrict__ Jg,
+            float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
+            int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
+  __shared__ int J[RO_MAX_R];
+  for (int k = threadIdx.x; k < r; k += blockDim.x) J[k] = Jg[k];
+  __syncthreads();
+  const int lane = lane_id(), w = wave_id();
+  const int l32 = lane & 31, kh = lane >> 5;
+  const int64_t row_base = (int64_t)blockIdx.y * RO_ROWS + w * 32;
+  const int64_t col_base = (int64_t)blockIdx.x * RO_COLS;
+  const int64_t mn = m * n;
+  // this lane's operand coordinates
+  const int64_t arow = row_base + l32;             // A-operand row (a row of the tile)
+  int64_t bcol[RO_TN];
+#pragma unroll
+  for (int tn = 0; tn < RO_TN; ++tn) bcol[tn] = col_base + tn * 32 + l32;
+
+  // element offsets of this lane's outputs, -1 when out of range
+  int64_t off[RO_TN][16];
+#pragma unroll
+  for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t i = row_base + mfma32_row(v, lane);
+      const int64_t j = col_base + tn * 32 + l32;
+      off[tn][v] = (i < m && j < n) ? i * n + j : -1;
+    }
+
+  float ghat[RO_TN][16], ebar[RO_TN][16];
+#pragma unroll
+  for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) { ghat[tn][v] = 0.f; ebar[tn][v] = 0.f; }
+
+  for (int wk = 0; wk < N; ++wk) {
+    const float* Gi = G + (int64_t)wk * mn;
+    float* Ei = E + (int64_t)wk * mn;
+    const float* Qi = Q + (int64_t)wk * r * D;
+    // prefetch M^(i) = G + E for this tile
+    float mv[RO_TN][16];
+#pragma unroll
+    for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        mv[tn][v] = off[tn][v] >= 0 ? Gi[off[tn][v]] + Ei[off[tn][v]] : 0.f;
+
+    f32x16 acc[RO_TN];
+#pragma unroll
+    for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[tn][v] = 0.f;
+
+#pragma unroll 4
+    for (int k0 = 0; k0 < r; k0 += 2) {
+      const int k = k0 + kh;
+      const bool kok = k < r;
+      float a, b[RO_TN];
+      if (!RIGHT) {
+        // left: rows are a (< d), cols are b (< D):  A = P[a][k] = Ut[J[k]][a], B = Q[k][b]
+        a = (kok && arow < d) ? Ut[(int64_t)J[k] * d + arow] : 0.f;
+#pragma unroll
+        for (int tn = 0; tn < RO_TN; ++tn) b[tn] = (kok && bcol[tn] < D) ? Qi[(int64_t)k * D + bcol[tn]] : 0.f;
+      } else {
+        // right: rows are b (< D), cols are a (< d):  A = Q[k][b], B = P^T[k][a] = Ut[J[k]][a]
+        a = (kok && arow < D) ? Qi[(int64_t)k * D + arow] : 0.f;
+#pragma unroll
+        for (int tn = 0; tn < RO_TN; ++tn) b[tn] = (kok && bcol[tn] < d) ? Ut[(int64_t)J[k] * d + bcol[tn]] : 0.f;
+      }
+#pragma unroll
+      for (int tn = 0; tn < RO_TN; ++tn) acc[tn] = mfma32(a, b[tn], acc[tn]);
+    }
+
+#pragma unroll
+    for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        if (off[tn][v] < 0) continue;
+        const float c = acc[tn][v];
+        const float e = mv[tn][v] - c;
+        Ei[off[tn][v]] = e;
+        ebar[tn][v] += e;
+        ghat[tn][v] += c;
+      }
+  }
+
+  const float fN = (float)N;
+#pragma unroll
+  for (int tn = 0; tn < RO_TN; ++tn)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t o = off[tn][v];
+      if (o < 0) continue;
+      Ebar[o] = ebar[tn][v] / fN;
+      const float gh = ghat[tn][v] / fN;
+      float x = X[o];
+      if (OPT == 0) {
+        const float mm = op.beta1 * S1[o] + (1.0f - op.beta1) * gh;
+        S1[o] = mm;
+        x = x - op.lr * mm;
+      } else {
+        const float m1 = op.beta1 * S1[o] + (1.0f - op.beta1) * gh;
+        const float m2 = op.beta2 * S2[o] + (1.0f - op.beta2) * gh * gh;
+        S1[o] = m1;
+        S2[o] = m2;
+        x = x - op.lr * m1 / (sqrtf(m2) + op.eps);
+      }
+      X[o] = x;
+    }
+}
+
+hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
+  if (v.r > RO_MAX_R) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + RO_ROWS - 1) / RO_ROWS));
+#define GLR_RO(OPT, R)                                                                              \
+  hipLaunchKernelGGL((k_resid_opt<OPT, R>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q,    \
+                     v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
+  if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
+  else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
+#undef GLR_RO
+  return hipGetLastError();
+}
+
+// Algorithm 3 at a refresh step: E^(i) = 0, Ebar = 0, Ghat = Mbar.
+template <int OPT>
+__global__ void k_full_refresh(const float* __restrict__ Mbar, float* __restrict__ E,
+                               float* __restrict__ Ebar, float* __restrict__ X,
+                               float* __restrict__ S1, float* __restrict__ S2, int64_t mn, int N,
+                               OptParams op) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
+    const float gh = Mbar[i];
+    for (int w = 0; w < N; ++w) E[(int64_t)w * mn + i] = 0.f;
+    Ebar[i] = 0.f;
+    float x = X[i];
+    if (OPT == 0) {
+      const float mm = op.beta1 * S1[i] + (1.0f - op.beta1) * gh;
+      S1[i] = mm;
+      x = x - op.lr * mm;
+    } else {
+      const float m1 = op.beta1 * S1[i] + (1.0f - op.beta1) * gh;
+      const float m2 = op.beta2 * S2[i] + (1.0f - op.beta2) * gh * gh;
+      S1[i] = m1;
+      S2[i] = m2;
+      x = x - op.lr * m1 / (sqrtf(m2) + op.eps);
+    }
+    X[i] = x;
+  }
+}
+
+hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s) {
+  const int64_t mn = v.m * v.n;
+  if (o.opt == 0)
+    hipLaunchKernelGGL(k_full_refresh<0>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, v.E,
+                       v.Ebar, v.X, v.S1, v.S2, mn, v.N, o);
+  else
+    hipLaunchKernelGGL(k_full_refresh<1>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, v.E,
+                       v.Ebar, v.X, v.S1, v.S2, mn, v.N, o);
+  return hipGetLastError();
+}
+
+}  // namespace glr

@@ -1,0 +1,100 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the
+same seeded inputs, step by step (relative Frobenius <= 1e-4 per step,
+<= 1e-3 after T steps; J identical at every non-refresh step)."""
+import numpy as np
+import pytest
+
+from oracle.philox import gaussian_vectors
+from synth import get_workload
+from tests.parity import run_parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _print_case(name, **kw):
+    print(f"[parity] {name} {kw}", flush=True)
+
+
+@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left"])
+def test_trajectory_parity(gpu_lib, name):
+    _print_case(name)
+    wl = get_workload(name)
+    log = run_parity(gpu_lib, wl)
+    assert len(log) == wl.steps * len(wl.shapes)
+
+
+def test_many_shapes_vector_case_and_full_rank(gpu_lib):
+    # d = 1 (the vector problem), r >= d, square, both orientations, ragged tiles
+    _print_case("mixed_small")
+    run_parity(gpu_lib, get_workload("mixed_small"))
+
+
+@pytest.mark.parametrize("name", ["one_256x128", "tiny_left"])
+def test_exact_selection_parity(gpu_lib, name):
+    _print_case(name, select="exact")
+    run_parity(gpu_lib, get_workload(name), select="exact")
+
+
+@pytest.mark.parametrize("name", ["one_256x128", "ragged_right"])
+def test_refresh_full_parity(gpu_lib, name):
+    # Algorithm 3: E = 0 and Ghat = Mbar at refresh steps
+    _print_case(name, refresh="full")
+
+    def check(comp, o, t, l, rec):
+        if o["refresh"]:
+            assert float(comp.E(l).abs().max()) == 0.0
+
+    run_parity(gpu_lib, get_workload(name), refresh="full", check=check)
+
+
+def test_cold_start_refresh_parity(gpu_lib):
+    _print_case("tiny_left", cold_start=True)
+    run_parity(gpu_lib, get_workload("tiny_left"), cold_start=True)
+
+
+def test_exact_compression_when_rank_at_most_r(gpu_lib):
+    import torch
+    from synth import planted_matrix
+    wl = get_workload("lowrank_exact")
+    _print_case("lowrank_exact")
+    comp = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr)
+    X = [torch.zeros(m, n, device="cuda") for m, n in wl.shapes]
+    for t in range(wl.steps):
+        G = [torch.from_numpy(np.stack([planted_matrix(wl, l).astype(np.float32)] * wl.workers)).cuda()
+             for l in range(len(wl.shapes))]
+        comp.step(X, G, t)
+        torch.cuda.synchronize()
+        for l in range(len(wl.shapes)):
+            scale = float(G[l].abs().max())
+            assert float(comp.E(l).abs().max()) < 1e-5 * scale
+
+
+def test_selection_scores_are_the_bilinear_forms(gpu_lib):
+    """At a non-refresh step the GPU's scores equal (u_j^T Mbar v_j)^2 for the
+    GPU's own U, with v_j from the specified Philox stream (checked in fp64)."""
+    import torch
+    from oracle.method import Oracle
+    from synth import gradient_batch, planted_matrix
+    wl = get_workload("mid_left")
+    _print_case("mid_left", check="scores")
+    comp = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
+                              seed=wl.seed)
+    orc = Oracle.from_workload(wl)
+    planted = planted_matrix(wl, 0)
+    X = [torch.zeros(*wl.shapes[0], device="cuda")]
+    for t in range(3):
+        g = gradient_batch(wl, 0, t, planted)
+        ut_before = comp.Ut(0).double().cpu().numpy()
+        comp.step(X, [torch.from_numpy(g).cuda()], t)
+        torch.cuda.synchronize()
+        o = orc.step([g], t)[0]
+        if o["refresh"]:
+            continue
+        m, n = wl.shapes[0]
+        d, D = min(m, n), max(m, n)
+        v = gaussian_vectors(wl.seed, t, 0, np.arange(d), D).astype(np.float64)
+        mbar = o["mbar"]
+        lam = np.einsum("ja,ab,jb->j", ut_before, mbar, v)
+        sc = comp.score(0).double().cpu().numpy()
+        scale = np.max(lam ** 2)
+        assert np.abs(sc - lam ** 2).max() < 1e-4 * scale
