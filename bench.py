@@ -1,0 +1,272 @@
+#!/usr/bin/env python3
+"""Benchmark of the GreedyLore compression step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+
+One step is one pass of the whole path over one batch of worker gradients:
+error feedback + worker mean, the semi-lazy subspace (a full Jacobi SVD
+refresh every tau steps, Approx-Top-r selection otherwise), projection,
+residual, mean, reconstruction and the MSGD/Adam update.  Steps t = W .. W+K-1
+of the trajectory are timed (warm-up t = 0 .. W-1 includes the cold first
+refresh), so K a multiple of tau times whole refresh periods.
+
+Inputs are resident in HBM before the timed region: the planted part of the
+synthetic gradients is drawn on the host, the per-step noise on the device
+from a seeded torch generator, into a pool of distinct gradient batches.
+
+Prints one JSON line: ms/step, effective GB/s, the roofline of the dominant
+kernel group (live HIP-event timing on the library's stream), the per-group
+breakdown, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12           # bytes/s
+FP32_MFMA_PEAK = 157.3e12   # flop/s, dense
+FP64_MFMA_PEAK = 78.6e12
+METRIC = "ms/step and effective HBM GB/s for compress+EF+update; % of roofline"
+
+
+def dims(shape):
+    m, n = shape
+    return m, n, min(m, n), max(m, n)
+
+
+def jac_pairs(d, jb=16):
+    nb = (d + jb - 1) // jb
+    seats = max(2, nb + (nb & 1))
+    return seats // 2, seats - 1
+
+
+def group_work(wl, name, launches_per_step=None):
+    """Algorithmic bytes and flops of ONE launch of a kernel group, summed
+    over the matrices of the workload (each group launches once per matrix
+    per step, so per-launch figures are per matrix; we report the mean)."""
+    N = wl.workers
+    byts = flops = flops64 = 0.0
+    for shape in wl.shapes:
+        m, n, d, D = dims(shape)
+        r = min(wl.rank, d)
+        mn = m * n
+        adam = wl.opt == "adam"
+        if name == "ef_mean":
+            byts += 4.0 * (N + 2) * mn
+        elif name == "select":
+            flops += 2.0 * d * d * D
+            byts += 4.0 * (d * D + d * d)
+        elif name == "proj":
+            flops += 2.0 * r * d * D * N
+            byts += 8.0 * N * mn + 4.0 * N * r * D
+        elif name == "resid_opt":
+            flops += 2.0 * r * d * D * N
+            byts += (12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D
+        elif name == "jac_round":
+            pairs, _ = jac_pairs(d)
+            flops64 += pairs * 2.0 * 32 * 32 * D
+            flops += pairs * 2.0 * 32 * 32 * (D + d)
+    k = len(wl.shapes)
+    return byts / k, flops / k, flops64 / k
+
+
+def roofline_entry(wl, name, total_ms, launches):
+    if launches == 0 or total_ms <= 0:
+        return None
+    avg_s = total_ms / 1e3 / launches
+    byts, flops, flops64 = group_work(wl, name)
+    t_hbm = byts / HBM_PEAK
+    t_mfma = flops / FP32_MFMA_PEAK + flops64 / FP64_MFMA_PEAK
+    if t_hbm == 0 and t_mfma == 0:
+        return None
+    if t_hbm >= t_mfma:
+        return {"kernel": name, "bound": "hbm", "achieved": byts / avg_s / 1e9,
+                "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": t_hbm / avg_s,
+                "avg_us": avg_s * 1e6, "launches": launches, "bytes_per_launch": byts,
+                "flops_per_launch": flops + flops64}
+    tot = flops + flops64
+    return {"kernel": name, "bound": "mfma", "achieved": tot / avg_s / 1e12,
+            "peak": tot / t_mfma / 1e12, "unit": "TFLOP/s", "frac": t_mfma / avg_s,
+            "avg_us": avg_s * 1e6, "launches": launches, "bytes_per_launch": byts,
+            "flops_per_launch": tot}
+
+
+def step_bytes(wl):
+    """Algorithmic HBM bytes of one step: per worker read G, read E, write E
+    (12 B/elem) plus the optimizer (16 B/elem MSGD, 24 Adam)."""
+    tot = 0
+    for shape in wl.shapes:
+        m, n, _, _ = dims(shape)
+        tot += (12 * wl.workers + (24 if wl.opt == "adam" else 16)) * m * n
+    return tot
+
+
+def make_pool(wl, pool, device, seed=1234):
+    import numpy as np
+    import torch
+    from synth import noise_level, planted_matrix
+    planted = [torch.from_numpy(planted_matrix(wl, l).astype(np.float32)).to(device)
+               for l in range(len(wl.shapes))]
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    batches = []
+    for _ in range(pool):
+        gs = []
+        for l, (m, n) in enumerate(wl.shapes):
+            g = torch.randn((wl.workers, m, n), generator=gen, device=device, dtype=torch.float32)
+            g.mul_(noise_level(wl, l)).add_(planted[l])
+            gs.append(g)
+        batches.append(gs)
+    return batches
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle (as it stands) on a bounded sample of the same workload.
+
+    Sample: one non-refresh step of the oracle on the full workload (Approx-
+    Top-r with per-worker bilinear forms, projection, residual, optimizer),
+    and one Jacobi sweep on a d' x D slice of the averaged matrix, scaled by
+    (d/d')^2 and by the sweep count of the GPU refresh to estimate a refresh.
+    Returns ms/step averaged over one refresh period."""
+    import numpy as np
+    from oracle.method import Oracle
+    from oracle.svd import left_svd
+    from synth import gradient_batch, planted_matrix
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    grads = [gradient_batch(wl, l, 1, planted_matrix(wl, l)) for l in range(len(wl.shapes))]
+    orc = Oracle.from_workload(wl)
+    orc.t_next = 1
+    t0 = time.perf_counter()
+    orc.step(grads, 1)
+    nonref = time.perf_counter() - t0
+    svd_est = 0.0
+    for l, (m, n) in enumerate(wl.shapes):
+        d, D = min(m, n), max(m, n)
+        g = np.asarray(grads[l], dtype=np.float64).mean(axis=0)
+        mo = g.T if m > n else g
+        dp = min(d, 256)
+        t0 = time.perf_counter()
+        left_svd(mo[:dp], max_sweeps=1)
+        one = time.perf_counter() - t0
+        svd_est += one * (d / dp) ** 2
+    return nonref, svd_est, threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="layer_4096")
+    ap.add_argument("--pool", type=int, default=11)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: the N workers of the method are simulated on one "
+              "GPU, and multi-GPU runs are not part of this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2507_08784_amd as glr
+    from synth import get_workload
+    glr.load()   # no CPU fallback: fails loudly if the library is missing
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    wl = get_workload(args.workload)
+
+    pool_bytes = sum(wl.workers * m * n * 4 for m, n in wl.shapes)
+    pool = max(1, min(args.pool, int(40e9 // pool_bytes)))
+    print(f"[bench] workload {wl.name}: shapes {list(wl.shapes)[:3]}{'...' if len(wl.shapes) > 3 else ''} "
+          f"N={wl.workers} r={wl.rank} tau={wl.tau} opt={wl.opt}; pool {pool}", file=sys.stderr, flush=True)
+    batches = make_pool(wl, pool, dev)
+    comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
+                          beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, device=dev)
+    X = [torch.zeros(m, n, dtype=torch.float32, device=dev) for m, n in wl.shapes]
+    torch.cuda.synchronize()
+
+    t_w = time.perf_counter()
+    for t in range(args.warmup):
+        comp.step(X, batches[t % pool], t)
+    torch.cuda.synchronize()
+    print(f"[bench] warm-up {args.warmup} steps {time.perf_counter() - t_w:.2f}s", file=sys.stderr, flush=True)
+    comp.profile(not args.no_profile)
+    comp.profile_reset()
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, args.warmup + args.steps):
+        comp.step(X, batches[t % pool], t)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    status = comp.sync_status()
+    if status not in (0, 7):
+        raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
+    prof = comp.profile_query() if not args.no_profile else {}
+    sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
+    n_refresh = sum(1 for t in range(args.warmup, args.warmup + args.steps) if t % wl.tau == 0)
+    print(f"[bench] timed {args.steps} steps ({n_refresh} refresh): {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    kernels = []
+    for name in ("ef_mean", "select", "proj", "resid_opt", "jac_round"):
+        if name in prof:
+            e = roofline_entry(wl, name, *prof[name])
+            if e:
+                e["total_ms"] = prof[name][0]
+                kernels.append(e)
+    groups = {k: {"total_ms": v[0], "launches": v[1]} for k, v in prof.items() if v[1]}
+    dominant = max(kernels, key=lambda e: e["total_ms"]) if kernels else None
+    roof = None
+    if dominant:
+        roof = {k: dominant[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
+        roof["kernel"] = dominant["kernel"]
+        roof["traffic"] = None
+
+    eff = step_bytes(wl) / (ms_per_step / 1e3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms/step",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (planted-spectrum gradients + seeded Gaussian noise, resident in HBM)",
+        "config": {"workload": wl.name, "shapes": [list(s) for s in wl.shapes][:4],
+                   "num_matrices": len(wl.shapes), "simulated_workers": wl.workers,
+                   "rank": wl.rank, "tau": wl.tau, "optimizer": wl.opt,
+                   "refresh_steps_timed": n_refresh},
+        "effective_GBps": round(eff, 1),
+        "roofline": roof,
+        "kernels": kernels,
+        "groups": groups,
+        "refresh_sweeps_last": sweeps,
+        "status": glr.STATUS_NAMES.get(status, status),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        nonref, svd_est, threads = cpu_baseline(wl, 30.0)
+        sw = max(1, max(sweeps))
+        ms = (wl.tau * nonref + svd_est * sw) / wl.tau * 1e3
+        out["cpu_baseline"] = {
+            "value": round(ms, 1), "unit": "ms/step", "cores": threads, "kind": "oracle",
+            "sample": (f"one non-refresh oracle step of {wl.name} ({nonref:.2f}s) plus one Jacobi sweep "
+                       f"on a 256-row slice of the averaged matrix scaled by (d/256)^2 x {sw} sweeps "
+                       f"({svd_est * sw:.1f}s per refresh), averaged over tau={wl.tau} steps"),
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -102,7 +102,9 @@ typedef struct {
   int32_t select;              /* glr_select */
   uint64_t seed;               /* Philox4x32-10 key of the random vectors v_j */
   int32_t max_sweeps;          /* bound on Jacobi sweeps per refresh, >= 1 */
-  float tol;                   /* Jacobi stop: max |w_p.w_q| / (|w_p||w_q|) <= tol, in (0, 1) */
+  float tol;                   /* Jacobi stop, in (0, 1): every pair of rows of W = U^T Mbar has
+                                  |w_p.w_q| <= tol max(|w_p|, f) max(|w_q|, f),
+                                  f = (2^-24 / tol) max_k |w_k| */
   uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START */
 } glr_config;
 
@@ -120,7 +122,8 @@ typedef struct {
   uint64_t off_S1;             /* m x n fp32: MSGD buffer M, or Adam first moment M */
   uint64_t off_S2;             /* m x n fp32: Adam second moment V (0 for MSGD: absent) */
   uint64_t off_Rbar;           /* r x D fp32: mean over workers of Q^(i) = P^T M^(i) (oriented) */
-  uint64_t off_info;           /* 16 int32: [0] sweeps of the last refresh, [1] converged flag */
+  uint64_t off_info;           /* 64 int32: [0] sweeps of the last refresh, [1] converged flag,
+                                  [2 + s] float bits of sweep s's largest pair off-norm */
 } glr_mat_layout;
 
 typedef struct glr_handle glr_handle;
@@ -164,6 +167,30 @@ glr_status glr_next_step(const glr_handle* h, int64_t* next_t);
 
 /* Frees the handle (host memory only). */
 glr_status glr_destroy(glr_handle* h);
+
+/* Optional timing of the launch groups of glr_step with HIP events recorded on
+ * the step's stream (off by default; recording adds two events per group).
+ * Groups: see glr_prof_group.  glr_profile_query waits for the last recorded
+ * event and returns the summed milliseconds and the number of timed launches
+ * of one group since the last reset. */
+typedef enum {
+  GLR_PROF_EF_MEAN = 0,      /* worker mean with error feedback */
+  GLR_PROF_SELECT = 1,       /* Approx-Top-r (or exact) scores */
+  GLR_PROF_TOPR = 2,         /* argtop_r */
+  GLR_PROF_PROJ = 3,         /* Q^(i) = P^T M^(i) */
+  GLR_PROF_RBAR = 4,         /* Rbar = mean Q^(i) */
+  GLR_PROF_RESID_OPT = 5,    /* residual + mean + reconstruction + optimizer */
+  GLR_PROF_FULL_REFRESH = 6, /* Algorithm 3 refresh update */
+  GLR_PROF_JAC_INIT = 7,     /* refresh: Jacobi initialisation (warm start product) */
+  GLR_PROF_JAC_ROUND = 8,    /* refresh: one Jacobi round (gram + solve + apply) */
+  GLR_PROF_JAC_FINISH = 9,   /* refresh: norms, sort, permutation */
+  GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
+  GLR_PROF_COUNT = 11
+} glr_prof_group;
+
+glr_status glr_profile_enable(glr_handle* h, int32_t on);
+glr_status glr_profile_reset(glr_handle* h);
+glr_status glr_profile_query(glr_handle* h, int32_t group, double* total_ms, int64_t* launches);
 
 const char* glr_status_string(glr_status s);
 

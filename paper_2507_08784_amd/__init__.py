@@ -27,8 +27,10 @@ COLD_START = 0x2
 EXPORTED = (
     "glr_validate_config", "glr_workspace_bytes", "glr_state_layout", "glr_create", "glr_step",
     "glr_sync_status", "glr_resume", "glr_next_step", "glr_destroy", "glr_status_string",
-    "glr_last_error",
+    "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
 )
+PROF_GROUPS = ("ef_mean", "select", "topr", "proj", "rbar", "resid_opt", "full_refresh",
+               "jac_init", "jac_round", "jac_finish", "refresh")
 
 
 class GlrError(RuntimeError):
@@ -89,6 +91,9 @@ def load():
         "glr_destroy": (I32, [VP]),
         "glr_status_string": (ctypes.c_char_p, [I32]),
         "glr_last_error": (ctypes.c_char_p, [VP]),
+        "glr_profile_enable": (I32, [VP, I32]),
+        "glr_profile_reset": (I32, [VP]),
+        "glr_profile_query": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -100,7 +105,7 @@ def load():
 
 def make_config(shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999,
                 eps=1e-8, refresh="compressed", select="approx", seed=0, max_sweeps=30,
-                tol=1e-7, flags=0):
+                tol=1e-6, flags=0):
     """(Config, keep-alive shape array) for the C ABI."""
     arr = (Shape * len(shapes))(*[Shape(int(m), int(n)) for m, n in shapes])
     cfg = Config(
@@ -141,7 +146,7 @@ class GreedyLore:
 
     def __init__(self, shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999,
                  eps=1e-8, refresh="compressed", select="approx", seed=0, max_sweeps=30,
-                 tol=1e-7, check_finite=False, cold_start=False, device="cuda", stream=None):
+                 tol=1e-6, check_finite=False, cold_start=False, device="cuda", stream=None):
         import torch
         self.lib = load()
         self.torch = torch
@@ -211,6 +216,22 @@ class GreedyLore:
         _check(self.lib.glr_next_step(self.handle, ctypes.byref(t)), self.handle)
         return t.value
 
+    def profile(self, on=True):
+        _check(self.lib.glr_profile_enable(self.handle, 1 if on else 0), self.handle)
+
+    def profile_reset(self):
+        _check(self.lib.glr_profile_reset(self.handle), self.handle)
+
+    def profile_query(self):
+        """{group: (total_ms, launches)} since the last reset."""
+        out = {}
+        for i, name in enumerate(PROF_GROUPS):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            _check(self.lib.glr_profile_query(self.handle, i, ctypes.byref(ms), ctypes.byref(n)),
+                   self.handle)
+            out[name] = (ms.value, n.value)
+        return out
+
     # ------------------------------------------------------------ state views
     def _view(self, off, count, dtype):
         torch = self.torch
@@ -259,7 +280,14 @@ class GreedyLore:
 
     def info(self, mat):
         L = self.layouts[mat]
-        return self._view(L.off_info, 16, self.torch.int32)
+        return self._view(L.off_info, 64, self.torch.int32)
+
+    def sweep_history(self, mat):
+        """(sweeps, converged, [largest pair off-norm of each sweep])."""
+        inf = self.info(mat).cpu()
+        n = int(inf[0])
+        hist = inf[2:2 + min(n, 60)].view(self.torch.float32).tolist()
+        return n, bool(inf[1]), hist
 
     def P(self, mat):
         """d x r: the selected columns of U (P = U[:, J])."""

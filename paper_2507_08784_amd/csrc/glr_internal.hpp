@@ -10,11 +10,16 @@ constexpr int kJB = 16;   // rows per Jacobi block; a pair holds 2 * kJB rows
 constexpr int kJP = 32;
 
 // Per-refresh control words of the block Jacobi (device memory).
+constexpr int kInfoInts = 64;   // per-matrix info block in the state
+constexpr int kHistory = 60;    // sweeps whose off-norm is recorded
+
 struct JacCtl {
   uint32_t converged;
   uint32_t sweeps;
-  uint32_t sweep_max_bits;   // float bits of the largest pair off-norm this sweep
-  uint32_t pad[13];
+  uint32_t sweep_max_bits;     // float bits of the largest pair off-norm this sweep
+  uint32_t pad;
+  uint64_t rowmax2_bits;       // double bits of the largest squared row norm seen
+  uint32_t history[kHistory];  // float bits of each sweep's largest off-norm
 };
 
 // One matrix of the current step, as the kernels see it.
@@ -58,7 +63,7 @@ int jac_blocks(int64_t d);
 int jac_seats(int64_t d);
 int jac_slices(int64_t d, int64_t D);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
-hipError_t launch_jac_round(const MatView& v, int round, float tol, hipStream_t s);
+hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inner, hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
 

@@ -6,12 +6,12 @@
 // as a whole:
 //   gram   : the pair Gram W_p W_p^T in fp64 (fp64 MFMA, column slices in
 //            parallel, partial sums per slice)
-//   solve  : cyclic two-sided Jacobi on the 2kJB x 2kJB Gram in LDS (fp64);
-//            its eigenvectors V give the rotation
-//   apply  : rows of [W | U^T] <- V^T rows (fp32 MFMA, in place)
-// A sweep is one tournament (every pair of blocks meets once).  The sweep
-// stops when every pair met in a sweep has  max |w_p.w_q| / (|w_p| |w_q|)
-// <= tol.  The final singular values are the row norms of W, sorted
+//   solve  : cyclic two-sided Jacobi on the 2kJB x 2kJB Gram in LDS (fp64)
+//            gives its eigenvectors V
+//   apply  : rows of [W | U^T] <- V^T rows, in place, as w + (V - I)^T w
+//            (fp32 MFMA)
+// A sweep is one tournament (every pair of blocks meets once).  The sweeps
+// stop when every pair met in a sweep passes the measure of k_jac_solve.  The final singular values are the row norms of W, sorted
 // descending (ties keep the lower row first); U^T rows follow the sort.
 #include "glr_device.hpp"
 #include "glr_internal.hpp"
@@ -26,8 +26,8 @@ int jac_seats(int64_t d) {
 // column slices per pair for the Gram, so that pairs x slices fills the chip
 int jac_slices(int64_t d, int64_t D) {
   int pairs = jac_seats(d) / 2;
-  int64_t s = (512 + pairs - 1) / pairs;
-  int64_t maxs = (D + 255) / 256;
+  int64_t s = (1024 + pairs - 1) / pairs;
+  int64_t maxs = (D + 127) / 128;
   if (s > maxs) s = maxs;
   if (s < 1) s = 1;
   return (int)s;
@@ -87,6 +87,7 @@ __global__ void k_ctl_reset(JacCtl* ctl) {
     ctl->converged = 0;
     ctl->sweeps = 0;
     ctl->sweep_max_bits = 0;
+    ctl->rowmax2_bits = 0;
   }
 }
 
@@ -148,7 +149,8 @@ hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// one round
+// one round: gram (partial pair Grams over column slices), solve (one block
+// per pair), apply (column chunks of every pair)
 // ---------------------------------------------------------------------------
 // partial pair Gram over one column slice: part[pair][slice][32][32] (fp64)
 __global__ void __launch_bounds__(256)
@@ -175,12 +177,19 @@ k_jac_gram(const float* __restrict__ W, int64_t d, int64_t D, const JacCtl* __re
     rok[i] = grow < d;
     wrow[i] = W + (rok[i] ? grow : 0) * D;
   }
-  for (int64_t c0 = c_begin; c0 < c_end; c0 += 64) {
+  float x[8];
+  auto fetch = [&](int64_t c0) {
     const int64_t c = c0 + cl;
     const bool cok = c < c_end;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) S[cl][rb + 4 * i] = (rok[i] && cok) ? wrow[i][c] : 0.f;
+    for (int i = 0; i < 8; ++i) x[i] = (rok[i] && cok) ? wrow[i][c] : 0.f;
+  };
+  if (c_begin < c_end) fetch(c_begin);
+  for (int64_t c0 = c_begin; c0 < c_end; c0 += 64) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) S[cl][rb + 4 * i] = x[i];
     __syncthreads();
+    if (c0 + 64 < c_end) fetch(c0 + 64);
 #pragma unroll
     for (int ks = 0; ks < 16; ++ks) {
       const int k = 4 * ks + (lane >> 4);
@@ -199,117 +208,114 @@ k_jac_gram(const float* __restrict__ W, int64_t d, int64_t D, const JacCtl* __re
   }
 }
 
-// rotation of the pair: eigenvectors of its Gram by cyclic Jacobi (fp64, LDS)
-__global__ void __launch_bounds__(64)
+constexpr int JAC_CHUNK = 512;   // columns of [W | Utw] rotated by one block
+
+// Eigenvectors V of the pair Gram by cyclic two-sided Jacobi in LDS (fp64).
+// Convergence measure of a pair (p, q):
+//   |w_p . w_q| / (max(|w_p|, f) max(|w_q|, f)),   f = eta * max_k |w_k|,
+// with eta = 2^-24 / tol: rows above the floor f are orthogonalised to a
+// relative tolerance tol; below it, to the absolute level 2^-24 max_k |w_k|
+// that fp32 data resolves (a backward error at fp32 rounding).
+__global__ void __launch_bounds__(256)
 k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ ctl, int round,
-            int seats, int nb, float tol, float* __restrict__ Vout, int* __restrict__ skip) {
+            int seats, int nb, float tol, int max_inner, float* __restrict__ Vout,
+            int* __restrict__ skip) {
   if (ctl->converged) return;
   const int pair = blockIdx.x;
   int bi, bj;
   pair_blocks(round, pair, seats, bi, bj);
   if (bi >= nb && bj >= nb) return;
-  __shared__ double G[kJP][kJP + 1];
-  __shared__ double V[kJP][kJP + 1];
-  __shared__ int pp[kJP / 2], qq[kJP / 2];
-  __shared__ double cs[kJP / 2], sn[kJP / 2];
-  __shared__ double red[64];
-  const int lane = threadIdx.x;
+  __shared__ double Gb[2][kJP][kJP + 1];
+  __shared__ double Vb[2][kJP][kJP + 1];
+  __shared__ double cx[kJP], sx[kJP];
+  __shared__ int px[kJP];
+  __shared__ double red[4];
+  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const double* src = part + (int64_t)pair * nslices * (kJP * kJP);
-  for (int e = lane; e < kJP * kJP; e += 64) {
+  double dmax = 0.0;
+  for (int e = tid; e < kJP * kJP; e += 256) {
     double s = 0.0;
     for (int k = 0; k < nslices; ++k) s += src[(int64_t)k * kJP * kJP + e];
-    G[e / kJP][e % kJP] = s;
-    V[e / kJP][e % kJP] = (e / kJP == e % kJP) ? 1.0 : 0.0;
+    Gb[0][e / kJP][e % kJP] = s;
+    Vb[0][e / kJP][e % kJP] = (e / kJP == e % kJP) ? 1.0 : 0.0;
+    if (e / kJP == e % kJP) dmax = fmax(dmax, s);
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, o, 64));
+  if (lane == 0) red[w] = dmax;
   __syncthreads();
-  // largest relative off-diagonal entry before the rotation
-  double mx = 0.0;
-  for (int e = lane; e < kJP * kJP; e += 64) {
+  dmax = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  __syncthreads();
+  if (tid == 0 && dmax > 0.0)
+    atomicMax((unsigned long long*)&ctl->rowmax2_bits, (unsigned long long)__double_as_longlong(dmax));
+  const double rowmax2 = fmax(dmax, __longlong_as_double((long long)ctl->rowmax2_bits));
+  const double eta = 0x1p-24 / (double)tol;
+  const double floor2 = eta * eta * rowmax2;
+  double m = 0.0;
+  for (int e = tid; e < kJP * kJP; e += 256) {
     const int p = e / kJP, q = e % kJP;
     if (p < q) {
-      const double den = G[p][p] * G[q][q];
-      if (den > 0.0) mx = fmax(mx, fabs(G[p][q]) / sqrt(den));
+      const double den = fmax(Gb[0][p][p], floor2) * fmax(Gb[0][q][q], floor2);
+      if (den > 0.0) m = fmax(m, fabs(Gb[0][p][q]) / sqrt(den));
     }
   }
-  red[lane] = mx;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o, 64));
+  if (lane == 0) red[w] = m;
   __syncthreads();
-  for (int o = 32; o > 0; o >>= 1) {
-    if (lane < o) red[lane] = fmax(red[lane], red[lane + o]);
-    __syncthreads();
-  }
-  const double off0 = red[0];
-  if (lane == 0) atomicMax(&ctl->sweep_max_bits, __float_as_uint((float)off0));
-  if (off0 <= (double)tol) {
-    if (lane == 0) skip[pair] = 1;
+  m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  if (tid == 0) atomicMax(&ctl->sweep_max_bits, __float_as_uint((float)m));
+  if (m <= (double)tol) {
+    if (tid == 0) skip[pair] = 1;
     return;
   }
-  for (int sweep = 0; sweep < 12; ++sweep) {
+  int cur = 0;
+  for (int sweep = 0; sweep < max_inner; ++sweep) {
     for (int rd = 0; rd < kJP - 1; ++rd) {
-      if (lane < kJP / 2) {
-        int p, q;
+      if (tid < kJP / 2) {
         const int last = kJP - 1;
-        if (lane == 0) { p = rd; q = last; }
-        else { p = (rd + lane) % last; q = (rd - lane + last) % last; }
-        if (p > q) { int t = p; p = q; q = t; }
-        const double gpq = G[p][q], gpp = G[p][p], gqq = G[q][q];
+        int p, q;
+        if (tid == 0) { p = rd; q = last; }
+        else { p = (rd + tid) % last; q = (rd - tid + last) % last; }
+        if (p > q) { const int t = p; p = q; q = t; }
+        const double gpq = Gb[cur][p][q], gpp = Gb[cur][p][p], gqq = Gb[cur][q][q];
         double c = 1.0, s = 0.0;
-        if (gpq != 0.0 && fabs(gpq) > 1e-16 * sqrt(gpp * gqq)) {
+        if (gpq != 0.0 && fabs(gpq) > 1e-17 * sqrt(gpp * gqq)) {
           const double zeta = (gqq - gpp) / (2.0 * gpq);
-          const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + hypot(1.0, zeta));
+          const double az = fabs(zeta);
+          const double root = az < 1e150 ? sqrt(1.0 + zeta * zeta) : az;
+          const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (az + root);
           c = 1.0 / sqrt(1.0 + t * t);
           s = c * t;
         }
-        pp[lane] = p; qq[lane] = q; cs[lane] = c; sn[lane] = s;
+        // new col p = c col_p - s col_q ; new col q = s col_p + c col_q
+        cx[p] = c; sx[p] = -s; px[p] = q;
+        cx[q] = c; sx[q] = s;  px[q] = p;
       }
       __syncthreads();
-      for (int idx = lane; idx < (kJP / 2) * kJP; idx += 64) {
-        const int k = idx / kJP, x = idx % kJP;
-        const int p = pp[k], q = qq[k];
-        const double c = cs[k], s = sn[k];
-        const double gp = G[p][x], gq = G[q][x];
-        G[p][x] = c * gp - s * gq;
-        G[q][x] = s * gp + c * gq;
+      const int nxt = cur ^ 1;
+      for (int e = tid; e < kJP * kJP; e += 256) {
+        const int x = e / kJP, y = e % kJP;
+        const int qx = px[x], qy = px[y];
+        const double ax = cx[x], bx = sx[x], ay = cx[y], by = sx[y];
+        Gb[nxt][x][y] = ax * (ay * Gb[cur][x][y] + by * Gb[cur][x][qy]) +
+                        bx * (ay * Gb[cur][qx][y] + by * Gb[cur][qx][qy]);
+        Vb[nxt][x][y] = ay * Vb[cur][x][y] + by * Vb[cur][x][qy];
       }
       __syncthreads();
-      for (int idx = lane; idx < (kJP / 2) * kJP; idx += 64) {
-        const int k = idx / kJP, x = idx % kJP;
-        const int p = pp[k], q = qq[k];
-        const double c = cs[k], s = sn[k];
-        const double gp = G[x][p], gq = G[x][q];
-        G[x][p] = c * gp - s * gq;
-        G[x][q] = s * gp + c * gq;
-        const double vp = V[x][p], vq = V[x][q];
-        V[x][p] = c * vp - s * vq;
-        V[x][q] = s * vp + c * vq;
-      }
-      __syncthreads();
+      cur = nxt;
     }
-    double m2 = 0.0;
-    for (int e = lane; e < kJP * kJP; e += 64) {
-      const int p = e / kJP, q = e % kJP;
-      if (p < q) {
-        const double den = G[p][p] * G[q][q];
-        if (den > 0.0) m2 = fmax(m2, fabs(G[p][q]) / sqrt(den));
-      }
-    }
-    red[lane] = m2;
-    __syncthreads();
-    for (int o = 32; o > 0; o >>= 1) {
-      if (lane < o) red[lane] = fmax(red[lane], red[lane + o]);
-      __syncthreads();
-    }
-    const double done = red[0];
-    __syncthreads();
-    if (done <= 1e-15) break;
   }
   float* vo = Vout + (int64_t)pair * kJP * kJP;
-  for (int e = lane; e < kJP * kJP; e += 64) vo[e] = (float)V[e / kJP][e % kJP];
-  if (lane == 0) skip[pair] = 0;
+  for (int e = tid; e < kJP * kJP; e += 256) vo[e] = (float)(Vb[cur][e / kJP][e % kJP]);
+  if (tid == 0) skip[pair] = 0;
 }
 
-// rows of the pair in [W | Utw] <- V^T rows; chunk of 512 columns per block
-constexpr int JAC_CHUNK = 512;
-
+// rows of the pair in [W | Utw] <- V^T rows on this block's chunk, computed
+// as w + (V - I)^T w (fp32 MFMA).  The k index is permuted so that the B
+// operand held by each lane is exactly the set of rows that lane outputs:
+// physical row of k = 2kk + h is mfma32_row(kk, 32h), and B register kk is
+// output register kk.
 __global__ void __launch_bounds__(256)
 k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D,
             const float* __restrict__ Vin, const int* __restrict__ skip,
@@ -321,18 +327,16 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
   pair_blocks(round, pair, seats, bi, bj);
   if (bi >= nb && bj >= nb) return;
   const int lane = lane_id(), w = wave_id();
-  const int l32 = lane & 31, kh = lane >> 5;
+  const int l32 = lane & 31;
   const float* V = Vin + (int64_t)pair * kJP * kJP;
-  // A[i][k] = V^T[i][k] = V[k][i]
   float a[kJP / 2];
+  int64_t rows[kJP / 2];
 #pragma unroll
-  for (int kk = 0; kk < kJP / 2; ++kk) a[kk] = V[(2 * kk + kh) * kJP + l32];
-  int64_t brow[kJP / 2];
-#pragma unroll
-  for (int kk = 0; kk < kJP / 2; ++kk) brow[kk] = pair_row(2 * kk + kh, bi, bj);
-  int64_t orow[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) orow[v] = pair_row(mfma32_row(v, lane), bi, bj);
+  for (int kk = 0; kk < kJP / 2; ++kk) {
+    const int pr = mfma32_row(kk, lane);
+    a[kk] = V[pr * kJP + l32] - (pr == l32 ? 1.0f : 0.0f);
+    rows[kk] = pair_row(pr, bi, bj);
+  }
   const int64_t Dt = D + d;
   const int64_t c0 = (int64_t)blockIdx.y * JAC_CHUNK;
   for (int it = 0; it < JAC_CHUNK / 128; ++it) {
@@ -347,7 +351,7 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
     float b[kJP / 2];
 #pragma unroll
     for (int kk = 0; kk < kJP / 2; ++kk)
-      b[kk] = (cok && brow[kk] < d) ? base[brow[kk] * ld + cc] : 0.f;
+      b[kk] = (cok && rows[kk] < d) ? base[rows[kk] * ld + cc] : 0.f;
     f32x16 acc;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
@@ -355,18 +359,18 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
     for (int kk = 0; kk < kJP / 2; ++kk) acc = mfma32(a[kk], b[kk], acc);
 #pragma unroll
     for (int v = 0; v < 16; ++v)
-      if (cok && orow[v] < d) base[orow[v] * ld + cc] = acc[v];
+      if (cok && rows[v] < d) base[rows[v] * ld + cc] = b[v] + acc[v];
   }
 }
 
-hipError_t launch_jac_round(const MatView& v, int round, float tol, hipStream_t s) {
+hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inner, hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   const int nsl = jac_slices(v.d, v.D);
   const int slice_cols = (int)(((v.D + nsl - 1) / nsl + 63) / 64 * 64);
   hipLaunchKernelGGL(k_jac_gram, dim3(pairs, nsl), dim3(256), 0, s, v.W, v.d, v.D, v.ctl, round,
                      seats, nb, slice_cols, v.gram_part);
-  hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(64), 0, s, v.gram_part, nsl, v.ctl, round,
-                     seats, nb, tol, v.Vrot, v.skip);
+  hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.gram_part, nsl, v.ctl, round,
+                     seats, nb, tol, max_inner, v.Vrot, v.skip);
   const int64_t Dt = v.D + v.d;
   hipLaunchKernelGGL(k_jac_apply, dim3(pairs, (unsigned)((Dt + JAC_CHUNK - 1) / JAC_CHUNK)),
                      dim3(256), 0, s, v.W, v.Utw, v.d, v.D, v.Vrot, v.skip, v.ctl, round, seats, nb);
@@ -375,6 +379,7 @@ hipError_t launch_jac_round(const MatView& v, int round, float tol, hipStream_t 
 
 __global__ void k_jac_check(JacCtl* ctl, float tol) {
   if (threadIdx.x != 0 || ctl->converged) return;
+  if (ctl->sweeps < (uint32_t)kHistory) ctl->history[ctl->sweeps] = ctl->sweep_max_bits;
   ctl->sweeps += 1;
   if (__uint_as_float(ctl->sweep_max_bits) <= tol) ctl->converged = 1;
   ctl->sweep_max_bits = 0;
@@ -431,6 +436,8 @@ __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict
     if (k == 0) {
       info[0] = (int)ctl->sweeps;
       info[1] = (int)ctl->converged;
+      for (int i = 0; i < kHistory; ++i)
+        info[2 + i] = i < (int)ctl->sweeps ? (int)ctl->history[i] : 0;
       if (!ctl->converged) atomicOr(status, 2u);
     }
   }

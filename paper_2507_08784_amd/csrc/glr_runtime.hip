@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -119,7 +120,7 @@ void mat_layout(const glr_config* c, int mat, uint64_t base, glr_mat_layout* L, 
   L->off_S1 = take(mn * 4);
   L->off_S2 = c->opt == GLR_ADAM ? take(mn * 4) : 0;
   L->off_Rbar = take((uint64_t)x.r * (uint64_t)x.D * 4);
-  L->off_info = take(16 * 4);
+  L->off_info = take(kInfoInts * 4);
   *end = o;
 }
 
@@ -174,6 +175,11 @@ bool aligned(const void* p) { return ((uintptr_t)p % kAlign) == 0; }
 
 }  // namespace
 
+struct ProfMark {
+  int group;
+  hipEvent_t a, b;
+};
+
 struct glr_handle {
   glr_config cfg;
   std::vector<glr_shape> shapes;
@@ -185,6 +191,13 @@ struct glr_handle {
   int64_t next_t = 0;
   bool suspect = false;
   std::string err;
+  int jac_inner = 1;   // inner Jacobi sweeps per pair visit
+  bool prof = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<ProfMark> marks;
+  double prof_ms[GLR_PROF_COUNT] = {0};
+  int64_t prof_n[GLR_PROF_COUNT] = {0};
 };
 
 namespace {
@@ -236,6 +249,54 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   return v;
 }
 
+hipError_t prof_event(glr_handle* h, hipEvent_t* ev) {
+  if (h->ev_used == h->ev_pool.size()) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    h->ev_pool.push_back(e);
+  }
+  *ev = h->ev_pool[h->ev_used++];
+  return hipSuccess;
+}
+
+// RAII bracket of one launch group with two events on the step's stream
+struct ProfScope {
+  glr_handle* h;
+  hipStream_t s;
+  int group;
+  hipEvent_t a = nullptr;
+  hipError_t err = hipSuccess;
+  ProfScope(glr_handle* h_, hipStream_t s_, int g) : h(h_), s(s_), group(g) {
+    if (!h->prof) return;
+    err = prof_event(h, &a);
+    if (err == hipSuccess) err = hipEventRecord(a, s);
+  }
+  ~ProfScope() {
+    if (!h->prof || err != hipSuccess) return;
+    hipEvent_t b;
+    if (prof_event(h, &b) != hipSuccess) return;
+    if (hipEventRecord(b, s) != hipSuccess) return;
+    h->marks.push_back({group, a, b});
+  }
+};
+
+// folds recorded marks into the totals (waits for them) and recycles events
+hipError_t prof_collect(glr_handle* h) {
+  for (const ProfMark& m : h->marks) {
+    hipError_t e = hipEventSynchronize(m.b);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, m.a, m.b);
+    if (e != hipSuccess) return e;
+    h->prof_ms[m.group] += ms;
+    h->prof_n[m.group] += 1;
+  }
+  h->marks.clear();
+  h->ev_used = 0;
+  return hipSuccess;
+}
+
 #define GLR_HIP(h, call)                                 \
   do {                                                   \
     hipError_t e_ = (call);                              \
@@ -246,16 +307,24 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
 glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
-  GLR_HIP(h, launch_jac_init(v, warm, s));
+  ProfScope all(h, s, GLR_PROF_REFRESH);
+  {
+    ProfScope p(h, s, GLR_PROF_JAC_INIT);
+    GLR_HIP(h, launch_jac_init(v, warm, s));
+  }
   const int rounds = jac_seats(v.d) - 1;
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
-    for (int rd = 0; rd < rounds; ++rd) GLR_HIP(h, launch_jac_round(v, rd, c.tol, s));
+    for (int rd = 0; rd < rounds; ++rd) {
+      ProfScope p(h, s, GLR_PROF_JAC_ROUND);
+      GLR_HIP(h, launch_jac_round(v, rd, c.tol, h->jac_inner, s));
+    }
     GLR_HIP(h, launch_jac_check(v, c.tol, s));
     uint32_t conv = 0;
     GLR_HIP(h, hipMemcpyAsync(&conv, &v.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
     GLR_HIP(h, hipStreamSynchronize(s));
     if (conv) break;
   }
+  ProfScope p(h, s, GLR_PROF_JAC_FINISH);
   GLR_HIP(h, launch_jac_finish(v, c.max_sweeps, s));
   return GLR_OK;
 }
@@ -265,20 +334,36 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
   MatView v = view_of(h, mat, X, G);
   const bool refresh = (t % c.tau) == 0;
   OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
-  GLR_HIP(h, launch_ef_mean(v, (c.flags & GLR_CHECK_FINITE) != 0, s));
+  {
+    ProfScope p(h, s, GLR_PROF_EF_MEAN);
+    GLR_HIP(h, launch_ef_mean(v, (c.flags & GLR_CHECK_FINITE) != 0, s));
+  }
   if (refresh) {
     glr_status st = refresh_svd(h, v, t, s);
     if (st != GLR_OK) return st;
   } else if (v.r < v.d) {
-    GLR_HIP(h, launch_sel_scores(v, c.select == GLR_SELECT_APPROX, c.seed, t, s));
+    {
+      ProfScope p(h, s, GLR_PROF_SELECT);
+      GLR_HIP(h, launch_sel_scores(v, c.select == GLR_SELECT_APPROX, c.seed, t, s));
+    }
+    ProfScope p(h, s, GLR_PROF_TOPR);
     GLR_HIP(h, launch_topr(v, s));
   }
-  GLR_HIP(h, launch_proj(v, s));
-  GLR_HIP(h, launch_rbar(v, s));
-  if (refresh && c.refresh == GLR_REFRESH_FULL)
+  {
+    ProfScope p(h, s, GLR_PROF_PROJ);
+    GLR_HIP(h, launch_proj(v, s));
+  }
+  {
+    ProfScope p(h, s, GLR_PROF_RBAR);
+    GLR_HIP(h, launch_rbar(v, s));
+  }
+  if (refresh && c.refresh == GLR_REFRESH_FULL) {
+    ProfScope p(h, s, GLR_PROF_FULL_REFRESH);
     GLR_HIP(h, launch_full_refresh(v, op, s));
-  else
+  } else {
+    ProfScope p(h, s, GLR_PROF_RESID_OPT);
     GLR_HIP(h, launch_resid_opt(v, op, s));
+  }
   return GLR_OK;
 }
 
@@ -336,6 +421,10 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   h->shapes.assign(cfg->shapes, cfg->shapes + cfg->num_mats);
   h->cfg.shapes = h->shapes.data();
   h->ws = wl;
+  if (const char* e = getenv("GLR_JAC_INNER")) {
+    const int v = atoi(e);
+    if (v >= 1 && v <= 16) h->jac_inner = v;
+  }
   h->state = (char*)d_state;
   h->work = (char*)d_ws;
   uint64_t o = kHeaderBytes;
@@ -410,7 +499,32 @@ glr_status glr_next_step(const glr_handle* h, int64_t* next_t) {
 }
 
 glr_status glr_destroy(glr_handle* h) {
+  if (!h) return GLR_OK;
+  for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
   delete h;
+  return GLR_OK;
+}
+
+glr_status glr_profile_enable(glr_handle* h, int32_t on) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  h->prof = on != 0;
+  return GLR_OK;
+}
+
+glr_status glr_profile_reset(glr_handle* h) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  GLR_HIP(h, prof_collect(h));
+  for (int i = 0; i < GLR_PROF_COUNT; ++i) { h->prof_ms[i] = 0.0; h->prof_n[i] = 0; }
+  return GLR_OK;
+}
+
+glr_status glr_profile_query(glr_handle* h, int32_t group, double* total_ms, int64_t* launches) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (group < 0 || group >= GLR_PROF_COUNT || !total_ms || !launches)
+    return fail(h, GLR_ERR_INVALID_ARG, "bad profile group or output pointer");
+  GLR_HIP(h, prof_collect(h));
+  *total_ms = h->prof_ms[group];
+  *launches = h->prof_n[group];
   return GLR_OK;
 }
 

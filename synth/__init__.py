@@ -11,4 +11,5 @@ from .gen import (  # noqa: F401
     planted_factors,
     planted_matrix,
     gradient_batch,
+    noise_level,
 )

@@ -145,6 +145,11 @@ def planted_factors(wl: Workload, mat: int):
     return us, np.asarray(s, dtype=np.float64), vs, float(nu)
 
 
+def noise_level(wl: Workload, mat: int) -> float:
+    """nu, the standard deviation of the per-step Gaussian noise."""
+    return float(_spectrum(wl, mat)[1])
+
+
 def planted_matrix(wl: Workload, mat: int) -> np.ndarray:
     us, s, vs, _ = planted_factors(wl, mat)
     return (us * s) @ vs.T

@@ -51,7 +51,7 @@ def selection_margin(score, r):
 
 
 def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_start=False,
-               max_sweeps=30, tol=1e-7, check=None):
+               max_sweeps=30, tol=1e-6, check=None):
     """Runs both paths; returns a list of per-step dicts of relative errors.
     Raises AssertionError at the first step over the bars."""
     import torch

@@ -101,7 +101,7 @@ def test_layout_is_aligned_disjoint_and_sized(opt):
         assert (L.m, L.n, L.d, L.D, L.right, L.r) == (m, n, d, D, int(m > n), min(8, d))
         parts = [(L.off_E, 3 * m * n * 4), (L.off_Ebar, m * n * 4), (L.off_U, d * d * 4),
                  (L.off_sigma, d * 4), (L.off_J, L.r * 4), (L.off_score, d * 4),
-                 (L.off_S1, m * n * 4), (L.off_Rbar, L.r * D * 4), (L.off_info, 64)]
+                 (L.off_S1, m * n * 4), (L.off_Rbar, L.r * D * 4), (L.off_info, 256)]
         if opt == "adam":
             parts.append((L.off_S2, m * n * 4))
         else:
