@@ -185,7 +185,8 @@ typedef enum {
   GLR_PROF_JAC_ROUND = 8,    /* refresh: one Jacobi round (gram + solve + apply) */
   GLR_PROF_JAC_FINISH = 9,   /* refresh: norms, sort, permutation */
   GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
-  GLR_PROF_COUNT = 11
+  GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration */
+  GLR_PROF_COUNT = 12
 } glr_prof_group;
 
 glr_status glr_profile_enable(glr_handle* h, int32_t on);

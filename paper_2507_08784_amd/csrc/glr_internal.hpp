@@ -22,6 +22,21 @@ struct JacCtl {
   uint32_t history[kHistory];  // float bits of each sweep's largest off-norm
 };
 
+// Control words of the subspace iteration (device memory).
+struct SubCtl {
+  int iters;
+  int converged;
+  double change2;              // squared Frobenius norm of the last subspace change
+  uint32_t history[kHistory];  // float bits of each iteration's change / sqrt(K)
+};
+
+constexpr int kMaxSubK = 256;   // largest rank the subspace-iteration refresh takes
+
+// The tau = 1 refresh needs only span(U[:, :r]): subspace iteration then, on
+// an oversampled block of sub_block(r, d) directions.
+inline bool use_subspace(int tau, int r, int64_t d) { return tau == 1 && r < d && r <= kMaxSubK; }
+inline int sub_block(int r, int64_t d) { return (int)((int64_t)(2 * r) < d ? 2 * r : d); }
+
 // One matrix of the current step, as the kernels see it.
 struct MatView {
   int64_t m, n, d, D;
@@ -39,6 +54,13 @@ struct MatView {
   float* Mbar;   float* Q;     float* lam_part;
   float* W;      float* Utw;   double* gram_part; float* Vrot; int* skip;
   JacCtl* ctl;   float* sigma_w; int* perm;
+  // subspace iteration
+  float* sub_P;  float* sub_Pn; float* sub_Z;  float* sub_Zt; float* sub_R; float* sub_part;
+  double* sub_S; double* sub_L; double* sub_Dinv; double* sub_Li; double* sub_T;
+  float* sub_Linv; float* sub_C; double* sub_sums; SubCtl* sub_ctl;
+  // Rayleigh-Ritz: block Jacobi SVD of the K x D projection
+  float* rr_Utw; float* rr_Y; double* rr_gram; float* rr_V; int* rr_skip; JacCtl* rr_ctl;
+  float* rr_sigw; int* rr_perm;
 };
 
 struct OptParams {
@@ -62,9 +84,17 @@ hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t
 int jac_blocks(int64_t d);
 int jac_seats(int64_t d);
 int jac_slices(int64_t d, int64_t D);
+hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
 hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inner, hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
+
+// subspace iteration (tau = 1)
+size_t sub_part_floats(int K, int64_t d, int64_t D);
+hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStream_t s);
+hipError_t launch_sub_iter(const MatView& v, float tol, hipStream_t s);
+hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s);
+hipError_t launch_sub_rr_end(const MatView& v, hipStream_t s);
 
 }  // namespace glr

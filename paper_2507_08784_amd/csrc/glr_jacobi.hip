@@ -130,6 +130,11 @@ static inline int grid1(int64_t n) {
   return (int)g;
 }
 
+hipError_t launch_jac_reset(const MatView& v, hipStream_t s) {
+  hipLaunchKernelGGL(k_ctl_reset, dim3(1), dim3(64), 0, s, v.ctl);
+  return hipGetLastError();
+}
+
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s) {
   hipLaunchKernelGGL(k_ctl_reset, dim3(1), dim3(64), 0, s, v.ctl);
   if (warm) {

@@ -30,7 +30,11 @@ thread_local std::string g_create_error;
 
 struct WsLayout {
   uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_V, off_skip, off_ctl, off_sigw,
-      off_perm, bytes;
+      off_perm;
+  uint64_t off_sP, off_sPn, off_sZ, off_sZt, off_sR, off_spart, off_sS, off_sL, off_sDinv, off_sLi,
+      off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
+  uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rskip, off_rctl, off_rsigw, off_rperm;
+  uint64_t bytes;
 };
 
 struct Dims {
@@ -135,19 +139,36 @@ uint64_t state_bytes_of(const glr_config* c) {
 
 WsLayout ws_layout(const glr_config* c) {
   uint64_t mx_mn = 0, mx_Q = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
+  uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
+  uint64_t r_gram = 0, r_pairs = 0;
+  auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
   for (int i = 0; i < c->num_mats; ++i) {
     const Dims x = dims_of(c, i);
-    const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
-    const uint64_t sl = (uint64_t)jac_slices(x.d, x.D);
-    auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
     mx(mx_mn, (uint64_t)(x.m * x.n));
     mx(mx_Q, (uint64_t)c->num_workers * (uint64_t)x.r * (uint64_t)x.D);
     mx(mx_lam, (uint64_t)((x.D + 127) / 128) * (uint64_t)x.d);
-    mx(mx_dD, (uint64_t)(x.d * x.D));
-    mx(mx_dd, (uint64_t)(x.d * x.d));
-    mx(mx_gram, pairs * sl * kJP * kJP);
-    mx(mx_pairs, pairs);
     mx(mx_d, (uint64_t)x.d);
+    if (use_subspace(c->tau, x.r, x.d)) {
+      const int Ki = sub_block(x.r, x.d);
+      const uint64_t K = (uint64_t)Ki, Kp = (K + 31) / 32 * 32;
+      mx(s_Kd, K * (uint64_t)x.d);
+      mx(s_KD, K * (uint64_t)x.D);
+      mx(s_part, (uint64_t)sub_part_floats(Ki, x.d, x.D));
+      const uint64_t rp = (uint64_t)jac_seats(Ki) / 2;
+      mx(r_pairs, rp);
+      mx(r_gram, rp * (uint64_t)jac_slices(Ki, x.D) * kJP * kJP);
+      mx(s_KK, K * K);
+      mx(s_Kp2, Kp * Kp);
+      mx(s_nt, Kp / 32);
+      mx(s_sums, (uint64_t)((x.d + 127) / 128) * ((K + 127) / 128));
+    } else {
+      const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
+      const uint64_t sl = (uint64_t)jac_slices(x.d, x.D);
+      mx(mx_dD, (uint64_t)(x.d * x.D));
+      mx(mx_dd, (uint64_t)(x.d * x.d));
+      mx(mx_gram, pairs * sl * kJP * kJP);
+      mx(mx_pairs, pairs);
+    }
   }
   WsLayout w;
   uint64_t o = 0;
@@ -167,6 +188,29 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_ctl = take(sizeof(JacCtl));
   w.off_sigw = take(mx_d * 4);
   w.off_perm = take(mx_d * 4);
+  w.off_sP = take(s_Kd * 4);
+  w.off_sPn = take(s_Kd * 4);
+  w.off_sZ = take(s_KD * 4);
+  w.off_sZt = take(s_KD * 4);
+  w.off_sR = take(s_Kd * 4);
+  w.off_spart = take(s_part * 4);
+  w.off_sS = take(s_KK * 8);
+  w.off_sL = take(s_Kp2 * 8);
+  w.off_sDinv = take(s_nt * 32 * 32 * 8);
+  w.off_sLi = take(s_Kp2 * 8);
+  w.off_sT = take(8 * 32 * 32 * 8);
+  w.off_sLinv = take(s_Kp2 * 4);
+  w.off_sC = take(s_KK * 4);
+  w.off_ssums = take(s_sums * 8);
+  w.off_sctl = take(sizeof(SubCtl));
+  w.off_rUtw = take(s_KK * 4);
+  w.off_rY = take(s_KK * 4);
+  w.off_rgram = take(r_gram * 8);
+  w.off_rV = take(r_pairs * kJP * kJP * 4);
+  w.off_rskip = take(r_pairs * 4);
+  w.off_rctl = take(sizeof(JacCtl));
+  w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
+  w.off_rperm = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
   w.bytes = o;
   return w;
 }
@@ -192,6 +236,7 @@ struct glr_handle {
   bool suspect = false;
   std::string err;
   int jac_inner = 1;   // inner Jacobi sweeps per pair visit
+  int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
@@ -246,6 +291,29 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   v.ctl = (JacCtl*)(w + h->ws.off_ctl);
   v.sigma_w = (float*)(w + h->ws.off_sigw);
   v.perm = (int*)(w + h->ws.off_perm);
+  v.sub_P = (float*)(w + h->ws.off_sP);
+  v.sub_Pn = (float*)(w + h->ws.off_sPn);
+  v.sub_Z = (float*)(w + h->ws.off_sZ);
+  v.sub_Zt = (float*)(w + h->ws.off_sZt);
+  v.sub_R = (float*)(w + h->ws.off_sR);
+  v.sub_part = (float*)(w + h->ws.off_spart);
+  v.sub_S = (double*)(w + h->ws.off_sS);
+  v.sub_L = (double*)(w + h->ws.off_sL);
+  v.sub_Dinv = (double*)(w + h->ws.off_sDinv);
+  v.sub_Li = (double*)(w + h->ws.off_sLi);
+  v.sub_T = (double*)(w + h->ws.off_sT);
+  v.sub_Linv = (float*)(w + h->ws.off_sLinv);
+  v.sub_C = (float*)(w + h->ws.off_sC);
+  v.sub_sums = (double*)(w + h->ws.off_ssums);
+  v.sub_ctl = (SubCtl*)(w + h->ws.off_sctl);
+  v.rr_Utw = (float*)(w + h->ws.off_rUtw);
+  v.rr_Y = (float*)(w + h->ws.off_rY);
+  v.rr_gram = (double*)(w + h->ws.off_rgram);
+  v.rr_V = (float*)(w + h->ws.off_rV);
+  v.rr_skip = (int*)(w + h->ws.off_rskip);
+  v.rr_ctl = (JacCtl*)(w + h->ws.off_rctl);
+  v.rr_sigw = (float*)(w + h->ws.off_rsigw);
+  v.rr_perm = (int*)(w + h->ws.off_rperm);
   return v;
 }
 
@@ -329,6 +397,42 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   return GLR_OK;
 }
 
+// tau = 1 refresh: top-r block of U by oversampled subspace iteration and a
+// Rayleigh-Ritz step (block Jacobi SVD of the K x D projection)
+glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
+  const float sub_tol = 10.0f * c.tol;
+  const int iters = warm ? h->sub_iters_warm : h->sub_iters_cold;
+  ProfScope all(h, s, GLR_PROF_REFRESH);
+  {
+    ProfScope p(h, s, GLR_PROF_JAC_INIT);
+    GLR_HIP(h, launch_sub_start(v, warm, c.seed, s));
+  }
+  for (int it = 0; it < iters; ++it) {
+    ProfScope p(h, s, GLR_PROF_SUB_ITER);
+    GLR_HIP(h, launch_sub_iter(v, sub_tol, s));
+  }
+  MatView rr;
+  GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
+  const int rounds = jac_seats(rr.d) - 1;
+  for (int sw = 0; sw < c.max_sweeps; ++sw) {
+    for (int rd = 0; rd < rounds; ++rd) {
+      ProfScope p(h, s, GLR_PROF_JAC_ROUND);
+      GLR_HIP(h, launch_jac_round(rr, rd, c.tol, h->jac_inner, s));
+    }
+    GLR_HIP(h, launch_jac_check(rr, c.tol, s));
+    uint32_t conv = 0;
+    GLR_HIP(h, hipMemcpyAsync(&conv, &rr.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
+    GLR_HIP(h, hipStreamSynchronize(s));
+    if (conv) break;
+  }
+  ProfScope p(h, s, GLR_PROF_JAC_FINISH);
+  GLR_HIP(h, launch_jac_finish(rr, c.max_sweeps, s));
+  GLR_HIP(h, launch_sub_rr_end(v, s));
+  return GLR_OK;
+}
+
 glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   MatView v = view_of(h, mat, X, G);
@@ -339,7 +443,7 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
     GLR_HIP(h, launch_ef_mean(v, (c.flags & GLR_CHECK_FINITE) != 0, s));
   }
   if (refresh) {
-    glr_status st = refresh_svd(h, v, t, s);
+    glr_status st = use_subspace(c.tau, v.r, v.d) ? refresh_subspace(h, v, t, s) : refresh_svd(h, v, t, s);
     if (st != GLR_OK) return st;
   } else if (v.r < v.d) {
     {
@@ -424,6 +528,10 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   if (const char* e = getenv("GLR_JAC_INNER")) {
     const int v = atoi(e);
     if (v >= 1 && v <= 16) h->jac_inner = v;
+  }
+  if (const char* e = getenv("GLR_SUB_ITERS")) {
+    const int v = atoi(e);
+    if (v >= 1 && v <= 64) h->sub_iters_warm = v;
   }
   h->state = (char*)d_state;
   h->work = (char*)d_ws;

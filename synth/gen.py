@@ -229,6 +229,13 @@ def _mk():
                  recipe="lowrank", params=(("rank", 4),)))
     add(Workload("zero_grad", ((32, 64),), 2, 4, 2, 4, "adam", 1e-3, 0.9,
                  recipe="zero"))
+    # tau = 1: every step a refresh, only the top-r block of U is used
+    add(Workload("tau1_left", ((64, 300),), 3, 8, 1, 6, "adam", 1e-3, 0.9,
+                 recipe="geometric", params=(("rank", 16), ("nu", 1e-3))))
+    add(Workload("tau1_right", ((500, 96),), 2, 12, 1, 5, "msgd", 0.01, 0.9,
+                 recipe="geometric", params=(("rank", 24), ("nu", 5e-4))))
+    add(Workload("tau1_k40", ((200, 1000),), 2, 40, 1, 4, "adam", 1e-3, 0.9,
+                 recipe="geometric", params=(("rank", 60), ("decay", 0.93), ("nu", 1e-4))))
     return w
 
 

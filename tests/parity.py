@@ -93,7 +93,9 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
             jg = comp.J(l).cpu().numpy()
             pg = ut[jg].T
             po = o["P"]
-            rec["orth"] = float(np.abs(ut @ ut.T - np.eye(d)).max())
+            # the tau = 1 refresh defines only rows 0..r-1 of U^T (its top-r block)
+            uo = ut[:r] if (wl.tau == 1 and r < d) else ut
+            rec["orth"] = float(np.abs(uo @ uo.T - np.eye(uo.shape[0])).max())
             assert rec["orth"] < 1e-5, (t, l, rec)
             if not o["refresh"] and r < d:
                 margin = selection_margin(o["score"], r)
@@ -113,7 +115,8 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
                               floor=1e-3 * mi * np.sqrt(m * n))
             if o["refresh"]:
                 sg = comp.sigma(l).double().cpu().numpy()
-                k = min(d, r + 4)
+                # the tau = 1 refresh returns Ritz values of its top-r block
+                k = r if (wl.tau == 1 and r < d) else min(d, r + 4)
                 rec["sigma"] = float(np.abs(sg[:k] - o["sigma"][:k]).max() / max(o["sigma"][0], 1e-300))
                 assert rec["sigma"] < 1e-5, (t, l, rec)
             assert rec["proj"] < step_tol, f"t={t} mat={l}: proj rel {rec['proj']:.3e} ({rec})"

@@ -47,6 +47,19 @@ def test_refresh_full_parity(gpu_lib, name):
     run_parity(gpu_lib, get_workload(name), refresh="full", check=check)
 
 
+@pytest.mark.parametrize("name", ["tau1_left", "tau1_right", "tau1_k40"])
+def test_tau1_subspace_iteration_parity(gpu_lib, name):
+    # tau = 1: the refresh computes only span(U[:, :r]) by subspace iteration
+    _print_case(name)
+    wl = get_workload(name)
+
+    def check(comp, o, t, l, rec):
+        its, conv, hist = comp.sweep_history(l)
+        assert conv, (t, its, hist)
+
+    run_parity(gpu_lib, wl, check=check)
+
+
 def test_cold_start_refresh_parity(gpu_lib):
     _print_case("tiny_left", cold_start=True)
     run_parity(gpu_lib, get_workload("tiny_left"), cold_start=True)
