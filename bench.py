@@ -68,10 +68,16 @@ def group_work(wl, name, launches_per_step=None):
         elif name == "resid_opt":
             flops += 2.0 * r * d * D * N
             byts += (12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D
-        elif name == "jac_round":
+        elif name == "jac_gram_solve":
+            # pair Grams (fp64 MFMA): 32 x 32 x D per pair
             pairs, _ = jac_pairs(d)
             flops64 += pairs * 2.0 * 32 * 32 * D
+            byts += pairs * 32.0 * D * 4
+        elif name == "jac_apply":
+            # rotation of 32 rows of [W | U^T] per pair: read + write
+            pairs, _ = jac_pairs(d)
             flops += pairs * 2.0 * 32 * 32 * (D + d)
+            byts += pairs * 32.0 * (D + d) * 8
     k = len(wl.shapes)
     return byts / k, flops / k, flops64 / k
 
@@ -171,6 +177,7 @@ def main():
     ap.add_argument("--pool", type=int, default=11)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--tol", type=float, default=1e-6, help="refresh tolerance")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -195,7 +202,8 @@ def main():
           f"N={wl.workers} r={wl.rank} tau={wl.tau} opt={wl.opt}; pool {pool}", file=sys.stderr, flush=True)
     batches = make_pool(wl, pool, dev)
     comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
-                          beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, device=dev)
+                          beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, tol=args.tol,
+                          device=dev)
     X = [torch.zeros(m, n, dtype=torch.float32, device=dev) for m, n in wl.shapes]
     torch.cuda.synchronize()
 
@@ -223,7 +231,7 @@ def main():
     print(f"[bench] timed {args.steps} steps ({n_refresh} refresh): {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     kernels = []
-    for name in ("ef_mean", "select", "proj", "resid_opt", "jac_round"):
+    for name in ("ef_mean", "select", "proj", "resid_opt", "jac_gram_solve", "jac_apply"):
         if name in prof:
             e = roofline_entry(wl, name, *prof[name])
             if e:

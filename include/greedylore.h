@@ -182,11 +182,12 @@ typedef enum {
   GLR_PROF_RESID_OPT = 5,    /* residual + mean + reconstruction + optimizer */
   GLR_PROF_FULL_REFRESH = 6, /* Algorithm 3 refresh update */
   GLR_PROF_JAC_INIT = 7,     /* refresh: Jacobi initialisation (warm start product) */
-  GLR_PROF_JAC_ROUND = 8,    /* refresh: one Jacobi round (gram + solve + apply) */
+  GLR_PROF_JAC_ROUND = 8,    /* refresh: pair Grams and pair eigensolves of one Jacobi round */
   GLR_PROF_JAC_FINISH = 9,   /* refresh: norms, sort, permutation */
   GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
   GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration */
-  GLR_PROF_COUNT = 12
+  GLR_PROF_JAC_APPLY = 12,   /* refresh: rotations of one Jacobi round */
+  GLR_PROF_COUNT = 13
 } glr_prof_group;
 
 glr_status glr_profile_enable(glr_handle* h, int32_t on);

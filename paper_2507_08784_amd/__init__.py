@@ -30,7 +30,7 @@ EXPORTED = (
     "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
 )
 PROF_GROUPS = ("ef_mean", "select", "topr", "proj", "rbar", "resid_opt", "full_refresh",
-               "jac_init", "jac_round", "jac_finish", "refresh", "sub_iter")
+               "jac_init", "jac_gram_solve", "jac_finish", "refresh", "sub_iter", "jac_apply")
 
 
 class GlrError(RuntimeError):

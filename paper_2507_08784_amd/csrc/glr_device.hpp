@@ -121,21 +121,24 @@ struct LoadK {
   }
 };
 
-// Element (r, k) at base[k * ld + r] (+ base2): contiguous along r.
-template <int R, int BK, bool FUSED>
+// Element (r, k) at base[krow(k) * ld + r] (+ base2): contiguous along r;
+// krow(k) = rows[k] when GATHER, else k.
+template <int R, int BK, bool FUSED, bool GATHER = false>
 struct LoadR {
   static constexpr int RQ = R / 4;
   static constexpr int NV = (BK * RQ + kThreads - 1) / kThreads;
   const float* base;
   const float* base2;
+  const int* rows;
   int64_t ld;
   int r0, nr, K;
   bool vec;
   int kl[NV], rq[NV];
   float4 v[NV];
 
-  __device__ LoadR(const float* b, const float* b2, int64_t ld_, int r0_, int nr_, int K_)
-      : base(b), base2(b2), ld(ld_), r0(r0_), nr(nr_), K(K_) {
+  __device__ LoadR(const float* b, const float* b2, int64_t ld_, int r0_, int nr_, int K_,
+                   const int* rows_ = nullptr)
+      : base(b), base2(b2), rows(rows_), ld(ld_), r0(r0_), nr(nr_), K(K_) {
     vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & 15) == 0) &&
           (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & 15) == 0));
 #pragma unroll
@@ -157,7 +160,8 @@ struct LoadR {
       int r = r0 + 4 * rq[i];
       float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
       if (kl[i] < BK && k < K) {
-        int64_t off = (int64_t)k * ld + r;
+        const int64_t kr = GATHER ? (int64_t)rows[k] : (int64_t)k;
+        int64_t off = kr * ld + r;
         if (vec && r + 3 < nr) {
           x = *reinterpret_cast<const float4*>(base + off);
           if (FUSED) {

@@ -86,7 +86,8 @@ int jac_seats(int64_t d);
 int jac_slices(int64_t d, int64_t D);
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
-hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inner, hipStream_t s);
+hipError_t launch_jac_gram_solve(const MatView& v, int round, float tol, int max_inner, hipStream_t s);
+hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
 

@@ -11,8 +11,9 @@
 //   apply  : rows of [W | U^T] <- V^T rows, in place, as w + (V - I)^T w
 //            (fp32 MFMA)
 // A sweep is one tournament (every pair of blocks meets once).  The sweeps
-// stop when every pair met in a sweep passes the measure of k_jac_solve.  The final singular values are the row norms of W, sorted
-// descending (ties keep the lower row first); U^T rows follow the sort.
+// stop when every pair met in a sweep passes the measure of k_jac_solve.
+// The final singular values are the row norms of W, sorted descending (ties
+// keep the lower row first); U^T rows follow the sort.
 #include "glr_device.hpp"
 #include "glr_internal.hpp"
 
@@ -368,7 +369,7 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
   }
 }
 
-hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inner, hipStream_t s) {
+hipError_t launch_jac_gram_solve(const MatView& v, int round, float tol, int max_inner, hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   const int nsl = jac_slices(v.d, v.D);
   const int slice_cols = (int)(((v.D + nsl - 1) / nsl + 63) / 64 * 64);
@@ -376,6 +377,11 @@ hipError_t launch_jac_round(const MatView& v, int round, float tol, int max_inne
                      seats, nb, slice_cols, v.gram_part);
   hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.gram_part, nsl, v.ctl, round,
                      seats, nb, tol, max_inner, v.Vrot, v.skip);
+  return hipGetLastError();
+}
+
+hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s) {
+  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   const int64_t Dt = v.D + v.d;
   hipLaunchKernelGGL(k_jac_apply, dim3(pairs, (unsigned)((Dt + JAC_CHUNK - 1) / JAC_CHUNK)),
                      dim3(256), 0, s, v.W, v.Utw, v.d, v.D, v.Vrot, v.skip, v.ctl, round, seats, nb);

@@ -383,8 +383,12 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   const int rounds = jac_seats(v.d) - 1;
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
-      ProfScope p(h, s, GLR_PROF_JAC_ROUND);
-      GLR_HIP(h, launch_jac_round(v, rd, c.tol, h->jac_inner, s));
+      {
+        ProfScope p(h, s, GLR_PROF_JAC_ROUND);
+        GLR_HIP(h, launch_jac_gram_solve(v, rd, c.tol, h->jac_inner, s));
+      }
+      ProfScope p(h, s, GLR_PROF_JAC_APPLY);
+      GLR_HIP(h, launch_jac_apply(v, rd, s));
     }
     GLR_HIP(h, launch_jac_check(v, c.tol, s));
     uint32_t conv = 0;
@@ -418,8 +422,12 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   const int rounds = jac_seats(rr.d) - 1;
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
-      ProfScope p(h, s, GLR_PROF_JAC_ROUND);
-      GLR_HIP(h, launch_jac_round(rr, rd, c.tol, h->jac_inner, s));
+      {
+        ProfScope p(h, s, GLR_PROF_JAC_ROUND);
+        GLR_HIP(h, launch_jac_gram_solve(rr, rd, c.tol, h->jac_inner, s));
+      }
+      ProfScope p(h, s, GLR_PROF_JAC_APPLY);
+      GLR_HIP(h, launch_jac_apply(rr, rd, s));
     }
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
     uint32_t conv = 0;

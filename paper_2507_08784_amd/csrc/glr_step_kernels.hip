@@ -314,8 +314,8 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
                          v.Ut, v.J, v.Q, v.d, v.D, r);                                            \
   } while (0)
   if (r <= 32) GLR_PROJ(32, 128, 1, 4);
-  else if (r <= 64) GLR_PROJ(64, 128, 1, 4);
-  else GLR_PROJ(128, 128, 2, 2);
+  else if (r <= 64) GLR_PROJ(64, 64, 2, 2);
+  else GLR_PROJ(128, 64, 2, 2);
 #undef GLR_PROJ
   return hipGetLastError();
 }
@@ -337,130 +337,165 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// S5 + S7 + S8 fused, one pass over the m x n tile:
+// S5 + S7 + S8 fused, one pass over a 128 x 64 tile of the m x n layout:
 //   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
 //   E^(i) <- G^(i) + E^(i) - C^(i);  Ebar = (1/N) sum_i E^(i)
 //   Ghat  = (1/N) sum_i C^(i)  (= P Rbar);  optimizer on X with Ghat.
-// Each wave owns 32 rows x 64 columns; a block stacks 4 waves (128 x 64).
+// The product is computed transposed (MFMA rows = tile columns) so that each
+// lane holds 4 consecutive columns of a row: G, E, X and the optimizer state
+// move as 16-byte vectors.  P (gathered rows of U^T) and Q^(i) are staged
+// through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
-constexpr int RO_ROWS = 128, RO_COLS = 64, RO_TN = 2;
-constexpr int RO_MAX_R = 1024;
+constexpr int RO_ROWS = 128, RO_COLS = 64;
 
 template <int OPT, bool RIGHT>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
-            const float* __restrict__ Q, const float* __restrict__ Ut, const int* __restrict__ Jg,
+            const float* __restrict__ Q, const float* __restrict__ Ut, const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
-  __shared__ int J[RO_MAX_R];
-  for (int k = threadIdx.x; k < r; k += blockDim.x) J[k] = Jg[k];
-  __syncthreads();
-  const int lane = lane_id(), w = wave_id();
-  const int l32 = lane & 31, kh = lane >> 5;
-  const int64_t row_base = (int64_t)blockIdx.y * RO_ROWS + w * 32;
-  const int64_t col_base = (int64_t)blockIdx.x * RO_COLS;
+  using T = MfmaTile<RO_COLS, RO_ROWS, 1, 4>;   // engine rows = tile columns
+  __shared__ __align__(16) float smem[T::LDS_FLOATS];
+  const int c0 = blockIdx.x * RO_COLS;   // first column of the tile
+  const int r0 = blockIdx.y * RO_ROWS;   // first row of the tile
   const int64_t mn = m * n;
-  // this lane's operand coordinates
-  const int64_t arow = row_base + l32;             // A-operand row (a row of the tile)
-  int64_t bcol[RO_TN];
+  const bool vec = (n & 3) == 0;
+  // this lane's outputs: for tm, g: row = r0 + ec, columns cb .. cb+3
+  const int lane = lane_id();
+  const int ec = (wave_id() % 4) * 32 + (lane & 31);
+  const int64_t row = r0 + ec;
+  const int cl = c0 + 4 * (lane >> 5);   // column of (tm, g) is cl + 32 tm + 8 g
+  const int64_t rbase = row * n;
+  auto ncols = [&](int tm, int g) -> int {
+    const int64_t cb = cl + 32 * tm + 8 * g;
+    return row < m ? (int)(n - cb >= 4 ? 4 : (n - cb > 0 ? n - cb : 0)) : 0;
+  };
+  float ghat[2][16], ebar[2][16];
 #pragma unroll
-  for (int tn = 0; tn < RO_TN; ++tn) bcol[tn] = col_base + tn * 32 + l32;
-
-  // element offsets of this lane's outputs, -1 when out of range
-  int64_t off[RO_TN][16];
+  for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-  for (int tn = 0; tn < RO_TN; ++tn)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t i = row_base + mfma32_row(v, lane);
-      const int64_t j = col_base + tn * 32 + l32;
-      off[tn][v] = (i < m && j < n) ? i * n + j : -1;
-    }
-
-  float ghat[RO_TN][16], ebar[RO_TN][16];
-#pragma unroll
-  for (int tn = 0; tn < RO_TN; ++tn)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) { ghat[tn][v] = 0.f; ebar[tn][v] = 0.f; }
+    for (int v = 0; v < 16; ++v) { ghat[tm][v] = 0.f; ebar[tm][v] = 0.f; }
 
   for (int wk = 0; wk < N; ++wk) {
     const float* Gi = G + (int64_t)wk * mn;
     float* Ei = E + (int64_t)wk * mn;
     const float* Qi = Q + (int64_t)wk * r * D;
-    // prefetch M^(i) = G + E for this tile
-    float mv[RO_TN][16];
+    // M^(i) = G + E for this lane's elements, in flight during the product
+    float mv[2][16];
 #pragma unroll
-    for (int tn = 0; tn < RO_TN; ++tn)
+    for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        mv[tn][v] = off[tn][v] >= 0 ? Gi[off[tn][v]] + Ei[off[tn][v]] : 0.f;
-
-    f32x16 acc[RO_TN];
+      for (int g = 0; g < 4; ++g) {
+        const int64_t o = rbase + cl + 32 * tm + 8 * g;
+        const int nc = ncols(tm, g);
+        if (vec && nc == 4) {
+          const float4 a = load_nt4(Gi + o);
+          const float4 b = *reinterpret_cast<const float4*>(Ei + o);
+          mv[tm][4 * g + 0] = a.x + b.x; mv[tm][4 * g + 1] = a.y + b.y;
+          mv[tm][4 * g + 2] = a.z + b.z; mv[tm][4 * g + 3] = a.w + b.w;
+        } else {
 #pragma unroll
-    for (int tn = 0; tn < RO_TN; ++tn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[tn][v] = 0.f;
-
-#pragma unroll 4
-    for (int k0 = 0; k0 < r; k0 += 2) {
-      const int k = k0 + kh;
-      const bool kok = k < r;
-      float a, b[RO_TN];
-      if (!RIGHT) {
-        // left: rows are a (< d), cols are b (< D):  A = P[a][k] = Ut[J[k]][a], B = Q[k][b]
-        a = (kok && arow < d) ? Ut[(int64_t)J[k] * d + arow] : 0.f;
-#pragma unroll
-        for (int tn = 0; tn < RO_TN; ++tn) b[tn] = (kok && bcol[tn] < D) ? Qi[(int64_t)k * D + bcol[tn]] : 0.f;
-      } else {
-        // right: rows are b (< D), cols are a (< d):  A = Q[k][b], B = P^T[k][a] = Ut[J[k]][a]
-        a = (kok && arow < D) ? Qi[(int64_t)k * D + arow] : 0.f;
-#pragma unroll
-        for (int tn = 0; tn < RO_TN; ++tn) b[tn] = (kok && bcol[tn] < d) ? Ut[(int64_t)J[k] * d + bcol[tn]] : 0.f;
+          for (int e = 0; e < 4; ++e)
+            mv[tm][4 * g + e] = e < nc ? Gi[o + e] + Ei[o + e] : 0.f;
+        }
       }
-#pragma unroll
-      for (int tn = 0; tn < RO_TN; ++tn) acc[tn] = mfma32(a, b[tn], acc[tn]);
+    T tile;
+    if (!RIGHT) {
+      // rows a < d, columns b < D: C[a][b] = sum_k Ut[J[k]][a] Q[k][b]
+      LoadR<RO_COLS, 32, false> la(Qi, nullptr, D, c0, (int)D, r);
+      LoadR<RO_ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+      tile.run(la, lb, r, smem);
+    } else {
+      // rows b < D, columns a < d: C[b][a] = sum_k Q[k][b] Ut[J[k]][a]
+      LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
+      LoadR<RO_ROWS, 32, false> lb(Qi, nullptr, D, r0, (int)D, r);
+      tile.run(la, lb, r, smem);
     }
-
 #pragma unroll
-    for (int tn = 0; tn < RO_TN; ++tn)
+    for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        if (off[tn][v] < 0) continue;
-        const float c = acc[tn][v];
-        const float e = mv[tn][v] - c;
-        Ei[off[tn][v]] = e;
-        ebar[tn][v] += e;
-        ghat[tn][v] += c;
+      for (int g = 0; g < 4; ++g) {
+        float ev[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int v = 4 * g + e;
+          const float c = tile.acc[tm][0][v];
+          ev[e] = mv[tm][v] - c;
+          ghat[tm][v] += c;
+          ebar[tm][v] += ev[e];
+        }
+        const int64_t o = rbase + cl + 32 * tm + 8 * g;
+        const int nc = ncols(tm, g);
+        if (vec && nc == 4) {
+          *reinterpret_cast<float4*>(Ei + o) = make_float4(ev[0], ev[1], ev[2], ev[3]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (e < nc) Ei[o + e] = ev[e];
+        }
       }
   }
 
   const float fN = (float)N;
 #pragma unroll
-  for (int tn = 0; tn < RO_TN; ++tn)
+  for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t o = off[tn][v];
-      if (o < 0) continue;
-      Ebar[o] = ebar[tn][v] / fN;
-      const float gh = ghat[tn][v] / fN;
-      float x = X[o];
-      if (OPT == 0) {
-        const float mm = op.beta1 * S1[o] + (1.0f - op.beta1) * gh;
-        S1[o] = mm;
-        x = x - op.lr * mm;
+    for (int g = 0; g < 4; ++g) {
+      const int64_t o = rbase + cl + 32 * tm + 8 * g;
+      const int nc = ncols(tm, g);
+      if (nc == 0) continue;
+      const bool full = vec && nc == 4;
+      float xv[4], s1[4], s2[4], eb[4];
+      if (full) {
+        const float4 a = *reinterpret_cast<const float4*>(X + o);
+        const float4 b = *reinterpret_cast<const float4*>(S1 + o);
+        xv[0] = a.x; xv[1] = a.y; xv[2] = a.z; xv[3] = a.w;
+        s1[0] = b.x; s1[1] = b.y; s1[2] = b.z; s1[3] = b.w;
+        if (OPT == 1) {
+          const float4 c = *reinterpret_cast<const float4*>(S2 + o);
+          s2[0] = c.x; s2[1] = c.y; s2[2] = c.z; s2[3] = c.w;
+        }
       } else {
-        const float m1 = op.beta1 * S1[o] + (1.0f - op.beta1) * gh;
-        const float m2 = op.beta2 * S2[o] + (1.0f - op.beta2) * gh * gh;
-        S1[o] = m1;
-        S2[o] = m2;
-        x = x - op.lr * m1 / (sqrtf(m2) + op.eps);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xv[e] = e < nc ? X[o + e] : 0.f;
+          s1[e] = e < nc ? S1[o + e] : 0.f;
+          if (OPT == 1) s2[e] = e < nc ? S2[o + e] : 0.f;
+        }
       }
-      X[o] = x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = 4 * g + e;
+        eb[e] = ebar[tm][v] / fN;
+        const float gh = ghat[tm][v] / fN;
+        if (OPT == 0) {
+          s1[e] = op.beta1 * s1[e] + (1.0f - op.beta1) * gh;
+          xv[e] = xv[e] - op.lr * s1[e];
+        } else {
+          s1[e] = op.beta1 * s1[e] + (1.0f - op.beta1) * gh;
+          s2[e] = op.beta2 * s2[e] + (1.0f - op.beta2) * gh * gh;
+          xv[e] = xv[e] - op.lr * s1[e] / (sqrtf(s2[e]) + op.eps);
+        }
+      }
+      if (full) {
+        *reinterpret_cast<float4*>(Ebar + o) = make_float4(eb[0], eb[1], eb[2], eb[3]);
+        *reinterpret_cast<float4*>(X + o) = make_float4(xv[0], xv[1], xv[2], xv[3]);
+        *reinterpret_cast<float4*>(S1 + o) = make_float4(s1[0], s1[1], s1[2], s1[3]);
+        if (OPT == 1) *reinterpret_cast<float4*>(S2 + o) = make_float4(s2[0], s2[1], s2[2], s2[3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (e >= nc) continue;
+          Ebar[o + e] = eb[e];
+          X[o + e] = xv[e];
+          S1[o + e] = s1[e];
+          if (OPT == 1) S2[o + e] = s2[e];
+        }
+      }
     }
 }
 
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  if (v.r > RO_MAX_R) return hipErrorInvalidValue;
   dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + RO_ROWS - 1) / RO_ROWS));
 #define GLR_RO(OPT, R)                                                                              \
   hipLaunchKernelGGL((k_resid_opt<OPT, R>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q,    \
