@@ -240,8 +240,15 @@ k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ c
   const double* src = part + (int64_t)pair * nslices * (kJP * kJP);
   double dmax = 0.0;
   for (int e = tid; e < kJP * kJP; e += 256) {
+    // slice partials summed in slice order; loads issued 8 at a time
     double s = 0.0;
-    for (int k = 0; k < nslices; ++k) s += src[(int64_t)k * kJP * kJP + e];
+    for (int k0 = 0; k0 < nslices; k0 += 8) {
+      double t[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t[j] = k0 + j < nslices ? src[(int64_t)(k0 + j) * kJP * kJP + e] : 0.0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += t[j];
+    }
     Gb[0][e / kJP][e % kJP] = s;
     Vb[0][e / kJP][e % kJP] = (e / kJP == e % kJP) ? 1.0 : 0.0;
     if (e / kJP == e % kJP) dmax = fmax(dmax, s);

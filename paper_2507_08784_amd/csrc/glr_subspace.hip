@@ -110,8 +110,15 @@ __global__ void k_reduce_splits(const float* __restrict__ part, int splits, int6
                                 float* __restrict__ out32, double* __restrict__ out64) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += stride) {
+    // partials summed in split order; loads issued 8 at a time
     double s = 0.0;
-    for (int z = 0; z < splits; ++z) s += (double)part[(int64_t)z * count + i];
+    for (int z0 = 0; z0 < splits; z0 += 8) {
+      float t[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t[j] = z0 + j < splits ? part[(int64_t)(z0 + j) * count + i] : 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += (double)t[j];
+    }
     if (out32) out32[i] = (float)s;
     if (out64) out64[i] = s;
   }
