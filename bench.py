@@ -227,6 +227,7 @@ def main():
         raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
     prof = comp.profile_query() if not args.no_profile else {}
     sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
+    history = [round(h, 9) for h in comp.sweep_history(0)[2]]
     n_refresh = sum(1 for t in range(args.warmup, args.warmup + args.steps) if t % wl.tau == 0)
     print(f"[bench] timed {args.steps} steps ({n_refresh} refresh): {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
@@ -260,6 +261,7 @@ def main():
         "kernels": kernels,
         "groups": groups,
         "refresh_sweeps_last": sweeps,
+        "refresh_history_last": history,
         "status": glr.STATUS_NAMES.get(status, status),
     }
     if not args.no_cpu_baseline:
