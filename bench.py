@@ -14,9 +14,12 @@ Inputs are resident in HBM before the timed region: the planted part of the
 synthetic gradients is drawn on the host, the per-step noise on the device
 from a seeded torch generator, into a pool of distinct gradient batches.
 
-Prints one JSON line: ms/step, effective GB/s, the roofline of the dominant
-kernel group (live HIP-event timing on the library's stream), the per-group
-breakdown, and the CPU oracle timed on a bounded sample.
+Steps t = W .. W+K-1 are timed with no instrumentation inside the step; the
+next K steps run again with HIP events around every launch group, on the
+library's stream, for the per-kernel averages.  Prints one JSON line: ms/step,
+effective GB/s, the roofline of the dominant kernel (its algorithmic work per
+launch over its average event-timed duration), the per-kernel breakdown, and
+the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -46,61 +49,95 @@ def jac_pairs(d, jb=16):
     return seats // 2, seats - 1
 
 
-def group_work(wl, name, launches_per_step=None):
-    """Algorithmic bytes and flops of ONE launch of a kernel group, summed
-    over the matrices of the workload (each group launches once per matrix
-    per step, so per-launch figures are per matrix; we report the mean)."""
+def uses_subspace(wl, d):
+    r = min(wl.rank, d)
+    return wl.tau == 1 and r < d and r <= 256
+
+
+FP64_ALU_PEAK = 78.6e12     # fp64 vector flop/s (the pair eigensolves)
+
+# groups that are one kernel launch each (the candidates for the dominant kernel)
+KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_gram", "jac_solve", "jac_apply",
+                 "rr_gram", "rr_solve", "rr_apply", "sub_z", "sub_p", "sub_chol")
+
+
+def jacobi_work(kind, d, D):
+    """Per-launch work of one Jacobi round on a d x D row set (16-row blocks,
+    32-row pairs): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64 ALU flops)."""
+    pairs, _ = jac_pairs(d)
+    if kind == "gram":      # 32 x 32 pair Grams over D columns (fp64 MFMA)
+        return pairs * 32.0 * D * 4, 0.0, pairs * 2.0 * 32 * 32 * D, 0.0
+    if kind == "solve":     # one cyclic sweep of 32 x 32 two-sided Jacobi per pair:
+        # 496 rotations, each updating two rows and two columns of G and two columns of V
+        return 0.0, 0.0, 0.0, pairs * 496.0 * (6 * 32 * 3)
+    # apply: read + write the 32 rows of [W | U^T] of every pair
+    return pairs * 32.0 * (D + d) * 8, pairs * 2.0 * 32 * 32 * (D + d), 0.0, 0.0
+
+
+def group_work(wl, name):
+    """Algorithmic bytes and flops of ONE launch of a kernel group, averaged
+    over the matrices of the workload that launch it: (bytes, fp32 MFMA
+    flops, fp64 MFMA flops, fp64 ALU flops)."""
     N = wl.workers
-    byts = flops = flops64 = 0.0
+    tot = [0.0, 0.0, 0.0, 0.0]
+    count = 0
     for shape in wl.shapes:
         m, n, d, D = dims(shape)
         r = min(wl.rank, d)
         mn = m * n
         adam = wl.opt == "adam"
+        sub = uses_subspace(wl, d)
+        K = min(2 * r, d)
+        w = None
         if name == "ef_mean":
-            byts += 4.0 * (N + 2) * mn
-        elif name == "select":
-            flops += 2.0 * d * d * D
-            byts += 4.0 * (d * D + d * d)
+            w = (4.0 * (N + 2) * mn, 0, 0, 0)
+        elif name == "select" and r < d:
+            w = (4.0 * (d * D + d * d), 2.0 * d * d * D, 0, 0)
         elif name == "proj":
-            flops += 2.0 * r * d * D * N
-            byts += 8.0 * N * mn + 4.0 * N * r * D
+            w = (8.0 * N * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
         elif name == "resid_opt":
-            flops += 2.0 * r * d * D * N
-            byts += (12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D
-        elif name == "jac_gram_solve":
-            # pair Grams (fp64 MFMA): 32 x 32 x D per pair
-            pairs, _ = jac_pairs(d)
-            flops64 += pairs * 2.0 * 32 * 32 * D
-            byts += pairs * 32.0 * D * 4
-        elif name == "jac_apply":
-            # rotation of 32 rows of [W | U^T] per pair: read + write
-            pairs, _ = jac_pairs(d)
-            flops += pairs * 2.0 * 32 * 32 * (D + d)
-            byts += pairs * 32.0 * (D + d) * 8
-    k = len(wl.shapes)
-    return byts / k, flops / k, flops64 / k
+            w = ((12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
+        elif name.startswith("jac_") and not sub:
+            w = jacobi_work(name[4:], d, D)
+        elif name.startswith("rr_") and sub:
+            w = jacobi_work(name[3:], K, D)
+        elif name in ("sub_z", "sub_p") and sub:
+            w = (4.0 * (d * D + K * d + K * D), 2.0 * K * d * D, 0, 0)
+        elif name == "sub_chol" and sub:
+            w = (0.0, 0.0, 0.0, 2.0 * K ** 3 / 3.0)
+        if w is not None:
+            count += 1
+            for i in range(4):
+                tot[i] += w[i]
+    if count == 0:
+        return None
+    return tuple(x / count for x in tot)
 
 
 def roofline_entry(wl, name, total_ms, launches):
-    if launches == 0 or total_ms <= 0:
+    work = group_work(wl, name)
+    if work is None or launches == 0 or total_ms <= 0:
         return None
     avg_s = total_ms / 1e3 / launches
-    byts, flops, flops64 = group_work(wl, name)
+    byts, f32, f64, alu = work
     t_hbm = byts / HBM_PEAK
-    t_mfma = flops / FP32_MFMA_PEAK + flops64 / FP64_MFMA_PEAK
-    if t_hbm == 0 and t_mfma == 0:
+    t_mfma = f32 / FP32_MFMA_PEAK + f64 / FP64_MFMA_PEAK
+    t_alu = alu / FP64_ALU_PEAK
+    base = {"kernel": name, "avg_us": avg_s * 1e6, "launches": launches,
+            "bytes_per_launch": byts, "flops_per_launch": f32 + f64 + alu}
+    if t_hbm == 0 and t_mfma == 0 and t_alu == 0:
         return None
-    if t_hbm >= t_mfma:
-        return {"kernel": name, "bound": "hbm", "achieved": byts / avg_s / 1e9,
-                "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": t_hbm / avg_s,
-                "avg_us": avg_s * 1e6, "launches": launches, "bytes_per_launch": byts,
-                "flops_per_launch": flops + flops64}
-    tot = flops + flops64
-    return {"kernel": name, "bound": "mfma", "achieved": tot / avg_s / 1e12,
-            "peak": tot / t_mfma / 1e12, "unit": "TFLOP/s", "frac": t_mfma / avg_s,
-            "avg_us": avg_s * 1e6, "launches": launches, "bytes_per_launch": byts,
-            "flops_per_launch": tot}
+    if t_hbm >= t_mfma and t_hbm >= t_alu:
+        base.update({"bound": "hbm", "achieved": byts / avg_s / 1e9, "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": t_hbm / avg_s})
+    elif t_mfma >= t_alu:
+        fl = f32 + f64
+        base.update({"bound": "mfma", "achieved": fl / avg_s / 1e12, "peak": fl / t_mfma / 1e12,
+                     "unit": "TFLOP/s", "frac": t_mfma / avg_s})
+    else:
+        base.update({"bound": "alu", "achieved": alu / avg_s / 1e12, "peak": FP64_ALU_PEAK / 1e12,
+                     "unit": "TFLOP/s", "frac": t_alu / avg_s})
+    return base
 
 
 def step_bytes(wl):
@@ -212,9 +249,7 @@ def main():
         comp.step(X, batches[t % pool], t)
     torch.cuda.synchronize()
     print(f"[bench] warm-up {args.warmup} steps {time.perf_counter() - t_w:.2f}s", file=sys.stderr, flush=True)
-    comp.profile(not args.no_profile)
-    comp.profile_reset()
-
+    # pass 1: the timed region (no event brackets inside the step)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(args.warmup, args.warmup + args.steps):
@@ -225,15 +260,34 @@ def main():
     status = comp.sync_status()
     if status not in (0, 7):
         raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
-    prof = comp.profile_query() if not args.no_profile else {}
     sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
     history = [round(h, 9) for h in comp.sweep_history(0)[2]]
     n_refresh = sum(1 for t in range(args.warmup, args.warmup + args.steps) if t % wl.tau == 0)
-    print(f"[bench] timed {args.steps} steps ({n_refresh} refresh): {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {args.steps} steps ({n_refresh} refresh): {ms_per_step:.3f} ms/step",
+          file=sys.stderr, flush=True)
+
+    # pass 2: the next K steps (the same number of refreshes when K is a
+    # multiple of tau) with HIP events around every launch group, on the
+    # library's stream: per-kernel averages for the roofline
+    prof, prof_ms = {}, None
+    if not args.no_profile:
+        comp.profile(True)
+        comp.profile_reset()
+        t1 = time.perf_counter()
+        for t in range(args.warmup + args.steps, args.warmup + 2 * args.steps):
+            comp.step(X, batches[t % pool], t)
+        torch.cuda.synchronize()
+        prof_ms = (time.perf_counter() - t1) * 1e3 / args.steps
+        prof = comp.profile_query()
+        comp.profile(False)
+        status = comp.sync_status()
+        if status not in (0, 7):
+            raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
+        print(f"[bench] profiled pass: {prof_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     kernels = []
-    for name in ("ef_mean", "select", "proj", "resid_opt", "jac_gram_solve", "jac_apply"):
-        if name in prof:
+    for name in KERNEL_GROUPS:
+        if name in prof and prof[name][1]:
             e = roofline_entry(wl, name, *prof[name])
             if e:
                 e["total_ms"] = prof[name][0]
@@ -244,6 +298,7 @@ def main():
     if dominant:
         roof = {k: dominant[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
         roof["kernel"] = dominant["kernel"]
+        roof["avg_us"] = dominant["avg_us"]
         roof["traffic"] = None
 
     eff = step_bytes(wl) / (ms_per_step / 1e3) / 1e9
@@ -258,6 +313,7 @@ def main():
                    "refresh_steps_timed": n_refresh},
         "effective_GBps": round(eff, 1),
         "roofline": roof,
+        "profiled_ms_per_step": None if prof_ms is None else round(prof_ms, 4),
         "kernels": kernels,
         "groups": groups,
         "refresh_sweeps_last": sweeps,

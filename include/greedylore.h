@@ -103,8 +103,8 @@ typedef struct {
   uint64_t seed;               /* Philox4x32-10 key of the random vectors v_j */
   int32_t max_sweeps;          /* bound on Jacobi sweeps per refresh, >= 1 */
   float tol;                   /* Jacobi stop, in (0, 1): every pair of rows of W = U^T Mbar has
-                                  |w_p.w_q| <= tol max(|w_p|, f) max(|w_q|, f),
-                                  f = (2^-24 / tol) max_k |w_k| */
+                                  |w_p.w_q| <= tol max(|w_p||w_q|, ||w_p|^2 - |w_q|^2|, f^2),
+                                  f = 2^-10 max_k |w_k| (cosine and rotation angle below tol) */
   uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START */
 } glr_config;
 
@@ -182,12 +182,20 @@ typedef enum {
   GLR_PROF_RESID_OPT = 5,    /* residual + mean + reconstruction + optimizer */
   GLR_PROF_FULL_REFRESH = 6, /* Algorithm 3 refresh update */
   GLR_PROF_JAC_INIT = 7,     /* refresh: Jacobi initialisation (warm start product) */
-  GLR_PROF_JAC_ROUND = 8,    /* refresh: pair Grams and pair eigensolves of one Jacobi round */
+  GLR_PROF_JAC_GRAM = 8,     /* refresh: partial pair Grams of one Jacobi round */
   GLR_PROF_JAC_FINISH = 9,   /* refresh: norms, sort, permutation */
   GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
-  GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration */
+  GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration (all its launches) */
   GLR_PROF_JAC_APPLY = 12,   /* refresh: rotations of one Jacobi round */
-  GLR_PROF_COUNT = 13
+  GLR_PROF_JAC_SOLVE = 13,   /* refresh: pair eigensolves of one Jacobi round */
+  GLR_PROF_RR_GRAM = 14,     /* tau = 1 Rayleigh-Ritz Jacobi (K x D): pair Grams */
+  GLR_PROF_RR_SOLVE = 15,    /* tau = 1 Rayleigh-Ritz Jacobi: pair eigensolves */
+  GLR_PROF_RR_APPLY = 16,    /* tau = 1 Rayleigh-Ritz Jacobi: rotations */
+  GLR_PROF_SUB_Z = 17,       /* tau = 1: Z = P^T Mo (K x D product) */
+  GLR_PROF_SUB_P = 18,       /* tau = 1: Z Mo^T (K x d split-K product, before its reduction) */
+  GLR_PROF_SUB_ORTH = 19,    /* tau = 1: CholeskyQR2 orthonormalisations (all their launches) */
+  GLR_PROF_SUB_CHOL = 20,    /* tau = 1: K x K Cholesky factor and inverse */
+  GLR_PROF_COUNT = 21
 } glr_prof_group;
 
 glr_status glr_profile_enable(glr_handle* h, int32_t on);

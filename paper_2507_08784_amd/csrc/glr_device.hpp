@@ -243,8 +243,11 @@ struct MfmaTile {
     }
   }
 
+  // acc += A B over K.  With `dacc`, the fp32 accumulators are added into
+  // fp64 ones after every 16 BK slices and cleared, so that rounding grows with
+  // that length only (dacc holds the result then; acc is zero).
   template <class LA, class LB>
-  __device__ void run(LA& la, LB& lb, int K, float* smem) {
+  __device__ void run(LA& la, LB& lb, int K, float* smem, double (*dacc)[TN][16] = nullptr) {
     float* As = smem;
     float* Bs = smem + SA;
     const int nk = (K + BK - 1) / BK;
@@ -261,6 +264,17 @@ struct MfmaTile {
         lb.fetch((kb + 1) * BK);
       }
       compute(As, Bs);
+      if (dacc && ((kb & 15) == 15 || !more)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              dacc[i][j][v] += (double)acc[i][j][v];
+              acc[i][j][v] = 0.f;
+            }
+      }
       __syncthreads();
       if (more) {
         la.template put<PA>(As);

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "greedylore.h"
+
 namespace glr {
 
 constexpr int kJB = 16;   // rows per Jacobi block; a pair holds 2 * kJB rows
@@ -31,6 +33,8 @@ struct SubCtl {
 };
 
 constexpr int kMaxSubK = 256;   // largest rank the subspace-iteration refresh takes
+constexpr int kCholTile = 64;   // tile of the K x K Cholesky factorisation
+inline int chol_pad(int K) { return (K + kCholTile - 1) / kCholTile * kCholTile; }
 
 // The tau = 1 refresh needs only span(U[:, :r]): subspace iteration then, on
 // an oversampled block of sub_block(r, d) directions.
@@ -63,6 +67,15 @@ struct MatView {
   float* rr_sigw; int* rr_perm;
 };
 
+// Optional timing brackets around launch groups (glr_prof_group ids); a
+// no-op unless the host runtime installs a callback.
+struct ProfHook {
+  void* ctx = nullptr;
+  void (*fn)(void* ctx, int group, int begin) = nullptr;
+  void begin(int g) const { if (fn) fn(ctx, g, 1); }
+  void end(int g) const { if (fn) fn(ctx, g, 0); }
+};
+
 struct OptParams {
   int opt;                   // 0 MSGD, 1 Adam
   float lr, beta1, beta2, eps;
@@ -86,15 +99,18 @@ int jac_seats(int64_t d);
 int jac_slices(int64_t d, int64_t D);
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
-hipError_t launch_jac_gram_solve(const MatView& v, int round, float tol, int max_inner, hipStream_t s);
+hipError_t launch_jac_gram(const MatView& v, int round, hipStream_t s);
+hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                            hipStream_t s);
 hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
+hipError_t launch_reorth(const MatView& v, hipStream_t s);
 
 // subspace iteration (tau = 1)
 size_t sub_part_floats(int K, int64_t d, int64_t D);
 hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStream_t s);
-hipError_t launch_sub_iter(const MatView& v, float tol, hipStream_t s);
+hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hipStream_t s);
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s);
 hipError_t launch_sub_rr_end(const MatView& v, hipStream_t s);
 

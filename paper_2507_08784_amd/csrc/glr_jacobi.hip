@@ -217,41 +217,64 @@ k_jac_gram(const float* __restrict__ W, int64_t d, int64_t D, const JacCtl* __re
 constexpr int JAC_CHUNK = 512;   // columns of [W | Utw] rotated by one block
 
 // Eigenvectors V of the pair Gram by cyclic two-sided Jacobi in LDS (fp64).
-// Convergence measure of a pair (p, q):
-//   |w_p . w_q| / (max(|w_p|, f) max(|w_q|, f)),   f = eta * max_k |w_k|,
-// with eta = 2^-24 / tol: rows above the floor f are orthogonalised to a
-// relative tolerance tol; below it, to the absolute level 2^-24 max_k |w_k|
-// that fp32 data resolves (a backward error at fp32 rounding).
+// Convergence measure of a pair of rows (p, q):
+//   |w_p . w_q| / max(|w_p| |w_q|,  | |w_p|^2 - |w_q|^2 |,  f^2),
+//   f = 2^-10 max_k |w_k|.
+// Below tol it bounds both the cosine of the two rows and the angle of the
+// rotation that would still separate them, so that a converged basis is
+// accurate for every singular-vector subspace whose gap in sigma^2 is above
+// f^2 = 2^-20 sigma_1^2 -- far below what the fp32 data resolves -- without
+// chasing orthogonality between tiny rows that fp32 rounding re-creates.
+//
+// A sweep of the 32 x 32 eigenproblem is 31 steps of 16 disjoint rotations
+// (circle method).  In a step, thread (a, b) of the 256 owns the 2 x 2 block
+// rows {p_a, q_a} x columns {p_b, q_b} of G and of V, so that the update
+// G <- J^T G J, V <- V J is in place and private to the thread; thread (a, a)
+// first computes rotation a from its own diagonal block.
+__device__ __forceinline__ void inner_pair(int rd, int k, int& p, int& q) {
+  constexpr int last = kJP - 1;
+  if (k == 0) { p = rd; q = last; }
+  else { p = (rd + k) % last; q = (rd - k + last) % last; }
+  if (p > q) { const int t = p; p = q; q = t; }
+}
+
 __global__ void __launch_bounds__(256)
 k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ ctl, int round,
-            int seats, int nb, float tol, int max_inner, float* __restrict__ Vout,
+            int seats, int nb, float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
             int* __restrict__ skip) {
   if (ctl->converged) return;
   const int pair = blockIdx.x;
   int bi, bj;
   pair_blocks(round, pair, seats, bi, bj);
   if (bi >= nb && bj >= nb) return;
-  __shared__ double Gb[2][kJP][kJP + 1];
-  __shared__ double Vb[2][kJP][kJP + 1];
-  __shared__ double cx[kJP], sx[kJP];
-  __shared__ int px[kJP];
+  __shared__ double G[kJP][kJP + 1];
+  __shared__ double V[kJP][kJP + 1];
+  __shared__ double rc[kJP / 2], rs[kJP / 2];
   __shared__ double red[4];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+  const double rm_prev = __longlong_as_double((long long)ctl->rowmax2_bits);
+  // slice partials summed in slice order; all loads of a batch issued together
   const double* src = part + (int64_t)pair * nslices * (kJP * kJP);
+  double g[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int z0 = 0; z0 < nslices; z0 += 8) {
+    double t[4][8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        t[k][j] = z0 + j < nslices ? src[(int64_t)(z0 + j) * kJP * kJP + tid + 256 * k] : 0.0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) g[k] += t[k][j];
+  }
   double dmax = 0.0;
-  for (int e = tid; e < kJP * kJP; e += 256) {
-    // slice partials summed in slice order; loads issued 8 at a time
-    double s = 0.0;
-    for (int k0 = 0; k0 < nslices; k0 += 8) {
-      double t[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) t[j] = k0 + j < nslices ? src[(int64_t)(k0 + j) * kJP * kJP + e] : 0.0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) s += t[j];
-    }
-    Gb[0][e / kJP][e % kJP] = s;
-    Vb[0][e / kJP][e % kJP] = (e / kJP == e % kJP) ? 1.0 : 0.0;
-    if (e / kJP == e % kJP) dmax = fmax(dmax, s);
+  for (int k = 0; k < 4; ++k) {
+    const int e = tid + 256 * k, x = e / kJP, y = e % kJP;
+    G[x][y] = g[k];
+    V[x][y] = x == y ? 1.0 : 0.0;
+    if (x == y) dmax = fmax(dmax, g[k]);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, o, 64));
@@ -261,37 +284,36 @@ k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ c
   __syncthreads();
   if (tid == 0 && dmax > 0.0)
     atomicMax((unsigned long long*)&ctl->rowmax2_bits, (unsigned long long)__double_as_longlong(dmax));
-  const double rowmax2 = fmax(dmax, __longlong_as_double((long long)ctl->rowmax2_bits));
-  const double eta = 0x1p-24 / (double)tol;
-  const double floor2 = eta * eta * rowmax2;
-  double m = 0.0;
-  for (int e = tid; e < kJP * kJP; e += 256) {
-    const int p = e / kJP, q = e % kJP;
-    if (p < q) {
-      const double den = fmax(Gb[0][p][p], floor2) * fmax(Gb[0][q][q], floor2);
-      if (den > 0.0) m = fmax(m, fabs(Gb[0][p][q]) / sqrt(den));
+  const double rowmax2 = fmax(dmax, rm_prev);
+  const double floor2 = floor_rel2 * rowmax2;
+  double m2 = 0.0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int e = tid + 256 * k, x = e / kJP, y = e % kJP;
+    if (x < y) {
+      const double gxx = G[x][x], gyy = G[y][y];
+      const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
+      if (den > 0.0) m2 = fmax(m2, (g[k] / den) * (g[k] / den));
     }
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o, 64));
-  if (lane == 0) red[w] = m;
+  for (int o = 32; o > 0; o >>= 1) m2 = fmax(m2, __shfl_xor(m2, o, 64));
+  if (lane == 0) red[w] = m2;
   __syncthreads();
-  m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  const double m = sqrt(fmax(fmax(red[0], red[1]), fmax(red[2], red[3])));
   if (tid == 0) atomicMax(&ctl->sweep_max_bits, __float_as_uint((float)m));
   if (m <= (double)tol) {
     if (tid == 0) skip[pair] = 1;
     return;
   }
-  int cur = 0;
+  const int a = tid >> 4, b = tid & 15;
   for (int sweep = 0; sweep < max_inner; ++sweep) {
     for (int rd = 0; rd < kJP - 1; ++rd) {
-      if (tid < kJP / 2) {
-        const int last = kJP - 1;
-        int p, q;
-        if (tid == 0) { p = rd; q = last; }
-        else { p = (rd + tid) % last; q = (rd - tid + last) % last; }
-        if (p > q) { const int t = p; p = q; q = t; }
-        const double gpq = Gb[cur][p][q], gpp = Gb[cur][p][p], gqq = Gb[cur][q][q];
+      int pa, qa, pb, qb;
+      inner_pair(rd, a, pa, qa);
+      inner_pair(rd, b, pb, qb);
+      if (a == b) {
+        const double gpq = G[pa][qa], gpp = G[pa][pa], gqq = G[qa][qa];
         double c = 1.0, s = 0.0;
         if (gpq != 0.0 && fabs(gpq) > 1e-17 * sqrt(gpp * gqq)) {
           const double zeta = (gqq - gpp) / (2.0 * gpq);
@@ -301,26 +323,33 @@ k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ c
           c = 1.0 / sqrt(1.0 + t * t);
           s = c * t;
         }
-        // new col p = c col_p - s col_q ; new col q = s col_p + c col_q
-        cx[p] = c; sx[p] = -s; px[p] = q;
-        cx[q] = c; sx[q] = s;  px[q] = p;
+        rc[a] = c;
+        rs[a] = s;
       }
       __syncthreads();
-      const int nxt = cur ^ 1;
-      for (int e = tid; e < kJP * kJP; e += 256) {
-        const int x = e / kJP, y = e % kJP;
-        const int qx = px[x], qy = px[y];
-        const double ax = cx[x], bx = sx[x], ay = cx[y], by = sx[y];
-        Gb[nxt][x][y] = ax * (ay * Gb[cur][x][y] + by * Gb[cur][x][qy]) +
-                        bx * (ay * Gb[cur][qx][y] + by * Gb[cur][qx][qy]);
-        Vb[nxt][x][y] = ay * Vb[cur][x][y] + by * Vb[cur][x][qy];
-      }
+      // J restricted to a pair (p, q) is [[c, s], [-s, c]]
+      const double ca = rc[a], sa = rs[a], cb = rc[b], sb = rs[b];
+      const double g00 = G[pa][pb], g01 = G[pa][qb], g10 = G[qa][pb], g11 = G[qa][qb];
+      const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
+      const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
+      G[pa][pb] = ca * t00 - sa * t10;
+      G[pa][qb] = ca * t01 - sa * t11;
+      G[qa][pb] = sa * t00 + ca * t10;
+      G[qa][qb] = sa * t01 + ca * t11;
+      const double v00 = V[pa][pb], v01 = V[pa][qb], v10 = V[qa][pb], v11 = V[qa][qb];
+      V[pa][pb] = v00 * cb - v01 * sb;
+      V[pa][qb] = v00 * sb + v01 * cb;
+      V[qa][pb] = v10 * cb - v11 * sb;
+      V[qa][qb] = v10 * sb + v11 * cb;
       __syncthreads();
-      cur = nxt;
     }
   }
   float* vo = Vout + (int64_t)pair * kJP * kJP;
-  for (int e = tid; e < kJP * kJP; e += 256) vo[e] = (float)(Vb[cur][e / kJP][e % kJP]);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int e = tid + 256 * k;
+    vo[e] = (float)V[e / kJP][e % kJP];
+  }
   if (tid == 0) skip[pair] = 0;
 }
 
@@ -376,14 +405,21 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
   }
 }
 
-hipError_t launch_jac_gram_solve(const MatView& v, int round, float tol, int max_inner, hipStream_t s) {
+hipError_t launch_jac_gram(const MatView& v, int round, hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   const int nsl = jac_slices(v.d, v.D);
   const int slice_cols = (int)(((v.D + nsl - 1) / nsl + 63) / 64 * 64);
   hipLaunchKernelGGL(k_jac_gram, dim3(pairs, nsl), dim3(256), 0, s, v.W, v.d, v.D, v.ctl, round,
                      seats, nb, slice_cols, v.gram_part);
+  return hipGetLastError();
+}
+
+hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                            hipStream_t s) {
+  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
+  const int nsl = jac_slices(v.d, v.D);
   hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.gram_part, nsl, v.ctl, round,
-                     seats, nb, tol, max_inner, v.Vrot, v.skip);
+                     seats, nb, tol, max_inner, floor_rel2, v.Vrot, v.skip);
   return hipGetLastError();
 }
 

@@ -150,7 +150,7 @@ WsLayout ws_layout(const glr_config* c) {
     mx(mx_d, (uint64_t)x.d);
     if (use_subspace(c->tau, x.r, x.d)) {
       const int Ki = sub_block(x.r, x.d);
-      const uint64_t K = (uint64_t)Ki, Kp = (K + 31) / 32 * 32;
+      const uint64_t K = (uint64_t)Ki, Kp = (uint64_t)chol_pad(Ki);
       mx(s_Kd, K * (uint64_t)x.d);
       mx(s_KD, K * (uint64_t)x.D);
       mx(s_part, (uint64_t)sub_part_floats(Ki, x.d, x.D));
@@ -159,7 +159,7 @@ WsLayout ws_layout(const glr_config* c) {
       mx(r_gram, rp * (uint64_t)jac_slices(Ki, x.D) * kJP * kJP);
       mx(s_KK, K * K);
       mx(s_Kp2, Kp * Kp);
-      mx(s_nt, Kp / 32);
+      mx(s_nt, Kp / kCholTile);
       mx(s_sums, (uint64_t)((x.d + 127) / 128) * ((K + 127) / 128));
     } else {
       const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
@@ -196,9 +196,9 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_spart = take(s_part * 4);
   w.off_sS = take(s_KK * 8);
   w.off_sL = take(s_Kp2 * 8);
-  w.off_sDinv = take(s_nt * 32 * 32 * 8);
+  w.off_sDinv = take(s_nt * kCholTile * kCholTile * 8);
   w.off_sLi = take(s_Kp2 * 8);
-  w.off_sT = take(8 * 32 * 32 * 8);
+  w.off_sT = take(s_Kp2 * 8);
   w.off_sLinv = take(s_Kp2 * 4);
   w.off_sC = take(s_KK * 4);
   w.off_ssums = take(s_sums * 8);
@@ -236,6 +236,7 @@ struct glr_handle {
   bool suspect = false;
   std::string err;
   int jac_inner = 1;   // inner Jacobi sweeps per pair visit
+  double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
   int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
@@ -349,6 +350,27 @@ struct ProfScope {
   }
 };
 
+// the same brackets for groups inside a launcher (ProfHook callback)
+struct HookCtx {
+  glr_handle* h;
+  hipStream_t s;
+  hipEvent_t open[GLR_PROF_COUNT];
+};
+
+void prof_hook_fn(void* ctx, int group, int begin) {
+  HookCtx* c = static_cast<HookCtx*>(ctx);
+  glr_handle* h = c->h;
+  if (!h->prof || group < 0 || group >= GLR_PROF_COUNT) return;
+  hipEvent_t e;
+  if (prof_event(h, &e) != hipSuccess || hipEventRecord(e, c->s) != hipSuccess) return;
+  if (begin) {
+    c->open[group] = e;
+  } else if (c->open[group]) {
+    h->marks.push_back({group, c->open[group], e});
+    c->open[group] = nullptr;
+  }
+}
+
 // folds recorded marks into the totals (waits for them) and recycles events
 hipError_t prof_collect(glr_handle* h) {
   for (const ProfMark& m : h->marks) {
@@ -384,8 +406,12 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
       {
-        ProfScope p(h, s, GLR_PROF_JAC_ROUND);
-        GLR_HIP(h, launch_jac_gram_solve(v, rd, c.tol, h->jac_inner, s));
+        ProfScope p(h, s, GLR_PROF_JAC_GRAM);
+        GLR_HIP(h, launch_jac_gram(v, rd, s));
+      }
+      {
+        ProfScope p(h, s, GLR_PROF_JAC_SOLVE);
+        GLR_HIP(h, launch_jac_solve(v, rd, c.tol, h->jac_inner, h->jac_floor2, s));
       }
       ProfScope p(h, s, GLR_PROF_JAC_APPLY);
       GLR_HIP(h, launch_jac_apply(v, rd, s));
@@ -398,6 +424,7 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   }
   ProfScope p(h, s, GLR_PROF_JAC_FINISH);
   GLR_HIP(h, launch_jac_finish(v, c.max_sweeps, s));
+  GLR_HIP(h, launch_reorth(v, s));
   return GLR_OK;
 }
 
@@ -413,9 +440,11 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
     ProfScope p(h, s, GLR_PROF_JAC_INIT);
     GLR_HIP(h, launch_sub_start(v, warm, c.seed, s));
   }
+  HookCtx hc{h, s, {}};
+  const ProfHook hook{&hc, prof_hook_fn};
   for (int it = 0; it < iters; ++it) {
     ProfScope p(h, s, GLR_PROF_SUB_ITER);
-    GLR_HIP(h, launch_sub_iter(v, sub_tol, s));
+    GLR_HIP(h, launch_sub_iter(v, sub_tol, hook, s));
   }
   MatView rr;
   GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
@@ -423,10 +452,14 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
       {
-        ProfScope p(h, s, GLR_PROF_JAC_ROUND);
-        GLR_HIP(h, launch_jac_gram_solve(rr, rd, c.tol, h->jac_inner, s));
+        ProfScope p(h, s, GLR_PROF_RR_GRAM);
+        GLR_HIP(h, launch_jac_gram(rr, rd, s));
       }
-      ProfScope p(h, s, GLR_PROF_JAC_APPLY);
+      {
+        ProfScope p(h, s, GLR_PROF_RR_SOLVE);
+        GLR_HIP(h, launch_jac_solve(rr, rd, c.tol, h->jac_inner, h->jac_floor2, s));
+      }
+      ProfScope p(h, s, GLR_PROF_RR_APPLY);
       GLR_HIP(h, launch_jac_apply(rr, rd, s));
     }
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
@@ -533,6 +566,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   h->shapes.assign(cfg->shapes, cfg->shapes + cfg->num_mats);
   h->cfg.shapes = h->shapes.data();
   h->ws = wl;
+  if (const char* e = getenv("GLR_JAC_FLOOR")) h->jac_floor2 = ldexp(1.0, -2 * atoi(e));
   if (const char* e = getenv("GLR_JAC_INNER")) {
     const int v = atoi(e);
     if (v >= 1 && v <= 16) h->jac_inner = v;

@@ -274,14 +274,22 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
   const float* Gi = G + (int64_t)w * dD;
   const float* Ei = E + (int64_t)w * dD;
   T tile;
+  // Q is accumulated in fp64 across the 32-long slices of the d contraction
+  double dacc[T::TM][T::TN][16];
+#pragma unroll
+  for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < T::TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dacc[tm][tn][v] = 0.0;
   LoadK<BM, 32, false, true> la(Ut, nullptr, d, m0, r, (int)d, J);
   if (RIGHT) {
     // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
     LoadK<BN, 32, true, false> lb(Gi, Ei, d, n0, (int)D, (int)d, nullptr);
-    tile.run(la, lb, (int)d, smem);
+    tile.run(la, lb, (int)d, smem, dacc);
   } else {
     LoadR<BN, 32, true> lb(Gi, Ei, D, n0, (int)D, (int)d);
-    tile.run(la, lb, (int)d, smem);
+    tile.run(la, lb, (int)d, smem, dacc);
   }
   float* Qi = Q + (int64_t)w * r * D;
 #pragma unroll
@@ -293,7 +301,7 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int k = m0 + tile.row(tm, v);
-        if (k < r) Qi[(int64_t)k * D + b] = tile.acc[tm][tn][v];
+        if (k < r) Qi[(int64_t)k * D + b] = (float)dacc[tm][tn][v];
       }
     }
 }
@@ -351,7 +359,8 @@ constexpr int RO_ROWS = 128, RO_COLS = 64;
 template <int OPT, bool RIGHT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
-            const float* __restrict__ Q, const float* __restrict__ Ut, const int* __restrict__ J,
+            const float* __restrict__ Q, const float* __restrict__ Rbar, const float* __restrict__ Ut,
+            const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
   using T = MfmaTile<RO_COLS, RO_ROWS, 1, 4>;   // engine rows = tile columns
@@ -370,18 +379,18 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     const int64_t cb = cl + 32 * tm + 8 * g;
     return row < m ? (int)(n - cb >= 4 ? 4 : (n - cb > 0 ? n - cb : 0)) : 0;
   };
-  float ghat[2][16], ebar[2][16];
+  float ebar[2][16];
 #pragma unroll
   for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) { ghat[tm][v] = 0.f; ebar[tm][v] = 0.f; }
+    for (int v = 0; v < 16; ++v) ebar[tm][v] = 0.f;
 
   for (int wk = 0; wk < N; ++wk) {
     const float* Gi = G + (int64_t)wk * mn;
     float* Ei = E + (int64_t)wk * mn;
     const float* Qi = Q + (int64_t)wk * r * D;
-    // M^(i) = G + E for this lane's elements, in flight during the product
-    float mv[2][16];
+    // G^(i) and E^(i) for this lane's elements, in flight during the product
+    float gv[2][16], eo[2][16];
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
@@ -391,12 +400,14 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
         if (vec && nc == 4) {
           const float4 a = load_nt4(Gi + o);
           const float4 b = *reinterpret_cast<const float4*>(Ei + o);
-          mv[tm][4 * g + 0] = a.x + b.x; mv[tm][4 * g + 1] = a.y + b.y;
-          mv[tm][4 * g + 2] = a.z + b.z; mv[tm][4 * g + 3] = a.w + b.w;
+          gv[tm][4 * g + 0] = a.x; gv[tm][4 * g + 1] = a.y; gv[tm][4 * g + 2] = a.z; gv[tm][4 * g + 3] = a.w;
+          eo[tm][4 * g + 0] = b.x; eo[tm][4 * g + 1] = b.y; eo[tm][4 * g + 2] = b.z; eo[tm][4 * g + 3] = b.w;
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            mv[tm][4 * g + e] = e < nc ? Gi[o + e] + Ei[o + e] : 0.f;
+          for (int e = 0; e < 4; ++e) {
+            gv[tm][4 * g + e] = e < nc ? Gi[o + e] : 0.f;
+            eo[tm][4 * g + e] = e < nc ? Ei[o + e] : 0.f;
+          }
         }
       }
     T tile;
@@ -420,8 +431,8 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
         for (int e = 0; e < 4; ++e) {
           const int v = 4 * g + e;
           const float c = tile.acc[tm][0][v];
-          ev[e] = mv[tm][v] - c;
-          ghat[tm][v] += c;
+          // (G - P Q) + E: G and P Q nearly cancel, E is the small part
+          ev[e] = (gv[tm][v] - c) + eo[tm][v];
           ebar[tm][v] += ev[e];
         }
         const int64_t o = rbase + cl + 32 * tm + 8 * g;
@@ -436,6 +447,17 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
       }
   }
 
+  // Ghat = P Rbar (the reconstruction of the averaged payload)
+  T tile;
+  if (!RIGHT) {
+    LoadR<RO_COLS, 32, false> la(Rbar, nullptr, D, c0, (int)D, r);
+    LoadR<RO_ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+    tile.run(la, lb, r, smem);
+  } else {
+    LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
+    LoadR<RO_ROWS, 32, false> lb(Rbar, nullptr, D, r0, (int)D, r);
+    tile.run(la, lb, r, smem);
+  }
   const float fN = (float)N;
 #pragma unroll
   for (int tm = 0; tm < 2; ++tm)
@@ -467,7 +489,7 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
       for (int e = 0; e < 4; ++e) {
         const int v = 4 * g + e;
         eb[e] = ebar[tm][v] / fN;
-        const float gh = ghat[tm][v] / fN;
+        const float gh = tile.acc[tm][0][v];
         if (OPT == 0) {
           s1[e] = op.beta1 * s1[e] + (1.0f - op.beta1) * gh;
           xv[e] = xv[e] - op.lr * s1[e];
@@ -499,7 +521,7 @@ hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s)
   dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + RO_ROWS - 1) / RO_ROWS));
 #define GLR_RO(OPT, R)                                                                              \
   hipLaunchKernelGGL((k_resid_opt<OPT, R>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q,    \
-                     v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
+                     v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
   if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
   else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
 #undef GLR_RO

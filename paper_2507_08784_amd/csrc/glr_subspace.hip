@@ -27,6 +27,7 @@ namespace glr {
 // slices of `kslice`; slice z writes C + z * cstride.
 //   EPI 0: C = acc
 //   EPI 1: C = X - acc, and per block the sum of squares of C (fp64) in sums
+//   EPI 2: C = X - acc
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool B_KC, int EPI>
 __global__ void __launch_bounds__(256)
@@ -63,6 +64,8 @@ k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, in
         if (i >= M) continue;
         if (EPI == 0) {
           Cz[(int64_t)i * ldc + j] = tile.acc[tm][tn][v];
+        } else if (EPI == 2) {
+          Cz[(int64_t)i * ldc + j] = X[(int64_t)i * ldc + j] - tile.acc[tm][tn][v];
         } else {
           const float o = X[(int64_t)i * ldc + j] - tile.acc[tm][tn][v];
           Cz[(int64_t)i * ldc + j] = o;
@@ -132,164 +135,357 @@ static int grid_n(int64_t n) {
 }
 
 // ---------------------------------------------------------------------------
-// Cholesky S = L L^T and the inverse L^-1 of a K x K (K <= kMaxSubK) matrix,
-// fp64, one block of 4 waves, 32 x 32 tiles (Kp = K rounded up to 32; the
-// padding is the identity).  Lm, Dinv, Li are fp64 scratch in global memory
-// (L2-resident); the result is written as fp32 Linv (Kp x Kp, zero above the
-// diagonal).  A non-positive pivot sets status bit 4 and is replaced by a
-// tiny positive value so that the sweep can continue.
+// fp64-accumulated Gram products of fp32 rows, C = A B^T (A: M x Kc, B: N x Kc,
+// row-major and contiguous along k): fp32 inputs widened to fp64, fp64 MFMA
+// on 64 x 64 tiles (each wave a 32 x 32 quadrant), grid.z splitting the
+// contraction into slices of kslice.
+//   EPI 0: slice z of C (fp64) at out64 + z M ldo
+//   EPI 1: out32 = (C - I) / 2 (one slice): the Newton-Schulz correction
 // ---------------------------------------------------------------------------
-constexpr int kTile = 32;
-
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+template <int EPI>
+__global__ void __launch_bounds__(256)
+k_gram64(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, int64_t ldb, int M,
+         int N, int Kc, int kslice, double* __restrict__ out64, float* __restrict__ out32, int64_t ldo) {
+  __shared__ float As[32][65];
+  __shared__ float Bs[32][65];
+  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const int k0 = blockIdx.z * kslice;
+  const int k1 = Kc < k0 + kslice ? Kc : k0 + kslice;
+  const int lr = tid >> 2, kq = (tid & 3) * 8;     // loader: row, k offset
+  const bool aok = m0 + lr < M, bok = n0 + lr < N;
+  const float* ap = A + (int64_t)(aok ? m0 + lr : 0) * lda;
+  const float* bp = B + (int64_t)(bok ? n0 + lr : 0) * ldb;
+  const int wi = (w >> 1) * 32, wj = (w & 1) * 32;
+  f64x4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+  float ra[8], rb[8];
+  auto fetch = [&](int kb) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = kb + kq + e;
+      ra[e] = (aok && k < k1) ? ap[k] : 0.f;
+      rb[e] = (bok && k < k1) ? bp[k] : 0.f;
+    }
+  };
+  if (k0 < k1) fetch(k0);
+  for (int kb = k0; kb < k1; kb += 32) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      As[kq + e][lr] = ra[e];
+      Bs[kq + e][lr] = rb[e];
+    }
+    __syncthreads();
+    if (kb + 32 < k1) fetch(kb + 32);
+#pragma unroll
+    for (int ks = 0; ks < 32; ks += 4) {
+      const int k = ks + (lane >> 4);
+      const double a0 = As[k][wi + (lane & 15)], a1 = As[k][wi + 16 + (lane & 15)];
+      const double b0 = Bs[k][wj + (lane & 15)], b1 = Bs[k][wj + 16 + (lane & 15)];
+      acc[0][0] = mfma64(a0, b0, acc[0][0]);
+      acc[0][1] = mfma64(a0, b1, acc[0][1]);
+      acc[1][0] = mfma64(a1, b0, acc[1][0]);
+      acc[1][1] = mfma64(a1, b1, acc[1][1]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = m0 + wi + 16 * x + 4 * v + (lane >> 4);
+        const int j = n0 + wj + 16 * y + (lane & 15);
+        if (i >= M || j >= N) continue;
+        if (EPI == 0) out64[((int64_t)blockIdx.z * M + i) * ldo + j] = acc[x][y][v];
+        else out32[(int64_t)i * ldo + j] = (float)(0.5 * (acc[x][y][v] - (i == j ? 1.0 : 0.0)));
+      }
 }
 
-// C (32x32) = / -= / = -(A B), one wave.  A tile row-major (lda); B given as
-// B[k][j] at Bp[k * ldb + j], or as rows B[j][k] at Bp[j * ldb + k] (b_rows).
-// mode 0: C = A B;  1: C -= A B;  2: C = -(A B).
-__device__ __forceinline__ void tile_mm(const double* A, int lda, const double* Bp, int ldb, bool b_rows, double* Cp,
-                        int ldc, int mode, double (*Bs)[kTile + 1]) {
-  const int lane = lane_id();
-  const int i = lane & 31, half = lane >> 5;
-  for (int e = lane; e < kTile * kTile; e += 64) {
-    const int j = e / kTile, k = e % kTile;   // Bs[j][k] = B(k, j)
-    Bs[j][k] = b_rows ? Bp[j * ldb + k] : Bp[k * ldb + j];
-  }
-  double a[kTile];
-#pragma unroll
-  for (int k = 0; k < kTile; ++k) a[k] = A[i * lda + k];
-  wave_lds_sync();
-  double acc[16];
-#pragma unroll
-  for (int jj = 0; jj < 16; ++jj) {
-    const int j = half * 16 + jj;
+// out[i] = sum over splits of part[s * count + i] in a fixed order (fp64)
+__global__ void k_reduce_splits64(const double* __restrict__ part, int splits, int64_t count,
+                                  double* __restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += stride) {
     double s = 0.0;
+    for (int z0 = 0; z0 < splits; z0 += 8) {
+      double t[8];
 #pragma unroll
-    for (int k = 0; k < kTile; ++k) s += a[k] * Bs[j][k];
-    acc[jj] = s;
-  }
+      for (int j = 0; j < 8; ++j) t[j] = z0 + j < splits ? part[(int64_t)(z0 + j) * count + i] : 0.0;
 #pragma unroll
-  for (int jj = 0; jj < 16; ++jj) {
-    const int j = half * 16 + jj;
-    double* c = Cp + i * ldc + j;
-    if (mode == 0) *c = acc[jj];
-    else if (mode == 1) *c -= acc[jj];
-    else *c = -acc[jj];
+      for (int j = 0; j < 8; ++j) s += t[j];
+    }
+    out[i] = s;
   }
-  wave_lds_sync();
+}
+
+// One Newton-Schulz step towards the nearest orthonormal rows,
+//   U^T <- U^T - (U^T U - I) U^T / 2,
+// with the Gram in fp64: it removes the orthogonality drift that the fp32
+// rotations of a refresh accumulate.  Uses W (d x D >= d x d) and Utw as
+// scratch.
+hipError_t launch_reorth(const MatView& v, hipStream_t s) {
+  const int d = (int)v.d;
+  dim3 g64((d + 63) / 64, (d + 63) / 64, 1);
+  hipLaunchKernelGGL(k_gram64<1>, g64, dim3(256), 0, s, v.Ut, (int64_t)d, v.Ut, (int64_t)d, d, d, d, d,
+                     (double*)nullptr, v.Utw, (int64_t)d);
+  GemmPlan p1{1, d};
+  gemm_launch<false, 2>(v.Utw, d, v.Ut, d, v.W, d, d, d, d, p1, 0, v.Ut, nullptr, s);
+  hipError_t e = hipMemcpyAsync(v.Ut, v.W, (size_t)d * d * 4, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+
+// ---------------------------------------------------------------------------
+// Cholesky S = L L^T and X = L^-1 of the K x K Gram (fp64), blocked in 64 x 64
+// tiles (Kp = K rounded up to 64; the padding is the identity).  One launch
+// per block column p after a first launch that factors tile (0, 0):
+//   trailing tiles (I, Kq), p < Kq <= I:  L_Ip = S_Ip D_p^T,  L_Kqp likewise,
+//       S_IKq -= L_Ip L_Kqp^T; the tile (p+1, p+1) then factors itself and
+//       inverts its factor into D_{p+1} (in LDS);
+//   block row p of X:  X_pp = D_p,  X_pc = -D_p sum_{c <= k < p} L_pk X_kc.
+// Every tile a launch reads was finished by an earlier launch.  Products are
+// fp64 MFMA on LDS tiles.  The result is written as fp32 Linv (Kp x Kp, zero
+// above the diagonal).  A non-positive pivot sets status bit 4 and is replaced
+// by a tiny positive value so that the iteration can continue.
+// ---------------------------------------------------------------------------
+constexpr int CT = kCholTile;
+constexpr int CLD = CT + 1;
+typedef double CTile[CLD];
+
+__device__ __forceinline__ int chol_row(int x, int v) {
+  return (wave_id() >> 1) * 32 + 16 * x + 4 * v + (lane_id() >> 4);
+}
+__device__ __forceinline__ int chol_col(int y) { return (wave_id() & 1) * 32 + 16 * y + (lane_id() & 15); }
+
+// acc (+)= sign * A B^T, A and B 64 x 64 in LDS (rows of B are output columns);
+// each wave owns one 32 x 32 quadrant of the output
+__device__ __forceinline__ void tile_abt(const CTile* A, const CTile* B, double sign, f64x4 (&acc)[2][2]) {
+  const int lane = lane_id(), w = wave_id();
+  const int ri = (w >> 1) * 32 + (lane & 15), cj = (w & 1) * 32 + (lane & 15);
+  const int kk = lane >> 4;
+#pragma unroll 4
+  for (int k0 = 0; k0 < CT; k0 += 4) {
+    const int k = k0 + kk;
+    const double a0 = sign * A[ri][k], a1 = sign * A[ri + 16][k];
+    const double b0 = B[cj][k], b1 = B[cj + 16][k];
+    acc[0][0] = mfma64(a0, b0, acc[0][0]);
+    acc[0][1] = mfma64(a0, b1, acc[0][1]);
+    acc[1][0] = mfma64(a1, b0, acc[1][0]);
+    acc[1][1] = mfma64(a1, b1, acc[1][1]);
+  }
+}
+
+__device__ __forceinline__ void acc_zero(f64x4 (&acc)[2][2]) {
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+}
+
+// LDS tile <- global tile (row-major, ld), optionally transposed
+__device__ __forceinline__ void tile_load(const double* __restrict__ src, int64_t ld, CTile* dst, bool tr) {
+  for (int e = threadIdx.x; e < CT * CT; e += 256) {
+    const int i = e / CT, j = e % CT;
+    const double x = src[(int64_t)i * ld + j];
+    if (tr) dst[j][i] = x;
+    else dst[i][j] = x;
+  }
+}
+
+// global tile <- LDS tile (lower triangle only when `lower`: zeros above)
+__device__ __forceinline__ void tile_store(const CTile* src, double* __restrict__ dst, int64_t ld, bool lower) {
+  for (int e = threadIdx.x; e < CT * CT; e += 256) {
+    const int i = e / CT, j = e % CT;
+    dst[(int64_t)i * ld + j] = (lower && j > i) ? 0.0 : src[i][j];
+  }
+}
+
+__device__ __forceinline__ void tile_store32(const CTile* src, float* __restrict__ dst, int64_t ld) {
+  for (int e = threadIdx.x; e < CT * CT; e += 256) {
+    const int i = e / CT, j = e % CT;
+    dst[(int64_t)i * ld + j] = (float)src[i][j];
+  }
+}
+
+__device__ __forceinline__ void acc_to_lds(const f64x4 (&acc)[2][2], CTile* dst, bool tr) {
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = chol_row(x, v), j = chol_col(y);
+        if (tr) dst[j][i] = acc[x][y][v];
+        else dst[i][j] = acc[x][y][v];
+      }
+}
+
+// in-place Cholesky of the SPD tile T (lower triangle), then Dl = T^-1
+__device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
+  const int tid = threadIdx.x;
+  bool bad = false;
+  for (int j = 0; j < CT; ++j) {
+    double piv = T[j][j];
+    if (!(piv > 0.0)) { bad = true; piv = 1e-300; }
+    const double ljj = sqrt(piv), inv = 1.0 / ljj;
+    __syncthreads();
+    if (tid < CT) {
+      if (tid > j) T[tid][j] *= inv;
+      else if (tid == j) T[j][j] = ljj;
+    }
+    __syncthreads();
+    for (int e = tid; e < CT * CT; e += 256) {
+      const int i = e / CT, k = e % CT;
+      if (k > j && k <= i) T[i][k] -= T[i][j] * T[k][j];
+    }
+    __syncthreads();
+  }
+  if (bad && tid == 0) atomicOr(status, 4u);
+  for (int e = tid; e < CT * CT; e += 256) Dl[e / CT][e % CT] = (e / CT == e % CT) ? 1.0 : 0.0;
+  __syncthreads();
+  // right-looking forward substitution: row j of T^-1 is final once scaled
+  for (int j = 0; j < CT; ++j) {
+    const double inv = 1.0 / T[j][j];
+    if (tid <= j) Dl[j][tid] *= inv;
+    __syncthreads();
+    for (int e = tid; e < CT * CT; e += 256) {
+      const int i = e / CT, c = e % CT;
+      if (i > j && c <= j) Dl[i][c] -= T[i][j] * Dl[j][c];
+    }
+    __syncthreads();
+  }
+}
+
+// copy S (K x K) into the padded work matrix; block 0 factors tile (0, 0)
+__global__ void __launch_bounds__(256)
+k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ Sw,
+             double* __restrict__ Lm, double* __restrict__ Dm, uint32_t* __restrict__ status) {
+  const int64_t n = (int64_t)Kp * Kp;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
+    const int i = (int)(e / Kp), j = (int)(e % Kp);
+    Sw[e] = (i < K && j < K) ? S[(int64_t)i * K + j] : (i == j ? 1.0 : 0.0);
+  }
+  if (blockIdx.x != 0) return;
+  __shared__ CTile T[CT], Dl[CT];
+  for (int e = threadIdx.x; e < CT * CT; e += 256) {
+    const int i = e / CT, j = e % CT;
+    T[i][j] = (i < K && j < K) ? S[(int64_t)i * K + j] : (i == j ? 1.0 : 0.0);
+  }
+  __syncthreads();
+  chol_tile(T, Dl, status);
+  tile_store(T, Lm, Kp, true);
+  tile_store(Dl, Dm, CT, false);
 }
 
 __global__ void __launch_bounds__(256)
-k_chol_inv(const double* __restrict__ S, int K, int Kp, double* __restrict__ Lm,
-           double* __restrict__ Dinv, double* __restrict__ Li, double* __restrict__ Tw,
-           float* __restrict__ Linv, uint32_t* __restrict__ status) {
-  __shared__ double Bs[4][kTile][kTile + 1];
-  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-  const int nt = Kp / kTile;
-  for (int e = tid; e < Kp * Kp; e += 256) {
-    const int i = e / Kp, j = e % Kp;
-    double x;
-    if (i < K && j < K) x = S[(int64_t)i * K + j];
-    else x = (i == j) ? 1.0 : 0.0;
-    Lm[e] = x;
-    Li[e] = 0.0;
+k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, double* __restrict__ Dm,
+            double* __restrict__ Xm, float* __restrict__ Linv, uint32_t* __restrict__ status) {
+  __shared__ CTile A[CT], B[CT], C[CT];
+  const int nt = Kp / CT;
+  const int mrows = nt - p - 1;
+  const int ntrail = mrows * (mrows + 1) / 2;
+  const int b = blockIdx.x;
+  const double* Dp = Dm + (int64_t)p * CT * CT;
+  auto tile = [&](double* base, int I, int J) { return base + (int64_t)I * CT * Kp + (int64_t)J * CT; };
+  f64x4 acc[2][2];
+  if (b < ntrail) {
+    int ip = 0;
+    while ((ip + 1) * (ip + 2) / 2 <= b) ++ip;
+    const int jp = b - ip * (ip + 1) / 2;
+    const int I = p + 1 + ip, Kq = p + 1 + jp;
+    tile_load(Dp, CT, A, false);
+    tile_load(tile(Sw, I, p), Kp, B, false);
+    __syncthreads();
+    acc_zero(acc);
+    tile_abt(B, A, 1.0, acc);          // L_Ip = S_Ip D_p^T
+    __syncthreads();
+    acc_to_lds(acc, B, false);
+    if (Kq != I) {
+      tile_load(tile(Sw, Kq, p), Kp, C, false);
+      __syncthreads();
+      acc_zero(acc);
+      tile_abt(C, A, 1.0, acc);        // L_Kqp
+      __syncthreads();
+      acc_to_lds(acc, C, false);
+    }
+    __syncthreads();
+    const CTile* Lk = (Kq != I) ? C : B;
+    // acc = S_IKq - L_Ip L_Kqp^T
+    double* sik = tile(Sw, I, Kq);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[x][y][v] = sik[(int64_t)chol_row(x, v) * Kp + chol_col(y)];
+    tile_abt(B, Lk, -1.0, acc);
+    if (Kq == p + 1) tile_store(B, tile(Lm, I, p), Kp, false);
+    if (I == p + 1 && Kq == p + 1) {
+      __syncthreads();
+      acc_to_lds(acc, A, false);
+      __syncthreads();
+      chol_tile(A, B, status);
+      tile_store(A, tile(Lm, I, I), Kp, true);
+      tile_store(B, Dm + (int64_t)I * CT * CT, CT, false);
+    } else {
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sik[(int64_t)chol_row(x, v) * Kp + chol_col(y)] = acc[x][y][v];
+    }
+    return;
   }
+  // block row p of X = L^-1, column block c
+  const int c = b - ntrail;
+  float* lo = Linv + (int64_t)p * CT * Kp + (int64_t)c * CT;
+  if (c > p) {
+    for (int e = threadIdx.x; e < CT * CT; e += 256) lo[(int64_t)(e / CT) * Kp + e % CT] = 0.f;
+    return;
+  }
+  tile_load(Dp, CT, A, false);
+  if (c == p) {
+    __syncthreads();
+    tile_store(A, tile(Xm, p, p), Kp, false);
+    tile_store32(A, lo, Kp);
+    return;
+  }
+  acc_zero(acc);
+  for (int k = c; k < p; ++k) {
+    tile_load(tile(Lm, p, k), Kp, B, false);
+    tile_load(tile(Xm, k, c), Kp, C, true);
+    __syncthreads();
+    tile_abt(B, C, 1.0, acc);          // T += L_pk X_kc
+    __syncthreads();
+  }
+  acc_to_lds(acc, C, true);            // C = T^T
   __syncthreads();
-  for (int J = 0; J < nt; ++J) {
-    double* TJJ = Lm + (J * kTile) * Kp + J * kTile;
-    double* DJ = Dinv + J * kTile * kTile;
-    if (w == 0) {
-      // factor the diagonal tile in this wave's LDS tile (right-looking)
-      double (*Tl)[kTile + 1] = Bs[0];
-      for (int e = lane; e < kTile * kTile; e += 64) Tl[e / kTile][e % kTile] = TJJ[(e / kTile) * Kp + e % kTile];
-      wave_lds_sync();
-      bool bad = false;
-      for (int j = 0; j < kTile; ++j) {
-        double piv = Tl[j][j];
-        if (!(piv > 0.0)) { bad = true; piv = 1e-300; }
-        const double ljj = sqrt(piv);
-        wave_lds_sync();
-        if (lane < kTile) {
-          if (lane > j) Tl[lane][j] = Tl[lane][j] / ljj;
-          else if (lane == j) Tl[j][j] = ljj;
-        }
-        wave_lds_sync();
-        for (int e = lane; e < kTile * kTile; e += 64) {
-          const int i = e / kTile, k = e % kTile;
-          if (k > j && k <= i) Tl[i][k] -= Tl[i][j] * Tl[k][j];
-        }
-        wave_lds_sync();
-      }
-      if (bad && lane == 0) atomicOr(status, 4u);
-      for (int e = lane; e < kTile * kTile; e += 64) {
-        const int i = e / kTile, k = e % kTile;
-        TJJ[i * Kp + k] = (k <= i) ? Tl[i][k] : 0.0;
-      }
-      // inverse of the lower-triangular tile: lane c solves L x = e_c
-      if (lane < kTile) {
-        const int c = lane;
-        double x[kTile];
-#pragma unroll
-        for (int ii = 0; ii < kTile; ++ii) {
-          double sacc = (ii == c) ? 1.0 : 0.0;
-#pragma unroll
-          for (int k = 0; k < ii; ++k) sacc -= Tl[ii][k] * x[k];
-          x[ii] = sacc / Tl[ii][ii];
-        }
-#pragma unroll
-        for (int ii = 0; ii < kTile; ++ii) DJ[ii * kTile + c] = x[ii];
-      }
-      wave_lds_sync();
-    }
-    __syncthreads();
-    // panel: L_IJ = A_IJ inv(L_JJ)^T
-    for (int I = J + 1 + w; I < nt; I += 4) {
-      double* AIJ = Lm + (I * kTile) * Kp + J * kTile;
-      tile_mm(AIJ, Kp, DJ, kTile, true, Tw + w * kTile * kTile, kTile, 0, Bs[w]);
-      // copy back (tile_mm cannot write in place: it reads A rows lazily)
-      for (int e = lane; e < kTile * kTile; e += 64)
-        AIJ[(e / kTile) * Kp + e % kTile] = Tw[w * kTile * kTile + e];
-      wave_lds_sync();
-    }
-    __syncthreads();
-    // trailing update: A_IK -= L_IJ L_KJ^T for J < K <= I
-    int idx = 0;
-    for (int I = J + 1; I < nt; ++I)
-      for (int Kq = J + 1; Kq <= I; ++Kq, ++idx) {
-        if (idx % 4 != w) continue;
-        tile_mm(Lm + (I * kTile) * Kp + J * kTile, Kp, Lm + (Kq * kTile) * Kp + J * kTile, Kp, true,
-                Lm + (I * kTile) * Kp + Kq * kTile, Kp, 1, Bs[w]);
-      }
-    __syncthreads();
-  }
-  // inverse by diagonals: Li_II = Dinv_I; Li_IJ = -Dinv_I sum_{J<=Kq<I} L_IKq Li_KqJ
-  for (int I = w; I < nt; I += 4)
-    for (int e = lane; e < kTile * kTile; e += 64)
-      Li[(I * kTile + e / kTile) * Kp + I * kTile + e % kTile] = Dinv[I * kTile * kTile + e];
+  acc_zero(acc);
+  tile_abt(A, C, -1.0, acc);           // X_pc = -D_p T
   __syncthreads();
-  for (int dl = 1; dl < nt; ++dl) {
-    for (int J = w; J + dl < nt; J += 4) {
-      const int I = J + dl;
-      double* T = Tw + w * kTile * kTile;
-      for (int e = lane; e < kTile * kTile; e += 64) T[e] = 0.0;
-      wave_lds_sync();
-      for (int Kq = J; Kq < I; ++Kq) {
-        // T -= -(L_IKq Li_KqJ)  ==  T += L_IKq Li_KqJ  (accumulated as T -= (-1) ...)
-        double* Tn = Tw + (4 + w) * kTile * kTile;
-        tile_mm(Lm + (I * kTile) * Kp + Kq * kTile, Kp, Li + (Kq * kTile) * Kp + J * kTile, Kp,
-                false, Tn, kTile, 0, Bs[w]);
-        for (int e = lane; e < kTile * kTile; e += 64) T[e] += Tn[e];
-        wave_lds_sync();
-      }
-      tile_mm(Dinv + I * kTile * kTile, kTile, T, kTile, false,
-              Li + (I * kTile) * Kp + J * kTile, Kp, 2, Bs[w]);
-    }
-    __syncthreads();
+  acc_to_lds(acc, B, false);
+  __syncthreads();
+  tile_store(B, tile(Xm, p, c), Kp, false);
+  tile_store32(B, lo, Kp);
+}
+
+static hipError_t launch_chol_inv(const MatView& v, int K, hipStream_t s) {
+  const int Kp = chol_pad(K), nt = Kp / CT;
+  hipLaunchKernelGGL(k_chol_first, dim3(16), dim3(256), 0, s, v.sub_S, K, Kp, v.sub_T, v.sub_L,
+                     v.sub_Dinv, v.status);
+  for (int p = 0; p < nt; ++p) {
+    const int m = nt - p - 1;
+    hipLaunchKernelGGL(k_chol_step, dim3(m * (m + 1) / 2 + nt), dim3(256), 0, s, p, Kp, v.sub_T,
+                       v.sub_L, v.sub_Dinv, v.sub_Li, v.sub_Linv, v.status);
   }
-  for (int e = tid; e < Kp * Kp; e += 256) Linv[e] = (float)Li[e];
+  return hipGetLastError();
 }
 
 // cold start: rows of P^T drawn from N(0, 1) with Philox (key seed ^ const)
@@ -349,20 +545,25 @@ size_t sub_part_floats(int K, int64_t d, int64_t D) {
   upd(K, (int)d, (int)D);
   return mx;
 }
-static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, hipStream_t s) {
-  const int Kp = (K + kTile - 1) / kTile * kTile;
+static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, const ProfHook& prof,
+                            hipStream_t s) {
+  const int Kp = chol_pad(K);
+  prof.begin(GLR_PROF_SUB_ORTH);
   for (int pass = 0; pass < 2; ++pass) {
     GemmPlan pg = plan_splits(K, K, (int)L);
     gemm_launch<true, 0>(Y, L, Y, L, v.sub_part, K, K, K, (int)L, pg, (int64_t)K * K, nullptr, nullptr, s);
     hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
                        pg.splits, (int64_t)K * K, (float*)nullptr, v.sub_S);
-    hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, v.sub_S, K, Kp, v.sub_L, v.sub_Dinv,
-                       v.sub_Li, v.sub_T, v.sub_Linv, v.status);
+    prof.begin(GLR_PROF_SUB_CHOL);
+    hipError_t ce = launch_chol_inv(v, K, s);
+    if (ce != hipSuccess) return ce;
+    prof.end(GLR_PROF_SUB_CHOL);
     GemmPlan p1{1, K};
     gemm_launch<false, 0>(v.sub_Linv, Kp, Y, L, Ytmp, L, K, (int)L, K, p1, 0, nullptr, nullptr, s);
     hipError_t e = hipMemcpyAsync(Y, Ytmp, (size_t)K * L * 4, hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
   }
+  prof.end(GLR_PROF_SUB_ORTH);
   return hipGetLastError();
 }
 
@@ -378,30 +579,34 @@ hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStrea
                        v.sub_P, K, v.d, k0, k1, (uint32_t)v.mat);
   }
   hipLaunchKernelGGL(k_sub_reset, dim3(1), dim3(64), 0, s, v.sub_ctl);
-  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, s);
+  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, ProfHook{}, s);
 }
 
 // one iteration; writes the subspace change into sub_ctl
-hipError_t launch_sub_iter(const MatView& v, float tol, hipStream_t s) {
+hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d, D = v.D;
   // Z = P^T Mo  (K x D)
   GemmPlan p1{1, (int)d};
+  prof.begin(GLR_PROF_SUB_Z);
   if (v.right)   // Mo[a][b] = Mbar[b][a]: B(k=a, j=b) at Mbar[b d + a]
     gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
   else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
     gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
-  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, s);
+  prof.end(GLR_PROF_SUB_Z);
+  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, prof, s);
   if (e != hipSuccess) return e;
   // P_new = Z Mo^T  (K x d): B(k=b, j=a) = Mo[a][b]
   GemmPlan p2 = plan_splits(K, (int)d, (int)D);
+  prof.begin(GLR_PROF_SUB_P);
   if (v.right)   // Mbar[b d + a]: contiguous along j
     gemm_launch<false, 0>(v.sub_Z, D, v.Mbar, d, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr, nullptr, s);
   else           // Mbar[a D + b]: contiguous along k
     gemm_launch<true, 0>(v.sub_Z, D, v.Mbar, D, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr, nullptr, s);
+  prof.end(GLR_PROF_SUB_P);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_part,
                      p2.splits, (int64_t)K * d, v.sub_Pn, (double*)nullptr);
-  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, s);
+  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, prof, s);
   if (e != hipSuccess) return e;
   // change: R = P_new - (P_new P^T) P ;  C = P_new P^T (K x K)
   GemmPlan pc = plan_splits(K, K, (int)d);

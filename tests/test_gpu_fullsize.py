@@ -1,0 +1,265 @@
+"""GPU checks at the workloads' full shapes, in the launch configuration the
+benchmark times (same library, same kernels, the full N x m x n batches).
+
+The oracle cannot run a complete step at these sizes in a test's time, so:
+  * the streaming parts (error feedback, projection, residual, mean,
+    reconstruction, optimizer) are checked on sampled columns of the oriented
+    problem, which are independent of one another given P: the oracle's
+    formulas run in fp64 on the same fp32 inputs and the GPU's P;
+  * the refresh basis is checked against properties that hold at any size
+    (orthonormality, the eigen-residual of M-bar M-bar^T, descending sigma,
+    the trace and Eckart-Young identities) and, for the gapped 4096 x 4096
+    layer, against the top-r subspace of M-bar from an fp64 symmetric
+    eigensolver;
+  * the Approx-Top-r scores are checked at sampled indices (every selected
+    index, the runners-up and random others) against fp64 bilinear forms with
+    the v_j of the Philox stream, and J against the fp64 ranking of them.
+"""
+import numpy as np
+import pytest
+
+from oracle.method import adam_update, argtop_r, msgd_update
+from oracle.philox import gaussian_vectors
+from synth import get_workload, noise_level, planted_matrix
+
+pytestmark = pytest.mark.gpu
+
+STEP_TOL = 1e-4      # relative Frobenius bar per step
+MARGIN = 1e-4        # selection margin below which either choice is correct
+
+
+def _say(*a):
+    print("[fullsize]", *a, flush=True)
+
+
+def _oriented(a, right):
+    """m x n (or N x m x n) -> d x D (N x d x D) view of the oriented problem."""
+    return a.transpose(-1, -2) if right else a
+
+
+class Run:
+    """The HIP path on device-resident batches: planted part from the input
+    generator, per-step noise from a seeded torch generator on the device."""
+
+    def __init__(self, glr, wl, seed=4321):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
+                                   beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed)
+        self.planted = [torch.from_numpy(planted_matrix(wl, l).astype(np.float32)).cuda()
+                        for l in range(len(wl.shapes))]
+        self.gen = torch.Generator(device="cuda")
+        self.gen.manual_seed(seed)
+        self.X = [torch.zeros(m, n, dtype=torch.float32, device="cuda") for m, n in wl.shapes]
+        self.t = 0
+
+    def batch(self):
+        torch = self.torch
+        out = []
+        for l, (m, n) in enumerate(self.wl.shapes):
+            g = torch.randn((self.wl.workers, m, n), generator=self.gen, device="cuda", dtype=torch.float32)
+            out.append(g.mul_(noise_level(self.wl, l)).add_(self.planted[l]))
+        return out
+
+    def step(self, G):
+        self.comp.step(self.X, G, self.t)
+        self.torch.cuda.synchronize()
+        st = self.comp.sync_status()
+        assert st in (0, 7), f"t={self.t}: device status {st}"
+        self.t += 1
+
+
+def _rel(a, b, floor=0.0):
+    den = max(float(np.linalg.norm(b)), floor)
+    return float(np.linalg.norm(a - b)) / den if den > 0 else float(np.linalg.norm(a))
+
+
+def check_columns(run, l, G, before, cols):
+    """The oracle's step on sampled columns of matrix l (fp64), given the
+    GPU's P, against the GPU's E, E-bar, X and optimizer state."""
+    wl, comp = run.wl, run.comp
+    m, n = wl.shapes[l]
+    right = m > n
+    P = comp.P(l).double().cpu().numpy()                       # d x r
+    Gc = _oriented(G[l], right)[:, :, cols].double().cpu().numpy()   # N x d x c
+    E0 = before["E"]                                            # N x d x c (fp64)
+    Mi = Gc + E0
+    Q = np.einsum("ar,iac->irc", P, Mi)
+    E1 = Mi - np.einsum("ar,irc->iac", P, Q)
+    ghat = P @ Q.mean(axis=0)
+    if wl.opt == "msgd":
+        x1, s1 = msgd_update(before["X"], before["S1"], ghat, wl.lr, wl.beta1)
+        s2 = None
+    else:
+        x1, s1, s2 = adam_update(before["X"], before["S1"], before["S2"], ghat, wl.lr, wl.beta1,
+                                 wl.beta2, wl.eps)
+    gE = _oriented(comp.E(l), right)[:, :, cols].double().cpu().numpy()
+    gEb = _oriented(comp.Ebar(l), right)[:, cols].double().cpu().numpy()
+    gX = _oriented(run.X[l], right)[:, cols].double().cpu().numpy()
+    gS1 = _oriented(comp.S1(l), right)[:, cols].double().cpu().numpy()
+    scale = float(np.linalg.norm(Mi)) / np.sqrt(Mi.shape[0])
+    rec = {"E": _rel(gE, E1, 1e-3 * scale * np.sqrt(Mi.shape[0])),
+           "Ebar": _rel(gEb, E1.mean(axis=0), 1e-3 * scale),
+           "X": _rel(gX, x1), "S1": _rel(gS1, s1)}
+    if s2 is not None:
+        gS2 = _oriented(comp.S2(l), right)[:, cols].double().cpu().numpy()
+        rec["S2"] = _rel(gS2, s2)
+    for k, v in rec.items():
+        assert v < STEP_TOL, f"t={run.t - 1} mat={l} columns {cols[:4]}...: {k} rel {v:.3e} ({rec})"
+    return rec
+
+
+def snapshot_columns(run, l, cols):
+    comp, wl = run.comp, run.wl
+    m, n = wl.shapes[l]
+    right = m > n
+    snap = {"E": _oriented(comp.E(l), right)[:, :, cols].double().cpu().numpy(),
+            "X": _oriented(run.X[l], right)[:, cols].double().cpu().numpy(),
+            "S1": _oriented(comp.S1(l), right)[:, cols].double().cpu().numpy()}
+    if wl.opt == "adam":
+        snap["S2"] = _oriented(comp.S2(l), right)[:, cols].double().cpu().numpy()
+    return snap
+
+
+def mbar64(run, l, G, ebar_prev):
+    """M-bar = E-bar_{t-1} + mean_i G_i in fp64 on the device, oriented d x D."""
+    import torch
+    m, n = run.wl.shapes[l]
+    mb = G[l].mean(dim=0, dtype=torch.float64) + ebar_prev
+    return _oriented(mb, m > n).contiguous()
+
+
+def check_refresh(run, l, mb, rows, res_tol=1e-5):
+    """Basis properties at a refresh step; rows = how many rows of U^T are
+    defined (d, or the top block of the tau = 1 refresh)."""
+    torch = run.torch
+    comp = run.comp
+    Ut = comp.Ut(l)[:rows].double()
+    sig = comp.sigma(l)[:rows].double()
+    J = comp.J(l).long()
+    orth = float((Ut @ Ut.T - torch.eye(rows, dtype=torch.float64, device="cuda")).abs().max())
+    assert orth < 1e-5, f"mat {l}: ||U U^T - I||_max = {orth:.3e}"
+    assert bool((sig[1:] <= sig[:-1]).all()), f"mat {l}: sigma not descending"
+    s1 = float(sig[0])
+    # eigen-residual of M-bar M-bar^T for every defined row
+    A = Ut @ mb                                   # rows x D
+    R = A @ mb.T - sig[:, None] ** 2 * Ut         # rows x d
+    res = float(R.norm(dim=1).max()) / max(s1 * s1, 1e-300)
+    assert res < res_tol, f"mat {l}: eigen-residual {res:.3e} sigma_1^2"
+    # sigma_j = ||u_j^T M-bar||
+    sg = float((A.norm(dim=1) - sig).abs().max()) / max(s1, 1e-300)
+    assert sg < 1e-5, f"mat {l}: sigma vs ||u_j^T Mbar|| {sg:.3e}"
+    fro2 = float((mb * mb).sum())
+    if rows == mb.shape[0]:
+        tr = abs(float((sig ** 2).sum()) - fro2) / fro2
+        assert tr < 1e-5, f"mat {l}: trace identity {tr:.3e}"
+    P = comp.P(l).double()
+    ey = abs(float(((P.T @ mb) ** 2).sum()) - float((sig[J[J < rows]] ** 2).sum())) / fro2
+    assert ey < 1e-5, f"mat {l}: Eckart-Young identity {ey:.3e}"
+    return {"orth": orth, "res": res, "sigma": sg}
+
+
+def check_selection(run, l, mb, t, rng, extra=48):
+    """Sampled Approx-Top-r scores against fp64 bilinear forms; J against
+    the fp64 ranking of the candidates."""
+    wl, comp = run.wl, run.comp
+    m, n = wl.shapes[l]
+    d, D = min(m, n), max(m, n)
+    r = min(wl.rank, d)
+    score = comp.score(l).double().cpu().numpy()
+    J = np.sort(comp.J(l).cpu().numpy())
+    assert np.array_equal(J, np.sort(argtop_r(score, r))), f"mat {l}: J is not argtop_r of the scores"
+    order = np.argsort(-score, kind="stable")
+    cand = order[: min(d, r + 16)]
+    rest = np.setdiff1d(np.arange(d), cand)
+    others = rng.choice(rest, size=min(extra, len(rest)), replace=False) if len(rest) else rest
+    idx = np.concatenate([cand, others]).astype(np.int64)
+    v = gaussian_vectors(wl.seed, t, l, idx, D).astype(np.float64)        # k x D
+    U = comp.Ut(l).double()[run.torch.from_numpy(idx).cuda()]             # k x d
+    a = (U @ mb).cpu().numpy()                                           # k x D
+    lam = np.einsum("kb,kb->k", a, v)
+    # fp32 products accumulated over d and D: a bar on lambda of 1e-5 of the
+    # Cauchy-Schwarz bound |u_j^T Mbar| |v_j|
+    delta = 1e-5 * np.linalg.norm(a, axis=1) * np.linalg.norm(v, axis=1)
+    err = np.abs(score[idx] - lam ** 2)
+    bound = 2 * np.abs(lam) * delta + delta ** 2
+    bad = np.nonzero(err > bound)[0]
+    assert len(bad) == 0, f"mat {l}: score {idx[bad[0]]} gpu {score[idx[bad[0]]]:.6e} fp64 {lam[bad[0]] ** 2:.6e}"
+    s64 = lam ** 2
+    ranked = np.argsort(-s64, kind="stable")
+    if len(idx) > r:
+        margin = (s64[ranked[r - 1]] - s64[ranked[r]]) / max(s64[ranked[r - 1]], 1e-300)
+        if margin >= MARGIN:
+            assert np.array_equal(np.sort(idx[ranked[:r]]), J), f"mat {l}: J differs from the fp64 ranking"
+        return {"margin": float(margin)}
+    return {}
+
+
+def run_fullsize(glr, name, steps, sample_cols=6, seed=7, ref_top=False):
+    import torch
+    wl = get_workload(name)
+    _say(name, "shapes", list(wl.shapes)[:3], "N", wl.workers, "r", wl.rank, "tau", wl.tau, "steps", steps)
+    run = Run(glr, wl)
+    rng = np.random.default_rng(seed)
+    mats = list(range(len(wl.shapes)))
+    if len(mats) > 6:      # many small matrices: every refresh, a sample of the rest
+        mats = sorted(set(rng.choice(mats, size=6, replace=False).tolist()) | {0, len(mats) - 1})
+    for t in range(steps):
+        G = run.batch()
+        refresh = t % wl.tau == 0
+        cols, before, ebar = {}, {}, {}
+        for l in mats:
+            m, n = wl.shapes[l]
+            D = max(m, n)
+            c = np.unique(np.concatenate([rng.choice(D, size=min(sample_cols, D), replace=False), [D - 1]]))
+            cols[l] = torch.from_numpy(c).cuda()
+            before[l] = snapshot_columns(run, l, cols[l])
+            ebar[l] = run.comp.Ebar(l).double().clone()
+        run.step(G)
+        for l in mats:
+            m, n = wl.shapes[l]
+            d = min(m, n)
+            r = min(wl.rank, d)
+            mb = mbar64(run, l, G, ebar[l])
+            rec = {"t": t, "mat": l}
+            if refresh and r < d:
+                sub = wl.tau == 1 and r <= 256
+                rows = min(d, 2 * r) if sub else d
+                rec.update(check_refresh(run, l, mb, r if sub else rows))
+                if ref_top:
+                    G64 = (mb @ mb.T).cpu().numpy()
+                    w, V = np.linalg.eigh(G64)
+                    Po = V[:, ::-1][:, :r]
+                    Pg = run.comp.P(l).double().cpu().numpy()
+                    rec["proj"] = _rel(Pg @ Pg.T, Po @ Po.T)
+                    gap = (w[::-1][r - 1] - w[::-1][r]) / w[-1]
+                    rec["gap_sigma2"] = float(gap)
+                    assert rec["proj"] < STEP_TOL, f"mat {l}: projector vs fp64 top-r {rec['proj']:.3e}"
+            elif r < d:
+                rec.update(check_selection(run, l, mb, t, rng))
+            rec.update(check_columns(run, l, G, before[l], cols[l]))
+            _say(rec)
+            del mb
+        del G
+    return run
+
+
+@pytest.mark.parametrize("name,steps,ref", [
+    ("layer_4096", 2, False),
+    ("layer_4096_gap", 2, True),
+])
+def test_layer_4096(gpu_lib, name, steps, ref):
+    run_fullsize(gpu_lib, name, steps, ref_top=ref)
+
+
+def test_transformer_block(gpu_lib):
+    run_fullsize(gpu_lib, "block_4096_gap", 2)
+
+
+def test_conv_50(gpu_lib):
+    run_fullsize(gpu_lib, "conv_50_gap", 2)
+
+
+def test_large_tau1(gpu_lib):
+    run_fullsize(gpu_lib, "large_8192x28672", 2, sample_cols=4)
