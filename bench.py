@@ -57,21 +57,25 @@ def uses_subspace(wl, d):
 FP64_ALU_PEAK = 78.6e12     # fp64 vector flop/s (the pair eigensolves)
 
 # groups that are one kernel launch each (the candidates for the dominant kernel)
-KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_gram", "jac_solve", "jac_apply",
-                 "rr_gram", "rr_solve", "rr_apply", "sub_z", "sub_p", "sub_chol")
+KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_rotate", "jac_solve",
+                 "rr_rotate", "rr_solve", "sub_z", "sub_p", "sub_chol")
 
 
-def jacobi_work(kind, d, D):
-    """Per-launch work of one Jacobi round on a d x D row set (16-row blocks,
-    32-row pairs): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64 ALU flops)."""
+def jacobi_work(kind, d):
+    """Per-launch work of one Jacobi round on the fp64 Gram of d rows (16-row
+    blocks, 32-row pairs): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64 ALU
+    flops)."""
     pairs, _ = jac_pairs(d)
-    if kind == "gram":      # 32 x 32 pair Grams over D columns (fp64 MFMA)
-        return pairs * 32.0 * D * 4, 0.0, pairs * 2.0 * 32 * 32 * D, 0.0
-    if kind == "solve":     # one cyclic sweep of 32 x 32 two-sided Jacobi per pair:
-        # 496 rotations, each updating two rows and two columns of G and two columns of V
-        return 0.0, 0.0, 0.0, pairs * 496.0 * (6 * 32 * 3)
-    # apply: read + write the 32 rows of [W | U^T] of every pair
-    return pairs * 32.0 * (D + d) * 8, pairs * 2.0 * 32 * 32 * (D + d), 0.0, 0.0
+    nb = (d + 15) // 16
+    if kind == "rotate":
+        # A <- J^T A J on the packed upper blocks (read + write, two 32 x 32 x 32
+        # fp64 products per pair of pairs) and U^T <- J^T U^T (read + write the
+        # 32 rows of every pair, one 32 x 32 x d fp32 product per pair)
+        return (2.0 * nb * (nb + 1) / 2 * 256 * 8 + pairs * 32.0 * d * 8,
+                pairs * 2.0 * 32 * 32 * d, pairs * (pairs + 1) / 2 * 2 * 2.0 * 32 ** 3, 0.0)
+    # solve: one cyclic sweep of 32 x 32 two-sided Jacobi per pair: 496
+    # rotations, each updating two rows and two columns of G and two columns of V
+    return 0.0, 0.0, 0.0, pairs * 496.0 * (6 * 32 * 3)
 
 
 def group_work(wl, name):
@@ -98,9 +102,9 @@ def group_work(wl, name):
         elif name == "resid_opt":
             w = ((12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
         elif name.startswith("jac_") and not sub:
-            w = jacobi_work(name[4:], d, D)
+            w = jacobi_work(name[4:], d)
         elif name.startswith("rr_") and sub:
-            w = jacobi_work(name[3:], K, D)
+            w = jacobi_work(name[3:], K)
         elif name in ("sub_z", "sub_p") and sub:
             w = (4.0 * (d * D + K * d + K * D), 2.0 * K * d * D, 0, 0)
         elif name == "sub_chol" and sub:

@@ -181,21 +181,19 @@ typedef enum {
   GLR_PROF_RBAR = 4,         /* Rbar = mean Q^(i) */
   GLR_PROF_RESID_OPT = 5,    /* residual + mean + reconstruction + optimizer */
   GLR_PROF_FULL_REFRESH = 6, /* Algorithm 3 refresh update */
-  GLR_PROF_JAC_INIT = 7,     /* refresh: Jacobi initialisation (warm start product) */
-  GLR_PROF_JAC_GRAM = 8,     /* refresh: partial pair Grams of one Jacobi round */
-  GLR_PROF_JAC_FINISH = 9,   /* refresh: norms, sort, permutation */
+  GLR_PROF_JAC_INIT = 7,     /* refresh: warm-start product and the fp64 Gram */
+  GLR_PROF_JAC_ROTATE = 8,   /* refresh: one round's Gram update and rotation of U^T rows */
+  GLR_PROF_JAC_FINISH = 9,   /* refresh: sigma, sort, permutation, re-orthonormalisation */
   GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
   GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration (all its launches) */
-  GLR_PROF_JAC_APPLY = 12,   /* refresh: rotations of one Jacobi round */
-  GLR_PROF_JAC_SOLVE = 13,   /* refresh: pair eigensolves of one Jacobi round */
-  GLR_PROF_RR_GRAM = 14,     /* tau = 1 Rayleigh-Ritz Jacobi (K x D): pair Grams */
-  GLR_PROF_RR_SOLVE = 15,    /* tau = 1 Rayleigh-Ritz Jacobi: pair eigensolves */
-  GLR_PROF_RR_APPLY = 16,    /* tau = 1 Rayleigh-Ritz Jacobi: rotations */
-  GLR_PROF_SUB_Z = 17,       /* tau = 1: Z = P^T Mo (K x D product) */
-  GLR_PROF_SUB_P = 18,       /* tau = 1: Z Mo^T (K x d split-K product, before its reduction) */
-  GLR_PROF_SUB_ORTH = 19,    /* tau = 1: CholeskyQR2 orthonormalisations (all their launches) */
-  GLR_PROF_SUB_CHOL = 20,    /* tau = 1: K x K Cholesky factor and inverse */
-  GLR_PROF_COUNT = 21
+  GLR_PROF_JAC_SOLVE = 12,   /* refresh: pair eigensolves of one Jacobi round */
+  GLR_PROF_RR_ROTATE = 13,   /* tau = 1 Rayleigh-Ritz Jacobi (K x K Gram): update and rotation */
+  GLR_PROF_RR_SOLVE = 14,    /* tau = 1 Rayleigh-Ritz Jacobi: pair eigensolves */
+  GLR_PROF_SUB_Z = 15,       /* tau = 1: Z = P^T Mo (K x D product) */
+  GLR_PROF_SUB_P = 16,       /* tau = 1: Z Mo^T (K x d split-K product, before its reduction) */
+  GLR_PROF_SUB_ORTH = 17,    /* tau = 1: CholeskyQR2 orthonormalisations (all their launches) */
+  GLR_PROF_SUB_CHOL = 18,    /* tau = 1: K x K Cholesky factor and inverse */
+  GLR_PROF_COUNT = 19
 } glr_prof_group;
 
 glr_status glr_profile_enable(glr_handle* h, int32_t on);

@@ -11,6 +11,13 @@ namespace glr {
 constexpr int kJB = 16;   // rows per Jacobi block; a pair holds 2 * kJB rows
 constexpr int kJP = 32;
 
+// The fp64 Gram A = W W^T of a refresh is kept packed by 16 x 16 blocks:
+// block (a, b), a <= b, row-major, at pk_off(a, b, nb) doubles.
+__host__ __device__ inline int64_t pk_off(int a, int b, int nb) {
+  return ((int64_t)a * nb - (int64_t)a * (a - 1) / 2 + (b - a)) * (kJB * kJB);
+}
+__host__ __device__ inline int64_t pk_doubles(int nb) { return (int64_t)nb * (nb + 1) / 2 * (kJB * kJB); }
+
 // Per-refresh control words of the block Jacobi (device memory).
 constexpr int kInfoInts = 64;   // per-matrix info block in the state
 constexpr int kHistory = 60;    // sweeps whose off-norm is recorded
@@ -56,15 +63,16 @@ struct MatView {
   float* X;      const float* G;
   // workspace
   float* Mbar;   float* Q;     float* lam_part;
-  float* W;      float* Utw;   double* gram_part; float* Vrot; int* skip;
+  float* W;      float* Utw;   double* Apk;  float* Vrot;   double* V64;   int* skip;
+  double* gpart;   // split-contraction partials of the Gram (or null)
   JacCtl* ctl;   float* sigma_w; int* perm;
   // subspace iteration
   float* sub_P;  float* sub_Pn; float* sub_Z;  float* sub_Zt; float* sub_R; float* sub_part;
   double* sub_S; double* sub_L; double* sub_Dinv; double* sub_Li; double* sub_T;
   float* sub_Linv; float* sub_C; double* sub_sums; SubCtl* sub_ctl;
-  // Rayleigh-Ritz: block Jacobi SVD of the K x D projection
-  float* rr_Utw; float* rr_Y; double* rr_gram; float* rr_V; int* rr_skip; JacCtl* rr_ctl;
-  float* rr_sigw; int* rr_perm;
+  // Rayleigh-Ritz: Jacobi on the fp64 Gram of the K x D projection
+  float* rr_Utw; float* rr_Y; double* rr_Apk; float* rr_V; double* rr_V64; int* rr_skip;
+  JacCtl* rr_ctl; float* rr_sigw; int* rr_perm; double* rr_gpart;
 };
 
 // Optional timing brackets around launch groups (glr_prof_group ids); a
@@ -93,19 +101,22 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s);
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s);
 hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s);
 
-// block one-sided Jacobi
+// Jacobi on the fp64 Gram of the rows of W
 int jac_blocks(int64_t d);
 int jac_seats(int64_t d);
-int jac_slices(int64_t d, int64_t D);
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
-hipError_t launch_jac_gram(const MatView& v, int round, hipStream_t s);
+hipError_t launch_jac_rotate(const MatView& v, int round, hipStream_t s);
 hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                             hipStream_t s);
-hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s);
 hipError_t launch_reorth(const MatView& v, hipStream_t s);
+
+// A (packed fp64 blocks, zero padded) = W W^T for n rows of length Kc (ld)
+int gram_splits(int64_t n, int64_t Kc);
+hipError_t launch_gram_packed(const float* W, int64_t ld, int64_t n, int64_t Kc, double* Apk, double* part64,
+                              hipStream_t s);
 
 // subspace iteration (tau = 1)
 size_t sub_part_floats(int K, int64_t d, int64_t D);

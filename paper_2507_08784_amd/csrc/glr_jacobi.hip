@@ -1,19 +1,21 @@
 // Refresh step: complete left singular basis U of Mbar (d x D) by block
-// one-sided (Hestenes) Jacobi on the rows of W = U^T Mo.
+// Jacobi on the fp64 Gram A = W W^T of the rows of W = U_0^T Mo (U_0 the
+// previous basis, or I): the eigenvectors of A are the left singular vectors.
 //
-// Rows are grouped in blocks of kJB; a round of the round-robin tournament
-// pairs the blocks two by two, and each pair (2 kJB rows) is orthogonalised
-// as a whole:
-//   gram   : the pair Gram W_p W_p^T in fp64 (fp64 MFMA, column slices in
-//            parallel, partial sums per slice)
-//   solve  : cyclic two-sided Jacobi on the 2kJB x 2kJB Gram in LDS (fp64)
-//            gives its eigenvectors V
-//   apply  : rows of [W | U^T] <- V^T rows, in place, as w + (V - I)^T w
-//            (fp32 MFMA)
+// A is formed once per refresh (fp64-accumulated products of the fp32 rows)
+// and kept packed by 16 x 16 blocks.  Rows are grouped in blocks of kJB; a
+// round of the round-robin tournament pairs the blocks two by two, and each
+// pair (2 kJB rows) is treated as a whole:
+//   solve  : cyclic two-sided Jacobi on the pair's 32 x 32 diagonal block of
+//            A in LDS (fp64) gives its eigenvectors V
+//   update : A <- J^T A J with J = diag(V_pair), block by block: the 32 x 32
+//            block (P, Q) of two pairs becomes V_P^T A_PQ V_Q (fp64 MFMA)
+//   apply  : rows of U^T <- V^T rows, in place, as u + (V - I)^T u
+//            (fp32 MFMA), in the same launch as the update
 // A sweep is one tournament (every pair of blocks meets once).  The sweeps
 // stop when every pair met in a sweep passes the measure of k_jac_solve.
-// The final singular values are the row norms of W, sorted descending (ties
-// keep the lower row first); U^T rows follow the sort.
+// The singular values are sqrt(diag A), sorted descending (ties keep the
+// lower row first); U^T rows follow the sort.
 #include "glr_device.hpp"
 #include "glr_internal.hpp"
 
@@ -24,16 +26,6 @@ int jac_seats(int64_t d) {
   int nb = jac_blocks(d);
   return nb + (nb & 1) < 2 ? 2 : nb + (nb & 1);
 }
-// column slices per pair for the Gram, so that pairs x slices fills the chip
-int jac_slices(int64_t d, int64_t D) {
-  int pairs = jac_seats(d) / 2;
-  int64_t s = (1024 + pairs - 1) / pairs;
-  int64_t maxs = (D + 127) / 128;
-  if (s > maxs) s = maxs;
-  if (s < 1) s = 1;
-  return (int)s;
-}
-
 // blocks met by `pair` in `round` of the circle-method tournament on `seats`
 __device__ __forceinline__ void pair_blocks(int round, int pair, int seats, int& bi, int& bj) {
   const int last = seats - 1;
@@ -151,70 +143,24 @@ hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s) {
     dim3 grid((unsigned)((v.D + 31) / 32), (unsigned)((v.d + 31) / 32));
     hipLaunchKernelGGL(k_jac_copy_cold, grid, dim3(256), 0, s, v.Mbar, v.W, v.d, v.D, v.right ? 1 : 0);
   }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_gram_packed(v.W, v.D, v.d, v.D, v.Apk, v.gpart, s);
 }
 
 // ---------------------------------------------------------------------------
-// one round: gram (partial pair Grams over column slices), solve (one block
-// per pair), apply (column chunks of every pair)
+// one round: solve (one block per pair), update (one block per two pairs),
+// apply (column chunks of every pair's rows of U^T)
 // ---------------------------------------------------------------------------
-// partial pair Gram over one column slice: part[pair][slice][32][32] (fp64)
-__global__ void __launch_bounds__(256)
-k_jac_gram(const float* __restrict__ W, int64_t d, int64_t D, const JacCtl* __restrict__ ctl,
-           int round, int seats, int nb, int slice_cols, double* __restrict__ part) {
-  if (ctl->converged) return;
-  const int pair = blockIdx.x, slice = blockIdx.y, nslices = gridDim.y;
-  int bi, bj;
-  pair_blocks(round, pair, seats, bi, bj);
-  if (bi >= nb && bj >= nb) return;
-  __shared__ float S[64][kJP + 1];
-  const int lane = lane_id(), w = wave_id();
-  const int I = w >> 1, Jb = w & 1;
-  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-  const int64_t c_begin = (int64_t)slice * slice_cols;
-  const int64_t c_end = c_begin + slice_cols < D ? c_begin + slice_cols : D;
-  // loader mapping: lane = column within the 64-column chunk, 8 rows per thread
-  const int cl = threadIdx.x & 63, rb = threadIdx.x >> 6;
-  const float* wrow[8];
-  bool rok[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int64_t grow = pair_row(rb + 4 * i, bi, bj);
-    rok[i] = grow < d;
-    wrow[i] = W + (rok[i] ? grow : 0) * D;
-  }
-  float x[8];
-  auto fetch = [&](int64_t c0) {
-    const int64_t c = c0 + cl;
-    const bool cok = c < c_end;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = (rok[i] && cok) ? wrow[i][c] : 0.f;
-  };
-  if (c_begin < c_end) fetch(c_begin);
-  for (int64_t c0 = c_begin; c0 < c_end; c0 += 64) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) S[cl][rb + 4 * i] = x[i];
-    __syncthreads();
-    if (c0 + 64 < c_end) fetch(c0 + 64);
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      const int k = 4 * ks + (lane >> 4);
-      const double a = (double)S[k][16 * I + (lane & 15)];
-      const double b = (double)S[k][16 * Jb + (lane & 15)];
-      acc = mfma64(a, b, acc);
-    }
-    __syncthreads();
-  }
-  double* out = part + ((int64_t)pair * nslices + slice) * (kJP * kJP);
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int i = 16 * I + 4 * v + (lane >> 4);
-    const int j = 16 * Jb + (lane & 15);
-    out[i * kJP + j] = acc[v];
-  }
+// entry (x, y) of the 32 x 32 block of A whose rows are the blocks (bx0, bx1)
+// and columns (by0, by1); zero for padding blocks
+__device__ __forceinline__ double pk_get(const double* __restrict__ Apk, int nb, int bx, int by, int lx,
+                                         int ly) {
+  if (bx >= nb || by >= nb) return 0.0;
+  return bx <= by ? Apk[pk_off(bx, by, nb) + lx * kJB + ly] : Apk[pk_off(by, bx, nb) + ly * kJB + lx];
 }
 
-constexpr int JAC_CHUNK = 512;   // columns of [W | Utw] rotated by one block
+constexpr int JAC_CHUNK = 512;   // columns of U^T rotated by one block
 
 // Eigenvectors V of the pair Gram by cyclic two-sided Jacobi in LDS (fp64).
 // Convergence measure of a pair of rows (p, q):
@@ -239,9 +185,9 @@ __device__ __forceinline__ void inner_pair(int rd, int k, int& p, int& q) {
 }
 
 __global__ void __launch_bounds__(256)
-k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ ctl, int round,
-            int seats, int nb, float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
-            int* __restrict__ skip) {
+k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb,
+            float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
+            double* __restrict__ V64, int* __restrict__ skip) {
   if (ctl->converged) return;
   const int pair = blockIdx.x;
   int bi, bj;
@@ -253,20 +199,12 @@ k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ c
   __shared__ double red[4];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const double rm_prev = __longlong_as_double((long long)ctl->rowmax2_bits);
-  // slice partials summed in slice order; all loads of a batch issued together
-  const double* src = part + (int64_t)pair * nslices * (kJP * kJP);
-  double g[4] = {0.0, 0.0, 0.0, 0.0};
-  for (int z0 = 0; z0 < nslices; z0 += 8) {
-    double t[4][8];
+  // the pair's diagonal 32 x 32 block of A
+  double g[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        t[k][j] = z0 + j < nslices ? src[(int64_t)(z0 + j) * kJP * kJP + tid + 256 * k] : 0.0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) g[k] += t[k][j];
+  for (int k = 0; k < 4; ++k) {
+    const int e = tid + 256 * k, x = e / kJP, y = e % kJP;
+    g[k] = pk_get(Apk, nb, x < kJB ? bi : bj, y < kJB ? bi : bj, x % kJB, y % kJB);
   }
   double dmax = 0.0;
 #pragma unroll
@@ -345,25 +283,24 @@ k_jac_solve(const double* __restrict__ part, int nslices, JacCtl* __restrict__ c
     }
   }
   float* vo = Vout + (int64_t)pair * kJP * kJP;
+  double* vd = V64 + (int64_t)pair * kJP * kJP;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int e = tid + 256 * k;
     vo[e] = (float)V[e / kJP][e % kJP];
+    vd[e] = V[e / kJP][e % kJP];
   }
   if (tid == 0) skip[pair] = 0;
 }
 
-// rows of the pair in [W | Utw] <- V^T rows on this block's chunk, computed
+// rows of the pair in U^T <- V^T rows on this block's chunk, computed
 // as w + (V - I)^T w (fp32 MFMA).  The k index is permuted so that the B
 // operand held by each lane is exactly the set of rows that lane outputs:
 // physical row of k = 2kk + h is mfma32_row(kk, 32h), and B register kk is
 // output register kk.
-__global__ void __launch_bounds__(256)
-k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D,
-            const float* __restrict__ Vin, const int* __restrict__ skip,
-            const JacCtl* __restrict__ ctl, int round, int seats, int nb) {
-  if (ctl->converged) return;
-  const int pair = blockIdx.x;
+__device__ __forceinline__ void apply_chunk(float* __restrict__ Utw, int64_t d, const float* __restrict__ Vin,
+                                            const int* __restrict__ skip, int round, int seats, int nb,
+                                            int pair, int chunk) {
   if (skip[pair]) return;
   int bi, bj;
   pair_blocks(round, pair, seats, bi, bj);
@@ -379,21 +316,15 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
     a[kk] = V[pr * kJP + l32] - (pr == l32 ? 1.0f : 0.0f);
     rows[kk] = pair_row(pr, bi, bj);
   }
-  const int64_t Dt = D + d;
-  const int64_t c0 = (int64_t)blockIdx.y * JAC_CHUNK;
+  const int64_t c0 = (int64_t)chunk * JAC_CHUNK;
   for (int it = 0; it < JAC_CHUNK / 128; ++it) {
     const int64_t cb = c0 + it * 128 + w * 32;
-    if (cb >= Dt) break;
-    const int64_t c = cb + l32;
-    const bool cok = c < Dt;
-    float* base;
-    int64_t ld, cc;
-    if (c < D) { base = W; ld = D; cc = c; }
-    else { base = Utw; ld = d; cc = c - D; }
+    if (cb >= d) break;
+    const int64_t cc = cb + l32;
+    const bool cok = cc < d;
     float b[kJP / 2];
 #pragma unroll
-    for (int kk = 0; kk < kJP / 2; ++kk)
-      b[kk] = (cok && rows[kk] < d) ? base[rows[kk] * ld + cc] : 0.f;
+    for (int kk = 0; kk < kJP / 2; ++kk) b[kk] = (cok && rows[kk] < d) ? Utw[rows[kk] * d + cc] : 0.f;
     f32x16 acc;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
@@ -401,33 +332,131 @@ k_jac_apply(float* __restrict__ W, float* __restrict__ Utw, int64_t d, int64_t D
     for (int kk = 0; kk < kJP / 2; ++kk) acc = mfma32(a[kk], b[kk], acc);
 #pragma unroll
     for (int v = 0; v < 16; ++v)
-      if (cok && rows[v] < d) base[rows[v] * ld + cc] = b[v] + acc[v];
+      if (cok && rows[v] < d) Utw[rows[v] * d + cc] = b[v] + acc[v];
   }
 }
 
-hipError_t launch_jac_gram(const MatView& v, int round, hipStream_t s) {
+// A <- J^T A J: the 32 x 32 block of rows of pair P and columns of pair Q
+// (P <= Q) becomes V_P^T A_PQ V_Q (fp64 MFMA; V_P held in registers as the
+// A operand of the second product, V_Q read as the B operand of the first).
+// A workgroup takes one P and up to kUpdQ consecutive Q.  The 16 x 16 blocks
+// of A are read and written whole (coalesced) through one LDS tile; blocks
+// below the diagonal are not stored, so each stored block is written by
+// exactly one workgroup.
+constexpr int kUpdQ = 4;
+
+__device__ __forceinline__ void update_group(double* __restrict__ Apk, const double* __restrict__ V64,
+                                             const int* __restrict__ skip, int round, int seats, int nb,
+                                             int pairs, int P, int Q0, double (*S)[kJP + 1]) {
+  int pi, pj;
+  pair_blocks(round, P, seats, pi, pj);
+  if (pi >= nb && pj >= nb) return;
+  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+  const int wi = (w >> 1) * 16, wj = (w & 1) * 16;   // wave w: result block (w >> 1, w & 1)
+  const int li = lane & 15, lk = lane >> 4;
+  const int er = tid / kJB, ec = tid % kJB;             // element of a 16 x 16 block
+  const bool sp = skip[P] != 0;
+  const double* vp = V64 + (int64_t)P * kJP * kJP;
+  double vpo[kJP / 4];
+#pragma unroll
+  for (int k = 0; k < kJP / 4; ++k) {
+    const int kk = 4 * k + lk;
+    vpo[k] = sp ? (kk == wi + li ? 1.0 : 0.0) : vp[kk * kJP + wi + li];
+  }
+  for (int q = 0; q < kUpdQ; ++q) {
+    const int Q = Q0 + q;
+    if (Q >= pairs) break;
+    int qi, qj;
+    pair_blocks(round, Q, seats, qi, qj);
+    if (qi >= nb && qj >= nb) continue;
+    const bool sq = skip[Q] != 0;
+    if (sp && sq) continue;
+    const double* vq = V64 + (int64_t)Q * kJP * kJP;
+    double sv[4], vqo[kJP / 4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int bx = (k >> 1) ? pj : pi, by = (k & 1) ? qj : qi;
+      sv[k] = (bx < nb && by < nb) ? Apk[(bx <= by ? pk_off(bx, by, nb) : pk_off(by, bx, nb)) + tid] : 0.0;
+    }
+#pragma unroll
+    for (int k = 0; k < kJP / 4; ++k) {
+      const int kk = 4 * k + lk;
+      vqo[k] = sq ? (kk == wj + li ? 1.0 : 0.0) : vq[kk * kJP + wj + li];
+    }
+    __syncthreads();   // the previous Q is done with S
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int h = k >> 1, g = k & 1;
+      const int bx = h ? pj : pi, by = g ? qj : qi;
+      if (bx <= by) S[h * kJB + er][g * kJB + ec] = sv[k];
+      else S[h * kJB + ec][g * kJB + er] = sv[k];
+    }
+    __syncthreads();
+    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < kJP / 4; ++k) acc = mfma64(S[wi + li][4 * k + lk], vqo[k], acc);   // T = A_PQ V_Q
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
+    __syncthreads();
+    acc = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < kJP / 4; ++k) acc = mfma64(vpo[k], S[4 * k + lk][wj + li], acc);  // V_P^T T
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int h = k >> 1, g = k & 1;
+      if (P == Q && h == 1 && g == 0) continue;   // the transpose of block (0, 1)
+      const int bx = h ? pj : pi, by = g ? qj : qi;
+      if (bx >= nb || by >= nb) continue;
+      if (bx <= by) Apk[pk_off(bx, by, nb) + tid] = S[h * kJB + er][g * kJB + ec];
+      else Apk[pk_off(by, bx, nb) + tid] = S[h * kJB + ec][g * kJB + er];
+    }
+  }
+}
+
+// one launch per round after the solve: workgroups [0, n_upd) update A,
+// the rest rotate the pairs' rows of U^T (chunks of JAC_CHUNK columns)
+__global__ void __launch_bounds__(256)
+k_jac_rotate(double* __restrict__ Apk, const double* __restrict__ V64, float* __restrict__ Utw, int64_t d,
+             const float* __restrict__ V32, const int* __restrict__ skip, const JacCtl* __restrict__ ctl,
+             int round, int seats, int nb, int pairs, int n_upd, int chunks) {
+  if (ctl->converged) return;
+  __shared__ double S[kJP][kJP + 1];
+  const int b = blockIdx.x;
+  if (b < n_upd) {
+    int P = 0, rem = b;
+    for (;;) {
+      const int cnt = (pairs - P + kUpdQ - 1) / kUpdQ;
+      if (rem < cnt) break;
+      rem -= cnt;
+      ++P;
+    }
+    update_group(Apk, V64, skip, round, seats, nb, pairs, P, P + rem * kUpdQ, S);
+  } else {
+    const int idx = b - n_upd;
+    apply_chunk(Utw, d, V32, skip, round, seats, nb, idx / chunks, idx % chunks);
+  }
+}
+
+hipError_t launch_jac_rotate(const MatView& v, int round, hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
-  const int nsl = jac_slices(v.d, v.D);
-  const int slice_cols = (int)(((v.D + nsl - 1) / nsl + 63) / 64 * 64);
-  hipLaunchKernelGGL(k_jac_gram, dim3(pairs, nsl), dim3(256), 0, s, v.W, v.d, v.D, v.ctl, round,
-                     seats, nb, slice_cols, v.gram_part);
+  int n_upd = 0;
+  for (int P = 0; P < pairs; ++P) n_upd += (pairs - P + kUpdQ - 1) / kUpdQ;
+  const int chunks = (int)((v.d + JAC_CHUNK - 1) / JAC_CHUNK);
+  hipLaunchKernelGGL(k_jac_rotate, dim3((unsigned)(n_upd + pairs * chunks)), dim3(256), 0, s, v.Apk, v.V64,
+                     v.Utw, v.d, v.Vrot, v.skip, v.ctl, round, seats, nb, pairs, n_upd, chunks);
   return hipGetLastError();
 }
 
 hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                             hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
-  const int nsl = jac_slices(v.d, v.D);
-  hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.gram_part, nsl, v.ctl, round,
-                     seats, nb, tol, max_inner, floor_rel2, v.Vrot, v.skip);
-  return hipGetLastError();
-}
-
-hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s) {
-  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
-  const int64_t Dt = v.D + v.d;
-  hipLaunchKernelGGL(k_jac_apply, dim3(pairs, (unsigned)((Dt + JAC_CHUNK - 1) / JAC_CHUNK)),
-                     dim3(256), 0, s, v.W, v.Utw, v.d, v.D, v.Vrot, v.skip, v.ctl, round, seats, nb);
+  hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.Apk, v.ctl, round, seats, nb, tol,
+                     max_inner, floor_rel2, v.Vrot, v.V64, v.skip);
   return hipGetLastError();
 }
 
@@ -445,22 +474,13 @@ hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// finish: sigma_j = ||W_j|| (fp64 sum), sort descending, permute U^T rows
+// finish: sigma_j = sqrt(A_jj), sort descending, permute U^T rows
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256)
-k_rownorm(const float* __restrict__ W, int64_t D, float* __restrict__ sig) {
-  const int64_t j = blockIdx.x;
-  const float* row = W + j * D;
-  double s = 0.0;
-  for (int64_t b = threadIdx.x; b < D; b += blockDim.x) {
-    const double x = row[b];
-    s += x * x;
-  }
-  __shared__ double red[4];
-  s = wave_sum(s);
-  if (lane_id() == 0) red[wave_id()] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) sig[j] = (float)sqrt(red[0] + red[1] + red[2] + red[3]);
+__global__ void k_diag_sqrt(const double* __restrict__ Apk, int64_t d, int nb, float* __restrict__ sig) {
+  const int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (j >= d) return;
+  const int b = (int)(j / kJB), l = (int)(j % kJB);
+  sig[j] = (float)sqrt(fmax(Apk[pk_off(b, b, nb) + l * (kJB + 1)], 0.0));
 }
 
 __global__ void __launch_bounds__(1024)
@@ -498,7 +518,8 @@ __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict
 }
 
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s) {
-  hipLaunchKernelGGL(k_rownorm, dim3((unsigned)v.d), dim3(256), 0, s, v.W, v.D, v.sigma_w);
+  hipLaunchKernelGGL(k_diag_sqrt, dim3((unsigned)((v.d + 255) / 256)), dim3(256), 0, s, v.Apk, v.d,
+                     jac_blocks(v.d), v.sigma_w);
   int n_pad = 2;
   while (n_pad < v.d) n_pad <<= 1;
   hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d,

@@ -29,11 +29,12 @@ inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign
 thread_local std::string g_create_error;
 
 struct WsLayout {
-  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_V, off_skip, off_ctl, off_sigw,
-      off_perm;
+  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_V, off_V64, off_gpart, off_skip,
+      off_ctl, off_sigw, off_perm;
   uint64_t off_sP, off_sPn, off_sZ, off_sZt, off_sR, off_spart, off_sS, off_sL, off_sDinv, off_sLi,
       off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
-  uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rskip, off_rctl, off_rsigw, off_rperm;
+  uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rV64, off_rgpart, off_rskip, off_rctl, off_rsigw,
+      off_rperm;
   uint64_t bytes;
 };
 
@@ -140,7 +141,7 @@ uint64_t state_bytes_of(const glr_config* c) {
 WsLayout ws_layout(const glr_config* c) {
   uint64_t mx_mn = 0, mx_Q = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
   uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
-  uint64_t r_gram = 0, r_pairs = 0;
+  uint64_t r_gram = 0, r_pairs = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
   for (int i = 0; i < c->num_mats; ++i) {
     const Dims x = dims_of(c, i);
@@ -156,17 +157,20 @@ WsLayout ws_layout(const glr_config* c) {
       mx(s_part, (uint64_t)sub_part_floats(Ki, x.d, x.D));
       const uint64_t rp = (uint64_t)jac_seats(Ki) / 2;
       mx(r_pairs, rp);
-      mx(r_gram, rp * (uint64_t)jac_slices(Ki, x.D) * kJP * kJP);
+      mx(r_gram, (uint64_t)pk_doubles(jac_blocks(Ki)));
+      const int rs = gram_splits(Ki, x.D);
+      if (rs > 1) mx(r_gpart, (uint64_t)rs * K * K);
       mx(s_KK, K * K);
       mx(s_Kp2, Kp * Kp);
       mx(s_nt, Kp / kCholTile);
       mx(s_sums, (uint64_t)((x.d + 127) / 128) * ((K + 127) / 128));
     } else {
       const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
-      const uint64_t sl = (uint64_t)jac_slices(x.d, x.D);
       mx(mx_dD, (uint64_t)(x.d * x.D));
       mx(mx_dd, (uint64_t)(x.d * x.d));
-      mx(mx_gram, pairs * sl * kJP * kJP);
+      mx(mx_gram, (uint64_t)pk_doubles(jac_blocks(x.d)));
+      const int gs = gram_splits(x.d, x.D);
+      if (gs > 1) mx(mx_gpart, (uint64_t)gs * (uint64_t)(x.d * x.d));
       mx(mx_pairs, pairs);
     }
   }
@@ -184,6 +188,8 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_Utw = take(mx_dd * 4);
   w.off_gram = take(mx_gram * 8);
   w.off_V = take(mx_pairs * kJP * kJP * 4);
+  w.off_V64 = take(mx_pairs * kJP * kJP * 8);
+  w.off_gpart = take(mx_gpart * 8);
   w.off_skip = take(mx_pairs * 4);
   w.off_ctl = take(sizeof(JacCtl));
   w.off_sigw = take(mx_d * 4);
@@ -207,6 +213,8 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rY = take(s_KK * 4);
   w.off_rgram = take(r_gram * 8);
   w.off_rV = take(r_pairs * kJP * kJP * 4);
+  w.off_rV64 = take(r_pairs * kJP * kJP * 8);
+  w.off_rgpart = take(r_gpart * 8);
   w.off_rskip = take(r_pairs * 4);
   w.off_rctl = take(sizeof(JacCtl));
   w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
@@ -286,8 +294,10 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   v.lam_part = (float*)(w + h->ws.off_lam);
   v.W = (float*)(w + h->ws.off_W);
   v.Utw = (float*)(w + h->ws.off_Utw);
-  v.gram_part = (double*)(w + h->ws.off_gram);
+  v.Apk = (double*)(w + h->ws.off_gram);
   v.Vrot = (float*)(w + h->ws.off_V);
+  v.V64 = (double*)(w + h->ws.off_V64);
+  v.gpart = (double*)(w + h->ws.off_gpart);   // sized for every matrix whose Gram is split
   v.skip = (int*)(w + h->ws.off_skip);
   v.ctl = (JacCtl*)(w + h->ws.off_ctl);
   v.sigma_w = (float*)(w + h->ws.off_sigw);
@@ -309,8 +319,10 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   v.sub_ctl = (SubCtl*)(w + h->ws.off_sctl);
   v.rr_Utw = (float*)(w + h->ws.off_rUtw);
   v.rr_Y = (float*)(w + h->ws.off_rY);
-  v.rr_gram = (double*)(w + h->ws.off_rgram);
+  v.rr_Apk = (double*)(w + h->ws.off_rgram);
   v.rr_V = (float*)(w + h->ws.off_rV);
+  v.rr_V64 = (double*)(w + h->ws.off_rV64);
+  v.rr_gpart = (double*)(w + h->ws.off_rgpart);
   v.rr_skip = (int*)(w + h->ws.off_rskip);
   v.rr_ctl = (JacCtl*)(w + h->ws.off_rctl);
   v.rr_sigw = (float*)(w + h->ws.off_rsigw);
@@ -406,15 +418,11 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
       {
-        ProfScope p(h, s, GLR_PROF_JAC_GRAM);
-        GLR_HIP(h, launch_jac_gram(v, rd, s));
-      }
-      {
         ProfScope p(h, s, GLR_PROF_JAC_SOLVE);
         GLR_HIP(h, launch_jac_solve(v, rd, c.tol, h->jac_inner, h->jac_floor2, s));
       }
-      ProfScope p(h, s, GLR_PROF_JAC_APPLY);
-      GLR_HIP(h, launch_jac_apply(v, rd, s));
+      ProfScope p(h, s, GLR_PROF_JAC_ROTATE);
+      GLR_HIP(h, launch_jac_rotate(v, rd, s));
     }
     GLR_HIP(h, launch_jac_check(v, c.tol, s));
     uint32_t conv = 0;
@@ -452,15 +460,11 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     for (int rd = 0; rd < rounds; ++rd) {
       {
-        ProfScope p(h, s, GLR_PROF_RR_GRAM);
-        GLR_HIP(h, launch_jac_gram(rr, rd, s));
-      }
-      {
         ProfScope p(h, s, GLR_PROF_RR_SOLVE);
         GLR_HIP(h, launch_jac_solve(rr, rd, c.tol, h->jac_inner, h->jac_floor2, s));
       }
-      ProfScope p(h, s, GLR_PROF_RR_APPLY);
-      GLR_HIP(h, launch_jac_apply(rr, rd, s));
+      ProfScope p(h, s, GLR_PROF_RR_ROTATE);
+      GLR_HIP(h, launch_jac_rotate(rr, rd, s));
     }
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
     uint32_t conv = 0;

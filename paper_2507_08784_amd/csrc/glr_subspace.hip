@@ -139,8 +139,10 @@ static int grid_n(int64_t n) {
 // row-major and contiguous along k): fp32 inputs widened to fp64, fp64 MFMA
 // on 64 x 64 tiles (each wave a 32 x 32 quadrant), grid.z splitting the
 // contraction into slices of kslice.
-//   EPI 0: slice z of C (fp64) at out64 + z M ldo
+//   EPI 0: slice z of C (fp64) at out64 + z M ldo (tiles below the block
+//          diagonal skipped: only the upper blocks of a symmetric C are read)
 //   EPI 1: out32 = (C - I) / 2 (one slice): the Newton-Schulz correction
+//   EPI 2: C packed by 16 x 16 blocks (a <= b) at out64 (one slice), ldo = nb
 // ---------------------------------------------------------------------------
 template <int EPI>
 __global__ void __launch_bounds__(256)
@@ -150,6 +152,7 @@ k_gram64(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, 
   __shared__ float Bs[32][65];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  if (EPI != 1 && m0 >= n0 + 64) return;
   const int k0 = blockIdx.z * kslice;
   const int k1 = Kc < k0 + kslice ? Kc : k0 + kslice;
   const int lr = tid >> 2, kq = (tid & 3) * 8;     // loader: row, k offset
@@ -201,8 +204,13 @@ k_gram64(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, 
         const int i = m0 + wi + 16 * x + 4 * v + (lane >> 4);
         const int j = n0 + wj + 16 * y + (lane & 15);
         if (i >= M || j >= N) continue;
-        if (EPI == 0) out64[((int64_t)blockIdx.z * M + i) * ldo + j] = acc[x][y][v];
-        else out32[(int64_t)i * ldo + j] = (float)(0.5 * (acc[x][y][v] - (i == j ? 1.0 : 0.0)));
+        if (EPI == 0) {
+          out64[((int64_t)blockIdx.z * M + i) * ldo + j] = acc[x][y][v];
+        } else if (EPI == 1) {
+          out32[(int64_t)i * ldo + j] = (float)(0.5 * (acc[x][y][v] - (i == j ? 1.0 : 0.0)));
+        } else if (i / kJB <= j / kJB) {
+          out64[pk_off(i / kJB, j / kJB, (int)ldo) + (i % kJB) * kJB + (j % kJB)] = acc[x][y][v];
+        }
       }
 }
 
@@ -221,6 +229,57 @@ __global__ void k_reduce_splits64(const double* __restrict__ part, int splits, i
     }
     out[i] = s;
   }
+}
+
+// packed upper blocks of the sum over splits of n x n partials (fixed order)
+__global__ void k_reduce_pack(const double* __restrict__ part, int splits, int n, int nb,
+                              double* __restrict__ Apk) {
+  const int64_t count = (int64_t)n * n;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += stride) {
+    const int i = (int)(e / n), j = (int)(e % n);
+    if (i / kJB > j / kJB) continue;
+    double s = 0.0;
+    for (int z0 = 0; z0 < splits; z0 += 8) {
+      double t[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t[q] = z0 + q < splits ? part[(int64_t)(z0 + q) * count + e] : 0.0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) s += t[q];
+    }
+    Apk[pk_off(i / kJB, j / kJB, nb) + (i % kJB) * kJB + (j % kJB)] = s;
+  }
+}
+
+// contraction splits of the n x n Gram over Kc: enough workgroups for the
+// chip when the tiles alone are few, slices of at least 512
+int gram_splits(int64_t n, int64_t Kc) {
+  const int64_t t = (n + 63) / 64;
+  const int64_t tiles = t * (t + 1) / 2;
+  if (tiles >= 256) return 1;
+  int64_t sp = (512 + tiles - 1) / tiles;
+  const int64_t mx = (Kc + 511) / 512;
+  if (sp > mx) sp = mx;
+  return sp < 1 ? 1 : (int)sp;
+}
+
+hipError_t launch_gram_packed(const float* W, int64_t ld, int64_t n, int64_t Kc, double* Apk, double* part64,
+                              hipStream_t s) {
+  const int nb = (int)((n + kJB - 1) / kJB);
+  hipError_t e = launch_fill_zero(Apk, (size_t)pk_doubles(nb) * 8, s);
+  if (e != hipSuccess) return e;
+  const int t = (int)((n + 63) / 64);
+  const int splits = part64 ? gram_splits(n, Kc) : 1;
+  if (splits == 1) {
+    hipLaunchKernelGGL(k_gram64<2>, dim3(t, t, 1), dim3(256), 0, s, W, ld, W, ld, (int)n, (int)n, (int)Kc,
+                       (int)Kc, Apk, (float*)nullptr, (int64_t)nb);
+  } else {
+    const int kslice = (int)(((Kc + splits - 1) / splits + 31) / 32 * 32);
+    hipLaunchKernelGGL(k_gram64<0>, dim3(t, t, splits), dim3(256), 0, s, W, ld, W, ld, (int)n, (int)n,
+                       (int)Kc, kslice, part64, (float*)nullptr, n);
+    hipLaunchKernelGGL(k_reduce_pack, dim3(grid_n(n * n)), dim3(256), 0, s, part64, splits, (int)n, nb, Apk);
+  }
+  return hipGetLastError();
 }
 
 // One Newton-Schulz step towards the nearest orthonormal rows,
@@ -624,9 +683,10 @@ hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hi
   return hipGetLastError();
 }
 
-// Rayleigh-Ritz: B = P^T Mo (K x D) into sub_Z; a MatView whose block Jacobi
-// computes the SVD of B (rows): B = Y Sigma V^T, Y written to rr_Y, Sigma to
-// the state's sigma, J = 0..r-1, info and status as for a full refresh.
+// Rayleigh-Ritz: B = P^T Mo (K x D) into sub_Z and its fp64 Gram; a MatView
+// whose Jacobi finds the eigenvectors Y of B B^T (the left singular vectors of
+// B): Y written to rr_Y, sqrt of the eigenvalues to the state's sigma,
+// J = 0..r-1, info and status as for a full refresh.
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d, D = v.D;
@@ -642,13 +702,17 @@ hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
   rr->W = v.sub_Z;
   rr->Utw = v.rr_Utw;
   rr->Ut = v.rr_Y;
-  rr->gram_part = v.rr_gram;
+  rr->Apk = v.rr_Apk;
   rr->Vrot = v.rr_V;
+  rr->V64 = v.rr_V64;
+  rr->gpart = v.rr_gpart;
   rr->skip = v.rr_skip;
   rr->ctl = v.rr_ctl;
   rr->sigma_w = v.rr_sigw;
   rr->perm = v.rr_perm;
   hipError_t e = launch_eye(v.rr_Utw, K, s);
+  if (e != hipSuccess) return e;
+  e = launch_gram_packed(v.sub_Z, D, K, D, v.rr_Apk, v.rr_gpart, s);
   if (e != hipSuccess) return e;
   return launch_jac_reset(*rr, s);
 }
