@@ -63,7 +63,7 @@ struct MatView {
   float* X;      const float* G;
   // workspace
   float* Mbar;   float* Q;     float* lam_part;
-  float* W;      float* Utw;   double* Apk;  float* Vrot;   double* V64;   int* skip;
+  float* W;      float* Utw;   double* Apk;  double* Apk2; float* Vrot;   double* V64;   int* skip;
   double* gpart;   // split-contraction partials of the Gram (or null)
   JacCtl* ctl;   float* sigma_w; int* perm;
   // subspace iteration
@@ -107,6 +107,9 @@ int jac_seats(int64_t d);
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
 hipError_t launch_jac_rotate(const MatView& v, int round, hipStream_t s);
+// reorders the rows by descending diag(A): A (into Apk2) and U^T (into W);
+// the caller then swaps Apk <-> Apk2 and Utw <-> W
+hipError_t launch_jac_sort(const MatView& v, hipStream_t s);
 hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                             hipStream_t s);
 hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s);

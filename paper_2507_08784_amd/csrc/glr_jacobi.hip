@@ -517,6 +517,45 @@ __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict
   }
 }
 
+// A' = P A P^T (packed) for the row permutation perm, and U^T' = P U^T
+__global__ void __launch_bounds__(256)
+k_pk_permute(const double* __restrict__ A, double* __restrict__ B, const int* __restrict__ perm, int64_t d,
+             int nb) {
+  // one workgroup per stored block (a, b), a <= b; one thread per entry
+  int64_t blk = blockIdx.x;
+  int a = 0;
+  while (blk >= nb - a) { blk -= nb - a; ++a; }
+  const int b = a + (int)blk;
+  const int r = threadIdx.x / kJB, c = threadIdx.x % kJB;
+  const int64_t i = (int64_t)a * kJB + r, j = (int64_t)b * kJB + c;
+  double x = 0.0;
+  if (i < d && j < d) {
+    const int pi = perm[i], pj = perm[j];
+    x = pk_get(A, nb, pi / kJB, pj / kJB, pi % kJB, pj % kJB);
+  }
+  B[pk_off(a, b, nb) + threadIdx.x] = x;
+}
+
+__global__ void k_row_gather(const float* __restrict__ src, float* __restrict__ dst, const int* __restrict__ perm,
+                             int64_t d) {
+  const int64_t k = blockIdx.x;
+  const int64_t p = perm[k];
+  for (int64_t a = threadIdx.x; a < d; a += blockDim.x) dst[k * d + a] = src[p * d + a];
+}
+
+hipError_t launch_jac_sort(const MatView& v, hipStream_t s) {
+  const int nb = jac_blocks(v.d);
+  hipLaunchKernelGGL(k_diag_sqrt, dim3((unsigned)((v.d + 255) / 256)), dim3(256), 0, s, v.Apk, v.d, nb,
+                     v.sigma_w);
+  int n_pad = 2;
+  while (n_pad < v.d) n_pad <<= 1;
+  hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d, n_pad, v.perm);
+  hipLaunchKernelGGL(k_pk_permute, dim3((unsigned)(nb * (nb + 1) / 2)), dim3(256), 0, s, v.Apk, v.Apk2, v.perm,
+                     v.d, nb);
+  hipLaunchKernelGGL(k_row_gather, dim3((unsigned)v.d), dim3(256), 0, s, v.Utw, v.W, v.perm, v.d);
+  return hipGetLastError();
+}
+
 hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s) {
   hipLaunchKernelGGL(k_diag_sqrt, dim3((unsigned)((v.d + 255) / 256)), dim3(256), 0, s, v.Apk, v.d,
                      jac_blocks(v.d), v.sigma_w);

@@ -8,6 +8,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/greedylore.h"
@@ -29,7 +30,7 @@ inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign
 thread_local std::string g_create_error;
 
 struct WsLayout {
-  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_V, off_V64, off_gpart, off_skip,
+  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_gram2, off_V, off_V64, off_gpart, off_skip,
       off_ctl, off_sigw, off_perm;
   uint64_t off_sP, off_sPn, off_sZ, off_sZt, off_sR, off_spart, off_sS, off_sL, off_sDinv, off_sLi,
       off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
@@ -187,6 +188,7 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_W = take(mx_dD * 4);
   w.off_Utw = take(mx_dd * 4);
   w.off_gram = take(mx_gram * 8);
+  w.off_gram2 = take(mx_gram * 8);
   w.off_V = take(mx_pairs * kJP * kJP * 4);
   w.off_V64 = take(mx_pairs * kJP * kJP * 8);
   w.off_gpart = take(mx_gpart * 8);
@@ -244,6 +246,7 @@ struct glr_handle {
   bool suspect = false;
   std::string err;
   int jac_inner = 1;   // inner Jacobi sweeps per pair visit
+  int jac_sort = 1;    // reorder rows by descending norm before every sweep
   double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
   int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
   bool prof = false;
@@ -295,6 +298,7 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   v.W = (float*)(w + h->ws.off_W);
   v.Utw = (float*)(w + h->ws.off_Utw);
   v.Apk = (double*)(w + h->ws.off_gram);
+  v.Apk2 = (double*)(w + h->ws.off_gram2);
   v.Vrot = (float*)(w + h->ws.off_V);
   v.V64 = (double*)(w + h->ws.off_V64);
   v.gpart = (double*)(w + h->ws.off_gpart);   // sized for every matrix whose Gram is split
@@ -406,9 +410,10 @@ hipError_t prof_collect(glr_handle* h) {
   } while (0)
 
 // Semi-Lazy SVD refresh: complete U of Mbar by block one-sided Jacobi
-glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s) {
+glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
+  MatView v = v0;   // the sort swaps Apk <-> Apk2 and Utw <-> W
   ProfScope all(h, s, GLR_PROF_REFRESH);
   {
     ProfScope p(h, s, GLR_PROF_JAC_INIT);
@@ -416,6 +421,11 @@ glr_status refresh_svd(glr_handle* h, const MatView& v, int64_t t, hipStream_t s
   }
   const int rounds = jac_seats(v.d) - 1;
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
+    if (h->jac_sort == 1 || (h->jac_sort == 2 && sw == 0)) {
+      GLR_HIP(h, launch_jac_sort(v, s));
+      std::swap(v.Apk, v.Apk2);
+      std::swap(v.Utw, v.W);
+    }
     for (int rd = 0; rd < rounds; ++rd) {
       {
         ProfScope p(h, s, GLR_PROF_JAC_SOLVE);
@@ -571,6 +581,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   h->cfg.shapes = h->shapes.data();
   h->ws = wl;
   if (const char* e = getenv("GLR_JAC_FLOOR")) h->jac_floor2 = ldexp(1.0, -2 * atoi(e));
+  if (const char* e = getenv("GLR_JAC_SORT")) h->jac_sort = atoi(e);
   if (const char* e = getenv("GLR_JAC_INNER")) {
     const int v = atoi(e);
     if (v >= 1 && v <= 16) h->jac_inner = v;
