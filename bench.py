@@ -24,6 +24,7 @@ the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -144,6 +145,56 @@ def roofline_entry(wl, name, total_ms, launches):
     return base
 
 
+# kernel group -> HIP source that defines it (for the traffic bookkeeping)
+KERNEL_SOURCES = {
+    "ef_mean": "glr_step_kernels.hip", "select": "glr_step_kernels.hip", "proj": "glr_step_kernels.hip",
+    "resid_opt": "glr_step_kernels.hip", "jac_rotate": "glr_jacobi.hip", "jac_solve": "glr_jacobi.hip",
+    "rr_rotate": "glr_jacobi.hip", "rr_solve": "glr_jacobi.hip", "sub_z": "glr_subspace.hip",
+    "sub_p": "glr_subspace.hip", "sub_chol": "glr_subspace.hip",
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_sha256(name):
+    """Digest of the source of a kernel group (its .hip file and the shared
+    device headers): a traffic figure applies only to the code it was taken on."""
+    src = os.path.join(ROOT, "paper_2507_08784_amd", "csrc")
+    h = hashlib.sha256()
+    for f in (KERNEL_SOURCES[name], "glr_device.hpp", "glr_internal.hpp"):
+        with open(os.path.join(src, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, name):
+    """HBM bytes per launch from the committed rocprofv3 counter runs
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading on a
+    plain copy of known size), or None when there is none for this kernel,
+    workload and source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            table = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    e = table.get(workload, {}).get(name)
+    if not e or e.get("source_sha256") != source_sha256(name):
+        return None
+    return e.get("bytes_per_launch")
+
+
+def copy_probe(device):
+    """A plain device-to-device copy of 1 GiB, three times: the calibration
+    kernel for the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = 1 << 28
+    a = torch.ones(n, dtype=torch.float32, device=device)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 3}), flush=True)
+
+
 def step_bytes(wl):
     """Algorithmic HBM bytes of one step: per worker read G, read E, write E
     (12 B/elem) plus the optimizer (16 B/elem MSGD, 24 Adam)."""
@@ -219,6 +270,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--tol", type=float, default=1e-6, help="refresh tolerance")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run the 1 GiB copy that calibrates the HBM traffic counters")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -235,6 +288,9 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.copy_probe:
+        copy_probe(dev)
+        return
     wl = get_workload(args.workload)
 
     pool_bytes = sum(wl.workers * m * n * 4 for m, n in wl.shapes)
@@ -303,7 +359,7 @@ def main():
         roof = {k: dominant[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
         roof["kernel"] = dominant["kernel"]
         roof["avg_us"] = dominant["avg_us"]
-        roof["traffic"] = None
+        roof["traffic"] = measured_traffic(wl.name, dominant["kernel"])
 
     eff = step_bytes(wl) / (ms_per_step / 1e3) / 1e9
     out = {
