@@ -173,10 +173,50 @@ constexpr int JAC_CHUNK = 512;   // columns of U^T rotated by one block
 // chasing orthogonality between tiny rows that fp32 rounding re-creates.
 //
 // A sweep of the 32 x 32 eigenproblem is 31 steps of 16 disjoint rotations
-// (circle method).  In a step, thread (a, b) of the 256 owns the 2 x 2 block
-// rows {p_a, q_a} x columns {p_b, q_b} of G and of V, so that the update
-// G <- J^T G J, V <- V J is in place and private to the thread; thread (a, a)
-// first computes rotation a from its own diagonal block.
+// (circle method); when the rows inside each of the two blocks already meet
+// the measure, only the 16 steps between the blocks are taken.  In a step,
+// thread (a, b) of the 256 owns the 2 x 2 block rows {p_a, q_a} x columns
+// {p_b, q_b} of G and of V, so that the update G <- J^T G J, V <- V J is in
+// place and private to the thread; thread (a, a) first computes rotation a
+// from its own diagonal block.
+// Rotation J = [[c, s], [-s, c]] that diagonalises [[gpp, gpq], [gpq, gqq]]:
+// t = tan(theta) = sign(d h) |h| / (|d| + sqrt(d^2 + h^2)), d = gqq - gpp,
+// h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  d and h are first scaled by a
+// power of two (exact) so that the square root, the reciprocal and the
+// reciprocal square root can start from fp32 estimates, each refined by one
+// Newton step in fp64 (relative error ~1e-14, far below what the iteration
+// needs; c^2 + s^2 = 1 to the same level).
+__device__ __forceinline__ void jac_rotation(double gpp, double gqq, double gpq, double& c, double& s) {
+  c = 1.0;
+  s = 0.0;
+  if (gpq == 0.0 || gpq * gpq <= 1e-34 * (gpp * gqq)) return;
+  const double d0 = gqq - gpp, h0 = 2.0 * gpq;
+  int ex;
+  (void)frexp(fmax(fabs(d0), fabs(h0)), &ex);
+  const double dd = ldexp(d0, -ex), h = ldexp(h0, -ex);   // max(|dd|, |h|) in [0.5, 1)
+  const double x = dd * dd + h * h;
+  const double yr = (double)rsqrtf((float)x);
+  double r = x * yr;
+  r = r + 0.5 * yr * (x - r * r);                         // sqrt(x)
+  const double den = fabs(dd) + r;
+  double q = (double)(1.0f / (float)den);
+  q = q * (2.0 - den * q);                                // 1 / den
+  double t = fabs(h) * q;
+  if ((dd < 0.0) != (h < 0.0)) t = -t;
+  const double z = 1.0 + t * t;
+  double y = (double)rsqrtf((float)z);
+  y = y * (1.5 - 0.5 * z * y * y);                        // 1 / sqrt(z)
+  c = y;
+  s = y * t;
+}
+
+// step k of the 16 steps that pair each row of one block with each row of
+// the other: rows (k, 16 + (k + step) mod 16)
+__device__ __forceinline__ void cross_pair(int step, int k, int& p, int& q) {
+  p = k;
+  q = kJB + ((k + step) & (kJB - 1));
+}
+
 __device__ __forceinline__ void inner_pair(int rd, int k, int& p, int& q) {
   constexpr int last = kJP - 1;
   if (k == 0) { p = rd; q = last; }
@@ -196,7 +236,7 @@ k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
   __shared__ double G[kJP][kJP + 1];
   __shared__ double V[kJP][kJP + 1];
   __shared__ double rc[kJP / 2], rs[kJP / 2];
-  __shared__ double red[4];
+  __shared__ double red[4], redw[4];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const double rm_prev = __longlong_as_double((long long)ctl->rowmax2_bits);
   // the pair's diagonal 32 x 32 block of A
@@ -224,43 +264,50 @@ k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
     atomicMax((unsigned long long*)&ctl->rowmax2_bits, (unsigned long long)__double_as_longlong(dmax));
   const double rowmax2 = fmax(dmax, rm_prev);
   const double floor2 = floor_rel2 * rowmax2;
-  double m2 = 0.0;
+  double m2 = 0.0, mw2 = 0.0;   // all pairs / pairs inside one block
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int e = tid + 256 * k, x = e / kJP, y = e % kJP;
     if (x < y) {
       const double gxx = G[x][x], gyy = G[y][y];
       const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
-      if (den > 0.0) m2 = fmax(m2, (g[k] / den) * (g[k] / den));
+      if (den > 0.0) {
+        const double q2 = (g[k] / den) * (g[k] / den);
+        m2 = fmax(m2, q2);
+        if ((x < kJB) == (y < kJB)) mw2 = fmax(mw2, q2);
+      }
     }
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) m2 = fmax(m2, __shfl_xor(m2, o, 64));
-  if (lane == 0) red[w] = m2;
+  for (int o = 32; o > 0; o >>= 1) {
+    m2 = fmax(m2, __shfl_xor(m2, o, 64));
+    mw2 = fmax(mw2, __shfl_xor(mw2, o, 64));
+  }
+  if (lane == 0) { red[w] = m2; redw[w] = mw2; }
   __syncthreads();
   const double m = sqrt(fmax(fmax(red[0], red[1]), fmax(red[2], red[3])));
+  // rows inside each block already orthogonal: only the 16 cross steps
+  const bool cross_only = sqrt(fmax(fmax(redw[0], redw[1]), fmax(redw[2], redw[3]))) <= (double)tol;
   if (tid == 0) atomicMax(&ctl->sweep_max_bits, __float_as_uint((float)m));
   if (m <= (double)tol) {
     if (tid == 0) skip[pair] = 1;
     return;
   }
   const int a = tid >> 4, b = tid & 15;
+  const int steps = cross_only ? kJB : kJP - 1;
   for (int sweep = 0; sweep < max_inner; ++sweep) {
-    for (int rd = 0; rd < kJP - 1; ++rd) {
+    for (int rd = 0; rd < steps; ++rd) {
       int pa, qa, pb, qb;
-      inner_pair(rd, a, pa, qa);
-      inner_pair(rd, b, pb, qb);
+      if (cross_only) {
+        cross_pair(rd, a, pa, qa);
+        cross_pair(rd, b, pb, qb);
+      } else {
+        inner_pair(rd, a, pa, qa);
+        inner_pair(rd, b, pb, qb);
+      }
       if (a == b) {
-        const double gpq = G[pa][qa], gpp = G[pa][pa], gqq = G[qa][qa];
-        double c = 1.0, s = 0.0;
-        if (gpq != 0.0 && fabs(gpq) > 1e-17 * sqrt(gpp * gqq)) {
-          const double zeta = (gqq - gpp) / (2.0 * gpq);
-          const double az = fabs(zeta);
-          const double root = az < 1e150 ? sqrt(1.0 + zeta * zeta) : az;
-          const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (az + root);
-          c = 1.0 / sqrt(1.0 + t * t);
-          s = c * t;
-        }
+        double c, s;
+        jac_rotation(G[pa][pa], G[qa][qa], G[pa][qa], c, s);
         rc[a] = c;
         rs[a] = s;
       }
