@@ -58,8 +58,8 @@ def uses_subspace(wl, d):
 FP64_ALU_PEAK = 78.6e12     # fp64 vector flop/s (the pair eigensolves)
 
 # groups that are one kernel launch each (the candidates for the dominant kernel)
-KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_rotate", "jac_solve",
-                 "rr_rotate", "rr_solve", "sub_z", "sub_p", "sub_chol")
+KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_update", "jac_solve",
+                 "rr_update", "rr_solve", "sub_z", "sub_p", "sub_chol")
 
 
 def jacobi_work(kind, d):
@@ -68,15 +68,15 @@ def jacobi_work(kind, d):
     flops)."""
     pairs, _ = jac_pairs(d)
     nb = (d + 15) // 16
-    if kind == "rotate":
-        # A <- J^T A J on the packed upper blocks (read + write, two 32 x 32 x 32
-        # fp64 products per pair of pairs) and U^T <- J^T U^T (read + write the
-        # 32 rows of every pair, one 32 x 32 x d fp32 product per pair)
-        return (2.0 * nb * (nb + 1) / 2 * 256 * 8 + pairs * 32.0 * d * 8,
-                pairs * 2.0 * 32 * 32 * d, pairs * (pairs + 1) / 2 * 2 * 2.0 * 32 ** 3, 0.0)
-    # solve: one cyclic sweep of 32 x 32 two-sided Jacobi per pair: 496
-    # rotations, each updating two rows and two columns of G and two columns of V
-    return 0.0, 0.0, 0.0, pairs * 496.0 * (6 * 32 * 3)
+    if kind == "update":
+        # A <- J^T A J on the packed upper blocks: read + write, two 32 x 32 x 32
+        # fp64 products per pair of pairs
+        return 2.0 * nb * (nb + 1) / 2 * 256 * 8, 0.0, pairs * (pairs + 1) / 2 * 2 * 2.0 * 32 ** 3, 0.0
+    # solve: one cyclic sweep of 32 x 32 two-sided Jacobi per pair (496
+    # rotations, each updating two rows and two columns of G and two columns
+    # of V), in the same launch as the previous round's U^T <- J^T U^T (read
+    # + write the 32 rows of every pair, one 32 x 32 x d fp32 product each)
+    return pairs * 32.0 * d * 8, pairs * 2.0 * 32 * 32 * d, 0.0, pairs * 496.0 * (6 * 32 * 3)
 
 
 def group_work(wl, name):
@@ -148,8 +148,8 @@ def roofline_entry(wl, name, total_ms, launches):
 # kernel group -> HIP source that defines it (for the traffic bookkeeping)
 KERNEL_SOURCES = {
     "ef_mean": "glr_step_kernels.hip", "select": "glr_step_kernels.hip", "proj": "glr_step_kernels.hip",
-    "resid_opt": "glr_step_kernels.hip", "jac_rotate": "glr_jacobi.hip", "jac_solve": "glr_jacobi.hip",
-    "rr_rotate": "glr_jacobi.hip", "rr_solve": "glr_jacobi.hip", "sub_z": "glr_subspace.hip",
+    "resid_opt": "glr_step_kernels.hip", "jac_update": "glr_jacobi.hip", "jac_solve": "glr_jacobi.hip",
+    "rr_update": "glr_jacobi.hip", "rr_solve": "glr_jacobi.hip", "sub_z": "glr_subspace.hip",
     "sub_p": "glr_subspace.hip", "sub_chol": "glr_subspace.hip",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")

@@ -182,13 +182,14 @@ typedef enum {
   GLR_PROF_RESID_OPT = 5,    /* residual + mean + reconstruction + optimizer */
   GLR_PROF_FULL_REFRESH = 6, /* Algorithm 3 refresh update */
   GLR_PROF_JAC_INIT = 7,     /* refresh: warm-start product and the fp64 Gram */
-  GLR_PROF_JAC_ROTATE = 8,   /* refresh: one round's Gram update and rotation of U^T rows */
+  GLR_PROF_JAC_UPDATE = 8,   /* refresh: two-sided update of the fp64 Gram in one Jacobi round */
   GLR_PROF_JAC_FINISH = 9,   /* refresh: sigma, sort, permutation, re-orthonormalisation */
   GLR_PROF_REFRESH = 10,     /* refresh: whole basis computation */
   GLR_PROF_SUB_ITER = 11,    /* tau = 1 refresh: one subspace iteration (all its launches) */
-  GLR_PROF_JAC_SOLVE = 12,   /* refresh: pair eigensolves of one Jacobi round */
-  GLR_PROF_RR_ROTATE = 13,   /* tau = 1 Rayleigh-Ritz Jacobi (K x K Gram): update and rotation */
-  GLR_PROF_RR_SOLVE = 14,    /* tau = 1 Rayleigh-Ritz Jacobi: pair eigensolves */
+  GLR_PROF_JAC_SOLVE = 12,   /* refresh: pair eigensolves of one round, with the previous round's
+                                rotation of U^T rows in the same launch */
+  GLR_PROF_RR_UPDATE = 13,   /* tau = 1 Rayleigh-Ritz Jacobi (K x K Gram): Gram update */
+  GLR_PROF_RR_SOLVE = 14,    /* tau = 1 Rayleigh-Ritz Jacobi: pair eigensolves and rotations */
   GLR_PROF_SUB_Z = 15,       /* tau = 1: Z = P^T Mo (K x D product) */
   GLR_PROF_SUB_P = 16,       /* tau = 1: Z Mo^T (K x d split-K product, before its reduction) */
   GLR_PROF_SUB_ORTH = 17,    /* tau = 1: CholeskyQR2 orthonormalisations (all their launches) */

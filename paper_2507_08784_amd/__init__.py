@@ -30,8 +30,8 @@ EXPORTED = (
     "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
 )
 PROF_GROUPS = ("ef_mean", "select", "topr", "proj", "rbar", "resid_opt", "full_refresh",
-               "jac_init", "jac_rotate", "jac_finish", "refresh", "sub_iter", "jac_solve",
-               "rr_rotate", "rr_solve", "sub_z", "sub_p", "sub_orth", "sub_chol")
+               "jac_init", "jac_update", "jac_finish", "refresh", "sub_iter", "jac_solve",
+               "rr_update", "rr_solve", "sub_z", "sub_p", "sub_orth", "sub_chol")
 
 
 class GlrError(RuntimeError):

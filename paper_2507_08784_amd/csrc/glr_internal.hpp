@@ -106,7 +106,12 @@ int jac_blocks(int64_t d);
 int jac_seats(int64_t d);
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
-hipError_t launch_jac_rotate(const MatView& v, int round, hipStream_t s);
+// one round = update(round) after solve(round); the rotation of U^T rows by
+// round k runs inside solve_apply(k + 1), or apply(k) after the last round
+hipError_t launch_jac_update(const MatView& v, int round, hipStream_t s);
+hipError_t launch_jac_solve_apply(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                                  hipStream_t s);
+hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s);
 // reorders the rows by descending diag(A): A (into Apk2) and U^T (into W);
 // the caller then swaps Apk <-> Apk2 and Utw <-> W
 hipError_t launch_jac_sort(const MatView& v, hipStream_t s);

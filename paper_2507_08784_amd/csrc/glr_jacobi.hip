@@ -11,7 +11,7 @@
 //   update : A <- J^T A J with J = diag(V_pair), block by block: the 32 x 32
 //            block (P, Q) of two pairs becomes V_P^T A_PQ V_Q (fp64 MFMA)
 //   apply  : rows of U^T <- V^T rows, in place, as u + (V - I)^T u
-//            (fp32 MFMA), in the same launch as the update
+//            (fp32 MFMA), in the same launch as the next round's solves
 // A sweep is one tournament (every pair of blocks meets once).  The sweeps
 // stop when every pair met in a sweep passes the measure of k_jac_solve.
 // The singular values are sqrt(diag A), sorted descending (ties keep the
@@ -224,12 +224,10 @@ __device__ __forceinline__ void inner_pair(int rd, int k, int& p, int& q) {
   if (p > q) { const int t = p; p = q; q = t; }
 }
 
-__global__ void __launch_bounds__(256)
-k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb,
-            float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
-            double* __restrict__ V64, int* __restrict__ skip) {
-  if (ctl->converged) return;
-  const int pair = blockIdx.x;
+__device__ __forceinline__ void solve_pair(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
+                                           int seats, int nb, float tol, int max_inner, double floor_rel2,
+                                           float* __restrict__ Vout, double* __restrict__ V64,
+                                           int* __restrict__ skip, int pair) {
   int bi, bj;
   pair_blocks(round, pair, seats, bi, bj);
   if (bi >= nb && bj >= nb) return;
@@ -390,7 +388,7 @@ __device__ __forceinline__ void apply_chunk(float* __restrict__ Utw, int64_t d, 
 // of A are read and written whole (coalesced) through one LDS tile; blocks
 // below the diagonal are not stored, so each stored block is written by
 // exactly one workgroup.
-constexpr int kUpdQ = 4;
+constexpr int kUpdQ = 2;
 
 __device__ __forceinline__ void update_group(double* __restrict__ Apk, const double* __restrict__ V64,
                                              const int* __restrict__ skip, int round, int seats, int nb,
@@ -465,45 +463,106 @@ __device__ __forceinline__ void update_group(double* __restrict__ Apk, const dou
   }
 }
 
-// one launch per round after the solve: workgroups [0, n_upd) update A,
-// the rest rotate the pairs' rows of U^T (chunks of JAC_CHUNK columns)
+// A <- J^T A J for one round (one P and up to kUpdQ consecutive Q per workgroup)
 __global__ void __launch_bounds__(256)
-k_jac_rotate(double* __restrict__ Apk, const double* __restrict__ V64, float* __restrict__ Utw, int64_t d,
-             const float* __restrict__ V32, const int* __restrict__ skip, const JacCtl* __restrict__ ctl,
-             int round, int seats, int nb, int pairs, int n_upd, int chunks) {
+k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int* __restrict__ skip,
+             const JacCtl* __restrict__ ctl, int round, int seats, int nb, int pairs) {
   if (ctl->converged) return;
   __shared__ double S[kJP][kJP + 1];
+  int P = 0, rem = blockIdx.x;
+  for (;;) {
+    const int cnt = (pairs - P + kUpdQ - 1) / kUpdQ;
+    if (rem < cnt) break;
+    rem -= cnt;
+    ++P;
+  }
+  update_group(Apk, V64, skip, round, seats, nb, pairs, P, P + rem * kUpdQ, S);
+}
+
+// the pair eigensolves of one round
+__global__ void __launch_bounds__(256)
+k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb, float tol,
+            int max_inner, double floor_rel2, float* __restrict__ Vout, double* __restrict__ V64,
+            int* __restrict__ skip) {
+  if (ctl->converged) return;
+  solve_pair(Apk, ctl, round, seats, nb, tol, max_inner, floor_rel2, Vout, V64, skip, blockIdx.x);
+}
+
+// the pair eigensolves of round `round` (workgroups [0, pairs)) together with
+// the rotation of U^T rows by the previous round's V (the rest): the rotation
+// does not depend on the new solves, and the solves leave most of the chip idle
+__global__ void __launch_bounds__(256)
+k_jac_solve_apply(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb,
+                  float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
+                  double* __restrict__ V64, int* __restrict__ skip, float* __restrict__ Utw, int64_t d,
+                  const float* __restrict__ Vprev, const int* __restrict__ skip_prev, int pairs, int chunks) {
+  if (ctl->converged) return;
   const int b = blockIdx.x;
-  if (b < n_upd) {
-    int P = 0, rem = b;
-    for (;;) {
-      const int cnt = (pairs - P + kUpdQ - 1) / kUpdQ;
-      if (rem < cnt) break;
-      rem -= cnt;
-      ++P;
-    }
-    update_group(Apk, V64, skip, round, seats, nb, pairs, P, P + rem * kUpdQ, S);
+  if (b < pairs) {
+    solve_pair(Apk, ctl, round, seats, nb, tol, max_inner, floor_rel2, Vout, V64, skip, b);
   } else {
-    const int idx = b - n_upd;
-    apply_chunk(Utw, d, V32, skip, round, seats, nb, idx / chunks, idx % chunks);
+    const int idx = b - pairs;
+    apply_chunk(Utw, d, Vprev, skip_prev, round - 1, seats, nb, idx / chunks, idx % chunks);
   }
 }
 
-hipError_t launch_jac_rotate(const MatView& v, int round, hipStream_t s) {
+// U^T rows of the last round of a sweep
+__global__ void __launch_bounds__(256)
+k_jac_apply(float* __restrict__ Utw, int64_t d, const float* __restrict__ V32, const int* __restrict__ skip,
+            const JacCtl* __restrict__ ctl, int round, int seats, int nb, int chunks) {
+  if (ctl->converged) return;
+  apply_chunk(Utw, d, V32, skip, round, seats, nb, blockIdx.x / chunks, blockIdx.x % chunks);
+}
+
+// per-round buffers alternate between two copies (round parity), so that a
+// round's solves can run while the previous round's rotations are applied
+struct RoundBufs {
+  float* V32;
+  double* V64;
+  int* skip;
+};
+static RoundBufs round_bufs(const MatView& v, int round) {
+  const int pairs = jac_seats(v.d) / 2, par = round & 1;
+  return {v.Vrot + (int64_t)par * pairs * kJP * kJP, v.V64 + (int64_t)par * pairs * kJP * kJP,
+          v.skip + (int64_t)par * pairs};
+}
+
+hipError_t launch_jac_update(const MatView& v, int round, hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   int n_upd = 0;
   for (int P = 0; P < pairs; ++P) n_upd += (pairs - P + kUpdQ - 1) / kUpdQ;
+  const RoundBufs rb = round_bufs(v, round);
+  hipLaunchKernelGGL(k_jac_update, dim3((unsigned)n_upd), dim3(256), 0, s, v.Apk, rb.V64, rb.skip, v.ctl, round,
+                     seats, nb, pairs);
+  return hipGetLastError();
+}
+
+hipError_t launch_jac_solve_apply(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                                  hipStream_t s) {
+  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
   const int chunks = (int)((v.d + JAC_CHUNK - 1) / JAC_CHUNK);
-  hipLaunchKernelGGL(k_jac_rotate, dim3((unsigned)(n_upd + pairs * chunks)), dim3(256), 0, s, v.Apk, v.V64,
-                     v.Utw, v.d, v.Vrot, v.skip, v.ctl, round, seats, nb, pairs, n_upd, chunks);
+  const RoundBufs rb = round_bufs(v, round), pb = round_bufs(v, round - 1);
+  hipLaunchKernelGGL(k_jac_solve_apply, dim3((unsigned)(pairs + pairs * chunks)), dim3(256), 0, s, v.Apk, v.ctl,
+                     round, seats, nb, tol, max_inner, floor_rel2, rb.V32, rb.V64, rb.skip, v.Utw, v.d, pb.V32,
+                     pb.skip, pairs, chunks);
+  return hipGetLastError();
+}
+
+hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s) {
+  const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
+  const int chunks = (int)((v.d + JAC_CHUNK - 1) / JAC_CHUNK);
+  const RoundBufs rb = round_bufs(v, round);
+  hipLaunchKernelGGL(k_jac_apply, dim3((unsigned)(pairs * chunks)), dim3(256), 0, s, v.Utw, v.d, rb.V32, rb.skip,
+                     v.ctl, round, seats, nb, chunks);
   return hipGetLastError();
 }
 
 hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                             hipStream_t s) {
   const int nb = jac_blocks(v.d), seats = jac_seats(v.d), pairs = seats / 2;
+  const RoundBufs rb = round_bufs(v, round);
   hipLaunchKernelGGL(k_jac_solve, dim3(pairs), dim3(256), 0, s, v.Apk, v.ctl, round, seats, nb, tol,
-                     max_inner, floor_rel2, v.Vrot, v.V64, v.skip);
+                     max_inner, floor_rel2, rb.V32, rb.V64, rb.skip);
   return hipGetLastError();
 }
 

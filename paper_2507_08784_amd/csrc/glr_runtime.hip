@@ -189,10 +189,10 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_Utw = take(mx_dd * 4);
   w.off_gram = take(mx_gram * 8);
   w.off_gram2 = take(mx_gram * 8);
-  w.off_V = take(mx_pairs * kJP * kJP * 4);
-  w.off_V64 = take(mx_pairs * kJP * kJP * 8);
+  w.off_V = take(2 * mx_pairs * kJP * kJP * 4);    // two copies: round parity
+  w.off_V64 = take(2 * mx_pairs * kJP * kJP * 8);
   w.off_gpart = take(mx_gpart * 8);
-  w.off_skip = take(mx_pairs * 4);
+  w.off_skip = take(2 * mx_pairs * 4);
   w.off_ctl = take(sizeof(JacCtl));
   w.off_sigw = take(mx_d * 4);
   w.off_perm = take(mx_d * 4);
@@ -214,10 +214,10 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rUtw = take(s_KK * 4);
   w.off_rY = take(s_KK * 4);
   w.off_rgram = take(r_gram * 8);
-  w.off_rV = take(r_pairs * kJP * kJP * 4);
-  w.off_rV64 = take(r_pairs * kJP * kJP * 8);
+  w.off_rV = take(2 * r_pairs * kJP * kJP * 4);
+  w.off_rV64 = take(2 * r_pairs * kJP * kJP * 8);
   w.off_rgpart = take(r_gpart * 8);
-  w.off_rskip = take(r_pairs * 4);
+  w.off_rskip = take(2 * r_pairs * 4);
   w.off_rctl = take(sizeof(JacCtl));
   w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
   w.off_rperm = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
@@ -409,6 +409,28 @@ hipError_t prof_collect(glr_handle* h) {
     if (e_ != hipSuccess) return hip_fail(h, e_, #call); \
   } while (0)
 
+// one sweep of the round-robin tournament: solve(0), then per round the Gram
+// update and the next round's solves fused with this round's U rotation
+hipError_t jacobi_sweep(glr_handle* h, const MatView& v, int rounds, int g_solve, int g_update, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  hipError_t e;
+  {
+    ProfScope p(h, s, g_solve);
+    if ((e = launch_jac_solve(v, 0, c.tol, h->jac_inner, h->jac_floor2, s)) != hipSuccess) return e;
+  }
+  for (int rd = 0; rd < rounds; ++rd) {
+    {
+      ProfScope p(h, s, g_update);
+      if ((e = launch_jac_update(v, rd, s)) != hipSuccess) return e;
+    }
+    ProfScope p(h, s, g_solve);
+    if (rd + 1 < rounds) e = launch_jac_solve_apply(v, rd + 1, c.tol, h->jac_inner, h->jac_floor2, s);
+    else e = launch_jac_apply(v, rd, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 // Semi-Lazy SVD refresh: complete U of Mbar by block one-sided Jacobi
 glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
@@ -426,14 +448,7 @@ glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t 
       std::swap(v.Apk, v.Apk2);
       std::swap(v.Utw, v.W);
     }
-    for (int rd = 0; rd < rounds; ++rd) {
-      {
-        ProfScope p(h, s, GLR_PROF_JAC_SOLVE);
-        GLR_HIP(h, launch_jac_solve(v, rd, c.tol, h->jac_inner, h->jac_floor2, s));
-      }
-      ProfScope p(h, s, GLR_PROF_JAC_ROTATE);
-      GLR_HIP(h, launch_jac_rotate(v, rd, s));
-    }
+    GLR_HIP(h, jacobi_sweep(h, v, rounds, GLR_PROF_JAC_SOLVE, GLR_PROF_JAC_UPDATE, s));
     GLR_HIP(h, launch_jac_check(v, c.tol, s));
     uint32_t conv = 0;
     GLR_HIP(h, hipMemcpyAsync(&conv, &v.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
@@ -468,14 +483,7 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
   const int rounds = jac_seats(rr.d) - 1;
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
-    for (int rd = 0; rd < rounds; ++rd) {
-      {
-        ProfScope p(h, s, GLR_PROF_RR_SOLVE);
-        GLR_HIP(h, launch_jac_solve(rr, rd, c.tol, h->jac_inner, h->jac_floor2, s));
-      }
-      ProfScope p(h, s, GLR_PROF_RR_ROTATE);
-      GLR_HIP(h, launch_jac_rotate(rr, rd, s));
-    }
+    GLR_HIP(h, jacobi_sweep(h, rr, rounds, GLR_PROF_RR_SOLVE, GLR_PROF_RR_UPDATE, s));
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
     uint32_t conv = 0;
     GLR_HIP(h, hipMemcpyAsync(&conv, &rr.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
