@@ -431,7 +431,8 @@ hipError_t jacobi_sweep(glr_handle* h, const MatView& v, int rounds, int g_solve
   return hipSuccess;
 }
 
-// Semi-Lazy SVD refresh: complete U of Mbar by block one-sided Jacobi
+// Semi-Lazy SVD refresh: complete U of Mbar by block Jacobi on the fp64 Gram of
+// W = U_prev^T Mo
 glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
