@@ -62,7 +62,7 @@ struct MatView {
   // caller buffers
   float* X;      const float* G;
   // workspace
-  float* Mbar;   float* Q;     float* lam_part;
+  float* Mbar;   float* Q;     float* Qpart; float* lam_part;
   float* W;      float* Utw;   double* Apk;  double* Apk2; float* Vrot;   double* V64;   int* skip;
   double* gpart;   // split-contraction partials of the Gram (or null)
   JacCtl* ctl;   float* sigma_w; int* perm;
@@ -83,6 +83,18 @@ struct ProfHook {
   void begin(int g) const { if (fn) fn(ctx, g, 1); }
   void end(int g) const { if (fn) fn(ctx, g, 0); }
 };
+
+// slices of the d contraction of the projection: enough workgroups to fill
+// the chip (tiles of 64 columns of D, one rank tile, per worker), slices of at
+// least 256
+inline int proj_splits(int64_t d, int64_t D, int r, int N) {
+  const int64_t tiles = ((D + 63) / 64) * ((r + 127) / 128) * N;
+  if (tiles >= 2048) return 1;
+  int64_t sp = (2048 + tiles - 1) / tiles;
+  const int64_t mx = d / 256;
+  if (sp > mx) sp = mx;
+  return sp < 1 ? 1 : (int)sp;
+}
 
 struct OptParams {
   int opt;                   // 0 MSGD, 1 Adam

@@ -30,7 +30,7 @@ inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign
 thread_local std::string g_create_error;
 
 struct WsLayout {
-  uint64_t off_Mbar, off_Q, off_lam, off_W, off_Utw, off_gram, off_gram2, off_V, off_V64, off_gpart, off_skip,
+  uint64_t off_Mbar, off_Q, off_Qpart, off_lam, off_W, off_Utw, off_gram, off_gram2, off_V, off_V64, off_gpart, off_skip,
       off_ctl, off_sigw, off_perm;
   uint64_t off_sP, off_sPn, off_sZ, off_sZt, off_sR, off_spart, off_sS, off_sL, off_sDinv, off_sLi,
       off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
@@ -140,7 +140,7 @@ uint64_t state_bytes_of(const glr_config* c) {
 }
 
 WsLayout ws_layout(const glr_config* c) {
-  uint64_t mx_mn = 0, mx_Q = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
+  uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
   uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
   uint64_t r_gram = 0, r_pairs = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
@@ -148,6 +148,8 @@ WsLayout ws_layout(const glr_config* c) {
     const Dims x = dims_of(c, i);
     mx(mx_mn, (uint64_t)(x.m * x.n));
     mx(mx_Q, (uint64_t)c->num_workers * (uint64_t)x.r * (uint64_t)x.D);
+    const int ps = proj_splits(x.d, x.D, x.r, c->num_workers);
+    if (ps > 1) mx(mx_Qp, (uint64_t)ps * c->num_workers * (uint64_t)x.r * (uint64_t)x.D);
     mx(mx_lam, (uint64_t)((x.D + 127) / 128) * (uint64_t)x.d);
     mx(mx_d, (uint64_t)x.d);
     if (use_subspace(c->tau, x.r, x.d)) {
@@ -184,6 +186,7 @@ WsLayout ws_layout(const glr_config* c) {
   };
   w.off_Mbar = take(mx_mn * 4);
   w.off_Q = take(mx_Q * 4);
+  w.off_Qpart = take(mx_Qp * 4);
   w.off_lam = take(mx_lam * 4);
   w.off_W = take(mx_dD * 4);
   w.off_Utw = take(mx_dd * 4);
@@ -294,6 +297,7 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   char* w = h->work;
   v.Mbar = (float*)(w + h->ws.off_Mbar);
   v.Q = (float*)(w + h->ws.off_Q);
+  v.Qpart = (float*)(w + h->ws.off_Qpart);
   v.lam_part = (float*)(w + h->ws.off_lam);
   v.W = (float*)(w + h->ws.off_W);
   v.Utw = (float*)(w + h->ws.off_Utw);

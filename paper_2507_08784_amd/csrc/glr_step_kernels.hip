@@ -264,17 +264,20 @@ hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
 template <int BM, int BN, int WM, int WN, bool RIGHT>
 __global__ void __launch_bounds__(256)
 k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
-       const int* __restrict__ J, float* __restrict__ Q, int64_t d, int64_t D, int r) {
+       const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
   using T = MfmaTile<BM, BN, WM, WN>;
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
   const int n0 = blockIdx.x * BN;   // b
   const int m0 = blockIdx.y * BM;   // k (rank index)
-  const int w = blockIdx.z;
+  const int w = blockIdx.z % N;     // worker
+  const int z = blockIdx.z / N;     // slice of the d contraction
+  const int64_t k0 = (int64_t)z * kslice;
+  const int klen = (int)(d - k0 < kslice ? d - k0 : kslice);
   const int64_t dD = d * D;
   const float* Gi = G + (int64_t)w * dD;
   const float* Ei = E + (int64_t)w * dD;
   T tile;
-  // Q is accumulated in fp64 across the 32-long slices of the d contraction
+  // fp32 accumulators are added into fp64 ones every 512 terms of the slice
   double dacc[T::TM][T::TN][16];
 #pragma unroll
   for (int tm = 0; tm < T::TM; ++tm)
@@ -282,16 +285,16 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
     for (int tn = 0; tn < T::TN; ++tn)
 #pragma unroll
       for (int v = 0; v < 16; ++v) dacc[tm][tn][v] = 0.0;
-  LoadK<BM, 32, false, true> la(Ut, nullptr, d, m0, r, (int)d, J);
+  LoadK<BM, 32, false, true> la(Ut + k0, nullptr, d, m0, r, klen, J);
   if (RIGHT) {
     // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
-    LoadK<BN, 32, true, false> lb(Gi, Ei, d, n0, (int)D, (int)d, nullptr);
-    tile.run(la, lb, (int)d, smem, dacc);
+    LoadK<BN, 32, true, false> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
+    tile.run(la, lb, klen, smem, dacc);
   } else {
-    LoadR<BN, 32, true> lb(Gi, Ei, D, n0, (int)D, (int)d);
-    tile.run(la, lb, (int)d, smem, dacc);
+    LoadR<BN, 32, true> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
+    tile.run(la, lb, klen, smem, dacc);
   }
-  float* Qi = Q + (int64_t)w * r * D;
+  float* Qz = Qpart + ((int64_t)z * N + w) * r * D;
 #pragma unroll
   for (int tm = 0; tm < T::TM; ++tm)
 #pragma unroll
@@ -301,25 +304,28 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int k = m0 + tile.row(tm, v);
-        if (k < r) Qi[(int64_t)k * D + b] = (float)dacc[tm][tn][v];
+        if (k < r) Qz[(int64_t)k * D + b] = (float)dacc[tm][tn][v];
       }
     }
 }
 
 hipError_t launch_proj(const MatView& v, hipStream_t s) {
   const int r = v.r;
+  const int splits = proj_splits(v.d, v.D, r, v.N);
+  const int64_t kslice = ((v.d + splits - 1) / splits + 31) / 32 * 32;
+  float* const out = splits > 1 ? v.Qpart : v.Q;
   dim3 grid;
-  grid.z = v.N;
+  grid.z = (unsigned)(v.N * splits);
 #define GLR_PROJ(BM, BN, WM, WN)                                                                  \
   do {                                                                                            \
     grid.x = (unsigned)((v.D + BN - 1) / BN);                                                     \
     grid.y = (unsigned)((r + BM - 1) / BM);                                                       \
     if (v.right)                                                                                  \
       hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true>), grid, dim3(kThreads), 0, s, v.G, v.E,    \
-                         v.Ut, v.J, v.Q, v.d, v.D, r);                                            \
+                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
     else                                                                                          \
       hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false>), grid, dim3(kThreads), 0, s, v.G, v.E,   \
-                         v.Ut, v.J, v.Q, v.d, v.D, r);                                            \
+                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
   } while (0)
   if (r <= 32) GLR_PROJ(32, 128, 1, 4);
   else if (r <= 64) GLR_PROJ(64, 64, 2, 2);
@@ -328,19 +334,32 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// S6: Rbar = (1/N) sum_i Q^(i), fixed worker order
-__global__ void k_rbar(const float* __restrict__ Q, int N, int64_t rD, float* __restrict__ Rbar) {
+// S6 (with the slices of the projection): Q^(i) = sum over slices of the
+// partial products, Rbar = (1/N) sum_i Q^(i); both sums in a fixed order, fp64
+__global__ void k_proj_reduce(const float* __restrict__ part, int splits, int N, int64_t rD, float* __restrict__ Q,
+                              float* __restrict__ Rbar) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < rD; i += stride) {
-    float acc = 0.f;
-    for (int w = 0; w < N; ++w) acc += Q[(int64_t)w * rD + i];
-    Rbar[i] = acc / (float)N;
+    double rsum = 0.0;
+    for (int w = 0; w < N; ++w) {
+      double q = 0.0;
+      if (splits > 1) {
+        for (int z = 0; z < splits; ++z) q += (double)part[((int64_t)z * N + w) * rD + i];
+        Q[(int64_t)w * rD + i] = (float)q;
+      } else {
+        q = (double)Q[(int64_t)w * rD + i];
+      }
+      rsum += q;
+    }
+    Rbar[i] = (float)(rsum / (double)N);
   }
 }
 
 hipError_t launch_rbar(const MatView& v, hipStream_t s) {
   const int64_t rD = (int64_t)v.r * v.D;
-  hipLaunchKernelGGL(k_rbar, dim3(grid_for(rD)), dim3(kThreads), 0, s, v.Q, v.N, rD, v.Rbar);
+  const int splits = proj_splits(v.d, v.D, v.r, v.N);
+  hipLaunchKernelGGL(k_proj_reduce, dim3(grid_for(rD)), dim3(kThreads), 0, s, v.Qpart, splits, v.N, rD, v.Q,
+                     v.Rbar);
   return hipGetLastError();
 }
 
@@ -354,34 +373,38 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // move as 16-byte vectors.  P (gathered rows of U^T) and Q^(i) are staged
 // through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
-constexpr int RO_ROWS = 128, RO_COLS = 64;
+constexpr int RO_COLS = 64;
 
-template <int OPT, bool RIGHT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int OPT, bool RIGHT, int ROWS>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ROWS == 64 ? 3 : 2, ROWS == 64 ? 3 : 2)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
             const float* __restrict__ Q, const float* __restrict__ Rbar, const float* __restrict__ Ut,
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
-  using T = MfmaTile<RO_COLS, RO_ROWS, 1, 4>;   // engine rows = tile columns
+  // engine rows = tile columns; each wave owns 32 tile rows, one per lane
+  constexpr int WN = ROWS / 32, WM = 4 / WN;
+  using T = MfmaTile<RO_COLS, ROWS, WM, WN>;
+  constexpr int TM = T::TM;
+  static_assert(T::TN == 1, "one tile row per lane");
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
   const int c0 = blockIdx.x * RO_COLS;   // first column of the tile
-  const int r0 = blockIdx.y * RO_ROWS;   // first row of the tile
+  const int r0 = blockIdx.y * ROWS;      // first row of the tile
   const int64_t mn = m * n;
   const bool vec = (n & 3) == 0;
   // this lane's outputs: for tm, g: row = r0 + ec, columns cb .. cb+3
   const int lane = lane_id();
-  const int ec = (wave_id() % 4) * 32 + (lane & 31);
+  const int ec = (wave_id() % WN) * 32 + (lane & 31);
   const int64_t row = r0 + ec;
-  const int cl = c0 + 4 * (lane >> 5);   // column of (tm, g) is cl + 32 tm + 8 g
+  const int cl = c0 + (wave_id() / WN) * T::WTM + 4 * (lane >> 5);   // column of (tm, g): cl + 32 tm + 8 g
   const int64_t rbase = row * n;
   auto ncols = [&](int tm, int g) -> int {
     const int64_t cb = cl + 32 * tm + 8 * g;
     return row < m ? (int)(n - cb >= 4 ? 4 : (n - cb > 0 ? n - cb : 0)) : 0;
   };
-  float ebar[2][16];
+  float ebar[TM][16];
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int v = 0; v < 16; ++v) ebar[tm][v] = 0.f;
 
@@ -390,9 +413,9 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     float* Ei = E + (int64_t)wk * mn;
     const float* Qi = Q + (int64_t)wk * r * D;
     // G^(i) and E^(i) for this lane's elements, in flight during the product
-    float gv[2][16], eo[2][16];
+    float gv[TM][16], eo[TM][16];
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int64_t o = rbase + cl + 32 * tm + 8 * g;
@@ -414,16 +437,16 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     if (!RIGHT) {
       // rows a < d, columns b < D: C[a][b] = sum_k Ut[J[k]][a] Q[k][b]
       LoadR<RO_COLS, 32, false> la(Qi, nullptr, D, c0, (int)D, r);
-      LoadR<RO_ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+      LoadR<ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
       tile.run(la, lb, r, smem);
     } else {
       // rows b < D, columns a < d: C[b][a] = sum_k Q[k][b] Ut[J[k]][a]
       LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
-      LoadR<RO_ROWS, 32, false> lb(Qi, nullptr, D, r0, (int)D, r);
+      LoadR<ROWS, 32, false> lb(Qi, nullptr, D, r0, (int)D, r);
       tile.run(la, lb, r, smem);
     }
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         float ev[4];
@@ -451,16 +474,16 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
   T tile;
   if (!RIGHT) {
     LoadR<RO_COLS, 32, false> la(Rbar, nullptr, D, c0, (int)D, r);
-    LoadR<RO_ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+    LoadR<ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
     tile.run(la, lb, r, smem);
   } else {
     LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
-    LoadR<RO_ROWS, 32, false> lb(Rbar, nullptr, D, r0, (int)D, r);
+    LoadR<ROWS, 32, false> lb(Rbar, nullptr, D, r0, (int)D, r);
     tile.run(la, lb, r, smem);
   }
   const float fN = (float)N;
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int64_t o = rbase + cl + 32 * tm + 8 * g;
@@ -518,12 +541,21 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
 }
 
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + RO_ROWS - 1) / RO_ROWS));
-#define GLR_RO(OPT, R)                                                                              \
-  hipLaunchKernelGGL((k_resid_opt<OPT, R>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q,    \
+  // 64-row tiles halve each lane's share of G, E and E-bar; 128-row tiles
+  // when the matrix has too few rows of tiles otherwise
+  const bool small = (v.m + 63) / 64 * ((v.n + RO_COLS - 1) / RO_COLS) >= 1024;
+  const int rows = small ? 64 : 128;
+  dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + rows - 1) / rows));
+#define GLR_RO(OPT, R, ROWS)                                                                        \
+  hipLaunchKernelGGL((k_resid_opt<OPT, R, ROWS>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q, \
                      v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
-  if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
-  else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
+  if (small) {
+    if (o.opt == 0) { if (v.right) GLR_RO(0, true, 64); else GLR_RO(0, false, 64); }
+    else            { if (v.right) GLR_RO(1, true, 64); else GLR_RO(1, false, 64); }
+  } else {
+    if (o.opt == 0) { if (v.right) GLR_RO(0, true, 128); else GLR_RO(0, false, 128); }
+    else            { if (v.right) GLR_RO(1, true, 128); else GLR_RO(1, false, 128); }
+  }
 #undef GLR_RO
   return hipGetLastError();
 }
