@@ -437,20 +437,25 @@ __device__ __forceinline__ void update_group(double* __restrict__ Apk, const dou
       else S[h * kJB + ec][g * kJB + er] = sv[k];
     }
     __syncthreads();
-    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+    // a pair that met the stopping rule this round has V = I: its product is skipped
+    if (!sq) {
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int k = 0; k < kJP / 4; ++k) acc = mfma64(S[wi + li][4 * k + lk], vqo[k], acc);   // T = A_PQ V_Q
-    __syncthreads();
+      for (int k = 0; k < kJP / 4; ++k) acc = mfma64(S[wi + li][4 * k + lk], vqo[k], acc);   // T = A_PQ V_Q
+      __syncthreads();
 #pragma unroll
-    for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
-    __syncthreads();
-    acc = f64x4{0.0, 0.0, 0.0, 0.0};
+      for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
+      __syncthreads();
+    }
+    if (!sp) {
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int k = 0; k < kJP / 4; ++k) acc = mfma64(vpo[k], S[4 * k + lk][wj + li], acc);  // V_P^T T
-    __syncthreads();
+      for (int k = 0; k < kJP / 4; ++k) acc = mfma64(vpo[k], S[4 * k + lk][wj + li], acc);  // V_P^T T
+      __syncthreads();
 #pragma unroll
-    for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
-    __syncthreads();
+      for (int v = 0; v < 4; ++v) S[wi + 4 * v + lk][wj + li] = acc[v];
+      __syncthreads();
+    }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int h = k >> 1, g = k & 1;
