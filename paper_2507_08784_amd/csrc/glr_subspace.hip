@@ -365,10 +365,19 @@ __device__ __forceinline__ void tile_store(const CTile* src, double* __restrict_
   }
 }
 
-__device__ __forceinline__ void tile_store32(const CTile* src, float* __restrict__ dst, int64_t ld) {
+// 1 / sqrt(S_ii) for i < K (1 where S_ii is not positive, and in the padding)
+__device__ __forceinline__ double chol_scale(const double* __restrict__ S, int K, int i) {
+  if (i >= K) return 1.0;
+  const double dii = S[(int64_t)i * K + i];
+  return dii > 0.0 ? 1.0 / sqrt(dii) : 1.0;
+}
+
+// global fp32 tile <- LDS tile with column j scaled by 1 / sqrt(S_cc), c = c0 + j
+__device__ __forceinline__ void tile_store32(const CTile* src, float* __restrict__ dst, int64_t ld,
+                                             const double* __restrict__ S, int K, int c0) {
   for (int e = threadIdx.x; e < CT * CT; e += 256) {
     const int i = e / CT, j = e % CT;
-    dst[(int64_t)i * ld + j] = (float)src[i][j];
+    dst[(int64_t)i * ld + j] = (float)(src[i][j] * chol_scale(S, K, c0 + j));
   }
 }
 
@@ -385,56 +394,148 @@ __device__ __forceinline__ void acc_to_lds(const f64x4 (&acc)[2][2], CTile* dst,
       }
 }
 
-// in-place Cholesky of the SPD tile T (lower triangle), then Dl = T^-1
-__device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
-  const int tid = threadIdx.x;
-  bool bad = false;
-  for (int j = 0; j < CT; ++j) {
-    double piv = T[j][j];
+__device__ __forceinline__ double lane_bcast(double x, int l) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// One wave factors the 16 x 16 diagonal block of T at offset o and inverts
+// the factor: lane l holds row l % 16 in registers.  Right-looking: after step
+// j, column j of L is final and row j of X = L^-1 is final once scaled by
+// 1 / L_jj; the later rows then subtract L_ij X_j.  L replaces the block
+// (zeros above the diagonal), X goes into Dl at the same place.
+__device__ __forceinline__ void chol16(CTile* T, CTile* Dl, int o, bool& bad) {
+  const int li = lane_id() & 15;
+  double a[16], y[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    a[k] = T[o + li][o + k];
+    y[k] = (k == li) ? 1.0 : 0.0;
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    double piv = lane_bcast(a[j], j);
     if (!(piv > 0.0)) { bad = true; piv = 1e-300; }
     const double ljj = sqrt(piv), inv = 1.0 / ljj;
+    a[j] = (li > j) ? a[j] * inv : ((li == j) ? ljj : 0.0);
+#pragma unroll
+    for (int k = j + 1; k < 16; ++k) a[k] = fma(-a[j], lane_bcast(a[j], k), a[k]);
+    const double sc = (li == j) ? inv : 1.0;
+    const double coef = (li > j) ? a[j] : 0.0;
+#pragma unroll
+    for (int c = 0; c <= j; ++c) {
+      y[c] *= sc;
+      y[c] = fma(-coef, lane_bcast(y[c], j), y[c]);
+    }
+  }
+  if (lane_id() < 16) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      T[o + li][o + k] = a[k];
+      Dl[o + li][o + k] = y[k];
+    }
+  }
+}
+
+// acc (+)= sign * X Y^T for 16 x 16 blocks of LDS tiles: X at (xr, xc) of
+// tile Xs, Y at (yr, yc) of tile Ys; output C[4v + lane/16][lane % 16]
+__device__ __forceinline__ f64x4 blk_abt(const CTile* Xs, int xr, int xc, const CTile* Ys, int yr, int yc,
+                                         double sign, f64x4 acc) {
+  const int l = lane_id(), r = l & 15, kk = l >> 4;
+#pragma unroll
+  for (int k0 = 0; k0 < 16; k0 += 4)
+    acc = mfma64(sign * Xs[xr + r][xc + k0 + kk], Ys[yr + r][yc + k0 + kk], acc);
+  return acc;
+}
+// acc (+)= sign * X Y for 16 x 16 blocks (Y read down its columns)
+__device__ __forceinline__ f64x4 blk_ab(const CTile* Xs, int xr, int xc, const CTile* Ys, int yr, int yc,
+                                        double sign, f64x4 acc) {
+  const int l = lane_id(), r = l & 15, kk = l >> 4;
+#pragma unroll
+  for (int k0 = 0; k0 < 16; k0 += 4)
+    acc = mfma64(sign * Xs[xr + r][xc + k0 + kk], Ys[yr + k0 + kk][yc + r], acc);
+  return acc;
+}
+__device__ __forceinline__ void blk_store(CTile* Cs, int cr, int cc, f64x4 acc) {
+  const int l = lane_id();
+#pragma unroll
+  for (int v = 0; v < 4; ++v) Cs[cr + 4 * v + (l >> 4)][cc + (l & 15)] = acc[v];
+}
+__device__ __forceinline__ f64x4 blk_load(const CTile* Cs, int cr, int cc) {
+  const int l = lane_id();
+  f64x4 acc;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) acc[v] = Cs[cr + 4 * v + (l >> 4)][cc + (l & 15)];
+  return acc;
+}
+
+// In-place Cholesky of the SPD tile T (lower triangle; zeros above), then
+// Dl = T^-1.  Blocked in 16-column panels: one wave factors and inverts the
+// diagonal block, the blocks below it become L_iq = A_iq X_qq^T and the
+// trailing lower blocks take A_ij -= L_iq L_jq^T (fp64 MFMA, one block per
+// wave).  The off-diagonal blocks of X then follow block row by block row:
+// X_ij = -X_ii sum_{j <= k < i} L_ik X_kj.
+__device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
+  const int w = wave_id();
+  for (int e = threadIdx.x; e < CT * CT; e += 256) Dl[e / CT][e % CT] = 0.0;
+  bool bad = false;
+  __syncthreads();
+  for (int q = 0; q < 4; ++q) {
+    const int o = 16 * q;
+    if (w == 0) chol16(T, Dl, o, bad);
     __syncthreads();
-    if (tid < CT) {
-      if (tid > j) T[tid][j] *= inv;
-      else if (tid == j) T[j][j] = ljj;
+    if (w < 3 - q) {
+      const int i = 16 * (q + 1 + w);
+      const f64x4 acc = blk_abt(T, i, o, Dl, o, o, 1.0, f64x4{0.0, 0.0, 0.0, 0.0});
+      blk_store(T, i, o, acc);
     }
     __syncthreads();
-    for (int e = tid; e < CT * CT; e += 256) {
-      const int i = e / CT, k = e % CT;
-      if (k > j && k <= i) T[i][k] -= T[i][j] * T[k][j];
+    const int nblk = (3 - q) * (4 - q) / 2;
+    for (int b = w; b < nblk; b += 4) {
+      int bi = q + 1, rem = b;
+      while (rem > bi - q - 1) { rem -= bi - q; ++bi; }
+      const int bj = q + 1 + rem;
+      f64x4 acc = blk_load(T, 16 * bi, 16 * bj);
+      acc = blk_abt(T, 16 * bi, o, T, 16 * bj, o, -1.0, acc);
+      blk_store(T, 16 * bi, 16 * bj, acc);
     }
     __syncthreads();
   }
-  if (bad && tid == 0) atomicOr(status, 4u);
-  for (int e = tid; e < CT * CT; e += 256) Dl[e / CT][e % CT] = (e / CT == e % CT) ? 1.0 : 0.0;
-  __syncthreads();
-  // right-looking forward substitution: row j of T^-1 is final once scaled
-  for (int j = 0; j < CT; ++j) {
-    const double inv = 1.0 / T[j][j];
-    if (tid <= j) Dl[j][tid] *= inv;
+  if (bad && threadIdx.x == 0) atomicOr(status, 4u);
+  for (int bi = 1; bi < 4; ++bi) {
+    if (w < bi) {
+      f64x4 acc{0.0, 0.0, 0.0, 0.0};
+      for (int k = w; k < bi; ++k) acc = blk_ab(T, 16 * bi, 16 * k, Dl, 16 * k, 16 * w, 1.0, acc);
+      blk_store(Dl, 16 * bi, 16 * w, acc);
+    }
     __syncthreads();
-    for (int e = tid; e < CT * CT; e += 256) {
-      const int i = e / CT, c = e % CT;
-      if (i > j && c <= j) Dl[i][c] -= T[i][j] * Dl[j][c];
+    if (w < bi) {
+      const f64x4 acc = blk_ab(Dl, 16 * bi, 16 * bi, Dl, 16 * bi, 16 * w, -1.0, f64x4{0.0, 0.0, 0.0, 0.0});
+      blk_store(Dl, 16 * bi, 16 * w, acc);
     }
     __syncthreads();
   }
 }
 
-// copy S (K x K) into the padded work matrix; block 0 factors tile (0, 0)
+// copy the scaled Gram D^-1/2 S D^-1/2 (K x K, D = diag S) into the padded
+// work matrix; block 0 factors tile (0, 0)
 __global__ void __launch_bounds__(256)
 k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ Sw,
              double* __restrict__ Lm, double* __restrict__ Dm, uint32_t* __restrict__ status) {
   const int64_t n = (int64_t)Kp * Kp;
   for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
     const int i = (int)(e / Kp), j = (int)(e % Kp);
-    Sw[e] = (i < K && j < K) ? S[(int64_t)i * K + j] : (i == j ? 1.0 : 0.0);
+    Sw[e] = (i < K && j < K) ? S[(int64_t)i * K + j] * chol_scale(S, K, i) * chol_scale(S, K, j)
+                             : (i == j ? 1.0 : 0.0);
   }
   if (blockIdx.x != 0) return;
   __shared__ CTile T[CT], Dl[CT];
   for (int e = threadIdx.x; e < CT * CT; e += 256) {
     const int i = e / CT, j = e % CT;
-    T[i][j] = (i < K && j < K) ? S[(int64_t)i * K + j] : (i == j ? 1.0 : 0.0);
+    T[i][j] = (i < K && j < K) ? S[(int64_t)i * K + j] * chol_scale(S, K, i) * chol_scale(S, K, j)
+                               : (i == j ? 1.0 : 0.0);
   }
   __syncthreads();
   chol_tile(T, Dl, status);
@@ -444,7 +545,8 @@ k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ S
 
 __global__ void __launch_bounds__(256)
 k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, double* __restrict__ Dm,
-            double* __restrict__ Xm, float* __restrict__ Linv, uint32_t* __restrict__ status) {
+            double* __restrict__ Xm, float* __restrict__ Linv, const double* __restrict__ S, int K,
+            uint32_t* __restrict__ status) {
   __shared__ CTile A[CT], B[CT], C[CT];
   const int nt = Kp / CT;
   const int mrows = nt - p - 1;
@@ -513,7 +615,7 @@ k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, dou
   if (c == p) {
     __syncthreads();
     tile_store(A, tile(Xm, p, p), Kp, false);
-    tile_store32(A, lo, Kp);
+    tile_store32(A, lo, Kp, S, K, c * CT);
     return;
   }
   acc_zero(acc);
@@ -532,7 +634,7 @@ k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, dou
   acc_to_lds(acc, B, false);
   __syncthreads();
   tile_store(B, tile(Xm, p, c), Kp, false);
-  tile_store32(B, lo, Kp);
+  tile_store32(B, lo, Kp, S, K, c * CT);
 }
 
 static hipError_t launch_chol_inv(const MatView& v, int K, hipStream_t s) {
@@ -542,7 +644,7 @@ static hipError_t launch_chol_inv(const MatView& v, int K, hipStream_t s) {
   for (int p = 0; p < nt; ++p) {
     const int m = nt - p - 1;
     hipLaunchKernelGGL(k_chol_step, dim3(m * (m + 1) / 2 + nt), dim3(256), 0, s, p, Kp, v.sub_T,
-                       v.sub_L, v.sub_Dinv, v.sub_Li, v.sub_Linv, v.status);
+                       v.sub_L, v.sub_Dinv, v.sub_Li, v.sub_Linv, v.sub_S, K, v.status);
   }
   return hipGetLastError();
 }
@@ -604,11 +706,13 @@ size_t sub_part_floats(int K, int64_t d, int64_t D) {
   upd(K, (int)d, (int)D);
   return mx;
 }
-static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, const ProfHook& prof,
-                            hipStream_t s) {
+// Rows of Y (K x L) <- an orthonormal basis of their span by `passes`
+// rounds of CholeskyQR on the diagonally scaled Gram
+static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, int passes,
+                            const ProfHook& prof, hipStream_t s) {
   const int Kp = chol_pad(K);
   prof.begin(GLR_PROF_SUB_ORTH);
-  for (int pass = 0; pass < 2; ++pass) {
+  for (int pass = 0; pass < passes; ++pass) {
     GemmPlan pg = plan_splits(K, K, (int)L);
     gemm_launch<true, 0>(Y, L, Y, L, v.sub_part, K, K, K, (int)L, pg, (int64_t)K * K, nullptr, nullptr, s);
     hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
@@ -638,7 +742,9 @@ hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStrea
                        v.sub_P, K, v.d, k0, k1, (uint32_t)v.mat);
   }
   hipLaunchKernelGGL(k_sub_reset, dim3(1), dim3(64), 0, s, v.sub_ctl);
-  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, ProfHook{}, s);
+  // warm rows are the previous Ritz vectors, orthonormal already
+  if (warm) return hipGetLastError();
+  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, 2, ProfHook{}, s);
 }
 
 // one iteration; writes the subspace change into sub_ctl
@@ -653,7 +759,9 @@ hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hi
   else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
     gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
   prof.end(GLR_PROF_SUB_Z);
-  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, prof, s);
+  // Z only carries the span into the next product: one scaled pass keeps it
+  // well conditioned
+  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, 1, prof, s);
   if (e != hipSuccess) return e;
   // P_new = Z Mo^T  (K x d): B(k=b, j=a) = Mo[a][b]
   GemmPlan p2 = plan_splits(K, (int)d, (int)D);
@@ -665,7 +773,7 @@ hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hi
   prof.end(GLR_PROF_SUB_P);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_part,
                      p2.splits, (int64_t)K * d, v.sub_Pn, (double*)nullptr);
-  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, prof, s);
+  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, 2, prof, s);
   if (e != hipSuccess) return e;
   // change: R = P_new - (P_new P^T) P ;  C = P_new P^T (K x K)
   GemmPlan pc = plan_splits(K, K, (int)d);
