@@ -44,10 +44,15 @@ def dims(shape):
     return m, n, min(m, n), max(m, n)
 
 
-def jac_pairs(d, jb=16):
+def jac_groups(d, jb=16):
+    """(groups per round, rounds per sweep) of the Jacobi tournament: seats
+    = the smallest power of 4 holding the 16-row blocks, groups of 4 blocks,
+    (seats - 1) / 3 rounds."""
     nb = (d + jb - 1) // jb
-    seats = max(2, nb + (nb & 1))
-    return seats // 2, seats - 1
+    seats = 4
+    while seats < nb:
+        seats *= 4
+    return seats // 4, (seats - 1) // 3
 
 
 def uses_subspace(wl, d):
@@ -64,19 +69,19 @@ KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_update", "jac_so
 
 def jacobi_work(kind, d):
     """Per-launch work of one Jacobi round on the fp64 Gram of d rows (16-row
-    blocks, 32-row pairs): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64 ALU
-    flops)."""
-    pairs, _ = jac_pairs(d)
+    blocks, 64-row groups): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64
+    ALU flops)."""
+    groups, _ = jac_groups(d)
     nb = (d + 15) // 16
     if kind == "update":
-        # A <- J^T A J on the packed upper blocks: read + write, two 32 x 32 x 32
-        # fp64 products per pair of pairs
-        return 2.0 * nb * (nb + 1) / 2 * 256 * 8, 0.0, pairs * (pairs + 1) / 2 * 2 * 2.0 * 32 ** 3, 0.0
-    # solve: one cyclic sweep of 32 x 32 two-sided Jacobi per pair (496
+        # A <- J^T A J on the packed upper blocks: read + write, two 64 x 64 x 64
+        # fp64 products per pair of groups
+        return 2.0 * nb * (nb + 1) / 2 * 256 * 8, 0.0, groups * (groups + 1) / 2 * 2 * 2.0 * 64 ** 3, 0.0
+    # solve: one cyclic sweep of 64 x 64 two-sided Jacobi per group (2016
     # rotations, each updating two rows and two columns of G and two columns
     # of V), in the same launch as the previous round's U^T <- J^T U^T (read
-    # + write the 32 rows of every pair, one 32 x 32 x d fp32 product each)
-    return pairs * 32.0 * d * 8, pairs * 2.0 * 32 * 32 * d, 0.0, pairs * 496.0 * (6 * 32 * 3)
+    # + write the 64 rows of every group, one 64 x 64 x d fp32 product each)
+    return groups * 64.0 * d * 8, groups * 2.0 * 64 * 64 * d, 0.0, groups * 2016.0 * (6 * 64 * 3)
 
 
 def group_work(wl, name):

@@ -140,9 +140,9 @@ uint64_t state_bytes_of(const glr_config* c) {
 }
 
 WsLayout ws_layout(const glr_config* c) {
-  uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_pairs = 0, mx_d = 0;
+  uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_groups = 0, mx_d = 0;
   uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
-  uint64_t r_gram = 0, r_pairs = 0, r_gpart = 0, mx_gpart = 0;
+  uint64_t r_gram = 0, r_groups = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
   for (int i = 0; i < c->num_mats; ++i) {
     const Dims x = dims_of(c, i);
@@ -158,8 +158,7 @@ WsLayout ws_layout(const glr_config* c) {
       mx(s_Kd, K * (uint64_t)x.d);
       mx(s_KD, K * (uint64_t)x.D);
       mx(s_part, (uint64_t)sub_part_floats(Ki, x.d, x.D));
-      const uint64_t rp = (uint64_t)jac_seats(Ki) / 2;
-      mx(r_pairs, rp);
+      mx(r_groups, (uint64_t)jac_groups(Ki));
       mx(r_gram, (uint64_t)pk_doubles(jac_blocks(Ki)));
       const int rs = gram_splits(Ki, x.D);
       if (rs > 1) mx(r_gpart, (uint64_t)rs * K * K);
@@ -168,13 +167,12 @@ WsLayout ws_layout(const glr_config* c) {
       mx(s_nt, Kp / kCholTile);
       mx(s_sums, (uint64_t)((x.d + 127) / 128) * ((K + 127) / 128));
     } else {
-      const uint64_t pairs = (uint64_t)jac_seats(x.d) / 2;
       mx(mx_dD, (uint64_t)(x.d * x.D));
       mx(mx_dd, (uint64_t)(x.d * x.d));
       mx(mx_gram, (uint64_t)pk_doubles(jac_blocks(x.d)));
       const int gs = gram_splits(x.d, x.D);
       if (gs > 1) mx(mx_gpart, (uint64_t)gs * (uint64_t)(x.d * x.d));
-      mx(mx_pairs, pairs);
+      mx(mx_groups, (uint64_t)jac_groups(x.d));
     }
   }
   WsLayout w;
@@ -192,10 +190,10 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_Utw = take(mx_dd * 4);
   w.off_gram = take(mx_gram * 8);
   w.off_gram2 = take(mx_gram * 8);
-  w.off_V = take(2 * mx_pairs * kJP * kJP * 4);    // two copies: round parity
-  w.off_V64 = take(2 * mx_pairs * kJP * kJP * 8);
+  w.off_V = take(2 * mx_groups * kJR * kJR * 4);    // two copies: round parity
+  w.off_V64 = take(2 * mx_groups * kJR * kJR * 8);
   w.off_gpart = take(mx_gpart * 8);
-  w.off_skip = take(2 * mx_pairs * 4);
+  w.off_skip = take(2 * mx_groups * 4);
   w.off_ctl = take(sizeof(JacCtl));
   w.off_sigw = take(mx_d * 4);
   w.off_perm = take(mx_d * 4);
@@ -217,10 +215,10 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rUtw = take(s_KK * 4);
   w.off_rY = take(s_KK * 4);
   w.off_rgram = take(r_gram * 8);
-  w.off_rV = take(2 * r_pairs * kJP * kJP * 4);
-  w.off_rV64 = take(2 * r_pairs * kJP * kJP * 8);
+  w.off_rV = take(2 * r_groups * kJR * kJR * 4);
+  w.off_rV64 = take(2 * r_groups * kJR * kJR * 8);
   w.off_rgpart = take(r_gpart * 8);
-  w.off_rskip = take(2 * r_pairs * 4);
+  w.off_rskip = take(2 * r_groups * 4);
   w.off_rctl = take(sizeof(JacCtl));
   w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
   w.off_rperm = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
@@ -446,7 +444,7 @@ glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t 
     ProfScope p(h, s, GLR_PROF_JAC_INIT);
     GLR_HIP(h, launch_jac_init(v, warm, s));
   }
-  const int rounds = jac_seats(v.d) - 1;
+  const int rounds = jac_rounds(v.d);
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     if (h->jac_sort == 1 || (h->jac_sort == 2 && sw == 0)) {
       GLR_HIP(h, launch_jac_sort(v, s));
@@ -486,7 +484,7 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   }
   MatView rr;
   GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
-  const int rounds = jac_seats(rr.d) - 1;
+  const int rounds = jac_rounds(rr.d);
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     GLR_HIP(h, jacobi_sweep(h, rr, rounds, GLR_PROF_RR_SOLVE, GLR_PROF_RR_UPDATE, s));
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
