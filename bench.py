@@ -45,14 +45,18 @@ def dims(shape):
 
 
 def jac_groups(d, jb=16):
-    """(groups per round, rounds per sweep) of the Jacobi tournament: seats
-    = the smallest power of 4 holding the 16-row blocks, groups of 4 blocks,
-    (seats - 1) / 3 rounds."""
+    """(blocks per group, groups per round, rounds per sweep) of the Jacobi
+    tournament: groups of four on 4^j seats when the 16-row blocks nearly fill
+    a power of 4 of at least 64 (S - 1) / 3 rounds), pairs otherwise (circle
+    method, S - 1 rounds)."""
     nb = (d + jb - 1) // jb
-    seats = 4
-    while seats < nb:
-        seats *= 4
-    return seats // 4, (seats - 1) // 3
+    s4 = 4
+    while s4 < nb:
+        s4 *= 4
+    if nb >= 64 and 4 * nb >= 3 * s4:
+        return 4, s4 // 4, (s4 - 1) // 3
+    seats = max(2, nb + (nb & 1))
+    return 2, seats // 2, seats - 1
 
 
 def uses_subspace(wl, d):
@@ -69,19 +73,21 @@ KERNEL_GROUPS = ("ef_mean", "select", "proj", "resid_opt", "jac_update", "jac_so
 
 def jacobi_work(kind, d):
     """Per-launch work of one Jacobi round on the fp64 Gram of d rows (16-row
-    blocks, 64-row groups): (bytes, fp32 MFMA flops, fp64 MFMA flops, fp64
-    ALU flops)."""
-    groups, _ = jac_groups(d)
+    blocks, groups of NG blocks = NR rows): (bytes, fp32 MFMA flops, fp64
+    MFMA flops, fp64 ALU flops)."""
+    ng, groups, _ = jac_groups(d)
+    nr = 16 * ng
     nb = (d + 15) // 16
     if kind == "update":
-        # A <- J^T A J on the packed upper blocks: read + write, two 64 x 64 x 64
+        # A <- J^T A J on the packed upper blocks: read + write, two NR x NR x NR
         # fp64 products per pair of groups
-        return 2.0 * nb * (nb + 1) / 2 * 256 * 8, 0.0, groups * (groups + 1) / 2 * 2 * 2.0 * 64 ** 3, 0.0
-    # solve: one cyclic sweep of 64 x 64 two-sided Jacobi per group (2016
-    # rotations, each updating two rows and two columns of G and two columns
-    # of V), in the same launch as the previous round's U^T <- J^T U^T (read
-    # + write the 64 rows of every group, one 64 x 64 x d fp32 product each)
-    return groups * 64.0 * d * 8, groups * 2.0 * 64 * 64 * d, 0.0, groups * 2016.0 * (6 * 64 * 3)
+        return 2.0 * nb * (nb + 1) / 2 * 256 * 8, 0.0, groups * (groups + 1) / 2 * 2 * 2.0 * nr ** 3, 0.0
+    # solve: one cyclic sweep of NR x NR two-sided Jacobi per group (NR (NR - 1)
+    # / 2 rotations, each updating two rows and two columns of G and two
+    # columns of V), in the same launch as the previous round's U^T <- J^T U^T
+    # (read + write the NR rows of every group, one NR x NR x d fp32 product)
+    rot = nr * (nr - 1) / 2
+    return groups * nr * d * 8.0, groups * 2.0 * nr * nr * d, 0.0, groups * rot * (6 * nr * 3)
 
 
 def group_work(wl, name):

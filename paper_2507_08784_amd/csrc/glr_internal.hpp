@@ -9,8 +9,6 @@
 namespace glr {
 
 constexpr int kJB = 16;   // rows per Jacobi block
-constexpr int kJG = 4;    // blocks per Jacobi group
-constexpr int kJR = kJG * kJB;   // rows per group
 
 // The fp64 Gram A = W W^T of a refresh is kept packed by 16 x 16 blocks:
 // block (a, b), a <= b, row-major, at pk_off(a, b, nb) doubles.
@@ -117,8 +115,10 @@ hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t
 // Jacobi on the fp64 Gram of the rows of W
 int jac_blocks(int64_t d);
 int jac_seats(int64_t d);
+int jac_group_blocks(int64_t d);
 int jac_groups(int64_t d);
 int jac_rounds(int64_t d);
+int64_t jac_vbuf(int64_t d);   // entries of one round's group rotations
 hipError_t launch_jac_reset(const MatView& v, hipStream_t s);
 hipError_t launch_jac_init(const MatView& v, bool warm, hipStream_t s);
 // one round = update(round) after solve(round); the rotation of U^T rows by

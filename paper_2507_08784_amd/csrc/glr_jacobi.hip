@@ -4,34 +4,54 @@
 //
 // A is formed once per refresh (fp64-accumulated products of the fp32 rows)
 // and kept packed by 16 x 16 blocks.  Rows are grouped in blocks of kJB; a
-// round splits the blocks into groups of four (kJR = 64 rows), and each group
-// is treated as a whole:
-//   solve  : one cyclic two-sided Jacobi sweep on the group's 64 x 64
+// round splits the blocks into groups of NG (two or four, NR = 16 NG rows),
+// and each group is treated as a whole:
+//   solve  : one cyclic two-sided Jacobi sweep on the group's NR x NR
 //            diagonal block of A in LDS (fp64) gives the rotation V
-//   update : A <- J^T A J with J = diag(V_group), block by block: the 64 x 64
+//   update : A <- J^T A J with J = diag(V_group), block by block: the NR x NR
 //            block (g, h) of two groups becomes V_g^T A_gh V_h (fp64 MFMA)
 //   apply  : rows of U^T <- V^T rows, in place, as u + (V - I)^T u
 //            (fp32 MFMA), in the same launch as the next round's solves
-// A sweep is (S - 1) / 3 rounds for S = 4^j seats (blocks and empty padding
-// blocks): every two blocks share a group in exactly one round, so a sweep
-// meets every pair of blocks once while A and U^T are streamed only once per
-// round.  The sweeps stop when every group solved in a sweep passes the
-// measure of the solve.  The singular values are sqrt(diag A), sorted
-// descending (ties keep the lower row first); U^T rows follow the sort.
+// A sweep meets every pair of blocks once: S - 1 rounds of pairs (circle
+// method on S seats), or (S - 1) / 3 rounds of groups of four for S = 4^j
+// seats, so that A and U^T are streamed a third as often; pairs serve small
+// d, where the rounds are bound by the latency of the solves, and block
+// counts far from a power of 4.  Padding seats hold empty blocks.  The
+// sweeps stop when every group solved in a sweep passes the measure of the
+// solve.  The singular values are sqrt(diag A), sorted descending (ties keep
+// the lower row first); U^T rows follow the sort.
 #include "glr_device.hpp"
 #include "glr_internal.hpp"
 
 namespace glr {
 
 int jac_blocks(int64_t d) { return (int)((d + kJB - 1) / kJB); }
-int jac_seats(int64_t d) {
-  const int nb = jac_blocks(d);
-  int s = kJG;
-  while (s < nb) s *= 4;
+static int pow4_at_least(int n) {
+  int s = 4;
+  while (s < n) s *= 4;
   return s;
 }
-int jac_groups(int64_t d) { return jac_seats(d) / kJG; }
-int jac_rounds(int64_t d) { return (jac_seats(d) - 1) / 3; }
+// Blocks per group: four when the 16-row blocks nearly fill a power of 4 of
+// at least 64 seats (the rounds then stream A and U^T a third as often as
+// pairs do), two otherwise (fewer seats wasted on padding, and for small d a
+// round is bound by the latency of its solves, which is shorter for pairs).
+int jac_group_blocks(int64_t d) {
+  const int nb = jac_blocks(d);
+  return (nb >= 64 && 4 * nb >= 3 * pow4_at_least(nb)) ? 4 : 2;
+}
+int jac_seats(int64_t d) {
+  const int nb = jac_blocks(d);
+  if (jac_group_blocks(d) == 4) return pow4_at_least(nb);
+  return nb + (nb & 1) < 2 ? 2 : nb + (nb & 1);
+}
+int jac_groups(int64_t d) { return jac_seats(d) / jac_group_blocks(d); }
+int jac_rounds(int64_t d) {
+  return jac_group_blocks(d) == 4 ? (jac_seats(d) - 1) / 3 : jac_seats(d) - 1;
+}
+int64_t jac_vbuf(int64_t d) {
+  const int64_t nr = (int64_t)jac_group_blocks(d) * kJB;
+  return (int64_t)jac_groups(d) * nr * nr;
+}
 
 // Block indices are vectors over F_2 (S = 2^k seats, k even), read as
 // vectors of k/2 digits over F_4 = {0, 1, w, w^2}, a digit being two bits
@@ -41,26 +61,40 @@ __device__ __forceinline__ uint32_t f4_times_w(uint32_t x) {
   const uint32_t h = (x >> 1) & 0x55555555u, l = x & 0x55555555u;
   return ((h ^ l) << 1) | h;
 }
-// Blocks of group g in round t.  The rounds are the (S - 1) / 3 lines
-// {0, v, w v, w^2 v} through the origin (v with leading digit 1): they cover
-// every non-zero vector exactly once.  The groups of a round are the cosets
-// x0 + line, so two blocks a, b share a group exactly in the round whose line
-// holds a ^ b.  Member m of a group is the block whose digit p (the leading
-// digit of v) equals m; x0 is g with a zero digit inserted at p.
-__device__ __forceinline__ void group_blocks(int t, int g, int (&blk)[kJG]) {
-  int p = 0, base = 0;
-  while (t >= base + (1 << (2 * p))) {
-    base += 1 << (2 * p);
-    ++p;
+// Blocks of group g in round t.
+// Groups of four: the rounds are the (S - 1) / 3 lines {0, v, w v, w^2 v}
+// through the origin (v with leading digit 1), which cover every non-zero
+// vector exactly once.  The groups of a round are the cosets x0 + line, so
+// two blocks a, b share a group exactly in the round whose line holds a ^ b.
+// Member m of a group is the block whose digit p (the leading digit of v)
+// equals m; x0 is g with a zero digit inserted at p.
+// Pairs: the circle method on the seats (seat S - 1 fixed, the others turn).
+template <int NG>
+__device__ __forceinline__ void group_blocks(int t, int g, int seats, int (&blk)[NG]) {
+  if constexpr (NG == 4) {
+    int p = 0, base = 0;
+    while (t >= base + (1 << (2 * p))) {
+      base += 1 << (2 * p);
+      ++p;
+    }
+    const uint32_t v = (1u << (2 * p)) | (uint32_t)(t - base);
+    const uint32_t v2 = f4_times_w(v), v3 = v ^ v2;
+    const uint32_t low = (1u << (2 * p)) - 1u;
+    const uint32_t x0 = (((uint32_t)g & ~low) << 2) | ((uint32_t)g & low);
+    blk[0] = (int)x0;
+    blk[1] = (int)(x0 ^ v);
+    blk[2] = (int)(x0 ^ v2);
+    blk[3] = (int)(x0 ^ v3);
+  } else {
+    const int last = seats - 1;
+    if (g == 0) {
+      blk[0] = t;
+      blk[1] = last;
+    } else {
+      blk[0] = (t + g) % last;
+      blk[1] = (t - g + last) % last;
+    }
   }
-  const uint32_t v = (1u << (2 * p)) | (uint32_t)(t - base);
-  const uint32_t v2 = f4_times_w(v), v3 = v ^ v2;
-  const uint32_t low = (1u << (2 * p)) - 1u;
-  const uint32_t x0 = (((uint32_t)g & ~low) << 2) | ((uint32_t)g & low);
-  blk[0] = (int)x0;
-  blk[1] = (int)(x0 ^ v);
-  blk[2] = (int)(x0 ^ v2);
-  blk[3] = (int)(x0 ^ v3);
 }
 
 // ---------------------------------------------------------------------------
@@ -181,11 +215,6 @@ __device__ __forceinline__ double pk_get(const double* __restrict__ Apk, int nb,
   return bx <= by ? Apk[pk_off(bx, by, nb) + lx * kJB + ly] : Apk[pk_off(by, bx, nb) + ly * kJB + lx];
 }
 
-// columns of U^T rotated by one workgroup: 512 for 256 threads; the
-// 1024-thread workgroups beside the solves take 1024, so that the solves and
-// all the rotation workgroups of a round are resident together
-constexpr int JAC_CHUNK = 512;
-constexpr int JAC_CHUNK_WIDE = 1024;
 
 // Rotation V of a group's Gram by one cyclic two-sided Jacobi sweep in LDS
 // (fp64).  Convergence measure of a pair of rows (p, q):
@@ -197,13 +226,14 @@ constexpr int JAC_CHUNK_WIDE = 1024;
 // f^2 = 2^-20 sigma_1^2 -- far below what the fp32 data resolves -- without
 // chasing orthogonality between tiny rows that fp32 rounding re-creates.
 //
-// A sweep of the 64 x 64 eigenproblem is 63 steps of 32 disjoint rotations
-// (circle method); when the rows inside each of the four blocks already meet
-// the measure, only the 48 steps between blocks are taken (three pairings of
-// the blocks, 16 steps each).  In a step, each thread owns one 2 x 2 block
-// rows {p_a, q_a} x columns {p_b, q_b} of G and of V, so that the update
-// G <- J^T G J, V <- V J is in place and private to the thread; the thread
-// owning (a, a) first computes rotation a from that diagonal block.
+// A sweep of the NR x NR eigenproblem (NR = 16 NG rows) is NR - 1 steps of
+// NR / 2 disjoint rotations (circle method); when the rows inside each block
+// already meet the measure, only the steps between blocks are taken (16 per
+// pairing of the blocks: one pairing for NG = 2, three for NG = 4).  In a
+// step, each of the NR^2 / 4 threads owns one 2 x 2 block rows {p_a, q_a} x
+// columns {p_b, q_b} of G and of V, so that the update G <- J^T G J,
+// V <- V J is in place and private to the thread; the thread owning (a, a)
+// first computes rotation a from that diagonal block.
 // Rotation J = [[c, s], [-s, c]] that diagonalises [[gpp, gpq], [gpq, gqq]]:
 // t = tan(theta) = sign(d h) |h| / (|d| + sqrt(d^2 + h^2)), d = gqq - gpp,
 // h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  d and h are first scaled by a
@@ -229,84 +259,100 @@ __device__ __forceinline__ void jac_rotation(double gpp, double gqq, double gpq,
   s = y * t;
 }
 
-// rotation j of step `step` of the circle method on 64 rows (p and q in
+template <int NG>
+struct JacShape {
+  static constexpr int NR = NG * kJB;        // rows of a group
+  static constexpr int NT = NR * NR / 4;     // solve threads, one 2 x 2 block each
+  static constexpr int NW = NT / 64;
+  static constexpr int CROSS = (NG == 2 ? 1 : 3) * kJB;   // steps between blocks
+};
+
+// rotation j of step `step` of the circle method on NR rows (p and q in
 // either order: the rotation diagonalises the 2 x 2 block either way)
+template <int NR>
 __device__ __forceinline__ void full_pair(int step, int j, int& p, int& q) {
-  constexpr int last = kJR - 1;
+  constexpr int last = NR - 1;
   if (j == 0) { p = step; q = last; }
   else { p = (step + j) % last; q = (step - j + last) % last; }
 }
 
-// rotation j of step `step` of the 48 steps between blocks: block pairings
-// (0,1)(2,3), (0,2)(1,3), (0,3)(1,2) in turn, each for the 16 steps that
-// pair row k of one block with row (k + step) mod 16 of the other
+// rotation j of step `step` of the steps between blocks: for NG = 4 the
+// block pairings (0,1)(2,3), (0,2)(1,3), (0,3)(1,2) in turn, for NG = 2 the
+// pairing (0,1); each for the 16 steps that pair row k of one block with row
+// (k + step) mod 16 of the other
+template <int NG>
 __device__ __forceinline__ void cross_pair(int step, int j, int& p, int& q) {
   const int rho = step >> 4, k = step & (kJB - 1), half = j >> 4, kk = j & (kJB - 1);
   int ma, mb;
-  if (rho == 0) { ma = half ? 2 : 0; mb = half ? 3 : 1; }
+  if (NG == 2 || rho == 0) { ma = half ? 2 : 0; mb = half ? 3 : 1; }
   else if (rho == 1) { ma = half ? 1 : 0; mb = half ? 3 : 2; }
   else { ma = half ? 1 : 0; mb = half ? 2 : 3; }
   p = kJB * ma + kk;
   q = kJB * mb + ((kk + k) & (kJB - 1));
 }
 
+template <int NG>
 __device__ __forceinline__ void step_pair(bool cross, int step, int j, int& p, int& q) {
-  if (cross) cross_pair(step, j, p, q);
-  else full_pair(step, j, p, q);
+  if (cross) cross_pair<NG>(step, j, p, q);
+  else full_pair<JacShape<NG>::NR>(step, j, p, q);
 }
 
-__device__ __forceinline__ bool group_empty(const int (&blk)[kJG], int nb) {
-  return blk[0] >= nb && blk[1] >= nb && blk[2] >= nb && blk[3] >= nb;
+template <int NG>
+__device__ __forceinline__ bool group_empty(const int (&blk)[NG], int nb) {
+  bool e = true;
+#pragma unroll
+  for (int m = 0; m < NG; ++m) e = e && blk[m] >= nb;
+  return e;
 }
-
-// A group solve runs 1024 threads (16 waves): thread (a, b) owns the 2 x 2
-// block {p_a, q_a} x {p_b, q_b} of G and V, a = t / 32, b = t % 32.  With
-// four waves per SIMD the LDS latency of one wave hides behind the others.
-constexpr int kSolveThreads = kJR * kJR / 4;
-constexpr int kSolveWaves = kSolveThreads / 64;
 
 // LDS of a group solve; the rotation of U^T reuses it for V - I (fp32)
+template <int NG>
 struct SolveLds {
-  double G[kJR][kJR + 1];
-  double V[kJR][kJR + 1];
-  double rc[kJR / 2], rs[kJR / 2];
-  double red[kSolveWaves], redw[kSolveWaves];
+  static constexpr int NR = JacShape<NG>::NR;
+  double G[NR][NR + 1];
+  double V[NR][NR + 1];
+  double rc[NR / 2], rs[NR / 2];
+  double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
 };
+template <int NG>
 union JacLds {
-  SolveLds s;
-  float Va[kJR][kJR + 1];
+  SolveLds<NG> s;
+  float Va[JacShape<NG>::NR][JacShape<NG>::NR + 1];
 };
 
+template <int NG>
 __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
-                                            int nb, float tol, int max_inner, double floor_rel2,
+                                            int seats, int nb, float tol, int max_inner, double floor_rel2,
                                             float* __restrict__ Vout, double* __restrict__ V64,
-                                            int* __restrict__ skip, int grp, SolveLds& L) {
-  int blk[kJG];
-  group_blocks(round, grp, blk);
+                                            int* __restrict__ skip, int grp, SolveLds<NG>& L) {
+  using SH = JacShape<NG>;
+  constexpr int NR = SH::NR, NT = SH::NT, NW = SH::NW;
+  int blk[NG];
+  group_blocks<NG>(round, grp, seats, blk);
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-  if (group_empty(blk, nb)) {
+  if (group_empty<NG>(blk, nb)) {
     if (tid == 0) skip[grp] = 1;
     return;
   }
-  double (*G)[kJR + 1] = L.G;
-  double (*V)[kJR + 1] = L.V;
+  double (*G)[NR + 1] = L.G;
+  double (*V)[NR + 1] = L.V;
   double* rc = L.rc;
   double* rs = L.rs;
   double* red = L.red;
   double* redw = L.redw;
-  constexpr int NE = kJR * kJR / kSolveThreads;
+  constexpr int NE = NR * NR / NT;
   const double rm_prev = __longlong_as_double((long long)ctl->rowmax2_bits);
-  // the group's diagonal 64 x 64 block of A
+  // the group's diagonal NR x NR block of A
   double g[NE];
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
-    const int e = tid + kSolveThreads * k, x = e / kJR, y = e % kJR;
+    const int e = tid + NT * k, x = e / NR, y = e % NR;
     g[k] = pk_get(Apk, nb, blk[x / kJB], blk[y / kJB], x % kJB, y % kJB);
   }
   double dmax = 0.0;
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
-    const int e = tid + kSolveThreads * k, x = e / kJR, y = e % kJR;
+    const int e = tid + NT * k, x = e / NR, y = e % NR;
     G[x][y] = g[k];
     V[x][y] = x == y ? 1.0 : 0.0;
     if (x == y) dmax = fmax(dmax, g[k]);
@@ -317,7 +363,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   __syncthreads();
   dmax = 0.0;
 #pragma unroll
-  for (int i = 0; i < kSolveWaves; ++i) dmax = fmax(dmax, red[i]);
+  for (int i = 0; i < NW; ++i) dmax = fmax(dmax, red[i]);
   __syncthreads();
   if (tid == 0 && dmax > 0.0)
     atomicMax((unsigned long long*)&ctl->rowmax2_bits, (unsigned long long)__double_as_longlong(dmax));
@@ -326,7 +372,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   double m2 = 0.0, mw2 = 0.0;   // all pairs / pairs inside one block
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
-    const int e = tid + kSolveThreads * k, x = e / kJR, y = e % kJR;
+    const int e = tid + NT * k, x = e / NR, y = e % NR;
     if (x < y) {
       const double gxx = G[x][x], gyy = G[y][y];
       const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
@@ -347,7 +393,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   m2 = 0.0;
   mw2 = 0.0;
 #pragma unroll
-  for (int i = 0; i < kSolveWaves; ++i) {
+  for (int i = 0; i < NW; ++i) {
     m2 = fmax(m2, red[i]);
     mw2 = fmax(mw2, redw[i]);
   }
@@ -362,24 +408,24 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   // the 16 lanes of an LDS access share the row pair a and take 16
   // consecutive column pairs b, whose rows are (up to the wrap of the
   // circle) distinct modulo 16: few bank conflicts
-  const int a = tid >> 5, bb = tid & 31;
-  const int steps = cross ? 3 * kJB : kJR - 1;
+  const int a = tid / (NR / 2), bb = tid % (NR / 2);
+  const int steps = cross ? SH::CROSS : NR - 1;
   for (int sweep = 0; sweep < max_inner; ++sweep) {
     int pa = 0, qa = 0, pb = 0, qb = 0;
     for (int st = 0; st < steps; ++st) {
       // the pairs move by one place per step: p + 1, q + 1 on the circle of
-      // 63 (q = 63 stays), or q + 1 within its block between blocks
+      // NR - 1 (q = NR - 1 stays), or q + 1 within its block between blocks
       if (st == 0 || (cross && (st & (kJB - 1)) == 0)) {
-        step_pair(cross, st, a, pa, qa);
-        step_pair(cross, st, bb, pb, qb);
+        step_pair<NG>(cross, st, a, pa, qa);
+        step_pair<NG>(cross, st, bb, pb, qb);
       } else if (cross) {
         qa = (qa & ~(kJB - 1)) | ((qa + 1) & (kJB - 1));
         qb = (qb & ~(kJB - 1)) | ((qb + 1) & (kJB - 1));
       } else {
-        pa = pa == kJR - 2 ? 0 : pa + 1;
-        pb = pb == kJR - 2 ? 0 : pb + 1;
-        qa = qa == kJR - 1 ? qa : (qa == kJR - 2 ? 0 : qa + 1);
-        qb = qb == kJR - 1 ? qb : (qb == kJR - 2 ? 0 : qb + 1);
+        pa = pa == NR - 2 ? 0 : pa + 1;
+        pb = pb == NR - 2 ? 0 : pb + 1;
+        qa = qa == NR - 1 ? qa : (qa == NR - 2 ? 0 : qa + 1);
+        qb = qb == NR - 1 ? qb : (qb == NR - 2 ? 0 : qb + 1);
       }
       if (a == bb) {
         double c, sn;
@@ -406,89 +452,107 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
       __syncthreads();
     }
   }
-  float* vo = Vout + (int64_t)grp * kJR * kJR;
-  double* vd = V64 + (int64_t)grp * kJR * kJR;
+  float* vo = Vout + (int64_t)grp * NR * NR;
+  double* vd = V64 + (int64_t)grp * NR * NR;
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
-    const int e = tid + kSolveThreads * k;
-    vo[e] = (float)V[e / kJR][e % kJR];
-    vd[e] = V[e / kJR][e % kJR];
+    const int e = tid + NT * k;
+    vo[e] = (float)V[e / NR][e % NR];
+    vd[e] = V[e / NR][e % NR];
   }
   if (tid == 0) skip[grp] = 0;
 }
 
+// columns of U^T rotated by one workgroup of the given width: 512 for 256
+// threads; the 1024-thread workgroups beside the solves of four-block groups
+// take 1024, so that the solves and all the rotation workgroups of a round
+// are resident together
+constexpr int JAC_CHUNK = 512;
+constexpr int JAC_CHUNK_WIDE = 1024;
+
 // rows of the group in U^T <- V^T rows on this block's chunk, computed as
-// w + (V - I)^T w (fp32 MFMA, two 32-row output tiles, K = 64).  The k index
-// is permuted so that the B operand held by each lane is exactly the set of
-// rows that lane outputs: k slot kk < 16 of a lane is physical row
-// mfma32_row(kk, lane) (output tile 0, register kk) and slot 16 + kk is
-// 32 + mfma32_row(kk, lane) (output tile 1, register kk).
+// w + (V - I)^T w (fp32 MFMA, NR / 32 output tiles of 32 rows, K = NR).  The
+// k index is permuted so that the B operand held by each lane is exactly the
+// set of rows that lane outputs: k slot 16 h + kk of a lane is physical row
+// 32 h + mfma32_row(kk, lane), which is register kk of output tile h.
+template <int NG>
 __device__ __forceinline__ void apply_chunk(float* __restrict__ Utw, int64_t d, const float* __restrict__ Vin,
-                                            const int* __restrict__ skip, int round, int nb, int grp,
-                                            int chunk, int width, float (*Va)[kJR + 1]) {
+                                            const int* __restrict__ skip, int round, int seats, int nb,
+                                            int grp, int chunk, int width,
+                                            float (*Va)[JacShape<NG>::NR + 1]) {
+  constexpr int NR = JacShape<NG>::NR;
   if (skip[grp]) return;
-  int blk[kJG];
-  group_blocks(round, grp, blk);
-  if (group_empty(blk, nb)) return;
+  int blk[NG];
+  group_blocks<NG>(round, grp, seats, blk);
+  if (group_empty<NG>(blk, nb)) return;
   const int lane = lane_id(), w = wave_id();
   const int l32 = lane & 31, lh4 = 4 * (lane >> 5);
-  const float* V = Vin + (int64_t)grp * kJR * kJR;
-  constexpr int KS = kJR / 2;   // k slots of the two-row MFMA steps
-  for (int e = threadIdx.x; e < kJR * kJR; e += blockDim.x) {
-    const int i = e / kJR, j = e % kJR;
+  const float* V = Vin + (int64_t)grp * NR * NR;
+  constexpr int KS = NR / 2;   // k slots of the two-row MFMA steps
+  for (int e = threadIdx.x; e < NR * NR; e += blockDim.x) {
+    const int i = e / NR, j = e % NR;
     Va[i][j] = V[e] - (i == j ? 1.0f : 0.0f);
   }
   __syncthreads();
   // slot kk is row blk[m] * 16 + r of U^T with m = slot_block(kk) and
   // r = slot_row(kk) + 4 (lane / 32)
-  auto slot_block = [](int kk) { return (kk < 16 ? 0 : 2) + ((kk & 15) >= 8 ? 1 : 0); };
+  auto slot_block = [](int kk) { return 2 * (kk >> 4) + ((kk & 15) >= 8 ? 1 : 0); };
   auto slot_row = [](int kk) { return 8 * (((kk & 15) >> 2) & 1) + (kk & 3); };
-  int64_t first[kJG];   // row index of r = 4 (lane / 32) in each member block, -1 if padding
+  // d <= 8192: element offsets of U^T fit 32 bits, so every access is the
+  // uniform base plus a 32-bit lane offset
+  const int dd = (int)d;
+  int first[NG];   // row index of r = 4 (lane / 32) in each member block, -1 if padding
 #pragma unroll
-  for (int m = 0; m < kJG; ++m) first[m] = blk[m] < nb ? (int64_t)blk[m] * kJB + lh4 : -1;
-  const int64_t c0 = (int64_t)chunk * width;
+  for (int m = 0; m < NG; ++m) first[m] = blk[m] < nb ? blk[m] * kJB + lh4 : -1;
+  auto at = [&](int row, int col) -> float* {
+    return reinterpret_cast<float*>(reinterpret_cast<char*>(Utw) + ((uint32_t)(row * dd + col) << 2));
+  };
+  const int c0 = chunk * width;
   const int span = 32 * (int)(blockDim.x >> 6);   // columns per pass, 32 per wave
   for (int it = 0; it < width; it += span) {
-    const int64_t cb = c0 + it + w * 32;
-    if (cb >= d) break;
-    const int64_t cc = cb + l32;
-    const bool cok = cc < d;
+    const int cb = c0 + it + w * 32;
+    if (cb >= dd) break;
+    const int cc = cb + l32;
+    const bool cok = cc < dd;
     float b[KS];
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      const int64_t f = first[slot_block(kk)], row = f + slot_row(kk);
-      b[kk] = (cok && f >= 0 && row < d) ? Utw[row * d + cc] : 0.f;
+      const int f = first[slot_block(kk)], row = f + slot_row(kk);
+      b[kk] = (cok && f >= 0 && row < dd) ? *at(row, cc) : 0.f;
     }
     // output tile h: rows 32 h + mfma32_row(v, lane), held by slot 16 h + v
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < NR / 32; ++h) {
       f32x16 acc;
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[v] = 0.f;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        const int pr = (kk < 16 ? 0 : 32) + mfma32_row(kk & 15, lane);
+        const int pr = 32 * (kk >> 4) + mfma32_row(kk & 15, lane);
         acc = mfma32(Va[pr][32 * h + l32], b[kk], acc);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int kk = 16 * h + v;
-        const int64_t f = first[slot_block(kk)], row = f + slot_row(kk);
-        if (cok && f >= 0 && row < d) Utw[row * d + cc] = b[kk] + acc[v];
+        const int f = first[slot_block(kk)], row = f + slot_row(kk);
+        if (cok && f >= 0 && row < dd) *at(row, cc) = b[kk] + acc[v];
       }
     }
   }
 }
 
-// A <- J^T A J: the 64 x 64 block of rows of group g and columns of group h
+// A <- J^T A J: the NR x NR block of rows of group g and columns of group h
 // (g <= h) becomes V_g^T A_gh V_h (fp64 MFMA 16x16x4; wave w computes the
-// 32 x 32 quadrant (w / 2, w % 2) of each product).  The 16 x 16 blocks of A
-// are read and written whole (coalesced) through one LDS tile; blocks below
-// the diagonal are not stored, so each stored block is written by exactly
-// one workgroup.  A group whose V is the identity skips its product.
+// (NR / 2) x (NR / 2) quadrant (w / 2, w % 2) of each product).  The 16 x 16
+// blocks of A are read and written whole (coalesced) through one LDS tile;
+// blocks below the diagonal are not stored, so each stored block is written
+// by exactly one workgroup.  A group whose V is the identity skips its
+// product.
+template <int NG>
 __global__ void __launch_bounds__(256)
 k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int* __restrict__ skip,
-             const JacCtl* __restrict__ ctl, int round, int nb, int groups) {
+             const JacCtl* __restrict__ ctl, int round, int seats, int nb, int groups) {
+  constexpr int NR = JacShape<NG>::NR, TW = NR / 32;   // 16 x 16 tiles per quadrant side
   if (ctl->converged) return;
   int g = 0, rem = blockIdx.x;
   while (rem >= groups - g) {
@@ -498,93 +562,89 @@ k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int
   const int h = g + rem;
   const bool sg = skip[g] != 0, sh = skip[h] != 0;
   if (sg && sh) return;
-  int bg[kJG], bh[kJG];
-  group_blocks(round, g, bg);
-  group_blocks(round, h, bh);
-  __shared__ double S[kJR][kJR + 1];
+  int bg[NG], bh[NG];
+  group_blocks<NG>(round, g, seats, bg);
+  group_blocks<NG>(round, h, seats, bh);
+  __shared__ double S[NR][NR + 1];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const int er = tid / kJB, ec = tid % kJB;
-  const int R0 = (w >> 1) * 32, C0 = (w & 1) * 32, li = lane & 15, lk = lane >> 4;
-  double sv[kJG * kJG];
+  const int R0 = (w >> 1) * (NR / 2), C0 = (w & 1) * (NR / 2), li = lane & 15, lk = lane >> 4;
+  double sv[NG * NG];
 #pragma unroll
-  for (int mb = 0; mb < kJG * kJG; ++mb) {
-    const int bx = bg[mb >> 2], by = bh[mb & 3];
+  for (int mb = 0; mb < NG * NG; ++mb) {
+    const int bx = bg[mb / NG], by = bh[mb % NG];
     sv[mb] = (bx < nb && by < nb) ? Apk[(bx <= by ? pk_off(bx, by, nb) : pk_off(by, bx, nb)) + tid] : 0.0;
   }
   // B operand of T = A_gh V_h, fetched while the blocks land in LDS
-  double vb[kJR / 4][2];
+  double vb[NR / 4][TW];
   if (!sh) {
-    const double* vh = V64 + (int64_t)h * kJR * kJR;
+    const double* vh = V64 + (int64_t)h * NR * NR;
 #pragma unroll
-    for (int k = 0; k < kJR / 4; ++k) {
-      const int kr = 4 * k + lk;
-      vb[k][0] = vh[kr * kJR + C0 + li];
-      vb[k][1] = vh[kr * kJR + C0 + 16 + li];
-    }
+    for (int k = 0; k < NR / 4; ++k)
+#pragma unroll
+      for (int j = 0; j < TW; ++j) vb[k][j] = vh[(4 * k + lk) * NR + C0 + 16 * j + li];
   }
 #pragma unroll
-  for (int mb = 0; mb < kJG * kJG; ++mb) {
-    const int mx = mb >> 2, my = mb & 3;
+  for (int mb = 0; mb < NG * NG; ++mb) {
+    const int mx = mb / NG, my = mb % NG;
     if (bg[mx] <= bh[my]) S[kJB * mx + er][kJB * my + ec] = sv[mb];
     else S[kJB * mx + ec][kJB * my + er] = sv[mb];
   }
   __syncthreads();
-  f64x4 acc[2][2];
+  f64x4 acc[TW][TW];
   if (!sh) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TW; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+      for (int j = 0; j < TW; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int k = 0; k < kJR / 4; ++k) {
-      const double x0 = S[R0 + li][4 * k + lk], x1 = S[R0 + 16 + li][4 * k + lk];
-      acc[0][0] = mfma64(x0, vb[k][0], acc[0][0]);
-      acc[0][1] = mfma64(x0, vb[k][1], acc[0][1]);
-      acc[1][0] = mfma64(x1, vb[k][0], acc[1][0]);
-      acc[1][1] = mfma64(x1, vb[k][1], acc[1][1]);
-    }
+    for (int k = 0; k < NR / 4; ++k)
+#pragma unroll
+      for (int i = 0; i < TW; ++i) {
+        const double x = S[R0 + 16 * i + li][4 * k + lk];
+#pragma unroll
+        for (int j = 0; j < TW; ++j) acc[i][j] = mfma64(x, vb[k][j], acc[i][j]);
+      }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TW; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < TW; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) S[R0 + 16 * i + 4 * v + lk][C0 + 16 * j + li] = acc[i][j][v];
     __syncthreads();
   }
   if (!sg) {
-    const double* vg = V64 + (int64_t)g * kJR * kJR;
-    double va[kJR / 4][2];
+    const double* vg = V64 + (int64_t)g * NR * NR;
+    double va[NR / 4][TW];
 #pragma unroll
-    for (int k = 0; k < kJR / 4; ++k) {
-      const int kr = 4 * k + lk;
-      va[k][0] = vg[kr * kJR + R0 + li];
-      va[k][1] = vg[kr * kJR + R0 + 16 + li];
-    }
+    for (int k = 0; k < NR / 4; ++k)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TW; ++i) va[k][i] = vg[(4 * k + lk) * NR + R0 + 16 * i + li];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+    for (int i = 0; i < TW; ++i)
 #pragma unroll
-    for (int k = 0; k < kJR / 4; ++k) {
-      const double y0 = S[4 * k + lk][C0 + li], y1 = S[4 * k + lk][C0 + 16 + li];
-      acc[0][0] = mfma64(va[k][0], y0, acc[0][0]);
-      acc[0][1] = mfma64(va[k][0], y1, acc[0][1]);
-      acc[1][0] = mfma64(va[k][1], y0, acc[1][0]);
-      acc[1][1] = mfma64(va[k][1], y1, acc[1][1]);
-    }
+      for (int j = 0; j < TW; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < NR / 4; ++k)
+#pragma unroll
+      for (int j = 0; j < TW; ++j) {
+        const double y = S[4 * k + lk][C0 + 16 * j + li];
+#pragma unroll
+        for (int i = 0; i < TW; ++i) acc[i][j] = mfma64(va[k][i], y, acc[i][j]);
+      }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TW; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < TW; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) S[R0 + 16 * i + 4 * v + lk][C0 + 16 * j + li] = acc[i][j][v];
     __syncthreads();
   }
 #pragma unroll
-  for (int mb = 0; mb < kJG * kJG; ++mb) {
-    const int mx = mb >> 2, my = mb & 3;
+  for (int mb = 0; mb < NG * NG; ++mb) {
+    const int mx = mb / NG, my = mb % NG;
     const int bx = bg[mx], by = bh[my];
     if (bx >= nb || by >= nb) continue;
     if (bx <= by) Apk[pk_off(bx, by, nb) + tid] = S[kJB * mx + er][kJB * my + ec];
@@ -593,41 +653,45 @@ k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int
 }
 
 // the group solves of one round
-__global__ void __launch_bounds__(kSolveThreads)
-k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int nb, float tol,
+template <int NG>
+__global__ void __launch_bounds__(JacShape<NG>::NT)
+k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb, float tol,
             int max_inner, double floor_rel2, float* __restrict__ Vout, double* __restrict__ V64,
             int* __restrict__ skip) {
   if (ctl->converged) return;
-  __shared__ SolveLds lds;
-  solve_group(Apk, ctl, round, nb, tol, max_inner, floor_rel2, Vout, V64, skip, blockIdx.x, lds);
+  __shared__ SolveLds<NG> lds;
+  solve_group<NG>(Apk, ctl, round, seats, nb, tol, max_inner, floor_rel2, Vout, V64, skip, blockIdx.x, lds);
 }
 
 // the group solves of round `round` (workgroups [0, groups)) together with
 // the rotation of U^T rows by the previous round's V (the rest): the rotation
 // does not depend on the new solves, and the solves leave most of the chip idle
-__global__ void __launch_bounds__(kSolveThreads)
-k_jac_solve_apply(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int nb, float tol,
-                  int max_inner, double floor_rel2, float* __restrict__ Vout, double* __restrict__ V64,
-                  int* __restrict__ skip, float* __restrict__ Utw, int64_t d, const float* __restrict__ Vprev,
-                  const int* __restrict__ skip_prev, int groups, int chunks) {
+template <int NG>
+__global__ void __launch_bounds__(JacShape<NG>::NT)
+k_jac_solve_apply(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round, int seats, int nb,
+                  float tol, int max_inner, double floor_rel2, float* __restrict__ Vout,
+                  double* __restrict__ V64, int* __restrict__ skip, float* __restrict__ Utw, int64_t d,
+                  const float* __restrict__ Vprev, const int* __restrict__ skip_prev, int groups, int chunks,
+                  int width) {
   if (ctl->converged) return;
-  __shared__ JacLds lds;
+  __shared__ JacLds<NG> lds;
   const int b = blockIdx.x;
   if (b < groups) {
-    solve_group(Apk, ctl, round, nb, tol, max_inner, floor_rel2, Vout, V64, skip, b, lds.s);
+    solve_group<NG>(Apk, ctl, round, seats, nb, tol, max_inner, floor_rel2, Vout, V64, skip, b, lds.s);
   } else {
     const int idx = b - groups;
-    apply_chunk(Utw, d, Vprev, skip_prev, round - 1, nb, idx / chunks, idx % chunks, JAC_CHUNK_WIDE, lds.Va);
+    apply_chunk<NG>(Utw, d, Vprev, skip_prev, round - 1, seats, nb, idx / chunks, idx % chunks, width, lds.Va);
   }
 }
 
 // U^T rows of the last round of a sweep
+template <int NG>
 __global__ void __launch_bounds__(256)
 k_jac_apply(float* __restrict__ Utw, int64_t d, const float* __restrict__ V32, const int* __restrict__ skip,
-            const JacCtl* __restrict__ ctl, int round, int nb, int chunks) {
+            const JacCtl* __restrict__ ctl, int round, int seats, int nb, int chunks) {
   if (ctl->converged) return;
-  __shared__ float Va[kJR][kJR + 1];
-  apply_chunk(Utw, d, V32, skip, round, nb, blockIdx.x / chunks, blockIdx.x % chunks, JAC_CHUNK, Va);
+  __shared__ float Va[JacShape<NG>::NR][JacShape<NG>::NR + 1];
+  apply_chunk<NG>(Utw, d, V32, skip, round, seats, nb, blockIdx.x / chunks, blockIdx.x % chunks, JAC_CHUNK, Va);
 }
 
 // per-round buffers alternate between two copies (round parity), so that a
@@ -638,45 +702,66 @@ struct RoundBufs {
   int* skip;
 };
 static RoundBufs round_bufs(const MatView& v, int round) {
-  const int64_t groups = jac_groups(v.d), par = round & 1;
-  return {v.Vrot + par * groups * kJR * kJR, v.V64 + par * groups * kJR * kJR, v.skip + par * groups};
+  const int64_t vb = jac_vbuf(v.d), groups = jac_groups(v.d), par = round & 1;
+  return {v.Vrot + par * vb, v.V64 + par * vb, v.skip + par * groups};
 }
 
-hipError_t launch_jac_update(const MatView& v, int round, hipStream_t s) {
-  const int nb = jac_blocks(v.d), groups = jac_groups(v.d);
+template <int NG>
+static hipError_t update_ng(const MatView& v, int round, hipStream_t s) {
+  const int nb = jac_blocks(v.d), groups = jac_groups(v.d), seats = jac_seats(v.d);
   const RoundBufs rb = round_bufs(v, round);
-  hipLaunchKernelGGL(k_jac_update, dim3((unsigned)(groups * (groups + 1) / 2)), dim3(256), 0, s, v.Apk, rb.V64,
-                     rb.skip, v.ctl, round, nb, groups);
+  hipLaunchKernelGGL(k_jac_update<NG>, dim3((unsigned)(groups * (groups + 1) / 2)), dim3(256), 0, s, v.Apk,
+                     rb.V64, rb.skip, v.ctl, round, seats, nb, groups);
   return hipGetLastError();
 }
+hipError_t launch_jac_update(const MatView& v, int round, hipStream_t s) {
+  return jac_group_blocks(v.d) == 4 ? update_ng<4>(v, round, s) : update_ng<2>(v, round, s);
+}
 
+template <int NG>
+static hipError_t solve_apply_ng(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                                 hipStream_t s) {
+  const int nb = jac_blocks(v.d), groups = jac_groups(v.d), seats = jac_seats(v.d);
+  const int width = NG == 4 ? JAC_CHUNK_WIDE : JAC_CHUNK;
+  const int chunks = (int)((v.d + width - 1) / width);
+  const RoundBufs rb = round_bufs(v, round), pb = round_bufs(v, round - 1);
+  hipLaunchKernelGGL(k_jac_solve_apply<NG>, dim3((unsigned)(groups + groups * chunks)), dim3(JacShape<NG>::NT),
+                     0, s, v.Apk, v.ctl, round, seats, nb, tol, max_inner, floor_rel2, rb.V32, rb.V64, rb.skip,
+                     v.Utw, v.d, pb.V32, pb.skip, groups, chunks, width);
+  return hipGetLastError();
+}
 hipError_t launch_jac_solve_apply(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                                   hipStream_t s) {
-  const int nb = jac_blocks(v.d), groups = jac_groups(v.d);
-  const int chunks = (int)((v.d + JAC_CHUNK_WIDE - 1) / JAC_CHUNK_WIDE);
-  const RoundBufs rb = round_bufs(v, round), pb = round_bufs(v, round - 1);
-  hipLaunchKernelGGL(k_jac_solve_apply, dim3((unsigned)(groups + groups * chunks)), dim3(kSolveThreads), 0, s, v.Apk,
-                     v.ctl, round, nb, tol, max_inner, floor_rel2, rb.V32, rb.V64, rb.skip, v.Utw, v.d, pb.V32,
-                     pb.skip, groups, chunks);
-  return hipGetLastError();
+  return jac_group_blocks(v.d) == 4 ? solve_apply_ng<4>(v, round, tol, max_inner, floor_rel2, s)
+                                    : solve_apply_ng<2>(v, round, tol, max_inner, floor_rel2, s);
 }
 
-hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s) {
-  const int nb = jac_blocks(v.d), groups = jac_groups(v.d);
+template <int NG>
+static hipError_t apply_ng(const MatView& v, int round, hipStream_t s) {
+  const int nb = jac_blocks(v.d), groups = jac_groups(v.d), seats = jac_seats(v.d);
   const int chunks = (int)((v.d + JAC_CHUNK - 1) / JAC_CHUNK);
   const RoundBufs rb = round_bufs(v, round);
-  hipLaunchKernelGGL(k_jac_apply, dim3((unsigned)(groups * chunks)), dim3(256), 0, s, v.Utw, v.d, rb.V32,
-                     rb.skip, v.ctl, round, nb, chunks);
+  hipLaunchKernelGGL(k_jac_apply<NG>, dim3((unsigned)(groups * chunks)), dim3(256), 0, s, v.Utw, v.d, rb.V32,
+                     rb.skip, v.ctl, round, seats, nb, chunks);
   return hipGetLastError();
 }
+hipError_t launch_jac_apply(const MatView& v, int round, hipStream_t s) {
+  return jac_group_blocks(v.d) == 4 ? apply_ng<4>(v, round, s) : apply_ng<2>(v, round, s);
+}
 
+template <int NG>
+static hipError_t solve_ng(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
+                           hipStream_t s) {
+  const int nb = jac_blocks(v.d), groups = jac_groups(v.d), seats = jac_seats(v.d);
+  const RoundBufs rb = round_bufs(v, round);
+  hipLaunchKernelGGL(k_jac_solve<NG>, dim3(groups), dim3(JacShape<NG>::NT), 0, s, v.Apk, v.ctl, round, seats, nb,
+                     tol, max_inner, floor_rel2, rb.V32, rb.V64, rb.skip);
+  return hipGetLastError();
+}
 hipError_t launch_jac_solve(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                             hipStream_t s) {
-  const int nb = jac_blocks(v.d), groups = jac_groups(v.d);
-  const RoundBufs rb = round_bufs(v, round);
-  hipLaunchKernelGGL(k_jac_solve, dim3(groups), dim3(kSolveThreads), 0, s, v.Apk, v.ctl, round, nb, tol, max_inner,
-                     floor_rel2, rb.V32, rb.V64, rb.skip);
-  return hipGetLastError();
+  return jac_group_blocks(v.d) == 4 ? solve_ng<4>(v, round, tol, max_inner, floor_rel2, s)
+                                    : solve_ng<2>(v, round, tol, max_inner, floor_rel2, s);
 }
 
 __global__ void k_jac_check(JacCtl* ctl, float tol) {

@@ -140,9 +140,9 @@ uint64_t state_bytes_of(const glr_config* c) {
 }
 
 WsLayout ws_layout(const glr_config* c) {
-  uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_groups = 0, mx_d = 0;
+  uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_groups = 0, mx_vbuf = 0, mx_d = 0;
   uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
-  uint64_t r_gram = 0, r_groups = 0, r_gpart = 0, mx_gpart = 0;
+  uint64_t r_gram = 0, r_groups = 0, r_vbuf = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
   for (int i = 0; i < c->num_mats; ++i) {
     const Dims x = dims_of(c, i);
@@ -159,6 +159,7 @@ WsLayout ws_layout(const glr_config* c) {
       mx(s_KD, K * (uint64_t)x.D);
       mx(s_part, (uint64_t)sub_part_floats(Ki, x.d, x.D));
       mx(r_groups, (uint64_t)jac_groups(Ki));
+      mx(r_vbuf, (uint64_t)jac_vbuf(Ki));
       mx(r_gram, (uint64_t)pk_doubles(jac_blocks(Ki)));
       const int rs = gram_splits(Ki, x.D);
       if (rs > 1) mx(r_gpart, (uint64_t)rs * K * K);
@@ -173,6 +174,7 @@ WsLayout ws_layout(const glr_config* c) {
       const int gs = gram_splits(x.d, x.D);
       if (gs > 1) mx(mx_gpart, (uint64_t)gs * (uint64_t)(x.d * x.d));
       mx(mx_groups, (uint64_t)jac_groups(x.d));
+      mx(mx_vbuf, (uint64_t)jac_vbuf(x.d));
     }
   }
   WsLayout w;
@@ -190,8 +192,8 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_Utw = take(mx_dd * 4);
   w.off_gram = take(mx_gram * 8);
   w.off_gram2 = take(mx_gram * 8);
-  w.off_V = take(2 * mx_groups * kJR * kJR * 4);    // two copies: round parity
-  w.off_V64 = take(2 * mx_groups * kJR * kJR * 8);
+  w.off_V = take(2 * mx_vbuf * 4);    // two copies: round parity
+  w.off_V64 = take(2 * mx_vbuf * 8);
   w.off_gpart = take(mx_gpart * 8);
   w.off_skip = take(2 * mx_groups * 4);
   w.off_ctl = take(sizeof(JacCtl));
@@ -215,8 +217,8 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rUtw = take(s_KK * 4);
   w.off_rY = take(s_KK * 4);
   w.off_rgram = take(r_gram * 8);
-  w.off_rV = take(2 * r_groups * kJR * kJR * 4);
-  w.off_rV64 = take(2 * r_groups * kJR * kJR * 8);
+  w.off_rV = take(2 * r_vbuf * 4);
+  w.off_rV64 = take(2 * r_vbuf * 8);
   w.off_rgpart = take(r_gpart * 8);
   w.off_rskip = take(2 * r_groups * 4);
   w.off_rctl = take(sizeof(JacCtl));
