@@ -84,7 +84,8 @@ typedef enum { GLR_SELECT_APPROX = 0, GLR_SELECT_EXACT = 1 } glr_select;
 #define GLR_COLD_START   0x2u  /* start every refresh from U = I instead of the previous U */
 
 typedef struct {
-  int64_t m, n;                /* layer matrix shape, caller's row-major layout */
+  int64_t m, n;                /* layer matrix shape, caller's row-major layout;
+                                  m n < 2^30 and min(m, n) <= 8192 (GLR_ERR_SHAPE) */
 } glr_shape;
 
 typedef struct {

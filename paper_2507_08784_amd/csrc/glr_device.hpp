@@ -20,6 +20,22 @@ __device__ __forceinline__ float4 load_nt4(const float* p) {
   return make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// Raw buffer access to one fp32 array of at most 2^32 - 1 bytes: a uniform
+// 128-bit descriptor (base, size; no stride) plus a 32-bit byte offset per
+// lane.  Offsets at or beyond the size read 0 and drop the store, so a lane
+// outside the array passes kBufNone.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+constexpr uint32_t kBufNone = 0xFFFFFFFFu;
+__device__ __forceinline__ BufRsrc buf_rsrc(const float* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float buf_ld(BufRsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ void buf_st(BufRsrc r, uint32_t off, float x) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), r, (int)off, 0, 0);
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 

@@ -95,6 +95,8 @@ glr_status check_config(const glr_config* c, std::string* why) {
     const int64_t m = c->shapes[i].m, n = c->shapes[i].n;
     if (m < 1 || n < 1) return bad(GLR_ERR_SHAPE, fmt("matrix %d: shape %lldx%lld must be positive", i, (long long)m, (long long)n));
     if (m > kMaxDim || n > kMaxDim) return bad(GLR_ERR_SHAPE, fmt("matrix %d: dimension above 2^30", i));
+    if (m * n >= ((int64_t)1 << 30))   // buffer addressing of one matrix: below 4 GiB
+      return bad(GLR_ERR_SHAPE, fmt("matrix %d: m*n = %lld reaches 2^30", i, (long long)(m * n)));
     const Dims x = dims_of(c, i);
     if (x.d > kMaxSortDim)
       return bad(GLR_ERR_SHAPE, fmt("matrix %d: min(m, n) = %lld exceeds %lld", i, (long long)x.d, (long long)kMaxSortDim));

@@ -364,13 +364,15 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// S5 + S7 + S8 fused, one pass over a 128 x 64 tile of the m x n layout:
+// S5 + S7 + S8 fused, one pass over a ROWS x 64 tile of the m x n layout:
 //   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
-//   E^(i) <- G^(i) + E^(i) - C^(i);  Ebar = (1/N) sum_i E^(i)
-//   Ghat  = (1/N) sum_i C^(i)  (= P Rbar);  optimizer on X with Ghat.
-// The product is computed transposed (MFMA rows = tile columns) so that each
-// lane holds 4 consecutive columns of a row: G, E, X and the optimizer state
-// move as 16-byte vectors.  P (gathered rows of U^T) and Q^(i) are staged
+//   E^(i) <- (G^(i) - C^(i)) + E^(i);  Ebar = (1/N) sum_i E^(i)
+//   Ghat  = P Rbar;  optimizer on X with Ghat.
+// MFMA rows are tile rows and lanes are tile columns, so that a load or
+// store of one accumulator register moves two whole 128-byte rows of 32
+// columns: every written line of E, X, the optimizer state and Ebar is
+// covered by one instruction (partial-line writes make the memory side
+// fetch the line first).  P (gathered rows of U^T) and Q^(i) are staged
 // through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
 constexpr int RO_COLS = 64;
@@ -382,26 +384,30 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
-  // engine rows = tile columns; each wave owns 32 tile rows, one per lane
-  constexpr int WN = ROWS / 32, WM = 4 / WN;
-  using T = MfmaTile<RO_COLS, ROWS, WM, WN>;
+  using T = MfmaTile<ROWS, RO_COLS, 2, 2>;
   constexpr int TM = T::TM;
-  static_assert(T::TN == 1, "one tile row per lane");
+  static_assert(T::TN == 1, "one tile column per lane");
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
   const int c0 = blockIdx.x * RO_COLS;   // first column of the tile
   const int r0 = blockIdx.y * ROWS;      // first row of the tile
   const int64_t mn = m * n;
-  const bool vec = (n & 3) == 0;
-  // this lane's outputs: for tm, g: row = r0 + ec, columns cb .. cb+3
-  const int lane = lane_id();
-  const int ec = (wave_id() % WN) * 32 + (lane & 31);
-  const int64_t row = r0 + ec;
-  const int cl = c0 + (wave_id() / WN) * T::WTM + 4 * (lane >> 5);   // column of (tm, g): cl + 32 tm + 8 g
-  const int64_t rbase = row * n;
-  auto ncols = [&](int tm, int g) -> int {
-    const int64_t cb = cl + 32 * tm + 8 * g;
-    return row < m ? (int)(n - cb >= 4 ? 4 : (n - cb > 0 ? n - cb : 0)) : 0;
-  };
+  // this lane's outputs: column cc, rows r0 + row(tm, v) = rb[tm] + rv(v)
+  // with rv(v) = 8 (v / 4) + v % 4 the same in every lane
+  T geo;
+  const int64_t cc = c0 + geo.col(0);
+  const bool cok = cc < n;
+  // every m x n array is addressed as a buffer (m n 4 < 2^32 bytes): a
+  // uniform descriptor and one 32-bit byte offset per element, shared by all
+  // of them; elements outside the matrix take kBufNone
+  const uint32_t bytes = (uint32_t)(mn * 4);
+  uint32_t ob[TM][16];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t row = r0 + geo.row(tm, v);
+      ob[tm][v] = (cok && row < m) ? (uint32_t)((row * n + cc) * 4) : kBufNone;
+    }
   float ebar[TM][16];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -409,153 +415,86 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     for (int v = 0; v < 16; ++v) ebar[tm][v] = 0.f;
 
   for (int wk = 0; wk < N; ++wk) {
-    const float* Gi = G + (int64_t)wk * mn;
-    float* Ei = E + (int64_t)wk * mn;
+    const BufRsrc Gi = buf_rsrc(G + (int64_t)wk * mn, bytes);
+    const BufRsrc Ei = buf_rsrc(E + (int64_t)wk * mn, bytes);
     const float* Qi = Q + (int64_t)wk * r * D;
     // G^(i) and E^(i) for this lane's elements, in flight during the product
     float gv[TM][16], eo[TM][16];
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t o = rbase + cl + 32 * tm + 8 * g;
-        const int nc = ncols(tm, g);
-        if (vec && nc == 4) {
-          const float4 a = load_nt4(Gi + o);
-          const float4 b = *reinterpret_cast<const float4*>(Ei + o);
-          gv[tm][4 * g + 0] = a.x; gv[tm][4 * g + 1] = a.y; gv[tm][4 * g + 2] = a.z; gv[tm][4 * g + 3] = a.w;
-          eo[tm][4 * g + 0] = b.x; eo[tm][4 * g + 1] = b.y; eo[tm][4 * g + 2] = b.z; eo[tm][4 * g + 3] = b.w;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            gv[tm][4 * g + e] = e < nc ? Gi[o + e] : 0.f;
-            eo[tm][4 * g + e] = e < nc ? Ei[o + e] : 0.f;
-          }
-        }
+      for (int v = 0; v < 16; ++v) {
+        gv[tm][v] = buf_ld(Gi, ob[tm][v]);
+        eo[tm][v] = buf_ld(Ei, ob[tm][v]);
       }
     T tile;
     if (!RIGHT) {
       // rows a < d, columns b < D: C[a][b] = sum_k Ut[J[k]][a] Q[k][b]
-      LoadR<RO_COLS, 32, false> la(Qi, nullptr, D, c0, (int)D, r);
-      LoadR<ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+      LoadR<ROWS, 32, false, true> la(Ut, nullptr, d, r0, (int)d, r, J);
+      LoadR<RO_COLS, 32, false> lb(Qi, nullptr, D, c0, (int)D, r);
       tile.run(la, lb, r, smem);
     } else {
       // rows b < D, columns a < d: C[b][a] = sum_k Q[k][b] Ut[J[k]][a]
-      LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
-      LoadR<ROWS, 32, false> lb(Qi, nullptr, D, r0, (int)D, r);
+      LoadR<ROWS, 32, false> la(Qi, nullptr, D, r0, (int)D, r);
+      LoadR<RO_COLS, 32, false, true> lb(Ut, nullptr, d, c0, (int)d, r, J);
       tile.run(la, lb, r, smem);
     }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float ev[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int v = 4 * g + e;
-          const float c = tile.acc[tm][0][v];
-          // (G - P Q) + E: G and P Q nearly cancel, E is the small part
-          ev[e] = (gv[tm][v] - c) + eo[tm][v];
-          ebar[tm][v] += ev[e];
-        }
-        const int64_t o = rbase + cl + 32 * tm + 8 * g;
-        const int nc = ncols(tm, g);
-        if (vec && nc == 4) {
-          *reinterpret_cast<float4*>(Ei + o) = make_float4(ev[0], ev[1], ev[2], ev[3]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (e < nc) Ei[o + e] = ev[e];
-        }
+      for (int v = 0; v < 16; ++v) {
+        // (G - P Q) + E: G and P Q nearly cancel, E is the small part
+        const float ev = (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v];
+        ebar[tm][v] += ev;
+        buf_st(Ei, ob[tm][v], ev);
       }
   }
 
   // Ghat = P Rbar (the reconstruction of the averaged payload)
   T tile;
   if (!RIGHT) {
-    LoadR<RO_COLS, 32, false> la(Rbar, nullptr, D, c0, (int)D, r);
-    LoadR<ROWS, 32, false, true> lb(Ut, nullptr, d, r0, (int)d, r, J);
+    LoadR<ROWS, 32, false, true> la(Ut, nullptr, d, r0, (int)d, r, J);
+    LoadR<RO_COLS, 32, false> lb(Rbar, nullptr, D, c0, (int)D, r);
     tile.run(la, lb, r, smem);
   } else {
-    LoadR<RO_COLS, 32, false, true> la(Ut, nullptr, d, c0, (int)d, r, J);
-    LoadR<ROWS, 32, false> lb(Rbar, nullptr, D, r0, (int)D, r);
+    LoadR<ROWS, 32, false> la(Rbar, nullptr, D, r0, (int)D, r);
+    LoadR<RO_COLS, 32, false, true> lb(Ut, nullptr, d, c0, (int)d, r, J);
     tile.run(la, lb, r, smem);
   }
   const float fN = (float)N;
+  const BufRsrc Xr = buf_rsrc(X, bytes), S1r = buf_rsrc(S1, bytes), Ebr = buf_rsrc(Ebar, bytes);
+  const BufRsrc S2r = buf_rsrc(OPT == 1 ? S2 : S1, bytes);
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int64_t o = rbase + cl + 32 * tm + 8 * g;
-      const int nc = ncols(tm, g);
-      if (nc == 0) continue;
-      const bool full = vec && nc == 4;
-      float xv[4], s1[4], s2[4], eb[4];
-      if (full) {
-        const float4 a = *reinterpret_cast<const float4*>(X + o);
-        const float4 b = *reinterpret_cast<const float4*>(S1 + o);
-        xv[0] = a.x; xv[1] = a.y; xv[2] = a.z; xv[3] = a.w;
-        s1[0] = b.x; s1[1] = b.y; s1[2] = b.z; s1[3] = b.w;
-        if (OPT == 1) {
-          const float4 c = *reinterpret_cast<const float4*>(S2 + o);
-          s2[0] = c.x; s2[1] = c.y; s2[2] = c.z; s2[3] = c.w;
-        }
+    for (int v = 0; v < 16; ++v) {
+      const uint32_t o = ob[tm][v];
+      const float gh = tile.acc[tm][0][v];
+      float xv = buf_ld(Xr, o), s1 = buf_ld(S1r, o);
+      if (OPT == 0) {
+        s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+        xv = xv - op.lr * s1;
       } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          xv[e] = e < nc ? X[o + e] : 0.f;
-          s1[e] = e < nc ? S1[o + e] : 0.f;
-          if (OPT == 1) s2[e] = e < nc ? S2[o + e] : 0.f;
-        }
+        float s2 = buf_ld(S2r, o);
+        s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+        s2 = op.beta2 * s2 + (1.0f - op.beta2) * gh * gh;
+        xv = xv - op.lr * s1 / (sqrtf(s2) + op.eps);
+        buf_st(S2r, o, s2);
       }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int v = 4 * g + e;
-        eb[e] = ebar[tm][v] / fN;
-        const float gh = tile.acc[tm][0][v];
-        if (OPT == 0) {
-          s1[e] = op.beta1 * s1[e] + (1.0f - op.beta1) * gh;
-          xv[e] = xv[e] - op.lr * s1[e];
-        } else {
-          s1[e] = op.beta1 * s1[e] + (1.0f - op.beta1) * gh;
-          s2[e] = op.beta2 * s2[e] + (1.0f - op.beta2) * gh * gh;
-          xv[e] = xv[e] - op.lr * s1[e] / (sqrtf(s2[e]) + op.eps);
-        }
-      }
-      if (full) {
-        *reinterpret_cast<float4*>(Ebar + o) = make_float4(eb[0], eb[1], eb[2], eb[3]);
-        *reinterpret_cast<float4*>(X + o) = make_float4(xv[0], xv[1], xv[2], xv[3]);
-        *reinterpret_cast<float4*>(S1 + o) = make_float4(s1[0], s1[1], s1[2], s1[3]);
-        if (OPT == 1) *reinterpret_cast<float4*>(S2 + o) = make_float4(s2[0], s2[1], s2[2], s2[3]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (e >= nc) continue;
-          Ebar[o + e] = eb[e];
-          X[o + e] = xv[e];
-          S1[o + e] = s1[e];
-          if (OPT == 1) S2[o + e] = s2[e];
-        }
-      }
+      buf_st(Ebr, o, ebar[tm][v] / fN);
+      buf_st(Xr, o, xv);
+      buf_st(S1r, o, s1);
     }
 }
 
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  // 64-row tiles halve each lane's share of G, E and E-bar; 128-row tiles
-  // when the matrix has too few rows of tiles otherwise
-  const bool small = (v.m + 63) / 64 * ((v.n + RO_COLS - 1) / RO_COLS) >= 1024;
-  const int rows = small ? 64 : 128;
+  constexpr int rows = 64;
   dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + rows - 1) / rows));
-#define GLR_RO(OPT, R, ROWS)                                                                        \
-  hipLaunchKernelGGL((k_resid_opt<OPT, R, ROWS>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q, \
+#define GLR_RO(OPT, R)                                                                               \
+  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q, \
                      v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
-  if (small) {
-    if (o.opt == 0) { if (v.right) GLR_RO(0, true, 64); else GLR_RO(0, false, 64); }
-    else            { if (v.right) GLR_RO(1, true, 64); else GLR_RO(1, false, 64); }
-  } else {
-    if (o.opt == 0) { if (v.right) GLR_RO(0, true, 128); else GLR_RO(0, false, 128); }
-    else            { if (v.right) GLR_RO(1, true, 128); else GLR_RO(1, false, 128); }
-  }
+  if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
+  else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
 #undef GLR_RO
   return hipGetLastError();
 }

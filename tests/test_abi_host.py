@@ -49,6 +49,7 @@ def test_valid_config():
     (dict(select=3), 1), (dict(max_sweeps=0), 1), (dict(tol=0.0), 1), (dict(tol=1.0), 1),
     (dict(flags=0x80), 1), (dict(shapes=[(0, 5)]), 2), (dict(shapes=[(5, -1)]), 2),
     (dict(shapes=[(9000, 9000)]), 2), (dict(shapes=[(2000, 3000)], rank=2000), 2),
+    (dict(shapes=[(8192, 1 << 17)]), 2),   # m n = 2^30: beyond 32-bit byte offsets
 ])
 def test_invalid_configs_are_rejected(kw, code):
     cfg, _keep = _cfg(**kw)
