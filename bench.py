@@ -112,7 +112,9 @@ def group_work(wl, name):
         elif name == "proj":
             w = (8.0 * N * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
         elif name == "resid_opt":
-            w = ((12.0 * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
+            # G, E read and E written per worker; Mbar read and Ebar written;
+            # X and the optimizer state read and written
+            w = ((12.0 * N + 8 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * (N + 1), 0, 0)
         elif name.startswith("jac_") and not sub:
             w = jacobi_work(name[4:], d)
         elif name.startswith("rr_") and sub:

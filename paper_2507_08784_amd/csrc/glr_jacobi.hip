@@ -232,8 +232,8 @@ __device__ __forceinline__ double pk_get(const double* __restrict__ Apk, int nb,
 // pairing of the blocks: one pairing for NG = 2, three for NG = 4).  In a
 // step, each of the NR^2 / 4 threads owns one 2 x 2 block rows {p_a, q_a} x
 // columns {p_b, q_b} of G and of V, so that the update G <- J^T G J,
-// V <- V J is in place and private to the thread; the thread owning (a, a)
-// first computes rotation a from that diagonal block.
+// V <- V J is in place and private to the thread; the rotations are first
+// computed by one wave from the diagonal 2 x 2 blocks.
 // Rotation J = [[c, s], [-s, c]] that diagonalises [[gpp, gpq], [gpq, gqq]]:
 // t = tan(theta) = sign(d h) |h| / (|d| + sqrt(d^2 + h^2)), d = gqq - gpp,
 // h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  d and h are first scaled by a
@@ -311,8 +311,9 @@ struct SolveLds {
   static constexpr int NR = JacShape<NG>::NR;
   double G[NR][NR + 1];
   double V[NR][NR + 1];
-  double rc[NR / 2], rs[NR / 2];
+  double2 rot[NR / 2];               // (c, s) of the step's rotations
   double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
+  uint16_t pq[NR][NR / 2];           // p | q << 8 of rotation j at step st
 };
 template <int NG>
 union JacLds {
@@ -336,8 +337,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   }
   double (*G)[NR + 1] = L.G;
   double (*V)[NR + 1] = L.V;
-  double* rc = L.rc;
-  double* rs = L.rs;
+  double2* rot = L.rot;
   double* red = L.red;
   double* redw = L.redw;
   constexpr int NE = NR * NR / NT;
@@ -410,33 +410,30 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   // circle) distinct modulo 16: few bank conflicts
   const int a = tid / (NR / 2), bb = tid % (NR / 2);
   const int steps = cross ? SH::CROSS : NR - 1;
+  // the pairs of every step, tabulated once
+  for (int e = tid; e < steps * (NR / 2); e += NT) {
+    int p, q;
+    step_pair<NG>(cross, e / (NR / 2), e % (NR / 2), p, q);
+    L.pq[e / (NR / 2)][e % (NR / 2)] = (uint16_t)(p | (q << 8));
+  }
+  __syncthreads();
   for (int sweep = 0; sweep < max_inner; ++sweep) {
-    int pa = 0, qa = 0, pb = 0, qb = 0;
     for (int st = 0; st < steps; ++st) {
-      // the pairs move by one place per step: p + 1, q + 1 on the circle of
-      // NR - 1 (q = NR - 1 stays), or q + 1 within its block between blocks
-      if (st == 0 || (cross && (st & (kJB - 1)) == 0)) {
-        step_pair<NG>(cross, st, a, pa, qa);
-        step_pair<NG>(cross, st, bb, pb, qb);
-      } else if (cross) {
-        qa = (qa & ~(kJB - 1)) | ((qa + 1) & (kJB - 1));
-        qb = (qb & ~(kJB - 1)) | ((qb + 1) & (kJB - 1));
-      } else {
-        pa = pa == NR - 2 ? 0 : pa + 1;
-        pb = pb == NR - 2 ? 0 : pb + 1;
-        qa = qa == NR - 1 ? qa : (qa == NR - 2 ? 0 : qa + 1);
-        qb = qb == NR - 1 ? qb : (qb == NR - 2 ? 0 : qb + 1);
-      }
-      if (a == bb) {
+      const uint32_t ea = L.pq[st][a], eb = L.pq[st][bb];
+      const int pa = ea & 0xFF, qa = ea >> 8, pb = eb & 0xFF, qb = eb >> 8;
+      // the rotations come from wave 0 alone (its first NR / 2 lanes hold
+      // a = 0 and b = lane): the other waves skip the branch instead of
+      // issuing it under a mask
+      if (w == 0 && lane < NR / 2) {
         double c, sn;
-        jac_rotation(G[pa][pa], G[qa][qa], G[pa][qa], c, sn);
-        rc[a] = c;
-        rs[a] = sn;
+        jac_rotation(G[pb][pb], G[qb][qb], G[pb][qb], c, sn);
+        rot[bb] = double2{c, sn};
       }
       __syncthreads();
       // J restricted to a pair (p, q) is [[c, s], [-s, c]]; every entry
       // belongs to the 2 x 2 block of exactly one thread
-      const double ca = rc[a], sa = rs[a], cb = rc[bb], sb = rs[bb];
+      const double2 ra = rot[a], rb = rot[bb];
+      const double ca = ra.x, sa = ra.y, cb = rb.x, sb = rb.y;
       const double g00 = G[pa][pb], g01 = G[pa][qb], g10 = G[qa][pb], g11 = G[qa][qb];
       const double v00 = V[pa][pb], v01 = V[pa][qb], v10 = V[qa][pb], v11 = V[qa][qb];
       const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;

@@ -366,8 +366,9 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // S5 + S7 + S8 fused, one pass over a ROWS x 64 tile of the m x n layout:
 //   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
-//   E^(i) <- (G^(i) - C^(i)) + E^(i);  Ebar = (1/N) sum_i E^(i)
-//   Ghat  = P Rbar;  optimizer on X with Ghat.
+//   E^(i) <- (G^(i) - C^(i)) + E^(i)
+//   Ghat  = P Rbar;  Ebar = Mbar - Ghat (the mean of the E^(i) by
+//   linearity);  optimizer on X with Ghat.
 // MFMA rows are tile rows and lanes are tile columns, so that a load or
 // store of one accumulator register moves two whole 128-byte rows of 32
 // columns: every written line of E, X, the optimizer state and Ebar is
@@ -378,9 +379,10 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 constexpr int RO_COLS = 64;
 
 template <int OPT, bool RIGHT, int ROWS>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ROWS == 64 ? 3 : 2, ROWS == 64 ? 3 : 2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
-            const float* __restrict__ Q, const float* __restrict__ Rbar, const float* __restrict__ Ut,
+            const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
+            const float* __restrict__ Ut,
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
@@ -408,12 +410,6 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
       const int64_t row = r0 + geo.row(tm, v);
       ob[tm][v] = (cok && row < m) ? (uint32_t)((row * n + cc) * 4) : kBufNone;
     }
-  float ebar[TM][16];
-#pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) ebar[tm][v] = 0.f;
-
   for (int wk = 0; wk < N; ++wk) {
     const BufRsrc Gi = buf_rsrc(G + (int64_t)wk * mn, bytes);
     const BufRsrc Ei = buf_rsrc(E + (int64_t)wk * mn, bytes);
@@ -444,9 +440,7 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         // (G - P Q) + E: G and P Q nearly cancel, E is the small part
-        const float ev = (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v];
-        ebar[tm][v] += ev;
-        buf_st(Ei, ob[tm][v], ev);
+        buf_st(Ei, ob[tm][v], (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v]);
       }
   }
 
@@ -461,8 +455,8 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     LoadR<RO_COLS, 32, false, true> lb(Ut, nullptr, d, c0, (int)d, r, J);
     tile.run(la, lb, r, smem);
   }
-  const float fN = (float)N;
   const BufRsrc Xr = buf_rsrc(X, bytes), S1r = buf_rsrc(S1, bytes), Ebr = buf_rsrc(Ebar, bytes);
+  const BufRsrc Mr = buf_rsrc(Mbar, bytes);
   const BufRsrc S2r = buf_rsrc(OPT == 1 ? S2 : S1, bytes);
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -481,7 +475,7 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
         xv = xv - op.lr * s1 / (sqrtf(s2) + op.eps);
         buf_st(S2r, o, s2);
       }
-      buf_st(Ebr, o, ebar[tm][v] / fN);
+      buf_st(Ebr, o, buf_ld(Mr, o) - gh);
       buf_st(Xr, o, xv);
       buf_st(S1r, o, s1);
     }
@@ -491,8 +485,8 @@ hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s)
   constexpr int rows = 64;
   dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + rows - 1) / rows));
 #define GLR_RO(OPT, R)                                                                               \
-  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Q, \
-                     v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
+  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
+                     v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
   if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
   else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
 #undef GLR_RO
