@@ -262,7 +262,8 @@ __device__ __forceinline__ void jac_rotation(double gpp, double gqq, double gpq,
 template <int NG>
 struct JacShape {
   static constexpr int NR = NG * kJB;        // rows of a group
-  static constexpr int NT = NR * NR / 4;     // solve threads, one 2 x 2 block each
+  static constexpr int CPT = 1;              // 2 x 2 blocks per solve thread
+  static constexpr int NT = NR * NR / 4 / CPT;   // solve threads
   static constexpr int NW = NT / 64;
   static constexpr int CROSS = (NG == 2 ? 1 : 3) * kJB;   // steps between blocks
 };
@@ -408,7 +409,13 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   // the 16 lanes of an LDS access share the row pair a and take 16
   // consecutive column pairs b, whose rows are (up to the wrap of the
   // circle) distinct modulo 16: few bank conflicts
-  const int a = tid / (NR / 2), bb = tid % (NR / 2);
+  constexpr int CPT = SH::CPT;
+  // thread t owns the 2 x 2 blocks (a_i, b) with b = t % (NR / 2) and
+  // a_i = (t + NT i) / (NR / 2)
+  const int bb = tid % (NR / 2);
+  int ai[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) ai[i] = (tid + NT * i) / (NR / 2);
   const int steps = cross ? SH::CROSS : NR - 1;
   // the pairs of every step, tabulated once
   for (int e = tid; e < steps * (NR / 2); e += NT) {
@@ -419,8 +426,8 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   __syncthreads();
   for (int sweep = 0; sweep < max_inner; ++sweep) {
     for (int st = 0; st < steps; ++st) {
-      const uint32_t ea = L.pq[st][a], eb = L.pq[st][bb];
-      const int pa = ea & 0xFF, qa = ea >> 8, pb = eb & 0xFF, qb = eb >> 8;
+      const uint32_t eb = L.pq[st][bb];
+      const int pb = eb & 0xFF, qb = eb >> 8;
       // the rotations come from wave 0 alone (its first NR / 2 lanes hold
       // a = 0 and b = lane): the other waves skip the branch instead of
       // issuing it under a mask
@@ -431,21 +438,36 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
       }
       __syncthreads();
       // J restricted to a pair (p, q) is [[c, s], [-s, c]]; every entry
-      // belongs to the 2 x 2 block of exactly one thread
-      const double2 ra = rot[a], rb = rot[bb];
-      const double ca = ra.x, sa = ra.y, cb = rb.x, sb = rb.y;
-      const double g00 = G[pa][pb], g01 = G[pa][qb], g10 = G[qa][pb], g11 = G[qa][qb];
-      const double v00 = V[pa][pb], v01 = V[pa][qb], v10 = V[qa][pb], v11 = V[qa][qb];
-      const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
-      const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
-      G[pa][pb] = ca * t00 - sa * t10;
-      G[pa][qb] = ca * t01 - sa * t11;
-      G[qa][pb] = sa * t00 + ca * t10;
-      G[qa][qb] = sa * t01 + ca * t11;
-      V[pa][pb] = v00 * cb - v01 * sb;
-      V[pa][qb] = v00 * sb + v01 * cb;
-      V[qa][pb] = v10 * cb - v11 * sb;
-      V[qa][qb] = v10 * sb + v11 * cb;
+      // belongs to the 2 x 2 block of exactly one thread, and a thread's
+      // blocks are disjoint: all its reads come before its writes
+      const double2 rb = rot[bb];
+      const double cb = rb.x, sb = rb.y;
+      int pa[CPT], qa[CPT];
+      double ca[CPT], sa[CPT], g[CPT][4], vv[CPT][4];
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const uint32_t ea = L.pq[st][ai[i]];
+        pa[i] = ea & 0xFF;
+        qa[i] = ea >> 8;
+        const double2 ra = rot[ai[i]];
+        ca[i] = ra.x;
+        sa[i] = ra.y;
+        g[i][0] = G[pa[i]][pb]; g[i][1] = G[pa[i]][qb]; g[i][2] = G[qa[i]][pb]; g[i][3] = G[qa[i]][qb];
+        vv[i][0] = V[pa[i]][pb]; vv[i][1] = V[pa[i]][qb]; vv[i][2] = V[qa[i]][pb]; vv[i][3] = V[qa[i]][qb];
+      }
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const double t00 = g[i][0] * cb - g[i][1] * sb, t01 = g[i][0] * sb + g[i][1] * cb;
+        const double t10 = g[i][2] * cb - g[i][3] * sb, t11 = g[i][2] * sb + g[i][3] * cb;
+        G[pa[i]][pb] = ca[i] * t00 - sa[i] * t10;
+        G[pa[i]][qb] = ca[i] * t01 - sa[i] * t11;
+        G[qa[i]][pb] = sa[i] * t00 + ca[i] * t10;
+        G[qa[i]][qb] = sa[i] * t01 + ca[i] * t11;
+        V[pa[i]][pb] = vv[i][0] * cb - vv[i][1] * sb;
+        V[pa[i]][qb] = vv[i][0] * sb + vv[i][1] * cb;
+        V[qa[i]][pb] = vv[i][2] * cb - vv[i][3] * sb;
+        V[qa[i]][qb] = vv[i][2] * sb + vv[i][3] * cb;
+      }
       __syncthreads();
     }
   }
@@ -546,7 +568,7 @@ __device__ __forceinline__ void apply_chunk(float* __restrict__ Utw, int64_t d, 
 // by exactly one workgroup.  A group whose V is the identity skips its
 // product.
 template <int NG>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
 k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int* __restrict__ skip,
              const JacCtl* __restrict__ ctl, int round, int seats, int nb, int groups) {
   constexpr int NR = JacShape<NG>::NR, TW = NR / 32;   // 16 x 16 tiles per quadrant side

@@ -376,9 +376,7 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // fetch the line first).  P (gathered rows of U^T) and Q^(i) are staged
 // through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
-constexpr int RO_COLS = 64;
-
-template <int OPT, bool RIGHT, int ROWS>
+template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
             const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
@@ -386,7 +384,7 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
-  using T = MfmaTile<ROWS, RO_COLS, 2, 2>;
+  using T = MfmaTile<ROWS, RO_COLS, ROWS / 32, 128 / ROWS>;
   constexpr int TM = T::TM;
   static_assert(T::TN == 1, "one tile column per lane");
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
@@ -482,10 +480,10 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
 }
 
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  constexpr int rows = 64;
-  dim3 grid((unsigned)((v.n + RO_COLS - 1) / RO_COLS), (unsigned)((v.m + rows - 1) / rows));
+  constexpr int rows = 64, cols = 64;
+  dim3 grid((unsigned)((v.n + cols - 1) / cols), (unsigned)((v.m + rows - 1) / rows));
 #define GLR_RO(OPT, R)                                                                               \
-  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
+  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
                      v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
   if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
   else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
