@@ -103,7 +103,7 @@ def group_work(wl, name):
         mn = m * n
         adam = wl.opt == "adam"
         sub = uses_subspace(wl, d)
-        K = min(2 * r, d)
+        K = min(r + max(32, r // 4), d)
         w = None
         if name == "ef_mean":
             w = (4.0 * (N + 2) * mn, 0, 0, 0)

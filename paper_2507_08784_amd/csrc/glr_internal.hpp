@@ -45,7 +45,14 @@ inline int chol_pad(int K) { return (K + kCholTile - 1) / kCholTile * kCholTile;
 // The tau = 1 refresh needs only span(U[:, :r]): subspace iteration then, on
 // an oversampled block of sub_block(r, d) directions.
 inline bool use_subspace(int tau, int r, int64_t d) { return tau == 1 && r < d && r <= kMaxSubK; }
-inline int sub_block(int r, int64_t d) { return (int)((int64_t)(2 * r) < d ? 2 * r : d); }
+// rows of a subspace GEMM tile for an M-row product, and its tile count
+inline int gemm_rows(int M) { return M % 128 != 0 ? 64 : 128; }
+inline int gemm_blocks(int M, int N) { return ((N + 127) / 128) * ((M + gemm_rows(M) - 1) / gemm_rows(M)); }
+// oversampling: r / 4 extra directions, at least 32
+inline int sub_block(int r, int64_t d) {
+  const int64_t k = (int64_t)r + (r / 4 > 32 ? r / 4 : 32);
+  return (int)(k < d ? k : d);
+}
 
 // One matrix of the current step, as the kernels see it.
 struct MatView {

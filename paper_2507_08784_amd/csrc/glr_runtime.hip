@@ -168,7 +168,7 @@ WsLayout ws_layout(const glr_config* c) {
       mx(s_KK, K * K);
       mx(s_Kp2, Kp * Kp);
       mx(s_nt, Kp / kCholTile);
-      mx(s_sums, (uint64_t)((x.d + 127) / 128) * ((K + 127) / 128));
+      mx(s_sums, (uint64_t)gemm_blocks(Ki, (int)x.d));
     } else {
       mx(mx_dD, (uint64_t)(x.d * x.D));
       mx(mx_dd, (uint64_t)(x.d * x.d));

@@ -1,7 +1,7 @@
 // Refresh step when only the top-r block of U is consumed (tau = 1: every
 // step is a refresh and J = {0..r-1}, so only span(U[:, :r]) matters).
 //
-// Block subspace iteration on K = min(d, 2r) directions, orthonormalised
+// Block subspace iteration on K = min(d, r + max(32, r / 4)) directions, orthonormalised
 // after each half step:
 //     Z  = orth(P^T Mo)        (K x D)
 //     P^T = orth(Z Mo^T)       (K x d)
@@ -103,9 +103,15 @@ template <bool B_KC, int EPI>
 static void gemm_launch(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
                         int64_t ldc, int M, int N, int Kc, GemmPlan p, int64_t cstride,
                         const float* X, double* sums, hipStream_t s) {
-  dim3 grid((N + 127) / 128, (M + 127) / 128, p.splits);
-  hipLaunchKernelGGL((k_gemm<128, 128, 2, 2, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                     ldc, M, N, Kc, p.kslice, cstride, X, sums);
+  // 64-row tiles when M is not a multiple of 128 (no half-empty last row of tiles)
+  const int bm = gemm_rows(M);
+  dim3 grid((N + 127) / 128, (M + bm - 1) / bm, p.splits);
+  if (bm == 64)
+    hipLaunchKernelGGL((k_gemm<64, 128, 1, 4, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums);
+  else
+    hipLaunchKernelGGL((k_gemm<128, 128, 2, 2, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums);
 }
 
 // out[i] = sum over splits of part[s * count + i], in a fixed order, fp64
@@ -782,7 +788,7 @@ hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hi
                      pc.splits, (int64_t)K * K, v.sub_C, (double*)nullptr);
   GemmPlan p3{1, K};
   gemm_launch<false, 1>(v.sub_C, K, v.sub_P, d, v.sub_R, d, K, (int)d, K, p3, 0, v.sub_Pn, v.sub_sums, s);
-  const int nb = (int)(((d + 127) / 128) * ((K + 127) / 128));
+  const int nb = gemm_blocks(K, (int)d);
   hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, &v.sub_ctl->change2);
   hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, v.sub_ctl, K, tol);
   // P <- P_new

@@ -231,8 +231,7 @@ def run_fullsize(glr, name, steps, sample_cols=6, seed=7, ref_top=False):
             rec = {"t": t, "mat": l}
             if refresh and r < d:
                 sub = wl.tau == 1 and r <= 256
-                rows = min(d, 2 * r) if sub else d
-                rec.update(check_refresh(run, l, mb, r if sub else rows))
+                rec.update(check_refresh(run, l, mb, r if sub else d))
                 if ref_top:
                     G64 = (mb @ mb.T).cpu().numpy()
                     w, V = np.linalg.eigh(G64)
