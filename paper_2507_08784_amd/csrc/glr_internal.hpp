@@ -93,7 +93,15 @@ struct ProfHook {
 // slices of the d contraction of the projection: enough workgroups to fill
 // the chip (tiles of 64 columns of D, one rank tile, per worker), slices of at
 // least 256
+// Slices of the d contraction of the projection.  Above rank 128 one tile
+// covers all r rows and accumulates 512 terms in fp32 per slice (the slices
+// are added in fp64 by the reduction); otherwise slices are only made to
+// fill the chip, and the kernel itself adds fp32 partial sums of 512 terms
+// into fp64.
+constexpr int kProjWideRank = 128;
+constexpr int kProjWideSlice = 512;
 inline int proj_splits(int64_t d, int64_t D, int r, int N) {
+  if (r > kProjWideRank) return (int)((d + kProjWideSlice - 1) / kProjWideSlice);
   const int64_t tiles = ((D + 63) / 64) * ((r + 127) / 128) * N;
   if (tiles >= 2048) return 1;
   int64_t sp = (2048 + tiles - 1) / tiles;

@@ -261,7 +261,7 @@ hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
 // S4: Q^(i) = P^T M^(i), r x D per worker (both orientations), with
 // P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool RIGHT>
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
 __global__ void __launch_bounds__(256)
 k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
        const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
@@ -278,21 +278,26 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
   const float* Ei = E + (int64_t)w * dD;
   T tile;
   // fp32 accumulators are added into fp64 ones every 512 terms of the slice
-  double dacc[T::TM][T::TN][16];
+  // (FLUSH), or the slice itself is at most 512 terms
+  double dacc[FLUSH ? T::TM : 1][FLUSH ? T::TN : 1][16];
+  if (FLUSH) {
 #pragma unroll
-  for (int tm = 0; tm < T::TM; ++tm)
+    for (int tm = 0; tm < T::TM; ++tm)
 #pragma unroll
-    for (int tn = 0; tn < T::TN; ++tn)
+      for (int tn = 0; tn < T::TN; ++tn)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) dacc[tm][tn][v] = 0.0;
+        for (int v = 0; v < 16; ++v) dacc[FLUSH ? tm : 0][FLUSH ? tn : 0][v] = 0.0;
+  }
   LoadK<BM, 32, false, true> la(Ut + k0, nullptr, d, m0, r, klen, J);
   if (RIGHT) {
     // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
     LoadK<BN, 32, true, false> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
-    tile.run(la, lb, klen, smem, dacc);
+    if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
+    else tile.run(la, lb, klen, smem);
   } else {
     LoadR<BN, 32, true> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
-    tile.run(la, lb, klen, smem, dacc);
+    if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
+    else tile.run(la, lb, klen, smem);
   }
   float* Qz = Qpart + ((int64_t)z * N + w) * r * D;
 #pragma unroll
@@ -304,7 +309,7 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int k = m0 + tile.row(tm, v);
-        if (k < r) Qz[(int64_t)k * D + b] = (float)dacc[tm][tn][v];
+        if (k < r) Qz[(int64_t)k * D + b] = FLUSH ? (float)dacc[FLUSH ? tm : 0][FLUSH ? tn : 0][v] : tile.acc[tm][tn][v];
       }
     }
 }
@@ -312,24 +317,26 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
 hipError_t launch_proj(const MatView& v, hipStream_t s) {
   const int r = v.r;
   const int splits = proj_splits(v.d, v.D, r, v.N);
-  const int64_t kslice = ((v.d + splits - 1) / splits + 31) / 32 * 32;
+  const int64_t kslice = r > kProjWideRank ? kProjWideSlice
+                                           : ((v.d + splits - 1) / splits + 31) / 32 * 32;
   float* const out = splits > 1 ? v.Qpart : v.Q;
   dim3 grid;
   grid.z = (unsigned)(v.N * splits);
-#define GLR_PROJ(BM, BN, WM, WN)                                                                  \
+#define GLR_PROJ(BM, BN, WM, WN, FL)                                                              \
   do {                                                                                            \
     grid.x = (unsigned)((v.D + BN - 1) / BN);                                                     \
     grid.y = (unsigned)((r + BM - 1) / BM);                                                       \
     if (v.right)                                                                                  \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true>), grid, dim3(kThreads), 0, s, v.G, v.E,    \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL>), grid, dim3(kThreads), 0, s, v.G, v.E, \
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
     else                                                                                          \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false>), grid, dim3(kThreads), 0, s, v.G, v.E,   \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL>), grid, dim3(kThreads), 0, s, v.G, v.E,\
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
   } while (0)
-  if (r <= 32) GLR_PROJ(32, 128, 1, 4);
-  else if (r <= 64) GLR_PROJ(64, 64, 2, 2);
-  else GLR_PROJ(128, 64, 2, 2);
+  if (r <= 32) GLR_PROJ(32, 128, 1, 4, true);
+  else if (r <= 64) GLR_PROJ(64, 64, 2, 2, true);
+  else if (r <= kProjWideRank) GLR_PROJ(128, 64, 2, 2, true);
+  else GLR_PROJ(256, 64, 4, 1, false);
 #undef GLR_PROJ
   return hipGetLastError();
 }
