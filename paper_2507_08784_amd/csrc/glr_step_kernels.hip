@@ -486,12 +486,77 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
     }
 }
 
+// S5 above rank 128, where the rank-r products dominate: 128 x 128 tiles
+// (64 x 64 per wave), one worker after the other, E^(w) <- (G^(w) - P Q^(w))
+// + E^(w) streamed 16 elements per lane at a time after each product;
+// k_resid_opt then runs with no workers (Ghat, Ebar and the optimizer).
+constexpr int kResidWideRank = 128;
+
+template <bool RIGHT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_resid_wide(const float* __restrict__ G, float* __restrict__ E, const float* __restrict__ Q,
+             const float* __restrict__ Ut, const int* __restrict__ J, int64_t m, int64_t n, int64_t d,
+             int64_t D, int r, int N) {
+  using T = MfmaTile<128, 128, 2, 2>;
+  __shared__ __align__(16) float smem[T::LDS_FLOATS];
+  const int c0 = blockIdx.x * 128, r0 = blockIdx.y * 128;
+  const int64_t mn = m * n;
+  const uint32_t bytes = (uint32_t)(mn * 4);
+  for (int wk = 0; wk < N; ++wk) {
+    const float* Qi = Q + (int64_t)wk * r * D;
+    T tile;
+    if (!RIGHT) {
+      // rows a < d, columns b < D: C[a][b] = sum_k Ut[J[k]][a] Q[k][b]
+      LoadR<128, 32, false, true> la(Ut, nullptr, d, r0, (int)d, r, J);
+      LoadR<128, 32, false> lb(Qi, nullptr, D, c0, (int)D, r);
+      tile.run(la, lb, r, smem);
+    } else {
+      // rows b < D, columns a < d: C[b][a] = sum_k Q[k][b] Ut[J[k]][a]
+      LoadR<128, 32, false> la(Qi, nullptr, D, r0, (int)D, r);
+      LoadR<128, 32, false, true> lb(Ut, nullptr, d, c0, (int)d, r, J);
+      tile.run(la, lb, r, smem);
+    }
+    const BufRsrc Gw = buf_rsrc(G + (int64_t)wk * mn, bytes);
+    const BufRsrc Ew = buf_rsrc(E + (int64_t)wk * mn, bytes);
+#pragma unroll
+    for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < T::TN; ++tn) {
+        const int64_t col = c0 + tile.col(tn);
+        uint32_t ob[16];
+        float gv[16], eo[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t row = r0 + tile.row(tm, v);
+          ob[v] = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
+          gv[v] = buf_ld(Gw, ob[v]);
+          eo[v] = buf_ld(Ew, ob[v]);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          // (G - P Q) + E: G and P Q nearly cancel, E is the small part
+          buf_st(Ew, ob[v], (gv[v] - tile.acc[tm][tn][v]) + eo[v]);
+      }
+  }
+}
+
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
+  const bool wide = v.r > kResidWideRank;
+  if (wide) {
+    dim3 gw((unsigned)((v.n + 127) / 128), (unsigned)((v.m + 127) / 128));
+    if (v.right)
+      hipLaunchKernelGGL(k_resid_wide<true>, gw, dim3(kThreads), 0, s, v.G, v.E, v.Q, v.Ut, v.J, v.m, v.n,
+                         v.d, v.D, v.r, v.N);
+    else
+      hipLaunchKernelGGL(k_resid_wide<false>, gw, dim3(kThreads), 0, s, v.G, v.E, v.Q, v.Ut, v.J, v.m, v.n,
+                         v.d, v.D, v.r, v.N);
+  }
+  const int nfused = wide ? 0 : v.N;   // workers whose residual k_resid_opt updates
   constexpr int rows = 64, cols = 64;
   dim3 grid((unsigned)((v.n + cols - 1) / cols), (unsigned)((v.m + rows - 1) / rows));
 #define GLR_RO(OPT, R)                                                                               \
   hipLaunchKernelGGL((k_resid_opt<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
-                     v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o)
+                     v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, nfused, o)
   if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
   else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
 #undef GLR_RO
