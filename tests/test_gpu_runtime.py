@@ -1,0 +1,133 @@
+"""GPU runtime contract through the C ABI: the device status word (non-finite
+input under GLR_CHECK_FINITE), the step-order contract, resuming from a copy
+of the state blob, and bitwise determinism of repeated runs."""
+import numpy as np
+import pytest
+
+from synth import get_workload, gradient_batch, planted_matrix
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[runtime]", *a, flush=True)
+
+
+def _inputs(wl, steps):
+    import torch
+    planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
+    return [[torch.from_numpy(gradient_batch(wl, l, t, planted[l])).cuda() for l in range(len(wl.shapes))]
+            for t in range(steps)]
+
+
+def _make(glr, wl, **kw):
+    return glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                          seed=wl.seed, **kw)
+
+
+def _zeros(wl):
+    import torch
+    return [torch.zeros(m, n, device="cuda") for m, n in wl.shapes]
+
+
+def _blob(comp):
+    return comp.state[comp._s0: comp._s0 + comp.state_bytes]
+
+
+def test_nonfinite_gradient_is_reported_and_state_marked_suspect(gpu_lib):
+    import torch
+    wl = get_workload("one_256x128")
+    _say("one_256x128 check_finite")
+    comp = _make(gpu_lib, wl, check_finite=True)
+    X = _zeros(wl)
+    G = _inputs(wl, 2)
+    comp.step(X, G[0], 0)
+    assert comp.sync_status() == gpu_lib.GLR_OK
+    bad = G[1][0].clone()
+    bad[1, 3, 5] = float("nan")
+    comp.step(X, [bad], 1)
+    assert comp.sync_status() == 6          # GLR_ERR_NONFINITE
+    with pytest.raises(gpu_lib.GlrError) as ei:
+        comp.step(X, G[1], 2)
+    assert ei.value.status == 4             # GLR_ERR_STATE until the caller resumes
+    comp.resume(2)
+    comp.step(X, G[1], 2)
+    assert comp.sync_status() == gpu_lib.GLR_OK
+    torch.cuda.synchronize()
+
+
+def test_step_order_contract(gpu_lib):
+    import torch
+    wl = get_workload("one_256x128")
+    _say("one_256x128 order")
+    comp = _make(gpu_lib, wl)
+    X = _zeros(wl)
+    G = _inputs(wl, 3)
+    with pytest.raises(gpu_lib.GlrError) as ei:
+        comp.step(X, G[1], 1)               # must start at t = 0
+    assert ei.value.status == 4
+    comp.step(X, G[0], 0)
+    torch.cuda.synchronize()
+    x0 = X[0].clone()
+    e0 = comp.E(0).clone()
+    with pytest.raises(gpu_lib.GlrError):
+        comp.step(X, G[2], 2)               # skips t = 1: rejected before any launch
+    torch.cuda.synchronize()
+    assert torch.equal(X[0], x0) and torch.equal(comp.E(0), e0)
+    assert comp.next_step() == 1
+    comp.step(X, G[1], 1)
+    assert comp.sync_status() == gpu_lib.GLR_OK
+
+
+@pytest.mark.parametrize("name", ["one_256x128", "tau1_left"])
+def test_resume_from_a_copied_state_matches_the_uninterrupted_run(gpu_lib, name):
+    import torch
+    wl = get_workload(name)
+    T = min(wl.steps, 7)
+    cut = 3
+    _say(name, "resume at", cut, "of", T)
+    G = _inputs(wl, T)
+    a = _make(gpu_lib, wl)
+    Xa = _zeros(wl)
+    for t in range(T):
+        a.step(Xa, G[t], t)
+    b = _make(gpu_lib, wl)
+    Xb = _zeros(wl)
+    for t in range(cut):
+        b.step(Xb, G[t], t)
+    torch.cuda.synchronize()
+    c = _make(gpu_lib, wl)
+    _blob(c).copy_(_blob(b))
+    c.resume(cut)
+    Xc = [x.clone() for x in Xb]
+    del b
+    for t in range(cut, T):
+        c.step(Xc, G[t], t)
+    torch.cuda.synchronize()
+    assert a.sync_status() == gpu_lib.GLR_OK and c.sync_status() == gpu_lib.GLR_OK
+    for l in range(len(wl.shapes)):
+        assert torch.equal(Xa[l], Xc[l]), f"mat {l}: X differs after resume"
+        assert torch.equal(a.E(l), c.E(l)), f"mat {l}: E differs after resume"
+
+
+@pytest.mark.parametrize("name", ["mid_left", "tau1_right"])
+def test_repeated_runs_are_bitwise_identical(gpu_lib, name):
+    import torch
+    wl = get_workload(name)
+    T = min(wl.steps, wl.tau + 2)
+    _say(name, "determinism over", T, "steps")
+    G = _inputs(wl, T)
+    runs = []
+    for _ in range(2):
+        comp = _make(gpu_lib, wl)
+        X = _zeros(wl)
+        for t in range(T):
+            comp.step(X, G[t], t)
+        torch.cuda.synchronize()
+        runs.append((comp, X))
+    (c1, x1), (c2, x2) = runs
+    for l in range(len(wl.shapes)):
+        assert torch.equal(x1[l], x2[l])
+        assert torch.equal(c1.E(l), c2.E(l))
+        assert torch.equal(c1.Ut(l), c2.Ut(l))
+        assert torch.equal(c1.J(l), c2.J(l))
