@@ -230,10 +230,11 @@ __device__ __forceinline__ double pk_get(const double* __restrict__ Apk, int nb,
 // NR / 2 disjoint rotations (circle method); when the rows inside each block
 // already meet the measure, only the steps between blocks are taken (16 per
 // pairing of the blocks: one pairing for NG = 2, three for NG = 4).  In a
-// step, each of the NR^2 / 4 threads owns one 2 x 2 block rows {p_a, q_a} x
-// columns {p_b, q_b} of G and of V, so that the update G <- J^T G J,
-// V <- V J is in place and private to the thread; the rotations are first
-// computed by one wave from the diagonal 2 x 2 blocks.
+// step, a thread owns one 2 x 2 block rows {p_a, q_a} x columns {p_b, q_b}
+// (a <= b) of the upper triangle of G and one 2 x 2 block of V, so that the
+// update G <- J^T G J, V <- V J is in place and private to the thread; the
+// rotations are computed by one wave from the diagonal 2 x 2 blocks while
+// the other waves apply the previous step's rotations to V.
 // Rotation J = [[c, s], [-s, c]] that diagonalises [[gpp, gpq], [gpq, gqq]]:
 // t = tan(theta) = sign(d h) |h| / (|d| + sqrt(d^2 + h^2)), d = gqq - gpp,
 // h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  d and h are first scaled by a
@@ -306,15 +307,22 @@ __device__ __forceinline__ bool group_empty(const int (&blk)[NG], int nb) {
   return e;
 }
 
-// LDS of a group solve; the rotation of U^T reuses it for V - I (fp32)
+// LDS of a group solve; the rotation of U^T reuses it for V - I (fp32).
+// G lives in "slot" coordinates: at every step the rows of rotation j sit in
+// slots 2j (p) and 2j + 1 (q), and only the upper triangle is stored, packed
+// by rows (two copies, read one / write the other by step parity).
 template <int NG>
 struct SolveLds {
-  static constexpr int NR = JacShape<NG>::NR;
-  double G[NR][NR + 1];
-  double V[NR][NR + 1];
-  double2 rot[NR / 2];               // (c, s) of the step's rotations
+  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NPK = NR * (NR + 1) / 2;
+  double Gp[2][NPK];
+  double V[NR][NR + 1];              // row coordinates
+  double2 rot[2][NP];                // (c, s) of the rotations of two consecutive steps
+  double dg[NR];                     // initial diagonal (row coordinates)
   double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
-  uint16_t pq[NR][NR / 2];           // p | q << 8 of rotation j at step st
+  uint16_t pq[NR][NP];               // rows p | q << 8 of rotation j at step st
+  uint16_t blk[NP * (NP + 1) / 2];   // upper 2 x 2 block (a | b << 8) of each thread
+  uint8_t sig[4][NR];                // next slot of each slot: regular step, three pairing changes
+  uint8_t pos0[NR];                  // slot of each row at step 0
 };
 template <int NG>
 union JacLds {
@@ -322,13 +330,40 @@ union JacLds {
   float Va[JacShape<NG>::NR][JacShape<NG>::NR + 1];
 };
 
+// offset of packed upper entry (P, Q), P <= Q, of an NR x NR matrix
+template <int NR>
+__device__ __forceinline__ int tri(int P, int Q) {
+  return P * (2 * NR - P - 1) / 2 + Q;
+}
+
+// rotation j of the next step is formed from slot 2 X + sx (its p) and slot
+// 2 Y + sy (its q) of this step: the closed form of the slot permutation.
+// Circle: rows of rotation j at step s + 1 are p_{j+1}(s) and q_{j-1}(s),
+// with the ends adjusted; steps between blocks: p_j(s) and q_{j+1}(s), j + 1
+// taken within the 16 rotations of a half.
+template <int NP>
+__device__ __forceinline__ void next_source(bool cross, int j, int& X, int& sx, int& Y, int& sy) {
+  if (cross) {
+    X = j; sx = 0; Y = (j & ~(kJB - 1)) | ((j + 1) & (kJB - 1)); sy = 1;
+  } else if (j == 0) {
+    X = 1; sx = 0; Y = 0; sy = 1;
+  } else if (j == 1) {
+    X = 2; sx = 0; Y = 0; sy = 0;
+  } else if (j < NP - 1) {
+    X = j + 1; sx = 0; Y = j - 1; sy = 1;
+  } else {
+    X = NP - 1; sx = 1; Y = NP - 2; sy = 1;
+  }
+}
+
 template <int NG>
 __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
                                             int seats, int nb, float tol, int max_inner, double floor_rel2,
                                             float* __restrict__ Vout, double* __restrict__ V64,
                                             int* __restrict__ skip, int grp, SolveLds<NG>& L) {
   using SH = JacShape<NG>;
-  constexpr int NR = SH::NR, NT = SH::NT, NW = SH::NW;
+  constexpr int NR = SH::NR, NT = SH::NT, NW = SH::NW, NP = NR / 2, NUP = NP * (NP + 1) / 2;
+  static_assert(NUP <= NT, "one upper 2 x 2 block per thread");
   int blk[NG];
   group_blocks<NG>(round, grp, seats, blk);
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
@@ -336,9 +371,6 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
     if (tid == 0) skip[grp] = 1;
     return;
   }
-  double (*G)[NR + 1] = L.G;
-  double (*V)[NR + 1] = L.V;
-  double2* rot = L.rot;
   double* red = L.red;
   double* redw = L.redw;
   constexpr int NE = NR * NR / NT;
@@ -354,9 +386,10 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
-    G[x][y] = g[k];
-    V[x][y] = x == y ? 1.0 : 0.0;
-    if (x == y) dmax = fmax(dmax, g[k]);
+    if (x == y) {
+      L.dg[x] = g[k];
+      dmax = fmax(dmax, g[k]);
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) dmax = fmax(dmax, __shfl_xor(dmax, o, 64));
@@ -375,7 +408,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
     if (x < y) {
-      const double gxx = G[x][x], gyy = G[y][y];
+      const double gxx = L.dg[x], gyy = L.dg[y];
       const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
       if (den > 0.0) {
         const double q2 = (g[k] / den) * (g[k] / den);
@@ -406,68 +439,194 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
     if (tid == 0) skip[grp] = 1;
     return;
   }
-  // the 16 lanes of an LDS access share the row pair a and take 16
-  // consecutive column pairs b, whose rows are (up to the wrap of the
-  // circle) distinct modulo 16: few bank conflicts
-  constexpr int CPT = SH::CPT;
-  // thread t owns the 2 x 2 blocks (a_i, b) with b = t % (NR / 2) and
-  // a_i = (t + NT i) / (NR / 2)
-  const int bb = tid % (NR / 2);
-  int ai[CPT];
-#pragma unroll
-  for (int i = 0; i < CPT; ++i) ai[i] = (tid + NT * i) / (NR / 2);
   const int steps = cross ? SH::CROSS : NR - 1;
-  // the pairs of every step, tabulated once
-  for (int e = tid; e < steps * (NR / 2); e += NT) {
+  // ---- tables: rows of every step; slots of step 0; slot permutations ----
+  for (int e = tid; e < steps * NP; e += NT) {
     int p, q;
-    step_pair<NG>(cross, e / (NR / 2), e % (NR / 2), p, q);
-    L.pq[e / (NR / 2)][e % (NR / 2)] = (uint16_t)(p | (q << 8));
+    step_pair<NG>(cross, e / NP, e % NP, p, q);
+    L.pq[e / NP][e % NP] = (uint16_t)(p | (q << 8));
+  }
+  if (tid < NP) {
+    // regular step: slot 2 X + sx goes to 2j, slot 2 Y + sy to 2j + 1
+    int X, sx, Y, sy;
+    next_source<NP>(cross, tid, X, sx, Y, sy);
+    L.sig[0][2 * X + sx] = (uint8_t)(2 * tid);
+    L.sig[0][2 * Y + sy] = (uint8_t)(2 * tid + 1);
   }
   __syncthreads();
-  for (int sweep = 0; sweep < max_inner; ++sweep) {
-    for (int st = 0; st < steps; ++st) {
-      const uint32_t eb = L.pq[st][bb];
-      const int pb = eb & 0xFF, qb = eb >> 8;
-      // the rotations come from wave 0 alone (its first NR / 2 lanes hold
-      // a = 0 and b = lane): the other waves skip the branch instead of
-      // issuing it under a mask
-      if (w == 0 && lane < NR / 2) {
-        double c, sn;
-        jac_rotation(G[pb][pb], G[qb][qb], G[pb][qb], c, sn);
-        rot[bb] = double2{c, sn};
+  if (tid < NP) {
+    const uint32_t e = L.pq[0][tid];
+    L.pos0[e & 0xFF] = (uint8_t)(2 * tid);
+    L.pos0[e >> 8] = (uint8_t)(2 * tid + 1);
+  }
+  // four-block groups, steps between blocks: the block pairing changes after
+  // steps 15, 31 and 47 (the last back to the pairing of step 0)
+  if (NG == 4 && cross && tid < 3 * NP) {
+    const int c = tid / NP, j = tid % NP;
+    const int st = kJB * c + kJB - 1, sn = (st + 1) % steps;
+    const uint32_t en = L.pq[sn][j];
+    const int pn = en & 0xFF, qn = en >> 8;
+    // slots of rows pn, qn at step st
+    for (int i = 0; i < NP; ++i) {
+      const uint32_t eo = L.pq[st][i];
+      const int po = eo & 0xFF, qo = eo >> 8;
+      if (po == pn) L.sig[1 + c][2 * i] = (uint8_t)(2 * j);
+      if (qo == pn) L.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j);
+      if (po == qn) L.sig[1 + c][2 * i] = (uint8_t)(2 * j + 1);
+      if (qo == qn) L.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j + 1);
+    }
+  }
+  // upper 2 x 2 block of each thread: the NP blocks that form the next step's
+  // rotations first (wave 0, so that one wave computes them), then the rest
+  // in triangular order
+  if (tid < NUP) {
+    int rem = tid, a = 0;
+    while (rem >= NP - a) {
+      rem -= NP - a;
+      ++a;
+    }
+    const int b = a + rem;
+    int slot = -1, before = 0;
+    for (int j = 0; j < NP; ++j) {
+      int X, sx, Y, sy;
+      next_source<NP>(cross, j, X, sx, Y, sy);
+      const int oa = min(X, Y), ob = max(X, Y);
+      if (oa == a && ob == b) slot = j;
+      const int oi = oa * NP - oa * (oa - 1) / 2 + (ob - oa);   // triangular index of the owner block
+      before += oi < tid ? 1 : 0;
+    }
+    if (slot < 0) slot = NP + tid - before;
+    L.blk[slot] = (uint16_t)(a | (b << 8));
+  }
+  __syncthreads();
+  // G (slot coordinates, upper, copy 0) and V = I (row coordinates)
+#pragma unroll
+  for (int k = 0; k < NE; ++k) {
+    const int e = tid + NT * k, x = e / NR, y = e % NR;
+    const int P = L.pos0[x], Q = L.pos0[y];
+    if (P <= Q) L.Gp[0][tri<NR>(P, Q)] = g[k];
+    L.V[x][y] = x == y ? 1.0 : 0.0;
+  }
+  // this thread's block (a, b), a <= b, and its LDS offsets (in doubles):
+  // reads of this step's copy, writes of the next step's at the permuted slots
+  int ua = -1, ub = 0;
+  int rd[4] = {0, 0, 0, 0}, wr[4] = {0, 0, 0, 0};
+  if (tid < NUP) {
+    const uint32_t e = L.blk[tid];
+    ua = e & 0xFF;
+    ub = e >> 8;
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        const int P = 2 * ua + x, Q = 2 * ub + y;
+        rd[2 * x + y] = tri<NR>(min(P, Q), max(P, Q));
+        const int Pn = L.sig[0][P], Qn = L.sig[0][Q];
+        wr[2 * x + y] = tri<NR>(min(Pn, Qn), max(Pn, Qn));
       }
-      __syncthreads();
-      // J restricted to a pair (p, q) is [[c, s], [-s, c]]; every entry
-      // belongs to the 2 x 2 block of exactly one thread, and a thread's
-      // blocks are disjoint: all its reads come before its writes
-      const double2 rb = rot[bb];
+  }
+  // rotations owned by wave 0: the next step's rotation j = tid comes from
+  // entry (2 X + sx, 2 Y + sy) of this thread's block and the diagonal blocks
+  // of X and Y
+  const bool owner = tid < NP;
+  int osel = 0, odx = 0, ody = 0, osx = 0, osy = 0, ox = 0, oy = 0;
+  if (owner) {
+    int X, sx, Y, sy;
+    next_source<NP>(cross, tid, X, sx, Y, sy);
+    ox = X; oy = Y; osx = sx; osy = sy;
+    osel = X == ua ? 2 * sx + sy : 2 * sy + sx;
+    odx = tri<NR>(2 * X, 2 * X);
+    ody = tri<NR>(2 * Y, 2 * Y);
+  }
+  const int vb = tid % NP, vr = 2 * (tid / NP);
+  // J^T B J of a diagonal 2 x 2 block (g00, g01, g11) by its own rotation
+  auto diag_update = [](double g00, double g01, double g11, double c, double sn, double& n00, double& n01,
+                        double& n11) {
+    const double t00 = g00 * c - g01 * sn, t01 = g00 * sn + g01 * c;
+    const double t10 = g01 * c - g11 * sn, t11 = g01 * sn + g11 * c;
+    n00 = c * t00 - sn * t10;
+    n01 = c * t01 - sn * t11;
+    n11 = sn * t01 + c * t11;
+  };
+  // the rotations of a step from its copy of G (slots 2j, 2j + 1): step 0
+  // and the steps after a change of pairing
+  auto rotations_from_g = [&](int buf) {
+    if (w == 0 && lane < NP) {
+      const double* Gc = L.Gp[buf];
+      const int o = tri<NR>(2 * lane, 2 * lane);
+      double c, sn;
+      jac_rotation(Gc[o], Gc[o + NR - 2 * lane], Gc[o + 1], c, sn);
+      L.rot[buf][lane] = double2{c, sn};
+    }
+  };
+  __syncthreads();
+  rotations_from_g(0);
+  __syncthreads();
+  const int total = max_inner * steps;
+  for (int it = 0; it < total; ++it) {
+    const int st = it % steps, cur = it & 1, nxt = cur ^ 1;
+    const bool more = it + 1 < total;
+    const bool change = NG == 4 && cross && (st & (kJB - 1)) == kJB - 1;
+    const double* Gc = L.Gp[cur];
+    double* Gn = L.Gp[nxt];
+    if (ua >= 0) {
+      const double2 ra = L.rot[cur][ua], rb = L.rot[cur][ub];
+      const double ca = ra.x, sa = ra.y, cb = rb.x, sb = rb.y;
+      int w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
+      if (change) {
+        const int c = st >> 4;
+        int Pn[2], Qn[2];
+        Pn[0] = L.sig[1 + c][2 * ua]; Pn[1] = L.sig[1 + c][2 * ua + 1];
+        Qn[0] = L.sig[1 + c][2 * ub]; Qn[1] = L.sig[1 + c][2 * ub + 1];
+        w0 = tri<NR>(min(Pn[0], Qn[0]), max(Pn[0], Qn[0]));
+        w1 = tri<NR>(min(Pn[0], Qn[1]), max(Pn[0], Qn[1]));
+        w2 = tri<NR>(min(Pn[1], Qn[0]), max(Pn[1], Qn[0]));
+        w3 = tri<NR>(min(Pn[1], Qn[1]), max(Pn[1], Qn[1]));
+      }
+      if (ua == ub) {
+        double n00, n01, n11;
+        diag_update(Gc[rd[0]], Gc[rd[1]], Gc[rd[3]], ca, sa, n00, n01, n11);
+        Gn[w0] = n00;
+        Gn[w1] = n01;
+        Gn[w3] = n11;
+      } else {
+        const double g00 = Gc[rd[0]], g01 = Gc[rd[1]], g10 = Gc[rd[2]], g11 = Gc[rd[3]];
+        const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
+        const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
+        const double n00 = ca * t00 - sa * t10, n01 = ca * t01 - sa * t11;
+        const double n10 = sa * t00 + ca * t10, n11 = sa * t01 + ca * t11;
+        Gn[w0] = n00;
+        Gn[w1] = n01;
+        Gn[w2] = n10;
+        Gn[w3] = n11;
+        if (owner && more && !change) {
+          // new diagonal entries of the two slots from the old diagonal blocks
+          const double2 rx = ox == ua ? ra : rb, ry = ox == ua ? rb : ra;
+          double x00, x01, x11, y00, y01, y11;
+          diag_update(Gc[odx], Gc[odx + 1], Gc[odx + NR - 2 * ox], rx.x, rx.y, x00, x01, x11);
+          diag_update(Gc[ody], Gc[ody + 1], Gc[ody + NR - 2 * oy], ry.x, ry.y, y00, y01, y11);
+          const double gpq = osel == 0 ? n00 : (osel == 1 ? n01 : (osel == 2 ? n10 : n11));
+          double c, sn;
+          jac_rotation(osx == 0 ? x00 : x11, osy == 0 ? y00 : y11, gpq, c, sn);
+          L.rot[nxt][tid] = double2{c, sn};
+        }
+      }
+    }
+    {
+      // V <- V J on rows vr, vr + 1 (row coordinates): columns p, q of rotation vb
+      const uint32_t e = L.pq[st][vb];
+      const int pb = e & 0xFF, qb = e >> 8;
+      const double2 rb = L.rot[cur][vb];
       const double cb = rb.x, sb = rb.y;
-      int pa[CPT], qa[CPT];
-      double ca[CPT], sa[CPT], g[CPT][4], vv[CPT][4];
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const uint32_t ea = L.pq[st][ai[i]];
-        pa[i] = ea & 0xFF;
-        qa[i] = ea >> 8;
-        const double2 ra = rot[ai[i]];
-        ca[i] = ra.x;
-        sa[i] = ra.y;
-        g[i][0] = G[pa[i]][pb]; g[i][1] = G[pa[i]][qb]; g[i][2] = G[qa[i]][pb]; g[i][3] = G[qa[i]][qb];
-        vv[i][0] = V[pa[i]][pb]; vv[i][1] = V[pa[i]][qb]; vv[i][2] = V[qa[i]][pb]; vv[i][3] = V[qa[i]][qb];
-      }
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const double t00 = g[i][0] * cb - g[i][1] * sb, t01 = g[i][0] * sb + g[i][1] * cb;
-        const double t10 = g[i][2] * cb - g[i][3] * sb, t11 = g[i][2] * sb + g[i][3] * cb;
-        G[pa[i]][pb] = ca[i] * t00 - sa[i] * t10;
-        G[pa[i]][qb] = ca[i] * t01 - sa[i] * t11;
-        G[qa[i]][pb] = sa[i] * t00 + ca[i] * t10;
-        G[qa[i]][qb] = sa[i] * t01 + ca[i] * t11;
-        V[pa[i]][pb] = vv[i][0] * cb - vv[i][1] * sb;
-        V[pa[i]][qb] = vv[i][0] * sb + vv[i][1] * cb;
-        V[qa[i]][pb] = vv[i][2] * cb - vv[i][3] * sb;
-        V[qa[i]][qb] = vv[i][2] * sb + vv[i][3] * cb;
-      }
+      const double v00 = L.V[vr][pb], v01 = L.V[vr][qb], v10 = L.V[vr + 1][pb], v11 = L.V[vr + 1][qb];
+      L.V[vr][pb] = v00 * cb - v01 * sb;
+      L.V[vr][qb] = v00 * sb + v01 * cb;
+      L.V[vr + 1][pb] = v10 * cb - v11 * sb;
+      L.V[vr + 1][qb] = v10 * sb + v11 * cb;
+    }
+    __syncthreads();
+    if (more && change) {
+      rotations_from_g(nxt);
       __syncthreads();
     }
   }
@@ -476,8 +635,8 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k;
-    vo[e] = (float)V[e / NR][e % NR];
-    vd[e] = V[e / NR][e % NR];
+    vo[e] = (float)L.V[e / NR][e % NR];
+    vd[e] = L.V[e / NR][e % NR];
   }
   if (tid == 0) skip[grp] = 0;
 }

@@ -186,8 +186,15 @@ def check_selection(run, l, mb, t, rng, extra=48):
     a = (U @ mb).cpu().numpy()                                           # k x D
     lam = np.einsum("kb,kb->k", a, v)
     # fp32 products accumulated over d and D: a bar on lambda of 1e-5 of the
-    # Cauchy-Schwarz bound |u_j^T Mbar| |v_j|
-    delta = 1e-5 * np.linalg.norm(a, axis=1) * np.linalg.norm(v, axis=1)
+    # Cauchy-Schwarz bound |u_j^T Mbar| |v_j|, plus the rounding of the fp32
+    # sums themselves, which scales with all of Mbar rather than with the
+    # column's own |u_j^T Mbar| (for a column in the noise bulk the partial
+    # sums over d carry the large singular directions): a few units of
+    # eps_32 |Mbar|_F |u_j| |v_j| / sqrt(d), the errors of the d terms adding
+    # in quadrature
+    vn = np.linalg.norm(v, axis=1)
+    fro = float(np.sqrt(float((mb ** 2).sum())))
+    delta = 1e-5 * np.linalg.norm(a, axis=1) * vn + 4 * 2.0 ** -24 * fro * vn / np.sqrt(d)
     err = np.abs(score[idx] - lam ** 2)
     bound = 2 * np.abs(lam) * delta + delta ** 2
     bad = np.nonzero(err > bound)[0]
