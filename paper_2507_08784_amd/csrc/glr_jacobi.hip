@@ -263,8 +263,8 @@ __device__ __forceinline__ void jac_rotation(double gpp, double gqq, double gpq,
 template <int NG>
 struct JacShape {
   static constexpr int NR = NG * kJB;        // rows of a group
-  static constexpr int CPT = 1;              // 2 x 2 blocks per solve thread
-  static constexpr int NT = NR * NR / 4 / CPT;   // solve threads
+  static constexpr int NP = NR / 2;          // rotations per step
+  static constexpr int NT = NG == 4 ? 512 : 256;   // solve threads
   static constexpr int NW = NT / 64;
   static constexpr int CROSS = (NG == 2 ? 1 : 3) * kJB;   // steps between blocks
 };
@@ -272,7 +272,7 @@ struct JacShape {
 // rotation j of step `step` of the circle method on NR rows (p and q in
 // either order: the rotation diagonalises the 2 x 2 block either way)
 template <int NR>
-__device__ __forceinline__ void full_pair(int step, int j, int& p, int& q) {
+__host__ __device__ constexpr void full_pair(int step, int j, int& p, int& q) {
   constexpr int last = NR - 1;
   if (j == 0) { p = step; q = last; }
   else { p = (step + j) % last; q = (step - j + last) % last; }
@@ -283,9 +283,9 @@ __device__ __forceinline__ void full_pair(int step, int j, int& p, int& q) {
 // pairing (0,1); each for the 16 steps that pair row k of one block with row
 // (k + step) mod 16 of the other
 template <int NG>
-__device__ __forceinline__ void cross_pair(int step, int j, int& p, int& q) {
+__host__ __device__ constexpr void cross_pair(int step, int j, int& p, int& q) {
   const int rho = step >> 4, k = step & (kJB - 1), half = j >> 4, kk = j & (kJB - 1);
-  int ma, mb;
+  int ma = 0, mb = 1;
   if (NG == 2 || rho == 0) { ma = half ? 2 : 0; mb = half ? 3 : 1; }
   else if (rho == 1) { ma = half ? 1 : 0; mb = half ? 3 : 2; }
   else { ma = half ? 1 : 0; mb = half ? 2 : 3; }
@@ -294,7 +294,7 @@ __device__ __forceinline__ void cross_pair(int step, int j, int& p, int& q) {
 }
 
 template <int NG>
-__device__ __forceinline__ void step_pair(bool cross, int step, int j, int& p, int& q) {
+__host__ __device__ constexpr void step_pair(bool cross, int step, int j, int& p, int& q) {
   if (cross) cross_pair<NG>(step, j, p, q);
   else full_pair<JacShape<NG>::NR>(step, j, p, q);
 }
@@ -307,42 +307,15 @@ __device__ __forceinline__ bool group_empty(const int (&blk)[NG], int nb) {
   return e;
 }
 
-// LDS of a group solve; the rotation of U^T reuses it for V - I (fp32).
-// G lives in "slot" coordinates: at every step the rows of rotation j sit in
-// slots 2j (p) and 2j + 1 (q), and only the upper triangle is stored, packed
-// by rows (two copies, read one / write the other by step parity).
-template <int NG>
-struct SolveLds {
-  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NPK = NR * (NR + 1) / 2;
-  double Gp[2][NPK];
-  double V[NR][NR + 1];              // row coordinates
-  double2 rot[2][NP];                // (c, s) of the rotations of two consecutive steps
-  double dg[NR];                     // initial diagonal (row coordinates)
-  double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
-  uint16_t pq[NR][NP];               // rows p | q << 8 of rotation j at step st
-  uint16_t blk[NP * (NP + 1) / 2];   // upper 2 x 2 block (a | b << 8) of each thread
-  uint8_t sig[4][NR];                // next slot of each slot: regular step, three pairing changes
-  uint8_t pos0[NR];                  // slot of each row at step 0
-};
-template <int NG>
-union JacLds {
-  SolveLds<NG> s;
-  float Va[JacShape<NG>::NR][JacShape<NG>::NR + 1];
-};
-
-// offset of packed upper entry (P, Q), P <= Q, of an NR x NR matrix
-template <int NR>
-__device__ __forceinline__ int tri(int P, int Q) {
-  return P * (2 * NR - P - 1) / 2 + Q;
-}
-
-// rotation j of the next step is formed from slot 2 X + sx (its p) and slot
-// 2 Y + sy (its q) of this step: the closed form of the slot permutation.
-// Circle: rows of rotation j at step s + 1 are p_{j+1}(s) and q_{j-1}(s),
-// with the ends adjusted; steps between blocks: p_j(s) and q_{j+1}(s), j + 1
-// taken within the 16 rotations of a half.
+// The group solve keeps G in "slot" coordinates: at every step the rows of
+// rotation j sit in slots 2j (p) and 2j + 1 (q), so the data of a step moves
+// to the next step's slots by a fixed permutation.  Rotation j of the next
+// step is formed from slot 2 X + sx (its p) and slot 2 Y + sy (its q) of this
+// step.  Circle: the rows of rotation j at step s + 1 are p_{j+1}(s) and
+// q_{j-1}(s), with the ends adjusted; steps between blocks: p_j(s) and
+// q_{j+1}(s), j + 1 taken within the 16 rotations of a half.
 template <int NP>
-__device__ __forceinline__ void next_source(bool cross, int j, int& X, int& sx, int& Y, int& sy) {
+__host__ __device__ constexpr void next_source(bool cross, int j, int& X, int& sx, int& Y, int& sy) {
   if (cross) {
     X = j; sx = 0; Y = (j & ~(kJB - 1)) | ((j + 1) & (kJB - 1)); sy = 1;
   } else if (j == 0) {
@@ -356,14 +329,309 @@ __device__ __forceinline__ void next_source(bool cross, int j, int& X, int& sx, 
   }
 }
 
+// Tables of a group solve, fixed by the group size and the schedule (full
+// circle or steps between blocks), formed at compile time:
+//   pq[st][j]   rows p | q << 8 of rotation j at step st
+//   pos0[row]   slot of each row at step 0
+//   sig[c][P]   next slot of slot P: c = 0 a regular step; c = 1..3 the
+//               changes of block pairing after steps 15, 31, 47 (four-block
+//               groups, steps between blocks; the last back to step 0)
+//   blk[i]      upper 2 x 2 block (a | b << 8) of work item i: first the NP
+//               blocks that hold the next step's rotations (item j makes
+//               rotation j), then the others in triangular order
+template <int NG, bool CROSS>
+struct alignas(16) JacTab {
+  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NUP = NP * (NP + 1) / 2;
+  static constexpr int STEPS = CROSS ? JacShape<NG>::CROSS : NR - 1;
+  uint16_t pq[STEPS][NP];
+  uint16_t blk[NUP];
+  uint8_t sig[4][NR];
+  uint8_t pos0[NR];
+};
+
+template <int NG, bool CROSS>
+__host__ __device__ constexpr JacTab<NG, CROSS> make_jac_tab() {
+  using T = JacTab<NG, CROSS>;
+  constexpr int NP = T::NP, STEPS = T::STEPS;
+  T t{};
+  for (int st = 0; st < STEPS; ++st)
+    for (int j = 0; j < NP; ++j) {
+      int p = 0, q = 0;
+      step_pair<NG>(CROSS, st, j, p, q);
+      t.pq[st][j] = (uint16_t)(p | (q << 8));
+    }
+  for (int j = 0; j < NP; ++j) {
+    t.pos0[t.pq[0][j] & 0xFF] = (uint8_t)(2 * j);
+    t.pos0[t.pq[0][j] >> 8] = (uint8_t)(2 * j + 1);
+    int X = 0, sx = 0, Y = 0, sy = 0;
+    next_source<NP>(CROSS, j, X, sx, Y, sy);
+    t.sig[0][2 * X + sx] = (uint8_t)(2 * j);
+    t.sig[0][2 * Y + sy] = (uint8_t)(2 * j + 1);
+  }
+  if (NG == 4 && CROSS) {
+    for (int c = 0; c < 3; ++c) {
+      const int st = kJB * c + kJB - 1, sn = (st + 1) % STEPS;
+      for (int j = 0; j < NP; ++j) {
+        const int pn = t.pq[sn][j] & 0xFF, qn = t.pq[sn][j] >> 8;
+        for (int i = 0; i < NP; ++i) {
+          const int po = t.pq[st][i] & 0xFF, qo = t.pq[st][i] >> 8;
+          if (po == pn) t.sig[1 + c][2 * i] = (uint8_t)(2 * j);
+          if (qo == pn) t.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j);
+          if (po == qn) t.sig[1 + c][2 * i] = (uint8_t)(2 * j + 1);
+          if (qo == qn) t.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j + 1);
+        }
+      }
+    }
+  }
+  int next = NP;
+  for (int a = 0; a < NP; ++a)
+    for (int b = a; b < NP; ++b) {
+      int slot = -1;
+      for (int j = 0; j < NP; ++j) {
+        int X = 0, sx = 0, Y = 0, sy = 0;
+        next_source<NP>(CROSS, j, X, sx, Y, sy);
+        if ((X < Y ? X : Y) == a && (X < Y ? Y : X) == b) slot = j;
+      }
+      if (slot < 0) slot = next++;
+      t.blk[slot] = (uint16_t)(a | (b << 8));
+    }
+  return t;
+}
+
+__constant__ JacTab<2, false> kJacTab2f = make_jac_tab<2, false>();
+__constant__ JacTab<2, true> kJacTab2c = make_jac_tab<2, true>();
+__constant__ JacTab<4, false> kJacTab4f = make_jac_tab<4, false>();
+__constant__ JacTab<4, true> kJacTab4c = make_jac_tab<4, true>();
+
+template <int NG, bool CROSS>
+__device__ __forceinline__ const JacTab<NG, CROSS>& jac_tab();
+template <>
+__device__ __forceinline__ const JacTab<2, false>& jac_tab<2, false>() { return kJacTab2f; }
+template <>
+__device__ __forceinline__ const JacTab<2, true>& jac_tab<2, true>() { return kJacTab2c; }
+template <>
+__device__ __forceinline__ const JacTab<4, false>& jac_tab<4, false>() { return kJacTab4f; }
+template <>
+__device__ __forceinline__ const JacTab<4, true>& jac_tab<4, true>() { return kJacTab4c; }
+
+// LDS of a group solve; the rotation of U^T reuses it for V - I (fp32).
+// Only the upper triangle of G is kept (two copies, read one / write the
+// other by step parity); rows have an even stride, so that the two entries
+// of a 2 x 2 block row are one 16-byte load.
+template <int NR>
+__device__ __forceinline__ int gat(int P, int Q) {
+  return P * (NR + 2) + Q;
+}
+template <int NG>
+struct SolveLds {
+  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NPK = NR * (NR + 2);
+  double Gp[2][NPK];
+  double V[NR][NR + 1];              // row coordinates
+  double2 rot[2][NP];                // (c, s) of the rotations of two consecutive steps
+  double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
+  uint32_t pq[NR * NP / 2];          // the step table (uint16 pairs)
+};
+template <int NG>
+union JacLds {
+  SolveLds<NG> s;
+  float Va[JacShape<NG>::NR][JacShape<NG>::NR + 1];
+};
+
+// One cyclic sweep over the rotations of the group, on G in slot
+// coordinates (see JacTab), V <- V J in row coordinates.  Work items: the
+// NP (NP + 1) / 2 upper 2 x 2 blocks of G and the NR / 2 x NP 2 x 2 blocks
+// of V (rows 2 i, 2 i + 1; columns of rotation j), spread over 256 threads
+// (a few per thread: four waves keep the per-step scalar work of the loop
+// small).  One barrier per step: the items that produce the entry G[p'][q']
+// of a next-step rotation (all in wave 0) also form its new diagonal entries
+// from the old diagonal blocks of its two source rotations and compute it.
+template <int NG, bool CROSS>
+__device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
+  using SH = JacShape<NG>;
+  using TB = JacTab<NG, CROSS>;
+  constexpr int NR = SH::NR, NT = SH::NT, NP = NR / 2, NUP = NP * (NP + 1) / 2, STEPS = TB::STEPS;
+  constexpr int GB = (NUP + NT - 1) / NT;           // G items per thread
+  constexpr int VB = (NR / 2) * NP / NT;            // V items per thread
+  static_assert(VB * NT == (NR / 2) * NP, "V items fill the threads");
+  const TB& tab = jac_tab<NG, CROSS>();
+  const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+  // G items: item k of thread t is k NT + t; the items of the last set (when
+  // there are several) go to the last threads, away from wave 0, which forms
+  // the rotations
+  constexpr int REM = NUP - (GB - 1) * NT;
+  int rd[GB][2], wr[GB][4], ua[GB], ub[GB];
+  bool has[GB], dia[GB];
+#pragma unroll
+  for (int k = 0; k < GB; ++k) {
+    int item = k * NT + tid;
+    has[k] = item < NUP;
+    if (GB > 1 && k == GB - 1) {
+      item = k * NT + tid - (NT - REM);
+      has[k] = tid >= NT - REM;
+    }
+    const uint32_t e = has[k] ? tab.blk[item] : 0u;
+    ua[k] = e & 0xFF;
+    ub[k] = e >> 8;
+    dia[k] = ua[k] == ub[k];
+    const int P0 = 2 * ua[k], Q0 = 2 * ub[k];
+    rd[k][0] = gat<NR>(P0, Q0);
+    rd[k][1] = dia[k] ? gat<NR>(P0 + 1, Q0 + 1) : gat<NR>(P0 + 1, Q0);
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        const int Pn = tab.sig[0][P0 + x], Qn = tab.sig[0][Q0 + y];
+        wr[k][2 * x + y] = gat<NR>(min(Pn, Qn), max(Pn, Qn));
+      }
+  }
+  // rotation formed by this thread (item tid < NP of the first set)
+  const bool owner = tid < NP;
+  int osel = 0, odx = 0, ody = 0, osx = 0, osy = 0, ox = 0;
+  if (owner) {
+    int X = 0, sx = 0, Y = 0, sy = 0;
+    next_source<NP>(CROSS, tid, X, sx, Y, sy);
+    ox = X; osx = sx; osy = sy;
+    osel = X == ua[0] ? 2 * sx + sy : 2 * sy + sx;
+    odx = gat<NR>(2 * X, 2 * X);
+    ody = gat<NR>(2 * Y, 2 * Y);
+  }
+  const int vb = tid % NP, vr0 = 2 * (tid / NP);
+  // J^T B J of a diagonal 2 x 2 block (g00, g01, g11) by its own rotation
+  auto diag_update = [](double g00, double g01, double g11, double c, double sn, double& n00, double& n01,
+                        double& n11) {
+    const double t00 = g00 * c - g01 * sn, t01 = g00 * sn + g01 * c;
+    const double t10 = g01 * c - g11 * sn, t11 = g01 * sn + g11 * c;
+    n00 = c * t00 - sn * t10;
+    n01 = c * t01 - sn * t11;
+    n11 = sn * t01 + c * t11;
+  };
+  // the rotations of a step from its copy of G (slots 2j, 2j + 1): step 0
+  // and the steps after a change of pairing
+  auto rotations_from_g = [&](int buf) {
+    if (w == 0 && lane < NP) {
+      const double* Gc = L.Gp[buf];
+      const int o = gat<NR>(2 * lane, 2 * lane);
+      double c, sn;
+      jac_rotation(Gc[o], Gc[o + NR + 3], Gc[o + 1], c, sn);
+      L.rot[buf][lane] = double2{c, sn};
+    }
+  };
+  rotations_from_g(0);
+  __syncthreads();
+  const uint16_t* pq16 = reinterpret_cast<const uint16_t*>(L.pq);
+  for (int inner = 0; inner < max_inner; ++inner) {
+    for (int st = 0; st < STEPS; ++st) {
+      const int pcur = (inner * STEPS + st) & 1, pnxt = pcur ^ 1;
+      const bool more = st + 1 < STEPS || inner + 1 < max_inner;
+      const bool change = NG == 4 && CROSS && (st & (kJB - 1)) == kJB - 1;
+      const double* Gc = L.Gp[pcur];
+      double* Gn = L.Gp[pnxt];
+      const double2* rc = L.rot[pcur];
+      // every load of the step first (the stores go to the other copy of G
+      // and to this thread's own entries of V), then the arithmetic, then the
+      // stores: one LDS round trip per step
+      double2 g0[GB], g1[GB], ra[GB], rb[GB];
+#pragma unroll
+      for (int k = 0; k < GB; ++k) {
+        if (!has[k]) continue;
+        ra[k] = rc[ua[k]];
+        rb[k] = rc[ub[k]];
+        g0[k] = *reinterpret_cast<const double2*>(Gc + rd[k][0]);
+        if (dia[k]) g1[k].y = Gc[rd[k][1]];
+        else g1[k] = *reinterpret_cast<const double2*>(Gc + rd[k][1]);
+      }
+      double dx0 = 0.0, dx1 = 0.0, dx2 = 0.0, dy0 = 0.0, dy1 = 0.0, dy2 = 0.0;
+      const bool form = owner && more && !change;
+      if (form) {
+        dx0 = Gc[odx]; dx1 = Gc[odx + 1]; dx2 = Gc[odx + NR + 3];
+        dy0 = Gc[ody]; dy1 = Gc[ody + 1]; dy2 = Gc[ody + NR + 3];
+      }
+      const uint32_t e = pq16[st * NP + vb];
+      const int pv = e & 0xFF, qv = e >> 8;
+      const double2 rv = rc[vb];
+      double vv[VB][4];
+#pragma unroll
+      for (int k = 0; k < VB; ++k) {
+        const int vr = vr0 + k * (2 * NT / NP);
+        vv[k][0] = L.V[vr][pv]; vv[k][1] = L.V[vr][qv];
+        vv[k][2] = L.V[vr + 1][pv]; vv[k][3] = L.V[vr + 1][qv];
+      }
+      double n[GB][4];
+#pragma unroll
+      for (int k = 0; k < GB; ++k) {
+        if (!has[k]) continue;
+        const double ca = ra[k].x, sa = ra[k].y, cb = rb[k].x, sb = rb[k].y;
+        if (dia[k]) {
+          diag_update(g0[k].x, g0[k].y, g1[k].y, ca, sa, n[k][0], n[k][1], n[k][3]);
+          n[k][2] = n[k][1];
+        } else {
+          const double g00 = g0[k].x, g01 = g0[k].y, g10 = g1[k].x, g11 = g1[k].y;
+          const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
+          const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
+          n[k][0] = ca * t00 - sa * t10;
+          n[k][1] = ca * t01 - sa * t11;
+          n[k][2] = sa * t00 + ca * t10;
+          n[k][3] = sa * t01 + ca * t11;
+        }
+      }
+      if (form) {
+        // new diagonal entries of the two source slots from their old
+        // diagonal blocks, and the new entry between them from item 0
+        const double2 rx = ox == ua[0] ? ra[0] : rb[0], ry = ox == ua[0] ? rb[0] : ra[0];
+        double x00, x01, x11, y00, y01, y11;
+        diag_update(dx0, dx1, dx2, rx.x, rx.y, x00, x01, x11);
+        diag_update(dy0, dy1, dy2, ry.x, ry.y, y00, y01, y11);
+        const double gpq = osel == 0 ? n[0][0] : (osel == 1 ? n[0][1] : (osel == 2 ? n[0][2] : n[0][3]));
+        double c, sn;
+        jac_rotation(osx == 0 ? x00 : x11, osy == 0 ? y00 : y11, gpq, c, sn);
+        L.rot[pnxt][tid] = double2{c, sn};
+      }
+#pragma unroll
+      for (int k = 0; k < GB; ++k) {
+        if (!has[k]) continue;
+        int w0 = wr[k][0], w1 = wr[k][1], w2 = wr[k][2], w3 = wr[k][3];
+        if (change) {
+          const int c = st >> 4;
+          const int P0 = tab.sig[1 + c][2 * ua[k]], P1 = tab.sig[1 + c][2 * ua[k] + 1];
+          const int Q0 = tab.sig[1 + c][2 * ub[k]], Q1 = tab.sig[1 + c][2 * ub[k] + 1];
+          w0 = gat<NR>(min(P0, Q0), max(P0, Q0));
+          w1 = gat<NR>(min(P0, Q1), max(P0, Q1));
+          w2 = gat<NR>(min(P1, Q0), max(P1, Q0));
+          w3 = gat<NR>(min(P1, Q1), max(P1, Q1));
+        }
+        Gn[w0] = n[k][0];
+        Gn[w1] = n[k][1];
+        if (!dia[k]) Gn[w2] = n[k][2];
+        Gn[w3] = n[k][3];
+      }
+      {
+        // V <- V J on rows (row coordinates): columns p, q of rotation vb
+        const double cb = rv.x, sb = rv.y;
+#pragma unroll
+        for (int k = 0; k < VB; ++k) {
+          const int vr = vr0 + k * (2 * NT / NP);
+          L.V[vr][pv] = vv[k][0] * cb - vv[k][1] * sb;
+          L.V[vr][qv] = vv[k][0] * sb + vv[k][1] * cb;
+          L.V[vr + 1][pv] = vv[k][2] * cb - vv[k][3] * sb;
+          L.V[vr + 1][qv] = vv[k][2] * sb + vv[k][3] * cb;
+        }
+      }
+      __syncthreads();
+      if (more && change) {
+        rotations_from_g(pnxt);
+        __syncthreads();
+      }
+    }
+  }
+}
+
 template <int NG>
 __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
                                             int seats, int nb, float tol, int max_inner, double floor_rel2,
                                             float* __restrict__ Vout, double* __restrict__ V64,
                                             int* __restrict__ skip, int grp, SolveLds<NG>& L) {
   using SH = JacShape<NG>;
-  constexpr int NR = SH::NR, NT = SH::NT, NW = SH::NW, NP = NR / 2, NUP = NP * (NP + 1) / 2;
-  static_assert(NUP <= NT, "one upper 2 x 2 block per thread");
+  constexpr int NR = SH::NR, NT = SH::NT, NW = SH::NW;
   int blk[NG];
   group_blocks<NG>(round, grp, seats, blk);
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
@@ -375,19 +643,22 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   double* redw = L.redw;
   constexpr int NE = NR * NR / NT;
   const double rm_prev = __longlong_as_double((long long)ctl->rowmax2_bits);
-  // the group's diagonal NR x NR block of A
+  // the group's diagonal NR x NR block of A; element k of this thread is
+  // (x, y) = (tid / NR + k (NT / NR), tid % NR)
   double g[NE];
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
     g[k] = pk_get(Apk, nb, blk[x / kJB], blk[y / kJB], x % kJB, y % kJB);
   }
+  // the diagonal goes through V's storage (overwritten by V = I below)
+  double* dg = &L.V[0][0];
   double dmax = 0.0;
 #pragma unroll
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
     if (x == y) {
-      L.dg[x] = g[k];
+      dg[x] = g[k];
       dmax = fmax(dmax, g[k]);
     }
   }
@@ -408,7 +679,7 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
     if (x < y) {
-      const double gxx = L.dg[x], gyy = L.dg[y];
+      const double gxx = dg[x], gyy = dg[y];
       const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
       if (den > 0.0) {
         const double q2 = (g[k] / den) * (g[k] / den);
@@ -439,197 +710,25 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
     if (tid == 0) skip[grp] = 1;
     return;
   }
-  const int steps = cross ? SH::CROSS : NR - 1;
-  // ---- tables: rows of every step; slots of step 0; slot permutations ----
-  for (int e = tid; e < steps * NP; e += NT) {
-    int p, q;
-    step_pair<NG>(cross, e / NP, e % NP, p, q);
-    L.pq[e / NP][e % NP] = (uint16_t)(p | (q << 8));
-  }
-  if (tid < NP) {
-    // regular step: slot 2 X + sx goes to 2j, slot 2 Y + sy to 2j + 1
-    int X, sx, Y, sy;
-    next_source<NP>(cross, tid, X, sx, Y, sy);
-    L.sig[0][2 * X + sx] = (uint8_t)(2 * tid);
-    L.sig[0][2 * Y + sy] = (uint8_t)(2 * tid + 1);
-  }
-  __syncthreads();
-  if (tid < NP) {
-    const uint32_t e = L.pq[0][tid];
-    L.pos0[e & 0xFF] = (uint8_t)(2 * tid);
-    L.pos0[e >> 8] = (uint8_t)(2 * tid + 1);
-  }
-  // four-block groups, steps between blocks: the block pairing changes after
-  // steps 15, 31 and 47 (the last back to the pairing of step 0)
-  if (NG == 4 && cross && tid < 3 * NP) {
-    const int c = tid / NP, j = tid % NP;
-    const int st = kJB * c + kJB - 1, sn = (st + 1) % steps;
-    const uint32_t en = L.pq[sn][j];
-    const int pn = en & 0xFF, qn = en >> 8;
-    // slots of rows pn, qn at step st
-    for (int i = 0; i < NP; ++i) {
-      const uint32_t eo = L.pq[st][i];
-      const int po = eo & 0xFF, qo = eo >> 8;
-      if (po == pn) L.sig[1 + c][2 * i] = (uint8_t)(2 * j);
-      if (qo == pn) L.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j);
-      if (po == qn) L.sig[1 + c][2 * i] = (uint8_t)(2 * j + 1);
-      if (qo == qn) L.sig[1 + c][2 * i + 1] = (uint8_t)(2 * j + 1);
-    }
-  }
-  // upper 2 x 2 block of each thread: the NP blocks that form the next step's
-  // rotations first (wave 0, so that one wave computes them), then the rest
-  // in triangular order
-  if (tid < NUP) {
-    int rem = tid, a = 0;
-    while (rem >= NP - a) {
-      rem -= NP - a;
-      ++a;
-    }
-    const int b = a + rem;
-    int slot = -1, before = 0;
-    for (int j = 0; j < NP; ++j) {
-      int X, sx, Y, sy;
-      next_source<NP>(cross, j, X, sx, Y, sy);
-      const int oa = min(X, Y), ob = max(X, Y);
-      if (oa == a && ob == b) slot = j;
-      const int oi = oa * NP - oa * (oa - 1) / 2 + (ob - oa);   // triangular index of the owner block
-      before += oi < tid ? 1 : 0;
-    }
-    if (slot < 0) slot = NP + tid - before;
-    L.blk[slot] = (uint16_t)(a | (b << 8));
-  }
-  __syncthreads();
-  // G (slot coordinates, upper, copy 0) and V = I (row coordinates)
+  // the step table into LDS; G (slot coordinates, upper, copy 0); V = I
+  {
+    const uint8_t* pos0 = cross ? jac_tab<NG, true>().pos0 : jac_tab<NG, false>().pos0;
+    const uint32_t* src = cross ? reinterpret_cast<const uint32_t*>(jac_tab<NG, true>().pq)
+                                : reinterpret_cast<const uint32_t*>(jac_tab<NG, false>().pq);
+    const int words = (cross ? JacTab<NG, true>::STEPS : JacTab<NG, false>::STEPS) * (NR / 2) / 2;
+    for (int i = tid; i < words; i += NT) L.pq[i] = src[i];
+    __syncthreads();   // dg (in V's storage) is read above by every thread
 #pragma unroll
-  for (int k = 0; k < NE; ++k) {
-    const int e = tid + NT * k, x = e / NR, y = e % NR;
-    const int P = L.pos0[x], Q = L.pos0[y];
-    if (P <= Q) L.Gp[0][tri<NR>(P, Q)] = g[k];
-    L.V[x][y] = x == y ? 1.0 : 0.0;
-  }
-  // this thread's block (a, b), a <= b, and its LDS offsets (in doubles):
-  // reads of this step's copy, writes of the next step's at the permuted slots
-  int ua = -1, ub = 0;
-  int rd[4] = {0, 0, 0, 0}, wr[4] = {0, 0, 0, 0};
-  if (tid < NUP) {
-    const uint32_t e = L.blk[tid];
-    ua = e & 0xFF;
-    ub = e >> 8;
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const int P = 2 * ua + x, Q = 2 * ub + y;
-        rd[2 * x + y] = tri<NR>(min(P, Q), max(P, Q));
-        const int Pn = L.sig[0][P], Qn = L.sig[0][Q];
-        wr[2 * x + y] = tri<NR>(min(Pn, Qn), max(Pn, Qn));
-      }
-  }
-  // rotations owned by wave 0: the next step's rotation j = tid comes from
-  // entry (2 X + sx, 2 Y + sy) of this thread's block and the diagonal blocks
-  // of X and Y
-  const bool owner = tid < NP;
-  int osel = 0, odx = 0, ody = 0, osx = 0, osy = 0, ox = 0, oy = 0;
-  if (owner) {
-    int X, sx, Y, sy;
-    next_source<NP>(cross, tid, X, sx, Y, sy);
-    ox = X; oy = Y; osx = sx; osy = sy;
-    osel = X == ua ? 2 * sx + sy : 2 * sy + sx;
-    odx = tri<NR>(2 * X, 2 * X);
-    ody = tri<NR>(2 * Y, 2 * Y);
-  }
-  const int vb = tid % NP, vr = 2 * (tid / NP);
-  // J^T B J of a diagonal 2 x 2 block (g00, g01, g11) by its own rotation
-  auto diag_update = [](double g00, double g01, double g11, double c, double sn, double& n00, double& n01,
-                        double& n11) {
-    const double t00 = g00 * c - g01 * sn, t01 = g00 * sn + g01 * c;
-    const double t10 = g01 * c - g11 * sn, t11 = g01 * sn + g11 * c;
-    n00 = c * t00 - sn * t10;
-    n01 = c * t01 - sn * t11;
-    n11 = sn * t01 + c * t11;
-  };
-  // the rotations of a step from its copy of G (slots 2j, 2j + 1): step 0
-  // and the steps after a change of pairing
-  auto rotations_from_g = [&](int buf) {
-    if (w == 0 && lane < NP) {
-      const double* Gc = L.Gp[buf];
-      const int o = tri<NR>(2 * lane, 2 * lane);
-      double c, sn;
-      jac_rotation(Gc[o], Gc[o + NR - 2 * lane], Gc[o + 1], c, sn);
-      L.rot[buf][lane] = double2{c, sn};
-    }
-  };
-  __syncthreads();
-  rotations_from_g(0);
-  __syncthreads();
-  const int total = max_inner * steps;
-  for (int it = 0; it < total; ++it) {
-    const int st = it % steps, cur = it & 1, nxt = cur ^ 1;
-    const bool more = it + 1 < total;
-    const bool change = NG == 4 && cross && (st & (kJB - 1)) == kJB - 1;
-    const double* Gc = L.Gp[cur];
-    double* Gn = L.Gp[nxt];
-    if (ua >= 0) {
-      const double2 ra = L.rot[cur][ua], rb = L.rot[cur][ub];
-      const double ca = ra.x, sa = ra.y, cb = rb.x, sb = rb.y;
-      int w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
-      if (change) {
-        const int c = st >> 4;
-        int Pn[2], Qn[2];
-        Pn[0] = L.sig[1 + c][2 * ua]; Pn[1] = L.sig[1 + c][2 * ua + 1];
-        Qn[0] = L.sig[1 + c][2 * ub]; Qn[1] = L.sig[1 + c][2 * ub + 1];
-        w0 = tri<NR>(min(Pn[0], Qn[0]), max(Pn[0], Qn[0]));
-        w1 = tri<NR>(min(Pn[0], Qn[1]), max(Pn[0], Qn[1]));
-        w2 = tri<NR>(min(Pn[1], Qn[0]), max(Pn[1], Qn[0]));
-        w3 = tri<NR>(min(Pn[1], Qn[1]), max(Pn[1], Qn[1]));
-      }
-      if (ua == ub) {
-        double n00, n01, n11;
-        diag_update(Gc[rd[0]], Gc[rd[1]], Gc[rd[3]], ca, sa, n00, n01, n11);
-        Gn[w0] = n00;
-        Gn[w1] = n01;
-        Gn[w3] = n11;
-      } else {
-        const double g00 = Gc[rd[0]], g01 = Gc[rd[1]], g10 = Gc[rd[2]], g11 = Gc[rd[3]];
-        const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
-        const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
-        const double n00 = ca * t00 - sa * t10, n01 = ca * t01 - sa * t11;
-        const double n10 = sa * t00 + ca * t10, n11 = sa * t01 + ca * t11;
-        Gn[w0] = n00;
-        Gn[w1] = n01;
-        Gn[w2] = n10;
-        Gn[w3] = n11;
-        if (owner && more && !change) {
-          // new diagonal entries of the two slots from the old diagonal blocks
-          const double2 rx = ox == ua ? ra : rb, ry = ox == ua ? rb : ra;
-          double x00, x01, x11, y00, y01, y11;
-          diag_update(Gc[odx], Gc[odx + 1], Gc[odx + NR - 2 * ox], rx.x, rx.y, x00, x01, x11);
-          diag_update(Gc[ody], Gc[ody + 1], Gc[ody + NR - 2 * oy], ry.x, ry.y, y00, y01, y11);
-          const double gpq = osel == 0 ? n00 : (osel == 1 ? n01 : (osel == 2 ? n10 : n11));
-          double c, sn;
-          jac_rotation(osx == 0 ? x00 : x11, osy == 0 ? y00 : y11, gpq, c, sn);
-          L.rot[nxt][tid] = double2{c, sn};
-        }
-      }
-    }
-    {
-      // V <- V J on rows vr, vr + 1 (row coordinates): columns p, q of rotation vb
-      const uint32_t e = L.pq[st][vb];
-      const int pb = e & 0xFF, qb = e >> 8;
-      const double2 rb = L.rot[cur][vb];
-      const double cb = rb.x, sb = rb.y;
-      const double v00 = L.V[vr][pb], v01 = L.V[vr][qb], v10 = L.V[vr + 1][pb], v11 = L.V[vr + 1][qb];
-      L.V[vr][pb] = v00 * cb - v01 * sb;
-      L.V[vr][qb] = v00 * sb + v01 * cb;
-      L.V[vr + 1][pb] = v10 * cb - v11 * sb;
-      L.V[vr + 1][qb] = v10 * sb + v11 * cb;
+    for (int k = 0; k < NE; ++k) {
+      const int e = tid + NT * k, x = e / NR, y = e % NR;
+      const int P = pos0[x], Q = pos0[y];
+      if (P <= Q) L.Gp[0][gat<NR>(P, Q)] = g[k];
+      L.V[x][y] = x == y ? 1.0 : 0.0;
     }
     __syncthreads();
-    if (more && change) {
-      rotations_from_g(nxt);
-      __syncthreads();
-    }
   }
+  if (cross) sweep_group<NG, true>(L, max_inner);
+  else sweep_group<NG, false>(L, max_inner);
   float* vo = Vout + (int64_t)grp * NR * NR;
   double* vd = V64 + (int64_t)grp * NR * NR;
 #pragma unroll
@@ -641,12 +740,9 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   if (tid == 0) skip[grp] = 0;
 }
 
-// columns of U^T rotated by one workgroup of the given width: 512 for 256
-// threads; the 1024-thread workgroups beside the solves of four-block groups
-// take 1024, so that the solves and all the rotation workgroups of a round
-// are resident together
+// columns of U^T rotated by one workgroup of 256 threads (in proportion for
+// the larger workgroups beside the solves of four-block groups)
 constexpr int JAC_CHUNK = 512;
-constexpr int JAC_CHUNK_WIDE = 1024;
 
 // rows of the group in U^T <- V^T rows on this block's chunk, computed as
 // w + (V - I)^T w (fp32 MFMA, NR / 32 output tiles of 32 rows, K = NR).  The
@@ -727,12 +823,11 @@ __device__ __forceinline__ void apply_chunk(float* __restrict__ Utw, int64_t d, 
 // by exactly one workgroup.  A group whose V is the identity skips its
 // product.
 template <int NG>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
-k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int* __restrict__ skip,
-             const JacCtl* __restrict__ ctl, int round, int seats, int nb, int groups) {
+__device__ __forceinline__ void update_pair(double* __restrict__ Apk, const double* __restrict__ V64,
+                                            const int* __restrict__ skip, int round, int seats, int nb, int groups,
+                                            int bid, double (*S)[JacShape<NG>::NR + 1]) {
   constexpr int NR = JacShape<NG>::NR, TW = NR / 32;   // 16 x 16 tiles per quadrant side
-  if (ctl->converged) return;
-  int g = 0, rem = blockIdx.x;
+  int g = 0, rem = bid;
   while (rem >= groups - g) {
     rem -= groups - g;
     ++g;
@@ -743,7 +838,6 @@ k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int
   int bg[NG], bh[NG];
   group_blocks<NG>(round, g, seats, bg);
   group_blocks<NG>(round, h, seats, bh);
-  __shared__ double S[NR][NR + 1];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const int er = tid / kJB, ec = tid % kJB;
   const int R0 = (w >> 1) * (NR / 2), C0 = (w & 1) * (NR / 2), li = lane & 15, lk = lane >> 4;
@@ -841,6 +935,16 @@ k_jac_solve(const double* __restrict__ Apk, JacCtl* __restrict__ ctl, int round,
   solve_group<NG>(Apk, ctl, round, seats, nb, tol, max_inner, floor_rel2, Vout, V64, skip, blockIdx.x, lds);
 }
 
+// A <- J^T A J over all pairs of groups
+template <int NG>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+k_jac_update(double* __restrict__ Apk, const double* __restrict__ V64, const int* __restrict__ skip,
+             const JacCtl* __restrict__ ctl, int round, int seats, int nb, int groups) {
+  if (ctl->converged) return;
+  __shared__ double S[JacShape<NG>::NR][JacShape<NG>::NR + 1];
+  update_pair<NG>(Apk, V64, skip, round, seats, nb, groups, blockIdx.x, S);
+}
+
 // the group solves of round `round` (workgroups [0, groups)) together with
 // the rotation of U^T rows by the previous round's V (the rest): the rotation
 // does not depend on the new solves, and the solves leave most of the chip idle
@@ -900,7 +1004,7 @@ template <int NG>
 static hipError_t solve_apply_ng(const MatView& v, int round, float tol, int max_inner, double floor_rel2,
                                  hipStream_t s) {
   const int nb = jac_blocks(v.d), groups = jac_groups(v.d), seats = jac_seats(v.d);
-  const int width = NG == 4 ? JAC_CHUNK_WIDE : JAC_CHUNK;
+  const int width = JAC_CHUNK * JacShape<NG>::NT / 256;
   const int chunks = (int)((v.d + width - 1) / width);
   const RoundBufs rb = round_bufs(v, round), pb = round_bufs(v, round - 1);
   hipLaunchKernelGGL(k_jac_solve_apply<NG>, dim3((unsigned)(groups + groups * chunks)), dim3(JacShape<NG>::NT),
