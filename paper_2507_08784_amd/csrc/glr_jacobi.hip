@@ -336,18 +336,39 @@ __host__ __device__ constexpr void next_source(bool cross, int j, int& X, int& s
 //   sig[c][P]   next slot of slot P: c = 0 a regular step; c = 1..3 the
 //               changes of block pairing after steps 15, 31, 47 (four-block
 //               groups, steps between blocks; the last back to step 0)
-//   blk[i]      upper 2 x 2 block (a | b << 8) of work item i: first the NP
-//               blocks that hold the next step's rotations (item j makes
-//               rotation j), then the others in triangular order
+//   blk[i]      off-diagonal 2 x 2 block (a | b << 8, a < b) of work item i:
+//               first the NP blocks that hold the next step's rotations (item
+//               j makes rotation j), then the others in triangular order
+//   dsel[j]     which source of rotation j (0: X, 1: Y) has its diagonal 2 x 2
+//               block updated by item j (each diagonal block by one item)
 template <int NG, bool CROSS>
 struct alignas(16) JacTab {
-  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NUP = NP * (NP + 1) / 2;
+  static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NOFF = NP * (NP - 1) / 2;
   static constexpr int STEPS = CROSS ? JacShape<NG>::CROSS : NR - 1;
   uint16_t pq[STEPS][NP];
-  uint16_t blk[NUP];
+  uint16_t blk[NOFF];
   uint8_t sig[4][NR];
   uint8_t pos0[NR];
+  uint8_t dsel[NP];
 };
+
+// augmenting path for the matching of rotations j to their source pairs
+template <int NP>
+__host__ __device__ constexpr bool jt_augment(bool cross, int j, int* match, bool* seen) {
+  int X = 0, sx = 0, Y = 0, sy = 0;
+  next_source<NP>(cross, j, X, sx, Y, sy);
+  const int cand[2] = {X, Y};
+  for (int c = 0; c < 2; ++c) {
+    const int a = cand[c];
+    if (seen[a]) continue;
+    seen[a] = true;
+    if (match[a] < 0 || jt_augment<NP>(cross, match[a], match, seen)) {
+      match[a] = j;
+      return true;
+    }
+  }
+  return false;
+}
 
 template <int NG, bool CROSS>
 __host__ __device__ constexpr JacTab<NG, CROSS> make_jac_tab() {
@@ -385,7 +406,7 @@ __host__ __device__ constexpr JacTab<NG, CROSS> make_jac_tab() {
   }
   int next = NP;
   for (int a = 0; a < NP; ++a)
-    for (int b = a; b < NP; ++b) {
+    for (int b = a + 1; b < NP; ++b) {
       int slot = -1;
       for (int j = 0; j < NP; ++j) {
         int X = 0, sx = 0, Y = 0, sy = 0;
@@ -395,6 +416,20 @@ __host__ __device__ constexpr JacTab<NG, CROSS> make_jac_tab() {
       if (slot < 0) slot = next++;
       t.blk[slot] = (uint16_t)(a | (b << 8));
     }
+  // every pair is a source of exactly two rotations: a perfect matching of
+  // rotations to pairs exists (the sources form even cycles)
+  int match[NP] = {};
+  for (int a = 0; a < NP; ++a) match[a] = -1;
+  for (int j = 0; j < NP; ++j) {
+    bool seen[NP] = {};
+    jt_augment<NP>(CROSS, j, match, seen);
+  }
+  for (int a = 0; a < NP; ++a) {
+    const int j = match[a];
+    int X = 0, sx = 0, Y = 0, sy = 0;
+    next_source<NP>(CROSS, j, X, sx, Y, sy);
+    t.dsel[j] = (uint8_t)(a == X ? 0 : 1);
+  }
   return t;
 }
 
@@ -425,9 +460,12 @@ __device__ __forceinline__ int gat(int P, int Q) {
 template <int NG>
 struct SolveLds {
   static constexpr int NR = JacShape<NG>::NR, NP = NR / 2, NPK = NR * (NR + 2);
-  double Gp[2][NPK];
+  // past the matrix: a place for the stores of lanes without a block
+  static constexpr int NDUM = 4 * (JacShape<NG>::NT - NP * (NP - 1) / 2 + 64);
+  double Gp[2][NPK + NDUM];
   double V[NR][NR + 1];              // row coordinates
-  double2 rot[2][NP];                // (c, s) of the rotations of two consecutive steps
+  double2 rot[2][64];                // (c, s) of the rotations of two consecutive steps (lanes
+                                     // NP.. of wave 0 store theirs past the real ones)
   double red[JacShape<NG>::NW], redw[JacShape<NG>::NW];
   uint32_t pq[NR * NP / 2];          // the step table (uint16 pairs)
 };
@@ -449,52 +487,49 @@ template <int NG, bool CROSS>
 __device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
   using SH = JacShape<NG>;
   using TB = JacTab<NG, CROSS>;
-  constexpr int NR = SH::NR, NT = SH::NT, NP = NR / 2, NUP = NP * (NP + 1) / 2, STEPS = TB::STEPS;
-  constexpr int GB = (NUP + NT - 1) / NT;           // G items per thread
+  constexpr int NR = SH::NR, NT = SH::NT, NP = NR / 2, NOFF = NP * (NP - 1) / 2, STEPS = TB::STEPS;
+  constexpr int NPK = SolveLds<NG>::NPK;
   constexpr int VB = (NR / 2) * NP / NT;            // V items per thread
-  static_assert(VB * NT == (NR / 2) * NP, "V items fill the threads");
+  static_assert(NOFF <= NT && VB * NT == (NR / 2) * NP, "one G item, whole V items per thread");
   const TB& tab = jac_tab<NG, CROSS>();
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-  // G items: item k of thread t is k NT + t; the items of the last set (when
-  // there are several) go to the last threads, away from wave 0, which forms
-  // the rotations
-  constexpr int REM = NUP - (GB - 1) * NT;
-  int rd[GB][2], wr[GB][4], ua[GB], ub[GB];
-  bool has[GB], dia[GB];
-#pragma unroll
-  for (int k = 0; k < GB; ++k) {
-    int item = k * NT + tid;
-    has[k] = item < NUP;
-    if (GB > 1 && k == GB - 1) {
-      item = k * NT + tid - (NT - REM);
-      has[k] = tid >= NT - REM;
-    }
-    const uint32_t e = has[k] ? tab.blk[item] : 0u;
-    ua[k] = e & 0xFF;
-    ub[k] = e >> 8;
-    dia[k] = ua[k] == ub[k];
-    const int P0 = 2 * ua[k], Q0 = 2 * ub[k];
-    rd[k][0] = gat<NR>(P0, Q0);
-    rd[k][1] = dia[k] ? gat<NR>(P0 + 1, Q0 + 1) : gat<NR>(P0 + 1, Q0);
+  // this thread's off-diagonal 2 x 2 block (a, b), a < b, of G: the LDS
+  // offsets of its two rows now and of its four entries at the next step
+  // (threads without a block read block 0 and store into the dummy slots)
+  const bool has = tid < NOFF;
+  const uint32_t be = tab.blk[has ? tid : 0];
+  const int ua = be & 0xFF, ub = be >> 8;
+  const int rd0 = gat<NR>(2 * ua, 2 * ub), rd1 = gat<NR>(2 * ua + 1, 2 * ub);
+  auto dest4 = [&](const uint8_t* sg, int (&wo)[4]) {
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
       for (int y = 0; y < 2; ++y) {
-        const int Pn = tab.sig[0][P0 + x], Qn = tab.sig[0][Q0 + y];
-        wr[k][2 * x + y] = gat<NR>(min(Pn, Qn), max(Pn, Qn));
+        const int Pn = sg[2 * ua + x], Qn = sg[2 * ub + y];
+        wo[2 * x + y] = has ? gat<NR>(min(Pn, Qn), max(Pn, Qn)) : NPK + 4 * (tid - NOFF) + 2 * x + y;
       }
-  }
-  // rotation formed by this thread (item tid < NP of the first set)
-  const bool owner = tid < NP;
-  int osel = 0, odx = 0, ody = 0, osx = 0, osy = 0, ox = 0;
-  if (owner) {
-    int X = 0, sx = 0, Y = 0, sy = 0;
-    next_source<NP>(CROSS, tid, X, sx, Y, sy);
-    ox = X; osx = sx; osy = sy;
-    osel = X == ua[0] ? 2 * sx + sy : 2 * sy + sx;
-    odx = gat<NR>(2 * X, 2 * X);
-    ody = gat<NR>(2 * Y, 2 * Y);
-  }
+  };
+  int wr[4];
+  dest4(tab.sig[0], wr);
+  // wave 0: lane j < NP forms rotation j of the next step from entry (2 X +
+  // sx, 2 Y + sy) of its block and the diagonal blocks of X and Y, and
+  // stores the new diagonal block of one of them (dsel); the other lanes
+  // repeat lane 0's work into the dummy slots
+  const int oj = lane < NP ? lane : 0;
+  int ox = 0, osx = 0, oy = 0, osy = 0;
+  next_source<NP>(CROSS, oj, ox, osx, oy, osy);
+  const int osel = ox == ua ? 2 * osx + osy : 2 * osy + osx;
+  const int odx = gat<NR>(2 * ox, 2 * ox), ody = gat<NR>(2 * oy, 2 * oy);
+  const int dsel = tab.dsel[oj], dp = dsel == 0 ? ox : oy;
+  const bool ownr = w == 0 && lane < NP;
+  auto dest3 = [&](const uint8_t* sg, int (&wo)[3]) {
+    const int Pn = sg[2 * dp], Qn = sg[2 * dp + 1];
+    wo[0] = ownr ? gat<NR>(Pn, Pn) : NPK + 4 * (NT - NOFF + lane);
+    wo[1] = ownr ? gat<NR>(min(Pn, Qn), max(Pn, Qn)) : NPK + 4 * (NT - NOFF + lane) + 1;
+    wo[2] = ownr ? gat<NR>(Qn, Qn) : NPK + 4 * (NT - NOFF + lane) + 2;
+  };
+  int wd[3];
+  dest3(tab.sig[0], wd);
   const int vb = tid % NP, vr0 = 2 * (tid / NP);
   // J^T B J of a diagonal 2 x 2 block (g00, g01, g11) by its own rotation
   auto diag_update = [](double g00, double g01, double g11, double c, double sn, double& n00, double& n01,
@@ -530,22 +565,9 @@ __device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
       // every load of the step first (the stores go to the other copy of G
       // and to this thread's own entries of V), then the arithmetic, then the
       // stores: one LDS round trip per step
-      double2 g0[GB], g1[GB], ra[GB], rb[GB];
-#pragma unroll
-      for (int k = 0; k < GB; ++k) {
-        if (!has[k]) continue;
-        ra[k] = rc[ua[k]];
-        rb[k] = rc[ub[k]];
-        g0[k] = *reinterpret_cast<const double2*>(Gc + rd[k][0]);
-        if (dia[k]) g1[k].y = Gc[rd[k][1]];
-        else g1[k] = *reinterpret_cast<const double2*>(Gc + rd[k][1]);
-      }
-      double dx0 = 0.0, dx1 = 0.0, dx2 = 0.0, dy0 = 0.0, dy1 = 0.0, dy2 = 0.0;
-      const bool form = owner && more && !change;
-      if (form) {
-        dx0 = Gc[odx]; dx1 = Gc[odx + 1]; dx2 = Gc[odx + NR + 3];
-        dy0 = Gc[ody]; dy1 = Gc[ody + 1]; dy2 = Gc[ody + NR + 3];
-      }
+      const double2 ra = rc[ua], rb = rc[ub];
+      const double2 g0 = *reinterpret_cast<const double2*>(Gc + rd0);
+      const double2 g1 = *reinterpret_cast<const double2*>(Gc + rd1);
       const uint32_t e = pq16[st * NP + vb];
       const int pv = e & 0xFF, qv = e >> 8;
       const double2 rv = rc[vb];
@@ -556,70 +578,56 @@ __device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
         vv[k][0] = L.V[vr][pv]; vv[k][1] = L.V[vr][qv];
         vv[k][2] = L.V[vr + 1][pv]; vv[k][3] = L.V[vr + 1][qv];
       }
-      double n[GB][4];
-#pragma unroll
-      for (int k = 0; k < GB; ++k) {
-        if (!has[k]) continue;
-        const double ca = ra[k].x, sa = ra[k].y, cb = rb[k].x, sb = rb[k].y;
-        if (dia[k]) {
-          diag_update(g0[k].x, g0[k].y, g1[k].y, ca, sa, n[k][0], n[k][1], n[k][3]);
-          n[k][2] = n[k][1];
-        } else {
-          const double g00 = g0[k].x, g01 = g0[k].y, g10 = g1[k].x, g11 = g1[k].y;
-          const double t00 = g00 * cb - g01 * sb, t01 = g00 * sb + g01 * cb;
-          const double t10 = g10 * cb - g11 * sb, t11 = g10 * sb + g11 * cb;
-          n[k][0] = ca * t00 - sa * t10;
-          n[k][1] = ca * t01 - sa * t11;
-          n[k][2] = sa * t00 + ca * t10;
-          n[k][3] = sa * t01 + ca * t11;
-        }
+      if (change) {
+        const uint8_t* sg = tab.sig[1 + (st >> 4)];
+        dest4(sg, wr);
+        dest3(sg, wd);
       }
-      if (form) {
-        // new diagonal entries of the two source slots from their old
-        // diagonal blocks, and the new entry between them from item 0
-        const double2 rx = ox == ua[0] ? ra[0] : rb[0], ry = ox == ua[0] ? rb[0] : ra[0];
+      // off-diagonal block: G <- J_a^T G J_b
+      const double ca = ra.x, sa = ra.y, cb = rb.x, sb = rb.y;
+      const double t00 = g0.x * cb - g0.y * sb, t01 = g0.x * sb + g0.y * cb;
+      const double t10 = g1.x * cb - g1.y * sb, t11 = g1.x * sb + g1.y * cb;
+      const double n00 = ca * t00 - sa * t10, n01 = ca * t01 - sa * t11;
+      const double n10 = sa * t00 + ca * t10, n11 = sa * t01 + ca * t11;
+      if (w == 0) {
+        const double dx0 = Gc[odx], dx1 = Gc[odx + 1], dx2 = Gc[odx + NR + 3];
+        const double dy0 = Gc[ody], dy1 = Gc[ody + 1], dy2 = Gc[ody + NR + 3];
+        const double2 rx = ox == ua ? ra : rb, ry = ox == ua ? rb : ra;
         double x00, x01, x11, y00, y01, y11;
         diag_update(dx0, dx1, dx2, rx.x, rx.y, x00, x01, x11);
         diag_update(dy0, dy1, dy2, ry.x, ry.y, y00, y01, y11);
-        const double gpq = osel == 0 ? n[0][0] : (osel == 1 ? n[0][1] : (osel == 2 ? n[0][2] : n[0][3]));
-        double c, sn;
-        jac_rotation(osx == 0 ? x00 : x11, osy == 0 ? y00 : y11, gpq, c, sn);
-        L.rot[pnxt][tid] = double2{c, sn};
-      }
-#pragma unroll
-      for (int k = 0; k < GB; ++k) {
-        if (!has[k]) continue;
-        int w0 = wr[k][0], w1 = wr[k][1], w2 = wr[k][2], w3 = wr[k][3];
-        if (change) {
-          const int c = st >> 4;
-          const int P0 = tab.sig[1 + c][2 * ua[k]], P1 = tab.sig[1 + c][2 * ua[k] + 1];
-          const int Q0 = tab.sig[1 + c][2 * ub[k]], Q1 = tab.sig[1 + c][2 * ub[k] + 1];
-          w0 = gat<NR>(min(P0, Q0), max(P0, Q0));
-          w1 = gat<NR>(min(P0, Q1), max(P0, Q1));
-          w2 = gat<NR>(min(P1, Q0), max(P1, Q0));
-          w3 = gat<NR>(min(P1, Q1), max(P1, Q1));
+        if (more && !change) {
+          const double gpq = osel == 0 ? n00 : (osel == 1 ? n01 : (osel == 2 ? n10 : n11));
+          double c, sn;
+          jac_rotation(osx == 0 ? x00 : x11, osy == 0 ? y00 : y11, gpq, c, sn);
+          L.rot[pnxt][lane] = double2{c, sn};
         }
-        Gn[w0] = n[k][0];
-        Gn[w1] = n[k][1];
-        if (!dia[k]) Gn[w2] = n[k][2];
-        Gn[w3] = n[k][3];
+        Gn[wd[0]] = dsel == 0 ? x00 : y00;
+        Gn[wd[1]] = dsel == 0 ? x01 : y01;
+        Gn[wd[2]] = dsel == 0 ? x11 : y11;
       }
+      Gn[wr[0]] = n00;
+      Gn[wr[1]] = n01;
+      Gn[wr[2]] = n10;
+      Gn[wr[3]] = n11;
       {
         // V <- V J on rows (row coordinates): columns p, q of rotation vb
-        const double cb = rv.x, sb = rv.y;
+        const double cv = rv.x, sv = rv.y;
 #pragma unroll
         for (int k = 0; k < VB; ++k) {
           const int vr = vr0 + k * (2 * NT / NP);
-          L.V[vr][pv] = vv[k][0] * cb - vv[k][1] * sb;
-          L.V[vr][qv] = vv[k][0] * sb + vv[k][1] * cb;
-          L.V[vr + 1][pv] = vv[k][2] * cb - vv[k][3] * sb;
-          L.V[vr + 1][qv] = vv[k][2] * sb + vv[k][3] * cb;
+          L.V[vr][pv] = vv[k][0] * cv - vv[k][1] * sv;
+          L.V[vr][qv] = vv[k][0] * sv + vv[k][1] * cv;
+          L.V[vr + 1][pv] = vv[k][2] * cv - vv[k][3] * sv;
+          L.V[vr + 1][qv] = vv[k][2] * sv + vv[k][3] * cv;
         }
       }
       __syncthreads();
       if (more && change) {
         rotations_from_g(pnxt);
         __syncthreads();
+        dest4(tab.sig[0], wr);
+        dest3(tab.sig[0], wd);
       }
     }
   }
