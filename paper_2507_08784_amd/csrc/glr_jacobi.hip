@@ -237,27 +237,25 @@ __device__ __forceinline__ double pk_get(const double* __restrict__ Apk, int nb,
 // the other waves apply the previous step's rotations to V.
 // Rotation J = [[c, s], [-s, c]] that diagonalises [[gpp, gpq], [gpq, gqq]]:
 // t = tan(theta) = sign(d h) |h| / (|d| + sqrt(d^2 + h^2)), d = gqq - gpp,
-// h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  d and h are first scaled by a
-// power of two (exact) so that t can be formed in fp32; c then comes from an
-// fp32 estimate of 1 / sqrt(1 + t^2) refined by one Newton step in fp64, so
-// that c^2 + s^2 = 1 to ~1e-14 for the t used.  An fp32 angle leaves an
-// off-diagonal entry ~1e-7 of the one it removes, which the next sweeps take.
+// h = 2 gpq, c = 1 / sqrt(1 + t^2), s = c t.  t comes from the hardware fp64
+// square root and reciprocal (approximations: an inexact angle only leaves a
+// small share of the entry it removes for the next sweeps); c from the
+// hardware reciprocal square root refined by one Newton step, so that
+// c^2 + s^2 = 1 to ~1e-15 for the t used.  Gram entries of fp32 data stay far
+// inside the fp64 range, so d^2 + h^2 needs no scaling.  No rotation (c = 1,
+// s = 0) when gpq is zero or negligible against sqrt(gpp gqq); the choice is
+// a select, so that a wave forming rotations does not branch.
 __device__ __forceinline__ void jac_rotation(double gpp, double gqq, double gpq, double& c, double& s) {
-  c = 1.0;
-  s = 0.0;
-  if (gpq == 0.0 || gpq * gpq <= 1e-34 * (gpp * gqq)) return;
-  const double d0 = gqq - gpp, h0 = 2.0 * gpq;
-  int ex;
-  (void)frexp(fmax(fabs(d0), fabs(h0)), &ex);
-  const float dd = (float)ldexp(d0, -ex), h = (float)ldexp(h0, -ex);   // max(|dd|, |h|) in [0.5, 1)
-  const float r = __builtin_amdgcn_sqrtf(dd * dd + h * h);
-  const float tf = fabsf(h) * __builtin_amdgcn_rcpf(fabsf(dd) + r);
-  const double t = ((dd < 0.0f) != (h < 0.0f)) ? -(double)tf : (double)tf;
-  const double z = 1.0 + t * t;
-  double y = (double)__builtin_amdgcn_rsqf((float)z);
-  y = y * (1.5 - 0.5 * z * y * y);                        // 1 / sqrt(z)
-  c = y;
-  s = y * t;
+  const double d = gqq - gpp, h = 2.0 * gpq;
+  const double r = __builtin_amdgcn_sqrt(fma(d, d, h * h));
+  const double tm = fabs(h) * __builtin_amdgcn_rcp(fabs(d) + r);
+  const double t = ((d < 0.0) != (h < 0.0)) ? -tm : tm;
+  const double z = fma(t, t, 1.0);
+  double y = __builtin_amdgcn_rsq(z);
+  y = y * fma(-0.5 * z, y * y, 1.5);                     // 1 / sqrt(z)
+  const bool none = gpq == 0.0 || gpq * gpq <= 1e-34 * (gpp * gqq);
+  c = none ? 1.0 : y;
+  s = none ? 0.0 : y * t;
 }
 
 template <int NG>
@@ -568,6 +566,11 @@ __device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
       const double2 ra = rc[ua], rb = rc[ub];
       const double2 g0 = *reinterpret_cast<const double2*>(Gc + rd0);
       const double2 g1 = *reinterpret_cast<const double2*>(Gc + rd1);
+      double dx0 = 0.0, dx1 = 0.0, dx2 = 0.0, dy0 = 0.0, dy1 = 0.0, dy2 = 0.0;
+      if (w == 0) {
+        dx0 = Gc[odx]; dx1 = Gc[odx + 1]; dx2 = Gc[odx + NR + 3];
+        dy0 = Gc[ody]; dy1 = Gc[ody + 1]; dy2 = Gc[ody + NR + 3];
+      }
       const uint32_t e = pq16[st * NP + vb];
       const int pv = e & 0xFF, qv = e >> 8;
       const double2 rv = rc[vb];
@@ -590,8 +593,6 @@ __device__ __forceinline__ void sweep_group(SolveLds<NG>& L, int max_inner) {
       const double n00 = ca * t00 - sa * t10, n01 = ca * t01 - sa * t11;
       const double n10 = sa * t00 + ca * t10, n11 = sa * t01 + ca * t11;
       if (w == 0) {
-        const double dx0 = Gc[odx], dx1 = Gc[odx + 1], dx2 = Gc[odx + NR + 3];
-        const double dy0 = Gc[ody], dy1 = Gc[ody + 1], dy2 = Gc[ody + NR + 3];
         const double2 rx = ox == ua ? ra : rb, ry = ox == ua ? rb : ra;
         double x00, x01, x11, y00, y01, y11;
         diag_update(dx0, dx1, dx2, rx.x, rx.y, x00, x01, x11);
