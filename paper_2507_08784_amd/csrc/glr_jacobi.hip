@@ -1112,23 +1112,38 @@ __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict
   }
 }
 
-// A' = P A P^T (packed) for the row permutation perm, and U^T' = P U^T
+// A' = P A P^T (packed) for the row permutation perm, and U^T' = P U^T.
+// A random gather of 8-byte entries: each thread takes the same entry of
+// kPermBlocks consecutive stored blocks, issuing all its loads before its
+// stores, so that many loads are in flight per thread.
+constexpr int kPermBlocks = 8;
 __global__ void __launch_bounds__(256)
 k_pk_permute(const double* __restrict__ A, double* __restrict__ B, const int* __restrict__ perm, int64_t d,
              int nb) {
-  // one workgroup per stored block (a, b), a <= b; one thread per entry
-  int64_t blk = blockIdx.x;
-  int a = 0;
-  while (blk >= nb - a) { blk -= nb - a; ++a; }
-  const int b = a + (int)blk;
+  const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
   const int r = threadIdx.x / kJB, c = threadIdx.x % kJB;
-  const int64_t i = (int64_t)a * kJB + r, j = (int64_t)b * kJB + c;
-  double x = 0.0;
-  if (i < d && j < d) {
-    const int pi = perm[i], pj = perm[j];
-    x = pk_get(A, nb, pi / kJB, pj / kJB, pi % kJB, pj % kJB);
+  const int64_t first = (int64_t)blockIdx.x * kPermBlocks;
+  // (a, b) of the first block, then walk along the packed order
+  int64_t blk = first;
+  int a = 0;
+  while (a < nb && blk >= nb - a) { blk -= nb - a; ++a; }
+  int b = a + (int)blk;
+  double x[kPermBlocks];
+#pragma unroll
+  for (int q = 0; q < kPermBlocks; ++q) {
+    x[q] = 0.0;
+    if (first + q < nblk) {
+      const int64_t i = (int64_t)a * kJB + r, j = (int64_t)b * kJB + c;
+      if (i < d && j < d) {
+        const int pi = perm[i], pj = perm[j];
+        x[q] = pk_get(A, nb, pi / kJB, pj / kJB, pi % kJB, pj % kJB);
+      }
+      if (++b == nb) { ++a; b = a; }
+    }
   }
-  B[pk_off(a, b, nb) + threadIdx.x] = x;
+#pragma unroll
+  for (int q = 0; q < kPermBlocks; ++q)
+    if (first + q < nblk) B[(first + q) * (kJB * kJB) + threadIdx.x] = x[q];
 }
 
 __global__ void k_row_gather(const float* __restrict__ src, float* __restrict__ dst, const int* __restrict__ perm,
@@ -1145,8 +1160,9 @@ hipError_t launch_jac_sort(const MatView& v, hipStream_t s) {
   int n_pad = 2;
   while (n_pad < v.d) n_pad <<= 1;
   hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d, n_pad, v.perm);
-  hipLaunchKernelGGL(k_pk_permute, dim3((unsigned)(nb * (nb + 1) / 2)), dim3(256), 0, s, v.Apk, v.Apk2, v.perm,
-                     v.d, nb);
+  const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
+  hipLaunchKernelGGL(k_pk_permute, dim3((unsigned)((nblk + kPermBlocks - 1) / kPermBlocks)), dim3(256), 0, s, v.Apk,
+                     v.Apk2, v.perm, v.d, nb);
   hipLaunchKernelGGL(k_row_gather, dim3((unsigned)v.d), dim3(256), 0, s, v.Utw, v.W, v.perm, v.d);
   return hipGetLastError();
 }
