@@ -147,7 +147,9 @@ static int grid_n(int64_t n) {
 // contraction into slices of kslice.
 //   EPI 0: slice z of C (fp64) at out64 + z M ldo (tiles below the block
 //          diagonal skipped: only the upper blocks of a symmetric C are read)
-//   EPI 1: out32 = (C - I) / 2 (one slice): the Newton-Schulz correction
+//   EPI 1: out32 = (C - I) / 2 (one slice): the Newton-Schulz correction;
+//          A = B and C symmetric: the upper tiles only, each entry written
+//          to (i, j) and (j, i)
 //   EPI 2: C packed by 16 x 16 blocks (a <= b) at out64 (one slice), ldo = nb
 // ---------------------------------------------------------------------------
 template <int EPI>
@@ -158,7 +160,7 @@ k_gram64(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, 
   __shared__ float Bs[32][65];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
-  if (EPI != 1 && m0 >= n0 + 64) return;
+  if (m0 >= n0 + 64) return;
   const int k0 = blockIdx.z * kslice;
   const int k1 = Kc < k0 + kslice ? Kc : k0 + kslice;
   const int lr = tid >> 2, kq = (tid & 3) * 8;     // loader: row, k offset
@@ -213,7 +215,10 @@ k_gram64(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, 
         if (EPI == 0) {
           out64[((int64_t)blockIdx.z * M + i) * ldo + j] = acc[x][y][v];
         } else if (EPI == 1) {
-          out32[(int64_t)i * ldo + j] = (float)(0.5 * (acc[x][y][v] - (i == j ? 1.0 : 0.0)));
+          if (i > j) continue;   // the mirror of (j, i), written by that entry
+          const float c = (float)(0.5 * (acc[x][y][v] - (i == j ? 1.0 : 0.0)));
+          out32[(int64_t)i * ldo + j] = c;
+          out32[(int64_t)j * ldo + i] = c;
         } else if (i / kJB <= j / kJB) {
           out64[pk_off(i / kJB, j / kJB, (int)ldo) + (i % kJB) * kJB + (j % kJB)] = acc[x][y][v];
         }
