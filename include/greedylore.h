@@ -30,12 +30,22 @@
  * Memory ownership.  The caller owns every device buffer: the weights X, the
  * gradients G, the state blob and the workspace.  The library never allocates
  * device memory and never frees caller memory; the handle holds host metadata
- * only.  Device pointers must be 256-byte aligned and must not alias.
+ * and, with more than one matrix, up to four HIP streams and their events.
+ * Device pointers must be 256-byte aligned and must not alias.
  *
  * Streams.  `stream` arguments are hipStream_t values passed as void*; NULL is
- * the default stream.  glr_step enqueues its kernels on the stream; it blocks
- * the host only on refresh steps, where it reads the convergence flag of the
- * Jacobi sweeps (one 4-byte read per sweep).
+ * the default stream.  glr_step orders its work after what is already on the
+ * stream and before what the caller enqueues next.  With one matrix it
+ * enqueues its kernels on the stream itself.  With several, the matrices are
+ * spread over up to four non-blocking streams of the handle (created by
+ * glr_create, destroyed by glr_destroy), each with its own copy of the
+ * workspace scratch and its own host thread inside glr_step, forked from and
+ * joined back to `stream` with events; every matrix computes exactly what it
+ * computes alone (results are bitwise those of running the matrices in order).
+ * While profiling is enabled the matrices run in order on `stream`.  The
+ * environment variable GLR_LANES, read by glr_create, lowers the stream count.
+ * glr_step blocks the host only on refresh steps, where it reads the
+ * convergence flag of the Jacobi sweeps (one 4-byte read per sweep).
  *
  * Errors.  Every function returns a glr_status and never throws or aborts
  * across the ABI.  Argument and shape errors are detected before anything is
@@ -134,7 +144,8 @@ glr_status glr_validate_config(const glr_config* cfg);
 
 /* Bytes of caller-owned device memory a configuration needs; pure host.
  * state_bytes: persistent across steps (error buffers, U, optimizer state).
- * ws_bytes: scratch reused by every step. */
+ * ws_bytes: scratch reused by every step: one copy, sized by the largest
+ * matrix, per stream the matrices are spread over (min(num_mats, 4)). */
 glr_status glr_workspace_bytes(const glr_config* cfg, size_t* state_bytes, size_t* ws_bytes);
 
 /* Layout of matrix `mat` inside the state blob; pure host. */

@@ -2,12 +2,15 @@
 // checks, the state / workspace layout, and the launch sequence of one step.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -24,6 +27,7 @@ constexpr int64_t kMaxSortDim = 8192;   // LDS sort of d keys
 constexpr int kMaxRank = 1024;
 constexpr int kMaxWorkers = 4096;
 constexpr uint64_t kHeaderBytes = 256;  // device status word + padding
+constexpr int kMaxLanes = 4;            // streams the matrices of one step are spread over
 
 inline uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -36,6 +40,8 @@ struct WsLayout {
       off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
   uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rV64, off_rgpart, off_rskip, off_rctl, off_rsigw,
       off_rperm;
+  uint64_t lane_bytes;   // one copy of the scratch above, sized by the largest matrix
+  int lanes;             // copies: one per stream of glr_step
   uint64_t bytes;
 };
 
@@ -226,8 +232,36 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rctl = take(sizeof(JacCtl));
   w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
   w.off_rperm = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
-  w.bytes = o;
+  w.lane_bytes = o;
+  w.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
+  w.bytes = o * (uint64_t)w.lanes;
   return w;
+}
+
+// Matrix -> lane by longest-processing-time-first on an estimate of each matrix's
+// work over one refresh period: the per-step streaming of N m x n gradients plus
+// about ten Jacobi sweeps (d^3) and the re-orthonormalisation (d^2 D) per tau steps.
+std::vector<int> assign_lanes(const glr_config* c, int lanes) {
+  std::vector<std::pair<double, int>> w;
+  for (int i = 0; i < c->num_mats; ++i) {
+    const Dims x = dims_of(c, i);
+    const double d = (double)x.d, D = (double)x.D;
+    const double per_step = (double)c->num_workers * (double)x.m * (double)x.n;
+    w.push_back({per_step + 10.0 * (d * d * d + d * d * D) / (double)c->tau, i});
+  }
+  std::stable_sort(w.begin(), w.end(), [](const std::pair<double, int>& a, const std::pair<double, int>& b) {
+    return a.first > b.first;
+  });
+  std::vector<double> load((size_t)lanes, 0.0);
+  std::vector<int> lane((size_t)c->num_mats, 0);
+  for (const auto& it : w) {
+    int k = 0;
+    for (int j = 1; j < lanes; ++j)
+      if (load[(size_t)j] < load[(size_t)k]) k = j;
+    lane[(size_t)it.second] = k;
+    load[(size_t)k] += it.first;
+  }
+  return lane;
 }
 
 bool aligned(const void* p) { return ((uintptr_t)p % kAlign) == 0; }
@@ -255,6 +289,12 @@ struct glr_handle {
   double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
   int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
   bool prof = false;
+  int lanes = 1;                       // streams in use (<= ws.lanes)
+  std::vector<int> lane_of;            // lane of each matrix
+  hipStream_t lane_s[kMaxLanes] = {};  // non-blocking streams, created when ws.lanes > 1
+  hipEvent_t ev_fork = nullptr;
+  hipEvent_t ev_join[kMaxLanes] = {};
+  std::mutex mu;                       // err and suspect, written by the lane threads
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
   std::vector<ProfMark> marks;
@@ -265,16 +305,24 @@ struct glr_handle {
 namespace {
 
 glr_status fail(glr_handle* h, glr_status s, const std::string& m) {
-  if (h) h->err = m; else g_create_error = m;
+  if (h) {
+    std::lock_guard<std::mutex> lk(h->mu);
+    h->err = m;
+  } else {
+    g_create_error = m;
+  }
   return s;
 }
 
 glr_status hip_fail(glr_handle* h, hipError_t e, const char* where) {
-  if (h) h->suspect = true;
+  if (h) {
+    std::lock_guard<std::mutex> lk(h->mu);
+    h->suspect = true;
+  }
   return fail(h, GLR_ERR_DEVICE, fmt("%s: %s", where, hipGetErrorString(e)));
 }
 
-MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
+MatView view_of(glr_handle* h, int mat, float* X, const float* G, int lane) {
   const glr_mat_layout& L = h->lay[mat];
   MatView v;
   v.m = L.m; v.n = L.n; v.d = L.d; v.D = L.D;
@@ -296,7 +344,7 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G) {
   v.status = (uint32_t*)s;
   v.X = X;
   v.G = G;
-  char* w = h->work;
+  char* w = h->work + (uint64_t)lane * h->ws.lane_bytes;
   v.Mbar = (float*)(w + h->ws.off_Mbar);
   v.Q = (float*)(w + h->ws.off_Q);
   v.Qpart = (float*)(w + h->ws.off_Qpart);
@@ -503,9 +551,9 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   return GLR_OK;
 }
 
-glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s) {
+glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s, int lane) {
   const glr_config& c = h->cfg;
-  MatView v = view_of(h, mat, X, G);
+  MatView v = view_of(h, mat, X, G, lane);
   const bool refresh = (t % c.tau) == 0;
   OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
   {
@@ -539,6 +587,64 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
     GLR_HIP(h, launch_resid_opt(v, op, s));
   }
   return GLR_OK;
+}
+
+// the matrices of one lane, in index order, on that lane's stream and workspace
+glr_status run_lane(glr_handle* h, int lane, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+  for (int i = 0; i < h->cfg.num_mats; ++i) {
+    if (h->lane_of[(size_t)i] != lane) continue;
+    glr_status st = step_one(h, i, X[i], G[i], t, s, lane);
+    if (st != GLR_OK) return st;
+  }
+  return GLR_OK;
+}
+
+// Lanes run concurrently: each on its own stream, driven by its own host thread
+// (a refresh blocks its thread once per sweep on the convergence flag, so one
+// thread could not keep the other streams fed).  The lanes start after the work
+// already on `s` and `s` waits for all of them.
+glr_status step_lanes(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+  const int L = h->lanes;
+  GLR_HIP(h, hipEventRecord(h->ev_fork, s));
+  for (int k = 0; k < L; ++k) GLR_HIP(h, hipStreamWaitEvent(h->lane_s[k], h->ev_fork, 0));
+  glr_status st[kMaxLanes];
+  std::thread th[kMaxLanes];
+  for (int k = 1; k < L; ++k) {
+    st[k] = GLR_OK;
+    try {
+      th[k] = std::thread([h, k, X, G, t, &st] {
+        const hipError_t e = hipSetDevice(h->device);
+        st[k] = e == hipSuccess ? run_lane(h, k, X, G, t, h->lane_s[k]) : hip_fail(h, e, "hipSetDevice");
+      });
+    } catch (...) {
+      // no thread: this lane runs on the calling thread after lane 0
+    }
+  }
+  st[0] = run_lane(h, 0, X, G, t, h->lane_s[0]);
+  for (int k = 1; k < L; ++k) {
+    if (th[k].joinable()) th[k].join();
+    else st[k] = run_lane(h, k, X, G, t, h->lane_s[k]);
+  }
+  glr_status out = GLR_OK;
+  for (int k = 0; k < L; ++k)
+    if (out == GLR_OK && st[k] != GLR_OK) out = st[k];
+  for (int k = 0; k < L; ++k) {
+    hipError_t e = hipEventRecord(h->ev_join[k], h->lane_s[k]);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_join[k], 0);
+    if (e != hipSuccess && out == GLR_OK) out = hip_fail(h, e, "joining the lane streams");
+  }
+  return out;
+}
+
+void release_lanes(glr_handle* h) {
+  for (int k = 0; k < kMaxLanes; ++k) {
+    if (h->lane_s[k]) (void)hipStreamDestroy(h->lane_s[k]);
+    if (h->ev_join[k]) (void)hipEventDestroy(h->ev_join[k]);
+    h->lane_s[k] = nullptr;
+    h->ev_join[k] = nullptr;
+  }
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  h->ev_fork = nullptr;
 }
 
 }  // namespace
@@ -616,8 +722,20 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   for (int i = 0; e == hipSuccess && i < cfg->num_mats; ++i)
     e = launch_eye((float*)(h->state + h->lay[i].off_U), h->lay[i].d, st);
   if (e == hipSuccess) e = launch_fill_zero(d_ws, (size_t)wl.bytes, st);
+  h->lanes = wl.lanes;
+  if (const char* v = getenv("GLR_LANES")) {
+    const int k = atoi(v);
+    if (k >= 1 && k < h->lanes) h->lanes = k;
+  }
+  h->lane_of = assign_lanes(&h->cfg, h->lanes);
+  for (int k = 0; e == hipSuccess && h->lanes > 1 && k < h->lanes; ++k) {
+    e = hipStreamCreateWithFlags(&h->lane_s[k], hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[k], hipEventDisableTiming);
+  }
+  if (e == hipSuccess && h->lanes > 1) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
   if (e != hipSuccess) {
     std::string m = fmt("glr_create: %s", hipGetErrorString(e));
+    release_lanes(h);
     delete h;
     return fail(nullptr, GLR_ERR_DEVICE, m);
   }
@@ -637,9 +755,16 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64
       return fail(h, GLR_ERR_INVALID_ARG, fmt("matrix %d: buffers must be 256-byte aligned", i));
   }
   hipStream_t s = (hipStream_t)stream;
-  for (int i = 0; i < h->cfg.num_mats; ++i) {
-    glr_status st = step_one(h, i, X[i], G[i], t, s);
+  if (h->lanes > 1 && !h->prof) {
+    glr_status st = step_lanes(h, X, G, t, s);
     if (st != GLR_OK) return st;
+  } else {
+    // one matrix, or profiling: every matrix in order on `s` (event brackets
+    // then time one launch group at a time)
+    for (int i = 0; i < h->cfg.num_mats; ++i) {
+      glr_status st = step_one(h, i, X[i], G[i], t, s, h->lane_of[(size_t)i]);
+      if (st != GLR_OK) return st;
+    }
   }
   h->next_t = t + 1;
   return GLR_OK;
@@ -681,6 +806,7 @@ glr_status glr_next_step(const glr_handle* h, int64_t* next_t) {
 glr_status glr_destroy(glr_handle* h) {
   if (!h) return GLR_OK;
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+  release_lanes(h);
   delete h;
   return GLR_OK;
 }

@@ -131,3 +131,31 @@ def test_repeated_runs_are_bitwise_identical(gpu_lib, name):
         assert torch.equal(c1.E(l), c2.E(l))
         assert torch.equal(c1.Ut(l), c2.Ut(l))
         assert torch.equal(c1.J(l), c2.J(l))
+
+
+def test_concurrent_lanes_match_the_one_stream_order(gpu_lib, monkeypatch):
+    # several matrices run on up to four streams at once; each matrix's result
+    # must be bitwise that of running all of them in order on one stream
+    import torch
+    wl = get_workload("mixed_small")
+    T = min(wl.steps, wl.tau + 2)
+    _say("mixed_small lanes vs one stream over", T, "steps,", len(wl.shapes), "matrices")
+    G = _inputs(wl, T)
+    runs = []
+    for lanes in ("1", None):
+        if lanes is None:
+            monkeypatch.delenv("GLR_LANES", raising=False)
+        else:
+            monkeypatch.setenv("GLR_LANES", lanes)
+        comp = _make(gpu_lib, wl)
+        X = _zeros(wl)
+        for t in range(T):
+            comp.step(X, G[t], t)
+        assert comp.sync_status() == gpu_lib.GLR_OK
+        runs.append((comp, X))
+    (c1, x1), (c2, x2) = runs
+    for l in range(len(wl.shapes)):
+        assert torch.equal(x1[l], x2[l]), f"mat {l}: X differs"
+        assert torch.equal(c1.E(l), c2.E(l)), f"mat {l}: E differs"
+        assert torch.equal(c1.Ut(l), c2.Ut(l)), f"mat {l}: U differs"
+        assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
