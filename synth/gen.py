@@ -215,6 +215,16 @@ def _mk():
     add(Workload("large_8192x28672", ((8192, 28672),), 4, 256, 1, 10, "adam", 1e-3, 0.9,
                  recipe="cfg5"))
 
+    # ---- the four-block tournament off the 4096 shape: 256 seats holding 194
+    # blocks (62 padding seats, a ragged last block, right-oriented), and 64
+    # seats with a ragged last block; gapped at r for the fp64 projector check
+    add(Workload("seats256_right", ((3300, 3100),), 4, 48, 2, 3, "msgd", 0.01, 0.9,
+                 recipe="decay",
+                 params=(("rank", 96), ("decay", 0.95), ("nu", 5e-5), ("split", 48), ("div", 3.0))))
+    add(Workload("seats64_left", ((1012, 1100),), 4, 32, 2, 3, "adam", 1e-3, 0.9,
+                 recipe="decay",
+                 params=(("rank", 64), ("decay", 0.95), ("nu", 5e-5), ("split", 32), ("div", 3.0))))
+
     # ---- small parity cases: several tiles, ragged tails, both orientations
     add(Workload("tiny_left", ((40, 72),), 3, 5, 4, 10, "msgd", 0.05, 0.9,
                  recipe="geometric", params=(("rank", 12), ("nu", 1e-3))))

@@ -265,6 +265,13 @@ def test_layer_4096(gpu_lib, name, steps, ref):
     run_fullsize(gpu_lib, name, steps, ref_top=ref)
 
 
+@pytest.mark.parametrize("name", ["seats256_right", "seats64_left"])
+def test_four_block_groups_with_padding_and_ragged_blocks(gpu_lib, name):
+    # groups of four off the 4096 shape: padding seats (and groups with no
+    # block), a ragged last block, both orientations; a cold and a warm refresh
+    run_fullsize(gpu_lib, name, 3, ref_top=True)
+
+
 def test_transformer_block(gpu_lib):
     run_fullsize(gpu_lib, "block_4096_gap", 2)
 
