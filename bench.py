@@ -16,7 +16,9 @@ from a seeded torch generator, into a pool of distinct gradient batches.
 
 Steps t = W .. W+K-1 are timed with no instrumentation inside the step; the
 next K steps run again with HIP events around every launch group, on the
-library's stream, for the per-kernel averages.  Prints one JSON line: ms/step,
+library's stream, for the per-kernel averages; then 2 tau steps are timed one
+by one (median of the refresh steps and of the selection steps, and the
+sweeps of the cold first refresh and of the last warm one).  Prints one JSON line: ms/step,
 effective GB/s, the roofline of the dominant kernel (its algorithmic work per
 launch over its average event-timed duration), the per-kernel breakdown, and
 the CPU oracle timed on a bounded sample.
@@ -27,6 +29,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -318,8 +321,12 @@ def main():
     torch.cuda.synchronize()
 
     t_w = time.perf_counter()
+    cold_sweeps = None
     for t in range(args.warmup):
         comp.step(X, batches[t % pool], t)
+        if t == 0:
+            torch.cuda.synchronize()
+            cold_sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
     torch.cuda.synchronize()
     print(f"[bench] warm-up {args.warmup} steps {time.perf_counter() - t_w:.2f}s", file=sys.stderr, flush=True)
     # pass 1: the timed region (no event brackets inside the step)
@@ -358,6 +365,26 @@ def main():
             raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
         print(f"[bench] profiled pass: {prof_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
+    # pass 3: 2 tau more steps, each between two events on the step's stream:
+    # median time of a refresh step and of a selection step
+    t_next = args.warmup + (args.steps if args.no_profile else 2 * args.steps)
+    n3 = max(2, 2 * wl.tau)
+    per_type = {"refresh": [], "select": []}
+    stream = torch.cuda.current_stream(dev)
+    for t in range(t_next, t_next + n3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        comp.step(X, batches[t % pool], t)
+        e1.record(stream)
+        e1.synchronize()
+        per_type["refresh" if t % wl.tau == 0 else "select"].append(e0.elapsed_time(e1))
+    warm_sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
+    status = comp.sync_status()
+    if status not in (0, 7):
+        raise RuntimeError(f"device status {glr.STATUS_NAMES.get(status, status)}")
+    step_types = {k: {"median_ms": round(statistics.median(v), 4), "steps": len(v)}
+                  for k, v in per_type.items() if v}
+
     kernels = []
     for name in KERNEL_GROUPS:
         if name in prof and prof[name][1]:
@@ -391,6 +418,9 @@ def main():
         "groups": groups,
         "refresh_sweeps_last": sweeps,
         "refresh_history_last": history,
+        "step_types": step_types,
+        "refresh_sweeps_cold": cold_sweeps,
+        "refresh_sweeps_warm": warm_sweeps,
         "status": glr.STATUS_NAMES.get(status, status),
     }
     if not args.no_cpu_baseline:
