@@ -688,10 +688,11 @@ __device__ __forceinline__ void solve_group(const double* __restrict__ Apk, JacC
   for (int k = 0; k < NE; ++k) {
     const int e = tid + NT * k, x = e / NR, y = e % NR;
     if (x < y) {
-      const double gxx = dg[x], gyy = dg[y];
-      const double den = fmax(fmax(sqrt(gxx * gyy), fabs(gxx - gyy)), floor2);
-      if (den > 0.0) {
-        const double q2 = (g[k] / den) * (g[k] / den);
+      // (g / max(sqrt(gxx gyy), |gxx - gyy|, floor))^2, all terms squared
+      const double gxx = dg[x], gyy = dg[y], df = gxx - gyy;
+      const double den2 = fmax(fmax(gxx * gyy, df * df), floor2 * floor2);
+      if (den2 > 0.0) {
+        const double q2 = g[k] * g[k] / den2;
         m2 = fmax(m2, q2);
         if (x / kJB == y / kJB) mw2 = fmax(mw2, q2);
       }
