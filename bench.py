@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK = 8.0e12           # bytes/s
 FP32_MFMA_PEAK = 157.3e12   # flop/s, dense
 FP64_MFMA_PEAK = 78.6e12
+BF16_MFMA_PEAK = 2.5e15     # dense bf16 (the selection products of the approx_bf16 mode)
 METRIC = "ms/step and effective HBM GB/s for compress+EF+update; % of roofline"
 
 
@@ -135,14 +136,16 @@ def group_work(wl, name):
     return tuple(x / count for x in tot)
 
 
-def roofline_entry(wl, name, total_ms, launches):
+def roofline_entry(wl, name, total_ms, launches, select="approx"):
     work = group_work(wl, name)
     if work is None or launches == 0 or total_ms <= 0:
         return None
     avg_s = total_ms / 1e3 / launches
     byts, f32, f64, alu = work
     t_hbm = byts / HBM_PEAK
-    t_mfma = f32 / FP32_MFMA_PEAK + f64 / FP64_MFMA_PEAK
+    # the approx_bf16 selection runs its products on the bf16 matrix cores
+    f32_peak = BF16_MFMA_PEAK if (name == "select" and select == "approx_bf16") else FP32_MFMA_PEAK
+    t_mfma = f32 / f32_peak + f64 / FP64_MFMA_PEAK
     t_alu = alu / FP64_ALU_PEAK
     base = {"kernel": name, "avg_us": avg_s * 1e6, "launches": launches,
             "bytes_per_launch": byts, "flops_per_launch": f32 + f64 + alu}
@@ -286,6 +289,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--tol", type=float, default=1e-6, help="refresh tolerance")
+    ap.add_argument("--select", default="approx", choices=("approx", "exact", "approx_bf16"),
+                    help="selection mode (approx: the method's Approx-Top-r in fp32; approx_bf16: its "
+                         "products on bf16 roundings of U and Mbar, a mixed-precision mode)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy that calibrates the HBM traffic counters")
     args = ap.parse_args()
@@ -316,7 +322,7 @@ def main():
     batches = make_pool(wl, pool, dev)
     comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
                           beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, tol=args.tol,
-                          device=dev)
+                          select=args.select, device=dev)
     X = [torch.zeros(m, n, dtype=torch.float32, device=dev) for m, n in wl.shapes]
     torch.cuda.synchronize()
 
@@ -388,7 +394,7 @@ def main():
     kernels = []
     for name in KERNEL_GROUPS:
         if name in prof and prof[name][1]:
-            e = roofline_entry(wl, name, *prof[name])
+            e = roofline_entry(wl, name, *prof[name], select=args.select)
             if e:
                 e["total_ms"] = prof[name][0]
                 kernels.append(e)
@@ -405,12 +411,13 @@ def main():
     out = {
         "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms/step",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if args.select != "approx_bf16" else "f32 (selection products on bf16)",
         "data": "synthetic (planted-spectrum gradients + seeded Gaussian noise, resident in HBM)",
         "config": {"workload": wl.name, "shapes": [list(s) for s in wl.shapes][:4],
                    "num_matrices": len(wl.shapes), "simulated_workers": wl.workers,
                    "rank": wl.rank, "tau": wl.tau, "optimizer": wl.opt,
-                   "refresh_steps_timed": n_refresh},
+                   "refresh_steps_timed": n_refresh, "select": args.select},
         "effective_GBps": round(eff, 1),
         "roofline": roof,
         "profiled_ms_per_step": None if prof_ms is None else round(prof_ms, 4),

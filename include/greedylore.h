@@ -87,8 +87,12 @@ typedef enum { GLR_REFRESH_COMPRESSED = 0, GLR_REFRESH_FULL = 1 } glr_refresh;
 
 /* Non-refresh selection.  APPROX is Approx-Top-r (Algorithm 2): scores
  * lambdabar_j^2 with lambdabar_j = u_j^T Mbar v_j and v_j ~ N(0, I_D).
- * EXACT scores ||u_j^T Mbar||^2 (eq-semi-lazy-svd-2). */
-typedef enum { GLR_SELECT_APPROX = 0, GLR_SELECT_EXACT = 1 } glr_select;
+ * EXACT scores ||u_j^T Mbar||^2 (eq-semi-lazy-svd-2).  APPROX_BF16 is
+ * Approx-Top-r with the products of u_j and Mbar taken on their bf16
+ * roundings (round to nearest even; v_j and the sums stay fp32): a mixed
+ * precision mode for the ranking only (a score carries ~2^-8 relative error
+ * per term), on the bf16 matrix cores; everything else stays fp32. */
+typedef enum { GLR_SELECT_APPROX = 0, GLR_SELECT_EXACT = 1, GLR_SELECT_APPROX_BF16 = 2 } glr_select;
 
 #define GLR_CHECK_FINITE 0x1u  /* scan G for NaN/Inf during the worker mean */
 #define GLR_COLD_START   0x2u  /* start every refresh from U = I instead of the previous U */

@@ -79,6 +79,32 @@ def approx_lambdas(u, ms, v):
     return lam, lam.mean(axis=0)
 
 
+def bf16_round(x):
+    """Round to bfloat16 (1 sign, 8 exponent, 7 fraction bits: the upper half
+    of an IEEE binary32), to nearest with ties to even, through binary32 as
+    the fp32 device values are; returned as fp64.  Finite inputs only.
+
+    The binary32 pattern is split at bit 16: the upper half is kept and
+    incremented when the lower half exceeds 0x8000, or equals it with the
+    kept half odd (a carry into the exponent is the correct result)."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    bits = f.view(np.uint32).astype(np.uint64)
+    upper, lower = bits >> 16, bits & 0xFFFF
+    up = (lower > 0x8000) | ((lower == 0x8000) & ((upper & 1) == 1))
+    upper = upper + up.astype(np.uint64)
+    out = (upper << 16).astype(np.uint32).view(np.float32)
+    return out.astype(np.float64)
+
+
+def approx_lambdas_bf16(u, mbar, v):
+    """lambdabar_j = u_j^T Mbar v_j with u_j and Mbar rounded to bf16 (the
+    mixed-precision selection mode; v_j and the sums exact), on the mean
+    Mbar: the mode is defined on the mean, which equals the per-worker mean
+    of Algorithm 2 by linearity."""
+    z = bf16_round(u).T @ bf16_round(mbar)
+    return np.einsum("jb,jb->j", z, v)
+
+
 def msgd_update(x, b, ghat, lr, beta):
     """M_t = beta M_{t-1} + (1 - beta) G_t;  X_{t+1} = X_t - gamma M_t (eq-msgd)."""
     b = beta * b + (1.0 - beta) * ghat
@@ -126,7 +152,7 @@ class Oracle:
     eps: float = 1e-8
     seed: int = 0
     refresh: str = "compressed"   # "compressed" (Alg. 4) | "full" (Alg. 3)
-    select: str = "approx"        # "approx" (Alg. 2) | "exact" (eq-semi-lazy-svd-2)
+    select: str = "approx"        # "approx" (Alg. 2) | "exact" (eq-semi-lazy-svd-2) | "approx_bf16"
     svd_tol: float | None = None
     states: list = field(default_factory=list)
     t_next: int = 0
@@ -181,6 +207,11 @@ class Oracle:
                 lam_i, lam = approx_lambdas(st.u, ms, v)
                 score = lam * lam
                 out.update(lam=lam, lam_workers=lam_i)
+            elif self.select == "approx_bf16":
+                v = gaussian_vectors(self.seed, t, l, np.arange(d), D).astype(np.float64)
+                lam = approx_lambdas_bf16(st.u, mbar, v)
+                score = lam * lam
+                out.update(lam=lam)
             else:
                 score = exact_scores(st.u, mbar)
             jsel = argtop_r(score, r)

@@ -114,7 +114,7 @@ def make_config(shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta
         rank=rank, tau=tau, opt={"msgd": 0, "adam": 1}[opt] if isinstance(opt, str) else opt,
         lr=lr, beta1=beta1, beta2=beta2, eps=eps,
         refresh={"compressed": 0, "full": 1}[refresh] if isinstance(refresh, str) else refresh,
-        select={"approx": 0, "exact": 1}[select] if isinstance(select, str) else select,
+        select={"approx": 0, "exact": 1, "approx_bf16": 2}[select] if isinstance(select, str) else select,
         seed=seed, max_sweeps=max_sweeps, tol=tol, flags=flags)
     return cfg, arr
 

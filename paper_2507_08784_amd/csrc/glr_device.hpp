@@ -49,6 +49,14 @@ __device__ __forceinline__ int mfma32_row(int v, int lane) {
   return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 }
 
+// v_mfma_f32_32x32x16_bf16:  A 32x16, B 16x32 (bf16), C 32x32 (fp32, laid out
+// as for mfma32).  A[i][k] from lane i + 32 (k / 8), element k % 8; B[k][j]
+// from lane j + 32 (k / 8), element k % 8.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x16 mfma32_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 // v_mfma_f64_16x16x4_f64:  A 16x4, B 4x16, C 16x16 (fp64).
 //   A[i][k] from lane i + 16k; B[k][j] from lane j + 16k;
 //   C[i][j] in lane j + 16*(i%4), register i/4.
@@ -259,10 +267,33 @@ struct MfmaTile {
     }
   }
 
-  // acc += A B over K.  With `dacc`, the fp32 accumulators are added into
-  // fp64 ones after every 16 BK slices and cleared, so that rounding grows with
-  // that length only (dacc holds the result then; acc is zero).
-  template <class LA, class LB>
+  // the same product with both operands rounded to bf16 (to nearest even) as
+  // they leave LDS, fp32 accumulation: two bf16 MFMAs of depth 16 per slice
+  __device__ __forceinline__ void compute_bf16(const float* As, const float* Bs) {
+    const int kh = lane >> 5, l32 = lane & 31;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)As[(16 * ks + 8 * kh + e) * PA + wm * WTM + i * 32 + l32];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b[j][e] = (__bf16)Bs[(16 * ks + 8 * kh + e) * PB + wn * WTN + j * 32 + l32];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32_bf16(a[i], b[j], acc[i][j]);
+    }
+  }
+
+  // acc += A B over K (BF16: with both operands rounded to bf16).  With `dacc`,
+  // the fp32 accumulators are added into fp64 ones after every 16 BK slices
+  // and cleared, so that rounding grows with that length only (dacc holds the
+  // result then; acc is zero).
+  template <bool BF16 = false, class LA, class LB>
   __device__ void run(LA& la, LB& lb, int K, float* smem, double (*dacc)[TN][16] = nullptr) {
     float* As = smem;
     float* Bs = smem + SA;
@@ -279,7 +310,8 @@ struct MfmaTile {
         la.fetch((kb + 1) * BK);
         lb.fetch((kb + 1) * BK);
       }
-      compute(As, Bs);
+      if constexpr (BF16) compute_bf16(As, Bs);
+      else compute(As, Bs);
       if (dacc && ((kb & 15) == 15 || !more)) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)

@@ -119,7 +119,7 @@ struct OptParams {
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_eye(float* Ut, int64_t d, hipStream_t s);
 hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s);
-hipError_t launch_sel_scores(const MatView& v, bool approx, uint64_t seed, int64_t t, hipStream_t s);
+hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t seed, int64_t t, hipStream_t s);
 hipError_t launch_topr(const MatView& v, hipStream_t s);
 hipError_t launch_iota_J(const MatView& v, hipStream_t s);
 hipError_t launch_proj(const MatView& v, hipStream_t s);

@@ -92,7 +92,7 @@ glr_status check_config(const glr_config* c, std::string* why) {
   }
   if (c->refresh != GLR_REFRESH_COMPRESSED && c->refresh != GLR_REFRESH_FULL)
     return bad(GLR_ERR_INVALID_ARG, "unknown refresh mode");
-  if (c->select != GLR_SELECT_APPROX && c->select != GLR_SELECT_EXACT)
+  if (c->select != GLR_SELECT_APPROX && c->select != GLR_SELECT_EXACT && c->select != GLR_SELECT_APPROX_BF16)
     return bad(GLR_ERR_INVALID_ARG, "unknown select mode");
   if (c->max_sweeps < 1) return bad(GLR_ERR_INVALID_ARG, "max_sweeps must be >= 1");
   if (!(c->tol > 0.f && c->tol < 1.f)) return bad(GLR_ERR_INVALID_ARG, "tol must be in (0, 1)");
@@ -566,7 +566,8 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
   } else if (v.r < v.d) {
     {
       ProfScope p(h, s, GLR_PROF_SELECT);
-      GLR_HIP(h, launch_sel_scores(v, c.select == GLR_SELECT_APPROX, c.seed, t, s));
+      GLR_HIP(h, launch_sel_scores(v, c.select != GLR_SELECT_EXACT, c.select == GLR_SELECT_APPROX_BF16, c.seed, t,
+                                   s));
     }
     ProfScope p(h, s, GLR_PROF_TOPR);
     GLR_HIP(h, launch_topr(v, s));

@@ -97,7 +97,7 @@ hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
 // ---------------------------------------------------------------------------
 constexpr int SEL_BM = 128, SEL_BN = 128;
 
-template <bool RIGHT, bool APPROX>
+template <bool RIGHT, bool APPROX, bool BF16>
 __global__ void __launch_bounds__(256)
 k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d, int64_t D,
              float* __restrict__ part, uint32_t mat, uint32_t tstep, uint32_t key0, uint32_t key1) {
@@ -111,11 +111,11 @@ k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64
   if (RIGHT) {
     // Mo[a][b] = Mbar[b][a] : A[b][a] contiguous along a
     LoadK<SEL_BM, 32, false, false> la(Mbar, nullptr, d, m0, (int)D, (int)d, nullptr);
-    tile.run(la, lb, (int)d, smem);
+    tile.template run<BF16>(la, lb, (int)d, smem);
   } else {
     // Mo[a][b] = Mbar[a][b] : A[b][a] contiguous along b
     LoadR<SEL_BM, 32, false> la(Mbar, nullptr, D, m0, (int)D, (int)d);
-    tile.run(la, lb, (int)d, smem);
+    tile.template run<BF16>(la, lb, (int)d, smem);
   }
   const int lane = lane_id();
 #pragma unroll
@@ -165,15 +165,23 @@ __global__ void k_sel_finish(const float* __restrict__ part, int ntiles, int64_t
   score[j] = approx ? s * s : s;
 }
 
-hipError_t launch_sel_scores(const MatView& v, bool approx, uint64_t seed, int64_t t, hipStream_t s) {
+hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t seed, int64_t t, hipStream_t s) {
+  if (bf16 && !approx) return hipErrorInvalidValue;
   dim3 grid((unsigned)((v.d + SEL_BN - 1) / SEL_BN), (unsigned)((v.D + SEL_BM - 1) / SEL_BM));
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
-#define GLR_SEL(R, A)                                                                          \
-  hipLaunchKernelGGL((k_sel_scores<R, A>), grid, dim3(kThreads), 0, s, v.Mbar, v.Ut, v.d, v.D, \
+#define GLR_SEL(R, A, B)                                                                          \
+  hipLaunchKernelGGL((k_sel_scores<R, A, B>), grid, dim3(kThreads), 0, s, v.Mbar, v.Ut, v.d, v.D, \
                      v.lam_part, (uint32_t)v.mat, tt, k0, k1)
-  if (v.right) { if (approx) GLR_SEL(true, true); else GLR_SEL(true, false); }
-  else         { if (approx) GLR_SEL(false, true); else GLR_SEL(false, false); }
+  if (v.right) {
+    if (bf16) GLR_SEL(true, true, true);
+    else if (approx) GLR_SEL(true, true, false);
+    else GLR_SEL(true, false, false);
+  } else {
+    if (bf16) GLR_SEL(false, true, true);
+    else if (approx) GLR_SEL(false, true, false);
+    else GLR_SEL(false, false, false);
+  }
 #undef GLR_SEL
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

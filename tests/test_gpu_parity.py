@@ -111,3 +111,45 @@ def test_selection_scores_are_the_bilinear_forms(gpu_lib):
         sc = comp.score(0).double().cpu().numpy()
         scale = np.max(lam ** 2)
         assert np.abs(sc - lam ** 2).max() < 1e-4 * scale
+
+
+@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left"])
+def test_bf16_selection_parity(gpu_lib, name):
+    # mixed-precision selection (scores from bf16 roundings of U and Mbar on
+    # the bf16 matrix cores): trajectory parity with the oracle's same mode
+    # (J identical at every selection step); and at every selection step the
+    # GPU scores against the mode's formula evaluated in fp64 on the GPU's own
+    # U and Mbar (U's noise-bulk columns are not pinned column by column, and
+    # the oracle's fp64 error buffers move a few Mbar entries across a bf16
+    # rounding boundary), which they must match far more closely than the same
+    # formula without the rounding.  The GPU's Mbar is its previous E-bar plus
+    # the workers' mean gradient (the oracle's Mbar minus its previous mean E).
+    from oracle.method import approx_lambdas_bf16
+    from tests.parity import rel
+    _print_case(name + " select=approx_bf16")
+    wl = get_workload(name)
+    prev = {}
+
+    def check(comp, o, t, l, rec):
+        m, n = wl.shapes[l]
+        d, D = min(m, n), max(m, n)
+        ebar_g = comp.Ebar(l).double().cpu().numpy()
+        ebar_g = ebar_g.T if m > n else ebar_g
+        if not o["refresh"] and l in prev:
+            e_gpu, e_orc = prev[l]
+            mbar_g = e_gpu + (o["mbar"] - e_orc.mean(axis=0))
+            sg = comp.score(l).double().cpu().numpy()
+            ug = comp.Ut(l).double().cpu().numpy().T        # columns u_j
+            v = gaussian_vectors(wl.seed, t, l, np.arange(d), D).astype(np.float64)
+            lb = approx_lambdas_bf16(ug, mbar_g, v)
+            lu = np.einsum("jb,jb->j", ug.T @ mbar_g, v)
+            rec["score_bf16"] = rel(sg, lb * lb)
+            rec["score_unrounded"] = rel(sg, lu * lu)
+            assert rec["score_bf16"] < 1e-4, f"t={t} mat={l}: bf16 scores rel {rec['score_bf16']:.2e}"
+            assert rec["score_unrounded"] > 10 * rec["score_bf16"], (t, l, rec)
+        prev[l] = (ebar_g, o["E"])
+
+    log = run_parity(gpu_lib, wl, select="approx_bf16", check=check)
+    assert any("score_bf16" in r for r in log)
+    _print_case(name, score_bf16_max=max(r.get("score_bf16", 0.0) for r in log),
+                score_unrounded_min=min(r.get("score_unrounded", 1.0) for r in log))

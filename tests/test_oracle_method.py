@@ -10,8 +10,8 @@ import itertools
 import numpy as np
 import pytest
 
-from oracle.method import (Oracle, adam_update, approx_lambdas, argtop_r, compress,
-                           exact_scores, msgd_update, oriented_to_mn)
+from oracle.method import (Oracle, adam_update, approx_lambdas, approx_lambdas_bf16, argtop_r,
+                           bf16_round, compress, exact_scores, msgd_update, oriented_to_mn)
 from oracle.philox import gaussian_vectors
 from oracle.svd import left_svd
 from synth import get_workload, gradient_batch, planted_matrix
@@ -167,8 +167,67 @@ def _run(wl, steps=None, **kw):
     return orc, outs
 
 
+# ---------------------------------------------------------------- bf16 rounding
+# (the mixed-precision selection mode; bfloat16 = the upper half of a binary32)
+
+@pytest.mark.parametrize("x,want", [
+    (1.0, 1.0),
+    (1.0 + 2.0 ** -8, 1.0),                         # tie, kept half even: down
+    (1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -6),         # tie, kept half odd: up
+    (1.0 + 2.0 ** -8 + 2.0 ** -20, 1.0 + 2.0 ** -7),  # above the tie
+    (1.0 + 2.0 ** -8 - 2.0 ** -20, 1.0),            # below the tie
+    (-(1.0 + 3 * 2.0 ** -8), -(1.0 + 2.0 ** -6)),   # sign-symmetric
+    (2.0 - 2.0 ** -8, 2.0),                         # tie with odd fraction 127: carries into the exponent
+    (3.0, 3.0), (0.0, 0.0), (2.0 ** -130, 2.0 ** -130),
+    (np.float32(np.pi), 3.140625),                  # 0x40490FDB -> 0x4049
+])
+def test_bf16_round_values(x, want):
+    assert bf16_round(np.float64(x)) == want
+
+
+def test_bf16_round_is_the_nearest_bf16_with_ties_to_even():
+    # brute force over every low half of a few binary32 patterns: the result is
+    # the nearer of the two bf16 neighbours, found by comparing distances in
+    # fp64, the even one on a tie
+    for upper in (0x3F80, 0x3F81, 0x4049, 0xC2F7, 0x0001, 0x7F7E):
+        lows = np.arange(0x10000, dtype=np.uint64)
+        bits = ((np.uint64(upper) << np.uint64(16)) | lows).astype(np.uint32)
+        x = bits.view(np.float32).astype(np.float64)
+        lo = np.uint32(upper << 16)
+        hi = np.uint32((upper + 1) << 16)
+        a = np.array([lo], dtype=np.uint32).view(np.float32).astype(np.float64)[0]
+        b = np.array([hi], dtype=np.uint32).view(np.float32).astype(np.float64)[0]
+        da, db = np.abs(x - a), np.abs(x - b)
+        want = np.where(da < db, a, np.where(db < da, b, a if upper % 2 == 0 else b))
+        assert np.array_equal(bf16_round(x), want), hex(upper)
+
+
+def test_bf16_round_bound_and_idempotence():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(20000) * np.exp(rng.uniform(-30, 30, 20000))
+    y = bf16_round(x)
+    x32 = x.astype(np.float32).astype(np.float64)
+    # 8 significant bits: unit roundoff 2^-8 (half an ulp at the bottom of a binade)
+    assert np.all(np.abs(y - x32) <= 2.0 ** -8 * np.abs(x32))
+    assert np.array_equal(bf16_round(y), y)
+    o = np.sort(x)
+    assert np.all(np.diff(bf16_round(o)) >= 0)        # monotone
+
+
+def test_bf16_lambdas_equal_the_exact_ones_on_bf16_inputs():
+    # on inputs that bf16 holds exactly, the mode's lambdas are Algorithm 2's
+    rng = np.random.default_rng(6)
+    d, D, N = 12, 20, 3
+    u = rng.integers(-8, 9, (d, d)) * 2.0 ** -4
+    ms = rng.integers(-64, 65, (N, d, D)) * 2.0 ** -6
+    ms[1:] = ms[0]                       # identical workers: their mean is exact too
+    v = rng.standard_normal((d, D))
+    _, lam = approx_lambdas(u, ms, v)
+    assert np.allclose(approx_lambdas_bf16(u, ms[0], v), lam, rtol=1e-12, atol=1e-12)
+
+
 @pytest.mark.parametrize("name", ["tiny_left", "ragged_right", "mixed_small"])
-@pytest.mark.parametrize("select", ["approx", "exact"])
+@pytest.mark.parametrize("select", ["approx", "exact", "approx_bf16"])
 def test_step_invariants(name, select):
     wl = get_workload(name)
     _, outs = _run(wl, select=select)
