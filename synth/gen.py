@@ -225,6 +225,12 @@ def _mk():
                  recipe="decay",
                  params=(("rank", 64), ("decay", 0.95), ("nu", 5e-5), ("split", 32), ("div", 3.0))))
 
+    # ---- the largest full-basis refresh: d = 8192 (the LDS sort limit), pairs
+    # on 512 seats (511 rounds a sweep); gapped at r
+    add(Workload("max_8192", ((8192, 8256),), 2, 32, 2, 3, "msgd", 0.01, 0.9,
+                 recipe="decay",
+                 params=(("rank", 64), ("decay", 0.95), ("nu", 5e-5), ("split", 32), ("div", 3.0))))
+
     # ---- small parity cases: several tiles, ragged tails, both orientations
     add(Workload("tiny_left", ((40, 72),), 3, 5, 4, 10, "msgd", 0.05, 0.9,
                  recipe="geometric", params=(("rank", 12), ("nu", 1e-3))))

@@ -272,6 +272,13 @@ def test_four_block_groups_with_padding_and_ragged_blocks(gpu_lib, name):
     run_fullsize(gpu_lib, name, 3, ref_top=True)
 
 
+def test_largest_full_basis_refresh(gpu_lib):
+    # d = 8192, the largest min(m, n) the library takes: a cold and a warm
+    # complete basis (pairs tournament, 511 rounds a sweep) and a selection
+    # step over 8192 scores, checked by the size-independent properties
+    run_fullsize(gpu_lib, "max_8192", 3, sample_cols=4)
+
+
 def test_transformer_block(gpu_lib):
     run_fullsize(gpu_lib, "block_4096_gap", 2)
 
