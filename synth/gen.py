@@ -231,6 +231,12 @@ def _mk():
                  recipe="decay",
                  params=(("rank", 64), ("decay", 0.95), ("nu", 5e-5), ("split", 32), ("div", 3.0))))
 
+    # ---- the largest rank: r = 1024 of d = 1100 (four 256-row projection
+    # tiles, the wide residual), gapped at r
+    add(Workload("max_rank", ((1100, 1300),), 2, 1024, 2, 3, "msgd", 0.01, 0.9,
+                 recipe="decay",
+                 params=(("rank", 1100), ("decay", 0.998), ("nu", 5e-5), ("split", 1024), ("div", 3.0))))
+
     # ---- small parity cases: several tiles, ragged tails, both orientations
     add(Workload("tiny_left", ((40, 72),), 3, 5, 4, 10, "msgd", 0.05, 0.9,
                  recipe="geometric", params=(("rank", 12), ("nu", 1e-3))))
@@ -239,6 +245,8 @@ def _mk():
     add(Workload("mixed_small", ((96, 160), (170, 66), (33, 33), (1, 37), (5, 9)),
                  4, 4, 3, 7, "adam", 2e-3, 0.9,
                  recipe="geometric", params=(("rank", 8), ("nu", 1e-3))))
+    add(Workload("single_worker", ((64, 96),), 1, 6, 3, 7, "adam", 1e-3, 0.9,
+                 recipe="geometric", params=(("rank", 12), ("nu", 1e-3))))
     add(Workload("mid_left", ((256, 600),), 4, 16, 4, 9, "msgd", 0.01, 0.9,
                  recipe="geometric", params=(("rank", 40), ("nu", 2e-4))))
     add(Workload("lowrank_exact", ((48, 100), (90, 30)), 2, 6, 3, 6, "msgd", 0.01, 0.9,

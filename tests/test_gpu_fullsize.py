@@ -279,6 +279,11 @@ def test_largest_full_basis_refresh(gpu_lib):
     run_fullsize(gpu_lib, "max_8192", 3, sample_cols=4)
 
 
+def test_largest_rank(gpu_lib):
+    # r = 1024 (the largest rank the library takes) of d = 1100
+    run_fullsize(gpu_lib, "max_rank", 3, ref_top=True)
+
+
 def test_transformer_block(gpu_lib):
     run_fullsize(gpu_lib, "block_4096_gap", 2)
 

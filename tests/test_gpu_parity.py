@@ -15,7 +15,7 @@ def _print_case(name, **kw):
     print(f"[parity] {name} {kw}", flush=True)
 
 
-@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left"])
+@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left", "single_worker"])
 def test_trajectory_parity(gpu_lib, name):
     _print_case(name)
     wl = get_workload(name)
