@@ -38,10 +38,14 @@
  * stream and before what the caller enqueues next.  With one matrix it
  * enqueues its kernels on the stream itself.  With several, the matrices are
  * spread over up to four non-blocking streams of the handle (created by
- * glr_create, destroyed by glr_destroy), each with its own copy of the
- * workspace scratch and its own host thread inside glr_step, forked from and
- * joined back to `stream` with events; every matrix computes exactly what it
- * computes alone (results are bitwise those of running the matrices in order).
+ * glr_create, destroyed by glr_destroy), each with its own host thread inside
+ * glr_step, forked from and joined back to `stream` with events; every matrix
+ * computes exactly what it computes alone (results are bitwise those of
+ * running the matrices in order).  On refresh steps (tau > 1) of several
+ * matrices with d <= 2048 and one Jacobi group size, the sweeps of all of them
+ * run in shared launches on `stream` itself, with one convergence read per
+ * sweep for all matrices; each matrix still computes exactly what it computes
+ * alone.  GLR_JAC_JOINT=0, read by glr_create, turns this off.
  * While profiling is enabled the matrices run in order on `stream`.  The
  * environment variable GLR_LANES, read by glr_create, lowers the stream count.
  * glr_step blocks the host only on refresh steps, where it reads the
@@ -148,8 +152,8 @@ glr_status glr_validate_config(const glr_config* cfg);
 
 /* Bytes of caller-owned device memory a configuration needs; pure host.
  * state_bytes: persistent across steps (error buffers, U, optimizer state).
- * ws_bytes: scratch reused by every step: one copy, sized by the largest
- * matrix, per stream the matrices are spread over (min(num_mats, 4)). */
+ * ws_bytes: scratch reused by every step: one region per matrix, sized by
+ * that matrix. */
 glr_status glr_workspace_bytes(const glr_config* cfg, size_t* state_bytes, size_t* ws_bytes);
 
 /* Layout of matrix `mat` inside the state blob; pure host. */

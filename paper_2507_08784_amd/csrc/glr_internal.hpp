@@ -127,6 +127,34 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s);
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s);
 hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s);
 
+// One matrix of a joint refresh (device memory): its views for the two buffer
+// parities of the per-sweep reordering (v[1] is v[0] with Apk <-> Apk2 and
+// Utw <-> W) and the sizes of its tournament.
+struct JointMat {
+  MatView v[2];
+  int nb, seats, groups, rounds, chunks, width;
+};
+// Block-offset tables of the joint launches (each num + 1 ints; entry m is the
+// first block of matrix m, entry num the grid size)
+enum { kJointSolve = 0, kJointSolveApply, kJointUpdate, kJointDiag, kJointPermute, kJointGather, kJointKinds };
+// A joint refresh as the host sees it: device tables, and the grid sizes
+struct JointPlan {
+  const JointMat* jm = nullptr;
+  const int* first = nullptr;   // kJointKinds tables of num + 1 ints
+  int* flags = nullptr;         // num ints: converged flags for the host
+  int num = 0, ng = 0, rounds_max = 0, npad_max = 2;
+  int total[kJointKinds] = {};
+};
+// the sizes of matrix J.v[0]'s tournament and its block counts per launch kind
+void joint_fill(JointMat& J, int (&blocks)[kJointKinds]);
+hipError_t launch_joint_sort(const JointPlan& jp, int par, hipStream_t s);
+hipError_t launch_joint_solve(const JointPlan& jp, int par, int round, float tol, int max_inner, double floor_rel2,
+                              hipStream_t s);
+hipError_t launch_joint_solve_apply(const JointPlan& jp, int par, int round, float tol, int max_inner,
+                                    double floor_rel2, hipStream_t s);
+hipError_t launch_joint_update(const JointPlan& jp, int par, int round, hipStream_t s);
+hipError_t launch_joint_check(const JointPlan& jp, float tol, hipStream_t s);
+
 // Jacobi on the fp64 Gram of the rows of W
 int jac_blocks(int64_t d);
 int jac_seats(int64_t d);

@@ -1072,17 +1072,20 @@ hipError_t launch_jac_check(const MatView& v, float tol, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // finish: sigma_j = sqrt(A_jj), sort descending, permute U^T rows
 // ---------------------------------------------------------------------------
-__global__ void k_diag_sqrt(const double* __restrict__ Apk, int64_t d, int nb, float* __restrict__ sig) {
-  const int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+__device__ __forceinline__ void diag_sqrt_at(const double* __restrict__ Apk, int64_t d, int nb,
+                                             float* __restrict__ sig, int64_t j) {
   if (j >= d) return;
   const int b = (int)(j / kJB), l = (int)(j % kJB);
   sig[j] = (float)sqrt(fmax(Apk[pk_off(b, b, nb) + l * (kJB + 1)], 0.0));
 }
+__global__ void k_diag_sqrt(const double* __restrict__ Apk, int64_t d, int nb, float* __restrict__ sig) {
+  diag_sqrt_at(Apk, d, nb, sig, blockIdx.x * (int64_t)blockDim.x + threadIdx.x);
+}
 
-__global__ void __launch_bounds__(1024)
-k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ perm) {
-  extern __shared__ __align__(16) unsigned char dyn[];
-  uint64_t* keys = reinterpret_cast<uint64_t*>(dyn);
+// the descending order of sigma (ties to the smaller index) by one block, in
+// n_pad keys of LDS
+__device__ __forceinline__ void sort_desc_block(const float* __restrict__ sig, int d, int n_pad,
+                                                int* __restrict__ perm, uint64_t* keys) {
   for (int i = threadIdx.x; i < n_pad; i += blockDim.x) {
     if (i < d) keys[i] = ((uint64_t)(~float_order(sig[i])) << 32) | (uint32_t)i;
     else keys[i] = ~0ull;
@@ -1090,6 +1093,11 @@ k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ p
   __syncthreads();
   bitonic_sort(keys, n_pad);
   for (int i = threadIdx.x; i < d; i += blockDim.x) perm[i] = (int)(keys[i] & 0xFFFFFFFFu);
+}
+__global__ void __launch_bounds__(1024)
+k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ perm) {
+  extern __shared__ __align__(16) unsigned char dyn[];
+  sort_desc_block(sig, d, n_pad, perm, reinterpret_cast<uint64_t*>(dyn));
 }
 
 __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict__ sig_w,
@@ -1118,12 +1126,13 @@ __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict
 // kPermBlocks consecutive stored blocks, issuing all its loads before its
 // stores, so that many loads are in flight per thread.
 constexpr int kPermBlocks = 8;
-__global__ void __launch_bounds__(256)
-k_pk_permute(const double* __restrict__ A, double* __restrict__ B, const int* __restrict__ perm, int64_t d,
-             int nb) {
+// the kPermBlocks stored blocks from `bid * kPermBlocks` of B = A with rows and
+// columns reordered by perm
+__device__ __forceinline__ void pk_permute_blocks(const double* __restrict__ A, double* __restrict__ B,
+                                                  const int* __restrict__ perm, int64_t d, int nb, int64_t bid) {
   const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
   const int r = threadIdx.x / kJB, c = threadIdx.x % kJB;
-  const int64_t first = (int64_t)blockIdx.x * kPermBlocks;
+  const int64_t first = bid * kPermBlocks;
   // (a, b) of the first block, then walk along the packed order
   int64_t blk = first;
   int a = 0;
@@ -1146,12 +1155,20 @@ k_pk_permute(const double* __restrict__ A, double* __restrict__ B, const int* __
   for (int q = 0; q < kPermBlocks; ++q)
     if (first + q < nblk) B[(first + q) * (kJB * kJB) + threadIdx.x] = x[q];
 }
+__global__ void __launch_bounds__(256)
+k_pk_permute(const double* __restrict__ A, double* __restrict__ B, const int* __restrict__ perm, int64_t d,
+             int nb) {
+  pk_permute_blocks(A, B, perm, d, nb, blockIdx.x);
+}
 
-__global__ void k_row_gather(const float* __restrict__ src, float* __restrict__ dst, const int* __restrict__ perm,
-                             int64_t d) {
-  const int64_t k = blockIdx.x;
+__device__ __forceinline__ void row_gather_row(const float* __restrict__ src, float* __restrict__ dst,
+                                               const int* __restrict__ perm, int64_t d, int64_t k) {
   const int64_t p = perm[k];
   for (int64_t a = threadIdx.x; a < d; a += blockDim.x) dst[k * d + a] = src[p * d + a];
+}
+__global__ void k_row_gather(const float* __restrict__ src, float* __restrict__ dst, const int* __restrict__ perm,
+                             int64_t d) {
+  row_gather_row(src, dst, perm, d, blockIdx.x);
 }
 
 hipError_t launch_jac_sort(const MatView& v, hipStream_t s) {
@@ -1177,6 +1194,191 @@ hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s) {
                      n_pad, v.perm);
   hipLaunchKernelGGL(k_permute, dim3((unsigned)v.d), dim3(256), 0, s, v.Utw, v.sigma_w, v.perm, v.d,
                      v.Ut, v.sigma, v.J, v.r, v.ctl, v.info, v.status, max_sweeps);
+  return hipGetLastError();
+}
+
+
+// ---------------------------------------------------------------------------
+// Joint refresh: the sweeps of several matrices (one group size NG) in the
+// same launches.  Every matrix owns a range of blocks of each launch (tables
+// of first blocks); a block finds its matrix and runs the per-matrix code on
+// that matrix's buffers, so each matrix computes exactly what its own
+// launches compute.  A matrix past its last round, or converged, leaves.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int joint_find(const int* __restrict__ first, int num, int b) {
+  int lo = 0, hi = num - 1;   // the last m with first[m] <= b
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ void k_joint_diag_sqrt(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const MatView& v = jm[m].v[par];
+  if (v.ctl->converged) return;
+  diag_sqrt_at(v.Apk, v.d, jm[m].nb, v.sigma_w, (int64_t)(blockIdx.x - first[m]) * blockDim.x + threadIdx.x);
+}
+
+__global__ void __launch_bounds__(1024) k_joint_sort_desc(const JointMat* __restrict__ jm, int par) {
+  const MatView& v = jm[blockIdx.x].v[par];
+  if (v.ctl->converged) return;
+  extern __shared__ __align__(16) unsigned char dyn[];
+  int n_pad = 2;
+  while (n_pad < v.d) n_pad <<= 1;
+  sort_desc_block(v.sigma_w, (int)v.d, n_pad, v.perm, reinterpret_cast<uint64_t*>(dyn));
+}
+
+__global__ void __launch_bounds__(256)
+k_joint_pk_permute(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const MatView& v = jm[m].v[par];
+  if (v.ctl->converged) return;
+  pk_permute_blocks(v.Apk, v.Apk2, v.perm, v.d, jm[m].nb, blockIdx.x - first[m]);
+}
+
+__global__ void k_joint_row_gather(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const MatView& v = jm[m].v[par];
+  if (v.ctl->converged) return;
+  row_gather_row(v.Utw, v.W, v.perm, v.d, blockIdx.x - first[m]);
+}
+
+template <int NG>
+__global__ void __launch_bounds__(JacShape<NG>::NT)
+k_joint_solve(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par, int round,
+              float tol, int max_inner, double floor_rel2) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const JointMat& J = jm[m];
+  const MatView& v = J.v[par];
+  if (v.ctl->converged || round >= J.rounds) return;
+  __shared__ SolveLds<NG> lds;
+  const int64_t vb = (int64_t)J.groups * JacShape<NG>::NR * JacShape<NG>::NR, p = round & 1;
+  solve_group<NG>(v.Apk, v.ctl, round, J.seats, J.nb, tol, max_inner, floor_rel2, v.Vrot + p * vb, v.V64 + p * vb,
+                  v.skip + p * J.groups, blockIdx.x - first[m], lds);
+}
+
+// the solves of `round` (matrices with more rounds) beside the rotation of U^T
+// rows by round - 1 (matrices whose sweep reached it)
+template <int NG>
+__global__ void __launch_bounds__(JacShape<NG>::NT)
+k_joint_solve_apply(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par, int round,
+                    float tol, int max_inner, double floor_rel2) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const JointMat& J = jm[m];
+  const MatView& v = J.v[par];
+  if (v.ctl->converged || round > J.rounds) return;
+  __shared__ JacLds<NG> lds;
+  const int64_t vb = (int64_t)J.groups * JacShape<NG>::NR * JacShape<NG>::NR;
+  const int b = blockIdx.x - first[m];
+  if (b < J.groups) {
+    if (round < J.rounds) {
+      const int64_t p = round & 1;
+      solve_group<NG>(v.Apk, v.ctl, round, J.seats, J.nb, tol, max_inner, floor_rel2, v.Vrot + p * vb,
+                      v.V64 + p * vb, v.skip + p * J.groups, b, lds.s);
+    }
+  } else {
+    const int idx = b - J.groups;
+    const int64_t q = (round - 1) & 1;
+    apply_chunk<NG>(v.Utw, v.d, v.Vrot + q * vb, v.skip + q * J.groups, round - 1, J.seats, J.nb, idx / J.chunks,
+                    idx % J.chunks, J.width, lds.Va);
+  }
+}
+
+template <int NG>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+k_joint_update(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par, int round) {
+  const int m = joint_find(first, num, blockIdx.x);
+  const JointMat& J = jm[m];
+  const MatView& v = J.v[par];
+  if (v.ctl->converged || round >= J.rounds) return;
+  __shared__ double S[JacShape<NG>::NR][JacShape<NG>::NR + 1];
+  const int64_t vb = (int64_t)J.groups * JacShape<NG>::NR * JacShape<NG>::NR, p = round & 1;
+  update_pair<NG>(v.Apk, v.V64 + p * vb, v.skip + p * J.groups, round, J.seats, J.nb, J.groups,
+                  blockIdx.x - first[m], S);
+}
+
+// the sweep's check of every matrix, and its converged flag for the host
+__global__ void k_joint_check(const JointMat* __restrict__ jm, float tol, int* __restrict__ flags) {
+  JacCtl* ctl = jm[blockIdx.x].v[0].ctl;
+  if (threadIdx.x != 0) return;
+  if (!ctl->converged) {
+    if (ctl->sweeps < (uint32_t)kHistory) ctl->history[ctl->sweeps] = ctl->sweep_max_bits;
+    ctl->sweeps += 1;
+    if (__uint_as_float(ctl->sweep_max_bits) <= tol) ctl->converged = 1;
+    ctl->sweep_max_bits = 0;
+  }
+  flags[blockIdx.x] = (int)ctl->converged;
+}
+
+void joint_fill(JointMat& J, int (&blocks)[kJointKinds]) {
+  const int64_t d = J.v[0].d;
+  const int ng = jac_group_blocks(d);
+  J.nb = jac_blocks(d);
+  J.seats = jac_seats(d);
+  J.groups = jac_groups(d);
+  J.rounds = jac_rounds(d);
+  J.width = JAC_CHUNK * (ng == 4 ? JacShape<4>::NT : JacShape<2>::NT) / 256;
+  J.chunks = (int)((d + J.width - 1) / J.width);
+  const int64_t nblk = (int64_t)J.nb * (J.nb + 1) / 2;
+  blocks[kJointSolve] = J.groups;
+  blocks[kJointSolveApply] = J.groups + J.groups * J.chunks;
+  blocks[kJointUpdate] = J.groups * (J.groups + 1) / 2;
+  blocks[kJointDiag] = (int)((d + 255) / 256);
+  blocks[kJointPermute] = (int)((nblk + kPermBlocks - 1) / kPermBlocks);
+  blocks[kJointGather] = (int)d;
+}
+
+static const int* joint_table(const JointPlan& jp, int kind) { return jp.first + (int64_t)kind * (jp.num + 1); }
+
+hipError_t launch_joint_sort(const JointPlan& jp, int par, hipStream_t s) {
+  hipLaunchKernelGGL(k_joint_diag_sqrt, dim3((unsigned)jp.total[kJointDiag]), dim3(256), 0, s, jp.jm,
+                     joint_table(jp, kJointDiag), jp.num, par);
+  hipLaunchKernelGGL(k_joint_sort_desc, dim3((unsigned)jp.num), dim3(1024), (size_t)jp.npad_max * 8, s, jp.jm, par);
+  hipLaunchKernelGGL(k_joint_pk_permute, dim3((unsigned)jp.total[kJointPermute]), dim3(256), 0, s, jp.jm,
+                     joint_table(jp, kJointPermute), jp.num, par);
+  hipLaunchKernelGGL(k_joint_row_gather, dim3((unsigned)jp.total[kJointGather]), dim3(256), 0, s, jp.jm,
+                     joint_table(jp, kJointGather), jp.num, par);
+  return hipGetLastError();
+}
+
+hipError_t launch_joint_solve(const JointPlan& jp, int par, int round, float tol, int max_inner, double floor_rel2,
+                              hipStream_t s) {
+  const int* f = joint_table(jp, kJointSolve);
+  if (jp.ng == 4)
+    hipLaunchKernelGGL(k_joint_solve<4>, dim3((unsigned)jp.total[kJointSolve]), dim3(JacShape<4>::NT), 0, s, jp.jm,
+                       f, jp.num, par, round, tol, max_inner, floor_rel2);
+  else
+    hipLaunchKernelGGL(k_joint_solve<2>, dim3((unsigned)jp.total[kJointSolve]), dim3(JacShape<2>::NT), 0, s, jp.jm,
+                       f, jp.num, par, round, tol, max_inner, floor_rel2);
+  return hipGetLastError();
+}
+
+hipError_t launch_joint_solve_apply(const JointPlan& jp, int par, int round, float tol, int max_inner,
+                                    double floor_rel2, hipStream_t s) {
+  const int* f = joint_table(jp, kJointSolveApply);
+  const dim3 grid((unsigned)jp.total[kJointSolveApply]);
+  if (jp.ng == 4)
+    hipLaunchKernelGGL(k_joint_solve_apply<4>, grid, dim3(JacShape<4>::NT), 0, s, jp.jm, f, jp.num, par, round, tol,
+                       max_inner, floor_rel2);
+  else
+    hipLaunchKernelGGL(k_joint_solve_apply<2>, grid, dim3(JacShape<2>::NT), 0, s, jp.jm, f, jp.num, par, round, tol,
+                       max_inner, floor_rel2);
+  return hipGetLastError();
+}
+
+hipError_t launch_joint_update(const JointPlan& jp, int par, int round, hipStream_t s) {
+  const int* f = joint_table(jp, kJointUpdate);
+  const dim3 grid((unsigned)jp.total[kJointUpdate]);
+  if (jp.ng == 4) hipLaunchKernelGGL(k_joint_update<4>, grid, dim3(256), 0, s, jp.jm, f, jp.num, par, round);
+  else hipLaunchKernelGGL(k_joint_update<2>, grid, dim3(256), 0, s, jp.jm, f, jp.num, par, round);
+  return hipGetLastError();
+}
+
+hipError_t launch_joint_check(const JointPlan& jp, float tol, hipStream_t s) {
+  hipLaunchKernelGGL(k_joint_check, dim3((unsigned)jp.num), dim3(64), 0, s, jp.jm, tol, jp.flags);
   return hipGetLastError();
 }
 

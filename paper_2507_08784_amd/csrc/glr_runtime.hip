@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -40,9 +41,19 @@ struct WsLayout {
       off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
   uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rV64, off_rgpart, off_rskip, off_rctl, off_rsigw,
       off_rperm;
-  uint64_t lane_bytes;   // one copy of the scratch above, sized by the largest matrix
-  int lanes;             // copies: one per stream of glr_step
   uint64_t bytes;
+};
+
+// The workspace: one scratch region per matrix, sized by that matrix (so that
+// matrices on different streams, and the sweeps of a joint refresh, never
+// share one), then the views of the joint refresh (two per matrix: the
+// buffer parities of the reordering) and its per-launch block offsets.
+struct WsPlan {
+  std::vector<WsLayout> mats;
+  std::vector<uint64_t> base;
+  uint64_t off_views = 0, off_first = 0;
+  uint64_t bytes = 0;
+  int lanes = 1;
 };
 
 struct Dims {
@@ -147,12 +158,12 @@ uint64_t state_bytes_of(const glr_config* c) {
   return o;
 }
 
-WsLayout ws_layout(const glr_config* c) {
+WsLayout ws_layout(const glr_config* c, int first, int last) {
   uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_groups = 0, mx_vbuf = 0, mx_d = 0;
   uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
   uint64_t r_gram = 0, r_groups = 0, r_vbuf = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
-  for (int i = 0; i < c->num_mats; ++i) {
+  for (int i = first; i < last; ++i) {
     const Dims x = dims_of(c, i);
     mx(mx_mn, (uint64_t)(x.m * x.n));
     mx(mx_Q, (uint64_t)c->num_workers * (uint64_t)x.r * (uint64_t)x.D);
@@ -232,10 +243,25 @@ WsLayout ws_layout(const glr_config* c) {
   w.off_rctl = take(sizeof(JacCtl));
   w.off_rsigw = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
   w.off_rperm = take(s_Kd ? 2 * kMaxSubK * 4 : 4);
-  w.lane_bytes = o;
-  w.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
-  w.bytes = o * (uint64_t)w.lanes;
+  w.bytes = o;
   return w;
+}
+
+WsPlan ws_plan(const glr_config* c) {
+  WsPlan p;
+  uint64_t o = 0;
+  for (int i = 0; i < c->num_mats; ++i) {
+    p.mats.push_back(ws_layout(c, i, i + 1));
+    p.base.push_back(o);
+    o = align_up(o + p.mats.back().bytes);
+  }
+  p.off_views = o;
+  o = align_up(o + (uint64_t)c->num_mats * sizeof(JointMat));
+  p.off_first = o;   // kJointKinds tables of num_mats + 1 first blocks, then num_mats flags
+  o = align_up(o + ((uint64_t)kJointKinds * ((uint64_t)c->num_mats + 1) + (uint64_t)c->num_mats) * 4);
+  p.bytes = o;
+  p.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
+  return p;
 }
 
 // Matrix -> lane by longest-processing-time-first on an estimate of each matrix's
@@ -277,7 +303,7 @@ struct glr_handle {
   glr_config cfg;
   std::vector<glr_shape> shapes;
   std::vector<glr_mat_layout> lay;
-  WsLayout ws;
+  WsPlan ws;
   char* state = nullptr;
   char* work = nullptr;
   int device = 0;
@@ -289,7 +315,12 @@ struct glr_handle {
   double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
   int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
   bool prof = false;
-  int lanes = 1;                       // streams in use (<= ws.lanes)
+  bool joint = false;                  // refresh steps sweep all matrices in shared launches
+  std::vector<JointMat> jm;            // host copies of the joint tables (kept for the async upload)
+  std::vector<int> jfirst;
+  std::vector<int> jflags;             // converged flags read back after every joint sweep
+  JointPlan jp;
+  int lanes = 1;                       // streams in use (<= min(num_mats, 4))
   std::vector<int> lane_of;            // lane of each matrix
   hipStream_t lane_s[kMaxLanes] = {};  // non-blocking streams, created when ws.lanes > 1
   hipEvent_t ev_fork = nullptr;
@@ -344,47 +375,49 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G, int lane) {
   v.status = (uint32_t*)s;
   v.X = X;
   v.G = G;
-  char* w = h->work + (uint64_t)lane * h->ws.lane_bytes;
-  v.Mbar = (float*)(w + h->ws.off_Mbar);
-  v.Q = (float*)(w + h->ws.off_Q);
-  v.Qpart = (float*)(w + h->ws.off_Qpart);
-  v.lam_part = (float*)(w + h->ws.off_lam);
-  v.W = (float*)(w + h->ws.off_W);
-  v.Utw = (float*)(w + h->ws.off_Utw);
-  v.Apk = (double*)(w + h->ws.off_gram);
-  v.Apk2 = (double*)(w + h->ws.off_gram2);
-  v.Vrot = (float*)(w + h->ws.off_V);
-  v.V64 = (double*)(w + h->ws.off_V64);
-  v.gpart = (double*)(w + h->ws.off_gpart);   // sized for every matrix whose Gram is split
-  v.skip = (int*)(w + h->ws.off_skip);
-  v.ctl = (JacCtl*)(w + h->ws.off_ctl);
-  v.sigma_w = (float*)(w + h->ws.off_sigw);
-  v.perm = (int*)(w + h->ws.off_perm);
-  v.sub_P = (float*)(w + h->ws.off_sP);
-  v.sub_Pn = (float*)(w + h->ws.off_sPn);
-  v.sub_Z = (float*)(w + h->ws.off_sZ);
-  v.sub_Zt = (float*)(w + h->ws.off_sZt);
-  v.sub_R = (float*)(w + h->ws.off_sR);
-  v.sub_part = (float*)(w + h->ws.off_spart);
-  v.sub_S = (double*)(w + h->ws.off_sS);
-  v.sub_L = (double*)(w + h->ws.off_sL);
-  v.sub_Dinv = (double*)(w + h->ws.off_sDinv);
-  v.sub_Li = (double*)(w + h->ws.off_sLi);
-  v.sub_T = (double*)(w + h->ws.off_sT);
-  v.sub_Linv = (float*)(w + h->ws.off_sLinv);
-  v.sub_C = (float*)(w + h->ws.off_sC);
-  v.sub_sums = (double*)(w + h->ws.off_ssums);
-  v.sub_ctl = (SubCtl*)(w + h->ws.off_sctl);
-  v.rr_Utw = (float*)(w + h->ws.off_rUtw);
-  v.rr_Y = (float*)(w + h->ws.off_rY);
-  v.rr_Apk = (double*)(w + h->ws.off_rgram);
-  v.rr_V = (float*)(w + h->ws.off_rV);
-  v.rr_V64 = (double*)(w + h->ws.off_rV64);
-  v.rr_gpart = (double*)(w + h->ws.off_rgpart);
-  v.rr_skip = (int*)(w + h->ws.off_rskip);
-  v.rr_ctl = (JacCtl*)(w + h->ws.off_rctl);
-  v.rr_sigw = (float*)(w + h->ws.off_rsigw);
-  v.rr_perm = (int*)(w + h->ws.off_rperm);
+  (void)lane;
+  const WsLayout& WL = h->ws.mats[(size_t)mat];
+  char* w = h->work + h->ws.base[(size_t)mat];
+  v.Mbar = (float*)(w + WL.off_Mbar);
+  v.Q = (float*)(w + WL.off_Q);
+  v.Qpart = (float*)(w + WL.off_Qpart);
+  v.lam_part = (float*)(w + WL.off_lam);
+  v.W = (float*)(w + WL.off_W);
+  v.Utw = (float*)(w + WL.off_Utw);
+  v.Apk = (double*)(w + WL.off_gram);
+  v.Apk2 = (double*)(w + WL.off_gram2);
+  v.Vrot = (float*)(w + WL.off_V);
+  v.V64 = (double*)(w + WL.off_V64);
+  v.gpart = (double*)(w + WL.off_gpart);   // sized for every matrix whose Gram is split
+  v.skip = (int*)(w + WL.off_skip);
+  v.ctl = (JacCtl*)(w + WL.off_ctl);
+  v.sigma_w = (float*)(w + WL.off_sigw);
+  v.perm = (int*)(w + WL.off_perm);
+  v.sub_P = (float*)(w + WL.off_sP);
+  v.sub_Pn = (float*)(w + WL.off_sPn);
+  v.sub_Z = (float*)(w + WL.off_sZ);
+  v.sub_Zt = (float*)(w + WL.off_sZt);
+  v.sub_R = (float*)(w + WL.off_sR);
+  v.sub_part = (float*)(w + WL.off_spart);
+  v.sub_S = (double*)(w + WL.off_sS);
+  v.sub_L = (double*)(w + WL.off_sL);
+  v.sub_Dinv = (double*)(w + WL.off_sDinv);
+  v.sub_Li = (double*)(w + WL.off_sLi);
+  v.sub_T = (double*)(w + WL.off_sT);
+  v.sub_Linv = (float*)(w + WL.off_sLinv);
+  v.sub_C = (float*)(w + WL.off_sC);
+  v.sub_sums = (double*)(w + WL.off_ssums);
+  v.sub_ctl = (SubCtl*)(w + WL.off_sctl);
+  v.rr_Utw = (float*)(w + WL.off_rUtw);
+  v.rr_Y = (float*)(w + WL.off_rY);
+  v.rr_Apk = (double*)(w + WL.off_rgram);
+  v.rr_V = (float*)(w + WL.off_rV);
+  v.rr_V64 = (double*)(w + WL.off_rV64);
+  v.rr_gpart = (double*)(w + WL.off_rgpart);
+  v.rr_skip = (int*)(w + WL.off_rskip);
+  v.rr_ctl = (JacCtl*)(w + WL.off_rctl);
+  v.rr_sigw = (float*)(w + WL.off_rsigw);
+  v.rr_perm = (int*)(w + WL.off_rperm);
   return v;
 }
 
@@ -487,15 +520,28 @@ hipError_t jacobi_sweep(glr_handle* h, const MatView& v, int rounds, int g_solve
 
 // Semi-Lazy SVD refresh: complete U of Mbar by block Jacobi on the fp64 Gram of
 // W = U_prev^T Mo
+glr_status svd_begin(glr_handle* h, const MatView& v, int64_t t, hipStream_t s) {
+  const bool warm = t > 0 && !(h->cfg.flags & GLR_COLD_START);
+  ProfScope p(h, s, GLR_PROF_JAC_INIT);
+  GLR_HIP(h, launch_jac_init(v, warm, s));
+  return GLR_OK;
+}
+
+// sigma, the sorted U, and its re-orthonormalisation, from the view of the
+// last sweep
+glr_status svd_end(glr_handle* h, const MatView& v, hipStream_t s) {
+  ProfScope p(h, s, GLR_PROF_JAC_FINISH);
+  GLR_HIP(h, launch_jac_finish(v, h->cfg.max_sweeps, s));
+  GLR_HIP(h, launch_reorth(v, s));
+  return GLR_OK;
+}
+
 glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
-  const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
   MatView v = v0;   // the sort swaps Apk <-> Apk2 and Utw <-> W
   ProfScope all(h, s, GLR_PROF_REFRESH);
-  {
-    ProfScope p(h, s, GLR_PROF_JAC_INIT);
-    GLR_HIP(h, launch_jac_init(v, warm, s));
-  }
+  glr_status st = svd_begin(h, v, t, s);
+  if (st != GLR_OK) return st;
   const int rounds = jac_rounds(v.d);
   for (int sw = 0; sw < c.max_sweeps; ++sw) {
     if (h->jac_sort == 1 || (h->jac_sort == 2 && sw == 0)) {
@@ -510,10 +556,7 @@ glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t 
     GLR_HIP(h, hipStreamSynchronize(s));
     if (conv) break;
   }
-  ProfScope p(h, s, GLR_PROF_JAC_FINISH);
-  GLR_HIP(h, launch_jac_finish(v, c.max_sweeps, s));
-  GLR_HIP(h, launch_reorth(v, s));
-  return GLR_OK;
+  return svd_end(h, v, s);
 }
 
 // tau = 1 refresh: top-r block of U by oversampled subspace iteration and a
@@ -551,27 +594,17 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   return GLR_OK;
 }
 
-glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s, int lane) {
+// the error-feedback mean M-bar of one matrix
+glr_status step_head(glr_handle* h, const MatView& v, hipStream_t s) {
+  ProfScope p(h, s, GLR_PROF_EF_MEAN);
+  GLR_HIP(h, launch_ef_mean(v, (h->cfg.flags & GLR_CHECK_FINITE) != 0, s));
+  return GLR_OK;
+}
+
+// projection on the chosen columns, their mean, residual and optimizer update
+glr_status step_tail(glr_handle* h, const MatView& v, bool refresh, hipStream_t s) {
   const glr_config& c = h->cfg;
-  MatView v = view_of(h, mat, X, G, lane);
-  const bool refresh = (t % c.tau) == 0;
   OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
-  {
-    ProfScope p(h, s, GLR_PROF_EF_MEAN);
-    GLR_HIP(h, launch_ef_mean(v, (c.flags & GLR_CHECK_FINITE) != 0, s));
-  }
-  if (refresh) {
-    glr_status st = use_subspace(c.tau, v.r, v.d) ? refresh_subspace(h, v, t, s) : refresh_svd(h, v, t, s);
-    if (st != GLR_OK) return st;
-  } else if (v.r < v.d) {
-    {
-      ProfScope p(h, s, GLR_PROF_SELECT);
-      GLR_HIP(h, launch_sel_scores(v, c.select != GLR_SELECT_EXACT, c.select == GLR_SELECT_APPROX_BF16, c.seed, t,
-                                   s));
-    }
-    ProfScope p(h, s, GLR_PROF_TOPR);
-    GLR_HIP(h, launch_topr(v, s));
-  }
   {
     ProfScope p(h, s, GLR_PROF_PROJ);
     GLR_HIP(h, launch_proj(v, s));
@@ -590,11 +623,35 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
   return GLR_OK;
 }
 
-// the matrices of one lane, in index order, on that lane's stream and workspace
-glr_status run_lane(glr_handle* h, int lane, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s, int lane) {
+  const glr_config& c = h->cfg;
+  MatView v = view_of(h, mat, X, G, lane);
+  const bool refresh = (t % c.tau) == 0;
+  glr_status hs = step_head(h, v, s);
+  if (hs != GLR_OK) return hs;
+  if (refresh) {
+    glr_status st = use_subspace(c.tau, v.r, v.d) ? refresh_subspace(h, v, t, s) : refresh_svd(h, v, t, s);
+    if (st != GLR_OK) return st;
+  } else if (v.r < v.d) {
+    {
+      ProfScope p(h, s, GLR_PROF_SELECT);
+      GLR_HIP(h, launch_sel_scores(v, c.select != GLR_SELECT_EXACT, c.select == GLR_SELECT_APPROX_BF16, c.seed, t,
+                                   s));
+    }
+    ProfScope p(h, s, GLR_PROF_TOPR);
+    GLR_HIP(h, launch_topr(v, s));
+  }
+  return step_tail(h, v, refresh, s);
+}
+
+// per-matrix work (matrix, lane, the lane's stream)
+using MatFn = std::function<glr_status(int, int, hipStream_t)>;
+
+// the matrices of one lane, in index order, on that lane's stream
+glr_status run_lane(glr_handle* h, int lane, const MatFn& fn, hipStream_t s) {
   for (int i = 0; i < h->cfg.num_mats; ++i) {
     if (h->lane_of[(size_t)i] != lane) continue;
-    glr_status st = step_one(h, i, X[i], G[i], t, s, lane);
+    glr_status st = fn(i, lane, s);
     if (st != GLR_OK) return st;
   }
   return GLR_OK;
@@ -604,8 +661,9 @@ glr_status run_lane(glr_handle* h, int lane, float* const* X, const float* const
 // (a refresh blocks its thread once per sweep on the convergence flag, so one
 // thread could not keep the other streams fed).  The lanes start after the work
 // already on `s` and `s` waits for all of them.
-glr_status step_lanes(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+glr_status on_lanes(glr_handle* h, hipStream_t s, const MatFn& fn) {
   const int L = h->lanes;
+  if (L <= 1) return run_lane(h, 0, fn, s);
   GLR_HIP(h, hipEventRecord(h->ev_fork, s));
   for (int k = 0; k < L; ++k) GLR_HIP(h, hipStreamWaitEvent(h->lane_s[k], h->ev_fork, 0));
   glr_status st[kMaxLanes];
@@ -613,18 +671,18 @@ glr_status step_lanes(glr_handle* h, float* const* X, const float* const* G, int
   for (int k = 1; k < L; ++k) {
     st[k] = GLR_OK;
     try {
-      th[k] = std::thread([h, k, X, G, t, &st] {
+      th[k] = std::thread([h, k, &fn, &st] {
         const hipError_t e = hipSetDevice(h->device);
-        st[k] = e == hipSuccess ? run_lane(h, k, X, G, t, h->lane_s[k]) : hip_fail(h, e, "hipSetDevice");
+        st[k] = e == hipSuccess ? run_lane(h, k, fn, h->lane_s[k]) : hip_fail(h, e, "hipSetDevice");
       });
     } catch (...) {
       // no thread: this lane runs on the calling thread after lane 0
     }
   }
-  st[0] = run_lane(h, 0, X, G, t, h->lane_s[0]);
+  st[0] = run_lane(h, 0, fn, h->lane_s[0]);
   for (int k = 1; k < L; ++k) {
     if (th[k].joinable()) th[k].join();
-    else st[k] = run_lane(h, k, X, G, t, h->lane_s[k]);
+    else st[k] = run_lane(h, k, fn, h->lane_s[k]);
   }
   glr_status out = GLR_OK;
   for (int k = 0; k < L; ++k)
@@ -635,6 +693,110 @@ glr_status step_lanes(glr_handle* h, float* const* X, const float* const* G, int
     if (e != hipSuccess && out == GLR_OK) out = hip_fail(h, e, "joining the lane streams");
   }
   return out;
+}
+
+// A refresh step of several matrices: M-bar and the Jacobi start of every
+// matrix on the lanes; then the sweeps of all matrices in shared launches on
+// `s`, one convergence read per sweep for all of them (a matrix that has
+// converged leaves the launches); then sigma, U and the rest of the step on the
+// lanes.  Each matrix runs the same kernels on the same data as its own
+// refresh, so the results are bitwise those of the per-matrix order.
+glr_status step_joint(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  const int num = c.num_mats;
+  glr_status st = on_lanes(h, s, [&](int i, int lane, hipStream_t ls) -> glr_status {
+    const MatView v = view_of(h, i, X[i], G[i], lane);
+    const glr_status r = step_head(h, v, ls);
+    return r != GLR_OK ? r : svd_begin(h, v, t, ls);
+  });
+  if (st != GLR_OK) return st;
+  const JointPlan& jp = h->jp;
+  std::vector<int> last((size_t)num, -1);   // the sweep after which each matrix converged
+  int left = num, sweeps = 0;
+  for (int sw = 0; sw < c.max_sweeps && left > 0; ++sw, ++sweeps) {
+    const int par = sw & 1, p = par ^ 1;   // the sort reads parity par and fills the other
+    GLR_HIP(h, launch_joint_sort(jp, par, s));
+    GLR_HIP(h, launch_joint_solve(jp, p, 0, c.tol, h->jac_inner, h->jac_floor2, s));
+    for (int k = 0; k < jp.rounds_max; ++k) {
+      GLR_HIP(h, launch_joint_update(jp, p, k, s));
+      GLR_HIP(h, launch_joint_solve_apply(jp, p, k + 1, c.tol, h->jac_inner, h->jac_floor2, s));
+    }
+    GLR_HIP(h, launch_joint_check(jp, c.tol, s));
+    GLR_HIP(h, hipMemcpyAsync(h->jflags.data(), jp.flags, (size_t)num * sizeof(int), hipMemcpyDeviceToHost, s));
+    GLR_HIP(h, hipStreamSynchronize(s));
+    for (int i = 0; i < num; ++i)
+      if (h->jflags[(size_t)i] && last[(size_t)i] < 0) {
+        last[(size_t)i] = sw;
+        --left;
+      }
+  }
+  return on_lanes(h, s, [&](int i, int lane, hipStream_t ls) -> glr_status {
+    const MatView v = view_of(h, i, X[i], G[i], lane);
+    const int ran = last[(size_t)i] >= 0 ? last[(size_t)i] : sweeps - 1;
+    const glr_status r = svd_end(h, h->jm[(size_t)i].v[(ran + 1) & 1], ls);
+    return r != GLR_OK ? r : step_tail(h, v, true, ls);
+  });
+}
+
+// the joint tables: two views per matrix (the buffer parities of the
+// reordering) and the first block of each matrix in every joint launch
+hipError_t joint_setup(glr_handle* h, hipStream_t s) {
+  const int num = h->cfg.num_mats;
+  h->jm.resize((size_t)num);
+  std::vector<int> blocks((size_t)num * kJointKinds);
+  JointPlan& jp = h->jp;
+  jp.num = num;
+  jp.ng = jac_group_blocks(h->lay[0].d);
+  for (int i = 0; i < num; ++i) {
+    JointMat& J = h->jm[(size_t)i];
+    J.v[0] = view_of(h, i, nullptr, nullptr, 0);
+    J.v[1] = J.v[0];
+    std::swap(J.v[1].Apk, J.v[1].Apk2);
+    std::swap(J.v[1].Utw, J.v[1].W);
+    int b[kJointKinds];
+    joint_fill(J, b);
+    for (int k = 0; k < kJointKinds; ++k) blocks[(size_t)i * kJointKinds + k] = b[k];
+    jp.rounds_max = std::max(jp.rounds_max, J.rounds);
+    int n_pad = 2;
+    while (n_pad < J.v[0].d) n_pad <<= 1;
+    jp.npad_max = std::max(jp.npad_max, n_pad);
+  }
+  h->jfirst.assign((size_t)kJointKinds * (num + 1), 0);
+  for (int k = 0; k < kJointKinds; ++k) {
+    int64_t acc = 0;
+    for (int i = 0; i < num; ++i) {
+      h->jfirst[(size_t)k * (num + 1) + i] = (int)acc;
+      acc += blocks[(size_t)i * kJointKinds + k];
+    }
+    if (acc > INT32_MAX) return hipErrorInvalidValue;
+    h->jfirst[(size_t)k * (num + 1) + num] = (int)acc;
+    jp.total[k] = (int)acc;
+  }
+  h->jflags.assign((size_t)num, 0);
+  jp.jm = (const JointMat*)(h->work + h->ws.off_views);
+  jp.first = (const int*)(h->work + h->ws.off_first);
+  jp.flags = (int*)(h->work + h->ws.off_first) + (size_t)kJointKinds * (num + 1);
+  hipError_t e = hipMemcpyAsync((void*)jp.jm, h->jm.data(), (size_t)num * sizeof(JointMat), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync((void*)jp.first, h->jfirst.data(), h->jfirst.size() * sizeof(int), hipMemcpyHostToDevice, s);
+  return e;
+}
+
+// a refresh step sweeps all matrices jointly when they take the full-basis
+// refresh with one group size, the sweeps reorder every time, and no matrix is
+// large enough to fill the chip with its own launches (from d = 4096 on, the
+// per-matrix sweeps on concurrent streams measured a few per cent faster)
+constexpr int64_t kJointMaxDim = 2048;
+bool joint_allowed(const glr_handle* h) {
+  const glr_config& c = h->cfg;
+  if (c.num_mats < 2 || c.tau == 1 || h->jac_sort != 1) return false;
+  if (const char* e = getenv("GLR_JAC_JOINT"))
+    if (atoi(e) == 0) return false;
+  for (int i = 0; i < c.num_mats; ++i) {
+    const int64_t d = h->lay[(size_t)i].d;
+    if (d > kJointMaxDim || jac_group_blocks(d) != jac_group_blocks(h->lay[0].d)) return false;
+  }
+  return true;
 }
 
 void release_lanes(glr_handle* h) {
@@ -665,7 +827,7 @@ glr_status glr_workspace_bytes(const glr_config* cfg, size_t* state_bytes, size_
   if (s != GLR_OK) { g_create_error = why; return s; }
   if (!state_bytes || !ws_bytes) { g_create_error = "output pointer is NULL"; return GLR_ERR_INVALID_ARG; }
   *state_bytes = (size_t)state_bytes_of(cfg);
-  *ws_bytes = (size_t)ws_layout(cfg).bytes;
+  *ws_bytes = (size_t)ws_plan(cfg).bytes;
   return GLR_OK;
 }
 
@@ -691,7 +853,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   if (!aligned(d_state) || !aligned(d_ws))
     return fail(nullptr, GLR_ERR_INVALID_ARG, "state and workspace must be 256-byte aligned");
   const uint64_t need_s = state_bytes_of(cfg);
-  const WsLayout wl = ws_layout(cfg);
+  const WsPlan wl = ws_plan(cfg);
   if (state_bytes < need_s || ws_bytes < wl.bytes)
     return fail(nullptr, GLR_ERR_BUFFER_TOO_SMALL,
                 fmt("need %llu state bytes and %llu workspace bytes", (unsigned long long)need_s,
@@ -734,6 +896,10 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[k], hipEventDisableTiming);
   }
   if (e == hipSuccess && h->lanes > 1) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess && joint_allowed(h)) {
+    h->joint = true;
+    e = joint_setup(h, st);
+  }
   if (e != hipSuccess) {
     std::string m = fmt("glr_create: %s", hipGetErrorString(e));
     release_lanes(h);
@@ -756,8 +922,13 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64
       return fail(h, GLR_ERR_INVALID_ARG, fmt("matrix %d: buffers must be 256-byte aligned", i));
   }
   hipStream_t s = (hipStream_t)stream;
-  if (h->lanes > 1 && !h->prof) {
-    glr_status st = step_lanes(h, X, G, t, s);
+  if (h->joint && !h->prof && t % h->cfg.tau == 0) {
+    glr_status st = step_joint(h, X, G, t, s);
+    if (st != GLR_OK) return st;
+  } else if (h->lanes > 1 && !h->prof) {
+    glr_status st = on_lanes(h, s, [&](int i, int lane, hipStream_t ls) {
+      return step_one(h, i, X[i], G[i], t, ls, lane);
+    });
     if (st != GLR_OK) return st;
   } else {
     // one matrix, or profiling: every matrix in order on `s` (event brackets

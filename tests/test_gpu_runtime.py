@@ -159,3 +159,42 @@ def test_concurrent_lanes_match_the_one_stream_order(gpu_lib, monkeypatch):
         assert torch.equal(c1.E(l), c2.E(l)), f"mat {l}: E differs"
         assert torch.equal(c1.Ut(l), c2.Ut(l)), f"mat {l}: U differs"
         assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
+
+
+@pytest.mark.parametrize("name,override", [
+    ("mixed_small", {}),
+    # twelve of the conv layers, pairs of 16-row blocks, refreshed at t = 0 and 3
+    ("conv_50", {"tau": 3}),
+    # three matrices with d in [1009, 1024]: groups of four blocks, different sweep counts
+    ("seats64_left", {"shapes": ((1012, 1100), (1100, 1020), (1016, 1030)), "tau": 2}),
+])
+def test_joint_refresh_matches_the_per_matrix_sweeps(gpu_lib, monkeypatch, name, override):
+    # a refresh step of several matrices sweeps all of them in shared launches;
+    # every matrix must end bitwise where its own sweeps take it
+    import torch
+    wl = get_workload(name, **override)
+    if name == "conv_50":
+        wl = get_workload(name, shapes=wl.shapes[:12], **override)
+    T = min(wl.steps, wl.tau + 2)
+    _say(name, "joint vs per-matrix refresh over", T, "steps,", len(wl.shapes), "matrices")
+    G = _inputs(wl, T)
+    runs = []
+    for joint in ("0", None):
+        if joint is None:
+            monkeypatch.delenv("GLR_JAC_JOINT", raising=False)
+        else:
+            monkeypatch.setenv("GLR_JAC_JOINT", joint)
+        comp = _make(gpu_lib, wl)
+        X = _zeros(wl)
+        for t in range(T):
+            comp.step(X, G[t], t)
+        assert comp.sync_status() == gpu_lib.GLR_OK
+        runs.append((comp, X))
+    (c1, x1), (c2, x2) = runs
+    for l in range(len(wl.shapes)):
+        assert torch.equal(x1[l], x2[l]), f"mat {l}: X differs"
+        assert torch.equal(c1.E(l), c2.E(l)), f"mat {l}: E differs"
+        assert torch.equal(c1.Ut(l), c2.Ut(l)), f"mat {l}: U differs"
+        assert torch.equal(c1.sigma(l), c2.sigma(l)), f"mat {l}: sigma differs"
+        assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
+        assert torch.equal(c1.info(l), c2.info(l)), f"mat {l}: sweep record differs"
