@@ -45,7 +45,12 @@
  * matrices with d <= 2048 and one Jacobi group size, the sweeps of all of them
  * run in shared launches on `stream` itself, with one convergence read per
  * sweep for all matrices; each matrix still computes exactly what it computes
- * alone.  GLR_JAC_JOINT=0, read by glr_create, turns this off.
+ * alone.  GLR_JAC_JOINT=0, read by glr_create, turns this off.  Likewise a
+ * selection step of several matrices that all have d <= 2048, the same side
+ * (m > n or not) and the same rank r < d, r <= 128, launches each of its
+ * kernels once for all matrices on `stream`, after uploading that step's table
+ * of matrix views from pinned host memory the handle owns; GLR_GROUPED=0 turns
+ * this off.
  * While profiling is enabled the matrices run in order on `stream`.  The
  * environment variable GLR_LANES, read by glr_create, lowers the stream count.
  * glr_step blocks the host only on refresh steps, where it reads the

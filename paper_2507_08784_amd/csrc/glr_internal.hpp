@@ -110,6 +110,9 @@ inline int proj_splits(int64_t d, int64_t D, int r, int N) {
   return sp < 1 ? 1 : (int)sp;
 }
 
+// above this rank the residuals come first from a wider-tile kernel
+constexpr int kResidWideRank = 128;
+
 struct OptParams {
   int opt;                   // 0 MSGD, 1 Adam
   float lr, beta1, beta2, eps;
@@ -126,6 +129,32 @@ hipError_t launch_proj(const MatView& v, hipStream_t s);
 hipError_t launch_rbar(const MatView& v, hipStream_t s);
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s);
 hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s);
+
+// One matrix of a grouped selection step (device memory, rewritten every such
+// step: the view carries that step's X and G) and its projection slicing.
+struct GroupMat {
+  MatView v;
+  int splits, kslice;
+};
+// the kernels of a grouped selection step, each one launch over all matrices
+enum { kGrpEfMean = 0, kGrpSelScores, kGrpSelFinish, kGrpProj, kGrpRbar, kGrpResid, kGrpKinds };
+struct GroupPlan {
+  const GroupMat* gm = nullptr;   // num entries
+  const int* first = nullptr;     // kGrpKinds tables of num + 1 first blocks
+  int num = 0;
+  bool right = false;             // every matrix of the group has the same side, rank and kernel variants
+  int r = 0;
+  size_t topr_lds = 0;            // the largest matrix's top-r sort keys
+  int total[kGrpKinds] = {};
+};
+// the slicing of one matrix's projection and its block count in every grouped launch
+void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]);
+size_t topr_lds_bytes(int64_t d);
+// one selection step of every matrix of the plan: M-bar, the Approx-Top-r (or
+// exact) scores and their top r, the projection and its mean, the residual
+// and the optimizer update, seven launches in all
+hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
+                               int64_t t, const OptParams& o, hipStream_t s);
 
 // One matrix of a joint refresh (device memory): its views for the two buffer
 // parities of the per-sweep reordering (v[1] is v[0] with Apk <-> Apk2 and

@@ -52,6 +52,7 @@ struct WsPlan {
   std::vector<WsLayout> mats;
   std::vector<uint64_t> base;
   uint64_t off_views = 0, off_first = 0;
+  uint64_t off_gmats = 0, off_gfirst = 0;   // the grouped selection step
   uint64_t bytes = 0;
   int lanes = 1;
 };
@@ -259,6 +260,10 @@ WsPlan ws_plan(const glr_config* c) {
   o = align_up(o + (uint64_t)c->num_mats * sizeof(JointMat));
   p.off_first = o;   // kJointKinds tables of num_mats + 1 first blocks, then num_mats flags
   o = align_up(o + ((uint64_t)kJointKinds * ((uint64_t)c->num_mats + 1) + (uint64_t)c->num_mats) * 4);
+  p.off_gmats = o;
+  o = align_up(o + (uint64_t)c->num_mats * sizeof(GroupMat));
+  p.off_gfirst = o;
+  o = align_up(o + (uint64_t)kGrpKinds * ((uint64_t)c->num_mats + 1) * 4);
   p.bytes = o;
   p.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
   return p;
@@ -320,6 +325,12 @@ struct glr_handle {
   std::vector<int> jfirst;
   std::vector<int> jflags;             // converged flags read back after every joint sweep
   JointPlan jp;
+  bool grouped = false;                // selection steps launch each kernel once for all matrices
+  std::vector<int> gfirst;
+  GroupPlan gp;
+  GroupMat* gring = nullptr;           // pinned host copies of the per-step table, two slots
+  hipEvent_t gev[2] = {};              // the upload that last read each slot
+  int gslot = 0;
   int lanes = 1;                       // streams in use (<= min(num_mats, 4))
   std::vector<int> lane_of;            // lane of each matrix
   hipStream_t lane_s[kMaxLanes] = {};  // non-blocking streams, created when ws.lanes > 1
@@ -799,6 +810,90 @@ bool joint_allowed(const glr_handle* h) {
   return true;
 }
 
+// A selection step of several matrices: the per-step table of views (with
+// this step's X and G) goes up from a pinned slot, then each kernel of the
+// step runs once over all matrices on `s`.
+glr_status step_grouped(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+  const glr_config& c = h->cfg;
+  const int num = c.num_mats, slot = h->gslot;
+  h->gslot ^= 1;
+  GLR_HIP(h, hipEventSynchronize(h->gev[slot]));   // the upload that read this slot two steps ago
+  GroupMat* g = h->gring + (size_t)slot * num;
+  int blocks[kGrpKinds];
+  for (int i = 0; i < num; ++i) {
+    g[i].v = view_of(h, i, X[i], G[i], 0);
+    group_fill(g[i], blocks);
+  }
+  GLR_HIP(h, hipMemcpyAsync((void*)h->gp.gm, g, (size_t)num * sizeof(GroupMat), hipMemcpyHostToDevice, s));
+  GLR_HIP(h, hipEventRecord(h->gev[slot], s));
+  OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
+  GLR_HIP(h, launch_group_select(h->gp, (c.flags & GLR_CHECK_FINITE) != 0, c.select != GLR_SELECT_EXACT,
+                                 c.select == GLR_SELECT_APPROX_BF16, c.seed, t, op, s));
+  return GLR_OK;
+}
+
+// selection steps are grouped when every matrix has d <= 2048, a rank below d
+// and at most 128, and the same side (so the same kernel variants)
+bool group_allowed(const glr_handle* h) {
+  const glr_config& c = h->cfg;
+  if (c.num_mats < 2 || c.tau == 1) return false;
+  if (const char* e = getenv("GLR_GROUPED"))
+    if (atoi(e) == 0) return false;
+  const glr_mat_layout& L0 = h->lay[0];
+  for (int i = 0; i < c.num_mats; ++i) {
+    const glr_mat_layout& L = h->lay[(size_t)i];
+    if (L.d > kJointMaxDim || L.r >= L.d || L.r > kResidWideRank || L.r != L0.r || L.right != L0.right)
+      return false;
+  }
+  return true;
+}
+
+// block tables of the grouped launches, the pinned ring and its events
+hipError_t group_setup(glr_handle* h, hipStream_t s) {
+  const int num = h->cfg.num_mats;
+  GroupPlan& gp = h->gp;
+  gp.num = num;
+  gp.right = h->lay[0].right != 0;
+  gp.r = h->lay[0].r;
+  std::vector<int> blocks((size_t)num * kGrpKinds);
+  for (int i = 0; i < num; ++i) {
+    GroupMat g;
+    g.v = view_of(h, i, nullptr, nullptr, 0);
+    int b[kGrpKinds];
+    group_fill(g, b);
+    for (int k = 0; k < kGrpKinds; ++k) blocks[(size_t)i * kGrpKinds + k] = b[k];
+    gp.topr_lds = std::max(gp.topr_lds, topr_lds_bytes(g.v.d));
+  }
+  h->gfirst.assign((size_t)kGrpKinds * (num + 1), 0);
+  for (int k = 0; k < kGrpKinds; ++k) {
+    int64_t acc = 0;
+    for (int i = 0; i < num; ++i) {
+      h->gfirst[(size_t)k * (num + 1) + i] = (int)acc;
+      acc += blocks[(size_t)i * kGrpKinds + k];
+    }
+    if (acc > INT32_MAX) return hipErrorInvalidValue;
+    h->gfirst[(size_t)k * (num + 1) + num] = (int)acc;
+    gp.total[k] = (int)acc;
+  }
+  gp.gm = (const GroupMat*)(h->work + h->ws.off_gmats);
+  gp.first = (const int*)(h->work + h->ws.off_gfirst);
+  hipError_t e = hipMemcpyAsync((void*)gp.first, h->gfirst.data(), h->gfirst.size() * sizeof(int),
+                                hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&h->gring, 2 * (size_t)num * sizeof(GroupMat), hipHostMallocDefault);
+  for (int k = 0; e == hipSuccess && k < 2; ++k) e = hipEventCreateWithFlags(&h->gev[k], hipEventDisableTiming);
+  return e;
+}
+
+void release_group(glr_handle* h) {
+  for (int k = 0; k < 2; ++k) {
+    if (h->gev[k]) (void)hipEventSynchronize(h->gev[k]);
+    if (h->gev[k]) (void)hipEventDestroy(h->gev[k]);
+    h->gev[k] = nullptr;
+  }
+  if (h->gring) (void)hipHostFree(h->gring);
+  h->gring = nullptr;
+}
+
 void release_lanes(glr_handle* h) {
   for (int k = 0; k < kMaxLanes; ++k) {
     if (h->lane_s[k]) (void)hipStreamDestroy(h->lane_s[k]);
@@ -900,8 +995,13 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
     h->joint = true;
     e = joint_setup(h, st);
   }
+  if (e == hipSuccess && group_allowed(h)) {
+    h->grouped = true;
+    e = group_setup(h, st);
+  }
   if (e != hipSuccess) {
     std::string m = fmt("glr_create: %s", hipGetErrorString(e));
+    release_group(h);
     release_lanes(h);
     delete h;
     return fail(nullptr, GLR_ERR_DEVICE, m);
@@ -924,6 +1024,9 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64
   hipStream_t s = (hipStream_t)stream;
   if (h->joint && !h->prof && t % h->cfg.tau == 0) {
     glr_status st = step_joint(h, X, G, t, s);
+    if (st != GLR_OK) return st;
+  } else if (h->grouped && !h->prof && t % h->cfg.tau != 0) {
+    glr_status st = step_grouped(h, X, G, t, s);
     if (st != GLR_OK) return st;
   } else if (h->lanes > 1 && !h->prof) {
     glr_status st = on_lanes(h, s, [&](int i, int lane, hipStream_t ls) {
@@ -978,6 +1081,7 @@ glr_status glr_next_step(const glr_handle* h, int64_t* next_t) {
 glr_status glr_destroy(glr_handle* h) {
   if (!h) return GLR_OK;
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+  release_group(h);
   release_lanes(h);
   delete h;
   return GLR_OK;

@@ -46,14 +46,14 @@ hipError_t launch_eye(float* Ut, int64_t d, hipStream_t s) {
 // S1 + S2: Mbar = Ebar + (1/N) sum_i G^(i)   (m x n layout; Ebar is the mean
 // of the workers' error buffers left by the previous step)
 // ---------------------------------------------------------------------------
-__global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__ Ebar,
-                          float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status,
-                          int check) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+__device__ __forceinline__ void ef_mean_at(const float* __restrict__ G, const float* __restrict__ Ebar,
+                                           float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status, int check,
+                                           int64_t bx, int64_t gx) {
+  const int64_t stride = (int64_t)gx * blockDim.x;
   bool bad = false;
   if ((mn & 3) == 0) {
     const int64_t q = mn >> 2;
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < q; i += stride) {
+    for (int64_t i = bx * (int64_t)blockDim.x + threadIdx.x; i < q; i += stride) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int w = 0; w < N; ++w) {
         float4 g = load_nt4(G + (int64_t)w * mn + 4 * i);
@@ -69,7 +69,7 @@ __global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__
       reinterpret_cast<float4*>(Mbar)[i] = o;
     }
   } else {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
+    for (int64_t i = bx * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
       float acc = 0.f;
       for (int w = 0; w < N; ++w) {
         float g = G[(int64_t)w * mn + i];
@@ -80,6 +80,11 @@ __global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__
     }
   }
   if (check && bad) atomicOr(status, 1u);
+}
+__global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__ Ebar,
+                          float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status,
+                          int check) {
+  ef_mean_at(G, Ebar, Mbar, mn, N, status, check, blockIdx.x, gridDim.x);
 }
 
 hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
@@ -98,14 +103,14 @@ hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
 constexpr int SEL_BM = 128, SEL_BN = 128;
 
 template <bool RIGHT, bool APPROX, bool BF16>
-__global__ void __launch_bounds__(256)
-k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d, int64_t D,
-             float* __restrict__ part, uint32_t mat, uint32_t tstep, uint32_t key0, uint32_t key1) {
+__device__ __forceinline__ void sel_scores_at(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d,
+                                              int64_t D, float* __restrict__ part, uint32_t mat, uint32_t tstep,
+                                              uint32_t key0, uint32_t key1, int bx, int by) {
   using T = MfmaTile<SEL_BM, SEL_BN, 2, 2>;
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
   __shared__ float red[2][SEL_BN];
-  const int m0 = blockIdx.y * SEL_BM;   // rows: b in [0, D)
-  const int n0 = blockIdx.x * SEL_BN;   // cols: j in [0, d)
+  const int m0 = by * SEL_BM;   // rows: b in [0, D)
+  const int n0 = bx * SEL_BN;   // cols: j in [0, d)
   T tile;
   LoadK<SEL_BN, 32, false, false> lb(Ut, nullptr, d, n0, (int)d, (int)d, nullptr);
   if (RIGHT) {
@@ -151,18 +156,28 @@ k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64
   __syncthreads();
   if (threadIdx.x < SEL_BN) {
     const int j = n0 + threadIdx.x;
-    if (j < d) part[(int64_t)blockIdx.y * d + j] = red[0][threadIdx.x] + red[1][threadIdx.x];
+    if (j < d) part[(int64_t)by * d + j] = red[0][threadIdx.x] + red[1][threadIdx.x];
   }
+}
+template <bool RIGHT, bool APPROX, bool BF16>
+__global__ void __launch_bounds__(256)
+k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d, int64_t D,
+             float* __restrict__ part, uint32_t mat, uint32_t tstep, uint32_t key0, uint32_t key1) {
+  sel_scores_at<RIGHT, APPROX, BF16>(Mbar, Ut, d, D, part, mat, tstep, key0, key1, blockIdx.x, blockIdx.y);
 }
 
 // lambdabar / scores from the tile partials, summed in a fixed order
-__global__ void k_sel_finish(const float* __restrict__ part, int ntiles, int64_t d, int approx,
-                             float* __restrict__ score) {
-  int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+__device__ __forceinline__ void sel_finish_at(const float* __restrict__ part, int ntiles, int64_t d, int approx,
+                                              float* __restrict__ score, int64_t bx) {
+  int64_t j = bx * (int64_t)blockDim.x + threadIdx.x;
   if (j >= d) return;
   float s = 0.f;
   for (int t = 0; t < ntiles; ++t) s += part[(int64_t)t * d + j];
   score[j] = approx ? s * s : s;
+}
+__global__ void k_sel_finish(const float* __restrict__ part, int ntiles, int64_t d, int approx,
+                             float* __restrict__ score) {
+  sel_finish_at(part, ntiles, d, approx, score, blockIdx.x);
 }
 
 hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t seed, int64_t t, hipStream_t s) {
@@ -194,9 +209,8 @@ hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t 
 // argtop_r: descending score, ties to the smaller index; J ascending.
 // One block of 1024 threads; n_pad (power of two) 64-bit keys in LDS.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(1024)
-k_topr(const float* __restrict__ score, int d, int r, int n_pad, int* __restrict__ J) {
-  extern __shared__ __align__(16) unsigned char dyn[];
+__device__ __forceinline__ void topr_at(const float* __restrict__ score, int d, int r, int n_pad,
+                                        int* __restrict__ J, unsigned char* dyn) {
   uint64_t* keys = reinterpret_cast<uint64_t*>(dyn);
   for (int i = threadIdx.x; i < n_pad; i += blockDim.x) {
     if (i < d) {
@@ -241,6 +255,11 @@ k_topr(const float* __restrict__ score, int d, int r, int n_pad, int* __restrict
   for (int i = lo; i < lo + per && i < d; ++i)
     if (sel[i]) J[pos++] = i;
 }
+__global__ void __launch_bounds__(1024)
+k_topr(const float* __restrict__ score, int d, int r, int n_pad, int* __restrict__ J) {
+  extern __shared__ __align__(16) unsigned char dyn[];
+  topr_at(score, d, r, n_pad, J, dyn);
+}
 
 __global__ void k_iota(int* J, int r) {
   for (int i = threadIdx.x; i < r; i += blockDim.x) J[i] = i;
@@ -252,11 +271,16 @@ static int next_pow2(int64_t x) {
   return p;
 }
 
-hipError_t launch_topr(const MatView& v, hipStream_t s) {
-  const int n_pad = next_pow2(v.d < 2 ? 2 : v.d);
+size_t topr_lds_bytes(int64_t d) {
+  const int n_pad = next_pow2(d < 2 ? 2 : d);
   size_t lds = (size_t)n_pad * 8;
   if (lds < (size_t)(n_pad + 1024) * 4) lds = (size_t)(n_pad + 1024) * 4;
-  hipLaunchKernelGGL(k_topr, dim3(1), dim3(1024), lds, s, v.score, (int)v.d, v.r, n_pad, v.J);
+  return lds;
+}
+
+hipError_t launch_topr(const MatView& v, hipStream_t s) {
+  const int n_pad = next_pow2(v.d < 2 ? 2 : v.d);
+  hipLaunchKernelGGL(k_topr, dim3(1), dim3(1024), topr_lds_bytes(v.d), s, v.score, (int)v.d, v.r, n_pad, v.J);
   return hipGetLastError();
 }
 
@@ -270,15 +294,16 @@ hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
 // P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
-__global__ void __launch_bounds__(256)
-k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
-       const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
+__device__ __forceinline__ void proj_at(const float* __restrict__ G, const float* __restrict__ E,
+                                        const float* __restrict__ Ut, const int* __restrict__ J,
+                                        float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice,
+                                        int bx, int by, int bz) {
   using T = MfmaTile<BM, BN, WM, WN>;
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
-  const int n0 = blockIdx.x * BN;   // b
-  const int m0 = blockIdx.y * BM;   // k (rank index)
-  const int w = blockIdx.z % N;     // worker
-  const int z = blockIdx.z / N;     // slice of the d contraction
+  const int n0 = bx * BN;   // b
+  const int m0 = by * BM;   // k (rank index)
+  const int w = bz % N;     // worker
+  const int z = bz / N;     // slice of the d contraction
   const int64_t k0 = (int64_t)z * kslice;
   const int klen = (int)(d - k0 < kslice ? d - k0 : kslice);
   const int64_t dD = d * D;
@@ -321,6 +346,12 @@ k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __
       }
     }
 }
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
+__global__ void __launch_bounds__(256)
+k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
+       const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH>(G, E, Ut, J, Qpart, d, D, r, N, kslice, blockIdx.x, blockIdx.y, blockIdx.z);
+}
 
 hipError_t launch_proj(const MatView& v, hipStream_t s) {
   const int r = v.r;
@@ -351,10 +382,11 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
 
 // S6 (with the slices of the projection): Q^(i) = sum over slices of the
 // partial products, Rbar = (1/N) sum_i Q^(i); both sums in a fixed order, fp64
-__global__ void k_proj_reduce(const float* __restrict__ part, int splits, int N, int64_t rD, float* __restrict__ Q,
-                              float* __restrict__ Rbar) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < rD; i += stride) {
+__device__ __forceinline__ void proj_reduce_at(const float* __restrict__ part, int splits, int N, int64_t rD,
+                                               float* __restrict__ Q, float* __restrict__ Rbar, int64_t bx,
+                                               int64_t gx) {
+  const int64_t stride = (int64_t)gx * blockDim.x;
+  for (int64_t i = bx * (int64_t)blockDim.x + threadIdx.x; i < rD; i += stride) {
     double rsum = 0.0;
     for (int w = 0; w < N; ++w) {
       double q = 0.0;
@@ -368,6 +400,10 @@ __global__ void k_proj_reduce(const float* __restrict__ part, int splits, int N,
     }
     Rbar[i] = (float)(rsum / (double)N);
   }
+}
+__global__ void k_proj_reduce(const float* __restrict__ part, int splits, int N, int64_t rD, float* __restrict__ Q,
+                              float* __restrict__ Rbar) {
+  proj_reduce_at(part, splits, N, rD, Q, Rbar, blockIdx.x, gridDim.x);
 }
 
 hipError_t launch_rbar(const MatView& v, hipStream_t s) {
@@ -392,19 +428,19 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
 template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
-k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
+__device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float* __restrict__ E,
+                                             float* __restrict__ Ebar,
             const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
             const float* __restrict__ Ut,
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
-            int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
+            int64_t n, int64_t d, int64_t D, int r, int N, OptParams op, int bx, int by) {
   using T = MfmaTile<ROWS, RO_COLS, ROWS / 32, 128 / ROWS>;
   constexpr int TM = T::TM;
   static_assert(T::TN == 1, "one tile column per lane");
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
-  const int c0 = blockIdx.x * RO_COLS;   // first column of the tile
-  const int r0 = blockIdx.y * ROWS;      // first row of the tile
+  const int c0 = bx * RO_COLS;   // first column of the tile
+  const int r0 = by * ROWS;      // first row of the tile
   const int64_t mn = m * n;
   // this lane's outputs: column cc, rows r0 + row(tm, v) = rb[tm] + rv(v)
   // with rv(v) = 8 (v / 4) + v % 4 the same in every lane
@@ -493,12 +529,22 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
       buf_st(S1r, o, s1);
     }
 }
+template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
+            const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
+            const float* __restrict__ Ut,
+            const int* __restrict__ J,
+            float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
+            int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
+  resid_opt_at<OPT, RIGHT, ROWS, RO_COLS>(G, E, Ebar, Mbar, Q, Rbar, Ut, J, X, S1, S2, m, n, d, D, r, N, op,
+                                          blockIdx.x, blockIdx.y);
+}
 
 // S5 above rank 128, where the rank-r products dominate: 128 x 128 tiles
 // (64 x 64 per wave), one worker after the other, E^(w) <- (G^(w) - P Q^(w))
 // + E^(w) streamed 16 elements per lane at a time after each product;
 // k_resid_opt then runs with no workers (Ghat, Ebar and the optimizer).
-constexpr int kResidWideRank = 128;
 
 template <bool RIGHT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -606,6 +652,162 @@ hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t
   else
     hipLaunchKernelGGL(k_full_refresh<1>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, v.E,
                        v.Ebar, v.X, v.S1, v.S2, mn, v.N, o);
+  return hipGetLastError();
+}
+
+
+// ---------------------------------------------------------------------------
+// Grouped selection step: every kernel of a selection step in one launch over
+// all matrices.  Each matrix owns a range of blocks (tables of first blocks);
+// a block finds its matrix and runs the per-matrix body with the coordinates
+// it has in that matrix's own launch, so each matrix computes exactly what its
+// own launches compute.  Many small matrices then fill the chip together
+// instead of a few CUs each.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int group_find(const int* __restrict__ first, int num, int b) {
+  int lo = 0, hi = num - 1;   // the last m with first[m] <= b
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int dev_next_pow2(int64_t x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// projection tiles of rank r: BM x BN, WM x WN waves, fp64 flush of the slices
+#define GLR_PROJ_TIERS(X)                                   \
+  if (r <= 32) X(32, 128, 1, 4, true);                      \
+  else if (r <= 64) X(64, 64, 2, 2, true);                  \
+  else if (r <= kProjWideRank) X(128, 64, 2, 2, true);      \
+  else X(256, 64, 4, 1, false)
+
+__global__ void k_g_ef_mean(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, int check) {
+  const int m = group_find(first, num, blockIdx.x);
+  const MatView& v = gm[m].v;
+  ef_mean_at(v.G, v.Ebar, v.Mbar, v.m * v.n, v.N, v.status, check, blockIdx.x - first[m], first[m + 1] - first[m]);
+}
+
+template <bool RIGHT, bool APPROX, bool BF16>
+__global__ void __launch_bounds__(256)
+k_g_sel_scores(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, uint32_t tstep,
+               uint32_t key0, uint32_t key1) {
+  const int m = group_find(first, num, blockIdx.x);
+  const MatView& v = gm[m].v;
+  const int local = blockIdx.x - first[m], gx = (int)((v.d + SEL_BN - 1) / SEL_BN);
+  sel_scores_at<RIGHT, APPROX, BF16>(v.Mbar, v.Ut, v.d, v.D, v.lam_part, (uint32_t)v.mat, tstep, key0, key1,
+                                     local % gx, local / gx);
+}
+
+__global__ void k_g_sel_finish(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, int approx) {
+  const int m = group_find(first, num, blockIdx.x);
+  const MatView& v = gm[m].v;
+  sel_finish_at(v.lam_part, (int)((v.D + SEL_BM - 1) / SEL_BM), v.d, approx, v.score, blockIdx.x - first[m]);
+}
+
+__global__ void __launch_bounds__(1024) k_g_topr(const GroupMat* __restrict__ gm) {
+  extern __shared__ __align__(16) unsigned char dyn[];
+  const MatView& v = gm[blockIdx.x].v;
+  topr_at(v.score, (int)v.d, v.r, dev_next_pow2(v.d < 2 ? 2 : v.d), v.J, dyn);
+}
+
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
+__global__ void __launch_bounds__(256)
+k_g_proj(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num) {
+  const int m = group_find(first, num, blockIdx.x);
+  const GroupMat& g = gm[m];
+  const MatView& v = g.v;
+  const int gx = (int)((v.D + BN - 1) / BN), gy = (v.r + BM - 1) / BM;
+  const int local = blockIdx.x - first[m], rest = local / gx;
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH>(v.G, v.E, v.Ut, v.J, g.splits > 1 ? v.Qpart : v.Q, v.d, v.D, v.r, v.N,
+                                        g.kslice, local % gx, rest % gy, rest / gy);
+}
+
+__global__ void k_g_rbar(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num) {
+  const int m = group_find(first, num, blockIdx.x);
+  const GroupMat& g = gm[m];
+  const MatView& v = g.v;
+  proj_reduce_at(v.Qpart, g.splits, v.N, (int64_t)v.r * v.D, v.Q, v.Rbar, blockIdx.x - first[m],
+                 first[m + 1] - first[m]);
+}
+
+template <int OPT, bool RIGHT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+k_g_resid_opt(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, OptParams op) {
+  const int m = group_find(first, num, blockIdx.x);
+  const MatView& v = gm[m].v;
+  const int local = blockIdx.x - first[m], gx = (int)((v.n + 63) / 64);
+  resid_opt_at<OPT, RIGHT, 64, 64>(v.G, v.E, v.Ebar, v.Mbar, v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d,
+                                   v.D, v.r, v.N, op, local % gx, local / gx);
+}
+
+void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]) {
+  const MatView& v = g.v;
+  const int r = v.r;
+  g.splits = proj_splits(v.d, v.D, r, v.N);
+  g.kslice = r > kProjWideRank ? kProjWideSlice : (int)(((v.d + g.splits - 1) / g.splits + 31) / 32 * 32);
+  blocks[kGrpEfMean] = grid_for(v.m * v.n, 4);
+  blocks[kGrpSelScores] = (int)(((v.d + SEL_BN - 1) / SEL_BN) * ((v.D + SEL_BM - 1) / SEL_BM));
+  blocks[kGrpSelFinish] = grid_for(v.d);
+  int proj = 0;
+#define GLR_PROJ_BLOCKS(BM, BN, WM, WN, FL) proj = (int)(((v.D + BN - 1) / BN) * ((r + BM - 1) / BM) * v.N * g.splits)
+  GLR_PROJ_TIERS(GLR_PROJ_BLOCKS);
+#undef GLR_PROJ_BLOCKS
+  blocks[kGrpProj] = proj;
+  blocks[kGrpRbar] = grid_for((int64_t)r * v.D);
+  blocks[kGrpResid] = (int)(((v.n + 63) / 64) * ((v.m + 63) / 64));
+}
+
+hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
+                               int64_t t, const OptParams& o, hipStream_t s) {
+  if (bf16 && !approx) return hipErrorInvalidValue;
+  const int num = gp.num, r = gp.r;
+  const bool right = gp.right;
+  auto table = [&](int kind) { return gp.first + (int64_t)kind * (num + 1); };
+  auto grid = [&](int kind) { return dim3((unsigned)gp.total[kind]); };
+  hipLaunchKernelGGL(k_g_ef_mean, grid(kGrpEfMean), dim3(kThreads), 0, s, gp.gm, table(kGrpEfMean), num,
+                     check_finite ? 1 : 0);
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+  const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
+#define GLR_GSEL(R, A, B)                                                                                   \
+  hipLaunchKernelGGL((k_g_sel_scores<R, A, B>), grid(kGrpSelScores), dim3(kThreads), 0, s, gp.gm,          \
+                     table(kGrpSelScores), num, tt, k0, k1)
+  if (right) {
+    if (bf16) GLR_GSEL(true, true, true);
+    else if (approx) GLR_GSEL(true, true, false);
+    else GLR_GSEL(true, false, false);
+  } else {
+    if (bf16) GLR_GSEL(false, true, true);
+    else if (approx) GLR_GSEL(false, true, false);
+    else GLR_GSEL(false, false, false);
+  }
+#undef GLR_GSEL
+  hipLaunchKernelGGL(k_g_sel_finish, grid(kGrpSelFinish), dim3(kThreads), 0, s, gp.gm, table(kGrpSelFinish), num,
+                     approx ? 1 : 0);
+  hipLaunchKernelGGL(k_g_topr, dim3((unsigned)num), dim3(1024), gp.topr_lds, s, gp.gm);
+#define GLR_GPROJ(BM, BN, WM, WN, FL)                                                                       \
+  do {                                                                                                      \
+    if (right)                                                                                              \
+      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, true, FL>), grid(kGrpProj), dim3(kThreads), 0, s, gp.gm, \
+                         table(kGrpProj), num);                                                             \
+    else                                                                                                    \
+      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, false, FL>), grid(kGrpProj), dim3(kThreads), 0, s, gp.gm,\
+                         table(kGrpProj), num);                                                             \
+  } while (0)
+  GLR_PROJ_TIERS(GLR_GPROJ);
+#undef GLR_GPROJ
+  hipLaunchKernelGGL(k_g_rbar, grid(kGrpRbar), dim3(kThreads), 0, s, gp.gm, table(kGrpRbar), num);
+#define GLR_GRO(OPT, R)                                                                                     \
+  hipLaunchKernelGGL((k_g_resid_opt<OPT, R>), grid(kGrpResid), dim3(kThreads), 0, s, gp.gm, table(kGrpResid), \
+                     num, o)
+  if (o.opt == 0) { if (right) GLR_GRO(0, true); else GLR_GRO(0, false); }
+  else            { if (right) GLR_GRO(1, true); else GLR_GRO(1, false); }
+#undef GLR_GRO
   return hipGetLastError();
 }
 

@@ -198,3 +198,42 @@ def test_joint_refresh_matches_the_per_matrix_sweeps(gpu_lib, monkeypatch, name,
         assert torch.equal(c1.sigma(l), c2.sigma(l)), f"mat {l}: sigma differs"
         assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
         assert torch.equal(c1.info(l), c2.info(l)), f"mat {l}: sweep record differs"
+
+
+_RIGHT_TRIO = {"shapes": ((1100, 1012), (1030, 1016), (700, 96)), "tau": 3, "steps": 6}
+
+
+@pytest.mark.parametrize("name,override,select", [
+    ("conv_50", {"tau": 3}, "approx"),             # twelve conv layers, d < n, MSGD
+    ("seats64_left", _RIGHT_TRIO, "approx"),       # d = n < m, Adam
+    ("seats64_left", _RIGHT_TRIO, "exact"),
+    ("seats64_left", _RIGHT_TRIO, "approx_bf16"),
+])
+def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypatch, name, override, select):
+    # a selection step of several matrices launches each kernel once for all
+    # of them; every matrix must end bitwise where its own launches take it
+    import torch
+    wl = get_workload(name, **override)
+    if name == "conv_50":
+        wl = get_workload(name, shapes=wl.shapes[:12], **override)
+    T = min(wl.steps, wl.tau + 3)
+    _say(name, select, "grouped vs per-matrix selection over", T, "steps,", len(wl.shapes), "matrices")
+    G = _inputs(wl, T)
+    runs = []
+    for grouped in ("0", None):
+        if grouped is None:
+            monkeypatch.delenv("GLR_GROUPED", raising=False)
+        else:
+            monkeypatch.setenv("GLR_GROUPED", grouped)
+        comp = _make(gpu_lib, wl, select=select)
+        X = _zeros(wl)
+        for t in range(T):
+            comp.step(X, G[t], t)
+        assert comp.sync_status() == gpu_lib.GLR_OK
+        runs.append((comp, X))
+    (c1, x1), (c2, x2) = runs
+    for l in range(len(wl.shapes)):
+        assert torch.equal(x1[l], x2[l]), f"mat {l}: X differs"
+        assert torch.equal(c1.E(l), c2.E(l)), f"mat {l}: E differs"
+        assert torch.equal(c1.Ut(l), c2.Ut(l)), f"mat {l}: U differs"
+        assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
