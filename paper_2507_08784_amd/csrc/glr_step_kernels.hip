@@ -372,9 +372,11 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
       hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL>), grid, dim3(kThreads), 0, s, v.G, v.E,\
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
   } while (0)
+  // 64 < r <= 128 takes two 64-row rank tiles (G and E read twice): the
+  // 128-row tile keeps its fp64 accumulators in scratch memory and ran at half
+  // the speed
   if (r <= 32) GLR_PROJ(32, 128, 1, 4, true);
-  else if (r <= 64) GLR_PROJ(64, 64, 2, 2, true);
-  else if (r <= kProjWideRank) GLR_PROJ(128, 64, 2, 2, true);
+  else if (r <= kProjWideRank) GLR_PROJ(64, 64, 2, 2, true);
   else GLR_PROJ(256, 64, 4, 1, false);
 #undef GLR_PROJ
   return hipGetLastError();
@@ -683,8 +685,7 @@ __device__ __forceinline__ int dev_next_pow2(int64_t x) {
 // projection tiles of rank r: BM x BN, WM x WN waves, fp64 flush of the slices
 #define GLR_PROJ_TIERS(X)                                   \
   if (r <= 32) X(32, 128, 1, 4, true);                      \
-  else if (r <= 64) X(64, 64, 2, 2, true);                  \
-  else if (r <= kProjWideRank) X(128, 64, 2, 2, true);      \
+  else if (r <= kProjWideRank) X(64, 64, 2, 2, true);       \
   else X(256, 64, 4, 1, false)
 
 __global__ void k_g_ef_mean(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, int check) {
