@@ -115,3 +115,26 @@ def test_layout_is_aligned_disjoint_and_sized(opt):
         assert a1 <= b0
     assert spans[-1][1] <= sb
     assert wb > 0
+
+
+def test_workspace_holds_a_region_per_matrix():
+    # matrices running at the same time (concurrent streams, the joint sweeps
+    # of a refresh, the grouped launches of a selection step) never share
+    # scratch: the workspace of several matrices holds each one's own region
+    shapes = [(512, 576), (256, 2304), (1012, 1100), (130, 70)]
+    cfg, _keep = glr.make_config(shapes, 4, 8, 5)
+    _, total = glr.workspace_bytes(cfg)
+    alone = []
+    for s in shapes:
+        c1, _k1 = glr.make_config([s], 4, 8, 5)
+        alone.append(glr.workspace_bytes(c1)[1])
+    # each configuration also carries a few KiB of per-matrix launch tables
+    slack = 4096
+    assert total >= sum(alone) - slack * len(shapes)
+    # one region per matrix, sized by that matrix: not a copy of the largest
+    # matrix's region per stream
+    assert total <= sum(alone)
+    # and a matrix's region does not depend on the others
+    c2, _k2 = glr.make_config(shapes + [(4096, 4096)], 4, 8, 5)
+    c3, _k3 = glr.make_config([(4096, 4096)], 4, 8, 5)
+    assert glr.workspace_bytes(c2)[1] >= total + glr.workspace_bytes(c3)[1] - slack
