@@ -6,7 +6,7 @@
  * semi-lazy SVD subspace.  One call of glr_step performs, for every layer
  * matrix X in R^{m x n} (problem (1), Section I):
  *
- *   error feedback       M^(i) = G^(i) + E^(i)                (Section IV-A, eq-ef)
+ *   error feedback       M^(i) = G^(i) + E^(i)                (Section V-A, eq-ef)
  *   worker mean          Mbar  = (1/N) sum_i M^(i)           (All-Reduce of Alg. 3/4)
  *   subspace             t mod tau == 0: U = complete left singular basis of
  *                        Mbar, P = first r columns (eq-SVD-P1);

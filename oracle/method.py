@@ -13,6 +13,8 @@ One step t, following Algorithm 4 with Approx-Top-r (Algorithm 2):
   1. M^(i) = G^(i) (or G^(i)^T) + E^(i)                      [Alg. 3/4, EF]
   2. refresh iff t mod tau == 0                               [eq-SVD-P1]
   3. refresh:  Mbar = mean_i M^(i); U, Sigma = SVD(Mbar); J = {0..r-1}
+               (tau = 1, r < d: only U[:, :r] is ever read, so the top-r block
+               comes from oracle.subspace instead of the complete basis)
      else:     v_j ~ N(0, I_D); lambda_j^(i) = u_j^T M^(i) v_j;
                lambdabar = mean_i lambda^(i); J = argtop_r(lambdabar^2)
                ('exact' scores ||u_j^T Mbar||^2 instead, eq-semi-lazy-svd-2)
@@ -42,6 +44,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 from .philox import gaussian_vectors
+from .subspace import top_subspace
 from .svd import left_svd
 
 # ----------------------------------------------------------------------------
@@ -154,6 +157,12 @@ class Oracle:
     refresh: str = "compressed"   # "compressed" (Alg. 4) | "full" (Alg. 3)
     select: str = "approx"        # "approx" (Alg. 2) | "exact" (eq-semi-lazy-svd-2) | "approx_bf16"
     svd_tol: float | None = None
+    # refresh route when tau == 1 and r < d: "subspace" (top-r block by
+    # subspace iteration + Rayleigh-Ritz, oracle.subspace) or "full" (the
+    # complete one-sided Jacobi basis); both give the top-r span
+    tau1_route: str = "subspace"
+    sub_tol: float = 1e-12
+    sub_max_iters: int = 200
     states: list = field(default_factory=list)
     t_next: int = 0
 
@@ -176,16 +185,28 @@ class Oracle:
                    opt=wl.opt, lr=wl.lr, beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps,
                    seed=wl.seed, **kw)
 
-    def step(self, grads, t: int):
+    def uses_subspace(self, d, r):
+        return self.tau == 1 and r < d and self.tau1_route == "subspace"
+
+    def step(self, grads, t: int, handoff=None):
         """One step on every matrix.  grads[l] is N x m x n (any float dtype).
-        Returns one dict of intermediate values per matrix."""
+        Returns one dict of intermediate values per matrix.
+
+        handoff (optional) lets a parity harness continue from another
+        implementation's basis (the state hand-off for columns of U that the
+        data leave ill-defined): handoff.basis(l, t, out) is called after the
+        refresh with out holding this oracle's "U" (columns u_j), "sigma" and
+        "mbar", and returns the d x k basis to use from this step on (its
+        first r columns become P); handoff.selection(l, t, out, J) is called
+        after the selection with out holding "score", and returns the index
+        set to use."""
         if t != self.t_next:
             raise ValueError(f"steps run in order: expected t={self.t_next}, got {t}")
         self.t_next += 1
-        return [self._step_one(l, st, np.asarray(g, dtype=np.float64), t)
+        return [self._step_one(l, st, np.asarray(g, dtype=np.float64), t, handoff)
                 for l, (st, g) in enumerate(zip(self.states, grads))]
 
-    def _step_one(self, l, st: MatrixState, g, t):
+    def _step_one(self, l, st: MatrixState, g, t, handoff=None):
         n_w = self.workers
         d, D = min(st.m, st.n), max(st.m, st.n)
         r = min(self.rank, d)
@@ -196,11 +217,20 @@ class Oracle:
         mbar = ms.sum(axis=0) / n_w
         out["mbar"] = mbar
         if is_refresh:                                            # step 3
-            u, sigma, sweeps = left_svd(mbar, tol=self.svd_tol)
+            if self.uses_subspace(d, r):
+                u, sigma, sweeps, conv = top_subspace(mbar, r, seed=self.seed + 7919 * l + t,
+                                                      tol=self.sub_tol, max_iters=self.sub_max_iters)
+                out["converged"] = conv
+            else:
+                u, sigma, sweeps = left_svd(mbar, tol=self.svd_tol)
+            out.update(sigma=sigma, sweeps=sweeps, U_oracle=u)
+            if handoff is not None:
+                out["U"] = u
+                out["mbar"] = mbar
+                u = np.asarray(handoff.basis(l, t, out), dtype=np.float64)
             st.u = u
             st.sigma = sigma
             jsel = np.arange(r)
-            out.update(sigma=sigma, sweeps=sweeps)
         else:
             if self.select == "approx":
                 v = gaussian_vectors(self.seed, t, l, np.arange(d), D).astype(np.float64)
@@ -216,6 +246,9 @@ class Oracle:
                 score = exact_scores(st.u, mbar)
             jsel = argtop_r(score, r)
             out["score"] = score
+            out["J_oracle"] = jsel
+            if handoff is not None:
+                jsel = np.asarray(handoff.selection(l, t, out, jsel))
         p = st.u[:, jsel]                                         # step 4
         q = np.einsum("ak,iab->ikb", p, ms)                       # step 5
         rbar = q.sum(axis=0) / n_w                                # step 7

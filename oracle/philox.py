@@ -3,7 +3,7 @@
 TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
 The paper draws v_j ~ N(0, I_n) for j in [m] with a seed shared by all nodes
-(Section IV-C, eq:random-v) and fixes nothing else.  Both this oracle and the
+(Section V-C, eq:random-v) and fixes nothing else.  Both this oracle and the
 GPU path implement the same counter-based generator from its published
 definition, Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw,
 "Parallel random numbers: as easy as 1, 2, 3", SC'11):

@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
 The Semi-Lazy SVD operator needs, at every refresh step, the SVD of the
 averaged matrix and the *whole* orthonormal U, not only its first r columns
-(Section IV-B, eq-SVD-P1; Algorithm 3 returns U; the proof of Proposition 3
+(Section V-B, eq-SVD-P1; Algorithm 3 returns U; the proof of Proposition 3
 uses sum_j ||u_j^T G||^2 = ||G||^2, which needs U complete; the memory
 discussion prices U at min(m, n)^2).  The paper does not say how the SVD is
 computed.  The oracle uses the textbook one-sided Jacobi method (Hestenes 1958):

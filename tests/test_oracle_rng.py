@@ -1,5 +1,5 @@
 """Pins for the oracle's random vectors (Approx-Top-r draws v_j ~ N(0, I),
-Section IV-C, eq:random-v): the published Philox4x32-10 known answers, the
+Section V-C, eq:random-v): the published Philox4x32-10 known answers, the
 exactness of the uniform map, and distribution tests of Box-Muller."""
 import os
 

@@ -1,5 +1,5 @@
 """Pins for the oracle's complete left singular basis (Semi-Lazy SVD refresh,
-Section IV-B eq-SVD-P1; U must be complete for Proposition 3's proof)."""
+Section V-B eq-SVD-P1; U must be complete for Proposition 3's proof)."""
 import itertools
 
 import numpy as np
