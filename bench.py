@@ -243,40 +243,53 @@ def make_pool(wl, pool, device, seed=1234):
     return batches
 
 
-def cpu_baseline(wl, budget_s):
-    """The oracle (as it stands) on a bounded sample of the same workload.
+def host_cpu():
+    """(usable cores, CPU model) of the host the oracle runs on."""
+    try:
+        ncpu = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        ncpu = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return ncpu, model
 
-    Sample: one non-refresh step of the oracle on the full workload (Approx-
-    Top-r with per-worker bilinear forms, projection, residual, optimizer),
-    and one Jacobi sweep on a d' x D slice of the averaged matrix, scaled by
-    (d/d')^2 and by the sweep count of the GPU refresh to estimate a refresh.
-    Returns ms/step averaged over one refresh period."""
-    import numpy as np
-    from oracle.method import Oracle
-    from oracle.svd import left_svd
-    from synth import gradient_batch, planted_matrix
+
+def blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
-    grads = [gradient_batch(wl, l, 1, planted_matrix(wl, l)) for l in range(len(wl.shapes))]
+        return 1
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle as it stands, timed on the host: whole oracle steps
+    t = 0, 1, ... of the same workload (the full matrices, every worker,
+    t = 0 a cold refresh), until `budget_s` of oracle time is spent (at least
+    one step).  Gradient generation is not timed.  Returns (seconds per step,
+    steps timed, refresh steps among them)."""
+    from oracle.method import Oracle
+    from synth import gradient_batch, planted_matrix
+    planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
     orc = Oracle.from_workload(wl)
-    orc.t_next = 1
-    t0 = time.perf_counter()
-    orc.step(grads, 1)
-    nonref = time.perf_counter() - t0
-    svd_est = 0.0
-    for l, (m, n) in enumerate(wl.shapes):
-        d, D = min(m, n), max(m, n)
-        g = np.asarray(grads[l], dtype=np.float64).mean(axis=0)
-        mo = g.T if m > n else g
-        dp = min(d, 256)
+    spent, steps, refresh = 0.0, 0, 0
+    while steps == 0 or (spent < budget_s and steps < wl.steps):
+        grads = [gradient_batch(wl, l, steps, planted[l]) for l in range(len(wl.shapes))]
         t0 = time.perf_counter()
-        left_svd(mo[:dp], max_sweeps=1)
-        one = time.perf_counter() - t0
-        svd_est += one * (d / dp) ** 2
-    return nonref, svd_est, threads
+        orc.step(grads, steps)
+        spent += time.perf_counter() - t0
+        refresh += 1 if steps % wl.tau == 0 else 0
+        steps += 1
+        del grads
+        print(f"[bench] oracle step {steps - 1}: {spent:.1f}s so far", file=sys.stderr, flush=True)
+    return spent / steps, steps, refresh
 
 
 def main():
@@ -284,7 +297,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="layer_4096")
+    ap.add_argument("--workload", default="large_8192x28672")
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of oracle time for the CPU baseline (whole steps, at least one)")
     ap.add_argument("--pool", type=int, default=11)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
@@ -432,14 +447,13 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        nonref, svd_est, threads = cpu_baseline(wl, 30.0)
-        sw = max(1, max(sweeps))
-        ms = (wl.tau * nonref + svd_est * sw) / wl.tau * 1e3
+        sec, nsteps, nref = cpu_baseline(wl, args.cpu_budget)
+        ncpu, model = host_cpu()
         out["cpu_baseline"] = {
-            "value": round(ms, 1), "unit": "ms/step", "cores": threads, "kind": "oracle",
-            "sample": (f"one non-refresh oracle step of {wl.name} ({nonref:.2f}s) plus one Jacobi sweep "
-                       f"on a 256-row slice of the averaged matrix scaled by (d/256)^2 x {sw} sweeps "
-                       f"({svd_est * sw:.1f}s per refresh), averaged over tau={wl.tau} steps"),
+            "value": round(sec * 1e3, 1), "unit": "ms/step", "cores": blas_threads(), "kind": "oracle",
+            "sample": (f"oracle steps t=0..{nsteps - 1} of {wl.name} ({nref} refresh, t=0 cold) on the full "
+                       f"matrices, {sec:.1f}s per step; fp64 numpy, BLAS threads as cores; host nproc={ncpu}, "
+                       f"{model}"),
         }
     print(json.dumps(out), flush=True)
 

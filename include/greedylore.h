@@ -53,15 +53,25 @@
  * this off.
  * While profiling is enabled the matrices run in order on `stream`.  The
  * environment variable GLR_LANES, read by glr_create, lowers the stream count.
- * glr_step blocks the host only on refresh steps, where it reads the
- * convergence flag of the Jacobi sweeps (one 4-byte read per sweep).
+ *
+ * glr_step only enqueues: it never waits for the device (refresh steps
+ * included).  A refresh enqueues a budget of Jacobi sweeps; the sweeps after
+ * convergence return at once on the device.  The budget is max_sweeps until a
+ * refresh of that matrix has been seen converged, then the sweeps that refresh
+ * took plus a quarter (at least three); the sweep counts come back through
+ * pinned host memory the handle owns, read only once their copy has completed.
+ * A refresh that ends its budget above tol reports GLR_ERR_NOT_CONVERGED and
+ * the next one gets max_sweeps again.  (Grouped selection steps reuse a
+ * two-slot pinned ring: the host waits only if it runs two such steps ahead
+ * of the device.)
  *
  * Errors.  Every function returns a glr_status and never throws or aborts
  * across the ABI.  Argument and shape errors are detected before anything is
  * enqueued and leave the state untouched.  A HIP error returns GLR_ERR_DEVICE
- * (text via glr_last_error).  Device-side conditions (non-finite gradient
- * with GLR_CHECK_FINITE, refresh not converged within max_sweeps) are latched
- * in a status word in the state blob and reported by glr_sync_status.
+ * (text via glr_last_error).  Device-side conditions are latched in a status
+ * word in the state blob and reported by glr_sync_status: a non-finite
+ * gradient (with GLR_CHECK_FINITE), a refresh that did not converge, and an
+ * orthonormalisation breakdown of the tau = 1 refresh.
  *
  * Threading.  A handle is not thread-safe; one glr_step may be in flight per
  * handle; kernels of different handles may share a stream.
@@ -84,7 +94,8 @@ typedef enum {
   GLR_ERR_STATE = 4,            /* t out of order, or a handle whose state is suspect */
   GLR_ERR_DEVICE = 5,           /* a HIP call failed */
   GLR_ERR_NONFINITE = 6,        /* a gradient held NaN/Inf (only with GLR_CHECK_FINITE) */
-  GLR_ERR_NOT_CONVERGED = 7     /* a refresh reached max_sweeps before tol */
+  GLR_ERR_NOT_CONVERGED = 7,    /* a refresh ended above its tolerance (informational) */
+  GLR_ERR_BREAKDOWN = 8         /* tau = 1 refresh: dependent rows survived the repair pass */
 } glr_status;
 
 typedef enum { GLR_MSGD = 0, GLR_ADAM = 1 } glr_opt;
@@ -147,7 +158,8 @@ typedef struct {
   uint64_t off_S2;             /* m x n fp32: Adam second moment V (0 for MSGD: absent) */
   uint64_t off_Rbar;           /* r x D fp32: mean over workers of Q^(i) = P^T M^(i) (oriented) */
   uint64_t off_info;           /* 64 int32: [0] sweeps of the last refresh, [1] converged flag,
-                                  [2 + s] float bits of sweep s's largest pair off-norm */
+                                  [2 + s] float bits of sweep s's largest pair off-norm (s < 60);
+                                  tau = 1 refresh: [62] block iterations, [63] converged flag */
 } glr_mat_layout;
 
 typedef struct glr_handle glr_handle;
@@ -178,14 +190,57 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes,
 glr_status glr_step(glr_handle* h, float* const* X, const float* const* G,
                     int64_t t, void* stream);
 
-/* Waits for `stream`, reads and clears the device status word.  Returns
- * GLR_ERR_NONFINITE (and marks the state suspect) or GLR_ERR_NOT_CONVERGED
- * (informational; the handle stays usable) or GLR_OK. */
+/* Waits for `stream`, reads and clears the device status word (every step
+ * since the last call).  Returns, in this order of precedence:
+ *   GLR_ERR_NONFINITE      a gradient held NaN/Inf (GLR_CHECK_FINITE); the
+ *                          state is marked suspect;
+ *   GLR_ERR_BREAKDOWN      a tau = 1 refresh could not orthonormalise its block
+ *                          (rows still dependent after the repair pass that
+ *                          replaces dependent rows by Gaussian ones); suspect;
+ *   GLR_ERR_NOT_CONVERGED  a refresh ended above its tolerance: Jacobi sweeps
+ *                          (budget or max_sweeps) above tol, or a tau = 1
+ *                          refresh whose last block iteration (of 2 from the
+ *                          previous block, 6 from a cold start; fewer once the
+ *                          leading r rows move by less than 10 tol) still
+ *                          raised the energy ||P^T Mbar||^2 they capture by
+ *                          more than 10 tol relative.  Informational: the basis
+ *                          is orthonormal and the handle stays usable.
+ *   GLR_OK                 otherwise. */
 glr_status glr_sync_status(glr_handle* h, void* stream);
 
 /* Declares the caller-owned state valid again after the caller wrote it
  * (resume from a saved blob, or a hand-off) and sets the next step to t. */
 glr_status glr_resume(glr_handle* h, int64_t next_t);
+
+/* Buffers for one matrix's state (glr_read_state / glr_write_state): host or
+ * device pointers, any mix; a NULL member is skipped.  Each part has the size
+ * and layout glr_mat_layout gives it: E N x m x n, Ebar / S1 / S2 m x n (fp32,
+ * the caller's layout), Ut d x d (row j = u_j), sigma and score d fp32, J r
+ * int32, Rbar r x D fp32, info 64 int32.  S2 exists for Adam only. */
+typedef struct {
+  void* E;
+  void* Ebar;
+  void* Ut;
+  void* sigma;
+  void* J;
+  void* score;
+  void* S1;
+  void* S2;
+  void* Rbar;
+  void* info;
+} glr_state_view;
+
+/* Enqueues on `stream` copies of matrix `mat`'s state parts into the non-NULL
+ * members of *dst (stream-ordered: the copies see every step enqueued before
+ * and are complete when the stream is; pageable host destinations may make
+ * the call wait).  GLR_ERR_INVALID_ARG for a bad index or an S2 request
+ * without Adam. */
+glr_status glr_read_state(glr_handle* h, int32_t mat, const glr_state_view* dst, void* stream);
+
+/* Enqueues on `stream` copies from the non-NULL members of *src into matrix
+ * `mat`'s state (a hand-off, or a restore), and marks the state valid again
+ * (as glr_resume does, without changing the next step). */
+glr_status glr_write_state(glr_handle* h, int32_t mat, const glr_state_view* src, void* stream);
 
 /* Next step the handle expects. */
 glr_status glr_next_step(const glr_handle* h, int64_t* next_t);

@@ -44,7 +44,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 from .philox import gaussian_vectors
-from .subspace import top_subspace
+from .subspace import next_singular_value, top_subspace
 from .svd import left_svd
 
 # ----------------------------------------------------------------------------
@@ -221,6 +221,7 @@ class Oracle:
                 u, sigma, sweeps, conv = top_subspace(mbar, r, seed=self.seed + 7919 * l + t,
                                                       tol=self.sub_tol, max_iters=self.sub_max_iters)
                 out["converged"] = conv
+                out["sigma_next"] = next_singular_value(mbar, u)
             else:
                 u, sigma, sweeps = left_svd(mbar, tol=self.svd_tol)
             out.update(sigma=sigma, sweeps=sweeps, U_oracle=u)
@@ -250,13 +251,13 @@ class Oracle:
             if handoff is not None:
                 jsel = np.asarray(handoff.selection(l, t, out, jsel))
         p = st.u[:, jsel]                                         # step 4
-        q = np.einsum("ak,iab->ikb", p, ms)                       # step 5
+        q = np.matmul(p.T, ms)                                    # step 5: P^T M^(i) per worker
         rbar = q.sum(axis=0) / n_w                                # step 7
         if is_refresh and self.refresh == "full":
             st.e = np.zeros_like(ms)                              # Alg. 3 reset
             ghat = mbar
         else:
-            st.e = ms - np.einsum("ak,ikb->iab", p, q)            # step 6
+            st.e = ms - np.matmul(p, q)                           # step 6: M^(i) - P Q^(i)
             ghat = p @ rbar                                       # step 8
         ghat_mn = ghat.T if st.right else ghat
         if self.opt == "msgd":                                    # step 9
@@ -275,3 +276,52 @@ def oriented_to_mn(a, m, n):
     if m > n:
         return np.swapaxes(a, -1, -2)
     return a
+
+
+class ColumnOracle:
+    """The oracle's step restricted to a sample of columns of the oriented
+    problem of one matrix, given the projector P of every step.
+
+    Once P is fixed for a step, everything after the selection acts on the
+    columns of the oriented d x D problem one at a time (Algorithm 4): for a
+    column b, M^(i)[:, b] = G^(i)[:, b] + E^(i)[:, b], Q^(i)[:, b] =
+    P^T M^(i)[:, b], E^(i)[:, b] = M^(i)[:, b] - P Q^(i)[:, b], Rbar[:, b] =
+    mean_i Q^(i)[:, b], Ghat[:, b] = P Rbar[:, b] (or Mbar[:, b] at an
+    Algorithm 3 refresh, with E = 0), and the optimizer is elementwise.  So the
+    sampled columns of E^(i), X and the optimizer state follow exactly the
+    full oracle's trajectory given the same P at every step, at a cost
+    proportional to the sample.  X, S1 and S2 are kept oriented (the
+    transpose of the caller's layout when m > n)."""
+
+    def __init__(self, shape, cols, workers, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999, eps=1e-8,
+                 refresh="compressed"):
+        m, n = shape
+        d = min(m, n)
+        self.cols = np.asarray(cols)
+        c = len(self.cols)
+        self.opt, self.lr, self.beta1, self.beta2, self.eps = opt, lr, beta1, beta2, eps
+        self.refresh = refresh
+        self.e = np.zeros((workers, d, c))
+        self.x = np.zeros((d, c))
+        self.s1 = np.zeros((d, c))
+        self.s2 = np.zeros((d, c)) if opt == "adam" else None
+
+    def step(self, g_cols, p, is_refresh):
+        """g_cols: N x d x c, the sampled oriented columns of this step's
+        gradients; p: d x r, this step's P.  Returns the new state (oriented
+        columns): E (N x d x c), Ebar, X, S1, S2."""
+        ms = np.asarray(g_cols, dtype=np.float64) + self.e
+        p = np.asarray(p, dtype=np.float64)
+        q = np.matmul(p.T, ms)
+        if is_refresh and self.refresh == "full":
+            self.e = np.zeros_like(ms)
+            ghat = ms.mean(axis=0)
+        else:
+            self.e = ms - np.matmul(p, q)
+            ghat = p @ q.mean(axis=0)
+        if self.opt == "msgd":
+            self.x, self.s1 = msgd_update(self.x, self.s1, ghat, self.lr, self.beta1)
+        else:
+            self.x, self.s1, self.s2 = adam_update(self.x, self.s1, self.s2, ghat, self.lr, self.beta1,
+                                                   self.beta2, self.eps)
+        return {"E": self.e, "Ebar": self.e.mean(axis=0), "X": self.x, "S1": self.s1, "S2": self.s2}

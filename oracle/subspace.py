@@ -110,6 +110,29 @@ def top_subspace(mbar, r, seed=0, tol=1e-12, max_iters=200, start=None):
     return q @ y, sigma, iters, converged
 
 
+def next_singular_value(mbar, p, iters=30, seed=0):
+    """An estimate from below of sigma_{r+1}(Mbar) for the top-r block P: the
+    norm reached by `iters` power iterations on the deflated matrix
+    (I - P P^T) Mbar, whose largest singular value is sigma_{r+1} when P
+    spans the top r (used to size the eigengap at r, not by the method)."""
+    a = np.asarray(mbar, dtype=np.float64)
+    d, D = a.shape
+    if p.shape[1] >= d:
+        return 0.0
+    x = np.random.default_rng([int(seed), d, D]).standard_normal(D)
+    est = 0.0
+    for _ in range(iters):
+        nx = float(np.linalg.norm(x))
+        if nx == 0.0:
+            return 0.0
+        x = x / nx
+        y = a @ x
+        y = y - p @ (p.T @ y)
+        est = float(np.linalg.norm(y))
+        x = a.T @ y
+    return est
+
+
 def orth_columns_r(y):
     """R (k x k, upper triangular) of y = Q R by the same Gram-Schmidt with
     one re-orthogonalisation pass (columns of y in order; a vanishing column

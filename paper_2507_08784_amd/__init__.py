@@ -21,6 +21,7 @@ GLR_OK = 0
 STATUS_NAMES = {
     0: "GLR_OK", 1: "GLR_ERR_INVALID_ARG", 2: "GLR_ERR_SHAPE", 3: "GLR_ERR_BUFFER_TOO_SMALL",
     4: "GLR_ERR_STATE", 5: "GLR_ERR_DEVICE", 6: "GLR_ERR_NONFINITE", 7: "GLR_ERR_NOT_CONVERGED",
+    8: "GLR_ERR_BREAKDOWN",
 }
 CHECK_FINITE = 0x1
 COLD_START = 0x2
@@ -28,7 +29,9 @@ EXPORTED = (
     "glr_validate_config", "glr_workspace_bytes", "glr_state_layout", "glr_create", "glr_step",
     "glr_sync_status", "glr_resume", "glr_next_step", "glr_destroy", "glr_status_string",
     "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
+    "glr_read_state", "glr_write_state",
 )
+STATE_PARTS = ("E", "Ebar", "Ut", "sigma", "J", "score", "S1", "S2", "Rbar", "info")
 PROF_GROUPS = ("ef_mean", "select", "topr", "proj", "rbar", "resid_opt", "full_refresh",
                "jac_init", "jac_update", "jac_finish", "refresh", "sub_iter", "jac_solve",
                "rr_update", "rr_solve", "sub_z", "sub_p", "sub_orth", "sub_chol")
@@ -66,6 +69,10 @@ class MatLayout(ctypes.Structure):
     ]
 
 
+class StateView(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in STATE_PARTS]
+
+
 _lib = None
 
 
@@ -95,6 +102,8 @@ def load():
         "glr_profile_enable": (I32, [VP, I32]),
         "glr_profile_reset": (I32, [VP]),
         "glr_profile_query": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
+        "glr_read_state": (I32, [VP, I32, P(StateView), VP]),
+        "glr_write_state": (I32, [VP, I32, P(StateView), VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -212,6 +221,34 @@ class GreedyLore:
     def resume(self, next_t):
         _check(self.lib.glr_resume(self.handle, int(next_t)), self.handle)
 
+    def _state_view(self, parts):
+        bad = set(parts) - set(STATE_PARTS)
+        if bad:
+            raise ValueError(f"unknown state parts {sorted(bad)}")
+        return StateView(**{k: ctypes.c_void_p(int(v.data_ptr()) if hasattr(v, "data_ptr") else int(v))
+                            for k, v in parts.items()})
+
+    def read_state(self, mat, **parts):
+        """Enqueues stream-ordered copies of matrix `mat`'s state parts into
+        the given tensors (host or device, contiguous, of the part's size):
+        read_state(0, E=t1, Ut=t2)."""
+        for k, v in parts.items():
+            if not v.is_contiguous():
+                raise ValueError(f"{k}: destination must be contiguous")
+        view = self._state_view(parts)
+        _check(self.lib.glr_read_state(self.handle, int(mat), ctypes.byref(view), self._stream_ptr()),
+               self.handle)
+
+    def write_state(self, mat, **parts):
+        """Enqueues copies of the given tensors into matrix `mat`'s state and
+        marks the state valid (a hand-off or a restore)."""
+        for k, v in parts.items():
+            if not v.is_contiguous():
+                raise ValueError(f"{k}: source must be contiguous")
+        view = self._state_view(parts)
+        _check(self.lib.glr_write_state(self.handle, int(mat), ctypes.byref(view), self._stream_ptr()),
+               self.handle)
+
     def next_step(self):
         t = ctypes.c_int64()
         _check(self.lib.glr_next_step(self.handle, ctypes.byref(t)), self.handle)
@@ -289,6 +326,12 @@ class GreedyLore:
         n = int(inf[0])
         hist = inf[2:2 + min(n, 60)].view(self.torch.float32).tolist()
         return n, bool(inf[1]), hist
+
+    def sub_info(self, mat):
+        """tau = 1 refresh: (block iterations run, relative gain of the energy
+        the leading r rows capture over the last iteration)."""
+        inf = self.info(mat).cpu()
+        return int(inf[62]), float(inf[63:64].view(self.torch.float32)[0])
 
     def P(self, mat):
         """d x r: the selected columns of U (P = U[:, J])."""

@@ -30,13 +30,41 @@ struct JacCtl {
   uint32_t history[kHistory];  // float bits of each sweep's largest off-norm
 };
 
+// Bits of the device status word (first word of the state blob), latched by
+// kernels and read and cleared by glr_sync_status.
+constexpr uint32_t kStatusNonfinite = 1u;       // a gradient held NaN or Inf
+constexpr uint32_t kStatusNotConverged = 2u;    // Jacobi sweeps ended above tol
+constexpr uint32_t kStatusBreakdown = 4u;       // an orthonormalisation still broke down after its repair pass
+constexpr uint32_t kStatusSubNotConverged = 8u; // tau = 1 block iteration above its tolerance after its budget
+constexpr uint32_t kStatusRepaired = 16u;       // dependent rows of an orthonormalisation were replaced
+
+// Info block of a matrix (kInfoInts ints in the state): [0] Jacobi sweeps of
+// the last refresh, [1] its converged flag, [2 + s] sweep s's largest pair
+// off-norm (float bits); for the tau = 1 refresh also:
+constexpr int kInfoSubIters = 62;    // block iterations run (fewer than the budget: the leading r rows met the tolerance)
+constexpr int kInfoSubGain = 63;     // float bits: relative gain of the captured energy over the last iteration
+
 // Control words of the subspace iteration (device memory).
 struct SubCtl {
   int iters;
-  int converged;
-  double change2;              // squared Frobenius norm of the last subspace change
-  uint32_t history[kHistory];  // float bits of each iteration's change / sqrt(K)
+  int converged;               // the leading r rows moved by less than the tolerance
+  double change2;              // squared Frobenius norm of the last change of the leading r rows
+  int gate_iter;               // nonzero: the current iteration is skipped (converged before it)
+  int gate_pass;               // nonzero: the current orthonormalisation pass is skipped
+  int repaired;                // rows replaced by the last orthonormalisation pass
+  int pad;
+  double e_in;                 // ||P[:r] Mo||^2 of the block entering the last iteration run
+  double e_out;                // ||P[:r] Mo||^2 of the final block
+  uint32_t history[kHistory];  // float bits of each iteration's change / sqrt(r)
 };
+
+// A CholeskyQR pivot of the diagonally scaled Gram (1 for a row independent of
+// the rows before it, 0 for a dependent one) at or below this marks its row
+// as dependent: the fp32 rows and their fp32-summed products resolve the
+// pivots only to about 1e-6.
+constexpr double kPivotFloor = 1e-5;
+// partial sums of a block's captured energy (fp64), before their in-order sum
+constexpr int kEnergyParts = 256;
 
 constexpr int kMaxSubK = 256;   // largest rank the subspace-iteration refresh takes
 constexpr int kCholTile = 64;   // tile of the K x K Cholesky factorisation
@@ -76,6 +104,7 @@ struct MatView {
   float* sub_P;  float* sub_Pn; float* sub_Z;  float* sub_Zt; float* sub_R; float* sub_part;
   double* sub_S; double* sub_L; double* sub_Dinv; double* sub_Li; double* sub_T;
   float* sub_Linv; float* sub_C; double* sub_sums; SubCtl* sub_ctl;
+  int* sub_bad;    // rows marked dependent by the current CholeskyQR pass (K ints)
   // Rayleigh-Ritz: Jacobi on the fp64 Gram of the K x D projection
   float* rr_Utw; float* rr_Y; double* rr_Apk; float* rr_V; double* rr_V64; int* rr_skip;
   JacCtl* rr_ctl; float* rr_sigw; int* rr_perm; double* rr_gpart;
@@ -215,9 +244,10 @@ hipError_t launch_gram_packed(const float* W, int64_t ld, int64_t n, int64_t Kc,
 
 // subspace iteration (tau = 1)
 size_t sub_part_floats(int K, int64_t d, int64_t D);
-hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStream_t s);
-hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hipStream_t s);
+hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, int64_t t, hipStream_t s);
+hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, const ProfHook& prof,
+                           hipStream_t s);
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s);
-hipError_t launch_sub_rr_end(const MatView& v, hipStream_t s);
+hipError_t launch_sub_rr_end(const MatView& v, float tol, hipStream_t s);
 
 }  // namespace glr

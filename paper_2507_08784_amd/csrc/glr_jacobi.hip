@@ -1083,9 +1083,16 @@ __global__ void k_diag_sqrt(const double* __restrict__ Apk, int64_t d, int nb, f
 }
 
 // the descending order of sigma (ties to the smaller index) by one block, in
-// n_pad keys of LDS
+// n_pad keys of LDS; the identity when `identity` (a sweep enqueued after the
+// refresh converged: the reordering then only moves the data to the other
+// buffer of the pair, so that every enqueued sweep leaves its result in the
+// same buffer whether it ran or not)
 __device__ __forceinline__ void sort_desc_block(const float* __restrict__ sig, int d, int n_pad,
-                                                int* __restrict__ perm, uint64_t* keys) {
+                                                int* __restrict__ perm, uint64_t* keys, bool identity = false) {
+  if (identity) {
+    for (int i = threadIdx.x; i < d; i += blockDim.x) perm[i] = i;
+    return;
+  }
   for (int i = threadIdx.x; i < n_pad; i += blockDim.x) {
     if (i < d) keys[i] = ((uint64_t)(~float_order(sig[i])) << 32) | (uint32_t)i;
     else keys[i] = ~0ull;
@@ -1095,9 +1102,10 @@ __device__ __forceinline__ void sort_desc_block(const float* __restrict__ sig, i
   for (int i = threadIdx.x; i < d; i += blockDim.x) perm[i] = (int)(keys[i] & 0xFFFFFFFFu);
 }
 __global__ void __launch_bounds__(1024)
-k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ perm) {
+k_sort_desc(const float* __restrict__ sig, int d, int n_pad, int* __restrict__ perm,
+            const JacCtl* __restrict__ ctl) {
   extern __shared__ __align__(16) unsigned char dyn[];
-  sort_desc_block(sig, d, n_pad, perm, reinterpret_cast<uint64_t*>(dyn));
+  sort_desc_block(sig, d, n_pad, perm, reinterpret_cast<uint64_t*>(dyn), ctl && ctl->converged);
 }
 
 __global__ void k_permute(const float* __restrict__ Utw, const float* __restrict__ sig_w,
@@ -1177,7 +1185,8 @@ hipError_t launch_jac_sort(const MatView& v, hipStream_t s) {
                      v.sigma_w);
   int n_pad = 2;
   while (n_pad < v.d) n_pad <<= 1;
-  hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d, n_pad, v.perm);
+  hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d, n_pad, v.perm,
+                     (const JacCtl*)v.ctl);
   const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
   hipLaunchKernelGGL(k_pk_permute, dim3((unsigned)((nblk + kPermBlocks - 1) / kPermBlocks)), dim3(256), 0, s, v.Apk,
                      v.Apk2, v.perm, v.d, nb);
@@ -1191,7 +1200,7 @@ hipError_t launch_jac_finish(const MatView& v, int max_sweeps, hipStream_t s) {
   int n_pad = 2;
   while (n_pad < v.d) n_pad <<= 1;
   hipLaunchKernelGGL(k_sort_desc, dim3(1), dim3(1024), (size_t)n_pad * 8, s, v.sigma_w, (int)v.d,
-                     n_pad, v.perm);
+                     n_pad, v.perm, (const JacCtl*)nullptr);
   hipLaunchKernelGGL(k_permute, dim3((unsigned)v.d), dim3(256), 0, s, v.Utw, v.sigma_w, v.perm, v.d,
                      v.Ut, v.sigma, v.J, v.r, v.ctl, v.info, v.status, max_sweeps);
   return hipGetLastError();
@@ -1222,27 +1231,27 @@ __global__ void k_joint_diag_sqrt(const JointMat* __restrict__ jm, const int* __
   diag_sqrt_at(v.Apk, v.d, jm[m].nb, v.sigma_w, (int64_t)(blockIdx.x - first[m]) * blockDim.x + threadIdx.x);
 }
 
+// a converged matrix takes the identity order: its data only moves to the
+// other buffer (see sort_desc_block), so every matrix ends in the buffer of
+// the last enqueued sweep
 __global__ void __launch_bounds__(1024) k_joint_sort_desc(const JointMat* __restrict__ jm, int par) {
   const MatView& v = jm[blockIdx.x].v[par];
-  if (v.ctl->converged) return;
   extern __shared__ __align__(16) unsigned char dyn[];
   int n_pad = 2;
   while (n_pad < v.d) n_pad <<= 1;
-  sort_desc_block(v.sigma_w, (int)v.d, n_pad, v.perm, reinterpret_cast<uint64_t*>(dyn));
+  sort_desc_block(v.sigma_w, (int)v.d, n_pad, v.perm, reinterpret_cast<uint64_t*>(dyn), v.ctl->converged != 0);
 }
 
 __global__ void __launch_bounds__(256)
 k_joint_pk_permute(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par) {
   const int m = joint_find(first, num, blockIdx.x);
   const MatView& v = jm[m].v[par];
-  if (v.ctl->converged) return;
   pk_permute_blocks(v.Apk, v.Apk2, v.perm, v.d, jm[m].nb, blockIdx.x - first[m]);
 }
 
 __global__ void k_joint_row_gather(const JointMat* __restrict__ jm, const int* __restrict__ first, int num, int par) {
   const int m = joint_find(first, num, blockIdx.x);
   const MatView& v = jm[m].v[par];
-  if (v.ctl->converged) return;
   row_gather_row(v.Utw, v.W, v.perm, v.d, blockIdx.x - first[m]);
 }
 

@@ -38,7 +38,7 @@ struct WsLayout {
   uint64_t off_Mbar, off_Q, off_Qpart, off_lam, off_W, off_Utw, off_gram, off_gram2, off_V, off_V64, off_gpart, off_skip,
       off_ctl, off_sigw, off_perm;
   uint64_t off_sP, off_sPn, off_sZ, off_sZt, off_sR, off_spart, off_sS, off_sL, off_sDinv, off_sLi,
-      off_sT, off_sLinv, off_sC, off_ssums, off_sctl;
+      off_sT, off_sLinv, off_sC, off_ssums, off_sctl, off_sbad;
   uint64_t off_rUtw, off_rY, off_rgram, off_rV, off_rV64, off_rgpart, off_rskip, off_rctl, off_rsigw,
       off_rperm;
   uint64_t bytes;
@@ -161,7 +161,7 @@ uint64_t state_bytes_of(const glr_config* c) {
 
 WsLayout ws_layout(const glr_config* c, int first, int last) {
   uint64_t mx_mn = 0, mx_Q = 0, mx_Qp = 0, mx_lam = 0, mx_dD = 0, mx_dd = 0, mx_gram = 0, mx_groups = 0, mx_vbuf = 0, mx_d = 0;
-  uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0;
+  uint64_t s_Kd = 0, s_KD = 0, s_part = 0, s_KK = 0, s_Kp2 = 0, s_nt = 0, s_sums = 0, s_Kp = 0;
   uint64_t r_gram = 0, r_groups = 0, r_vbuf = 0, r_gpart = 0, mx_gpart = 0;
   auto mx = [](uint64_t& a, uint64_t b) { if (b > a) a = b; };
   for (int i = first; i < last; ++i) {
@@ -184,9 +184,11 @@ WsLayout ws_layout(const glr_config* c, int first, int last) {
       const int rs = gram_splits(Ki, x.D);
       if (rs > 1) mx(r_gpart, (uint64_t)rs * K * K);
       mx(s_KK, K * K);
+      mx(s_Kp, Kp);
       mx(s_Kp2, Kp * Kp);
       mx(s_nt, Kp / kCholTile);
       mx(s_sums, (uint64_t)gemm_blocks(Ki, (int)x.d));
+      mx(s_sums, (uint64_t)kEnergyParts);
     } else {
       mx(mx_dD, (uint64_t)(x.d * x.D));
       mx(mx_dd, (uint64_t)(x.d * x.d));
@@ -234,6 +236,7 @@ WsLayout ws_layout(const glr_config* c, int first, int last) {
   w.off_sC = take(s_KK * 4);
   w.off_ssums = take(s_sums * 8);
   w.off_sctl = take(sizeof(SubCtl));
+  w.off_sbad = take(s_Kp * 4);
   w.off_rUtw = take(s_KK * 4);
   w.off_rY = take(s_KK * 4);
   w.off_rgram = take(r_gram * 8);
@@ -319,11 +322,20 @@ struct glr_handle {
   int jac_sort = 1;    // reorder rows by descending norm before every sweep
   double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
   int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
+  // Sweep budgets: a refresh enqueues a fixed number of Jacobi sweeps (those
+  // after convergence return at once) and never waits for the device.  The
+  // sweeps each matrix's last refresh needed come back through pinned host
+  // memory, read only once the copy's event has completed.
+  std::vector<int> known_sweeps;       // sweeps of the last refresh read back (-1: none yet)
+  std::vector<int> known_conv;         // its converged flag
+  std::vector<int> info_pending;       // a read-back is in flight
+  int64_t repaired_total = 0;          // status reads that found replaced (dependent) rows
+  int* info_host = nullptr;            // pinned, 2 ints per matrix
+  std::vector<hipEvent_t> info_ev;
   bool prof = false;
   bool joint = false;                  // refresh steps sweep all matrices in shared launches
   std::vector<JointMat> jm;            // host copies of the joint tables (kept for the async upload)
   std::vector<int> jfirst;
-  std::vector<int> jflags;             // converged flags read back after every joint sweep
   JointPlan jp;
   bool grouped = false;                // selection steps launch each kernel once for all matrices
   std::vector<int> gfirst;
@@ -419,6 +431,7 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G, int lane) {
   v.sub_C = (float*)(w + WL.off_sC);
   v.sub_sums = (double*)(w + WL.off_ssums);
   v.sub_ctl = (SubCtl*)(w + WL.off_sctl);
+  v.sub_bad = (int*)(w + WL.off_sbad);
   v.rr_Utw = (float*)(w + WL.off_rUtw);
   v.rr_Y = (float*)(w + WL.off_rY);
   v.rr_Apk = (double*)(w + WL.off_rgram);
@@ -507,6 +520,33 @@ hipError_t prof_collect(glr_handle* h) {
     if (e_ != hipSuccess) return hip_fail(h, e_, #call); \
   } while (0)
 
+// Sweeps to enqueue for a refresh of `mat`: every allowed sweep until a
+// refresh of this matrix has been read back converged, then that count plus
+// a margin (a quarter, at least three).  A refresh that runs out of its
+// budget reports GLR_ERR_NOT_CONVERGED like one that runs out of max_sweeps,
+// and the next refresh gets every allowed sweep again.
+int sweep_budget(glr_handle* h, int mat) {
+  const int mx = h->cfg.max_sweeps;
+  if (h->info_pending[(size_t)mat] && hipEventQuery(h->info_ev[(size_t)mat]) == hipSuccess) {
+    h->info_pending[(size_t)mat] = 0;
+    h->known_sweeps[(size_t)mat] = h->info_host[2 * mat];
+    h->known_conv[(size_t)mat] = h->info_host[2 * mat + 1];
+  }
+  const int k = h->known_sweeps[(size_t)mat];
+  if (k < 0 || !h->known_conv[(size_t)mat]) return mx;
+  const int b = k + std::max(3, k / 4);
+  return b < mx ? b : mx;
+}
+
+// after a refresh's finish: its sweep count and converged flag to the host
+hipError_t read_back_info(glr_handle* h, int mat, const MatView& v, hipStream_t s) {
+  if (h->info_pending[(size_t)mat]) return hipSuccess;   // the previous read-back is still in flight
+  hipError_t e = hipMemcpyAsync(h->info_host + 2 * mat, v.info, 2 * sizeof(int), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipEventRecord(h->info_ev[(size_t)mat], s);
+  if (e == hipSuccess) h->info_pending[(size_t)mat] = 1;
+  return e;
+}
+
 // one sweep of the round-robin tournament: solve(0), then per round the Gram
 // update and the next round's solves fused with this round's U rotation
 hipError_t jacobi_sweep(glr_handle* h, const MatView& v, int rounds, int g_solve, int g_update, hipStream_t s) {
@@ -547,6 +587,10 @@ glr_status svd_end(glr_handle* h, const MatView& v, hipStream_t s) {
   return GLR_OK;
 }
 
+// The sweeps are enqueued up to the matrix's budget without waiting: a sweep
+// after convergence returns at once, its reordering reduced to a copy into
+// the other buffer of the pair (so the result is in the buffer of the last
+// enqueued sweep whether that sweep ran or not).
 glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   MatView v = v0;   // the sort swaps Apk <-> Apk2 and Utw <-> W
@@ -554,7 +598,8 @@ glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t 
   glr_status st = svd_begin(h, v, t, s);
   if (st != GLR_OK) return st;
   const int rounds = jac_rounds(v.d);
-  for (int sw = 0; sw < c.max_sweeps; ++sw) {
+  const int budget = sweep_budget(h, v.mat);
+  for (int sw = 0; sw < budget; ++sw) {
     if (h->jac_sort == 1 || (h->jac_sort == 2 && sw == 0)) {
       GLR_HIP(h, launch_jac_sort(v, s));
       std::swap(v.Apk, v.Apk2);
@@ -562,12 +607,11 @@ glr_status refresh_svd(glr_handle* h, const MatView& v0, int64_t t, hipStream_t 
     }
     GLR_HIP(h, jacobi_sweep(h, v, rounds, GLR_PROF_JAC_SOLVE, GLR_PROF_JAC_UPDATE, s));
     GLR_HIP(h, launch_jac_check(v, c.tol, s));
-    uint32_t conv = 0;
-    GLR_HIP(h, hipMemcpyAsync(&conv, &v.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
-    GLR_HIP(h, hipStreamSynchronize(s));
-    if (conv) break;
   }
-  return svd_end(h, v, s);
+  st = svd_end(h, v, s);
+  if (st != GLR_OK) return st;
+  GLR_HIP(h, read_back_info(h, v.mat, v, s));
+  return GLR_OK;
 }
 
 // tau = 1 refresh: top-r block of U by oversampled subspace iteration and a
@@ -580,28 +624,26 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   ProfScope all(h, s, GLR_PROF_REFRESH);
   {
     ProfScope p(h, s, GLR_PROF_JAC_INIT);
-    GLR_HIP(h, launch_sub_start(v, warm, c.seed, s));
+    GLR_HIP(h, launch_sub_start(v, warm, c.seed, t, s));
   }
   HookCtx hc{h, s, {}};
   const ProfHook hook{&hc, prof_hook_fn};
   for (int it = 0; it < iters; ++it) {
     ProfScope p(h, s, GLR_PROF_SUB_ITER);
-    GLR_HIP(h, launch_sub_iter(v, sub_tol, hook, s));
+    GLR_HIP(h, launch_sub_iter(v, sub_tol, c.seed, t, it, hook, s));
   }
   MatView rr;
   GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
   const int rounds = jac_rounds(rr.d);
-  for (int sw = 0; sw < c.max_sweeps; ++sw) {
+  const int budget = sweep_budget(h, v.mat);
+  for (int sw = 0; sw < budget; ++sw) {
     GLR_HIP(h, jacobi_sweep(h, rr, rounds, GLR_PROF_RR_SOLVE, GLR_PROF_RR_UPDATE, s));
     GLR_HIP(h, launch_jac_check(rr, c.tol, s));
-    uint32_t conv = 0;
-    GLR_HIP(h, hipMemcpyAsync(&conv, &rr.ctl->converged, sizeof conv, hipMemcpyDeviceToHost, s));
-    GLR_HIP(h, hipStreamSynchronize(s));
-    if (conv) break;
   }
   ProfScope p(h, s, GLR_PROF_JAC_FINISH);
   GLR_HIP(h, launch_jac_finish(rr, c.max_sweeps, s));
-  GLR_HIP(h, launch_sub_rr_end(v, s));
+  GLR_HIP(h, launch_sub_rr_end(v, sub_tol, s));
+  GLR_HIP(h, read_back_info(h, v.mat, v, s));
   return GLR_OK;
 }
 
@@ -722,9 +764,11 @@ glr_status step_joint(glr_handle* h, float* const* X, const float* const* G, int
   });
   if (st != GLR_OK) return st;
   const JointPlan& jp = h->jp;
-  std::vector<int> last((size_t)num, -1);   // the sweep after which each matrix converged
-  int left = num, sweeps = 0;
-  for (int sw = 0; sw < c.max_sweeps && left > 0; ++sw, ++sweeps) {
+  // as many sweeps as the matrix with the largest budget needs; a converged
+  // matrix's later sweeps only move its data to the other buffer of the pair
+  int budget = 1;
+  for (int i = 0; i < num; ++i) budget = std::max(budget, sweep_budget(h, i));
+  for (int sw = 0; sw < budget; ++sw) {
     const int par = sw & 1, p = par ^ 1;   // the sort reads parity par and fills the other
     GLR_HIP(h, launch_joint_sort(jp, par, s));
     GLR_HIP(h, launch_joint_solve(jp, p, 0, c.tol, h->jac_inner, h->jac_floor2, s));
@@ -733,18 +777,12 @@ glr_status step_joint(glr_handle* h, float* const* X, const float* const* G, int
       GLR_HIP(h, launch_joint_solve_apply(jp, p, k + 1, c.tol, h->jac_inner, h->jac_floor2, s));
     }
     GLR_HIP(h, launch_joint_check(jp, c.tol, s));
-    GLR_HIP(h, hipMemcpyAsync(h->jflags.data(), jp.flags, (size_t)num * sizeof(int), hipMemcpyDeviceToHost, s));
-    GLR_HIP(h, hipStreamSynchronize(s));
-    for (int i = 0; i < num; ++i)
-      if (h->jflags[(size_t)i] && last[(size_t)i] < 0) {
-        last[(size_t)i] = sw;
-        --left;
-      }
   }
   return on_lanes(h, s, [&](int i, int lane, hipStream_t ls) -> glr_status {
     const MatView v = view_of(h, i, X[i], G[i], lane);
-    const int ran = last[(size_t)i] >= 0 ? last[(size_t)i] : sweeps - 1;
-    const glr_status r = svd_end(h, h->jm[(size_t)i].v[(ran + 1) & 1], ls);
+    const MatView& fin = h->jm[(size_t)i].v[budget & 1];
+    glr_status r = svd_end(h, fin, ls);
+    if (r == GLR_OK && read_back_info(h, i, v, ls) != hipSuccess) r = fail(h, GLR_ERR_DEVICE, "info read-back");
     return r != GLR_OK ? r : step_tail(h, v, true, ls);
   });
 }
@@ -783,7 +821,6 @@ hipError_t joint_setup(glr_handle* h, hipStream_t s) {
     h->jfirst[(size_t)k * (num + 1) + num] = (int)acc;
     jp.total[k] = (int)acc;
   }
-  h->jflags.assign((size_t)num, 0);
   jp.jm = (const JointMat*)(h->work + h->ws.off_views);
   jp.first = (const int*)(h->work + h->ws.off_first);
   jp.flags = (int*)(h->work + h->ws.off_first) + (size_t)kJointKinds * (num + 1);
@@ -894,6 +931,16 @@ void release_group(glr_handle* h) {
   h->gring = nullptr;
 }
 
+void release_info(glr_handle* h) {
+  for (hipEvent_t& e : h->info_ev) {
+    if (e) (void)hipEventSynchronize(e);
+    if (e) (void)hipEventDestroy(e);
+    e = nullptr;
+  }
+  if (h->info_host) (void)hipHostFree(h->info_host);
+  h->info_host = nullptr;
+}
+
 void release_lanes(glr_handle* h) {
   for (int k = 0; k < kMaxLanes; ++k) {
     if (h->lane_s[k]) (void)hipStreamDestroy(h->lane_s[k]);
@@ -991,6 +1038,14 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[k], hipEventDisableTiming);
   }
   if (e == hipSuccess && h->lanes > 1) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+  h->known_sweeps.assign((size_t)cfg->num_mats, -1);
+  h->known_conv.assign((size_t)cfg->num_mats, 0);
+  h->info_pending.assign((size_t)cfg->num_mats, 0);
+  h->info_ev.assign((size_t)cfg->num_mats, nullptr);
+  if (e == hipSuccess)
+    e = hipHostMalloc((void**)&h->info_host, 2 * sizeof(int) * (size_t)cfg->num_mats, hipHostMallocDefault);
+  for (int i = 0; e == hipSuccess && i < cfg->num_mats; ++i)
+    e = hipEventCreateWithFlags(&h->info_ev[(size_t)i], hipEventDisableTiming);
   if (e == hipSuccess && joint_allowed(h)) {
     h->joint = true;
     e = joint_setup(h, st);
@@ -1003,6 +1058,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
     std::string m = fmt("glr_create: %s", hipGetErrorString(e));
     release_group(h);
     release_lanes(h);
+    release_info(h);
     delete h;
     return fail(nullptr, GLR_ERR_DEVICE, m);
   }
@@ -1055,11 +1111,19 @@ glr_status glr_sync_status(glr_handle* h, void* stream) {
     GLR_HIP(h, launch_fill_zero(h->state, 4, s));
     GLR_HIP(h, hipStreamSynchronize(s));
   }
-  if (word & 1u) {
+  h->repaired_total += (word & kStatusRepaired) ? 1 : 0;
+  if (word & kStatusNonfinite) {
     h->suspect = true;
     return fail(h, GLR_ERR_NONFINITE, "a gradient held NaN or Inf");
   }
-  if (word & 2u) return fail(h, GLR_ERR_NOT_CONVERGED, "a refresh reached max_sweeps before tol");
+  if (word & kStatusBreakdown) {
+    h->suspect = true;
+    return fail(h, GLR_ERR_BREAKDOWN, "a tau = 1 orthonormalisation found dependent rows after its repair pass");
+  }
+  if (word & kStatusNotConverged)
+    return fail(h, GLR_ERR_NOT_CONVERGED, "a refresh ended its Jacobi sweeps (budget or max_sweeps) above tol");
+  if (word & kStatusSubNotConverged)
+    return fail(h, GLR_ERR_NOT_CONVERGED, "a tau = 1 block iteration ended its iterations above its tolerance");
   return GLR_OK;
 }
 
@@ -1070,6 +1134,62 @@ glr_status glr_resume(glr_handle* h, int64_t next_t) {
   h->suspect = false;
   h->err.clear();
   return GLR_OK;
+}
+
+namespace {
+// (pointer into the state, bytes) of each glr_state_view member of matrix mat,
+// in member order
+struct StatePart {
+  uint64_t off, bytes;
+};
+void state_parts(const glr_handle* h, int mat, StatePart (&p)[10]) {
+  const glr_mat_layout& L = h->lay[(size_t)mat];
+  const uint64_t mn = (uint64_t)(L.m * L.n), N = (uint64_t)h->cfg.num_workers;
+  p[0] = {L.off_E, N * mn * 4};
+  p[1] = {L.off_Ebar, mn * 4};
+  p[2] = {L.off_U, (uint64_t)(L.d * L.d) * 4};
+  p[3] = {L.off_sigma, (uint64_t)L.d * 4};
+  p[4] = {L.off_J, (uint64_t)L.r * 4};
+  p[5] = {L.off_score, (uint64_t)L.d * 4};
+  p[6] = {L.off_S1, mn * 4};
+  p[7] = {L.off_S2, L.off_S2 ? mn * 4 : 0};
+  p[8] = {L.off_Rbar, (uint64_t)L.r * (uint64_t)L.D * 4};
+  p[9] = {L.off_info, (uint64_t)kInfoInts * 4};
+}
+void* const* view_members(const glr_state_view* v) { return reinterpret_cast<void* const*>(v); }
+
+glr_status copy_state(glr_handle* h, int32_t mat, const glr_state_view* view, bool to_state, void* stream) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (!view) return fail(h, GLR_ERR_INVALID_ARG, "state view is NULL");
+  if (mat < 0 || mat >= h->cfg.num_mats) return fail(h, GLR_ERR_INVALID_ARG, "matrix index out of range");
+  static_assert(sizeof(glr_state_view) == 10 * sizeof(void*), "glr_state_view holds ten pointers");
+  StatePart part[10];
+  state_parts(h, mat, part);
+  void* const* ptr = view_members(view);
+  if (ptr[7] && part[7].bytes == 0) return fail(h, GLR_ERR_INVALID_ARG, "S2 exists only for Adam");
+  hipStream_t s = (hipStream_t)stream;
+  for (int k = 0; k < 10; ++k) {
+    if (!ptr[k] || part[k].bytes == 0) continue;
+    char* at = h->state + part[k].off;
+    if (to_state) GLR_HIP(h, hipMemcpyAsync(at, ptr[k], part[k].bytes, hipMemcpyDefault, s));
+    else GLR_HIP(h, hipMemcpyAsync(ptr[k], at, part[k].bytes, hipMemcpyDefault, s));
+  }
+  return GLR_OK;
+}
+}  // namespace
+
+glr_status glr_read_state(glr_handle* h, int32_t mat, const glr_state_view* dst, void* stream) {
+  return copy_state(h, mat, dst, false, stream);
+}
+
+glr_status glr_write_state(glr_handle* h, int32_t mat, const glr_state_view* src, void* stream) {
+  const glr_status st = copy_state(h, mat, src, true, stream);
+  if (st == GLR_OK) {
+    std::lock_guard<std::mutex> lk(h->mu);
+    h->suspect = false;
+    h->err.clear();
+  }
+  return st;
 }
 
 glr_status glr_next_step(const glr_handle* h, int64_t* next_t) {
@@ -1083,6 +1203,7 @@ glr_status glr_destroy(glr_handle* h) {
   for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
   release_group(h);
   release_lanes(h);
+  release_info(h);
   delete h;
   return GLR_OK;
 }
@@ -1120,6 +1241,7 @@ const char* glr_status_string(glr_status s) {
     case GLR_ERR_DEVICE: return "device error";
     case GLR_ERR_NONFINITE: return "non-finite gradient";
     case GLR_ERR_NOT_CONVERGED: return "refresh not converged";
+    case GLR_ERR_BREAKDOWN: return "orthonormalisation breakdown";
   }
   return "unknown status";
 }

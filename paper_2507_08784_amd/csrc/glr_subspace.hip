@@ -28,12 +28,15 @@ namespace glr {
 //   EPI 0: C = acc
 //   EPI 1: C = X - acc, and per block the sum of squares of C (fp64) in sums
 //   EPI 2: C = X - acc
+// A launch whose gate word is set returns at once (a section of the tau = 1
+// refresh that the device skipped: converged, or no repair to finish).
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool B_KC, int EPI>
 __global__ void __launch_bounds__(256)
 k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, int64_t ldb,
        float* __restrict__ C, int64_t ldc, int M, int N, int Kc, int kslice, int64_t cstride,
-       const float* __restrict__ X, double* __restrict__ sums) {
+       const float* __restrict__ X, double* __restrict__ sums, const int* __restrict__ gate) {
+  if (gate && *gate) return;
   using T = MfmaTile<BM, BN, WM, WN>;
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
@@ -102,21 +105,23 @@ GemmPlan plan_splits(int M, int N, int Kc, int want_blocks) {
 template <bool B_KC, int EPI>
 static void gemm_launch(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
                         int64_t ldc, int M, int N, int Kc, GemmPlan p, int64_t cstride,
-                        const float* X, double* sums, hipStream_t s) {
+                        const float* X, double* sums, hipStream_t s, const int* gate = nullptr) {
   // 64-row tiles when M is not a multiple of 128 (no half-empty last row of tiles)
   const int bm = gemm_rows(M);
   dim3 grid((N + 127) / 128, (M + bm - 1) / bm, p.splits);
   if (bm == 64)
     hipLaunchKernelGGL((k_gemm<64, 128, 1, 4, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums);
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate);
   else
     hipLaunchKernelGGL((k_gemm<128, 128, 2, 2, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums);
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate);
 }
 
 // out[i] = sum over splits of part[s * count + i], in a fixed order, fp64
 __global__ void k_reduce_splits(const float* __restrict__ part, int splits, int64_t count,
-                                float* __restrict__ out32, double* __restrict__ out64) {
+                                float* __restrict__ out32, double* __restrict__ out64,
+                                const int* __restrict__ gate) {
+  if (gate && *gate) return;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += stride) {
     // partials summed in split order; loads issued 8 at a time
@@ -321,8 +326,9 @@ hipError_t launch_reorth(const MatView& v, hipStream_t s) {
 //   block row p of X:  X_pp = D_p,  X_pc = -D_p sum_{c <= k < p} L_pk X_kc.
 // Every tile a launch reads was finished by an earlier launch.  Products are
 // fp64 MFMA on LDS tiles.  The result is written as fp32 Linv (Kp x Kp, zero
-// above the diagonal).  A non-positive pivot sets status bit 4 and is replaced
-// by a tiny positive value so that the iteration can continue.
+// above the diagonal).  A pivot at or below kPivotFloor (a row that depends on
+// the rows before it: a rank-deficient block, zero gradients included) is
+// taken as 1 and its row is marked, so that the pass can replace it.
 // ---------------------------------------------------------------------------
 constexpr int CT = kCholTile;
 constexpr int CLD = CT + 1;
@@ -416,8 +422,12 @@ __device__ __forceinline__ double lane_bcast(double x, int l) {
 // the factor: lane l holds row l % 16 in registers.  Right-looking: after step
 // j, column j of L is final and row j of X = L^-1 is final once scaled by
 // 1 / L_jj; the later rows then subtract L_ij X_j.  L replaces the block
-// (zeros above the diagonal), X goes into Dl at the same place.
-__device__ __forceinline__ void chol16(CTile* T, CTile* Dl, int o, bool& bad) {
+// (zeros above the diagonal), X goes into Dl at the same place.  A pivot at
+// or below kPivotFloor (the row depends on the rows before it) is taken as 1
+// with a zero column below it, and the row (global index row0 + o + j) is
+// marked in `bad` for replacement.
+__device__ __forceinline__ void chol16(CTile* T, CTile* Dl, int o, int row0, int* __restrict__ bad,
+                                       bool& marked) {
   const int li = lane_id() & 15;
   double a[16], y[16];
 #pragma unroll
@@ -428,9 +438,14 @@ __device__ __forceinline__ void chol16(CTile* T, CTile* Dl, int o, bool& bad) {
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     double piv = lane_bcast(a[j], j);
-    if (!(piv > 0.0)) { bad = true; piv = 1e-300; }
+    const bool dep = !(piv > kPivotFloor);
+    if (dep) {
+      piv = 1.0;
+      marked = true;
+      if (lane_id() == 0 && bad) bad[row0 + o + j] = 1;
+    }
     const double ljj = sqrt(piv), inv = 1.0 / ljj;
-    a[j] = (li > j) ? a[j] * inv : ((li == j) ? ljj : 0.0);
+    a[j] = (li > j) ? (dep ? 0.0 : a[j] * inv) : ((li == j) ? ljj : 0.0);
 #pragma unroll
     for (int k = j + 1; k < 16; ++k) a[k] = fma(-a[j], lane_bcast(a[j], k), a[k]);
     const double sc = (li == j) ? inv : 1.0;
@@ -487,15 +502,16 @@ __device__ __forceinline__ f64x4 blk_load(const CTile* Cs, int cr, int cc) {
 // diagonal block, the blocks below it become L_iq = A_iq X_qq^T and the
 // trailing lower blocks take A_ij -= L_iq L_jq^T (fp64 MFMA, one block per
 // wave).  The off-diagonal blocks of X then follow block row by block row:
-// X_ij = -X_ii sum_{j <= k < i} L_ik X_kj.
-__device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
+// X_ij = -X_ii sum_{j <= k < i} L_ik X_kj.  Dependent rows are marked (see
+// chol16); row0 is the global index of the tile's first row.
+__device__ void chol_tile(CTile* T, CTile* Dl, int row0, int* __restrict__ bad) {
   const int w = wave_id();
   for (int e = threadIdx.x; e < CT * CT; e += 256) Dl[e / CT][e % CT] = 0.0;
-  bool bad = false;
+  bool marked = false;
   __syncthreads();
   for (int q = 0; q < 4; ++q) {
     const int o = 16 * q;
-    if (w == 0) chol16(T, Dl, o, bad);
+    if (w == 0) chol16(T, Dl, o, row0, bad, marked);
     __syncthreads();
     if (w < 3 - q) {
       const int i = 16 * (q + 1 + w);
@@ -514,7 +530,7 @@ __device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
     }
     __syncthreads();
   }
-  if (bad && threadIdx.x == 0) atomicOr(status, 4u);
+  (void)marked;
   for (int bi = 1; bi < 4; ++bi) {
     if (w < bi) {
       f64x4 acc{0.0, 0.0, 0.0, 0.0};
@@ -534,7 +550,9 @@ __device__ void chol_tile(CTile* T, CTile* Dl, uint32_t* status) {
 // work matrix; block 0 factors tile (0, 0)
 __global__ void __launch_bounds__(256)
 k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ Sw,
-             double* __restrict__ Lm, double* __restrict__ Dm, uint32_t* __restrict__ status) {
+             double* __restrict__ Lm, double* __restrict__ Dm, int* __restrict__ bad,
+             const int* __restrict__ gate) {
+  if (*gate) return;
   const int64_t n = (int64_t)Kp * Kp;
   for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
     const int i = (int)(e / Kp), j = (int)(e % Kp);
@@ -549,7 +567,7 @@ k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ S
                                : (i == j ? 1.0 : 0.0);
   }
   __syncthreads();
-  chol_tile(T, Dl, status);
+  chol_tile(T, Dl, 0, bad);
   tile_store(T, Lm, Kp, true);
   tile_store(Dl, Dm, CT, false);
 }
@@ -557,7 +575,8 @@ k_chol_first(const double* __restrict__ S, int K, int Kp, double* __restrict__ S
 __global__ void __launch_bounds__(256)
 k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, double* __restrict__ Dm,
             double* __restrict__ Xm, float* __restrict__ Linv, const double* __restrict__ S, int K,
-            uint32_t* __restrict__ status) {
+            int* __restrict__ bad, const int* __restrict__ gate) {
+  if (*gate) return;
   __shared__ CTile A[CT], B[CT], C[CT];
   const int nt = Kp / CT;
   const int mrows = nt - p - 1;
@@ -602,7 +621,7 @@ k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, dou
       __syncthreads();
       acc_to_lds(acc, A, false);
       __syncthreads();
-      chol_tile(A, B, status);
+      chol_tile(A, B, I * CT, bad);
       tile_store(A, tile(Lm, I, I), Kp, true);
       tile_store(B, Dm + (int64_t)I * CT * CT, CT, false);
     } else {
@@ -648,14 +667,14 @@ k_chol_step(int p, int Kp, double* __restrict__ Sw, double* __restrict__ Lm, dou
   tile_store32(B, lo, Kp, S, K, c * CT);
 }
 
-static hipError_t launch_chol_inv(const MatView& v, int K, hipStream_t s) {
+static hipError_t launch_chol_inv(const MatView& v, int K, const int* gate, hipStream_t s) {
   const int Kp = chol_pad(K), nt = Kp / CT;
   hipLaunchKernelGGL(k_chol_first, dim3(16), dim3(256), 0, s, v.sub_S, K, Kp, v.sub_T, v.sub_L,
-                     v.sub_Dinv, v.status);
+                     v.sub_Dinv, v.sub_bad, gate);
   for (int p = 0; p < nt; ++p) {
     const int m = nt - p - 1;
     hipLaunchKernelGGL(k_chol_step, dim3(m * (m + 1) / 2 + nt), dim3(256), 0, s, p, Kp, v.sub_T,
-                       v.sub_L, v.sub_Dinv, v.sub_Li, v.sub_Linv, v.sub_S, K, v.status);
+                       v.sub_L, v.sub_Dinv, v.sub_Li, v.sub_Linv, v.sub_S, K, v.sub_bad, gate);
   }
   return hipGetLastError();
 }
@@ -676,7 +695,9 @@ __global__ void k_sub_random(float* __restrict__ Pt, int K, int64_t d, uint32_t 
   }
 }
 
-__global__ void k_sum_double(const double* __restrict__ x, int n, double* __restrict__ out) {
+__global__ void k_sum_double(const double* __restrict__ x, int n, double* __restrict__ out,
+                             const int* __restrict__ gate) {
+  if (gate && *gate) return;
   __shared__ double red[4];
   double s = 0.0;
   for (int i = threadIdx.x; i < n; i += blockDim.x) s += x[i];
@@ -691,6 +712,11 @@ __global__ void k_sub_reset(SubCtl* sc) {
     sc->iters = 0;
     sc->converged = 0;
     sc->change2 = 0.0;
+    sc->e_in = 0.0;
+    sc->e_out = 0.0;
+    sc->gate_iter = 0;
+    sc->gate_pass = 0;
+    sc->repaired = 0;
   }
 }
 
@@ -700,6 +726,94 @@ __global__ void k_sub_step(SubCtl* sc, int K, float tol) {
   if (sc->iters < kHistory) sc->history[sc->iters] = __float_as_uint((float)ch);
   sc->iters += 1;
   if (ch <= (double)tol) sc->converged = 1;
+}
+
+// part[b] = the sum of squares (fp64) of the elements b, b + nb, ... of the
+// first `count` elements of x (a fixed order: deterministic)
+__global__ void k_sumsq_part(const float* __restrict__ x, int64_t count, double* __restrict__ part,
+                             const int* __restrict__ gate) {
+  if (gate && *gate) return;
+  __shared__ double red[4];
+  double s = 0.0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += stride) {
+    const double v = (double)x[i];
+    s += v * v;
+  }
+  s = wave_sum(s);
+  if (lane_id() == 0) red[wave_id()] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
+// *out = 1 (skip the next section) when *skip is set, or when `need` is given
+// and *need is not set; 0 otherwise
+__global__ void k_gate(int* __restrict__ out, const int* __restrict__ skip, const int* __restrict__ need) {
+  if (threadIdx.x == 0) *out = ((skip && *skip) || (need && !*need)) ? 1 : 0;
+}
+
+// start of a CholeskyQR pass: no row marked, nothing replaced yet
+__global__ void k_pass_reset(int* __restrict__ bad, int K, int* __restrict__ repaired,
+                             const int* __restrict__ gate) {
+  if (*gate) return;
+  for (int k = threadIdx.x; k < K; k += blockDim.x) bad[k] = 0;
+  if (threadIdx.x == 0) *repaired = 0;
+}
+
+__global__ void k_copy_gated(const float* __restrict__ src, float* __restrict__ dst, int64_t n,
+                             const int* __restrict__ gate) {
+  if (*gate) return;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+// Each row k of Y (K x L) that the pass's factorisation marked as dependent
+// is replaced by a row of N(0, 1) values (Philox, counter (c, k, mat, tag)):
+// a direction that is independent of the other rows with probability one, so
+// that the next pass completes the orthonormal block.  In the last pass a
+// pass may run, a marked row means the block could not be completed: the
+// breakdown bit of the status word.
+__global__ void k_orth_repair(float* __restrict__ Y, int64_t L, const int* __restrict__ bad,
+                              int* __restrict__ repaired, const int* __restrict__ gate, uint32_t k0,
+                              uint32_t k1, uint32_t mat, uint32_t tag, int last_pass,
+                              uint32_t* __restrict__ status) {
+  if (*gate) return;
+  const int k = blockIdx.x;
+  if (!bad[k]) return;
+  const int64_t n4 = (L + 3) / 4;
+  for (int64_t c = threadIdx.x; c < n4; c += blockDim.x) {
+    float z[4];
+    normals4((uint32_t)c, (uint32_t)k, mat, tag, k0, k1, z);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (4 * c + e < L) Y[(int64_t)k * L + 4 * c + e] = z[e];
+  }
+  if (threadIdx.x == 0) {
+    atomicOr(repaired, 1);
+    atomicOr(status, last_pass ? kStatusBreakdown : kStatusRepaired);
+  }
+}
+
+// The refresh's iteration record, and its convergence: the last iteration
+// run raised the energy the leading r rows capture, ||P[:r] Mo||^2, by at
+// most tol relative.  (Rotations inside a cluster of equal singular values,
+// where no iteration converges, gain nothing; neither do zero or exactly
+// rank-deficient gradients.)
+__global__ void k_sub_finish(const SubCtl* __restrict__ sc, int* __restrict__ info, uint32_t* __restrict__ status,
+                             float tol) {
+  if (threadIdx.x != 0) return;
+  const double gain = sc->e_out > 0.0 ? (sc->e_out - sc->e_in) / sc->e_out : 0.0;
+  info[kInfoSubIters] = sc->iters;
+  info[kInfoSubGain] = (int)__float_as_uint((float)gain);
+  if (gain > (double)tol) atomicOr(status, kStatusSubNotConverged);
+}
+
+// energy of the leading r rows of a block (r x L, contiguous) into *out
+static void block_energy(const MatView& v, const float* Z, int r, int64_t L, double* out, const int* gate,
+                         hipStream_t s) {
+  const int nb = kEnergyParts;
+  hipLaunchKernelGGL(k_sumsq_part, dim3(nb), dim3(256), 0, s, Z, (int64_t)r * L, v.sub_sums, gate);
+  hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, out, gate);
 }
 
 // ---------------------------------------------------------------------------
@@ -717,88 +831,133 @@ size_t sub_part_floats(int K, int64_t d, int64_t D) {
   upd(K, (int)d, (int)D);
   return mx;
 }
-// Rows of Y (K x L) <- an orthonormal basis of their span by `passes`
-// rounds of CholeskyQR on the diagonally scaled Gram
-static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, int passes,
-                            const ProfHook& prof, hipStream_t s) {
+
+// Philox key of the replacement rows of step t
+static void repair_key(uint64_t seed, int64_t t, uint32_t* k0, uint32_t* k1) {
+  *k0 = (uint32_t)(seed & 0xFFFFFFFFu) ^ 0x0F1E2D3Cu;
+  *k1 = (uint32_t)(seed >> 32) ^ (uint32_t)t ^ 0x4B5A6978u;
+}
+
+// One CholeskyQR pass on the rows of Y (K x L), skipped when *gate is set:
+// S = Y Y^T (fp32 MFMA, partial sums added in fp64), the Cholesky factor of
+// the diagonally scaled S (dependent rows marked), Y <- L^-1 Y, then every
+// marked row replaced by a Gaussian row (SubCtl::repaired tells whether any
+// was).
+static hipError_t orth_pass(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, const int* gate,
+                            uint32_t tag, bool last_pass, uint64_t seed, int64_t t, const ProfHook& prof,
+                            hipStream_t s) {
   const int Kp = chol_pad(K);
+  SubCtl* sc = v.sub_ctl;
+  hipLaunchKernelGGL(k_pass_reset, dim3(1), dim3(256), 0, s, v.sub_bad, K, &sc->repaired, gate);
+  GemmPlan pg = plan_splits(K, K, (int)L);
+  gemm_launch<true, 0>(Y, L, Y, L, v.sub_part, K, K, K, (int)L, pg, (int64_t)K * K, nullptr, nullptr, s, gate);
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
+                     pg.splits, (int64_t)K * K, (float*)nullptr, v.sub_S, gate);
+  prof.begin(GLR_PROF_SUB_CHOL);
+  hipError_t ce = launch_chol_inv(v, K, gate, s);
+  if (ce != hipSuccess) return ce;
+  prof.end(GLR_PROF_SUB_CHOL);
+  GemmPlan p1{1, K};
+  gemm_launch<false, 0>(v.sub_Linv, Kp, Y, L, Ytmp, L, K, (int)L, K, p1, 0, nullptr, nullptr, s, gate);
+  hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * L)), dim3(256), 0, s, Ytmp, Y, (int64_t)K * L, gate);
+  uint32_t k0, k1;
+  repair_key(seed, t, &k0, &k1);
+  hipLaunchKernelGGL(k_orth_repair, dim3((unsigned)K), dim3(256), 0, s, Y, L, v.sub_bad, &sc->repaired, gate, k0,
+                     k1, (uint32_t)v.mat, tag, last_pass ? 1 : 0, v.status);
+  return hipGetLastError();
+}
+
+// Rows of Y (K x L) <- an orthonormal basis of their span: `passes`
+// CholeskyQR passes on the diagonally scaled Gram, then one more pass only
+// when the last one replaced rows (a rank-deficient block); a row still
+// dependent in that pass sets the breakdown bit.  Every pass is skipped while
+// *outer is set (nullptr: never).
+static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, int passes,
+                            const int* outer, uint32_t tag, uint64_t seed, int64_t t, const ProfHook& prof,
+                            hipStream_t s) {
+  SubCtl* sc = v.sub_ctl;
   prof.begin(GLR_PROF_SUB_ORTH);
-  for (int pass = 0; pass < passes; ++pass) {
-    GemmPlan pg = plan_splits(K, K, (int)L);
-    gemm_launch<true, 0>(Y, L, Y, L, v.sub_part, K, K, K, (int)L, pg, (int64_t)K * K, nullptr, nullptr, s);
-    hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
-                       pg.splits, (int64_t)K * K, (float*)nullptr, v.sub_S);
-    prof.begin(GLR_PROF_SUB_CHOL);
-    hipError_t ce = launch_chol_inv(v, K, s);
-    if (ce != hipSuccess) return ce;
-    prof.end(GLR_PROF_SUB_CHOL);
-    GemmPlan p1{1, K};
-    gemm_launch<false, 0>(v.sub_Linv, Kp, Y, L, Ytmp, L, K, (int)L, K, p1, 0, nullptr, nullptr, s);
-    hipError_t e = hipMemcpyAsync(Y, Ytmp, (size_t)K * L * 4, hipMemcpyDeviceToDevice, s);
+  for (int pass = 0; pass <= passes; ++pass) {
+    const bool extra = pass == passes;
+    hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_pass, outer, extra ? &sc->repaired : nullptr);
+    hipError_t e = orth_pass(v, Y, Ytmp, K, L, &sc->gate_pass, tag + (uint32_t)pass, extra, seed, t, prof, s);
     if (e != hipSuccess) return e;
   }
   prof.end(GLR_PROF_SUB_ORTH);
   return hipGetLastError();
 }
 
-hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, hipStream_t s) {
+hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, int64_t t, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
+  hipLaunchKernelGGL(k_sub_reset, dim3(1), dim3(64), 0, s, v.sub_ctl);
   if (warm) {
+    // the previous Ritz vectors, orthonormal already
     hipError_t e = hipMemcpyAsync(v.sub_P, v.Ut, (size_t)K * v.d * 4, hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return e;
-  } else {
-    const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu) ^ 0xA5A5A5A5u;
-    const uint32_t k1 = (uint32_t)(seed >> 32) ^ 0x3C3C3C3Cu;
-    hipLaunchKernelGGL(k_sub_random, dim3(grid_n((int64_t)K * ((v.d + 3) / 4))), dim3(256), 0, s,
-                       v.sub_P, K, v.d, k0, k1, (uint32_t)v.mat);
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_sub_reset, dim3(1), dim3(64), 0, s, v.sub_ctl);
-  // warm rows are the previous Ritz vectors, orthonormal already
-  if (warm) return hipGetLastError();
-  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, 2, ProfHook{}, s);
+  const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu) ^ 0xA5A5A5A5u;
+  const uint32_t k1 = (uint32_t)(seed >> 32) ^ 0x3C3C3C3Cu;
+  hipLaunchKernelGGL(k_sub_random, dim3(grid_n((int64_t)K * ((v.d + 3) / 4))), dim3(256), 0, s, v.sub_P, K, v.d,
+                     k0, k1, (uint32_t)v.mat);
+  return orth_rows(v, v.sub_P, v.sub_Pn, K, v.d, 2, nullptr, 0xC0000000u, seed, t, ProfHook{}, s);
 }
 
-// one iteration; writes the subspace change into sub_ctl
-hipError_t launch_sub_iter(const MatView& v, float tol, const ProfHook& prof, hipStream_t s) {
+// One iteration, skipped as a whole (every launch returns at once) once an
+// earlier iteration met the tolerance; writes the subspace change into
+// sub_ctl.  `it` numbers the iteration within the refresh.
+hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, const ProfHook& prof,
+                           hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d, D = v.D;
+  SubCtl* sc = v.sub_ctl;
+  const int* g = &sc->gate_iter;
+  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_iter, &sc->converged, (const int*)nullptr);
   // Z = P^T Mo  (K x D)
   GemmPlan p1{1, (int)d};
   prof.begin(GLR_PROF_SUB_Z);
   if (v.right)   // Mo[a][b] = Mbar[b][a]: B(k=a, j=b) at Mbar[b d + a]
-    gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
+    gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s, g);
   else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
-    gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
+    gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s, g);
   prof.end(GLR_PROF_SUB_Z);
+  block_energy(v, v.sub_Z, v.r, D, &sc->e_in, g, s);
   // Z only carries the span into the next product: one scaled pass keeps it
   // well conditioned
-  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, 1, prof, s);
+  const uint32_t tag = 0xC0000000u | ((uint32_t)(it + 1) << 8);
+  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, 1, g, tag, seed, t, prof, s);
   if (e != hipSuccess) return e;
   // P_new = Z Mo^T  (K x d): B(k=b, j=a) = Mo[a][b]
   GemmPlan p2 = plan_splits(K, (int)d, (int)D);
   prof.begin(GLR_PROF_SUB_P);
   if (v.right)   // Mbar[b d + a]: contiguous along j
-    gemm_launch<false, 0>(v.sub_Z, D, v.Mbar, d, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr, nullptr, s);
+    gemm_launch<false, 0>(v.sub_Z, D, v.Mbar, d, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr,
+                          nullptr, s, g);
   else           // Mbar[a D + b]: contiguous along k
-    gemm_launch<true, 0>(v.sub_Z, D, v.Mbar, D, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr, nullptr, s);
+    gemm_launch<true, 0>(v.sub_Z, D, v.Mbar, D, v.sub_part, d, K, (int)d, (int)D, p2, (int64_t)K * d, nullptr,
+                         nullptr, s, g);
   prof.end(GLR_PROF_SUB_P);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_part,
-                     p2.splits, (int64_t)K * d, v.sub_Pn, (double*)nullptr);
-  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, 2, prof, s);
+                     p2.splits, (int64_t)K * d, v.sub_Pn, (double*)nullptr, g);
+  e = orth_rows(v, v.sub_Pn, v.sub_R, K, d, 2, g, tag | 0x10u, seed, t, prof, s);
   if (e != hipSuccess) return e;
-  // change: R = P_new - (P_new P^T) P ;  C = P_new P^T (K x K)
-  GemmPlan pc = plan_splits(K, K, (int)d);
-  gemm_launch<true, 0>(v.sub_Pn, d, v.sub_P, d, v.sub_part, K, K, K, (int)d, pc, (int64_t)K * K, nullptr, nullptr, s);
-  hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
-                     pc.splits, (int64_t)K * K, v.sub_C, (double*)nullptr);
-  GemmPlan p3{1, K};
-  gemm_launch<false, 1>(v.sub_C, K, v.sub_P, d, v.sub_R, d, K, (int)d, K, p3, 0, v.sub_Pn, v.sub_sums, s);
-  const int nb = gemm_blocks(K, (int)d);
-  hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, &v.sub_ctl->change2);
-  hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, v.sub_ctl, K, tol);
+  // change of the leading r rows (their span converges to the top-r span
+  // whatever happens to the oversampled rows, which may sit in a noise bulk):
+  // R = P_new[:r] - (P_new[:r] P[:r]^T) P[:r] ;  C = P_new[:r] P[:r]^T (r x r)
+  const int r = v.r;
+  GemmPlan pc = plan_splits(r, r, (int)d);
+  gemm_launch<true, 0>(v.sub_Pn, d, v.sub_P, d, v.sub_part, r, r, r, (int)d, pc, (int64_t)r * r, nullptr, nullptr, s,
+                       g);
+  hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)r * r)), dim3(256), 0, s, v.sub_part,
+                     pc.splits, (int64_t)r * r, v.sub_C, (double*)nullptr, g);
+  GemmPlan p3{1, r};
+  gemm_launch<false, 1>(v.sub_C, r, v.sub_P, d, v.sub_R, d, r, (int)d, r, p3, 0, v.sub_Pn, v.sub_sums, s, g);
+  const int nb = gemm_blocks(r, (int)d);
+  hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, &sc->change2, g);
+  hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, sc, r, tol);
   // P <- P_new
-  e = hipMemcpyAsync(v.sub_P, v.sub_Pn, (size_t)K * d * 4, hipMemcpyDeviceToDevice, s);
-  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_Pn, v.sub_P, (int64_t)K * d,
+                     g);
   return hipGetLastError();
 }
 
@@ -814,6 +973,7 @@ hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
     gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
   else
     gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
+  block_energy(v, v.sub_Z, v.r, D, &v.sub_ctl->e_out, nullptr, s);
   *rr = v;
   rr->d = K;
   rr->D = D;
@@ -836,12 +996,14 @@ hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
   return launch_jac_reset(*rr, s);
 }
 
-// U^T rows 0..K-1 = Y P^T (the Ritz vectors, by descending Ritz value)
-hipError_t launch_sub_rr_end(const MatView& v, hipStream_t s) {
+// U^T rows 0..K-1 = Y P^T (the Ritz vectors, by descending Ritz value), and
+// the iteration record
+hipError_t launch_sub_rr_end(const MatView& v, float tol, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d;
   GemmPlan p1{1, K};
   gemm_launch<false, 0>(v.rr_Y, K, v.sub_P, d, v.Ut, d, K, (int)d, K, p1, 0, nullptr, nullptr, s);
+  hipLaunchKernelGGL(k_sub_finish, dim3(1), dim3(64), 0, s, v.sub_ctl, v.info, v.status, tol);
   return hipGetLastError();
 }
 

@@ -1,8 +1,33 @@
 """Shared driver for the GPU parity tests: runs the HIP path (through the C
 ABI) and the CPU oracle side by side on identical seeded inputs and compares
 what is unique: projectors P P^T (never P itself: signs and rotations inside
-equal singular values are free), E^(i), X, the optimizer state, the
-selection J, and the singular values at refresh steps."""
+equal singular values are free), E^(i), E-bar, X, the optimizer state, the
+selection J, and the singular values at refresh steps.
+
+Hand-off mode (the default).  The columns of U inside a cluster of nearly
+equal singular values are fixed by the data only up to rotations inside the
+cluster, yet Approx-Top-r may select such columns.  So, after every refresh
+the oracle first checks the GPU's basis against its own fp64 one:
+  * orthonormality ||U U^T - I||_max <= 1e-5 (rows the refresh defines);
+  * the top singular values, |sigma_gpu - sigma| <= 1e-5 sigma_1;
+  * Eckart-Young: | ||Mbar - P P^T Mbar||^2 - sum_{k>r} sigma_k^2 | <=
+    1e-5 ||Mbar||^2 with the oracle's Mbar and sigma (holds at any gap);
+  * the top-r projector, rel(P P^T) <= 1e-4 when the relative eigengap
+    g = (sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 of the oracle's Mbar Mbar^T
+    is at least 1e-2; below that the projector moves by up to ~1/g times any
+    perturbation of Mbar Mbar^T (Davis-Kahan), so the bar is 1e-4 * (1e-2/g)
+    at that step only;
+and then continues from the GPU's basis.  At a selection step the oracle
+ranks its own fp64 scores on that basis; J must equal the GPU's unless the
+r-th and (r+1)-th scores are within 1e-4 relative (the margin rule), where
+the oracle takes the GPU's J.  Every step, whatever happened at the refresh,
+E^(i), E-bar, X and the optimizer state must be within 1e-4 relative
+(Frobenius), and X after T steps within 1e-3; nothing is carried over or
+widened from step to step.
+
+Strict mode (handoff=False): no adoption at all; every bar is the same 1e-4
+(and 1e-3 on X_T), so it only passes where every selected column is
+well separated from the unselected ones."""
 from __future__ import annotations
 
 import numpy as np
@@ -13,25 +38,11 @@ from synth import gradient_batch, planted_matrix
 # per-step and end-of-trajectory bars (relative Frobenius)
 STEP_TOL = 1e-4
 FINAL_TOL = 1e-3
-MARGIN = 1e-4   # selection margin below which either choice of J is correct
-# An individually selected singular vector u_j is fixed by fp32 data only up
-# to about eps32 * sigma_1 / min_k |sigma_j - sigma_k|; a step whose selected
-# columns sit that close to an unselected one gets the bar 64 eps32 / gap.
-EPS32 = 2.0 ** -24
-GAP_FACTOR = 64.0
-
-
-def selection_gap(sigma, jsel):
-    """min over j in J, k not in J of |sigma_j - sigma_k| / sigma_1."""
-    sigma = np.asarray(sigma, dtype=np.float64)
-    if sigma[0] <= 0:
-        return np.inf
-    mask = np.ones(len(sigma), dtype=bool)
-    mask[jsel] = False
-    if not mask.any():
-        return np.inf
-    rest = sigma[mask]
-    return float(min(np.abs(sigma[j] - rest).min() for j in jsel) / sigma[0])
+MARGIN = 1e-4        # selection margin below which either choice of J is correct
+ORTH_TOL = 1e-5
+SIGMA_TOL = 1e-5
+ENERGY_TOL = 1e-5
+GAP_FULL = 1e-2      # relative eigengap at r from which the projector bar is STEP_TOL
 
 
 def rel(a, b, floor=0.0):
@@ -50,8 +61,85 @@ def selection_margin(score, r):
     return (s[r - 1] - s[r]) / s[r - 1]
 
 
+def eigengap(sigma, r, sigma_next=None):
+    """(sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 (inf when r covers sigma);
+    sigma_next stands for sigma_{r+1} when sigma holds only the top r."""
+    s = np.asarray(sigma, dtype=np.float64)
+    if s[0] <= 0:
+        return np.inf
+    if r >= len(s):
+        if sigma_next is None:
+            return np.inf
+        return float((s[r - 1] ** 2 - sigma_next ** 2) / s[0] ** 2)
+    return float((s[r - 1] ** 2 - s[r] ** 2) / s[0] ** 2)
+
+
+def projector_bar(gap):
+    return STEP_TOL if gap >= GAP_FULL else STEP_TOL * GAP_FULL / max(gap, 1e-300)
+
+
+def refresh_rows(wl, d, r):
+    """Rows of U^T a refresh defines: the top block only when tau = 1 and the
+    library takes its subspace-iteration route (r < d, r <= 256)."""
+    return r if (wl.tau == 1 and r < d and r <= 256) else d
+
+
+class Handoff:
+    """The oracle's hand-off hooks (oracle.method.Oracle.step): check the
+    GPU's refresh and continue from its basis; take its J at margin-rule
+    steps only."""
+
+    def __init__(self, comp, wl, recs):
+        self.comp, self.wl, self.recs = comp, wl, recs
+
+    def basis(self, l, t, out):
+        m, n = self.wl.shapes[l]
+        d = min(m, n)
+        r = min(self.wl.rank, d)
+        rows = refresh_rows(self.wl, d, r)
+        rec = self.recs[l]
+        ut = self.comp.Ut(l).double().cpu().numpy()[:rows]
+        rec["orth"] = float(np.abs(ut @ ut.T - np.eye(rows)).max())
+        assert rec["orth"] < ORTH_TOL, (t, l, rec)
+        sig_o = out["sigma"]
+        sg = self.comp.sigma(l).double().cpu().numpy()
+        k = min(len(sig_o), rows, r + 4)
+        s1 = max(float(sig_o[0]), 1e-300)
+        rec["sigma"] = float(np.abs(sg[:k] - sig_o[:k]).max() / s1)
+        assert rec["sigma"] < SIGMA_TOL, (t, l, rec)
+        mbar = out["mbar"]
+        fro2 = float(np.sum(mbar * mbar))
+        pg = ut[:r].T
+        if fro2 > 0 and r < d:
+            tail = fro2 - float(np.sum((pg.T @ mbar) ** 2))
+            tail_o = fro2 - float(np.sum(np.asarray(sig_o[:r]) ** 2))
+            rec["energy"] = abs(tail - tail_o) / fro2
+            assert rec["energy"] < ENERGY_TOL, (t, l, rec)
+        po = out["U"][:, :r]
+        gap = eigengap(sig_o, r, out.get("sigma_next")) if r < d else np.inf
+        rec["gap"] = gap
+        rec["proj_bar"] = projector_bar(gap)
+        rec["proj"] = rel(pg @ pg.T, po @ po.T)
+        assert rec["proj"] < rec["proj_bar"], f"t={t} mat={l}: refresh projector rel {rec['proj']:.3e} ({rec})"
+        return ut.T
+
+    def selection(self, l, t, out, j_oracle):
+        m, n = self.wl.shapes[l]
+        d = min(m, n)
+        r = min(self.wl.rank, d)
+        rec = self.recs[l]
+        jg = np.sort(self.comp.J(l).cpu().numpy())
+        margin = selection_margin(out["score"], r)
+        rec["margin"] = margin
+        if margin < MARGIN:
+            rec["j_handoff"] = True
+            return jg
+        assert np.array_equal(jg, j_oracle), f"t={t} mat={l}: J {jg} != {j_oracle} (margin {margin:.2e})"
+        return j_oracle
+
+
 def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_start=False,
-               max_sweeps=30, tol=1e-6, check=None):
+               max_sweeps=30, tol=1e-6, check=None, handoff=True):
     """Runs both paths; returns a list of per-step dicts of relative errors.
     Raises AssertionError at the first step over the bars."""
     import torch
@@ -65,44 +153,45 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
     planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
     X = [torch.zeros(m, n, dtype=torch.float32, device="cuda") for (m, n) in wl.shapes]
     log = []
-    sig_last = [None] * len(wl.shapes)
-    carried = [STEP_TOL] * len(wl.shapes)
     for t in range(T):
         grads = [gradient_batch(wl, l, t, planted[l]) for l in range(len(wl.shapes))]
         G = [torch.from_numpy(g).cuda() for g in grads]
         comp.step(X, G, t)
         torch.cuda.synchronize()
-        res = orc.step(grads, t)
         st = comp.sync_status()
-        assert st in (0, 7), f"t={t}: device status {st}"
+        assert st == 0, f"t={t}: device status {glr.STATUS_NAMES.get(st, st)}"
+        recs = [{"t": t, "mat": l} for l in range(len(wl.shapes))]
+        res = orc.step(grads, t, handoff=Handoff(comp, wl, recs) if handoff else None)
         for l, o in enumerate(res):
             m, n = wl.shapes[l]
             d = min(m, n)
             r = min(wl.rank, d)
-            rec = {"t": t, "mat": l, "refresh": o["refresh"]}
-            if o["refresh"]:
-                sig_last[l] = o["sigma"]
-                step_tol = STEP_TOL
-            else:
-                gap = selection_gap(sig_last[l], o["J"]) if r < d else np.inf
-                rec["gap"] = gap
-                step_tol = max(STEP_TOL, GAP_FACTOR * EPS32 / gap)
-            carried[l] = max(carried[l], step_tol)
-            rec["tol"] = carried[l]
-            ut = comp.Ut(l).double().cpu().numpy()
+            rec = recs[l]
+            rec["refresh"] = o["refresh"]
             jg = comp.J(l).cpu().numpy()
+            rows = refresh_rows(wl, d, r)
+            ut = comp.Ut(l).double().cpu().numpy()[:rows]
             pg = ut[jg].T
             po = o["P"]
-            # the tau = 1 refresh defines only rows 0..r-1 of U^T (its top-r block)
-            uo = ut[:r] if (wl.tau == 1 and r < d) else ut
-            rec["orth"] = float(np.abs(uo @ uo.T - np.eye(uo.shape[0])).max())
-            assert rec["orth"] < 1e-5, (t, l, rec)
-            if not o["refresh"] and r < d:
-                margin = selection_margin(o["score"], r)
-                rec["margin"] = margin
-                assert margin >= MARGIN, f"t={t} mat={l}: selection margin {margin:.2e} is ambiguous"
-                assert np.array_equal(jg, o["J"]), f"t={t} mat={l}: J {jg} != {o['J']}"
-            rec["proj"] = rel(pg @ pg.T, po @ po.T)
+            if not handoff:
+                rec["orth"] = float(np.abs(ut @ ut.T - np.eye(rows)).max())
+                assert rec["orth"] < ORTH_TOL, (t, l, rec)
+                if o["refresh"]:
+                    sg = comp.sigma(l).double().cpu().numpy()
+                    k = min(len(o["sigma"]), rows, r + 4)
+                    rec["sigma"] = float(np.abs(sg[:k] - o["sigma"][:k]).max() / max(o["sigma"][0], 1e-300))
+                    assert rec["sigma"] < SIGMA_TOL, (t, l, rec)
+                elif r < d:
+                    rec["margin"] = selection_margin(o["score"], r)
+                    assert rec["margin"] >= MARGIN, f"t={t} mat={l}: selection margin {rec['margin']:.2e}"
+                    assert np.array_equal(np.sort(jg), o["J"]), f"t={t} mat={l}: J {jg} != {o['J']}"
+                rec["proj"] = rel(pg @ pg.T, po @ po.T)
+                assert rec["proj"] < STEP_TOL, f"t={t} mat={l}: proj rel {rec['proj']:.3e} ({rec})"
+            else:
+                # the oracle continued from the GPU's basis: the selected
+                # projectors coincide unless J differs
+                rec["proj_sel"] = rel(pg @ pg.T, po @ po.T)
+                assert rec["proj_sel"] < STEP_TOL, (t, l, rec)
             mi = np.abs(np.asarray(grads[l], dtype=np.float64)).max() + np.abs(o["E"]).max()
             e_o = oriented_to_mn(o["E"], m, n)
             e_g = comp.E(l).double().cpu().numpy()
@@ -113,21 +202,32 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
                 rec["S2"] = rel(comp.S2(l).double().cpu().numpy(), o["s2"])
             rec["Ebar"] = rel(comp.Ebar(l).double().cpu().numpy(), e_o.mean(axis=0),
                               floor=1e-3 * mi * np.sqrt(m * n))
-            if o["refresh"]:
-                sg = comp.sigma(l).double().cpu().numpy()
-                # the tau = 1 refresh returns Ritz values of its top-r block
-                k = r if (wl.tau == 1 and r < d) else min(d, r + 4)
-                rec["sigma"] = float(np.abs(sg[:k] - o["sigma"][:k]).max() / max(o["sigma"][0], 1e-300))
-                assert rec["sigma"] < 1e-5, (t, l, rec)
-            assert rec["proj"] < step_tol, f"t={t} mat={l}: proj rel {rec['proj']:.3e} ({rec})"
             for key in ("E", "X", "S1", "S2", "Ebar"):
                 if key in rec:
-                    assert rec[key] < carried[l], f"t={t} mat={l}: {key} rel {rec[key]:.3e} ({rec})"
+                    assert rec[key] < STEP_TOL, f"t={t} mat={l}: {key} rel {rec[key]:.3e} ({rec})"
             if check is not None:
                 check(comp, o, t, l, rec)
             log.append(rec)
     for l in range(len(wl.shapes)):
         final = rel(X[l].double().cpu().numpy(), orc.states[l].x)
-        bar = max(FINAL_TOL, 10 * carried[l])
-        assert final < bar, f"mat {l}: X after {T} steps rel {final:.3e} (bar {bar:.1e})"
+        log.append({"final_X": final, "mat": l})
+        assert final < FINAL_TOL, f"mat {l}: X after {T} steps rel {final:.3e} (bar {FINAL_TOL:.0e})"
+    summarize(wl.name, log)
     return log
+
+
+def summarize(name, log):
+    """Prints the largest value of every compared quantity (and the smallest
+    eigengap and selection margin, and how many J hand-offs took place)."""
+    keys = ("proj", "proj_sel", "E", "Ebar", "X", "S1", "S2", "orth", "sigma", "energy", "final_X")
+    out = {k: max(r[k] for r in log if k in r) for k in keys if any(k in r for r in log)}
+    gaps = [r["gap"] for r in log if "gap" in r and np.isfinite(r["gap"])]
+    if gaps:
+        out["min_gap"] = min(gaps)
+    margins = [r["margin"] for r in log if "margin" in r and np.isfinite(r["margin"])]
+    if margins:
+        out["min_margin"] = min(margins)
+    out["j_handoffs"] = sum(1 for r in log if r.get("j_handoff"))
+    print(f"[parity] {name} max " + " ".join(f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}"
+                                             for k, v in out.items()), flush=True)
+    return out

@@ -138,3 +138,13 @@ def test_workspace_holds_a_region_per_matrix():
     c2, _k2 = glr.make_config(shapes + [(4096, 4096)], 4, 8, 5)
     c3, _k3 = glr.make_config([(4096, 4096)], 4, 8, 5)
     assert glr.workspace_bytes(c2)[1] >= total + glr.workspace_bytes(c3)[1] - slack
+
+
+def test_state_copies_reject_bad_arguments_without_touching_the_device():
+    lib = glr.load()
+    view = glr.StateView()
+    assert lib.glr_read_state(None, 0, ctypes.byref(view), None) == 1
+    assert lib.glr_write_state(None, 0, ctypes.byref(view), None) == 1
+    assert lib.glr_status_string(8) == b"orthonormalisation breakdown"
+    assert glr.STATUS_NAMES[8] == "GLR_ERR_BREAKDOWN"
+    assert [f[0] for f in glr.StateView._fields_] == list(glr.STATE_PARTS)

@@ -1,16 +1,22 @@
 """GPU checks at the workloads' full shapes, in the launch configuration the
-benchmark times (same library, same kernels, the full N x m x n batches).
+benchmark times (same library, same kernels, the full N x m x n batches),
+over whole trajectories (T steps, or a stated prefix) in hand-off mode.
 
-The oracle cannot run a complete step at these sizes in a test's time, so:
+The oracle cannot run complete steps at these sizes in a test's time, so:
   * the streaming parts (error feedback, projection, residual, mean,
-    reconstruction, optimizer) are checked on sampled columns of the oriented
-    problem, which are independent of one another given P: the oracle's
-    formulas run in fp64 on the same fp32 inputs and the GPU's P;
-  * the refresh basis is checked against properties that hold at any size
-    (orthonormality, the eigen-residual of M-bar M-bar^T, descending sigma,
-    the trace and Eckart-Young identities) and, for the gapped 4096 x 4096
-    layer, against the top-r subspace of M-bar from an fp64 symmetric
-    eigensolver;
+    reconstruction, optimizer) run in the column-restricted oracle
+    (oracle.method.ColumnOracle) on sampled columns of the oriented problem,
+    which evolve independently given P: its own fp64 state from t = 0, fed
+    the GPU's P of every step once that P has passed the checks below, and
+    compared with the GPU's E, E-bar, X and optimizer state every step
+    (1e-4) and at the end (1e-3);
+  * the refresh basis is checked against the oracle's fp64 top-r route
+    (oracle.subspace.top_subspace on the step's Mbar: the GPU's previous E-bar
+    plus the workers' mean gradient, in fp64) for the projector (1e-4 where
+    the eigengap at r defines it) and the captured energy, and against
+    properties that hold at any size (orthonormality, the eigen-residual of
+    Mbar Mbar^T within the bound the Jacobi stopping rule gives, descending
+    sigma, the trace and Eckart-Young identities);
   * the Approx-Top-r scores are checked at sampled indices (every selected
     index, the runners-up and random others) against fp64 bilinear forms with
     the v_j of the Philox stream, and J against the fp64 ranking of them.
@@ -18,9 +24,11 @@ The oracle cannot run a complete step at these sizes in a test's time, so:
 import numpy as np
 import pytest
 
-from oracle.method import adam_update, argtop_r, msgd_update
+from oracle.method import ColumnOracle, argtop_r
 from oracle.philox import gaussian_vectors
+from oracle.subspace import next_singular_value, top_subspace
 from synth import get_workload, noise_level, planted_matrix
+from tests.parity import ENERGY_TOL, FINAL_TOL, eigengap, projector_bar, summarize
 
 pytestmark = pytest.mark.gpu
 
@@ -62,12 +70,14 @@ class Run:
             out.append(g.mul_(noise_level(self.wl, l)).add_(self.planted[l]))
         return out
 
-    def step(self, G):
+    def step(self, G, allow_unconverged=False):
         self.comp.step(self.X, G, self.t)
         self.torch.cuda.synchronize()
         st = self.comp.sync_status()
-        assert st in (0, 7), f"t={self.t}: device status {st}"
+        ok = (0, 7) if allow_unconverged else (0,)
+        assert st in ok, f"t={self.t}: device status {st}"
         self.t += 1
+        return st
 
 
 def _rel(a, b, floor=0.0):
@@ -75,51 +85,41 @@ def _rel(a, b, floor=0.0):
     return float(np.linalg.norm(a - b)) / den if den > 0 else float(np.linalg.norm(a))
 
 
-def check_columns(run, l, G, before, cols):
-    """The oracle's step on sampled columns of matrix l (fp64), given the
-    GPU's P, against the GPU's E, E-bar, X and optimizer state."""
-    wl, comp = run.wl, run.comp
-    m, n = wl.shapes[l]
-    right = m > n
-    P = comp.P(l).double().cpu().numpy()                       # d x r
-    Gc = _oriented(G[l], right)[:, :, cols].double().cpu().numpy()   # N x d x c
-    E0 = before["E"]                                            # N x d x c (fp64)
-    Mi = Gc + E0
-    Q = np.einsum("ar,iac->irc", P, Mi)
-    E1 = Mi - np.einsum("ar,irc->iac", P, Q)
-    ghat = P @ Q.mean(axis=0)
-    if wl.opt == "msgd":
-        x1, s1 = msgd_update(before["X"], before["S1"], ghat, wl.lr, wl.beta1)
-        s2 = None
-    else:
-        x1, s1, s2 = adam_update(before["X"], before["S1"], before["S2"], ghat, wl.lr, wl.beta1,
-                                 wl.beta2, wl.eps)
-    gE = _oriented(comp.E(l), right)[:, :, cols].double().cpu().numpy()
-    gEb = _oriented(comp.Ebar(l), right)[:, cols].double().cpu().numpy()
-    gX = _oriented(run.X[l], right)[:, cols].double().cpu().numpy()
-    gS1 = _oriented(comp.S1(l), right)[:, cols].double().cpu().numpy()
-    scale = float(np.linalg.norm(Mi)) / np.sqrt(Mi.shape[0])
-    rec = {"E": _rel(gE, E1, 1e-3 * scale * np.sqrt(Mi.shape[0])),
-           "Ebar": _rel(gEb, E1.mean(axis=0), 1e-3 * scale),
-           "X": _rel(gX, x1), "S1": _rel(gS1, s1)}
-    if s2 is not None:
-        gS2 = _oriented(comp.S2(l), right)[:, cols].double().cpu().numpy()
-        rec["S2"] = _rel(gS2, s2)
-    for k, v in rec.items():
-        assert v < STEP_TOL, f"t={run.t - 1} mat={l} columns {cols[:4]}...: {k} rel {v:.3e} ({rec})"
-    return rec
-
-
-def snapshot_columns(run, l, cols):
+def gpu_columns(run, l, cols):
+    """The GPU's state on the sampled oriented columns of matrix l, fp64."""
     comp, wl = run.comp, run.wl
     m, n = wl.shapes[l]
     right = m > n
-    snap = {"E": _oriented(comp.E(l), right)[:, :, cols].double().cpu().numpy(),
-            "X": _oriented(run.X[l], right)[:, cols].double().cpu().numpy(),
-            "S1": _oriented(comp.S1(l), right)[:, cols].double().cpu().numpy()}
+    out = {"E": _oriented(comp.E(l), right)[:, :, cols].double().cpu().numpy(),
+           "Ebar": _oriented(comp.Ebar(l), right)[:, cols].double().cpu().numpy(),
+           "X": _oriented(run.X[l], right)[:, cols].double().cpu().numpy(),
+           "S1": _oriented(comp.S1(l), right)[:, cols].double().cpu().numpy()}
     if wl.opt == "adam":
-        snap["S2"] = _oriented(comp.S2(l), right)[:, cols].double().cpu().numpy()
-    return snap
+        out["S2"] = _oriented(comp.S2(l), right)[:, cols].double().cpu().numpy()
+    return out
+
+
+def check_columns(run, l, G, col_oracle, cols, refresh):
+    """One step of the column-restricted oracle on the sampled columns, with
+    the GPU's P of this step (after the refresh / selection checks), against
+    the GPU's E, E-bar, X and optimizer state."""
+    wl, comp = run.wl, run.comp
+    m, n = wl.shapes[l]
+    right = m > n
+    P = comp.P(l).double().cpu().numpy()                             # d x r
+    Gc = _oriented(G[l], right)[:, :, cols].double().cpu().numpy()   # N x d x c
+    mi = Gc + col_oracle.e
+    o = col_oracle.step(Gc, P, refresh)
+    g = gpu_columns(run, l, cols)
+    scale = float(np.linalg.norm(mi)) / np.sqrt(mi.shape[0])
+    rec = {"E": _rel(g["E"], o["E"], 1e-3 * scale * np.sqrt(mi.shape[0])),
+           "Ebar": _rel(g["Ebar"], o["Ebar"], 1e-3 * scale),
+           "X": _rel(g["X"], o["X"]), "S1": _rel(g["S1"], o["S1"])}
+    if o["S2"] is not None:
+        rec["S2"] = _rel(g["S2"], o["S2"])
+    for k, v in rec.items():
+        assert v < STEP_TOL, f"t={run.t - 1} mat={l} columns {cols[:4]}...: {k} rel {v:.3e} ({rec})"
+    return rec
 
 
 def mbar64(run, l, G, ebar_prev):
@@ -130,7 +130,7 @@ def mbar64(run, l, G, ebar_prev):
     return _oriented(mb, m > n).contiguous()
 
 
-def check_refresh(run, l, mb, rows, tol=1e-6):
+def check_refresh(run, l, mb, rows, tol=1e-6, residual=True):
     """Basis properties at a refresh step; rows = how many rows of U^T are
     defined (d, or the top block of the tau = 1 refresh).
 
@@ -147,12 +147,16 @@ def check_refresh(run, l, mb, rows, tol=1e-6):
     assert orth < 1e-5, f"mat {l}: ||U U^T - I||_max = {orth:.3e}"
     assert bool((sig[1:] <= sig[:-1]).all()), f"mat {l}: sigma not descending"
     s1 = float(sig[0])
-    # eigen-residual of M-bar M-bar^T for every defined row
+    # eigen-residual of M-bar M-bar^T for every defined row (not for the Ritz
+    # vectors of a tau = 1 block whose eigengap at r is closed: no iteration
+    # converges there, and the refresh is judged by its energy)
     A = Ut @ mb                                   # rows x D
-    R = A @ mb.T - sig[:, None] ** 2 * Ut         # rows x d
-    res = float(R.norm(dim=1).max()) / max(s1 * s1, 1e-300)
-    res_tol = max(1e-5, tol * np.sqrt(mb.shape[0] - 1))
-    assert res < res_tol, f"mat {l}: eigen-residual {res:.3e} sigma_1^2 (bar {res_tol:.1e})"
+    res = None
+    if residual:
+        R = A @ mb.T - sig[:, None] ** 2 * Ut         # rows x d
+        res = float(R.norm(dim=1).max()) / max(s1 * s1, 1e-300)
+        res_tol = max(1e-5, tol * np.sqrt(mb.shape[0] - 1))
+        assert res < res_tol, f"mat {l}: eigen-residual {res:.3e} sigma_1^2 (bar {res_tol:.1e})"
     # sigma_j = ||u_j^T M-bar||
     sg = float((A.norm(dim=1) - sig).abs().max()) / max(s1, 1e-300)
     assert sg < 1e-5, f"mat {l}: sigma vs ||u_j^T Mbar|| {sg:.3e}"
@@ -164,6 +168,38 @@ def check_refresh(run, l, mb, rows, tol=1e-6):
     ey = abs(float(((P.T @ mb) ** 2).sum()) - float((sig[J[J < rows]] ** 2).sum())) / fro2
     assert ey < 1e-5, f"mat {l}: Eckart-Young identity {ey:.3e}"
     return {"orth": orth, "res": res, "sigma": sg}
+
+
+def check_projector(run, l, mb, prev, tol=1e-9, max_iters=80):
+    """The GPU's refresh projector against the oracle's fp64 top-r route on
+    the same Mbar (warm start from the oracle's own previous block, if any):
+    rel(P P^T) within the bar the eigengap at r allows, and the captured
+    energy within ENERGY_TOL of the oracle's.  Returns (record, oracle P)."""
+    wl, comp = run.wl, run.comp
+    m, n = wl.shapes[l]
+    d = min(m, n)
+    r = min(wl.rank, d)
+    a = mb.cpu().numpy()
+    if r > d // 2:
+        # most of the basis: an fp64 library eigensolver of Mbar Mbar^T (the
+        # Rayleigh-Ritz Jacobi of the oracle's route on r x r would take minutes)
+        w, V = np.linalg.eigh(a @ a.T)
+        w, V = w[::-1], V[:, ::-1]
+        po, iters, conv = V[:, :r], 0, True
+        sig = np.sqrt(np.maximum(w[:r], 0.0))
+        sn = float(np.sqrt(max(w[r], 0.0)))
+    else:
+        po, sig, iters, conv = top_subspace(a, r, seed=l, tol=tol, max_iters=max_iters, start=prev)
+        sn = next_singular_value(a, po)
+    gap = eigengap(sig, r, sn)
+    pg = comp.P(l).double().cpu().numpy()
+    fro2 = float(np.sum(a * a))
+    rec = {"gap": gap, "oracle_iters": iters, "oracle_conv": conv,
+           "proj": _rel(pg @ pg.T, po @ po.T), "proj_bar": projector_bar(gap),
+           "energy": abs(float(np.sum((pg.T @ a) ** 2)) - float(np.sum(sig ** 2))) / fro2}
+    assert rec["proj"] < rec["proj_bar"], f"mat {l}: refresh projector vs the oracle {rec}"
+    assert rec["energy"] < ENERGY_TOL, f"mat {l}: captured energy vs the oracle {rec}"
+    return rec, po
 
 
 def check_selection(run, l, mb, t, rng, extra=48):
@@ -209,88 +245,115 @@ def check_selection(run, l, mb, t, rng, extra=48):
     return {}
 
 
-def run_fullsize(glr, name, steps, sample_cols=6, seed=7, ref_top=False):
+def run_fullsize(glr, name, steps, sample_cols=8, seed=7, ref_steps=None, max_mats=8,
+                 unconverged_from=None):
+    """A trajectory of `steps` steps of workload `name` in hand-off mode (see
+    the module docstring).  ref_steps: refresh steps whose projector is
+    compared with the oracle's top-r route (None: every refresh).
+    unconverged_from: from this step on a refresh may report
+    GLR_ERR_NOT_CONVERGED (a closed eigengap at r, where no iteration
+    converges)."""
     import torch
     wl = get_workload(name)
     _say(name, "shapes", list(wl.shapes)[:3], "N", wl.workers, "r", wl.rank, "tau", wl.tau, "steps", steps)
     run = Run(glr, wl)
     rng = np.random.default_rng(seed)
     mats = list(range(len(wl.shapes)))
-    if len(mats) > 6:      # many small matrices: every refresh, a sample of the rest
-        mats = sorted(set(rng.choice(mats, size=6, replace=False).tolist()) | {0, len(mats) - 1})
+    if len(mats) > max_mats:      # many small matrices: the largest, the first, the last and a sample
+        big = max(mats, key=lambda i: wl.shapes[i][0] * wl.shapes[i][1])
+        mats = sorted(set(rng.choice(mats, size=max_mats - 3, replace=False).tolist()) | {0, len(mats) - 1, big})
+    cols, colo, prev = {}, {}, {}
+    for l in mats:
+        m, n = wl.shapes[l]
+        D = max(m, n)
+        c = np.unique(np.concatenate([rng.choice(D, size=min(sample_cols, D), replace=False), [D - 1]]))
+        cols[l] = torch.from_numpy(c).cuda()
+        colo[l] = ColumnOracle(wl.shapes[l], c, wl.workers, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                               beta2=wl.beta2, eps=wl.eps)
+        prev[l] = None
+    log = []
     for t in range(steps):
         G = run.batch()
         refresh = t % wl.tau == 0
-        cols, before, ebar = {}, {}, {}
-        for l in mats:
-            m, n = wl.shapes[l]
-            D = max(m, n)
-            c = np.unique(np.concatenate([rng.choice(D, size=min(sample_cols, D), replace=False), [D - 1]]))
-            cols[l] = torch.from_numpy(c).cuda()
-            before[l] = snapshot_columns(run, l, cols[l])
-            ebar[l] = run.comp.Ebar(l).double().clone()
-        run.step(G)
+        ebar = {l: run.comp.Ebar(l).double().clone() for l in mats}
+        st = run.step(G, allow_unconverged=unconverged_from is not None and t >= unconverged_from)
         for l in mats:
             m, n = wl.shapes[l]
             d = min(m, n)
             r = min(wl.rank, d)
             mb = mbar64(run, l, G, ebar[l])
-            rec = {"t": t, "mat": l}
+            rec = {"t": t, "mat": l, "status": st}
             if refresh and r < d:
                 sub = wl.tau == 1 and r <= 256
-                rec.update(check_refresh(run, l, mb, r if sub else d))
-                if ref_top:
-                    G64 = (mb @ mb.T).cpu().numpy()
-                    w, V = np.linalg.eigh(G64)
-                    Po = V[:, ::-1][:, :r]
-                    Pg = run.comp.P(l).double().cpu().numpy()
-                    rec["proj"] = _rel(Pg @ Pg.T, Po @ Po.T)
-                    gap = (w[::-1][r - 1] - w[::-1][r]) / w[-1]
-                    rec["gap_sigma2"] = float(gap)
-                    assert rec["proj"] < STEP_TOL, f"mat {l}: projector vs fp64 top-r {rec['proj']:.3e}"
+                closed = unconverged_from is not None and t >= unconverged_from
+                rec.update(check_refresh(run, l, mb, r if sub else d, residual=not closed))
+                if ref_steps is None or t in ref_steps:
+                    pr, prev[l] = check_projector(run, l, mb, prev[l])
+                    rec.update(pr)
             elif r < d:
                 rec.update(check_selection(run, l, mb, t, rng))
-            rec.update(check_columns(run, l, G, before[l], cols[l]))
+            rec.update(check_columns(run, l, G, colo[l], cols[l], refresh))
             _say(rec)
+            log.append(rec)
             del mb
         del G
+    for l in mats:
+        g = gpu_columns(run, l, cols[l])
+        final = _rel(g["X"], colo[l].x)
+        log.append({"final_X": final, "mat": l})
+        assert final < FINAL_TOL, f"mat {l}: X after {steps} steps rel {final:.3e}"
+    summarize(name, [r for r in log])
     return run
 
 
-@pytest.mark.parametrize("name,steps,ref", [
-    ("layer_4096", 2, False),
-    ("layer_4096_gap", 2, True),
-])
-def test_layer_4096(gpu_lib, name, steps, ref):
-    run_fullsize(gpu_lib, name, steps, ref_top=ref)
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,steps", [("layer_4096", 12), ("layer_4096_gap", 50)])
+def test_layer_4096(gpu_lib, name, steps):
+    # the gapped layer: all T = 50 steps (five refreshes, each against the
+    # oracle's top-r route); the layer as written has no gap at r = 64 (the
+    # noise bulk covers it): its first refresh period and the next refresh,
+    # basis properties only
+    run_fullsize(gpu_lib, name, steps, ref_steps=None if name.endswith("gap") else ())
 
 
 @pytest.mark.parametrize("name", ["seats256_right", "seats64_left"])
 def test_four_block_groups_with_padding_and_ragged_blocks(gpu_lib, name):
     # groups of four off the 4096 shape: padding seats (and groups with no
     # block), a ragged last block, both orientations; a cold and a warm refresh
-    run_fullsize(gpu_lib, name, 3, ref_top=True)
+    run_fullsize(gpu_lib, name, 3)
 
 
 def test_largest_full_basis_refresh(gpu_lib):
     # d = 8192, the largest min(m, n) the library takes: a cold and a warm
     # complete basis (pairs tournament, 511 rounds a sweep) and a selection
-    # step over 8192 scores, checked by the size-independent properties
+    # step over 8192 scores
     run_fullsize(gpu_lib, "max_8192", 3, sample_cols=4)
 
 
 def test_largest_rank(gpu_lib):
     # r = 1024 (the largest rank the library takes) of d = 1100
-    run_fullsize(gpu_lib, "max_rank", 3, ref_top=True)
+    run_fullsize(gpu_lib, "max_rank", 3)
 
 
+@pytest.mark.timeout(900)
 def test_transformer_block(gpu_lib):
-    run_fullsize(gpu_lib, "block_4096_gap", 2)
+    # all T = 20 steps, both refreshes of all seven matrices against the oracle
+    run_fullsize(gpu_lib, "block_4096_gap", 20)
 
 
+@pytest.mark.timeout(600)
 def test_conv_50(gpu_lib):
-    run_fullsize(gpu_lib, "conv_50_gap", 2)
+    # all T = 100 steps, five refreshes; eight of the fifty matrices checked
+    # (the largest, the first, the last and a seeded sample)
+    run_fullsize(gpu_lib, "conv_50_gap", 100)
 
 
+@pytest.mark.timeout(900)
 def test_large_tau1(gpu_lib):
-    run_fullsize(gpu_lib, "large_8192x28672", 2, sample_cols=4)
+    # all T = 10 steps (every one a refresh); the projector against the
+    # oracle's route at t = 0 and 1, where the gap at r = 256 is open (3 and
+    # about 1.5); from t = 2 the error feedback lifts the plateau directions
+    # (sigma 1/3 each step) to the r-th value, the gap closes and neither the
+    # block iteration nor the oracle's converges there: those refreshes are
+    # checked by their basis properties, and the trajectory by the columns
+    run_fullsize(gpu_lib, "large_8192x28672", 10, sample_cols=4, ref_steps=(0, 1), unconverged_from=2)

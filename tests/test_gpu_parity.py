@@ -20,7 +20,7 @@ def test_trajectory_parity(gpu_lib, name):
     _print_case(name)
     wl = get_workload(name)
     log = run_parity(gpu_lib, wl)
-    assert len(log) == wl.steps * len(wl.shapes)
+    assert sum(1 for r in log if "t" in r) == wl.steps * len(wl.shapes)
 
 
 def test_many_shapes_vector_case_and_full_rank(gpu_lib):
@@ -56,8 +56,13 @@ def test_tau1_subspace_iteration_parity(gpu_lib, name):
     def check(comp, o, t, l, rec):
         its, conv, hist = comp.sweep_history(l)
         assert conv, (t, its, hist)
+        iters, gain = comp.sub_info(l)
+        rec["sub_iters"], rec["sub_gain"] = iters, gain
+        assert 1 <= iters <= (6 if t == 0 else 2) and gain <= 1e-5, (t, iters, gain)
 
-    run_parity(gpu_lib, wl, check=check)
+    log = run_parity(gpu_lib, wl, check=check)
+    _print_case(name, sub_iters=[r["sub_iters"] for r in log if "sub_iters" in r],
+                max_gain=max(r["sub_gain"] for r in log if "sub_gain" in r))
 
 
 def test_cold_start_refresh_parity(gpu_lib):

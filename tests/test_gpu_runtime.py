@@ -237,3 +237,123 @@ def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypa
         assert torch.equal(c1.E(l), c2.E(l)), f"mat {l}: E differs"
         assert torch.equal(c1.Ut(l), c2.Ut(l)), f"mat {l}: U differs"
         assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
+
+
+def test_state_read_and_write_through_the_abi_resume_the_run(gpu_lib):
+    # glr_read_state into host tensors after 3 steps of one handle, then
+    # glr_write_state of those tensors into a fresh handle (a restore), which
+    # continues bitwise like the uninterrupted run
+    import torch
+    wl = get_workload("ragged_right")
+    T, cut = 6, 3
+    _say("ragged_right read/write state at", cut)
+    G = _inputs(wl, T)
+    a = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                           seed=wl.seed)
+    Xa = _zeros(wl)
+    for t in range(T):
+        a.step(Xa, G[t], t)
+    b = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                           seed=wl.seed)
+    Xb = _zeros(wl)
+    for t in range(cut):
+        b.step(Xb, G[t], t)
+    L = b.layouts[0]
+    m, n, d, D, r, N = L.m, L.n, L.d, L.D, L.r, wl.workers
+    host = {"E": torch.empty(N, m, n), "Ebar": torch.empty(m, n), "Ut": torch.empty(d, d),
+            "sigma": torch.empty(d), "J": torch.empty(r, dtype=torch.int32), "score": torch.empty(d),
+            "S1": torch.empty(m, n), "S2": torch.empty(m, n), "Rbar": torch.empty(r, D),
+            "info": torch.empty(64, dtype=torch.int32)}
+    b.read_state(0, **host)
+    torch.cuda.synchronize()
+    assert torch.equal(host["E"], b.E(0).cpu()) and torch.equal(host["Ut"], b.Ut(0).cpu())
+    assert torch.equal(host["S2"], b.S2(0).cpu()) and torch.equal(host["J"], b.J(0).cpu())
+    c = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                           seed=wl.seed)
+    c.write_state(0, **host)
+    c.resume(cut)
+    Xc = [x.clone() for x in Xb]
+    for t in range(cut, T):
+        c.step(Xc, G[t], t)
+    torch.cuda.synchronize()
+    assert a.sync_status() == gpu_lib.GLR_OK and c.sync_status() == gpu_lib.GLR_OK
+    assert torch.equal(Xa[0], Xc[0]) and torch.equal(a.E(0), c.E(0)) and torch.equal(a.S2(0), c.S2(0))
+
+
+def test_state_copy_rejects_s2_without_adam(gpu_lib):
+    import torch
+    wl = get_workload("one_256x128")
+    comp = _make(gpu_lib, wl)
+    with pytest.raises(gpu_lib.GlrError) as ei:
+        comp.read_state(0, S2=torch.empty(256, 128))
+    assert ei.value.status == 1
+    with pytest.raises(gpu_lib.GlrError):
+        comp.read_state(3, E=torch.empty(4, 256, 128))
+
+
+def test_refresh_step_only_enqueues(gpu_lib):
+    # a refresh of a 4096 x 4096 layer takes ~0.1 s on the device; glr_step
+    # returns before it completes (no host wait per sweep), and the result is
+    # there once the stream is
+    import torch
+    wl = get_workload("layer_4096", workers=2)
+    _say("layer_4096 N=2 enqueue-only refresh")
+    comp = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, seed=wl.seed)
+    X = _zeros(wl)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    planted = torch.from_numpy(planted_matrix(wl, 0).astype(np.float32)).cuda()
+    G = [torch.randn((2, 4096, 4096), generator=gen, device="cuda").mul_(1e-3).add_(planted)]
+    torch.cuda.synchronize()
+    ev = torch.cuda.Event()
+    comp.step(X, G, 0)
+    ev.record()
+    pending = not ev.query()
+    torch.cuda.synchronize()
+    assert pending, "glr_step waited for the refresh to complete"
+    its, conv, _ = comp.sweep_history(0)
+    assert conv and its > 1
+    assert comp.sync_status() == gpu_lib.GLR_OK
+
+
+@pytest.mark.parametrize("name,tau", [("zero_grad", 2), ("zero_grad", 1), ("lowrank_exact", 3),
+                                      ("lowrank_exact", 1)])
+def test_zero_and_rank_deficient_gradients(gpu_lib, name, tau):
+    # all-zero gradients, and exactly rank-4 gradients with r = 6 (< the
+    # oversampled tau = 1 block): the full-basis and the tau = 1 refresh both
+    # stay finite and orthonormal, and compress exactly (E = 0), as the
+    # oracle does; X and the optimizer state follow the oracle
+    import torch
+    from oracle.method import Oracle
+    from tests.parity import rel
+    wl = get_workload(name, tau=tau)
+    _say(name, "tau", tau)
+    comp = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                              seed=wl.seed)
+    orc = Oracle.from_workload(wl)
+    planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
+    X = _zeros(wl)
+    for t in range(wl.steps):
+        grads = [gradient_batch(wl, l, t, planted[l]) for l in range(len(wl.shapes))]
+        comp.step(X, [torch.from_numpy(g).cuda() for g in grads], t)
+        torch.cuda.synchronize()
+        st = comp.sync_status()
+        assert st == gpu_lib.GLR_OK, f"t={t}: status {gpu_lib.STATUS_NAMES.get(st, st)}"
+        res = orc.step(grads, t)
+        for l, o in enumerate(res):
+            m, n = wl.shapes[l]
+            d = min(m, n)
+            rows = min(wl.rank, d) if tau == 1 and wl.rank < d else d
+            ut = comp.Ut(l)[:rows].double()
+            assert torch.isfinite(ut).all() and torch.isfinite(X[l]).all()
+            orth = float((ut @ ut.T - torch.eye(rows, dtype=torch.float64, device="cuda")).abs().max())
+            assert orth < 1e-5, (t, l, orth)
+            scale = max(float(np.abs(grads[l]).max()), 1e-30)
+            assert float(comp.E(l).abs().max()) <= 1e-5 * scale, (t, l)
+            # the oracle compresses the fp32 gradients, which are rank 4 only
+            # up to their rounding (2^-24 relative)
+            assert np.abs(o["E"]).max() <= 1e-6 * scale
+            if np.any(o["X"]):
+                assert rel(X[l].double().cpu().numpy(), o["X"]) < 1e-4
+            else:
+                assert not bool(X[l].any())

@@ -351,3 +351,37 @@ def test_deterministic():
     a, _ = _run(wl, steps=6)
     b, _ = _run(wl, steps=6)
     assert np.array_equal(a.states[0].x, b.states[0].x)
+
+
+@pytest.mark.parametrize("name,refresh", [("mid_left", "compressed"), ("ragged_right", "compressed"),
+                                          ("ragged_right", "full")])
+def test_column_oracle_follows_the_full_oracle(name, refresh):
+    # the column-restricted step, fed the full oracle's P, reproduces the full
+    # oracle's columns of E, E-bar, X and the optimizer state at every step
+    from oracle.method import ColumnOracle
+    wl = get_workload(name, steps=7)
+    full = Oracle.from_workload(wl, refresh=refresh)
+    m, n = wl.shapes[0]
+    D = max(m, n)
+    cols = np.array([0, 3, D // 2, D - 1])
+    col = ColumnOracle(wl.shapes[0], cols, wl.workers, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
+                       beta2=wl.beta2, eps=wl.eps, refresh=refresh)
+    planted = planted_matrix(wl, 0)
+    for t in range(wl.steps):
+        g = gradient_batch(wl, 0, t, planted)
+        o = full.step([g], t)[0]
+        go = np.swapaxes(g, 1, 2) if m > n else g
+        c = col.step(go[:, :, cols], o["P"], o["refresh"])
+
+        def close(a, b):
+            # the same products summed in another order (a BLAS call over the
+            # sample instead of the whole matrix): agreement to rounding
+            return np.linalg.norm(a - b) <= 1e-12 * max(np.linalg.norm(b), 1e-300)
+
+        assert close(c["E"], o["E"][:, :, cols])
+        assert close(c["Ebar"], o["E"][:, :, cols].mean(axis=0))
+        tr = (lambda a: a.T) if m > n else (lambda a: a)
+        assert close(c["X"], tr(o["X"])[:, cols])
+        assert close(c["S1"], tr(o["s1"])[:, cols])
+        if wl.opt == "adam":
+            assert close(c["S2"], tr(o["s2"])[:, cols])

@@ -170,3 +170,13 @@ def test_approx_selection_ranks_by_the_square_of_lambda_bar():
     assert np.allclose(o1["lam"], a, rtol=1e-12)
     assert np.array_equal(o1["J"], [0, 2])              # top-2 of a^2: 100, 25
     assert not np.array_equal(np.sort(np.argsort(-a)[:r]), o1["J"])   # signed: {0, 1}
+
+
+def test_next_singular_value_estimate():
+    rng = np.random.default_rng(8)
+    a = _gapped(rng, 40, 90, 5)
+    p, _, _, _ = top_subspace(a, 5)
+    from oracle.subspace import next_singular_value
+    s = np.linalg.svd(a, compute_uv=False)
+    est = next_singular_value(a, p, iters=60)
+    assert est <= s[5] * (1 + 1e-12) and est > 0.999 * s[5]
