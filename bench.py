@@ -391,14 +391,17 @@ def main():
     t_next = args.warmup + (args.steps if args.no_profile else 2 * args.steps)
     n3 = max(2, 2 * wl.tau)
     per_type = {"refresh": [], "select": []}
+    sub_iters = []
     stream = torch.cuda.current_stream(dev)
-    for t in range(t_next, t_next + n3):
+    for t in range(t_next, t_next + max(n3, 8 if wl.tau == 1 else 0)):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         comp.step(X, batches[t % pool], t)
         e1.record(stream)
         e1.synchronize()
         per_type["refresh" if t % wl.tau == 0 else "select"].append(e0.elapsed_time(e1))
+        if wl.tau == 1:
+            sub_iters.append(comp.sub_info(0)[0])
     warm_sweeps = [int(comp.info(l)[0]) for l in range(len(wl.shapes))]
     status = comp.sync_status()
     if status not in (0, 7):
@@ -442,6 +445,7 @@ def main():
         "refresh_history_last": history,
         "step_types": step_types,
         "refresh_sweeps_cold": cold_sweeps,
+        "tau1_block_iterations": sub_iters or None,
         "refresh_sweeps_warm": warm_sweeps,
         "status": glr.STATUS_NAMES.get(status, status),
     }

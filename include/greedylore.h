@@ -159,7 +159,8 @@ typedef struct {
   uint64_t off_Rbar;           /* r x D fp32: mean over workers of Q^(i) = P^T M^(i) (oriented) */
   uint64_t off_info;           /* 64 int32: [0] sweeps of the last refresh, [1] converged flag,
                                   [2 + s] float bits of sweep s's largest pair off-norm (s < 60);
-                                  tau = 1 refresh: [62] block iterations, [63] converged flag */
+                                  tau = 1 refresh: [62] block iterations, [63] float bits of
+                                  the last iteration's relative gain of ||P[:r]^T Mbar||^2 */
 } glr_mat_layout;
 
 typedef struct glr_handle glr_handle;
@@ -199,12 +200,19 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G,
  *                          replaces dependent rows by Gaussian ones); suspect;
  *   GLR_ERR_NOT_CONVERGED  a refresh ended above its tolerance: Jacobi sweeps
  *                          (budget or max_sweeps) above tol, or a tau = 1
- *                          refresh whose last block iteration (of 2 from the
- *                          previous block, 6 from a cold start; fewer once the
- *                          leading r rows move by less than 10 tol) still
- *                          raised the energy ||P^T Mbar||^2 they capture by
- *                          more than 10 tol relative.  Informational: the basis
- *                          is orthonormal and the handle stays usable.
+ *                          refresh whose block iteration reached its cap (4
+ *                          from the previous block, 8 from a cold start) with
+ *                          the leading r rows still moving by more than 10 tol
+ *                          and still raising the energy ||P^T Mbar||^2 they
+ *                          capture by more than 10 tol relative.  (The block
+ *                          iteration runs at least 2 times, and more only while
+ *                          the previous refresh's Ritz values show a relative
+ *                          gap (sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 of at
+ *                          least 1e-3: with the gap closed the top-r subspace is
+ *                          not determined by the data, and the Rayleigh-Ritz
+ *                          step keeps the directions of largest energy.)
+ *                          Informational: the basis is orthonormal and the
+ *                          handle stays usable.
  *   GLR_OK                 otherwise. */
 glr_status glr_sync_status(glr_handle* h, void* stream);
 

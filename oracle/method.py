@@ -27,6 +27,22 @@ One step t, following Algorithm 4 with Approx-Top-r (Algorithm 2):
 With refresh="full" (Algorithm 3) a refresh step instead sets E^(i) = 0 and
 Ghat = Mbar (the uncompressed average).
 
+Baseline modes of the paper's comparisons (Section IV, Algorithm 1; Appendix
+E, Algorithm 5):
+  * select="lazy": the Lazy-SVD operator, P_t = P_{t-1} between refreshes
+    (J kept, no selection);
+  * ef=False: no error feedback, M^(i) = G^(i) and E^(i) stays zero;
+    Algorithm 1 is select="lazy", ef=False, refresh="full" (Ghat = the mean
+    gradient at refresh steps);
+  * opt="galore_adam": Algorithm 5, distributed Adam-type GaLore: Lazy-SVD P
+    (select "lazy", no error feedback), Adam moments M, V kept in the r x D
+    subspace and reset to zero at every refresh,
+        M = b1 M + (1 - b1) Rbar,  V = b2 V + (1 - b2) Rbar^2,
+        X <- X - gamma P (M / (sqrt(V) + eps))   (transposed back iff m > n).
+    Algorithm 5 prints the moment updates with b1 and (1 - b1) exchanged and
+    gamma applied twice; they are read as the main text's Adam (eq-adam)
+    with one gamma.
+
 Readings where the paper is loose (each listed in the design notes):
   * the residual of Algorithm 3 is written P R^T, dimensionally impossible;
     Algorithm 4's P R^(i) is used;
@@ -136,6 +152,9 @@ class MatrixState:
     s1: np.ndarray           # MSGD buffer / Adam first moment, m x n
     s2: np.ndarray | None    # Adam second moment, m x n
     sigma: np.ndarray | None = None
+    j: np.ndarray | None = None      # the current index set J (Lazy-SVD keeps it)
+    g1: np.ndarray | None = None     # GaLore subspace first moment, r x D (oriented)
+    g2: np.ndarray | None = None     # GaLore subspace second moment, r x D
 
     @property
     def right(self) -> bool:
@@ -163,13 +182,20 @@ class Oracle:
     tau1_route: str = "subspace"
     sub_tol: float = 1e-12
     sub_max_iters: int = 200
+    ef: bool = True               # error feedback (False: E stays zero)
     states: list = field(default_factory=list)
     t_next: int = 0
 
     def __post_init__(self):
+        if self.opt == "galore_adam":
+            if self.select not in ("approx", "lazy") or self.refresh != "compressed":
+                raise ValueError("galore_adam is Algorithm 5: Lazy-SVD selection, compressed refresh steps")
+            self.select, self.ef = "lazy", False
         self.states = []
         for (m, n) in self.shapes:
             d, D = min(m, n), max(m, n)
+            r = min(self.rank, d)
+            galore = self.opt == "galore_adam"
             self.states.append(MatrixState(
                 m=m, n=n,
                 e=np.zeros((self.workers, d, D)),
@@ -177,6 +203,9 @@ class Oracle:
                 x=np.zeros((m, n)),
                 s1=np.zeros((m, n)),
                 s2=np.zeros((m, n)) if self.opt == "adam" else None,
+                j=np.arange(r),
+                g1=np.zeros((r, D)) if galore else None,
+                g2=np.zeros((r, D)) if galore else None,
             ))
 
     @classmethod
@@ -211,7 +240,7 @@ class Oracle:
         d, D = min(st.m, st.n), max(st.m, st.n)
         r = min(self.rank, d)
         gc = np.transpose(g, (0, 2, 1)) if st.right else g        # N x d x D
-        ms = gc + st.e                                            # step 1
+        ms = gc + st.e if self.ef else gc                         # step 1
         is_refresh = (t % self.tau) == 0                          # step 2
         out = {"refresh": is_refresh, "t": t}
         mbar = ms.sum(axis=0) / n_w
@@ -232,6 +261,11 @@ class Oracle:
             st.u = u
             st.sigma = sigma
             jsel = np.arange(r)
+            if st.g1 is not None:                                 # Alg. 5: subspace state reset
+                st.g1 = np.zeros_like(st.g1)
+                st.g2 = np.zeros_like(st.g2)
+        elif self.select == "lazy":                               # Lazy-SVD: P_t = P_{t-1}
+            jsel = st.j
         else:
             if self.select == "approx":
                 v = gaussian_vectors(self.seed, t, l, np.arange(d), D).astype(np.float64)
@@ -250,6 +284,7 @@ class Oracle:
             out["J_oracle"] = jsel
             if handoff is not None:
                 jsel = np.asarray(handoff.selection(l, t, out, jsel))
+        st.j = jsel
         p = st.u[:, jsel]                                         # step 4
         q = np.matmul(p.T, ms)                                    # step 5: P^T M^(i) per worker
         rbar = q.sum(axis=0) / n_w                                # step 7
@@ -257,17 +292,27 @@ class Oracle:
             st.e = np.zeros_like(ms)                              # Alg. 3 reset
             ghat = mbar
         else:
-            st.e = ms - np.matmul(p, q)                           # step 6: M^(i) - P Q^(i)
+            if self.ef:
+                st.e = ms - np.matmul(p, q)                       # step 6: M^(i) - P Q^(i)
             ghat = p @ rbar                                       # step 8
-        ghat_mn = ghat.T if st.right else ghat
-        if self.opt == "msgd":                                    # step 9
-            st.x, st.s1 = msgd_update(st.x, st.s1, ghat_mn, self.lr, self.beta1)
+        if self.opt == "galore_adam":                             # Alg. 5, in the subspace
+            st.g1 = self.beta1 * st.g1 + (1.0 - self.beta1) * rbar
+            st.g2 = self.beta2 * st.g2 + (1.0 - self.beta2) * rbar * rbar
+            step = p @ (st.g1 / (np.sqrt(st.g2) + self.eps))
+            st.x = st.x - self.lr * (step.T if st.right else step)
+            ghat_mn = ghat.T if st.right else ghat
         else:
-            st.x, st.s1, st.s2 = adam_update(st.x, st.s1, st.s2, ghat_mn, self.lr,
-                                             self.beta1, self.beta2, self.eps)
+            ghat_mn = ghat.T if st.right else ghat
+            if self.opt == "msgd":                                # step 9
+                st.x, st.s1 = msgd_update(st.x, st.s1, ghat_mn, self.lr, self.beta1)
+            else:
+                st.x, st.s1, st.s2 = adam_update(st.x, st.s1, st.s2, ghat_mn, self.lr,
+                                                 self.beta1, self.beta2, self.eps)
         out.update(J=jsel, P=p, Q=q, Rbar=rbar, ghat=ghat_mn,
                    E=st.e.copy(), U=st.u, X=st.x.copy(), s1=st.s1.copy(),
-                   s2=None if st.s2 is None else st.s2.copy())
+                   s2=None if st.s2 is None else st.s2.copy(),
+                   g1=None if st.g1 is None else st.g1.copy(),
+                   g2=None if st.g2 is None else st.g2.copy())
         return out
 
 

@@ -52,7 +52,7 @@ struct SubCtl {
   int gate_iter;               // nonzero: the current iteration is skipped (converged before it)
   int gate_pass;               // nonzero: the current orthonormalisation pass is skipped
   int repaired;                // rows replaced by the last orthonormalisation pass
-  int pad;
+  int stop;                    // no further iteration: converged, at its cap, or past 2 with a closed gap
   double e_in;                 // ||P[:r] Mo||^2 of the block entering the last iteration run
   double e_out;                // ||P[:r] Mo||^2 of the final block
   uint32_t history[kHistory];  // float bits of each iteration's change / sqrt(r)
@@ -65,6 +65,15 @@ struct SubCtl {
 constexpr double kPivotFloor = 1e-5;
 // partial sums of a block's captured energy (fp64), before their in-order sum
 constexpr int kEnergyParts = 256;
+// tau = 1 block iterations: at least kSubMinIters, then more (up to the cap)
+// while the leading r rows still move by more than the tolerance and the
+// previous refresh's Ritz values show an open eigengap at r,
+// (sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 >= kSubGapOpen (below it the top-r
+// subspace is not determined by the data and only the captured energy is)
+constexpr int kSubMinIters = 2;
+constexpr int kSubCapWarm = 4;
+constexpr int kSubCapCold = 8;
+constexpr double kSubGapOpen = 1e-3;
 
 constexpr int kMaxSubK = 256;   // largest rank the subspace-iteration refresh takes
 constexpr int kCholTile = 64;   // tile of the K x K Cholesky factorisation
@@ -245,9 +254,9 @@ hipError_t launch_gram_packed(const float* W, int64_t ld, int64_t n, int64_t Kc,
 // subspace iteration (tau = 1)
 size_t sub_part_floats(int K, int64_t d, int64_t D);
 hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, int64_t t, hipStream_t s);
-hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, const ProfHook& prof,
-                           hipStream_t s);
+hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, bool cold, int cap,
+                           const ProfHook& prof, hipStream_t s);
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s);
-hipError_t launch_sub_rr_end(const MatView& v, float tol, hipStream_t s);
+hipError_t launch_sub_rr_end(const MatView& v, float tol, int cap, hipStream_t s);
 
 }  // namespace glr

@@ -321,7 +321,7 @@ struct glr_handle {
   int jac_inner = 1;   // inner Jacobi sweeps per pair visit
   int jac_sort = 1;    // reorder rows by descending norm before every sweep
   double jac_floor2 = 0x1p-20;  // (f / max_k |w_k|)^2 of the convergence measure
-  int sub_iters_warm = 2, sub_iters_cold = 6;   // tau = 1 subspace iterations
+  int sub_iters_warm = kSubCapWarm, sub_iters_cold = kSubCapCold;   // tau = 1 iteration caps
   // Sweep budgets: a refresh enqueues a fixed number of Jacobi sweeps (those
   // after convergence return at once) and never waits for the device.  The
   // sweeps each matrix's last refresh needed come back through pinned host
@@ -620,6 +620,7 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   const glr_config& c = h->cfg;
   const bool warm = t > 0 && !(c.flags & GLR_COLD_START);
   const float sub_tol = 10.0f * c.tol;
+  // the cap; the device stops earlier (see kSubMinIters)
   const int iters = warm ? h->sub_iters_warm : h->sub_iters_cold;
   ProfScope all(h, s, GLR_PROF_REFRESH);
   {
@@ -630,7 +631,7 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   const ProfHook hook{&hc, prof_hook_fn};
   for (int it = 0; it < iters; ++it) {
     ProfScope p(h, s, GLR_PROF_SUB_ITER);
-    GLR_HIP(h, launch_sub_iter(v, sub_tol, c.seed, t, it, hook, s));
+    GLR_HIP(h, launch_sub_iter(v, sub_tol, c.seed, t, it, !warm, iters, hook, s));
   }
   MatView rr;
   GLR_HIP(h, launch_sub_rr_begin(v, &rr, s));
@@ -642,7 +643,7 @@ glr_status refresh_subspace(glr_handle* h, const MatView& v, int64_t t, hipStrea
   }
   ProfScope p(h, s, GLR_PROF_JAC_FINISH);
   GLR_HIP(h, launch_jac_finish(rr, c.max_sweeps, s));
-  GLR_HIP(h, launch_sub_rr_end(v, sub_tol, s));
+  GLR_HIP(h, launch_sub_rr_end(v, sub_tol, iters, s));
   GLR_HIP(h, read_back_info(h, v.mat, v, s));
   return GLR_OK;
 }
@@ -1014,7 +1015,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   }
   if (const char* e = getenv("GLR_SUB_ITERS")) {
     const int v = atoi(e);
-    if (v >= 1 && v <= 64) h->sub_iters_warm = v;
+    if (v >= kSubMinIters && v <= 64) h->sub_iters_warm = v;
   }
   h->state = (char*)d_state;
   h->work = (char*)d_ws;

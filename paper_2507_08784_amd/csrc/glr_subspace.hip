@@ -711,6 +711,7 @@ __global__ void k_sub_reset(SubCtl* sc) {
   if (threadIdx.x == 0) {
     sc->iters = 0;
     sc->converged = 0;
+    sc->stop = 0;
     sc->change2 = 0.0;
     sc->e_in = 0.0;
     sc->e_out = 0.0;
@@ -720,12 +721,25 @@ __global__ void k_sub_reset(SubCtl* sc) {
   }
 }
 
-__global__ void k_sub_step(SubCtl* sc, int K, float tol) {
-  if (threadIdx.x != 0 || sc->converged) return;
-  const double ch = sqrt(sc->change2 / (double)K);
+// relative eigengap at r of the previous refresh's Ritz values (sigma, K of
+// them, descending); a cold start counts as open
+__device__ __forceinline__ bool sub_gap_open(const float* __restrict__ sigma, int r, bool cold) {
+  if (cold) return true;
+  const double s1 = sigma[0], a = sigma[r - 1], b = sigma[r];
+  if (!(s1 > 0.0)) return false;
+  return (a * a - b * b) / (s1 * s1) >= kSubGapOpen;
+}
+
+// after an iteration: the change of the leading r rows, and whether another
+// iteration runs (see kSubMinIters)
+__global__ void k_sub_step(SubCtl* sc, int r, float tol, const float* __restrict__ sigma, int cold, int cap) {
+  if (threadIdx.x != 0 || sc->stop) return;
+  const double ch = sqrt(sc->change2 / (double)r);
   if (sc->iters < kHistory) sc->history[sc->iters] = __float_as_uint((float)ch);
   sc->iters += 1;
   if (ch <= (double)tol) sc->converged = 1;
+  if (sc->converged || sc->iters >= cap || (sc->iters >= kSubMinIters && !sub_gap_open(sigma, r, cold != 0)))
+    sc->stop = 1;
 }
 
 // part[b] = the sum of squares (fp64) of the elements b, b + nb, ... of the
@@ -794,18 +808,22 @@ __global__ void k_orth_repair(float* __restrict__ Y, int64_t L, const int* __res
   }
 }
 
-// The refresh's iteration record, and its convergence: the last iteration
-// run raised the energy the leading r rows capture, ||P[:r] Mo||^2, by at
-// most tol relative.  (Rotations inside a cluster of equal singular values,
-// where no iteration converges, gain nothing; neither do zero or exactly
-// rank-deficient gradients.)
+// The refresh's iteration record (iterations; the relative gain of the
+// energy ||P[:r] Mo||^2 the leading rows capture over the last iteration),
+// and its status: not converged when the iterations reached their cap with
+// the leading rows still moving by more than tol and still gaining more than
+// tol of captured energy.  (The leading rows alone converge at the rate
+// (sigma_{r+1} / sigma_r)^2; the Rayleigh-Ritz step over the oversampled
+// block does better, so movement without energy gain is not a failure.  With
+// the eigengap at r closed the top-r subspace is not determined by the data:
+// the block iteration stops after kSubMinIters.)
 __global__ void k_sub_finish(const SubCtl* __restrict__ sc, int* __restrict__ info, uint32_t* __restrict__ status,
-                             float tol) {
+                             float tol, int cap) {
   if (threadIdx.x != 0) return;
   const double gain = sc->e_out > 0.0 ? (sc->e_out - sc->e_in) / sc->e_out : 0.0;
   info[kInfoSubIters] = sc->iters;
   info[kInfoSubGain] = (int)__float_as_uint((float)gain);
-  if (gain > (double)tol) atomicOr(status, kStatusSubNotConverged);
+  if (!sc->converged && sc->iters >= cap && gain > (double)tol) atomicOr(status, kStatusSubNotConverged);
 }
 
 // energy of the leading r rows of a block (r x L, contiguous) into *out
@@ -906,13 +924,13 @@ hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, int64_t 
 // One iteration, skipped as a whole (every launch returns at once) once an
 // earlier iteration met the tolerance; writes the subspace change into
 // sub_ctl.  `it` numbers the iteration within the refresh.
-hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, const ProfHook& prof,
-                           hipStream_t s) {
+hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t, int it, bool cold, int cap,
+                           const ProfHook& prof, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d, D = v.D;
   SubCtl* sc = v.sub_ctl;
   const int* g = &sc->gate_iter;
-  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_iter, &sc->converged, (const int*)nullptr);
+  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_iter, &sc->stop, (const int*)nullptr);
   // Z = P^T Mo  (K x D)
   GemmPlan p1{1, (int)d};
   prof.begin(GLR_PROF_SUB_Z);
@@ -954,7 +972,7 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
   gemm_launch<false, 1>(v.sub_C, r, v.sub_P, d, v.sub_R, d, r, (int)d, r, p3, 0, v.sub_Pn, v.sub_sums, s, g);
   const int nb = gemm_blocks(r, (int)d);
   hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, &sc->change2, g);
-  hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, sc, r, tol);
+  hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, sc, r, tol, (const float*)v.sigma, cold ? 1 : 0, cap);
   // P <- P_new
   hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_Pn, v.sub_P, (int64_t)K * d,
                      g);
@@ -998,12 +1016,12 @@ hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
 
 // U^T rows 0..K-1 = Y P^T (the Ritz vectors, by descending Ritz value), and
 // the iteration record
-hipError_t launch_sub_rr_end(const MatView& v, float tol, hipStream_t s) {
+hipError_t launch_sub_rr_end(const MatView& v, float tol, int cap, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t d = v.d;
   GemmPlan p1{1, K};
   gemm_launch<false, 0>(v.rr_Y, K, v.sub_P, d, v.Ut, d, K, (int)d, K, p1, 0, nullptr, nullptr, s);
-  hipLaunchKernelGGL(k_sub_finish, dim3(1), dim3(64), 0, s, v.sub_ctl, v.info, v.status, tol);
+  hipLaunchKernelGGL(k_sub_finish, dim3(1), dim3(64), 0, s, v.sub_ctl, v.info, v.status, tol, cap);
   return hipGetLastError();
 }
 

@@ -16,7 +16,10 @@ the oracle first checks the GPU's basis against its own fp64 one:
     g = (sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 of the oracle's Mbar Mbar^T
     is at least 1e-2; below that the projector moves by up to ~1/g times any
     perturbation of Mbar Mbar^T (Davis-Kahan), so the bar is 1e-4 * (1e-2/g)
-    at that step only;
+    at that step only, and below g = 1e-3 (a closed gap: the top-r subspace
+    is not determined by the data, and neither the GPU's iteration nor the
+    oracle's converges to a unique one) the projector is not compared and the
+    captured energy must be within 5e-4 ||Mbar||^2 of the oracle's;
 and then continues from the GPU's basis.  At a selection step the oracle
 ranks its own fp64 scores on that basis; J must equal the GPU's unless the
 r-th and (r+1)-th scores are within 1e-4 relative (the margin rule), where
@@ -43,6 +46,8 @@ ORTH_TOL = 1e-5
 SIGMA_TOL = 1e-5
 ENERGY_TOL = 1e-5
 GAP_FULL = 1e-2      # relative eigengap at r from which the projector bar is STEP_TOL
+GAP_CLOSED = 1e-3    # below it the top-r projector is not determined by the data
+ENERGY_TOL_CLOSED = 5e-4
 
 
 def rel(a, b, floor=0.0):
@@ -110,17 +115,21 @@ class Handoff:
         mbar = out["mbar"]
         fro2 = float(np.sum(mbar * mbar))
         pg = ut[:r].T
+        po = out["U"][:, :r]
+        gap = eigengap(sig_o, r, out.get("sigma_next")) if r < d else np.inf
+        rec["gap"] = gap
         if fro2 > 0 and r < d:
             tail = fro2 - float(np.sum((pg.T @ mbar) ** 2))
             tail_o = fro2 - float(np.sum(np.asarray(sig_o[:r]) ** 2))
             rec["energy"] = abs(tail - tail_o) / fro2
-            assert rec["energy"] < ENERGY_TOL, (t, l, rec)
-        po = out["U"][:, :r]
-        gap = eigengap(sig_o, r, out.get("sigma_next")) if r < d else np.inf
-        rec["gap"] = gap
-        rec["proj_bar"] = projector_bar(gap)
+            bar = ENERGY_TOL if gap >= GAP_CLOSED else ENERGY_TOL_CLOSED
+            assert rec["energy"] < bar, (t, l, rec)
         rec["proj"] = rel(pg @ pg.T, po @ po.T)
-        assert rec["proj"] < rec["proj_bar"], f"t={t} mat={l}: refresh projector rel {rec['proj']:.3e} ({rec})"
+        if gap >= GAP_CLOSED:
+            rec["proj_bar"] = projector_bar(gap)
+            assert rec["proj"] < rec["proj_bar"], f"t={t} mat={l}: refresh projector rel {rec['proj']:.3e} ({rec})"
+        else:
+            rec["proj_unpinned"] = True
         return ut.T
 
     def selection(self, l, t, out, j_oracle):
@@ -220,7 +229,9 @@ def summarize(name, log):
     """Prints the largest value of every compared quantity (and the smallest
     eigengap and selection margin, and how many J hand-offs took place)."""
     keys = ("proj", "proj_sel", "E", "Ebar", "X", "S1", "S2", "orth", "sigma", "energy", "final_X")
-    out = {k: max(r[k] for r in log if k in r) for k in keys if any(k in r for r in log)}
+    pinned = [r for r in log if not r.get("proj_unpinned")]
+    out = {k: max(r[k] for r in (pinned if k == "proj" else log) if k in r)
+           for k in keys if any(k in r for r in (pinned if k == "proj" else log))}
     gaps = [r["gap"] for r in log if "gap" in r and np.isfinite(r["gap"])]
     if gaps:
         out["min_gap"] = min(gaps)
@@ -228,6 +239,7 @@ def summarize(name, log):
     if margins:
         out["min_margin"] = min(margins)
     out["j_handoffs"] = sum(1 for r in log if r.get("j_handoff"))
+    out["closed_gap_refreshes"] = sum(1 for r in log if r.get("proj_unpinned"))
     print(f"[parity] {name} max " + " ".join(f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}"
                                              for k, v in out.items()), flush=True)
     return out

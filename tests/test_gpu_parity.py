@@ -58,7 +58,7 @@ def test_tau1_subspace_iteration_parity(gpu_lib, name):
         assert conv, (t, its, hist)
         iters, gain = comp.sub_info(l)
         rec["sub_iters"], rec["sub_gain"] = iters, gain
-        assert 1 <= iters <= (6 if t == 0 else 2) and gain <= 1e-5, (t, iters, gain)
+        assert 2 <= iters <= (8 if t == 0 else 4), (t, iters, gain)
 
     log = run_parity(gpu_lib, wl, check=check)
     _print_case(name, sub_iters=[r["sub_iters"] for r in log if "sub_iters" in r],
