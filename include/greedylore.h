@@ -184,6 +184,24 @@ glr_status glr_state_layout(const glr_config* cfg, int32_t mat, glr_mat_layout* 
 glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes,
                       void* d_ws, size_t ws_bytes, void* stream, glr_handle** out);
 
+/* glr_create for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * workspace is a static device array of GLR_STATIC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends; the caller
+ * still owns the state blob, X and G.  Creating, stepping and destroying such
+ * a handle calls no hipMalloc, hipFree, hipHostMalloc nor stream or event
+ * creation (profiling, if enabled, creates events).  Such a handle runs every
+ * matrix on `stream`, without grouped selection steps, and enqueues
+ * max_sweeps sweeps per refresh (no sweep counts come back to the host).
+ * GLR_ERR_BUFFER_TOO_SMALL when the configuration's workspace
+ * (glr_workspace_bytes) exceeds the array.  The array is shared by the handle
+ * and keeps its contents between handles (creation clears what must start
+ * at zero), so only one such handle may live per device at a time
+ * (GLR_ERR_STATE otherwise): calls of two handles on one device would race. */
+#define GLR_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+glr_status glr_create_static(const glr_config* cfg, void* d_state, size_t state_bytes, void* stream,
+                             glr_handle** out);
+
 /* Runs step t on every matrix.  X: host array of num_mats device pointers to
  * the m x n fp32 weights, updated in place.  G: host array of num_mats device
  * pointers, each to N contiguous m x n fp32 gradients (worker-major), read

@@ -29,8 +29,9 @@ EXPORTED = (
     "glr_validate_config", "glr_workspace_bytes", "glr_state_layout", "glr_create", "glr_step",
     "glr_sync_status", "glr_resume", "glr_next_step", "glr_destroy", "glr_status_string",
     "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
-    "glr_read_state", "glr_write_state",
+    "glr_read_state", "glr_write_state", "glr_create_static",
 )
+STATIC_SCRATCH_BYTES = 64 << 20
 STATE_PARTS = ("E", "Ebar", "Ut", "sigma", "J", "score", "S1", "S2", "Rbar", "info")
 PROF_GROUPS = ("ef_mean", "select", "topr", "proj", "rbar", "resid_opt", "full_refresh",
                "jac_init", "jac_update", "jac_finish", "refresh", "sub_iter", "jac_solve",
@@ -103,6 +104,7 @@ def load():
         "glr_profile_reset": (I32, [VP]),
         "glr_profile_query": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
         "glr_read_state": (I32, [VP, I32, P(StateView), VP]),
+        "glr_create_static": (I32, [P(Config), VP, ctypes.c_size_t, VP, P(VP)]),
         "glr_write_state": (I32, [VP, I32, P(StateView), VP]),
     }
     for name, (res, args) in sig.items():

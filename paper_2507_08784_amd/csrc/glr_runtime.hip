@@ -317,6 +317,7 @@ struct glr_handle {
   int device = 0;
   int64_t next_t = 0;
   bool suspect = false;
+  bool static_ws = false;              // the workspace is the static scratch array (glr_create_static)
   std::string err;
   int jac_inner = 1;   // inner Jacobi sweeps per pair visit
   int jac_sort = 1;    // reorder rows by descending norm before every sweep
@@ -527,6 +528,7 @@ hipError_t prof_collect(glr_handle* h) {
 // and the next refresh gets every allowed sweep again.
 int sweep_budget(glr_handle* h, int mat) {
   const int mx = h->cfg.max_sweeps;
+  if (!h->info_host) return mx;   // no read-back buffer (glr_create_static)
   if (h->info_pending[(size_t)mat] && hipEventQuery(h->info_ev[(size_t)mat]) == hipSuccess) {
     h->info_pending[(size_t)mat] = 0;
     h->known_sweeps[(size_t)mat] = h->info_host[2 * mat];
@@ -540,7 +542,7 @@ int sweep_budget(glr_handle* h, int mat) {
 
 // after a refresh's finish: its sweep count and converged flag to the host
 hipError_t read_back_info(glr_handle* h, int mat, const MatView& v, hipStream_t s) {
-  if (h->info_pending[(size_t)mat]) return hipSuccess;   // the previous read-back is still in flight
+  if (!h->info_host || h->info_pending[(size_t)mat]) return hipSuccess;   // the previous read-back is still in flight
   hipError_t e = hipMemcpyAsync(h->info_host + 2 * mat, v.info, 2 * sizeof(int), hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipEventRecord(h->info_ev[(size_t)mat], s);
   if (e == hipSuccess) h->info_pending[(size_t)mat] = 1;
@@ -874,7 +876,7 @@ glr_status step_grouped(glr_handle* h, float* const* X, const float* const* G, i
 // and at most 128, and the same side (so the same kernel variants)
 bool group_allowed(const glr_handle* h) {
   const glr_config& c = h->cfg;
-  if (c.num_mats < 2 || c.tau == 1) return false;
+  if (c.num_mats < 2 || c.tau == 1 || h->static_ws) return false;
   if (const char* e = getenv("GLR_GROUPED"))
     if (atoi(e) == 0) return false;
   const glr_mat_layout& L0 = h->lay[0];
@@ -985,8 +987,32 @@ glr_status glr_state_layout(const glr_config* cfg, int32_t mat, glr_mat_layout* 
   return GLR_OK;
 }
 
-glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, void* d_ws,
-                      size_t ws_bytes, void* stream, glr_handle** out) {
+}  // extern "C"
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// The workspace of handles made by glr_create_static: a file-scope device
+// array, which every device the library runs on holds (its own copy, at its
+// own address) until the process ends.  Host code never passes the array's
+// name as an address: the device address is taken once per device, with that
+// device current, by hipGetSymbolAddress, and only that address is used.
+// ---------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = GLR_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+void* g_static_ptr[kMaxDevices] = {};
+bool g_static_busy[kMaxDevices] = {};
+
+void static_release(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return;
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  g_static_busy[dev] = false;
+}
+
+glr_status create_impl(const glr_config* cfg, void* d_state, size_t state_bytes, void* d_ws, size_t ws_bytes,
+                       void* stream, glr_handle** out, bool static_ws) {
   std::string why;
   glr_status s = check_config(cfg, &why);
   if (s != GLR_OK) return fail(nullptr, s, why);
@@ -1019,6 +1045,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   }
   h->state = (char*)d_state;
   h->work = (char*)d_ws;
+  h->static_ws = static_ws;
   uint64_t o = kHeaderBytes;
   h->lay.resize(cfg->num_mats);
   for (int i = 0; i < cfg->num_mats; ++i) mat_layout(&h->cfg, i, o, &h->lay[i], &o);
@@ -1028,7 +1055,7 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   for (int i = 0; e == hipSuccess && i < cfg->num_mats; ++i)
     e = launch_eye((float*)(h->state + h->lay[i].off_U), h->lay[i].d, st);
   if (e == hipSuccess) e = launch_fill_zero(d_ws, (size_t)wl.bytes, st);
-  h->lanes = wl.lanes;
+  h->lanes = static_ws ? 1 : wl.lanes;   // no stream of its own without allocation
   if (const char* v = getenv("GLR_LANES")) {
     const int k = atoi(v);
     if (k >= 1 && k < h->lanes) h->lanes = k;
@@ -1043,9 +1070,9 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   h->known_conv.assign((size_t)cfg->num_mats, 0);
   h->info_pending.assign((size_t)cfg->num_mats, 0);
   h->info_ev.assign((size_t)cfg->num_mats, nullptr);
-  if (e == hipSuccess)
+  if (e == hipSuccess && !static_ws)
     e = hipHostMalloc((void**)&h->info_host, 2 * sizeof(int) * (size_t)cfg->num_mats, hipHostMallocDefault);
-  for (int i = 0; e == hipSuccess && i < cfg->num_mats; ++i)
+  for (int i = 0; e == hipSuccess && !static_ws && i < cfg->num_mats; ++i)
     e = hipEventCreateWithFlags(&h->info_ev[(size_t)i], hipEventDisableTiming);
   if (e == hipSuccess && joint_allowed(h)) {
     h->joint = true;
@@ -1065,6 +1092,53 @@ glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, 
   }
   *out = h;
   return GLR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+glr_status glr_create(const glr_config* cfg, void* d_state, size_t state_bytes, void* d_ws,
+                      size_t ws_bytes, void* stream, glr_handle** out) {
+  return create_impl(cfg, d_state, state_bytes, d_ws, ws_bytes, stream, out, false);
+}
+
+glr_status glr_create_static(const glr_config* cfg, void* d_state, size_t state_bytes, void* stream,
+                             glr_handle** out) {
+  std::string why;
+  glr_status s = check_config(cfg, &why);
+  if (s != GLR_OK) return fail(nullptr, s, why);
+  if (!out) return fail(nullptr, GLR_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  const uint64_t need = ws_plan(cfg).bytes;
+  if (need > kStaticScratchBytes)
+    return fail(nullptr, GLR_ERR_BUFFER_TOO_SMALL,
+                fmt("the configuration needs %llu workspace bytes; the static scratch holds %llu "
+                    "(use glr_create with a caller workspace)",
+                    (unsigned long long)need, (unsigned long long)kStaticScratchBytes));
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(nullptr, GLR_ERR_DEVICE, fmt("hipGetDevice: %s", hipGetErrorString(e)));
+  if (dev < 0 || dev >= kMaxDevices) return fail(nullptr, GLR_ERR_DEVICE, "device index out of range");
+  void* ptr = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (g_static_busy[dev])
+      return fail(nullptr, GLR_ERR_STATE,
+                  fmt("the static scratch of device %d belongs to another live handle (one at a time)", dev));
+    if (!g_static_ptr[dev]) {
+      e = hipGetSymbolAddress(&g_static_ptr[dev], HIP_SYMBOL(scratch));
+      if (e != hipSuccess) {
+        g_static_ptr[dev] = nullptr;
+        return fail(nullptr, GLR_ERR_DEVICE, fmt("hipGetSymbolAddress(scratch): %s", hipGetErrorString(e)));
+      }
+    }
+    ptr = g_static_ptr[dev];
+    g_static_busy[dev] = true;
+  }
+  s = create_impl(cfg, d_state, state_bytes, ptr, kStaticScratchBytes, stream, out, true);
+  if (s != GLR_OK) static_release(dev);
+  return s;
 }
 
 glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64_t t, void* stream) {
@@ -1205,6 +1279,7 @@ glr_status glr_destroy(glr_handle* h) {
   release_group(h);
   release_lanes(h);
   release_info(h);
+  if (h->static_ws) static_release(h->device);
   delete h;
   return GLR_OK;
 }
