@@ -98,7 +98,17 @@ typedef enum {
   GLR_ERR_BREAKDOWN = 8         /* tau = 1 refresh: dependent rows survived the repair pass */
 } glr_status;
 
-typedef enum { GLR_MSGD = 0, GLR_ADAM = 1 } glr_opt;
+/* Optimizers: MSGD (eq-msgd) and Adam (eq-adam) on the full m x n state, or
+ * GALORE_ADAM, the distributed Adam-type GaLore of Algorithm 5 (Appendix E,
+ * a baseline of the paper): Lazy-SVD projection (P kept between refreshes,
+ * as GLR_SELECT_LAZY), no error feedback (as GLR_NO_EF), Adam moments kept
+ * in the r x D subspace (S1 = M, S2 = V, the first r D floats of each, row
+ * major, oriented) and restarted from zero at every refresh, and the step
+ * X -= lr P (M / (sqrt(V) + eps)) (transposed back iff m > n); Rbar then
+ * holds that direction M / (sqrt(V) + eps) after the step.  Algorithm 5's
+ * printed moment updates exchange beta and 1 - beta and apply lr twice; the
+ * main text's Adam with one lr is used.  Requires GLR_REFRESH_COMPRESSED. */
+typedef enum { GLR_MSGD = 0, GLR_ADAM = 1, GLR_GALORE_ADAM = 2 } glr_opt;
 
 /* Refresh-step semantics.  COMPRESSED follows Algorithm 4 ("the complete
  * procedure"): refresh steps compress like every other step.  FULL follows
@@ -111,11 +121,21 @@ typedef enum { GLR_REFRESH_COMPRESSED = 0, GLR_REFRESH_FULL = 1 } glr_refresh;
  * Approx-Top-r with the products of u_j and Mbar taken on their bf16
  * roundings (round to nearest even; v_j and the sums stay fp32): a mixed
  * precision mode for the ranking only (a score carries ~2^-8 relative error
- * per term), on the bf16 matrix cores; everything else stays fp32. */
-typedef enum { GLR_SELECT_APPROX = 0, GLR_SELECT_EXACT = 1, GLR_SELECT_APPROX_BF16 = 2 } glr_select;
+ * per term), on the bf16 matrix cores; everything else stays fp32.  LAZY is
+ * the Lazy-SVD operator of the basic framework (Section IV, Algorithm 1, a
+ * baseline of the paper): P_t = P_{t-1} between refreshes (J and U kept, no
+ * scores).  Algorithm 1 itself is LAZY with GLR_NO_EF and
+ * GLR_REFRESH_FULL. */
+typedef enum {
+  GLR_SELECT_APPROX = 0,
+  GLR_SELECT_EXACT = 1,
+  GLR_SELECT_APPROX_BF16 = 2,
+  GLR_SELECT_LAZY = 3
+} glr_select;
 
 #define GLR_CHECK_FINITE 0x1u  /* scan G for NaN/Inf during the worker mean */
 #define GLR_COLD_START   0x2u  /* start every refresh from U = I instead of the previous U */
+#define GLR_NO_EF        0x4u  /* no error feedback: M^(i) = G^(i), E^(i) and Ebar stay zero */
 
 typedef struct {
   int64_t m, n;                /* layer matrix shape, caller's row-major layout;
@@ -140,7 +160,7 @@ typedef struct {
   float tol;                   /* Jacobi stop, in (0, 1): every pair of rows of W = U^T Mbar has
                                   |w_p.w_q| <= tol max(|w_p||w_q|, ||w_p|^2 - |w_q|^2|, f^2),
                                   f = 2^-10 max_k |w_k| (cosine and rotation angle below tol) */
-  uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START */
+  uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF */
 } glr_config;
 
 /* Byte offsets into the state blob for one matrix (all 256-byte aligned). */
@@ -154,13 +174,14 @@ typedef struct {
   uint64_t off_sigma;          /* d fp32: singular values of Mbar at the last refresh, descending */
   uint64_t off_J;              /* r int32: selected columns of U, ascending */
   uint64_t off_score;          /* d fp32: last selection scores (lambdabar^2 or ||u_j^T Mbar||^2) */
-  uint64_t off_S1;             /* m x n fp32: MSGD buffer M, or Adam first moment M */
-  uint64_t off_S2;             /* m x n fp32: Adam second moment V (0 for MSGD: absent) */
+  uint64_t off_S1;             /* m x n fp32: MSGD buffer M, or Adam first moment M (GaLore: r x D) */
+  uint64_t off_S2;             /* m x n fp32: Adam second moment V (GaLore: r x D; 0 for MSGD: absent) */
   uint64_t off_Rbar;           /* r x D fp32: mean over workers of Q^(i) = P^T M^(i) (oriented) */
   uint64_t off_info;           /* 64 int32: [0] sweeps of the last refresh, [1] converged flag,
                                   [2 + s] float bits of sweep s's largest pair off-norm (s < 60);
                                   tau = 1 refresh: [62] block iterations, [63] float bits of
-                                  the last iteration's relative gain of ||P[:r]^T Mbar||^2 */
+                                  the last iteration's relative gain of the energy ||P^T Mbar||^2
+                                  of the oversampled block */
 } glr_mat_layout;
 
 typedef struct glr_handle glr_handle;
@@ -221,8 +242,9 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G,
  *                          refresh whose block iteration reached its cap (4
  *                          from the previous block, 8 from a cold start) with
  *                          the leading r rows still moving by more than 10 tol
- *                          and still raising the energy ||P^T Mbar||^2 they
- *                          capture by more than 10 tol relative.  (The block
+ *                          and the oversampled block still raising the energy
+ *                          ||P^T Mbar||^2 it captures by more than 10 tol
+ *                          relative.  (The block
  *                          iteration runs at least 2 times, and more only while
  *                          the previous refresh's Ritz values show a relative
  *                          gap (sigma_r^2 - sigma_{r+1}^2) / sigma_1^2 of at

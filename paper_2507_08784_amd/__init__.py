@@ -25,6 +25,7 @@ STATUS_NAMES = {
 }
 CHECK_FINITE = 0x1
 COLD_START = 0x2
+NO_EF = 0x4
 EXPORTED = (
     "glr_validate_config", "glr_workspace_bytes", "glr_state_layout", "glr_create", "glr_step",
     "glr_sync_status", "glr_resume", "glr_next_step", "glr_destroy", "glr_status_string",
@@ -122,10 +123,10 @@ def make_config(shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta
     arr = (Shape * len(shapes))(*[Shape(int(m), int(n)) for m, n in shapes])
     cfg = Config(
         num_mats=len(shapes), shapes=ctypes.cast(arr, ctypes.POINTER(Shape)), num_workers=workers,
-        rank=rank, tau=tau, opt={"msgd": 0, "adam": 1}[opt] if isinstance(opt, str) else opt,
+        rank=rank, tau=tau, opt={"msgd": 0, "adam": 1, "galore_adam": 2}[opt] if isinstance(opt, str) else opt,
         lr=lr, beta1=beta1, beta2=beta2, eps=eps,
         refresh={"compressed": 0, "full": 1}[refresh] if isinstance(refresh, str) else refresh,
-        select={"approx": 0, "exact": 1, "approx_bf16": 2}[select] if isinstance(select, str) else select,
+        select={"approx": 0, "exact": 1, "approx_bf16": 2, "lazy": 3}[select] if isinstance(select, str) else select,
         seed=seed, max_sweeps=max_sweeps, tol=tol, flags=flags)
     return cfg, arr
 
@@ -158,14 +159,14 @@ class GreedyLore:
 
     def __init__(self, shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999,
                  eps=1e-8, refresh="compressed", select="approx", seed=0, max_sweeps=30,
-                 tol=1e-6, check_finite=False, cold_start=False, device="cuda", stream=None):
+                 tol=1e-6, check_finite=False, cold_start=False, ef=True, device="cuda", stream=None):
         import torch
         self.lib = load()
         self.torch = torch
         self.shapes = [tuple(int(x) for x in s) for s in shapes]
         self.workers = workers
         self.opt = opt
-        flags = (CHECK_FINITE if check_finite else 0) | (COLD_START if cold_start else 0)
+        flags = (CHECK_FINITE if check_finite else 0) | (COLD_START if cold_start else 0) | (0 if ef else NO_EF)
         self.cfg, self._shape_arr = make_config(self.shapes, workers, rank, tau, opt, lr, beta1,
                                                 beta2, eps, refresh, select, seed, max_sweeps,
                                                 tol, flags)

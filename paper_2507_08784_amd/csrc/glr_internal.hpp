@@ -42,7 +42,7 @@ constexpr uint32_t kStatusRepaired = 16u;       // dependent rows of an orthonor
 // the last refresh, [1] its converged flag, [2 + s] sweep s's largest pair
 // off-norm (float bits); for the tau = 1 refresh also:
 constexpr int kInfoSubIters = 62;    // block iterations run (fewer than the budget: the leading r rows met the tolerance)
-constexpr int kInfoSubGain = 63;     // float bits: relative gain of the captured energy over the last iteration
+constexpr int kInfoSubGain = 63;     // float bits: relative gain of the block's captured energy over the last iteration
 
 // Control words of the subspace iteration (device memory).
 struct SubCtl {
@@ -53,8 +53,8 @@ struct SubCtl {
   int gate_pass;               // nonzero: the current orthonormalisation pass is skipped
   int repaired;                // rows replaced by the last orthonormalisation pass
   int stop;                    // no further iteration: converged, at its cap, or past 2 with a closed gap
-  double e_in;                 // ||P[:r] Mo||^2 of the block entering the last iteration run
-  double e_out;                // ||P[:r] Mo||^2 of the final block
+  double e_in;                 // ||P Mo||^2 of the K-row block entering the last iteration run
+  double e_out;                // ||P Mo||^2 of the final block
   uint32_t history[kHistory];  // float bits of each iteration's change / sqrt(r)
 };
 
@@ -152,8 +152,9 @@ inline int proj_splits(int64_t d, int64_t D, int r, int N) {
 constexpr int kResidWideRank = 128;
 
 struct OptParams {
-  int opt;                   // 0 MSGD, 1 Adam
+  int opt;                   // 0 MSGD, 1 Adam, 2 plain step X -= lr Ghat (GaLore: Ghat = P Rhat)
   float lr, beta1, beta2, eps;
+  int ef = 1;                // error feedback: write E^(i) and Ebar = Mbar - Ghat (0: both stay zero)
 };
 
 // launchers (return the first launch error)
@@ -167,6 +168,9 @@ hipError_t launch_proj(const MatView& v, hipStream_t s);
 hipError_t launch_rbar(const MatView& v, hipStream_t s);
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s);
 hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s);
+// Algorithm 5 (GaLore Adam in the r x D subspace): S1, S2 <- the moments of
+// Rbar (from zero when `reset`), Rbar <- S1 / (sqrt(S2) + eps)
+hipError_t launch_galore_adam(const MatView& v, const OptParams& o, bool reset, hipStream_t s);
 
 // One matrix of a grouped selection step (device memory, rewritten every such
 // step: the view carries that step's X and G) and its projection slicing.

@@ -95,20 +95,25 @@ glr_status check_config(const glr_config* c, std::string* why) {
     return bad(GLR_ERR_INVALID_ARG, fmt("num_workers must be in [1, %d]", kMaxWorkers));
   if (c->rank < 1) return bad(GLR_ERR_INVALID_ARG, "rank must be >= 1");
   if (c->tau < 1) return bad(GLR_ERR_INVALID_ARG, "tau must be >= 1");
-  if (c->opt != GLR_MSGD && c->opt != GLR_ADAM) return bad(GLR_ERR_INVALID_ARG, "unknown optimizer");
+  if (c->opt != GLR_MSGD && c->opt != GLR_ADAM && c->opt != GLR_GALORE_ADAM)
+    return bad(GLR_ERR_INVALID_ARG, "unknown optimizer");
   if (!(std::isfinite(c->lr) && c->lr > 0.f)) return bad(GLR_ERR_INVALID_ARG, "lr must be finite and > 0");
   if (!(c->beta1 >= 0.f && c->beta1 < 1.f)) return bad(GLR_ERR_INVALID_ARG, "beta1 must be in [0, 1)");
-  if (c->opt == GLR_ADAM) {
+  if (c->opt == GLR_ADAM || c->opt == GLR_GALORE_ADAM) {
     if (!(c->beta2 >= 0.f && c->beta2 < 1.f)) return bad(GLR_ERR_INVALID_ARG, "beta2 must be in [0, 1)");
     if (!(std::isfinite(c->eps) && c->eps > 0.f)) return bad(GLR_ERR_INVALID_ARG, "eps must be finite and > 0");
   }
   if (c->refresh != GLR_REFRESH_COMPRESSED && c->refresh != GLR_REFRESH_FULL)
     return bad(GLR_ERR_INVALID_ARG, "unknown refresh mode");
-  if (c->select != GLR_SELECT_APPROX && c->select != GLR_SELECT_EXACT && c->select != GLR_SELECT_APPROX_BF16)
+  if (c->select != GLR_SELECT_APPROX && c->select != GLR_SELECT_EXACT && c->select != GLR_SELECT_APPROX_BF16 &&
+      c->select != GLR_SELECT_LAZY)
     return bad(GLR_ERR_INVALID_ARG, "unknown select mode");
+  if (c->opt == GLR_GALORE_ADAM && c->refresh != GLR_REFRESH_COMPRESSED)
+    return bad(GLR_ERR_INVALID_ARG, "GaLore Adam (Algorithm 5) compresses at refresh steps: use GLR_REFRESH_COMPRESSED");
   if (c->max_sweeps < 1) return bad(GLR_ERR_INVALID_ARG, "max_sweeps must be >= 1");
   if (!(c->tol > 0.f && c->tol < 1.f)) return bad(GLR_ERR_INVALID_ARG, "tol must be in (0, 1)");
-  if (c->flags & ~(GLR_CHECK_FINITE | GLR_COLD_START)) return bad(GLR_ERR_INVALID_ARG, "unknown flag bits");
+  if (c->flags & ~(GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF))
+    return bad(GLR_ERR_INVALID_ARG, "unknown flag bits");
   for (int i = 0; i < c->num_mats; ++i) {
     const int64_t m = c->shapes[i].m, n = c->shapes[i].n;
     if (m < 1 || n < 1) return bad(GLR_ERR_SHAPE, fmt("matrix %d: shape %lldx%lld must be positive", i, (long long)m, (long long)n));
@@ -144,7 +149,7 @@ void mat_layout(const glr_config* c, int mat, uint64_t base, glr_mat_layout* L, 
   L->off_J = take((uint64_t)x.r * 4);
   L->off_score = take((uint64_t)x.d * 4);
   L->off_S1 = take(mn * 4);
-  L->off_S2 = c->opt == GLR_ADAM ? take(mn * 4) : 0;
+  L->off_S2 = (c->opt == GLR_ADAM || c->opt == GLR_GALORE_ADAM) ? take(mn * 4) : 0;
   L->off_Rbar = take((uint64_t)x.r * (uint64_t)x.D * 4);
   L->off_info = take(kInfoInts * 4);
   *end = o;
@@ -333,6 +338,8 @@ struct glr_handle {
   int64_t repaired_total = 0;          // status reads that found replaced (dependent) rows
   int* info_host = nullptr;            // pinned, 2 ints per matrix
   std::vector<hipEvent_t> info_ev;
+  bool lazy = false;                   // P kept between refreshes (Lazy-SVD, GaLore)
+  bool ef = true;                      // error feedback
   bool prof = false;
   bool joint = false;                  // refresh steps sweep all matrices in shared launches
   std::vector<JointMat> jm;            // host copies of the joint tables (kept for the async upload)
@@ -660,7 +667,8 @@ glr_status step_head(glr_handle* h, const MatView& v, hipStream_t s) {
 // projection on the chosen columns, their mean, residual and optimizer update
 glr_status step_tail(glr_handle* h, const MatView& v, bool refresh, hipStream_t s) {
   const glr_config& c = h->cfg;
-  OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
+  const bool galore = c.opt == GLR_GALORE_ADAM;
+  OptParams op{galore ? 2 : c.opt, c.lr, c.beta1, c.beta2, c.eps, h->ef ? 1 : 0};
   {
     ProfScope p(h, s, GLR_PROF_PROJ);
     GLR_HIP(h, launch_proj(v, s));
@@ -669,6 +677,7 @@ glr_status step_tail(glr_handle* h, const MatView& v, bool refresh, hipStream_t 
     ProfScope p(h, s, GLR_PROF_RBAR);
     GLR_HIP(h, launch_rbar(v, s));
   }
+  if (galore) GLR_HIP(h, launch_galore_adam(v, op, refresh, s));
   if (refresh && c.refresh == GLR_REFRESH_FULL) {
     ProfScope p(h, s, GLR_PROF_FULL_REFRESH);
     GLR_HIP(h, launch_full_refresh(v, op, s));
@@ -688,7 +697,7 @@ glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t,
   if (refresh) {
     glr_status st = use_subspace(c.tau, v.r, v.d) ? refresh_subspace(h, v, t, s) : refresh_svd(h, v, t, s);
     if (st != GLR_OK) return st;
-  } else if (v.r < v.d) {
+  } else if (v.r < v.d && !h->lazy) {
     {
       ProfScope p(h, s, GLR_PROF_SELECT);
       GLR_HIP(h, launch_sel_scores(v, c.select != GLR_SELECT_EXACT, c.select == GLR_SELECT_APPROX_BF16, c.seed, t,
@@ -876,7 +885,7 @@ glr_status step_grouped(glr_handle* h, float* const* X, const float* const* G, i
 // and at most 128, and the same side (so the same kernel variants)
 bool group_allowed(const glr_handle* h) {
   const glr_config& c = h->cfg;
-  if (c.num_mats < 2 || c.tau == 1 || h->static_ws) return false;
+  if (c.num_mats < 2 || c.tau == 1 || h->static_ws || h->lazy || !h->ef || c.opt == GLR_GALORE_ADAM) return false;
   if (const char* e = getenv("GLR_GROUPED"))
     if (atoi(e) == 0) return false;
   const glr_mat_layout& L0 = h->lay[0];
@@ -1046,6 +1055,8 @@ glr_status create_impl(const glr_config* cfg, void* d_state, size_t state_bytes,
   h->state = (char*)d_state;
   h->work = (char*)d_ws;
   h->static_ws = static_ws;
+  h->lazy = cfg->select == GLR_SELECT_LAZY || cfg->opt == GLR_GALORE_ADAM;
+  h->ef = !(cfg->flags & GLR_NO_EF) && cfg->opt != GLR_GALORE_ADAM;
   uint64_t o = kHeaderBytes;
   h->lay.resize(cfg->num_mats);
   for (int i = 0; i < cfg->num_mats; ++i) mat_layout(&h->cfg, i, o, &h->lay[i], &o);

@@ -515,20 +515,25 @@ __device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float*
     for (int v = 0; v < 16; ++v) {
       const uint32_t o = ob[tm][v];
       const float gh = tile.acc[tm][0][v];
-      float xv = buf_ld(Xr, o), s1 = buf_ld(S1r, o);
-      if (OPT == 0) {
-        s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
-        xv = xv - op.lr * s1;
+      float xv = buf_ld(Xr, o);
+      if (OPT == 2) {
+        xv = xv - op.lr * gh;
       } else {
-        float s2 = buf_ld(S2r, o);
-        s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
-        s2 = op.beta2 * s2 + (1.0f - op.beta2) * gh * gh;
-        xv = xv - op.lr * s1 / (sqrtf(s2) + op.eps);
-        buf_st(S2r, o, s2);
+        float s1 = buf_ld(S1r, o);
+        if (OPT == 0) {
+          s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+          xv = xv - op.lr * s1;
+        } else {
+          float s2 = buf_ld(S2r, o);
+          s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+          s2 = op.beta2 * s2 + (1.0f - op.beta2) * gh * gh;
+          xv = xv - op.lr * s1 / (sqrtf(s2) + op.eps);
+          buf_st(S2r, o, s2);
+        }
+        buf_st(S1r, o, s1);
       }
-      buf_st(Ebr, o, buf_ld(Mr, o) - gh);
+      buf_st(Ebr, o, op.ef ? buf_ld(Mr, o) - gh : 0.0f);
       buf_st(Xr, o, xv);
-      buf_st(S1r, o, s1);
     }
 }
 template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
@@ -597,7 +602,7 @@ k_resid_wide(const float* __restrict__ G, float* __restrict__ E, const float* __
 }
 
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  const bool wide = v.r > kResidWideRank;
+  const bool wide = v.r > kResidWideRank && o.ef;
   if (wide) {
     dim3 gw((unsigned)((v.n + 127) / 128), (unsigned)((v.m + 127) / 128));
     if (v.right)
@@ -607,15 +612,42 @@ hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s)
       hipLaunchKernelGGL(k_resid_wide<false>, gw, dim3(kThreads), 0, s, v.G, v.E, v.Q, v.Ut, v.J, v.m, v.n,
                          v.d, v.D, v.r, v.N);
   }
-  const int nfused = wide ? 0 : v.N;   // workers whose residual k_resid_opt updates
+  const int nfused = (wide || !o.ef) ? 0 : v.N;   // workers whose residual k_resid_opt updates
   constexpr int rows = 64, cols = 64;
   dim3 grid((unsigned)((v.n + cols - 1) / cols), (unsigned)((v.m + rows - 1) / rows));
 #define GLR_RO(OPT, R)                                                                               \
   hipLaunchKernelGGL((k_resid_opt<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
                      v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, nfused, o)
-  if (o.opt == 0) { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
-  else            { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
+  if (o.opt == 0)      { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
+  else if (o.opt == 1) { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
+  else                 { if (v.right) GLR_RO(2, true); else GLR_RO(2, false); }
 #undef GLR_RO
+  return hipGetLastError();
+}
+
+// Algorithm 5 (distributed Adam-type GaLore): the Adam moments live in the
+// r x D subspace (S1 = M, S2 = V, row-major r x D, oriented) and restart from
+// zero at every refresh; the step direction Rhat = M / (sqrt(V) + eps)
+// replaces Rbar, so that the reconstruction P Rhat and X -= lr P Rhat follow
+// in k_resid_opt<2>.  Moments in the main text's form (eq-adam).
+__global__ void k_galore_adam(float* __restrict__ Rbar, float* __restrict__ S1, float* __restrict__ S2, int64_t n,
+                              float beta1, float beta2, float eps, int reset) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride) {
+    const float g = Rbar[i];
+    const float m0 = reset ? 0.0f : S1[i], v0 = reset ? 0.0f : S2[i];
+    const float m1 = beta1 * m0 + (1.0f - beta1) * g;
+    const float v1 = beta2 * v0 + (1.0f - beta2) * g * g;
+    S1[i] = m1;
+    S2[i] = v1;
+    Rbar[i] = m1 / (sqrtf(v1) + eps);
+  }
+}
+
+hipError_t launch_galore_adam(const MatView& v, const OptParams& o, bool reset, hipStream_t s) {
+  const int64_t n = (int64_t)v.r * v.D;
+  hipLaunchKernelGGL(k_galore_adam, dim3(grid_for(n)), dim3(256), 0, s, v.Rbar, v.S1, v.S2, n, o.beta1, o.beta2,
+                     o.eps, reset ? 1 : 0);
   return hipGetLastError();
 }
 

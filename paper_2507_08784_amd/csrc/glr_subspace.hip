@@ -809,14 +809,14 @@ __global__ void k_orth_repair(float* __restrict__ Y, int64_t L, const int* __res
 }
 
 // The refresh's iteration record (iterations; the relative gain of the
-// energy ||P[:r] Mo||^2 the leading rows capture over the last iteration),
+// energy ||P Mo||^2 the whole K-row block captures over the last iteration),
 // and its status: not converged when the iterations reached their cap with
-// the leading rows still moving by more than tol and still gaining more than
-// tol of captured energy.  (The leading rows alone converge at the rate
-// (sigma_{r+1} / sigma_r)^2; the Rayleigh-Ritz step over the oversampled
-// block does better, so movement without energy gain is not a failure.  With
-// the eigengap at r closed the top-r subspace is not determined by the data:
-// the block iteration stops after kSubMinIters.)
+// the leading rows still moving by more than tol and the block still gaining
+// more than tol of captured energy.  (The leading rows alone converge at the
+// rate (sigma_{r+1} / sigma_r)^2; the Rayleigh-Ritz step draws the top r from
+// the whole oversampled block, so movement without energy gain is not a
+// failure.  With the eigengap at r closed the top-r subspace is not
+// determined by the data: the block iteration stops after kSubMinIters.)
 __global__ void k_sub_finish(const SubCtl* __restrict__ sc, int* __restrict__ info, uint32_t* __restrict__ status,
                              float tol, int cap) {
   if (threadIdx.x != 0) return;
@@ -939,7 +939,7 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
   else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
     gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s, g);
   prof.end(GLR_PROF_SUB_Z);
-  block_energy(v, v.sub_Z, v.r, D, &sc->e_in, g, s);
+  block_energy(v, v.sub_Z, K, D, &sc->e_in, g, s);
   // Z only carries the span into the next product: one scaled pass keeps it
   // well conditioned
   const uint32_t tag = 0xC0000000u | ((uint32_t)(it + 1) << 8);
@@ -991,7 +991,7 @@ hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
     gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
   else
     gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
-  block_energy(v, v.sub_Z, v.r, D, &v.sub_ctl->e_out, nullptr, s);
+  block_energy(v, v.sub_Z, K, D, &v.sub_ctl->e_out, nullptr, s);
   *rr = v;
   rr->d = K;
   rr->D = D;
@@ -1021,6 +1021,15 @@ hipError_t launch_sub_rr_end(const MatView& v, float tol, int cap, hipStream_t s
   const int64_t d = v.d;
   GemmPlan p1{1, K};
   gemm_launch<false, 0>(v.rr_Y, K, v.sub_P, d, v.Ut, d, K, (int)d, K, p1, 0, nullptr, nullptr, s);
+  // one Newton-Schulz step on the K rows, U^T <- U^T - (U^T U - I) U^T / 2
+  // with the Gram in fp64 (the fp32 rotations of the Rayleigh-Ritz Jacobi
+  // leave drift of a few 1e-6 on rank-deficient blocks)
+  dim3 g64((K + 63) / 64, (K + 63) / 64, 1);
+  hipLaunchKernelGGL(k_gram64<1>, g64, dim3(256), 0, s, v.Ut, d, v.Ut, d, K, K, (int)d, (int)d, (double*)nullptr,
+                     v.sub_C, (int64_t)K);
+  gemm_launch<false, 2>(v.sub_C, K, v.Ut, d, v.sub_R, d, K, (int)d, K, p1, 0, v.Ut, nullptr, s);
+  hipError_t e = hipMemcpyAsync(v.Ut, v.sub_R, (size_t)K * d * 4, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_sub_finish, dim3(1), dim3(64), 0, s, v.sub_ctl, v.info, v.status, tol, cap);
   return hipGetLastError();
 }

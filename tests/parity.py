@@ -148,7 +148,7 @@ class Handoff:
 
 
 def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_start=False,
-               max_sweeps=30, tol=1e-6, check=None, handoff=True):
+               max_sweeps=30, tol=1e-6, check=None, handoff=True, ef=True):
     """Runs both paths; returns a list of per-step dicts of relative errors.
     Raises AssertionError at the first step over the bars."""
     import torch
@@ -157,8 +157,9 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
     comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
                           beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, refresh=refresh,
                           select=select, seed=wl.seed, max_sweeps=max_sweeps, tol=tol,
-                          cold_start=cold_start)
-    orc = Oracle.from_workload(wl, refresh=refresh, select=select)
+                          cold_start=cold_start, ef=ef)
+    orc = Oracle.from_workload(wl, refresh=refresh, select=select, ef=ef)
+    galore = wl.opt == "galore_adam"
     planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
     X = [torch.zeros(m, n, dtype=torch.float32, device="cuda") for (m, n) in wl.shapes]
     log = []
@@ -206,9 +207,15 @@ def run_parity(glr, wl, steps=None, refresh="compressed", select="approx", cold_
             e_g = comp.E(l).double().cpu().numpy()
             rec["E"] = rel(e_g, e_o, floor=1e-3 * mi * np.sqrt(e_o.size))
             rec["X"] = rel(X[l].double().cpu().numpy(), o["X"])
-            rec["S1"] = rel(comp.S1(l).double().cpu().numpy(), o["s1"])
-            if o["s2"] is not None:
-                rec["S2"] = rel(comp.S2(l).double().cpu().numpy(), o["s2"])
+            if galore:
+                # Algorithm 5's moments, r x D (oriented) at the start of S1 / S2
+                rD = o["g1"].size
+                rec["S1"] = rel(comp.S1(l).flatten()[:rD].double().cpu().numpy(), o["g1"].ravel())
+                rec["S2"] = rel(comp.S2(l).flatten()[:rD].double().cpu().numpy(), o["g2"].ravel())
+            else:
+                rec["S1"] = rel(comp.S1(l).double().cpu().numpy(), o["s1"])
+                if o["s2"] is not None:
+                    rec["S2"] = rel(comp.S2(l).double().cpu().numpy(), o["s2"])
             rec["Ebar"] = rel(comp.Ebar(l).double().cpu().numpy(), e_o.mean(axis=0),
                               floor=1e-3 * mi * np.sqrt(m * n))
             for key in ("E", "X", "S1", "S2", "Ebar"):

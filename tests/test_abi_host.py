@@ -46,7 +46,7 @@ def test_valid_config():
     (dict(workers=0), 1), (dict(rank=0), 1), (dict(tau=0), 1), (dict(opt=7), 1),
     (dict(lr=0.0), 1), (dict(lr=float("nan")), 1), (dict(beta1=1.0), 1), (dict(beta1=-0.1), 1),
     (dict(opt="adam", beta2=1.0), 1), (dict(opt="adam", eps=0.0), 1), (dict(refresh=5), 1),
-    (dict(select=3), 1), (dict(max_sweeps=0), 1), (dict(tol=0.0), 1), (dict(tol=1.0), 1),
+    (dict(select=4), 1), (dict(opt="galore_adam", refresh="full"), 1), (dict(max_sweeps=0), 1), (dict(tol=0.0), 1), (dict(tol=1.0), 1),
     (dict(flags=0x80), 1), (dict(shapes=[(0, 5)]), 2), (dict(shapes=[(5, -1)]), 2),
     (dict(shapes=[(9000, 9000)]), 2), (dict(shapes=[(2000, 3000)], rank=2000), 2),
     (dict(shapes=[(8192, 1 << 17)]), 2),   # m n = 2^30: beyond 32-bit byte offsets
