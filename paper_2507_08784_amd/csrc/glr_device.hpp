@@ -72,10 +72,21 @@ __device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 c) {
 // one feeds the MFMAs.
 // ---------------------------------------------------------------------------
 
+// LDS column swizzle of a k-major slice: element (k, r) sits at column
+// r ^ lds_swz(k).  It flips bits 2-3 of r only, so the 32 columns one MFMA
+// operand read covers stay a permutation of one aligned 32-column block
+// (conflict-free reads).
+__device__ __forceinline__ constexpr int lds_swz(int k) { return 4 * ((k >> 3) & 3); }
+
 // Element (r, k) at base[row(r) * ld + k] (+ base2[...] when fused): the
 // operand is contiguous along k.  Optional row gather through `rows`.
+// The transposing LDS store puts eight rows x eight float4 k-groups of a
+// half-wave in one LDS row pair; with the (R + 4)-float row pitch alone
+// those 32 stores meet in 8 banks, and the swizzle spreads them over 32.
 template <int R, int BK, bool FUSED, bool GATHER>
 struct LoadK {
+  static constexpr bool kSwz = true;
+  static_assert(R % 16 == 0, "swizzle stays inside the slice");
   static constexpr int KQ = BK / 4;                 // float4s per row slice
   static constexpr int NV = (R * KQ + kThreads - 1) / kThreads;
   const float* base;
@@ -136,11 +147,11 @@ struct LoadK {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       if (rl[i] >= R) continue;
-      int k = 4 * kq[i];
-      s[(k + 0) * P + rl[i]] = v[i].x;
-      s[(k + 1) * P + rl[i]] = v[i].y;
-      s[(k + 2) * P + rl[i]] = v[i].z;
-      s[(k + 3) * P + rl[i]] = v[i].w;
+      const int k = 4 * kq[i], c = rl[i] ^ lds_swz(k);   // k .. k+3 share the swizzle
+      s[(k + 0) * P + c] = v[i].x;
+      s[(k + 1) * P + c] = v[i].y;
+      s[(k + 2) * P + c] = v[i].z;
+      s[(k + 3) * P + c] = v[i].w;
     }
   }
 };
@@ -149,6 +160,7 @@ struct LoadK {
 // krow(k) = rows[k] when GATHER, else k.
 template <int R, int BK, bool FUSED, bool GATHER = false>
 struct LoadR {
+  static constexpr bool kSwz = false;
   static constexpr int RQ = R / 4;
   static constexpr int NV = (BK * RQ + kThreads - 1) / kThreads;
   const float* base;
@@ -251,15 +263,20 @@ struct MfmaTile {
   }
   __device__ __forceinline__ int col(int tn) const { return wn * WTN + tn * 32 + (lane & 31); }
 
+  // SWA / SWB: the operand's slice is stored with the lds_swz column swizzle
+  template <bool SWA, bool SWB>
   __device__ __forceinline__ void compute(const float* As, const float* Bs) {
     const int kh = lane >> 5, l32 = lane & 31;
 #pragma unroll
     for (int kk = 0; kk < BK / 2; ++kk) {
+      // rows 2 kk and 2 kk + 1 share one swizzle
+      const int ca = SWA ? (l32 ^ lds_swz(2 * kk)) : l32;
+      const int cb = SWB ? (l32 ^ lds_swz(2 * kk)) : l32;
       float a[TM], b[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = As[(2 * kk + kh) * PA + wm * WTM + i * 32 + l32];
+      for (int i = 0; i < TM; ++i) a[i] = As[(2 * kk + kh) * PA + wm * WTM + i * 32 + ca];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) b[j] = Bs[(2 * kk + kh) * PB + wn * WTN + j * 32 + l32];
+      for (int j = 0; j < TN; ++j) b[j] = Bs[(2 * kk + kh) * PB + wn * WTN + j * 32 + cb];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -269,19 +286,23 @@ struct MfmaTile {
 
   // the same product with both operands rounded to bf16 (to nearest even) as
   // they leave LDS, fp32 accumulation: two bf16 MFMAs of depth 16 per slice
+  template <bool SWA, bool SWB>
   __device__ __forceinline__ void compute_bf16(const float* As, const float* Bs) {
     const int kh = lane >> 5, l32 = lane & 31;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
+      // rows 16 ks + 8 kh .. + 7 share one swizzle
+      const int ca = SWA ? (l32 ^ lds_swz(16 * ks + 8 * kh)) : l32;
+      const int cb = SWB ? (l32 ^ lds_swz(16 * ks + 8 * kh)) : l32;
       bf16x8 a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)As[(16 * ks + 8 * kh + e) * PA + wm * WTM + i * 32 + l32];
+        for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)As[(16 * ks + 8 * kh + e) * PA + wm * WTM + i * 32 + ca];
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) b[j][e] = (__bf16)Bs[(16 * ks + 8 * kh + e) * PB + wn * WTN + j * 32 + l32];
+        for (int e = 0; e < 8; ++e) b[j][e] = (__bf16)Bs[(16 * ks + 8 * kh + e) * PB + wn * WTN + j * 32 + cb];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -310,8 +331,8 @@ struct MfmaTile {
         la.fetch((kb + 1) * BK);
         lb.fetch((kb + 1) * BK);
       }
-      if constexpr (BF16) compute_bf16(As, Bs);
-      else compute(As, Bs);
+      if constexpr (BF16) compute_bf16<LA::kSwz, LB::kSwz>(As, Bs);
+      else compute<LA::kSwz, LB::kSwz>(As, Bs);
       if (dacc && ((kb & 15) == 15 || !more)) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
