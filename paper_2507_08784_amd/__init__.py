@@ -8,6 +8,9 @@ is no CPU fallback: if the library was not built, load() raises.
     import paper_2507_08784_amd as glr
     comp = glr.GreedyLore(shapes=[(4096, 4096)], workers=8, rank=64, tau=10)
     comp.step([X], [G], t)          # G: N x m x n fp32 on cuda, X: m x n fp32
+
+`paper_2507_08784_amd.ddp.GreedyLoreHook` drives the same step from a
+DistributedDataParallel communication hook.
 """
 from __future__ import annotations
 
