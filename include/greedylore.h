@@ -57,8 +57,9 @@
  * glr_step only enqueues: it never waits for the device (refresh steps
  * included).  A refresh enqueues a budget of Jacobi sweeps; the sweeps after
  * convergence return at once on the device.  The budget is max_sweeps until a
- * refresh of that matrix has been seen converged, then the sweeps that refresh
- * took plus a quarter (at least three); the sweep counts come back through
+ * refresh of that matrix has been seen converged, then the most sweeps a
+ * converged refresh of it took plus half of that (at least four), capped at
+ * max_sweeps; the sweep counts come back through
  * pinned host memory the handle owns, read only once their copy has completed.
  * A refresh that ends its budget above tol reports GLR_ERR_NOT_CONVERGED and
  * the next one gets max_sweeps again.  (Grouped selection steps reuse a

@@ -332,7 +332,7 @@ struct glr_handle {
   // after convergence return at once) and never waits for the device.  The
   // sweeps each matrix's last refresh needed come back through pinned host
   // memory, read only once the copy's event has completed.
-  std::vector<int> known_sweeps;       // sweeps of the last refresh read back (-1: none yet)
+  std::vector<int> known_sweeps;       // most sweeps a converged refresh took (-1: none yet)
   std::vector<int> known_conv;         // its converged flag
   std::vector<int> info_pending;       // a read-back is in flight
   int64_t repaired_total = 0;          // status reads that found replaced (dependent) rows
@@ -529,21 +529,25 @@ hipError_t prof_collect(glr_handle* h) {
   } while (0)
 
 // Sweeps to enqueue for a refresh of `mat`: every allowed sweep until a
-// refresh of this matrix has been read back converged, then that count plus
-// a margin (a quarter, at least three).  A refresh that runs out of its
-// budget reports GLR_ERR_NOT_CONVERGED like one that runs out of max_sweeps,
-// and the next refresh gets every allowed sweep again.
+// refresh of this matrix has been read back converged, then the largest count
+// read back so far plus a margin of half of it (at least four): a warm
+// refresh can need more sweeps than the cold one before it (7 then 10 have
+// been seen on the gradients of a small network).  A refresh that runs out of
+// its budget reports GLR_ERR_NOT_CONVERGED like one that runs out of
+// max_sweeps, and the next refresh gets every allowed sweep again.
 int sweep_budget(glr_handle* h, int mat) {
   const int mx = h->cfg.max_sweeps;
   if (!h->info_host) return mx;   // no read-back buffer (glr_create_static)
   if (h->info_pending[(size_t)mat] && hipEventQuery(h->info_ev[(size_t)mat]) == hipSuccess) {
     h->info_pending[(size_t)mat] = 0;
-    h->known_sweeps[(size_t)mat] = h->info_host[2 * mat];
-    h->known_conv[(size_t)mat] = h->info_host[2 * mat + 1];
+    const int seen = h->info_host[2 * mat], conv = h->info_host[2 * mat + 1];
+    h->known_conv[(size_t)mat] = conv;
+    // a miss forgets the record: the next refresh takes max_sweeps
+    h->known_sweeps[(size_t)mat] = conv ? std::max(h->known_sweeps[(size_t)mat], seen) : -1;
   }
   const int k = h->known_sweeps[(size_t)mat];
   if (k < 0 || !h->known_conv[(size_t)mat]) return mx;
-  const int b = k + std::max(3, k / 4);
+  const int b = k + std::max(4, k / 2);
   return b < mx ? b : mx;
 }
 
