@@ -601,8 +601,177 @@ k_resid_wide(const float* __restrict__ G, float* __restrict__ E, const float* __
   }
 }
 
+// S5 + S7 + S8 above rank 128, the workers side by side: one 64 x 64 output
+// tile of the m x n layout per workgroup (a 32 x 32 MFMA block per wave).
+// Each k-slice of P (gathered rows of U^T) is staged once and multiplied
+// with the slices of Q^(w) of up to kNW workers into one accumulator per
+// worker, so that the MFMAs run back to back over the whole rank-r
+// contraction.  Then E^(w) <- (G^(w) - P Q^(w)) + E^(w) for each worker,
+// Ghat = (1/N) sum_w P Q^(w) (= P Rbar by linearity, with no product of its
+// own), Ebar = Mbar - Ghat and the optimizer on X.  More than kNW workers
+// take several groups (MULTI), the products of the earlier groups summed in
+// registers.
+constexpr int kNW = 4;
+constexpr int kNWTile = 64;
+template <int OPT, bool RIGHT, bool MULTI>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_resid_nw(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
+           const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Ut,
+           const int* __restrict__ J, float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2,
+           int64_t m, int64_t n, int64_t d, int64_t D, int r, int N, OptParams op, int rows_fast) {
+  constexpr int BK = 32, T = kNWTile;
+  constexpr int PT = T + 4, SL = BK * PT;        // LDS pitch and slice size (P, then one per worker)
+  __shared__ __align__(16) float smem[(1 + kNW) * SL];
+  const int lane = lane_id(), wv = wave_id();
+  const int wm = wv >> 1, wn = wv & 1;
+  const int kh = lane >> 5, l32 = lane & 31;
+  // row tiles are the fast index: the workgroups in flight share the Q
+  // slices of a few column tiles, so that each XCD's L2 holds them (and its
+  // rows of P) instead of every row tile streaming all of Q again (columns
+  // fast only when the column tiles exceed the grid's y extent)
+  const int r0 = (rows_fast ? blockIdx.x : blockIdx.y) * T, c0 = (rows_fast ? blockIdx.y : blockIdx.x) * T;
+  const int s0 = RIGHT ? c0 : r0, q0 = RIGHT ? r0 : c0;   // first P row / first Q column of the tile
+  // the P operand is the MFMA's A (left: tile rows) or B (right: tile columns)
+  const int soff = (RIGHT ? wn : wm) * 32 + l32, qoff = (RIGHT ? wm : wn) * 32 + l32;
+  const int64_t mn = m * n;
+  const uint32_t bytes = (uint32_t)(mn * 4);
+  const int64_t col = c0 + wn * 32 + l32;
+  float gs[MULTI ? 16 : 1];
+  if (MULTI) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) gs[MULTI ? v : 0] = 0.f;
+  }
+  f32x16 acc[kNW];
+  const int64_t rD = (int64_t)r * D;
+  const int nk = (r + BK - 1) / BK;
+  for (int w0 = 0; w0 < N; w0 += kNW) {
+    const int nw = N - w0 < kNW ? N - w0 : kNW;
+#pragma unroll
+    for (int w = 0; w < kNW; ++w)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[w][v] = 0.f;
+    LoadR<T, BK, false, true> ls(Ut, nullptr, d, s0, (int)d, r, J);
+    // the workers' Q slices share one geometry: loader w reads worker w0 + w
+    // (a worker beyond N reads nothing: contraction length 0)
+    LoadR<T, BK, false> lq(Q + (int64_t)w0 * rD, nullptr, D, q0, (int)D, r);
+    const bool qvec = lq.vec;   // float4 loads need every worker's slice 16-byte aligned
+    float4 qv[kNW][decltype(lq)::NV];
+    auto fetch = [&](int k0) {
+      ls.fetch(k0);
+#pragma unroll
+      for (int w = 0; w < kNW; ++w) {
+        lq.base = Q + (int64_t)(w0 + (w < nw ? w : 0)) * rD;
+        lq.vec = qvec && ((reinterpret_cast<uintptr_t>(lq.base) & 15) == 0);
+        lq.K = w < nw ? r : 0;
+        lq.fetch(k0);
+#pragma unroll
+        for (int i = 0; i < decltype(lq)::NV; ++i) qv[w][i] = lq.v[i];
+      }
+    };
+    auto put = [&]() {
+      ls.template put<PT>(smem);
+#pragma unroll
+      for (int w = 0; w < kNW; ++w) {
+#pragma unroll
+        for (int i = 0; i < decltype(lq)::NV; ++i) lq.v[i] = qv[w][i];
+        lq.template put<PT>(smem + (1 + w) * SL);
+      }
+    };
+    fetch(0);
+    put();
+    __syncthreads();
+    for (int kb = 0; kb < nk; ++kb) {
+      const bool more = kb + 1 < nk;
+      if (more) fetch((kb + 1) * BK);
+#pragma unroll
+      for (int kk = 0; kk < BK / 2; ++kk) {
+        const int row = (2 * kk + kh) * PT;
+        const float sv = smem[row + soff];
+#pragma unroll
+        for (int w = 0; w < kNW; ++w) {
+          if (w >= nw) break;
+          const float qw = smem[(1 + w) * SL + row + qoff];
+          acc[w] = RIGHT ? mfma32(qw, sv, acc[w]) : mfma32(sv, qw, acc[w]);
+        }
+      }
+      __syncthreads();
+      if (more) {
+        put();
+        __syncthreads();
+      }
+    }
+    // the residuals of this group's workers
+#pragma unroll
+    for (int w = 0; w < kNW; ++w) {
+      if (w >= nw) break;
+      const BufRsrc Gw = buf_rsrc(G + (int64_t)(w0 + w) * mn, bytes);
+      const BufRsrc Ew = buf_rsrc(E + (int64_t)(w0 + w) * mn, bytes);
+      uint32_t ob[16];
+      float gv[16], eo[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t row = r0 + wm * 32 + mfma32_row(v, lane);
+        ob[v] = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
+        gv[v] = buf_ld(Gw, ob[v]);
+        eo[v] = buf_ld(Ew, ob[v]);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        // (G - P Q) + E: G and P Q nearly cancel, E is the small part
+        buf_st(Ew, ob[v], (gv[v] - acc[w][v]) + eo[v]);
+        if (MULTI) gs[MULTI ? v : 0] += acc[w][v];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  const float inv_n = 1.0f / (float)N;
+  const BufRsrc Xr = buf_rsrc(X, bytes), S1r = buf_rsrc(S1, bytes), Ebr = buf_rsrc(Ebar, bytes);
+  const BufRsrc Mr = buf_rsrc(Mbar, bytes);
+  const BufRsrc S2r = buf_rsrc(OPT == 1 ? S2 : S1, bytes);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int64_t row = r0 + wm * 32 + mfma32_row(v, lane);
+    const uint32_t o = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
+    // workers beyond N hold zero products
+    const float sum = MULTI ? gs[MULTI ? v : 0] : ((acc[0][v] + acc[1][v]) + acc[2][v]) + acc[3][v];
+    const float gh = sum * inv_n;
+    float xv = buf_ld(Xr, o);
+    float s1 = buf_ld(S1r, o);
+    if (OPT == 0) {
+      s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+      xv = xv - op.lr * s1;
+    } else {
+      float s2 = buf_ld(S2r, o);
+      s1 = op.beta1 * s1 + (1.0f - op.beta1) * gh;
+      s2 = op.beta2 * s2 + (1.0f - op.beta2) * gh * gh;
+      xv = xv - op.lr * s1 / (sqrtf(s2) + op.eps);
+      buf_st(S2r, o, s2);
+    }
+    buf_st(S1r, o, s1);
+    buf_st(Ebr, o, buf_ld(Mr, o) - gh);
+    buf_st(Xr, o, xv);
+    if ((v & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
   const bool wide = v.r > kResidWideRank && o.ef;
+  if (wide && o.opt != 2) {
+    // MSGD / Adam with error feedback: one fused pass
+    const bool multi = v.N > kNW;
+    const unsigned rt = (unsigned)((v.m + kNWTile - 1) / kNWTile), ct = (unsigned)((v.n + kNWTile - 1) / kNWTile);
+    const int rows_fast = ct <= 65535u ? 1 : 0;
+    dim3 gw(rows_fast ? rt : ct, rows_fast ? ct : rt);
+#define GLR_RW(OPT, R, MU)                                                                                 \
+  hipLaunchKernelGGL((k_resid_nw<OPT, R, MU>), gw, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, v.Q, v.Ut, v.J, \
+                     v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o, rows_fast)
+#define GLR_RW2(OPT, R) do { if (multi) GLR_RW(OPT, R, true); else GLR_RW(OPT, R, false); } while (0)
+    if (o.opt == 0) { if (v.right) GLR_RW2(0, true); else GLR_RW2(0, false); }
+    else            { if (v.right) GLR_RW2(1, true); else GLR_RW2(1, false); }
+#undef GLR_RW2
+#undef GLR_RW
+    return hipGetLastError();
+  }
   if (wide) {
     dim3 gw((unsigned)((v.n + 127) / 128), (unsigned)((v.m + 127) / 128));
     if (v.right)

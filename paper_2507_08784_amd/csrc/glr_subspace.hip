@@ -102,6 +102,19 @@ GemmPlan plan_splits(int M, int N, int Kc, int want_blocks) {
   return {splits, kslice};
 }
 
+// Z = P^T Mo (K x D over d): the K x D tiles alone leave part of the chip
+// idle for a whole d-long contraction (1120 tiles of 64 x 128 at K = 320,
+// D = 28672), so the contraction is split into slices of at least 2048
+// (fp32 partials added in fp64 by k_reduce_splits)
+GemmPlan plan_z(int K, int64_t D, int64_t d) {
+  GemmPlan p = plan_splits(K, (int)D, (int)d, 2048);
+  if (p.kslice < 2048) {
+    p.kslice = (int)std::min<int64_t>(2048, (d + 31) / 32 * 32);
+    p.splits = (int)((d + p.kslice - 1) / p.kslice);
+  }
+  return p;
+}
+
 template <bool B_KC, int EPI>
 static void gemm_launch(const float* A, int64_t lda, const float* B, int64_t ldb, float* C,
                         int64_t ldc, int M, int N, int Kc, GemmPlan p, int64_t cstride,
@@ -847,6 +860,8 @@ size_t sub_part_floats(int K, int64_t d, int64_t D) {
   upd(K, K, (int)D);
   upd(K, K, (int)d);
   upd(K, (int)d, (int)D);
+  const GemmPlan pz = plan_z(K, D, d);
+  mx = std::max(mx, (size_t)pz.splits * K * D);
   return mx;
 }
 
@@ -905,6 +920,22 @@ static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int6
   return hipGetLastError();
 }
 
+// sub_Z = P^T Mo (K x D), skipped when *gate is set
+static void launch_z(const MatView& v, int K, const int* gate, hipStream_t s) {
+  const int64_t d = v.d, D = v.D;
+  const GemmPlan pz = plan_z(K, D, d);
+  float* out = pz.splits > 1 ? v.sub_part : v.sub_Z;
+  if (v.right)   // Mo[a][b] = Mbar[b][a]: B(k=a, j=b) at Mbar[b d + a]
+    gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, out, D, K, (int)D, (int)d, pz, (int64_t)K * D, nullptr, nullptr, s,
+                         gate);
+  else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
+    gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, out, D, K, (int)D, (int)d, pz, (int64_t)K * D, nullptr, nullptr, s,
+                          gate);
+  if (pz.splits > 1)
+    hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * D)), dim3(256), 0, s, v.sub_part, pz.splits,
+                       (int64_t)K * D, v.sub_Z, (double*)nullptr, gate);
+}
+
 hipError_t launch_sub_start(const MatView& v, bool warm, uint64_t seed, int64_t t, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   hipLaunchKernelGGL(k_sub_reset, dim3(1), dim3(64), 0, s, v.sub_ctl);
@@ -932,12 +963,8 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
   const int* g = &sc->gate_iter;
   hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_iter, &sc->stop, (const int*)nullptr);
   // Z = P^T Mo  (K x D)
-  GemmPlan p1{1, (int)d};
   prof.begin(GLR_PROF_SUB_Z);
-  if (v.right)   // Mo[a][b] = Mbar[b][a]: B(k=a, j=b) at Mbar[b d + a]
-    gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s, g);
-  else           // Mo = Mbar (d x D): B(k=a, j=b) at Mbar[a D + b]
-    gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s, g);
+  launch_z(v, K, g, s);
   prof.end(GLR_PROF_SUB_Z);
   block_energy(v, v.sub_Z, K, D, &sc->e_in, g, s);
   // Z only carries the span into the next product: one scaled pass keeps it
@@ -985,12 +1012,8 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
 // J = 0..r-1, info and status as for a full refresh.
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
-  const int64_t d = v.d, D = v.D;
-  GemmPlan p1{1, (int)d};
-  if (v.right)
-    gemm_launch<true, 0>(v.sub_P, d, v.Mbar, d, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
-  else
-    gemm_launch<false, 0>(v.sub_P, d, v.Mbar, D, v.sub_Z, D, K, (int)D, (int)d, p1, 0, nullptr, nullptr, s);
+  const int64_t D = v.D;
+  launch_z(v, K, nullptr, s);
   block_energy(v, v.sub_Z, K, D, &v.sub_ctl->e_out, nullptr, s);
   *rr = v;
   rr->d = K;

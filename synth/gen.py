@@ -253,6 +253,19 @@ def _mk():
                  recipe="lowrank", params=(("rank", 4),)))
     add(Workload("zero_grad", ((32, 64),), 2, 4, 2, 4, "adam", 1e-3, 0.9,
                  recipe="zero"))
+    # ranks above 128: the wide-rank residual/optimizer pass, ragged tiles,
+    # both orientations and both optimizers (and tau = 1 with such a rank)
+    add(Workload("wide_left", ((300, 700),), 3, 150, 3, 6, "msgd", 0.01, 0.9,
+                 recipe="geometric", params=(("rank", 200), ("decay", 0.985), ("nu", 1e-4))))
+    add(Workload("wide_right", ((650, 290),), 2, 140, 2, 5, "adam", 1e-3, 0.9,
+                 recipe="geometric", params=(("rank", 180), ("decay", 0.985), ("nu", 1e-4))))
+    # (gap factor 10 at r: error feedback lifts the discarded directions by
+    # about their own size per step, so the gap stays open over the 4 steps)
+    # (MSGD: Adam's first step X = -lr sign-like(Ghat) turns the ~1e-8
+    # rounding of the elements with |Ghat| near 1e-8 into O(lr) differences,
+    # and 234 000 elements hold a few such)
+    add(Workload("tau1_wide", ((260, 900),), 2, 136, 1, 4, "msgd", 0.01, 0.9,
+                 recipe="geometric", params=(("rank", 180), ("decay", 0.985), ("nu", 1e-4), ("div", 10.0))))
     # tau = 1: every step a refresh, only the top-r block of U is used
     add(Workload("tau1_left", ((64, 300),), 3, 8, 1, 6, "adam", 1e-3, 0.9,
                  recipe="geometric", params=(("rank", 16), ("nu", 1e-3))))

@@ -15,7 +15,8 @@ def _print_case(name, **kw):
     print(f"[parity] {name} {kw}", flush=True)
 
 
-@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left", "single_worker"])
+@pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left", "single_worker",
+                                  "wide_left", "wide_right"])
 def test_trajectory_parity(gpu_lib, name):
     _print_case(name)
     wl = get_workload(name)
@@ -47,7 +48,7 @@ def test_refresh_full_parity(gpu_lib, name):
     run_parity(gpu_lib, get_workload(name), refresh="full", check=check)
 
 
-@pytest.mark.parametrize("name", ["tau1_left", "tau1_right", "tau1_k40"])
+@pytest.mark.parametrize("name", ["tau1_left", "tau1_right", "tau1_k40", "tau1_wide"])
 def test_tau1_subspace_iteration_parity(gpu_lib, name):
     # tau = 1: the refresh computes only span(U[:, :r]) by subspace iteration
     _print_case(name)
