@@ -51,6 +51,8 @@ struct SubCtl {
   double change2;              // squared Frobenius norm of the last change of the leading r rows
   int gate_iter;               // nonzero: the current iteration is skipped (converged before it)
   int gate_pass;               // nonzero: the current orthonormalisation pass is skipped
+  int gate_rest;               // nonzero: the rest of the pass is skipped (gated, or its rows are
+                               // orthonormal already)
   int repaired;                // rows replaced by the last orthonormalisation pass
   int stop;                    // no further iteration: converged, at its cap, or past 2 with a closed gap
   double e_in;                 // ||P Mo||^2 of the K-row block entering the last iteration run
@@ -63,6 +65,10 @@ struct SubCtl {
 // as dependent: the fp32 rows and their fp32-summed products resolve the
 // pivots only to about 1e-6.
 constexpr double kPivotFloor = 1e-5;
+// A CholeskyQR pass after the first is skipped when the Gram of its rows is
+// the identity to within this (largest |cosine| between two rows and largest
+// |squared norm - 1|): about the resolution of the fp32-product Gram itself.
+constexpr double kOrthSkip = 4e-6;
 // partial sums of a block's captured energy (fp64), before their in-order sum
 constexpr int kEnergyParts = 256;
 // tau = 1 block iterations: at least kSubMinIters, then more (up to the cap)

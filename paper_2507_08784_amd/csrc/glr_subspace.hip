@@ -280,6 +280,20 @@ __global__ void k_reduce_pack(const double* __restrict__ part, int splits, int n
   }
 }
 
+// the Newton-Schulz correction (C - I) / 2 (fp32, K x K, both triangles)
+// from the fp64 partials of k_gram64<0> (upper tiles), summed in split order
+__global__ void k_ns_reduce(const double* __restrict__ part, int splits, int K, float* __restrict__ out) {
+  const int64_t count = (int64_t)K * K;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < count; e += stride) {
+    const int i = (int)(e / K), j = (int)(e % K);
+    const int64_t src = (int64_t)(i < j ? i : j) * K + (i < j ? j : i);
+    double c = 0.0;
+    for (int z = 0; z < splits; ++z) c += part[(int64_t)z * count + src];
+    out[e] = (float)(0.5 * (c - (i == j ? 1.0 : 0.0)));
+  }
+}
+
 // contraction splits of the n x n Gram over Kc: enough workgroups for the
 // chip when the tiles alone are few, slices of at least 512
 int gram_splits(int64_t n, int64_t Kc) {
@@ -871,14 +885,46 @@ static void repair_key(uint64_t seed, int64_t t, uint32_t* k0, uint32_t* k1) {
   *k1 = (uint32_t)(seed >> 32) ^ (uint32_t)t ^ 0x4B5A6978u;
 }
 
+// *out = 1 when *gate is set or the K x K Gram S (fp64) is the identity to
+// within kOrthSkip: the rows it came from are orthonormal, and the rest of
+// their CholeskyQR pass is skipped
+__global__ void __launch_bounds__(1024) k_orth_check(const double* __restrict__ S, int K, const int* __restrict__ gate,
+                                                     int* __restrict__ out) {
+  __shared__ double red[16];
+  if (*gate) {
+    if (threadIdx.x == 0) *out = 1;
+    return;
+  }
+  double mx = 0.0;
+  for (int e = threadIdx.x; e < K * K; e += blockDim.x) {
+    const int i = e / K, j = e % K;
+    const double sij = S[e];
+    if (i == j) {
+      mx = fmax(mx, fabs(sij - 1.0));
+    } else {
+      const double den = S[(int64_t)i * K + i] * S[(int64_t)j * K + j];
+      // a zero row is not orthonormal: no skip
+      mx = fmax(mx, den > 0.0 ? fabs(sij) / sqrt(den) : 1.0);
+    }
+  }
+  mx = wave_max(mx);
+  if (lane_id() == 0) red[wave_id()] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double m = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) m = fmax(m, red[w]);
+    *out = m <= kOrthSkip ? 1 : 0;
+  }
+}
+
 // One CholeskyQR pass on the rows of Y (K x L), skipped when *gate is set:
 // S = Y Y^T (fp32 MFMA, partial sums added in fp64), the Cholesky factor of
 // the diagonally scaled S (dependent rows marked), Y <- L^-1 Y, then every
 // marked row replaced by a Gaussian row (SubCtl::repaired tells whether any
 // was).
 static hipError_t orth_pass(const MatView& v, float* Y, float* Ytmp, int K, int64_t L, const int* gate,
-                            uint32_t tag, bool last_pass, uint64_t seed, int64_t t, const ProfHook& prof,
-                            hipStream_t s) {
+                            uint32_t tag, bool last_pass, bool check, uint64_t seed, int64_t t,
+                            const ProfHook& prof, hipStream_t s) {
   const int Kp = chol_pad(K);
   SubCtl* sc = v.sub_ctl;
   hipLaunchKernelGGL(k_pass_reset, dim3(1), dim3(256), 0, s, v.sub_bad, K, &sc->repaired, gate);
@@ -886,6 +932,11 @@ static hipError_t orth_pass(const MatView& v, float* Y, float* Ytmp, int K, int6
   gemm_launch<true, 0>(Y, L, Y, L, v.sub_part, K, K, K, (int)L, pg, (int64_t)K * K, nullptr, nullptr, s, gate);
   hipLaunchKernelGGL(k_reduce_splits, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.sub_part,
                      pg.splits, (int64_t)K * K, (float*)nullptr, v.sub_S, gate);
+  if (check) {
+    // a repeat pass on rows that came out orthonormal changes nothing
+    hipLaunchKernelGGL(k_orth_check, dim3(1), dim3(1024), 0, s, v.sub_S, K, gate, &sc->gate_rest);
+    gate = &sc->gate_rest;
+  }
   prof.begin(GLR_PROF_SUB_CHOL);
   hipError_t ce = launch_chol_inv(v, K, gate, s);
   if (ce != hipSuccess) return ce;
@@ -913,7 +964,8 @@ static hipError_t orth_rows(const MatView& v, float* Y, float* Ytmp, int K, int6
   for (int pass = 0; pass <= passes; ++pass) {
     const bool extra = pass == passes;
     hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, &sc->gate_pass, outer, extra ? &sc->repaired : nullptr);
-    hipError_t e = orth_pass(v, Y, Ytmp, K, L, &sc->gate_pass, tag + (uint32_t)pass, extra, seed, t, prof, s);
+    hipError_t e = orth_pass(v, Y, Ytmp, K, L, &sc->gate_pass, tag + (uint32_t)pass, extra, pass > 0 && !extra,
+                             seed, t, prof, s);
     if (e != hipSuccess) return e;
   }
   prof.end(GLR_PROF_SUB_ORTH);
@@ -967,11 +1019,16 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
   launch_z(v, K, g, s);
   prof.end(GLR_PROF_SUB_Z);
   block_energy(v, v.sub_Z, K, D, &sc->e_in, g, s);
-  // Z only carries the span into the next product: one scaled pass keeps it
-  // well conditioned
+  // Z only carries the span into the next product.  From a cold start one
+  // scaled pass keeps it well conditioned; from the previous Ritz vectors its
+  // rows are already near orthogonal (scaled by the singular values), which
+  // the diagonally scaled CholeskyQR of the next half step absorbs
   const uint32_t tag = 0xC0000000u | ((uint32_t)(it + 1) << 8);
-  hipError_t e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, 1, g, tag, seed, t, prof, s);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (cold) {
+    e = orth_rows(v, v.sub_Z, v.sub_Zt, K, D, 1, g, tag, seed, t, prof, s);
+    if (e != hipSuccess) return e;
+  }
   // P_new = Z Mo^T  (K x d): B(k=b, j=a) = Mo[a][b]
   GemmPlan p2 = plan_splits(K, (int)d, (int)D);
   prof.begin(GLR_PROF_SUB_P);
@@ -1046,10 +1103,21 @@ hipError_t launch_sub_rr_end(const MatView& v, float tol, int cap, hipStream_t s
   gemm_launch<false, 0>(v.rr_Y, K, v.sub_P, d, v.Ut, d, K, (int)d, K, p1, 0, nullptr, nullptr, s);
   // one Newton-Schulz step on the K rows, U^T <- U^T - (U^T U - I) U^T / 2
   // with the Gram in fp64 (the fp32 rotations of the Rayleigh-Ritz Jacobi
-  // leave drift of a few 1e-6 on rank-deficient blocks)
-  dim3 g64((K + 63) / 64, (K + 63) / 64, 1);
-  hipLaunchKernelGGL(k_gram64<1>, g64, dim3(256), 0, s, v.Ut, d, v.Ut, d, K, K, (int)d, (int)d, (double*)nullptr,
-                     v.sub_C, (int64_t)K);
+  // leave drift of a few 1e-6 on rank-deficient blocks).  The K x K tiles
+  // alone are too few for the chip (15 at K = 320): the d contraction is
+  // split, its fp64 partials summed in order by k_ns_reduce.
+  const int t64 = (K + 63) / 64;
+  const int sp = gram_splits(K, d);
+  if (sp > 1) {
+    const int kslice = (int)(((d + sp - 1) / sp + 31) / 32 * 32);
+    const int spe = (int)((d + kslice - 1) / kslice);
+    hipLaunchKernelGGL(k_gram64<0>, dim3(t64, t64, spe), dim3(256), 0, s, v.Ut, d, v.Ut, d, K, K, (int)d, kslice,
+                       v.rr_gpart, (float*)nullptr, (int64_t)K);
+    hipLaunchKernelGGL(k_ns_reduce, dim3(grid_n((int64_t)K * K)), dim3(256), 0, s, v.rr_gpart, spe, K, v.sub_C);
+  } else {
+    hipLaunchKernelGGL(k_gram64<1>, dim3(t64, t64, 1), dim3(256), 0, s, v.Ut, d, v.Ut, d, K, K, (int)d, (int)d,
+                       (double*)nullptr, v.sub_C, (int64_t)K);
+  }
   gemm_launch<false, 2>(v.sub_C, K, v.Ut, d, v.sub_R, d, K, (int)d, K, p1, 0, v.Ut, nullptr, s);
   hipError_t e = hipMemcpyAsync(v.Ut, v.sub_R, (size_t)K * d * 4, hipMemcpyDeviceToDevice, s);
   if (e != hipSuccess) return e;
