@@ -885,27 +885,34 @@ static void repair_key(uint64_t seed, int64_t t, uint32_t* k0, uint32_t* k1) {
   *k1 = (uint32_t)(seed >> 32) ^ (uint32_t)t ^ 0x4B5A6978u;
 }
 
+// the largest oversampled block: r + r / 4 at the largest subspace rank
+constexpr int kSubMaxBlock = kMaxSubK + kMaxSubK / 4;
+static_assert(kMaxSubK / 4 >= 32, "sub_block takes r + max(32, r / 4)");
+
 // *out = 1 when *gate is set or the K x K Gram S (fp64) is the identity to
 // within kOrthSkip: the rows it came from are orthonormal, and the rest of
 // their CholeskyQR pass is skipped
 __global__ void __launch_bounds__(1024) k_orth_check(const double* __restrict__ S, int K, const int* __restrict__ gate,
                                                      int* __restrict__ out) {
   __shared__ double red[16];
+  __shared__ double rs[kSubMaxBlock];   // 1 / sqrt(S_ii) (0 for a zero row)
   if (*gate) {
     if (threadIdx.x == 0) *out = 1;
     return;
   }
   double mx = 0.0;
+  for (int i = threadIdx.x; i < K; i += blockDim.x) {
+    const double sii = S[(int64_t)i * K + i];
+    rs[i] = sii > 0.0 ? 1.0 / sqrt(sii) : 0.0;
+    mx = fmax(mx, fabs(sii - 1.0));
+  }
+  __syncthreads();
   for (int e = threadIdx.x; e < K * K; e += blockDim.x) {
-    const int i = e / K, j = e % K;
-    const double sij = S[e];
-    if (i == j) {
-      mx = fmax(mx, fabs(sij - 1.0));
-    } else {
-      const double den = S[(int64_t)i * K + i] * S[(int64_t)j * K + j];
-      // a zero row is not orthonormal: no skip
-      mx = fmax(mx, den > 0.0 ? fabs(sij) / sqrt(den) : 1.0);
-    }
+    const int i = e / K, j = e - i * K;
+    if (i == j) continue;
+    const double si = rs[i], sj = rs[j];
+    // a zero row is not orthonormal: no skip
+    mx = fmax(mx, (si > 0.0 && sj > 0.0) ? fabs(S[e]) * si * sj : 1.0);
   }
   mx = wave_max(mx);
   if (lane_id() == 0) red[wave_id()] = mx;
