@@ -43,6 +43,14 @@ E, Algorithm 5):
     gamma applied twice; they are read as the main text's Adam (eq-adam)
     with one gamma.
 
+Storage mode store="bf16" (mixed precision; the paper does not fix a
+precision): the gradients G^(i) and the error buffers E^(i) are held in
+bfloat16.  The gradient used is the bf16 rounding of what the caller passes
+(bf16_round; idempotent on bf16 values), and after step 6 each E^(i) is
+replaced by the bf16 rounding of its fp32 value, so the next step's M^(i) and
+Mbar are formed from the stored (rounded) buffers.  Everything else, U, P, Q,
+Rbar, Ghat, X and the optimizer state, keeps its precision.
+
 Readings where the paper is loose (each listed in the design notes):
   * the residual of Algorithm 3 is written P R^T, dimensionally impossible;
     Algorithm 4's P R^(i) is used;
@@ -183,10 +191,13 @@ class Oracle:
     sub_tol: float = 1e-12
     sub_max_iters: int = 200
     ef: bool = True               # error feedback (False: E stays zero)
+    store: str = "fp32"           # "fp32" | "bf16": storage of G^(i) and E^(i)
     states: list = field(default_factory=list)
     t_next: int = 0
 
     def __post_init__(self):
+        if self.store not in ("fp32", "bf16"):
+            raise ValueError(f"unknown store {self.store!r}")
         if self.opt == "galore_adam":
             if self.select not in ("approx", "lazy") or self.refresh != "compressed":
                 raise ValueError("galore_adam is Algorithm 5: Lazy-SVD selection, compressed refresh steps")
@@ -239,6 +250,8 @@ class Oracle:
         n_w = self.workers
         d, D = min(st.m, st.n), max(st.m, st.n)
         r = min(self.rank, d)
+        if self.store == "bf16":
+            g = bf16_round(g)                                     # G^(i) held in bf16
         gc = np.transpose(g, (0, 2, 1)) if st.right else g        # N x d x D
         ms = gc + st.e if self.ef else gc                         # step 1
         is_refresh = (t % self.tau) == 0                          # step 2
@@ -294,6 +307,8 @@ class Oracle:
         else:
             if self.ef:
                 st.e = ms - np.matmul(p, q)                       # step 6: M^(i) - P Q^(i)
+                if self.store == "bf16":
+                    st.e = bf16_round(st.e)                       # E^(i) held in bf16
             ghat = p @ rbar                                       # step 8
         if self.opt == "galore_adam":                             # Alg. 5, in the subspace
             st.g1 = self.beta1 * st.g1 + (1.0 - self.beta1) * rbar
@@ -336,16 +351,20 @@ class ColumnOracle:
     sampled columns of E^(i), X and the optimizer state follow exactly the
     full oracle's trajectory given the same P at every step, at a cost
     proportional to the sample.  X, S1 and S2 are kept oriented (the
-    transpose of the caller's layout when m > n)."""
+    transpose of the caller's layout when m > n).  store="bf16" rounds the
+    gradient columns and the new residual columns to bf16 as Oracle does."""
 
     def __init__(self, shape, cols, workers, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999, eps=1e-8,
-                 refresh="compressed"):
+                 refresh="compressed", store="fp32"):
         m, n = shape
         d = min(m, n)
         self.cols = np.asarray(cols)
         c = len(self.cols)
         self.opt, self.lr, self.beta1, self.beta2, self.eps = opt, lr, beta1, beta2, eps
         self.refresh = refresh
+        if store not in ("fp32", "bf16"):
+            raise ValueError(f"unknown store {store!r}")
+        self.store = store
         self.e = np.zeros((workers, d, c))
         self.x = np.zeros((d, c))
         self.s1 = np.zeros((d, c))
@@ -355,7 +374,10 @@ class ColumnOracle:
         """g_cols: N x d x c, the sampled oriented columns of this step's
         gradients; p: d x r, this step's P.  Returns the new state (oriented
         columns): E (N x d x c), Ebar, X, S1, S2."""
-        ms = np.asarray(g_cols, dtype=np.float64) + self.e
+        g_cols = np.asarray(g_cols, dtype=np.float64)
+        if self.store == "bf16":
+            g_cols = bf16_round(g_cols)
+        ms = g_cols + self.e
         p = np.asarray(p, dtype=np.float64)
         q = np.matmul(p.T, ms)
         if is_refresh and self.refresh == "full":
@@ -363,6 +385,8 @@ class ColumnOracle:
             ghat = ms.mean(axis=0)
         else:
             self.e = ms - np.matmul(p, q)
+            if self.store == "bf16":
+                self.e = bf16_round(self.e)
             ghat = p @ q.mean(axis=0)
         if self.opt == "msgd":
             self.x, self.s1 = msgd_update(self.x, self.s1, ghat, self.lr, self.beta1)
