@@ -94,10 +94,11 @@ def jacobi_work(kind, d):
     return groups * nr * d * 8.0, groups * 2.0 * nr * nr * d, 0.0, groups * rot * (6 * nr * 3)
 
 
-def group_work(wl, name):
+def group_work(wl, name, esz=4):
     """Algorithmic bytes and flops of ONE launch of a kernel group, averaged
     over the matrices of the workload that launch it: (bytes, fp32 MFMA
-    flops, fp64 MFMA flops, fp64 ALU flops)."""
+    flops, fp64 MFMA flops, fp64 ALU flops).  esz: bytes of one element of G
+    and E (4, or 2 with bf16 storage)."""
     N = wl.workers
     tot = [0.0, 0.0, 0.0, 0.0]
     count = 0
@@ -110,18 +111,18 @@ def group_work(wl, name):
         K = min(r + max(32, r // 4), d)
         w = None
         if name == "ef_mean":
-            w = (4.0 * (N + 2) * mn, 0, 0, 0)
+            w = ((esz * N + 8.0) * mn, 0, 0, 0)
         elif name == "select" and r < d:
             w = (4.0 * (d * D + d * d), 2.0 * d * d * D, 0, 0)
         elif name == "proj":
-            w = (8.0 * N * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
+            w = (2.0 * esz * N * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
         elif name == "resid_opt":
             # G, E read and E written per worker; Mbar read and Ebar written;
             # X and the optimizer state read and written.  Products: P Q^(i)
             # per worker, and Ghat = P Rbar as a product of its own up to rank
             # 128 (above it Ghat is the mean of the workers' products)
             prods = N if r > 128 else N + 1
-            w = ((12.0 * N + 8 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * prods, 0, 0)
+            w = ((3.0 * esz * N + 8 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * prods, 0, 0)
         elif name.startswith("jac_") and not sub:
             w = jacobi_work(name[4:], d)
         elif name.startswith("rr_") and sub:
@@ -139,8 +140,8 @@ def group_work(wl, name):
     return tuple(x / count for x in tot)
 
 
-def roofline_entry(wl, name, total_ms, launches, select="approx"):
-    work = group_work(wl, name)
+def roofline_entry(wl, name, total_ms, launches, select="approx", esz=4):
+    work = group_work(wl, name, esz)
     if work is None or launches == 0 or total_ms <= 0:
         return None
     avg_s = total_ms / 1e3 / launches
@@ -217,17 +218,18 @@ def copy_probe(device):
     print(json.dumps({"copy_probe_bytes": 4 * n, "launches": 3}), flush=True)
 
 
-def step_bytes(wl):
+def step_bytes(wl, esz=4):
     """Algorithmic HBM bytes of one step: per worker read G, read E, write E
-    (12 B/elem) plus the optimizer (16 B/elem MSGD, 24 Adam)."""
+    (12 B/elem, 6 with bf16 storage) plus the optimizer (16 B/elem MSGD, 24
+    Adam)."""
     tot = 0
     for shape in wl.shapes:
         m, n, _, _ = dims(shape)
-        tot += (12 * wl.workers + (24 if wl.opt == "adam" else 16)) * m * n
+        tot += (3 * esz * wl.workers + (24 if wl.opt == "adam" else 16)) * m * n
     return tot
 
 
-def make_pool(wl, pool, device, seed=1234):
+def make_pool(wl, pool, device, seed=1234, store="fp32"):
     import numpy as np
     import torch
     from synth import noise_level, planted_matrix
@@ -241,7 +243,7 @@ def make_pool(wl, pool, device, seed=1234):
         for l, (m, n) in enumerate(wl.shapes):
             g = torch.randn((wl.workers, m, n), generator=gen, device=device, dtype=torch.float32)
             g.mul_(noise_level(wl, l)).add_(planted[l])
-            gs.append(g)
+            gs.append(g.to(torch.bfloat16) if store == "bf16" else g)
         batches.append(gs)
     return batches
 
@@ -272,7 +274,7 @@ def blas_threads():
         return 1
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, store="fp32"):
     """The oracle as it stands, timed on the host: whole oracle steps
     t = 0, 1, ... of the same workload (the full matrices, every worker,
     t = 0 a cold refresh), until `budget_s` of oracle time is spent (at least
@@ -281,7 +283,7 @@ def cpu_baseline(wl, budget_s):
     from oracle.method import Oracle
     from synth import gradient_batch, planted_matrix
     planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
-    orc = Oracle.from_workload(wl)
+    orc = Oracle.from_workload(wl, store=store)
     spent, steps, refresh = 0.0, 0, 0
     while steps == 0 or (spent < budget_s and steps < wl.steps):
         grads = [gradient_batch(wl, l, steps, planted[l]) for l in range(len(wl.shapes))]
@@ -310,6 +312,8 @@ def main():
     ap.add_argument("--select", default="approx", choices=("approx", "exact", "approx_bf16"),
                     help="selection mode (approx: the method's Approx-Top-r in fp32; approx_bf16: its "
                          "products on bf16 roundings of U and Mbar, a mixed-precision mode)")
+    ap.add_argument("--store", default="fp32", choices=("fp32", "bf16"),
+                    help="storage of the gradients and error buffers (bf16: a mixed-precision mode)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy that calibrates the HBM traffic counters")
     args = ap.parse_args()
@@ -337,10 +341,11 @@ def main():
     pool = max(1, min(args.pool, int(40e9 // pool_bytes)))
     print(f"[bench] workload {wl.name}: shapes {list(wl.shapes)[:3]}{'...' if len(wl.shapes) > 3 else ''} "
           f"N={wl.workers} r={wl.rank} tau={wl.tau} opt={wl.opt}; pool {pool}", file=sys.stderr, flush=True)
-    batches = make_pool(wl, pool, dev)
+    batches = make_pool(wl, pool, dev, store=args.store)
+    esz = 2 if args.store == "bf16" else 4
     comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
                           beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, tol=args.tol,
-                          select=args.select, device=dev)
+                          select=args.select, store=args.store, device=dev)
     X = [torch.zeros(m, n, dtype=torch.float32, device=dev) for m, n in wl.shapes]
     torch.cuda.synchronize()
 
@@ -425,7 +430,7 @@ def main():
     kernels = []
     for name in KERNEL_GROUPS:
         if name in prof and prof[name][1]:
-            e = roofline_entry(wl, name, *prof[name], select=args.select)
+            e = roofline_entry(wl, name, *prof[name], select=args.select, esz=esz)
             if e:
                 e["total_ms"] = prof[name][0]
                 kernels.append(e)
@@ -436,19 +441,20 @@ def main():
         roof = {k: dominant[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
         roof["kernel"] = dominant["kernel"]
         roof["avg_us"] = dominant["avg_us"]
-        roof["traffic"] = measured_traffic(wl.name, dominant["kernel"])
+        roof["traffic"] = measured_traffic(wl.name + (":bf16" if args.store == "bf16" else ""), dominant["kernel"])
 
-    eff = step_bytes(wl) / (ms_per_step / 1e3) / 1e9
+    eff = step_bytes(wl, esz) / (ms_per_step / 1e3) / 1e9
     out = {
         "metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms/step",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if args.select != "approx_bf16" else "f32 (selection products on bf16)",
+        "dtype": ("f32" if args.select != "approx_bf16" else "f32 (selection products on bf16)")
+                 + (" (G, E stored bf16)" if args.store == "bf16" else ""),
         "data": "synthetic (planted-spectrum gradients + seeded Gaussian noise, resident in HBM)",
         "config": {"workload": wl.name, "shapes": [list(s) for s in wl.shapes][:4],
                    "num_matrices": len(wl.shapes), "simulated_workers": wl.workers,
                    "rank": wl.rank, "tau": wl.tau, "optimizer": wl.opt,
-                   "refresh_steps_timed": n_refresh, "select": args.select},
+                   "refresh_steps_timed": n_refresh, "select": args.select, "store": args.store},
         "effective_GBps": round(eff, 1),
         "roofline": roof,
         "profiled_ms_per_step": None if prof_ms is None else round(prof_ms, 4),
@@ -464,7 +470,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        sec, nsteps, nref = cpu_baseline(wl, args.cpu_budget)
+        sec, nsteps, nref = cpu_baseline(wl, args.cpu_budget, args.store)
         ncpu, model = host_cpu()
         out["cpu_baseline"] = {
             "value": round(sec * 1e3, 1), "unit": "ms/step", "cores": blas_threads(), "kind": "oracle",

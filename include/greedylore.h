@@ -137,6 +137,15 @@ typedef enum {
 #define GLR_CHECK_FINITE 0x1u  /* scan G for NaN/Inf during the worker mean */
 #define GLR_COLD_START   0x2u  /* start every refresh from U = I instead of the previous U */
 #define GLR_NO_EF        0x4u  /* no error feedback: M^(i) = G^(i), E^(i) and Ebar stay zero */
+/* Mixed-precision storage (the paper fixes no precision): the gradients G^(i)
+ * and the error buffers E^(i) are bfloat16 (the upper half of an IEEE
+ * binary32), halving the bytes of the streaming passes.  Each G element is
+ * widened exactly; the residual M^(i) - P Q^(i) is formed in fp32 and stored
+ * rounded to nearest even; Ebar is the mean of the stored E^(i), so the next
+ * step's M^(i) and Mbar are those of the stored buffers.  U, Q, Rbar, X and
+ * the optimizer state stay fp32.  Steps run through glr_step_bf16.  MSGD and
+ * Adam only (GLR_ERR_INVALID_ARG with GLR_GALORE_ADAM). */
+#define GLR_STORE_BF16   0x8u
 
 typedef struct {
   int64_t m, n;                /* layer matrix shape, caller's row-major layout;
@@ -161,7 +170,7 @@ typedef struct {
   float tol;                   /* Jacobi stop, in (0, 1): every pair of rows of W = U^T Mbar has
                                   |w_p.w_q| <= tol max(|w_p||w_q|, ||w_p|^2 - |w_q|^2|, f^2),
                                   f = 2^-10 max_k |w_k| (cosine and rotation angle below tol) */
-  uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF */
+  uint32_t flags;              /* GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF | GLR_STORE_BF16 */
 } glr_config;
 
 /* Byte offsets into the state blob for one matrix (all 256-byte aligned). */
@@ -169,7 +178,8 @@ typedef struct {
   int64_t m, n, d, D;
   int32_t right;               /* 1 iff m > n (the method works on G^T) */
   int32_t r;                   /* effective rank min(rank, d) */
-  uint64_t off_E;              /* N x m x n fp32: error buffers E^(i), worker-major */
+  uint64_t off_E;              /* N x m x n fp32 (bf16 with GLR_STORE_BF16): error buffers
+                                  E^(i), worker-major */
   uint64_t off_Ebar;           /* m x n fp32: mean over workers of E^(i) */
   uint64_t off_U;              /* d x d fp32: row j holds u_j, the j-th column of U */
   uint64_t off_sigma;          /* d fp32: singular values of Mbar at the last refresh, descending */
@@ -231,6 +241,13 @@ glr_status glr_create_static(const glr_config* cfg, void* d_state, size_t state_
 glr_status glr_step(glr_handle* h, float* const* X, const float* const* G,
                     int64_t t, void* stream);
 
+/* glr_step for a handle created with GLR_STORE_BF16: each G[l] points to N
+ * contiguous m x n bfloat16 gradients (the bit patterns, worker-major), read
+ * only; X stays fp32.  GLR_ERR_INVALID_ARG on a handle without the flag (and
+ * glr_step on one with it). */
+glr_status glr_step_bf16(glr_handle* h, float* const* X, const uint16_t* const* G,
+                         int64_t t, void* stream);
+
 /* Waits for `stream`, reads and clears the device status word (every step
  * since the last call).  Returns, in this order of precedence:
  *   GLR_ERR_NONFINITE      a gradient held NaN/Inf (GLR_CHECK_FINITE); the
@@ -263,7 +280,8 @@ glr_status glr_resume(glr_handle* h, int64_t next_t);
 
 /* Buffers for one matrix's state (glr_read_state / glr_write_state): host or
  * device pointers, any mix; a NULL member is skipped.  Each part has the size
- * and layout glr_mat_layout gives it: E N x m x n, Ebar / S1 / S2 m x n (fp32,
+ * and layout glr_mat_layout gives it: E N x m x n (fp32, or bf16 with
+ * GLR_STORE_BF16), Ebar / S1 / S2 m x n (fp32,
  * the caller's layout), Ut d x d (row j = u_j), sigma and score d fp32, J r
  * int32, Rbar r x D fp32, info 64 int32.  S2 exists for Adam only. */
 typedef struct {

@@ -9,6 +9,9 @@ is no CPU fallback: if the library was not built, load() raises.
     comp = glr.GreedyLore(shapes=[(4096, 4096)], workers=8, rank=64, tau=10)
     comp.step([X], [G], t)          # G: N x m x n fp32 on cuda, X: m x n fp32
 
+With store="bf16" the gradients and error buffers are bfloat16 (G passed as
+torch.bfloat16 tensors; X stays fp32).
+
 `paper_2507_08784_amd.ddp.GreedyLoreHook` drives the same step from a
 DistributedDataParallel communication hook.
 """
@@ -29,11 +32,12 @@ STATUS_NAMES = {
 CHECK_FINITE = 0x1
 COLD_START = 0x2
 NO_EF = 0x4
+STORE_BF16 = 0x8
 EXPORTED = (
     "glr_validate_config", "glr_workspace_bytes", "glr_state_layout", "glr_create", "glr_step",
     "glr_sync_status", "glr_resume", "glr_next_step", "glr_destroy", "glr_status_string",
     "glr_last_error", "glr_profile_enable", "glr_profile_reset", "glr_profile_query",
-    "glr_read_state", "glr_write_state", "glr_create_static",
+    "glr_read_state", "glr_write_state", "glr_create_static", "glr_step_bf16",
 )
 STATIC_SCRATCH_BYTES = 64 << 20
 STATE_PARTS = ("E", "Ebar", "Ut", "sigma", "J", "score", "S1", "S2", "Rbar", "info")
@@ -98,6 +102,7 @@ def load():
         "glr_state_layout": (I32, [P(Config), I32, P(MatLayout)]),
         "glr_create": (I32, [P(Config), VP, ctypes.c_size_t, VP, ctypes.c_size_t, VP, P(VP)]),
         "glr_step": (I32, [VP, P(VP), P(VP), I64, VP]),
+        "glr_step_bf16": (I32, [VP, P(VP), P(VP), I64, VP]),
         "glr_sync_status": (I32, [VP, VP]),
         "glr_resume": (I32, [VP, I64]),
         "glr_next_step": (I32, [VP, P(I64)]),
@@ -162,14 +167,20 @@ class GreedyLore:
 
     def __init__(self, shapes, workers, rank, tau, opt="msgd", lr=0.01, beta1=0.9, beta2=0.999,
                  eps=1e-8, refresh="compressed", select="approx", seed=0, max_sweeps=30,
-                 tol=1e-6, check_finite=False, cold_start=False, ef=True, device="cuda", stream=None):
+                 tol=1e-6, check_finite=False, cold_start=False, ef=True, store="fp32", device="cuda",
+                 stream=None):
         import torch
         self.lib = load()
         self.torch = torch
         self.shapes = [tuple(int(x) for x in s) for s in shapes]
         self.workers = workers
         self.opt = opt
-        flags = (CHECK_FINITE if check_finite else 0) | (COLD_START if cold_start else 0) | (0 if ef else NO_EF)
+        if store not in ("fp32", "bf16"):
+            raise ValueError(f"store must be 'fp32' or 'bf16', not {store!r}")
+        self.store = store
+        self.gdtype = torch.bfloat16 if store == "bf16" else torch.float32
+        flags = ((CHECK_FINITE if check_finite else 0) | (COLD_START if cold_start else 0) | (0 if ef else NO_EF)
+                 | (STORE_BF16 if store == "bf16" else 0))
         self.cfg, self._shape_arr = make_config(self.shapes, workers, rank, tau, opt, lr, beta1,
                                                 beta2, eps, refresh, select, seed, max_sweeps,
                                                 tol, flags)
@@ -202,21 +213,23 @@ class GreedyLore:
 
     # ------------------------------------------------------------------ calls
     def step(self, X, G, t):
-        """One step t on every matrix: X[l] (m x n) is updated in place,
-        G[l] holds the N worker gradients (N x m x n), fp32 on this GPU."""
+        """One step t on every matrix: X[l] (m x n, fp32) is updated in place,
+        G[l] holds the N worker gradients (N x m x n) on this GPU, fp32 (bf16
+        with store="bf16")."""
         n = len(self.shapes)
         xs = (ctypes.c_void_p * n)(*[x.data_ptr() for x in X])
         gs = (ctypes.c_void_p * n)(*[g.data_ptr() for g in G])
         for l, ((m, nn), x, g) in enumerate(zip(self.shapes, X, G)):
-            if x.dtype != self.torch.float32 or g.dtype != self.torch.float32:
-                raise TypeError(f"matrix {l}: X and G must be float32")
+            if x.dtype != self.torch.float32 or g.dtype != self.gdtype:
+                raise TypeError(f"matrix {l}: X must be float32 and G {self.gdtype}")
             if tuple(x.shape) != (m, nn) or tuple(g.shape) != (self.workers, m, nn):
                 raise ValueError(f"matrix {l}: X must be {m}x{nn}, G {self.workers}x{m}x{nn}")
             if not (x.is_contiguous() and g.is_contiguous()):
                 raise ValueError(f"matrix {l}: X and G must be contiguous")
             if x.device != self.device or g.device != self.device:
                 raise ValueError(f"matrix {l}: X and G must live on {self.device}")
-        _check(self.lib.glr_step(self.handle, xs, gs, int(t), self._stream_ptr()), self.handle)
+        fn = self.lib.glr_step_bf16 if self.store == "bf16" else self.lib.glr_step
+        _check(fn(self.handle, xs, gs, int(t), self._stream_ptr()), self.handle)
 
     def sync_status(self):
         return self.lib.glr_sync_status(self.handle, self._stream_ptr())
@@ -284,8 +297,9 @@ class GreedyLore:
         return b.view(dtype)
 
     def E(self, mat):
+        """N x m x n error buffers (bf16 with store="bf16")."""
         L = self.layouts[mat]
-        return self._view(L.off_E, self.workers * L.m * L.n, self.torch.float32).view(self.workers, L.m, L.n)
+        return self._view(L.off_E, self.workers * L.m * L.n, self.gdtype).view(self.workers, L.m, L.n)
 
     def Ebar(self, mat):
         L = self.layouts[mat]

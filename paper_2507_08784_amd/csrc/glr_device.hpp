@@ -36,6 +36,60 @@ __device__ __forceinline__ void buf_st(BufRsrc r, uint32_t off, float x) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), r, (int)off, 0, 0);
 }
 
+// Storage of the gradients and error buffers: fp32, or bfloat16 (the upper
+// half of a binary32) with GLR_STORE_BF16.  A bf16 element widens exactly;
+// a store rounds to nearest even (v_cvt_pk_bf16_f32).
+typedef uint16_t bf16_t;
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+// the value a store of x into ST memory keeps
+template <class ST>
+__device__ __forceinline__ float stored(float x) {
+  if constexpr (sizeof(ST) == 2) return bf16_to_f32(f32_to_bf16(x));
+  else return x;
+}
+__device__ __forceinline__ float ld_e(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_e(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+// elements i .. i + 3 (p + i aligned to four elements)
+__device__ __forceinline__ float4 ld_e4(const float* p, int64_t i) {
+  return *reinterpret_cast<const float4*>(p + i);
+}
+__device__ __forceinline__ float4 ld_e4(const bf16_t* p, int64_t i) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p + i);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xFFFF0000u));
+}
+// the same, streaming (non-temporal)
+__device__ __forceinline__ float4 ld_nt_e4(const float* p, int64_t i) { return load_nt4(p + i); }
+__device__ __forceinline__ float4 ld_nt_e4(const bf16_t* p, int64_t i) {
+  typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+  const u32x2v u = __builtin_nontemporal_load(reinterpret_cast<const u32x2v*>(p + i));
+  return make_float4(__uint_as_float(u[0] << 16), __uint_as_float(u[0] & 0xFFFF0000u), __uint_as_float(u[1] << 16),
+                     __uint_as_float(u[1] & 0xFFFF0000u));
+}
+// buffer access to an ST array of `count` elements by the byte offset `off4`
+// the element would have in an fp32 array (kBufNone >> 1 still lies beyond
+// any bf16 array: count * 2 < 2^31)
+template <class ST>
+__device__ __forceinline__ BufRsrc buf_rsrc_s(const ST* p, int64_t count) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<ST*>(p), (short)0, (int)(count * (int64_t)sizeof(ST)),
+                                           0x00020000);
+}
+template <class ST>
+__device__ __forceinline__ float buf_lde(BufRsrc r, uint32_t off4) {
+  if constexpr (sizeof(ST) == 2)
+    return bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, (int)(off4 >> 1), 0, 0));
+  else
+    return buf_ld(r, off4);
+}
+template <class ST>
+__device__ __forceinline__ void buf_ste(BufRsrc r, uint32_t off4, float x) {
+  if constexpr (sizeof(ST) == 2)
+    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(x), r, (int)(off4 >> 1), 0, 0);
+  else
+    buf_st(r, off4, x);
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
@@ -79,18 +133,20 @@ __device__ __forceinline__ f64x4 mfma64(double a, double b, f64x4 c) {
 __device__ __forceinline__ constexpr int lds_swz(int k) { return 4 * ((k >> 3) & 3); }
 
 // Element (r, k) at base[row(r) * ld + k] (+ base2[...] when fused): the
-// operand is contiguous along k.  Optional row gather through `rows`.
+// operand is contiguous along k.  Optional row gather through `rows`.  ST is
+// the element type in memory (fp32, or bf16 widened as it loads).
 // The transposing LDS store puts eight rows x eight float4 k-groups of a
 // half-wave in one LDS row pair; with the (R + 4)-float row pitch alone
 // those 32 stores meet in 8 banks, and the swizzle spreads them over 32.
-template <int R, int BK, bool FUSED, bool GATHER>
+template <int R, int BK, bool FUSED, bool GATHER, class ST = float>
 struct LoadK {
   static constexpr bool kSwz = true;
   static_assert(R % 16 == 0, "swizzle stays inside the slice");
   static constexpr int KQ = BK / 4;                 // float4s per row slice
   static constexpr int NV = (R * KQ + kThreads - 1) / kThreads;
-  const float* base;
-  const float* base2;
+  static constexpr uintptr_t kAl = 4 * sizeof(ST) - 1;   // alignment of four elements
+  const ST* base;
+  const ST* base2;
   int64_t ld;
   int nrows, K;
   bool vec;
@@ -98,10 +154,10 @@ struct LoadK {
   int rl[NV], kq[NV];
   float4 v[NV];
 
-  __device__ LoadK(const float* b, const float* b2, int64_t ld_, int row0, int nrows_, int K_,
+  __device__ LoadK(const ST* b, const ST* b2, int64_t ld_, int row0, int nrows_, int K_,
                    const int* rows) : base(b), base2(b2), ld(ld_), nrows(nrows_), K(K_) {
-    vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & 15) == 0) &&
-          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & 15) == 0));
+    vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
+          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & kAl) == 0));
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       int idx = threadIdx.x + kThreads * i;
@@ -115,8 +171,8 @@ struct LoadK {
     }
   }
   __device__ __forceinline__ float ld1(int64_t off) const {
-    float x = base[off];
-    if (FUSED) x += base2[off];
+    float x = ld_e(base, off);
+    if (FUSED) x += ld_e(base2, off);
     return x;
   }
   __device__ __forceinline__ void fetch(int k0) {
@@ -127,9 +183,9 @@ struct LoadK {
       if (roff[i] >= 0) {
         int64_t off = roff[i] + k;
         if (vec && k + 3 < K) {
-          x = *reinterpret_cast<const float4*>(base + off);
+          x = ld_e4(base, off);
           if (FUSED) {
-            float4 y = *reinterpret_cast<const float4*>(base2 + off);
+            float4 y = ld_e4(base2, off);
             x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
           }
         } else {
@@ -157,14 +213,15 @@ struct LoadK {
 };
 
 // Element (r, k) at base[krow(k) * ld + r] (+ base2): contiguous along r;
-// krow(k) = rows[k] when GATHER, else k.
-template <int R, int BK, bool FUSED, bool GATHER = false>
+// krow(k) = rows[k] when GATHER, else k.  ST as for LoadK.
+template <int R, int BK, bool FUSED, bool GATHER = false, class ST = float>
 struct LoadR {
   static constexpr bool kSwz = false;
   static constexpr int RQ = R / 4;
   static constexpr int NV = (BK * RQ + kThreads - 1) / kThreads;
-  const float* base;
-  const float* base2;
+  static constexpr uintptr_t kAl = 4 * sizeof(ST) - 1;
+  const ST* base;
+  const ST* base2;
   const int* rows;
   int64_t ld;
   int r0, nr, K;
@@ -172,11 +229,11 @@ struct LoadR {
   int kl[NV], rq[NV];
   float4 v[NV];
 
-  __device__ LoadR(const float* b, const float* b2, int64_t ld_, int r0_, int nr_, int K_,
+  __device__ LoadR(const ST* b, const ST* b2, int64_t ld_, int r0_, int nr_, int K_,
                    const int* rows_ = nullptr)
       : base(b), base2(b2), rows(rows_), ld(ld_), r0(r0_), nr(nr_), K(K_) {
-    vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & 15) == 0) &&
-          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & 15) == 0));
+    vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
+          (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & kAl) == 0));
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       int idx = threadIdx.x + kThreads * i;
@@ -185,8 +242,8 @@ struct LoadR {
     }
   }
   __device__ __forceinline__ float ld1(int64_t off) const {
-    float x = base[off];
-    if (FUSED) x += base2[off];
+    float x = ld_e(base, off);
+    if (FUSED) x += ld_e(base2, off);
     return x;
   }
   __device__ __forceinline__ void fetch(int k0) {
@@ -199,9 +256,9 @@ struct LoadR {
         const int64_t kr = GATHER ? (int64_t)rows[k] : (int64_t)k;
         int64_t off = kr * ld + r;
         if (vec && r + 3 < nr) {
-          x = *reinterpret_cast<const float4*>(base + off);
+          x = ld_e4(base, off);
           if (FUSED) {
-            float4 y = *reinterpret_cast<const float4*>(base2 + off);
+            float4 y = ld_e4(base2, off);
             x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
           }
         } else {

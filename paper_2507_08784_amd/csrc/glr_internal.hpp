@@ -104,12 +104,13 @@ struct MatView {
   int r;                     // effective rank
   int N;                     // workers
   int mat;                   // matrix index (RNG counter)
-  // state
-  float* E;      float* Ebar;  float* Ut;   float* sigma;  int* J;
+  bool st16;                 // G^(i) and E^(i) are bf16 (GLR_STORE_BF16), else fp32
+  // state (E: N x m x n elements of the storage type)
+  void* E;       float* Ebar;  float* Ut;   float* sigma;  int* J;
   float* score;  float* S1;    float* S2;   float* Rbar;   int* info;
   uint32_t* status;
-  // caller buffers
-  float* X;      const float* G;
+  // caller buffers (G: N x m x n elements of the storage type)
+  float* X;      const void* G;
   // workspace
   float* Mbar;   float* Q;     float* Qpart; float* lam_part;
   float* W;      float* Utw;   double* Apk;  double* Apk2; float* Vrot;   double* V64;   int* skip;
@@ -190,6 +191,7 @@ struct GroupPlan {
   const int* first = nullptr;     // kGrpKinds tables of num + 1 first blocks
   int num = 0;
   bool right = false;             // every matrix of the group has the same side, rank and kernel variants
+  bool st16 = false;              // storage type of G and E (the handle's)
   int r = 0;
   size_t topr_lds = 0;            // the largest matrix's top-r sort keys
   int total[kGrpKinds] = {};

@@ -112,8 +112,10 @@ glr_status check_config(const glr_config* c, std::string* why) {
     return bad(GLR_ERR_INVALID_ARG, "GaLore Adam (Algorithm 5) compresses at refresh steps: use GLR_REFRESH_COMPRESSED");
   if (c->max_sweeps < 1) return bad(GLR_ERR_INVALID_ARG, "max_sweeps must be >= 1");
   if (!(c->tol > 0.f && c->tol < 1.f)) return bad(GLR_ERR_INVALID_ARG, "tol must be in (0, 1)");
-  if (c->flags & ~(GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF))
+  if (c->flags & ~(GLR_CHECK_FINITE | GLR_COLD_START | GLR_NO_EF | GLR_STORE_BF16))
     return bad(GLR_ERR_INVALID_ARG, "unknown flag bits");
+  if ((c->flags & GLR_STORE_BF16) && c->opt == GLR_GALORE_ADAM)
+    return bad(GLR_ERR_INVALID_ARG, "GLR_STORE_BF16 applies to MSGD and Adam (GaLore Adam keeps no error buffers)");
   for (int i = 0; i < c->num_mats; ++i) {
     const int64_t m = c->shapes[i].m, n = c->shapes[i].n;
     if (m < 1 || n < 1) return bad(GLR_ERR_SHAPE, fmt("matrix %d: shape %lldx%lld must be positive", i, (long long)m, (long long)n));
@@ -130,6 +132,9 @@ glr_status check_config(const glr_config* c, std::string* why) {
   return GLR_OK;
 }
 
+// bytes of one element of G^(i) and E^(i)
+uint64_t elem_bytes(const glr_config* c) { return (c->flags & GLR_STORE_BF16) ? 2 : 4; }
+
 void mat_layout(const glr_config* c, int mat, uint64_t base, glr_mat_layout* L, uint64_t* end) {
   const Dims x = dims_of(c, mat);
   const uint64_t N = (uint64_t)c->num_workers, mn = (uint64_t)(x.m * x.n);
@@ -142,7 +147,7 @@ void mat_layout(const glr_config* c, int mat, uint64_t base, glr_mat_layout* L, 
   L->m = x.m; L->n = x.n; L->d = x.d; L->D = x.D;
   L->right = x.right ? 1 : 0;
   L->r = x.r;
-  L->off_E = take(N * mn * 4);
+  L->off_E = take(N * mn * elem_bytes(c));
   L->off_Ebar = take(mn * 4);
   L->off_U = take((uint64_t)(x.d * x.d) * 4);
   L->off_sigma = take((uint64_t)x.d * 4);
@@ -384,7 +389,7 @@ glr_status hip_fail(glr_handle* h, hipError_t e, const char* where) {
   return fail(h, GLR_ERR_DEVICE, fmt("%s: %s", where, hipGetErrorString(e)));
 }
 
-MatView view_of(glr_handle* h, int mat, float* X, const float* G, int lane) {
+MatView view_of(glr_handle* h, int mat, float* X, const void* G, int lane) {
   const glr_mat_layout& L = h->lay[mat];
   MatView v;
   v.m = L.m; v.n = L.n; v.d = L.d; v.D = L.D;
@@ -393,7 +398,8 @@ MatView view_of(glr_handle* h, int mat, float* X, const float* G, int lane) {
   v.N = h->cfg.num_workers;
   v.mat = mat;
   char* s = h->state;
-  v.E = (float*)(s + L.off_E);
+  v.st16 = (h->cfg.flags & GLR_STORE_BF16) != 0;
+  v.E = s + L.off_E;
   v.Ebar = (float*)(s + L.off_Ebar);
   v.Ut = (float*)(s + L.off_U);
   v.sigma = (float*)(s + L.off_sigma);
@@ -692,7 +698,7 @@ glr_status step_tail(glr_handle* h, const MatView& v, bool refresh, hipStream_t 
   return GLR_OK;
 }
 
-glr_status step_one(glr_handle* h, int mat, float* X, const float* G, int64_t t, hipStream_t s, int lane) {
+glr_status step_one(glr_handle* h, int mat, float* X, const void* G, int64_t t, hipStream_t s, int lane) {
   const glr_config& c = h->cfg;
   MatView v = view_of(h, mat, X, G, lane);
   const bool refresh = (t % c.tau) == 0;
@@ -770,7 +776,7 @@ glr_status on_lanes(glr_handle* h, hipStream_t s, const MatFn& fn) {
 // converged leaves the launches); then sigma, U and the rest of the step on the
 // lanes.  Each matrix runs the same kernels on the same data as its own
 // refresh, so the results are bitwise those of the per-matrix order.
-glr_status step_joint(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+glr_status step_joint(glr_handle* h, float* const* X, const void* const* G, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   const int num = c.num_mats;
   glr_status st = on_lanes(h, s, [&](int i, int lane, hipStream_t ls) -> glr_status {
@@ -866,7 +872,7 @@ bool joint_allowed(const glr_handle* h) {
 // A selection step of several matrices: the per-step table of views (with
 // this step's X and G) goes up from a pinned slot, then each kernel of the
 // step runs once over all matrices on `s`.
-glr_status step_grouped(glr_handle* h, float* const* X, const float* const* G, int64_t t, hipStream_t s) {
+glr_status step_grouped(glr_handle* h, float* const* X, const void* const* G, int64_t t, hipStream_t s) {
   const glr_config& c = h->cfg;
   const int num = c.num_mats, slot = h->gslot;
   h->gslot ^= 1;
@@ -908,6 +914,7 @@ hipError_t group_setup(glr_handle* h, hipStream_t s) {
   gp.num = num;
   gp.right = h->lay[0].right != 0;
   gp.r = h->lay[0].r;
+  gp.st16 = (h->cfg.flags & GLR_STORE_BF16) != 0;
   std::vector<int> blocks((size_t)num * kGrpKinds);
   for (int i = 0; i < num; ++i) {
     GroupMat g;
@@ -1156,8 +1163,8 @@ glr_status glr_create_static(const glr_config* cfg, void* d_state, size_t state_
   return s;
 }
 
-glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64_t t, void* stream) {
-  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+namespace {
+glr_status step_impl(glr_handle* h, float* const* X, const void* const* G, int64_t t, void* stream) {
   if (h->suspect) return fail(h, GLR_ERR_STATE, "state is suspect after an earlier error; call glr_resume");
   if (t != h->next_t)
     return fail(h, GLR_ERR_STATE, fmt("steps run in order: expected t=%lld, got %lld", (long long)h->next_t, (long long)t));
@@ -1189,6 +1196,21 @@ glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64
   }
   h->next_t = t + 1;
   return GLR_OK;
+}
+}  // namespace
+
+glr_status glr_step(glr_handle* h, float* const* X, const float* const* G, int64_t t, void* stream) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (h->cfg.flags & GLR_STORE_BF16)
+    return fail(h, GLR_ERR_INVALID_ARG, "the handle stores G and E in bf16: call glr_step_bf16");
+  return step_impl(h, X, reinterpret_cast<const void* const*>(G), t, stream);
+}
+
+glr_status glr_step_bf16(glr_handle* h, float* const* X, const uint16_t* const* G, int64_t t, void* stream) {
+  if (!h) return fail(nullptr, GLR_ERR_INVALID_ARG, "handle is NULL");
+  if (!(h->cfg.flags & GLR_STORE_BF16))
+    return fail(h, GLR_ERR_INVALID_ARG, "the handle stores G and E in fp32: call glr_step");
+  return step_impl(h, X, reinterpret_cast<const void* const*>(G), t, stream);
 }
 
 glr_status glr_sync_status(glr_handle* h, void* stream) {
@@ -1235,7 +1257,7 @@ struct StatePart {
 void state_parts(const glr_handle* h, int mat, StatePart (&p)[10]) {
   const glr_mat_layout& L = h->lay[(size_t)mat];
   const uint64_t mn = (uint64_t)(L.m * L.n), N = (uint64_t)h->cfg.num_workers;
-  p[0] = {L.off_E, N * mn * 4};
+  p[0] = {L.off_E, N * mn * elem_bytes(&h->cfg)};
   p[1] = {L.off_Ebar, mn * 4};
   p[2] = {L.off_U, (uint64_t)(L.d * L.d) * 4};
   p[3] = {L.off_sigma, (uint64_t)L.d * 4};

@@ -44,9 +44,11 @@ hipError_t launch_eye(float* Ut, int64_t d, hipStream_t s) {
 
 // ---------------------------------------------------------------------------
 // S1 + S2: Mbar = Ebar + (1/N) sum_i G^(i)   (m x n layout; Ebar is the mean
-// of the workers' error buffers left by the previous step)
+// of the workers' error buffers left by the previous step; G in the storage
+// type ST)
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void ef_mean_at(const float* __restrict__ G, const float* __restrict__ Ebar,
+template <class ST>
+__device__ __forceinline__ void ef_mean_at(const ST* __restrict__ G, const float* __restrict__ Ebar,
                                            float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status, int check,
                                            int64_t bx, int64_t gx) {
   const int64_t stride = (int64_t)gx * blockDim.x;
@@ -56,7 +58,7 @@ __device__ __forceinline__ void ef_mean_at(const float* __restrict__ G, const fl
     for (int64_t i = bx * (int64_t)blockDim.x + threadIdx.x; i < q; i += stride) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int w = 0; w < N; ++w) {
-        float4 g = load_nt4(G + (int64_t)w * mn + 4 * i);
+        float4 g = ld_nt_e4(G, (int64_t)w * mn + 4 * i);
         if (check) bad |= !(isfinite(g.x) && isfinite(g.y) && isfinite(g.z) && isfinite(g.w));
         acc.x += g.x; acc.y += g.y; acc.z += g.z; acc.w += g.w;
       }
@@ -72,7 +74,7 @@ __device__ __forceinline__ void ef_mean_at(const float* __restrict__ G, const fl
     for (int64_t i = bx * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
       float acc = 0.f;
       for (int w = 0; w < N; ++w) {
-        float g = G[(int64_t)w * mn + i];
+        float g = ld_e(G, (int64_t)w * mn + i);
         if (check) bad |= !isfinite(g);
         acc += g;
       }
@@ -81,7 +83,8 @@ __device__ __forceinline__ void ef_mean_at(const float* __restrict__ G, const fl
   }
   if (check && bad) atomicOr(status, 1u);
 }
-__global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__ Ebar,
+template <class ST>
+__global__ void k_ef_mean(const ST* __restrict__ G, const float* __restrict__ Ebar,
                           float* __restrict__ Mbar, int64_t mn, int N, uint32_t* status,
                           int check) {
   ef_mean_at(G, Ebar, Mbar, mn, N, status, check, blockIdx.x, gridDim.x);
@@ -89,8 +92,12 @@ __global__ void k_ef_mean(const float* __restrict__ G, const float* __restrict__
 
 hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
   const int64_t mn = v.m * v.n;
-  hipLaunchKernelGGL(k_ef_mean, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.G, v.Ebar, v.Mbar,
-                     mn, v.N, v.status, check_finite ? 1 : 0);
+  if (v.st16)
+    hipLaunchKernelGGL(k_ef_mean<bf16_t>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, (const bf16_t*)v.G, v.Ebar,
+                       v.Mbar, mn, v.N, v.status, check_finite ? 1 : 0);
+  else
+    hipLaunchKernelGGL(k_ef_mean<float>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, (const float*)v.G, v.Ebar,
+                       v.Mbar, mn, v.N, v.status, check_finite ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -291,10 +298,11 @@ hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
 
 // ---------------------------------------------------------------------------
 // S4: Q^(i) = P^T M^(i), r x D per worker (both orientations), with
-// P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load.
+// P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load (G
+// and E in the storage type ST, widened to fp32 as they load).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
-__device__ __forceinline__ void proj_at(const float* __restrict__ G, const float* __restrict__ E,
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
+__device__ __forceinline__ void proj_at(const ST* __restrict__ G, const ST* __restrict__ E,
                                         const float* __restrict__ Ut, const int* __restrict__ J,
                                         float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice,
                                         int bx, int by, int bz) {
@@ -307,8 +315,8 @@ __device__ __forceinline__ void proj_at(const float* __restrict__ G, const float
   const int64_t k0 = (int64_t)z * kslice;
   const int klen = (int)(d - k0 < kslice ? d - k0 : kslice);
   const int64_t dD = d * D;
-  const float* Gi = G + (int64_t)w * dD;
-  const float* Ei = E + (int64_t)w * dD;
+  const ST* Gi = G + (int64_t)w * dD;
+  const ST* Ei = E + (int64_t)w * dD;
   T tile;
   // fp32 accumulators are added into fp64 ones every 512 terms of the slice
   // (FLUSH), or the slice itself is at most 512 terms
@@ -324,11 +332,11 @@ __device__ __forceinline__ void proj_at(const float* __restrict__ G, const float
   LoadK<BM, 32, false, true> la(Ut + k0, nullptr, d, m0, r, klen, J);
   if (RIGHT) {
     // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
-    LoadK<BN, 32, true, false> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
+    LoadK<BN, 32, true, false, ST> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
     if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
     else tile.run(la, lb, klen, smem);
   } else {
-    LoadR<BN, 32, true> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
+    LoadR<BN, 32, true, false, ST> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
     if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
     else tile.run(la, lb, klen, smem);
   }
@@ -346,15 +354,19 @@ __device__ __forceinline__ void proj_at(const float* __restrict__ G, const float
       }
     }
 }
-template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
 __global__ void __launch_bounds__(256)
-k_proj(const float* __restrict__ G, const float* __restrict__ E, const float* __restrict__ Ut,
+k_proj(const ST* __restrict__ G, const ST* __restrict__ E, const float* __restrict__ Ut,
        const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
-  proj_at<BM, BN, WM, WN, RIGHT, FLUSH>(G, E, Ut, J, Qpart, d, D, r, N, kslice, blockIdx.x, blockIdx.y, blockIdx.z);
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST>(G, E, Ut, J, Qpart, d, D, r, N, kslice, blockIdx.x, blockIdx.y,
+                                            blockIdx.z);
 }
 
-hipError_t launch_proj(const MatView& v, hipStream_t s) {
+template <class ST>
+static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
   const int r = v.r;
+  const ST* G = static_cast<const ST*>(v.G);
+  const ST* E = static_cast<const ST*>(v.E);
   const int splits = proj_splits(v.d, v.D, r, v.N);
   const int64_t kslice = r > kProjWideRank ? kProjWideSlice
                                            : ((v.d + splits - 1) / splits + 31) / 32 * 32;
@@ -366,10 +378,10 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
     grid.x = (unsigned)((v.D + BN - 1) / BN);                                                     \
     grid.y = (unsigned)((r + BM - 1) / BM);                                                       \
     if (v.right)                                                                                  \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL>), grid, dim3(kThreads), 0, s, v.G, v.E, \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL, ST>), grid, dim3(kThreads), 0, s, G, E, \
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
     else                                                                                          \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL>), grid, dim3(kThreads), 0, s, v.G, v.E,\
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL, ST>), grid, dim3(kThreads), 0, s, G, E,\
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
   } while (0)
   // 64 < r <= 128 takes two 64-row rank tiles (G and E read twice): the
@@ -380,6 +392,9 @@ hipError_t launch_proj(const MatView& v, hipStream_t s) {
   else GLR_PROJ(256, 64, 4, 1, false);
 #undef GLR_PROJ
   return hipGetLastError();
+}
+hipError_t launch_proj(const MatView& v, hipStream_t s) {
+  return v.st16 ? launch_proj_st<bf16_t>(v, s) : launch_proj_st<float>(v, s);
 }
 
 // S6 (with the slices of the projection): Q^(i) = sum over slices of the
@@ -421,7 +436,8 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 //   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
 //   E^(i) <- (G^(i) - C^(i)) + E^(i)
 //   Ghat  = P Rbar;  Ebar = Mbar - Ghat (the mean of the E^(i) by
-//   linearity);  optimizer on X with Ghat.
+//   linearity; with bf16 storage the mean of the stored, rounded E^(i));
+//   optimizer on X with Ghat.
 // MFMA rows are tile rows and lanes are tile columns, so that a load or
 // store of one accumulator register moves two whole 128-byte rows of 32
 // columns: every written line of E, X, the optimizer state and Ebar is
@@ -429,8 +445,8 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // fetch the line first).  P (gathered rows of U^T) and Q^(i) are staged
 // through LDS by the tile engine, 32 rank indices at a time.
 // ---------------------------------------------------------------------------
-template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
-__device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float* __restrict__ E,
+template <int OPT, bool RIGHT, int ROWS, int RO_COLS, class ST>
+__device__ __forceinline__ void resid_opt_at(const ST* __restrict__ G, ST* __restrict__ E,
                                              float* __restrict__ Ebar,
             const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
             const float* __restrict__ Ut,
@@ -461,9 +477,18 @@ __device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float*
       const int64_t row = r0 + geo.row(tm, v);
       ob[tm][v] = (cok && row < m) ? (uint32_t)((row * n + cc) * 4) : kBufNone;
     }
+  // with bf16 storage Ebar is the mean of the stored residuals
+  constexpr bool B16 = sizeof(ST) == 2;
+  float esum[B16 ? TM : 1][16];
+  if (B16) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) esum[B16 ? tm : 0][v] = 0.f;
+  }
   for (int wk = 0; wk < N; ++wk) {
-    const BufRsrc Gi = buf_rsrc(G + (int64_t)wk * mn, bytes);
-    const BufRsrc Ei = buf_rsrc(E + (int64_t)wk * mn, bytes);
+    const BufRsrc Gi = buf_rsrc_s(G + (int64_t)wk * mn, mn);
+    const BufRsrc Ei = buf_rsrc_s(E + (int64_t)wk * mn, mn);
     const float* Qi = Q + (int64_t)wk * r * D;
     // G^(i) and E^(i) for this lane's elements, in flight during the product
     float gv[TM][16], eo[TM][16];
@@ -471,8 +496,8 @@ __device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float*
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        gv[tm][v] = buf_ld(Gi, ob[tm][v]);
-        eo[tm][v] = buf_ld(Ei, ob[tm][v]);
+        gv[tm][v] = buf_lde<ST>(Gi, ob[tm][v]);
+        eo[tm][v] = buf_lde<ST>(Ei, ob[tm][v]);
       }
     T tile;
     if (!RIGHT) {
@@ -491,7 +516,9 @@ __device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float*
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         // (G - P Q) + E: G and P Q nearly cancel, E is the small part
-        buf_st(Ei, ob[tm][v], (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v]);
+        const float e = (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v];
+        buf_ste<ST>(Ei, ob[tm][v], e);
+        if (B16) esum[B16 ? tm : 0][v] += stored<ST>(e);
       }
   }
 
@@ -532,7 +559,8 @@ __device__ __forceinline__ void resid_opt_at(const float* __restrict__ G, float*
         }
         buf_st(S1r, o, s1);
       }
-      buf_st(Ebr, o, op.ef ? buf_ld(Mr, o) - gh : 0.0f);
+      const float eb = B16 ? esum[B16 ? tm : 0][v] / (float)(N > 0 ? N : 1) : buf_ld(Mr, o) - gh;
+      buf_st(Ebr, o, op.ef ? eb : 0.0f);
       buf_st(Xr, o, xv);
     }
 }
@@ -544,61 +572,20 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
             const int* __restrict__ J,
             float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2, int64_t m,
             int64_t n, int64_t d, int64_t D, int r, int N, OptParams op) {
-  resid_opt_at<OPT, RIGHT, ROWS, RO_COLS>(G, E, Ebar, Mbar, Q, Rbar, Ut, J, X, S1, S2, m, n, d, D, r, N, op,
-                                          blockIdx.x, blockIdx.y);
+  resid_opt_at<OPT, RIGHT, ROWS, RO_COLS, float>(G, E, Ebar, Mbar, Q, Rbar, Ut, J, X, S1, S2, m, n, d, D, r, N,
+                                                 op, blockIdx.x, blockIdx.y);
 }
-
-// S5 above rank 128, where the rank-r products dominate: 128 x 128 tiles
-// (64 x 64 per wave), one worker after the other, E^(w) <- (G^(w) - P Q^(w))
-// + E^(w) streamed 16 elements per lane at a time after each product;
-// k_resid_opt then runs with no workers (Ghat, Ebar and the optimizer).
-
-template <bool RIGHT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
-k_resid_wide(const float* __restrict__ G, float* __restrict__ E, const float* __restrict__ Q,
-             const float* __restrict__ Ut, const int* __restrict__ J, int64_t m, int64_t n, int64_t d,
-             int64_t D, int r, int N) {
-  using T = MfmaTile<128, 128, 2, 2>;
-  __shared__ __align__(16) float smem[T::LDS_FLOATS];
-  const int c0 = blockIdx.x * 128, r0 = blockIdx.y * 128;
-  const int64_t mn = m * n;
-  const uint32_t bytes = (uint32_t)(mn * 4);
-  for (int wk = 0; wk < N; ++wk) {
-    const float* Qi = Q + (int64_t)wk * r * D;
-    T tile;
-    if (!RIGHT) {
-      // rows a < d, columns b < D: C[a][b] = sum_k Ut[J[k]][a] Q[k][b]
-      LoadR<128, 32, false, true> la(Ut, nullptr, d, r0, (int)d, r, J);
-      LoadR<128, 32, false> lb(Qi, nullptr, D, c0, (int)D, r);
-      tile.run(la, lb, r, smem);
-    } else {
-      // rows b < D, columns a < d: C[b][a] = sum_k Q[k][b] Ut[J[k]][a]
-      LoadR<128, 32, false> la(Qi, nullptr, D, r0, (int)D, r);
-      LoadR<128, 32, false, true> lb(Ut, nullptr, d, c0, (int)d, r, J);
-      tile.run(la, lb, r, smem);
-    }
-    const BufRsrc Gw = buf_rsrc(G + (int64_t)wk * mn, bytes);
-    const BufRsrc Ew = buf_rsrc(E + (int64_t)wk * mn, bytes);
-#pragma unroll
-    for (int tm = 0; tm < T::TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < T::TN; ++tn) {
-        const int64_t col = c0 + tile.col(tn);
-        uint32_t ob[16];
-        float gv[16], eo[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int64_t row = r0 + tile.row(tm, v);
-          ob[v] = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
-          gv[v] = buf_ld(Gw, ob[v]);
-          eo[v] = buf_ld(Ew, ob[v]);
-        }
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          // (G - P Q) + E: G and P Q nearly cancel, E is the small part
-          buf_st(Ew, ob[v], (gv[v] - tile.acc[tm][tn][v]) + eo[v]);
-      }
-  }
+// the same with bf16 storage: the stored residuals' running sum (for Ebar)
+// takes 32 more registers per lane, so three waves per SIMD instead of four
+template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
+k_resid_opt16(const bf16_t* __restrict__ G, bf16_t* __restrict__ E, float* __restrict__ Ebar,
+              const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
+              const float* __restrict__ Ut, const int* __restrict__ J, float* __restrict__ X,
+              float* __restrict__ S1, float* __restrict__ S2, int64_t m, int64_t n, int64_t d, int64_t D, int r,
+              int N, OptParams op) {
+  resid_opt_at<OPT, RIGHT, ROWS, RO_COLS, bf16_t>(G, E, Ebar, Mbar, Q, Rbar, Ut, J, X, S1, S2, m, n, d, D, r, N,
+                                                  op, blockIdx.x, blockIdx.y);
 }
 
 // S5 + S7 + S8 above rank 128, the workers side by side: one 64 x 64 output
@@ -608,14 +595,14 @@ k_resid_wide(const float* __restrict__ G, float* __restrict__ E, const float* __
 // worker, so that the MFMAs run back to back over the whole rank-r
 // contraction.  Then E^(w) <- (G^(w) - P Q^(w)) + E^(w) for each worker,
 // Ghat = (1/N) sum_w P Q^(w) (= P Rbar by linearity, with no product of its
-// own), Ebar = Mbar - Ghat and the optimizer on X.  More than kNW workers
-// take several groups (MULTI), the products of the earlier groups summed in
-// registers.
+// own), Ebar = Mbar - Ghat (with bf16 storage the mean of the stored
+// residuals) and the optimizer on X.  More than kNW workers take several
+// groups (MULTI), the products of the earlier groups summed in registers.
 constexpr int kNW = 4;
 constexpr int kNWTile = 64;
-template <int OPT, bool RIGHT, bool MULTI>
+template <int OPT, bool RIGHT, bool MULTI, class ST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
-k_resid_nw(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
+k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Ebar,
            const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Ut,
            const int* __restrict__ J, float* __restrict__ X, float* __restrict__ S1, float* __restrict__ S2,
            int64_t m, int64_t n, int64_t d, int64_t D, int r, int N, OptParams op, int rows_fast) {
@@ -640,6 +627,12 @@ k_resid_nw(const float* __restrict__ G, float* __restrict__ E, float* __restrict
   if (MULTI) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) gs[MULTI ? v : 0] = 0.f;
+  }
+  constexpr bool B16 = sizeof(ST) == 2;
+  float esum[B16 ? 16 : 1];
+  if (B16) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) esum[B16 ? v : 0] = 0.f;
   }
   f32x16 acc[kNW];
   const int64_t rD = (int64_t)r * D;
@@ -704,21 +697,23 @@ k_resid_nw(const float* __restrict__ G, float* __restrict__ E, float* __restrict
 #pragma unroll
     for (int w = 0; w < kNW; ++w) {
       if (w >= nw) break;
-      const BufRsrc Gw = buf_rsrc(G + (int64_t)(w0 + w) * mn, bytes);
-      const BufRsrc Ew = buf_rsrc(E + (int64_t)(w0 + w) * mn, bytes);
+      const BufRsrc Gw = buf_rsrc_s(G + (int64_t)(w0 + w) * mn, mn);
+      const BufRsrc Ew = buf_rsrc_s(E + (int64_t)(w0 + w) * mn, mn);
       uint32_t ob[16];
       float gv[16], eo[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int64_t row = r0 + wm * 32 + mfma32_row(v, lane);
         ob[v] = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
-        gv[v] = buf_ld(Gw, ob[v]);
-        eo[v] = buf_ld(Ew, ob[v]);
+        gv[v] = buf_lde<ST>(Gw, ob[v]);
+        eo[v] = buf_lde<ST>(Ew, ob[v]);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         // (G - P Q) + E: G and P Q nearly cancel, E is the small part
-        buf_st(Ew, ob[v], (gv[v] - acc[w][v]) + eo[v]);
+        const float e = (gv[v] - acc[w][v]) + eo[v];
+        buf_ste<ST>(Ew, ob[v], e);
+        if (B16) esum[B16 ? v : 0] += stored<ST>(e);
         if (MULTI) gs[MULTI ? v : 0] += acc[w][v];
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -748,50 +743,55 @@ k_resid_nw(const float* __restrict__ G, float* __restrict__ E, float* __restrict
       buf_st(S2r, o, s2);
     }
     buf_st(S1r, o, s1);
-    buf_st(Ebr, o, buf_ld(Mr, o) - gh);
+    buf_st(Ebr, o, B16 ? esum[B16 ? v : 0] * inv_n : buf_ld(Mr, o) - gh);
     buf_st(Xr, o, xv);
     if ((v & 3) == 3) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
-  const bool wide = v.r > kResidWideRank && o.ef;
-  if (wide && o.opt != 2) {
-    // MSGD / Adam with error feedback: one fused pass
+template <class ST>
+static hipError_t launch_resid_opt_st(const MatView& v, const OptParams& o, hipStream_t s) {
+  const ST* G = static_cast<const ST*>(v.G);
+  ST* E = static_cast<ST*>(v.E);
+  if (v.r > kResidWideRank && o.ef) {
+    // MSGD / Adam with error feedback above rank 128 (GaLore runs without
+    // error feedback): one fused pass with the workers side by side
     const bool multi = v.N > kNW;
     const unsigned rt = (unsigned)((v.m + kNWTile - 1) / kNWTile), ct = (unsigned)((v.n + kNWTile - 1) / kNWTile);
     const int rows_fast = ct <= 65535u ? 1 : 0;
     dim3 gw(rows_fast ? rt : ct, rows_fast ? ct : rt);
-#define GLR_RW(OPT, R, MU)                                                                                 \
-  hipLaunchKernelGGL((k_resid_nw<OPT, R, MU>), gw, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, v.Q, v.Ut, v.J, \
+#define GLR_RW(OPT, R, MU)                                                                                   \
+  hipLaunchKernelGGL((k_resid_nw<OPT, R, MU, ST>), gw, dim3(kThreads), 0, s, G, E, v.Ebar, v.Mbar, v.Q, v.Ut, v.J, \
                      v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o, rows_fast)
 #define GLR_RW2(OPT, R) do { if (multi) GLR_RW(OPT, R, true); else GLR_RW(OPT, R, false); } while (0)
-    if (o.opt == 0) { if (v.right) GLR_RW2(0, true); else GLR_RW2(0, false); }
-    else            { if (v.right) GLR_RW2(1, true); else GLR_RW2(1, false); }
+    if (o.opt == 0)      { if (v.right) GLR_RW2(0, true); else GLR_RW2(0, false); }
+    else if (o.opt == 1) { if (v.right) GLR_RW2(1, true); else GLR_RW2(1, false); }
+    else return hipErrorInvalidValue;
 #undef GLR_RW2
 #undef GLR_RW
     return hipGetLastError();
   }
-  if (wide) {
-    dim3 gw((unsigned)((v.n + 127) / 128), (unsigned)((v.m + 127) / 128));
-    if (v.right)
-      hipLaunchKernelGGL(k_resid_wide<true>, gw, dim3(kThreads), 0, s, v.G, v.E, v.Q, v.Ut, v.J, v.m, v.n,
-                         v.d, v.D, v.r, v.N);
-    else
-      hipLaunchKernelGGL(k_resid_wide<false>, gw, dim3(kThreads), 0, s, v.G, v.E, v.Q, v.Ut, v.J, v.m, v.n,
-                         v.d, v.D, v.r, v.N);
-  }
-  const int nfused = (wide || !o.ef) ? 0 : v.N;   // workers whose residual k_resid_opt updates
+  const int nfused = o.ef ? v.N : 0;   // workers whose residual k_resid_opt updates
   constexpr int rows = 64, cols = 64;
   dim3 grid((unsigned)((v.n + cols - 1) / cols), (unsigned)((v.m + rows - 1) / rows));
-#define GLR_RO(OPT, R)                                                                               \
-  hipLaunchKernelGGL((k_resid_opt<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, v.G, v.E, v.Ebar, v.Mbar, \
-                     v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, nfused, o)
+#define GLR_RO(OPT, R)                                                                                     \
+  do {                                                                                                     \
+    if constexpr (sizeof(ST) == 2)                                                                         \
+      hipLaunchKernelGGL((k_resid_opt16<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, G, E, v.Ebar,    \
+                         v.Mbar, v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, nfused, o); \
+    else                                                                                                   \
+      hipLaunchKernelGGL((k_resid_opt<OPT, R, rows, cols>), grid, dim3(kThreads), 0, s, G, E, v.Ebar,      \
+                         v.Mbar, v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, nfused, o); \
+  } while (0)
   if (o.opt == 0)      { if (v.right) GLR_RO(0, true); else GLR_RO(0, false); }
   else if (o.opt == 1) { if (v.right) GLR_RO(1, true); else GLR_RO(1, false); }
-  else                 { if (v.right) GLR_RO(2, true); else GLR_RO(2, false); }
+  else if (sizeof(ST) == 2) return hipErrorInvalidValue;   // GaLore runs on fp32 storage only
+  else { if (v.right) GLR_RO(2, true); else GLR_RO(2, false); }
 #undef GLR_RO
   return hipGetLastError();
+}
+hipError_t launch_resid_opt(const MatView& v, const OptParams& o, hipStream_t s) {
+  return v.st16 ? launch_resid_opt_st<bf16_t>(v, o, s) : launch_resid_opt_st<float>(v, o, s);
 }
 
 // Algorithm 5 (distributed Adam-type GaLore): the Adam moments live in the
@@ -821,15 +821,15 @@ hipError_t launch_galore_adam(const MatView& v, const OptParams& o, bool reset, 
 }
 
 // Algorithm 3 at a refresh step: E^(i) = 0, Ebar = 0, Ghat = Mbar.
-template <int OPT>
-__global__ void k_full_refresh(const float* __restrict__ Mbar, float* __restrict__ E,
+template <int OPT, class ST>
+__global__ void k_full_refresh(const float* __restrict__ Mbar, ST* __restrict__ E,
                                float* __restrict__ Ebar, float* __restrict__ X,
                                float* __restrict__ S1, float* __restrict__ S2, int64_t mn, int N,
                                OptParams op) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < mn; i += stride) {
     const float gh = Mbar[i];
-    for (int w = 0; w < N; ++w) E[(int64_t)w * mn + i] = 0.f;
+    for (int w = 0; w < N; ++w) E[(int64_t)w * mn + i] = ST(0);
     Ebar[i] = 0.f;
     float x = X[i];
     if (OPT == 0) {
@@ -847,15 +847,20 @@ __global__ void k_full_refresh(const float* __restrict__ Mbar, float* __restrict
   }
 }
 
-hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s) {
+template <class ST>
+static hipError_t launch_full_refresh_st(const MatView& v, const OptParams& o, hipStream_t s) {
   const int64_t mn = v.m * v.n;
+  ST* E = static_cast<ST*>(v.E);
   if (o.opt == 0)
-    hipLaunchKernelGGL(k_full_refresh<0>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, v.E,
+    hipLaunchKernelGGL((k_full_refresh<0, ST>), dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, E,
                        v.Ebar, v.X, v.S1, v.S2, mn, v.N, o);
   else
-    hipLaunchKernelGGL(k_full_refresh<1>, dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, v.E,
+    hipLaunchKernelGGL((k_full_refresh<1, ST>), dim3(grid_for(mn, 4)), dim3(kThreads), 0, s, v.Mbar, E,
                        v.Ebar, v.X, v.S1, v.S2, mn, v.N, o);
   return hipGetLastError();
+}
+hipError_t launch_full_refresh(const MatView& v, const OptParams& o, hipStream_t s) {
+  return v.st16 ? launch_full_refresh_st<bf16_t>(v, o, s) : launch_full_refresh_st<float>(v, o, s);
 }
 
 
@@ -889,10 +894,12 @@ __device__ __forceinline__ int dev_next_pow2(int64_t x) {
   else if (r <= kProjWideRank) X(64, 64, 2, 2, true);       \
   else X(256, 64, 4, 1, false)
 
+template <class ST>
 __global__ void k_g_ef_mean(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, int check) {
   const int m = group_find(first, num, blockIdx.x);
   const MatView& v = gm[m].v;
-  ef_mean_at(v.G, v.Ebar, v.Mbar, v.m * v.n, v.N, v.status, check, blockIdx.x - first[m], first[m + 1] - first[m]);
+  ef_mean_at(static_cast<const ST*>(v.G), v.Ebar, v.Mbar, v.m * v.n, v.N, v.status, check, blockIdx.x - first[m],
+             first[m + 1] - first[m]);
 }
 
 template <bool RIGHT, bool APPROX, bool BF16>
@@ -918,7 +925,7 @@ __global__ void __launch_bounds__(1024) k_g_topr(const GroupMat* __restrict__ gm
   topr_at(v.score, (int)v.d, v.r, dev_next_pow2(v.d < 2 ? 2 : v.d), v.J, dyn);
 }
 
-template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH>
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
 __global__ void __launch_bounds__(256)
 k_g_proj(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num) {
   const int m = group_find(first, num, blockIdx.x);
@@ -926,8 +933,9 @@ k_g_proj(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num
   const MatView& v = g.v;
   const int gx = (int)((v.D + BN - 1) / BN), gy = (v.r + BM - 1) / BM;
   const int local = blockIdx.x - first[m], rest = local / gx;
-  proj_at<BM, BN, WM, WN, RIGHT, FLUSH>(v.G, v.E, v.Ut, v.J, g.splits > 1 ? v.Qpart : v.Q, v.d, v.D, v.r, v.N,
-                                        g.kslice, local % gx, rest % gy, rest / gy);
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST>(static_cast<const ST*>(v.G), static_cast<const ST*>(v.E), v.Ut, v.J,
+                                            g.splits > 1 ? v.Qpart : v.Q, v.d, v.D, v.r, v.N, g.kslice, local % gx,
+                                            rest % gy, rest / gy);
 }
 
 __global__ void k_g_rbar(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num) {
@@ -938,14 +946,25 @@ __global__ void k_g_rbar(const GroupMat* __restrict__ gm, const int* __restrict_
                  first[m + 1] - first[m]);
 }
 
-template <int OPT, bool RIGHT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
-k_g_resid_opt(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, OptParams op) {
+template <int OPT, bool RIGHT, class ST>
+__device__ __forceinline__ void g_resid_opt_at(const GroupMat* __restrict__ gm, const int* __restrict__ first,
+                                               int num, const OptParams& op) {
   const int m = group_find(first, num, blockIdx.x);
   const MatView& v = gm[m].v;
   const int local = blockIdx.x - first[m], gx = (int)((v.n + 63) / 64);
-  resid_opt_at<OPT, RIGHT, 64, 64>(v.G, v.E, v.Ebar, v.Mbar, v.Q, v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d,
-                                   v.D, v.r, v.N, op, local % gx, local / gx);
+  resid_opt_at<OPT, RIGHT, 64, 64, ST>(static_cast<const ST*>(v.G), static_cast<ST*>(v.E), v.Ebar, v.Mbar, v.Q,
+                                       v.Rbar, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, op,
+                                       local % gx, local / gx);
+}
+template <int OPT, bool RIGHT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+k_g_resid_opt(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, OptParams op) {
+  g_resid_opt_at<OPT, RIGHT, float>(gm, first, num, op);
+}
+template <int OPT, bool RIGHT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
+k_g_resid_opt16(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, OptParams op) {
+  g_resid_opt_at<OPT, RIGHT, bf16_t>(gm, first, num, op);
 }
 
 void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]) {
@@ -965,14 +984,15 @@ void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]) {
   blocks[kGrpResid] = (int)(((v.n + 63) / 64) * ((v.m + 63) / 64));
 }
 
-hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
-                               int64_t t, const OptParams& o, hipStream_t s) {
+template <class ST>
+static hipError_t launch_group_select_st(const GroupPlan& gp, bool check_finite, bool approx, bool bf16,
+                                         uint64_t seed, int64_t t, const OptParams& o, hipStream_t s) {
   if (bf16 && !approx) return hipErrorInvalidValue;
   const int num = gp.num, r = gp.r;
   const bool right = gp.right;
   auto table = [&](int kind) { return gp.first + (int64_t)kind * (num + 1); };
   auto grid = [&](int kind) { return dim3((unsigned)gp.total[kind]); };
-  hipLaunchKernelGGL(k_g_ef_mean, grid(kGrpEfMean), dim3(kThreads), 0, s, gp.gm, table(kGrpEfMean), num,
+  hipLaunchKernelGGL(k_g_ef_mean<ST>, grid(kGrpEfMean), dim3(kThreads), 0, s, gp.gm, table(kGrpEfMean), num,
                      check_finite ? 1 : 0);
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
@@ -995,22 +1015,33 @@ hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool appr
 #define GLR_GPROJ(BM, BN, WM, WN, FL)                                                                       \
   do {                                                                                                      \
     if (right)                                                                                              \
-      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, true, FL>), grid(kGrpProj), dim3(kThreads), 0, s, gp.gm, \
-                         table(kGrpProj), num);                                                             \
+      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, true, FL, ST>), grid(kGrpProj), dim3(kThreads), 0, s,    \
+                         gp.gm, table(kGrpProj), num);                                                      \
     else                                                                                                    \
-      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, false, FL>), grid(kGrpProj), dim3(kThreads), 0, s, gp.gm,\
-                         table(kGrpProj), num);                                                             \
+      hipLaunchKernelGGL((k_g_proj<BM, BN, WM, WN, false, FL, ST>), grid(kGrpProj), dim3(kThreads), 0, s,   \
+                         gp.gm, table(kGrpProj), num);                                                      \
   } while (0)
   GLR_PROJ_TIERS(GLR_GPROJ);
 #undef GLR_GPROJ
   hipLaunchKernelGGL(k_g_rbar, grid(kGrpRbar), dim3(kThreads), 0, s, gp.gm, table(kGrpRbar), num);
 #define GLR_GRO(OPT, R)                                                                                     \
-  hipLaunchKernelGGL((k_g_resid_opt<OPT, R>), grid(kGrpResid), dim3(kThreads), 0, s, gp.gm, table(kGrpResid), \
-                     num, o)
+  do {                                                                                                      \
+    if constexpr (sizeof(ST) == 2)                                                                          \
+      hipLaunchKernelGGL((k_g_resid_opt16<OPT, R>), grid(kGrpResid), dim3(kThreads), 0, s, gp.gm,           \
+                         table(kGrpResid), num, o);                                                         \
+    else                                                                                                    \
+      hipLaunchKernelGGL((k_g_resid_opt<OPT, R>), grid(kGrpResid), dim3(kThreads), 0, s, gp.gm,             \
+                         table(kGrpResid), num, o);                                                         \
+  } while (0)
   if (o.opt == 0) { if (right) GLR_GRO(0, true); else GLR_GRO(0, false); }
   else            { if (right) GLR_GRO(1, true); else GLR_GRO(1, false); }
 #undef GLR_GRO
   return hipGetLastError();
+}
+hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
+                               int64_t t, const OptParams& o, hipStream_t s) {
+  return gp.st16 ? launch_group_select_st<bf16_t>(gp, check_finite, approx, bf16, seed, t, o, s)
+                 : launch_group_select_st<float>(gp, check_finite, approx, bf16, seed, t, o, s);
 }
 
 }  // namespace glr

@@ -16,7 +16,7 @@ HEADER = os.path.join(ROOT, "include", "greedylore.h")
 def _declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(glr_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(glr_[a-z_0-9]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():
@@ -47,7 +47,8 @@ def test_valid_config():
     (dict(lr=0.0), 1), (dict(lr=float("nan")), 1), (dict(beta1=1.0), 1), (dict(beta1=-0.1), 1),
     (dict(opt="adam", beta2=1.0), 1), (dict(opt="adam", eps=0.0), 1), (dict(refresh=5), 1),
     (dict(select=4), 1), (dict(opt="galore_adam", refresh="full"), 1), (dict(max_sweeps=0), 1), (dict(tol=0.0), 1), (dict(tol=1.0), 1),
-    (dict(flags=0x80), 1), (dict(shapes=[(0, 5)]), 2), (dict(shapes=[(5, -1)]), 2),
+    (dict(flags=0x80), 1), (dict(opt="galore_adam", flags=glr.STORE_BF16), 1),
+    (dict(shapes=[(0, 5)]), 2), (dict(shapes=[(5, -1)]), 2),
     (dict(shapes=[(9000, 9000)]), 2), (dict(shapes=[(2000, 3000)], rank=2000), 2),
     (dict(shapes=[(8192, 1 << 17)]), 2),   # m n = 2^30: beyond 32-bit byte offsets
 ])
@@ -84,23 +85,26 @@ def test_create_rejects_bad_buffers_without_touching_the_device():
 def test_step_and_status_reject_null_handle():
     lib = glr.load()
     assert lib.glr_step(None, None, None, 0, None) == 1
+    assert lib.glr_step_bf16(None, None, None, 0, None) == 1
     assert lib.glr_sync_status(None, None) == 1
     assert lib.glr_resume(None, 0) == 1
     assert lib.glr_destroy(None) == 0
     assert lib.glr_status_string(4) == b"invalid state"
 
 
-@pytest.mark.parametrize("opt", ["msgd", "adam"])
-def test_layout_is_aligned_disjoint_and_sized(opt):
+@pytest.mark.parametrize("opt,store", [("msgd", "fp32"), ("adam", "fp32"), ("adam", "bf16")])
+def test_layout_is_aligned_disjoint_and_sized(opt, store):
     shapes = [(96, 160), (170, 66), (1, 37), (4096, 11008)]
-    cfg, _keep = glr.make_config(shapes, workers=3, rank=8, tau=4, opt=opt)
+    esz = 2 if store == "bf16" else 4
+    cfg, _keep = glr.make_config(shapes, workers=3, rank=8, tau=4, opt=opt,
+                                 flags=glr.STORE_BF16 if store == "bf16" else 0)
     sb, wb = glr.workspace_bytes(cfg)
     spans = [(0, 256)]
     for i, (m, n) in enumerate(shapes):
         L = glr.state_layout(cfg, i)
         d, D = min(m, n), max(m, n)
         assert (L.m, L.n, L.d, L.D, L.right, L.r) == (m, n, d, D, int(m > n), min(8, d))
-        parts = [(L.off_E, 3 * m * n * 4), (L.off_Ebar, m * n * 4), (L.off_U, d * d * 4),
+        parts = [(L.off_E, 3 * m * n * esz), (L.off_Ebar, m * n * 4), (L.off_U, d * d * 4),
                  (L.off_sigma, d * 4), (L.off_J, L.r * 4), (L.off_score, d * 4),
                  (L.off_S1, m * n * 4), (L.off_Rbar, L.r * D * 4), (L.off_info, 256)]
         if opt == "adam":

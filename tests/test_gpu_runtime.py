@@ -203,13 +203,16 @@ def test_joint_refresh_matches_the_per_matrix_sweeps(gpu_lib, monkeypatch, name,
 _RIGHT_TRIO = {"shapes": ((1100, 1012), (1030, 1016), (700, 96)), "tau": 3, "steps": 6}
 
 
-@pytest.mark.parametrize("name,override,select", [
-    ("conv_50", {"tau": 3}, "approx"),             # twelve conv layers, d < n, MSGD
-    ("seats64_left", _RIGHT_TRIO, "approx"),       # d = n < m, Adam
-    ("seats64_left", _RIGHT_TRIO, "exact"),
-    ("seats64_left", _RIGHT_TRIO, "approx_bf16"),
+@pytest.mark.parametrize("name,override,select,store", [
+    ("conv_50", {"tau": 3}, "approx", "fp32"),             # twelve conv layers, d < n, MSGD
+    ("seats64_left", _RIGHT_TRIO, "approx", "fp32"),       # d = n < m, Adam
+    ("seats64_left", _RIGHT_TRIO, "exact", "fp32"),
+    ("seats64_left", _RIGHT_TRIO, "approx_bf16", "fp32"),
+    ("conv_50", {"tau": 3}, "approx", "bf16"),             # bf16 gradients and error buffers
+    ("seats64_left", _RIGHT_TRIO, "approx", "bf16"),
 ])
-def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypatch, name, override, select):
+def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypatch, name, override, select,
+                                                               store):
     # a selection step of several matrices launches each kernel once for all
     # of them; every matrix must end bitwise where its own launches take it
     import torch
@@ -217,15 +220,17 @@ def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypa
     if name == "conv_50":
         wl = get_workload(name, shapes=wl.shapes[:12], **override)
     T = min(wl.steps, wl.tau + 3)
-    _say(name, select, "grouped vs per-matrix selection over", T, "steps,", len(wl.shapes), "matrices")
+    _say(name, select, store, "grouped vs per-matrix selection over", T, "steps,", len(wl.shapes), "matrices")
     G = _inputs(wl, T)
+    if store == "bf16":
+        G = [[g.to(torch.bfloat16) for g in gt] for gt in G]
     runs = []
     for grouped in ("0", None):
         if grouped is None:
             monkeypatch.delenv("GLR_GROUPED", raising=False)
         else:
             monkeypatch.setenv("GLR_GROUPED", grouped)
-        comp = _make(gpu_lib, wl, select=select)
+        comp = _make(gpu_lib, wl, select=select, store=store)
         X = _zeros(wl)
         for t in range(T):
             comp.step(X, G[t], t)
