@@ -728,7 +728,11 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
     const int64_t row = r0 + wm * 32 + mfma32_row(v, lane);
     const uint32_t o = (row < m && col < n) ? (uint32_t)((row * n + col) * 4) : kBufNone;
     // workers beyond N hold zero products
-    const float sum = MULTI ? gs[MULTI ? v : 0] : ((acc[0][v] + acc[1][v]) + acc[2][v]) + acc[3][v];
+    float sum = MULTI ? gs[MULTI ? v : 0] : acc[0][v];
+    if (!MULTI) {
+#pragma unroll
+      for (int w = 1; w < kNW; ++w) sum += acc[w][v];
+    }
     const float gh = sum * inv_n;
     float xv = buf_ld(Xr, o);
     float s1 = buf_ld(S1r, o);
