@@ -54,6 +54,9 @@ struct SubCtl {
   int gate_rest;               // nonzero: the rest of the pass is skipped (gated, or its rows are
                                // orthonormal already)
   int repaired;                // rows replaced by the last orthonormalisation pass
+  int reuse_z;                 // nonzero: a warm iteration met the tolerance; P keeps the basis it
+                               // started from and Z = P^T Mo of that basis serves the Rayleigh-Ritz
+                               // step (no product of its own)
   int stop;                    // no further iteration: converged, at its cap, or past 2 with a closed gap
   double e_in;                 // ||P Mo||^2 of the K-row block entering the last iteration run
   double e_out;                // ||P Mo||^2 of the final block

@@ -745,6 +745,7 @@ __global__ void k_sub_reset(SubCtl* sc) {
     sc->gate_iter = 0;
     sc->gate_pass = 0;
     sc->repaired = 0;
+    sc->reuse_z = 0;
   }
 }
 
@@ -767,6 +768,10 @@ __global__ void k_sub_step(SubCtl* sc, int r, float tol, const float* __restrict
   if (ch <= (double)tol) sc->converged = 1;
   if (sc->converged || sc->iters >= cap || (sc->iters >= kSubMinIters && !sub_gap_open(sigma, r, cold != 0)))
     sc->stop = 1;
+  // converged from a warm start: the basis this iteration started from is
+  // within the tolerance of the new one, and its Z (not orthonormalised on a
+  // warm start) is the Rayleigh-Ritz product of that basis
+  sc->reuse_z = (sc->converged && !cold) ? 1 : 0;
 }
 
 // part[b] = the sum of squares (fp64) of the elements b, b + nb, ... of the
@@ -802,8 +807,8 @@ __global__ void k_pass_reset(int* __restrict__ bad, int K, int* __restrict__ rep
 }
 
 __global__ void k_copy_gated(const float* __restrict__ src, float* __restrict__ dst, int64_t n,
-                             const int* __restrict__ gate) {
-  if (*gate) return;
+                             const int* __restrict__ gate, const int* __restrict__ gate2) {
+  if (*gate || (gate2 && *gate2)) return;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
 }
@@ -950,7 +955,8 @@ static hipError_t orth_pass(const MatView& v, float* Y, float* Ytmp, int K, int6
   prof.end(GLR_PROF_SUB_CHOL);
   GemmPlan p1{1, K};
   gemm_launch<false, 0>(v.sub_Linv, Kp, Y, L, Ytmp, L, K, (int)L, K, p1, 0, nullptr, nullptr, s, gate);
-  hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * L)), dim3(256), 0, s, Ytmp, Y, (int64_t)K * L, gate);
+  hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * L)), dim3(256), 0, s, Ytmp, Y, (int64_t)K * L, gate,
+                     (const int*)nullptr);
   uint32_t k0, k1;
   repair_key(seed, t, &k0, &k1);
   hipLaunchKernelGGL(k_orth_repair, dim3((unsigned)K), dim3(256), 0, s, Y, L, v.sub_bad, &sc->repaired, gate, k0,
@@ -1064,9 +1070,10 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
   const int nb = gemm_blocks(r, (int)d);
   hipLaunchKernelGGL(k_sum_double, dim3(1), dim3(256), 0, s, v.sub_sums, nb, &sc->change2, g);
   hipLaunchKernelGGL(k_sub_step, dim3(1), dim3(64), 0, s, sc, r, tol, (const float*)v.sigma, cold ? 1 : 0, cap);
-  // P <- P_new
+  // P <- P_new, unless this iteration converged from a warm start (then P
+  // and Z stay those of the basis it started from, for the Rayleigh-Ritz step)
   hipLaunchKernelGGL(k_copy_gated, dim3(grid_n((int64_t)K * d)), dim3(256), 0, s, v.sub_Pn, v.sub_P, (int64_t)K * d,
-                     g);
+                     g, (const int*)&sc->reuse_z);
   return hipGetLastError();
 }
 
@@ -1077,7 +1084,8 @@ hipError_t launch_sub_iter(const MatView& v, float tol, uint64_t seed, int64_t t
 hipError_t launch_sub_rr_begin(const MatView& v, MatView* rr, hipStream_t s) {
   const int K = sub_block(v.r, v.d);
   const int64_t D = v.D;
-  launch_z(v, K, nullptr, s);
+  // B = P^T Mo, or the last iteration's Z when it is that product already
+  launch_z(v, K, &v.sub_ctl->reuse_z, s);
   block_energy(v, v.sub_Z, K, D, &v.sub_ctl->e_out, nullptr, s);
   *rr = v;
   rr->d = K;
