@@ -20,6 +20,11 @@ The oracle cannot run complete steps at these sizes in a test's time, so:
   * the Approx-Top-r scores are checked at sampled indices (every selected
     index, the runners-up and random others) against fp64 bilinear forms with
     the v_j of the Philox stream, and J against the fp64 ranking of them.
+With bf16 storage (store="bf16") the gradients are the bf16 conversion of
+the same batches, the column oracle runs the same mode, and the sampled
+error buffers are compared as tests/parity.py compares them in that mode
+(each element within a bf16 step plus the fp32 residual's error, E and E-bar
+to the format's unit roundoff), then handed to the column oracle.
 """
 import numpy as np
 import pytest
@@ -28,8 +33,8 @@ from oracle.method import ColumnOracle, argtop_r
 from oracle.philox import gaussian_vectors
 from oracle.subspace import next_singular_value, top_subspace
 from synth import get_workload, noise_level, planted_matrix
-from tests.parity import (ENERGY_TOL, ENERGY_TOL_CLOSED, FINAL_TOL, GAP_CLOSED, eigengap, projector_bar,
-                          summarize)
+from tests.parity import (BF16_ABS, BF16_FLIPS, BF16_TOL, ENERGY_TOL, ENERGY_TOL_CLOSED, FINAL_TOL, GAP_CLOSED,
+                          eigengap, projector_bar, summarize)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,12 +55,13 @@ class Run:
     """The HIP path on device-resident batches: planted part from the input
     generator, per-step noise from a seeded torch generator on the device."""
 
-    def __init__(self, glr, wl, seed=4321):
+    def __init__(self, glr, wl, seed=4321, store="fp32"):
         import torch
         self.torch = torch
         self.wl = wl
+        self.store = store
         self.comp = glr.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr,
-                                   beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed)
+                                   beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, seed=wl.seed, store=store)
         self.planted = [torch.from_numpy(planted_matrix(wl, l).astype(np.float32)).cuda()
                         for l in range(len(wl.shapes))]
         self.gen = torch.Generator(device="cuda")
@@ -68,7 +74,8 @@ class Run:
         out = []
         for l, (m, n) in enumerate(self.wl.shapes):
             g = torch.randn((self.wl.workers, m, n), generator=self.gen, device="cuda", dtype=torch.float32)
-            out.append(g.mul_(noise_level(self.wl, l)).add_(self.planted[l]))
+            g = g.mul_(noise_level(self.wl, l)).add_(self.planted[l])
+            out.append(g.to(torch.bfloat16) if self.store == "bf16" else g)
         return out
 
     def step(self, G, allow_unconverged=False):
@@ -118,8 +125,20 @@ def check_columns(run, l, G, col_oracle, cols, refresh):
            "X": _rel(g["X"], o["X"]), "S1": _rel(g["S1"], o["S1"])}
     if o["S2"] is not None:
         rec["S2"] = _rel(g["S2"], o["S2"])
+    b16 = run.store == "bf16"
+    if b16:
+        e_g, e_o = g["E"], o["E"]
+        bar = 2.0 ** -7 * np.maximum(np.abs(e_g), np.abs(e_o)) + BF16_ABS * (np.abs(Gc).max() + np.abs(e_o).max())
+        elem = float((np.abs(e_g - e_o) / bar).max())
+        flips = int(np.count_nonzero(e_g != e_o))
+        assert elem <= 1.0, f"t={run.t - 1} mat={l}: E element off by {elem:.2f} of its bar"
+        assert flips <= BF16_FLIPS * e_o.size, (run.t - 1, l, flips)
+        col_oracle.e = e_g.copy()              # the column oracle continues from the stored buffers
     for k, v in rec.items():
-        assert v < STEP_TOL, f"t={run.t - 1} mat={l} columns {cols[:4]}...: {k} rel {v:.3e} ({rec})"
+        bar = BF16_TOL if (b16 and k in ("E", "Ebar")) else STEP_TOL
+        assert v < bar, f"t={run.t - 1} mat={l} columns {cols[:4]}...: {k} rel {v:.3e} ({rec})"
+    if b16:
+        rec["E_elem"] = elem
     return rec
 
 
@@ -252,7 +271,7 @@ def check_selection(run, l, mb, t, rng, extra=48):
 
 
 def run_fullsize(glr, name, steps, sample_cols=8, seed=7, ref_steps=None, max_mats=8,
-                 unconverged_from=None):
+                 unconverged_from=None, store="fp32"):
     """A trajectory of `steps` steps of workload `name` in hand-off mode (see
     the module docstring).  ref_steps: refresh steps whose projector is
     compared with the oracle's top-r route (None: every refresh).
@@ -262,7 +281,7 @@ def run_fullsize(glr, name, steps, sample_cols=8, seed=7, ref_steps=None, max_ma
     import torch
     wl = get_workload(name)
     _say(name, "shapes", list(wl.shapes)[:3], "N", wl.workers, "r", wl.rank, "tau", wl.tau, "steps", steps)
-    run = Run(glr, wl)
+    run = Run(glr, wl, store=store)
     rng = np.random.default_rng(seed)
     mats = list(range(len(wl.shapes)))
     if len(mats) > max_mats:      # many small matrices: the largest, the first, the last and a sample
@@ -275,7 +294,7 @@ def run_fullsize(glr, name, steps, sample_cols=8, seed=7, ref_steps=None, max_ma
         c = np.unique(np.concatenate([rng.choice(D, size=min(sample_cols, D), replace=False), [D - 1]]))
         cols[l] = torch.from_numpy(c).cuda()
         colo[l] = ColumnOracle(wl.shapes[l], c, wl.workers, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
-                               beta2=wl.beta2, eps=wl.eps)
+                               beta2=wl.beta2, eps=wl.eps, store=store)
         prev[l] = None
     log = []
     for t in range(steps):
@@ -363,3 +382,15 @@ def test_large_tau1(gpu_lib):
     # block iteration nor the oracle's converges there: those refreshes are
     # checked by their basis properties, and the trajectory by the columns
     run_fullsize(gpu_lib, "large_8192x28672", 10, sample_cols=4, ref_steps=(0, 1), unconverged_from=2)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,steps,kw", [
+    ("conv_50_gap", 22, {}),                                   # a refresh, a period of selections, a refresh
+    ("block_4096_gap", 12, {"max_mats": 3, "ref_steps": (0,)}),  # r = 128 kernels, both orientations, Adam
+    ("large_8192x28672", 4, {"sample_cols": 4, "ref_steps": (0, 1), "unconverged_from": 2}),
+])
+def test_bf16_storage_fullsize(gpu_lib, name, steps, kw):
+    # the bf16 storage mode at full size: sampled columns against the column
+    # oracle's same mode, the refresh and selection checks as in fp32
+    run_fullsize(gpu_lib, name, steps, store="bf16", **kw)
