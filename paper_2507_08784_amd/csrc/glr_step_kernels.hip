@@ -354,12 +354,26 @@ __device__ __forceinline__ void proj_at(const ST* __restrict__ G, const ST* __re
       }
     }
 }
+// gy > 1 (several rank tiles over the same columns of G and E): a 1-D grid
+// in which the gy rank tiles of a (column tile, worker, slice) triple are 8
+// blocks apart, so they run on the same XCD at the same time and the second
+// read of those columns hits that XCD's L2 (blocks go to the XCDs in turn);
+// gy = 1: the 3-D grid (x column tiles, z worker and slice)
 template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
 __global__ void __launch_bounds__(256)
 k_proj(const ST* __restrict__ G, const ST* __restrict__ E, const float* __restrict__ Ut,
-       const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice) {
-  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST>(G, E, Ut, J, Qpart, d, D, r, N, kslice, blockIdx.x, blockIdx.y,
-                                            blockIdx.z);
+       const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice,
+       int gx, int gy, int ntiles) {
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  if (gy > 1) {
+    const int L = blockIdx.x, xcd = L & 7, slot = L >> 3;
+    by = slot % gy;
+    const int tile = (slot / gy) * 8 + xcd;
+    if (tile >= ntiles) return;
+    bx = tile % gx;
+    bz = tile / gx;
+  }
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST>(G, E, Ut, J, Qpart, d, D, r, N, kslice, bx, by, bz);
 }
 
 template <class ST>
@@ -375,14 +389,18 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
   grid.z = (unsigned)(v.N * splits);
 #define GLR_PROJ(BM, BN, WM, WN, FL)                                                              \
   do {                                                                                            \
-    grid.x = (unsigned)((v.D + BN - 1) / BN);                                                     \
-    grid.y = (unsigned)((r + BM - 1) / BM);                                                       \
+    const int gx = (int)((v.D + BN - 1) / BN), gy = (r + BM - 1) / BM;                            \
+    const int ntiles = gx * (int)grid.z;                                                          \
+    dim3 gr = grid;                                                                               \
+    gr.x = (unsigned)gx;                                                                          \
+    gr.y = (unsigned)gy;                                                                          \
+    if (gy > 1) gr = dim3((unsigned)(((ntiles + 7) / 8) * 8 * gy));                               \
     if (v.right)                                                                                  \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL, ST>), grid, dim3(kThreads), 0, s, G, E, \
-                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL, ST>), gr, dim3(kThreads), 0, s, G, E,   \
+                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles);          \
     else                                                                                          \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL, ST>), grid, dim3(kThreads), 0, s, G, E,\
-                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice);                          \
+      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL, ST>), gr, dim3(kThreads), 0, s, G, E,  \
+                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles);          \
   } while (0)
   // 64 < r <= 128 takes two 64-row rank tiles (G and E read twice): the
   // 128-row tile keeps its fp64 accumulators in scratch memory and ran at half

@@ -259,6 +259,12 @@ def _mk():
                  recipe="geometric", params=(("rank", 200), ("decay", 0.985), ("nu", 1e-4))))
     add(Workload("wide_right", ((650, 290),), 2, 140, 2, 5, "adam", 1e-3, 0.9,
                  recipe="geometric", params=(("rank", 180), ("decay", 0.985), ("nu", 1e-4))))
+    # 64 < r <= 128: the projection's two 64-row rank tiles in the XCD order
+    # (ragged last column tile, a tile count that is not a multiple of 8)
+    add(Workload("two_tiles_left", ((300, 900),), 3, 100, 3, 6, "msgd", 0.01, 0.9,
+                 recipe="geometric", params=(("rank", 140), ("decay", 0.985), ("nu", 1e-4))))
+    add(Workload("two_tiles_right", ((900, 300),), 3, 100, 3, 6, "msgd", 0.01, 0.9,
+                 recipe="geometric", params=(("rank", 140), ("decay", 0.985), ("nu", 1e-4))))
     # (gap factor 10 at r: error feedback lifts the discarded directions by
     # about their own size per step, so the gap stays open over the 4 steps)
     # (MSGD: Adam's first step X = -lr sign-like(Ghat) turns the ~1e-8

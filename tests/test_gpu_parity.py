@@ -16,7 +16,7 @@ def _print_case(name, **kw):
 
 
 @pytest.mark.parametrize("name", ["one_256x128", "tiny_left", "ragged_right", "mid_left", "single_worker",
-                                  "wide_left", "wide_right"])
+                                  "wide_left", "wide_right", "two_tiles_left", "two_tiles_right"])
 def test_trajectory_parity(gpu_lib, name):
     _print_case(name)
     wl = get_workload(name)
