@@ -34,13 +34,16 @@ def _blob(comp):
     return comp.state[comp._s0: comp._s0 + comp.state_bytes]
 
 
-def test_nonfinite_gradient_is_reported_and_state_marked_suspect(gpu_lib):
+@pytest.mark.parametrize("store", ["fp32", "bf16"])
+def test_nonfinite_gradient_is_reported_and_state_marked_suspect(gpu_lib, store):
     import torch
     wl = get_workload("one_256x128")
-    _say("one_256x128 check_finite")
-    comp = _make(gpu_lib, wl, check_finite=True)
+    _say("one_256x128 check_finite", store)
+    comp = _make(gpu_lib, wl, check_finite=True, store=store)
     X = _zeros(wl)
     G = _inputs(wl, 2)
+    if store == "bf16":
+        G = [[g.to(torch.bfloat16) for g in gt] for gt in G]
     comp.step(X, G[0], 0)
     assert comp.sync_status() == gpu_lib.GLR_OK
     bad = G[1][0].clone()
@@ -244,28 +247,32 @@ def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypa
         assert torch.equal(c1.J(l), c2.J(l)), f"mat {l}: J differs"
 
 
-def test_state_read_and_write_through_the_abi_resume_the_run(gpu_lib):
+@pytest.mark.parametrize("store", ["fp32", "bf16"])
+def test_state_read_and_write_through_the_abi_resume_the_run(gpu_lib, store):
     # glr_read_state into host tensors after 3 steps of one handle, then
     # glr_write_state of those tensors into a fresh handle (a restore), which
-    # continues bitwise like the uninterrupted run
+    # continues bitwise like the uninterrupted run (E in the storage type)
     import torch
     wl = get_workload("ragged_right")
     T, cut = 6, 3
-    _say("ragged_right read/write state at", cut)
+    _say("ragged_right read/write state at", cut, store)
     G = _inputs(wl, T)
+    edt = torch.bfloat16 if store == "bf16" else torch.float32
+    if store == "bf16":
+        G = [[g.to(torch.bfloat16) for g in gt] for gt in G]
     a = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
-                           seed=wl.seed)
+                           seed=wl.seed, store=store)
     Xa = _zeros(wl)
     for t in range(T):
         a.step(Xa, G[t], t)
     b = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
-                           seed=wl.seed)
+                           seed=wl.seed, store=store)
     Xb = _zeros(wl)
     for t in range(cut):
         b.step(Xb, G[t], t)
     L = b.layouts[0]
     m, n, d, D, r, N = L.m, L.n, L.d, L.D, L.r, wl.workers
-    host = {"E": torch.empty(N, m, n), "Ebar": torch.empty(m, n), "Ut": torch.empty(d, d),
+    host = {"E": torch.empty(N, m, n, dtype=edt), "Ebar": torch.empty(m, n), "Ut": torch.empty(d, d),
             "sigma": torch.empty(d), "J": torch.empty(r, dtype=torch.int32), "score": torch.empty(d),
             "S1": torch.empty(m, n), "S2": torch.empty(m, n), "Rbar": torch.empty(r, D),
             "info": torch.empty(64, dtype=torch.int32)}
@@ -274,7 +281,7 @@ def test_state_read_and_write_through_the_abi_resume_the_run(gpu_lib):
     assert torch.equal(host["E"], b.E(0).cpu()) and torch.equal(host["Ut"], b.Ut(0).cpu())
     assert torch.equal(host["S2"], b.S2(0).cpu()) and torch.equal(host["J"], b.J(0).cpu())
     c = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
-                           seed=wl.seed)
+                           seed=wl.seed, store=store)
     c.write_state(0, **host)
     c.resume(cut)
     Xc = [x.clone() for x in Xb]
@@ -321,9 +328,10 @@ def test_refresh_step_only_enqueues(gpu_lib):
     assert comp.sync_status() == gpu_lib.GLR_OK
 
 
-@pytest.mark.parametrize("name,tau", [("zero_grad", 2), ("zero_grad", 1), ("lowrank_exact", 3),
-                                      ("lowrank_exact", 1)])
-def test_zero_and_rank_deficient_gradients(gpu_lib, name, tau):
+@pytest.mark.parametrize("name,tau,store", [("zero_grad", 2, "fp32"), ("zero_grad", 1, "fp32"),
+                                            ("lowrank_exact", 3, "fp32"), ("lowrank_exact", 1, "fp32"),
+                                            ("zero_grad", 2, "bf16"), ("zero_grad", 1, "bf16")])
+def test_zero_and_rank_deficient_gradients(gpu_lib, name, tau, store):
     # all-zero gradients, and exactly rank-4 gradients with r = 6 (< the
     # oversampled tau = 1 block): the full-basis and the tau = 1 refresh both
     # stay finite and orthonormal, and compress exactly (E = 0), as the
@@ -331,16 +339,19 @@ def test_zero_and_rank_deficient_gradients(gpu_lib, name, tau):
     import torch
     from oracle.method import Oracle
     from tests.parity import rel
+    # (bf16 storage with zero gradients only: a rank-4 matrix rounded to bf16
+    # is full rank at the 2^-9 level)
     wl = get_workload(name, tau=tau)
-    _say(name, "tau", tau)
+    _say(name, "tau", tau, store)
     comp = gpu_lib.GreedyLore(wl.shapes, wl.workers, wl.rank, wl.tau, opt=wl.opt, lr=wl.lr, beta1=wl.beta1,
-                              seed=wl.seed)
-    orc = Oracle.from_workload(wl)
+                              seed=wl.seed, store=store)
+    orc = Oracle.from_workload(wl, store=store)
+    gdt = torch.bfloat16 if store == "bf16" else torch.float32
     planted = [planted_matrix(wl, l) for l in range(len(wl.shapes))]
     X = _zeros(wl)
     for t in range(wl.steps):
         grads = [gradient_batch(wl, l, t, planted[l]) for l in range(len(wl.shapes))]
-        comp.step(X, [torch.from_numpy(g).cuda() for g in grads], t)
+        comp.step(X, [torch.from_numpy(g).cuda().to(gdt) for g in grads], t)
         torch.cuda.synchronize()
         st = comp.sync_status()
         assert st == gpu_lib.GLR_OK, f"t={t}: status {gpu_lib.STATUS_NAMES.get(st, st)}"
