@@ -204,9 +204,10 @@ void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]);
 size_t topr_lds_bytes(int64_t d);
 // one selection step of every matrix of the plan: M-bar, the Approx-Top-r (or
 // exact) scores and their top r, the projection and its mean, the residual
-// and the optimizer update, seven launches in all
+// and the optimizer update, seven launches in all (part 1: M-bar only; part
+// 2: the launches after it; 0: all)
 hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
-                               int64_t t, const OptParams& o, hipStream_t s);
+                               int64_t t, const OptParams& o, int part, hipStream_t s);
 
 // One matrix of a joint refresh (device memory): its views for the two buffer
 // parities of the per-sweep reordering (v[1] is v[0] with Apk <-> Apk2 and

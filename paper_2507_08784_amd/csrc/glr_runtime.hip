@@ -275,8 +275,8 @@ WsPlan ws_plan(const glr_config* c) {
   o = align_up(o + ((uint64_t)kJointKinds * ((uint64_t)c->num_mats + 1) + (uint64_t)c->num_mats) * 4);
   p.off_gmats = o;
   o = align_up(o + (uint64_t)c->num_mats * sizeof(GroupMat));
-  p.off_gfirst = o;
-  o = align_up(o + (uint64_t)kGrpKinds * ((uint64_t)c->num_mats + 1) * 4);
+  p.off_gfirst = o;   // the tables of the two halves of a split grouped step
+  o = align_up(o + (uint64_t)kGrpKinds * ((uint64_t)c->num_mats + 2) * 4);
   p.bytes = o;
   p.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
   return p;
@@ -353,6 +353,7 @@ struct glr_handle {
   bool grouped = false;                // selection steps launch each kernel once for all matrices
   std::vector<int> gfirst;
   GroupPlan gp;
+  GroupPlan gp2;                       // second half of a split grouped step (num 0: no split)
   GroupMat* gring = nullptr;           // pinned host copies of the per-step table, two slots
   hipEvent_t gev[2] = {};              // the upload that last read each slot
   int gslot = 0;
@@ -886,8 +887,24 @@ glr_status step_grouped(glr_handle* h, float* const* X, const void* const* G, in
   GLR_HIP(h, hipMemcpyAsync((void*)h->gp.gm, g, (size_t)num * sizeof(GroupMat), hipMemcpyHostToDevice, s));
   GLR_HIP(h, hipEventRecord(h->gev[slot], s));
   OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
-  GLR_HIP(h, launch_group_select(h->gp, (c.flags & GLR_CHECK_FINITE) != 0, c.select != GLR_SELECT_EXACT,
-                                 c.select == GLR_SELECT_APPROX_BF16, c.seed, t, op, s));
+  const bool fin = (c.flags & GLR_CHECK_FINITE) != 0, approx = c.select != GLR_SELECT_EXACT,
+             b16 = c.select == GLR_SELECT_APPROX_BF16;
+  if (h->gp2.num == 0) {
+    GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 0, s));
+    return GLR_OK;
+  }
+  // two halves, the second on a lane stream from the end of the first half's
+  // M-bar on: each half's launches alternate between the HBM-bound (M-bar,
+  // projection, residual) and the MFMA-bound (scores) kinds, so the
+  // staggered halves overlap the two
+  hipStream_t ls = h->lane_s[1];
+  GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 1, s));
+  GLR_HIP(h, hipEventRecord(h->ev_fork, s));
+  GLR_HIP(h, hipStreamWaitEvent(ls, h->ev_fork, 0));
+  GLR_HIP(h, launch_group_select(h->gp2, fin, approx, b16, c.seed, t, op, 0, ls));
+  GLR_HIP(h, hipEventRecord(h->ev_join[1], ls));
+  GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 2, s));
+  GLR_HIP(h, hipStreamWaitEvent(s, h->ev_join[1], 0));
   return GLR_OK;
 }
 
@@ -910,35 +927,58 @@ bool group_allowed(const glr_handle* h) {
 // block tables of the grouped launches, the pinned ring and its events
 hipError_t group_setup(glr_handle* h, hipStream_t s) {
   const int num = h->cfg.num_mats;
-  GroupPlan& gp = h->gp;
-  gp.num = num;
-  gp.right = h->lay[0].right != 0;
-  gp.r = h->lay[0].r;
-  gp.st16 = (h->cfg.flags & GLR_STORE_BF16) != 0;
+  // a split into two halves of about equal bytes needs a lane stream
+  int nA = num;
+  bool split = h->lanes > 1 && num >= 4;
+  if (const char* e = getenv("GLR_GROUP_SPLIT")) split = split && atoi(e) != 0;
+  if (split) {
+    double tot = 0.0, acc = 0.0;
+    for (int i = 0; i < num; ++i) tot += (double)h->lay[(size_t)i].m * (double)h->lay[(size_t)i].n;
+    nA = 0;
+    while (nA < num - 1 && acc + 0.5 * (double)h->lay[(size_t)nA].m * (double)h->lay[(size_t)nA].n < 0.5 * tot)
+      acc += (double)h->lay[(size_t)nA].m * (double)h->lay[(size_t)nA++].n;
+    if (nA < 1) nA = 1;
+  }
   std::vector<int> blocks((size_t)num * kGrpKinds);
+  size_t topr_lds = 0;
   for (int i = 0; i < num; ++i) {
     GroupMat g;
     g.v = view_of(h, i, nullptr, nullptr, 0);
     int b[kGrpKinds];
     group_fill(g, b);
     for (int k = 0; k < kGrpKinds; ++k) blocks[(size_t)i * kGrpKinds + k] = b[k];
-    gp.topr_lds = std::max(gp.topr_lds, topr_lds_bytes(g.v.d));
+    topr_lds = std::max(topr_lds, topr_lds_bytes(g.v.d));
   }
-  h->gfirst.assign((size_t)kGrpKinds * (num + 1), 0);
-  for (int k = 0; k < kGrpKinds; ++k) {
-    int64_t acc = 0;
-    for (int i = 0; i < num; ++i) {
-      h->gfirst[(size_t)k * (num + 1) + i] = (int)acc;
-      acc += blocks[(size_t)i * kGrpKinds + k];
+  const GroupMat* gm = (const GroupMat*)(h->work + h->ws.off_gmats);
+  const int* first = (const int*)(h->work + h->ws.off_gfirst);
+  h->gfirst.clear();
+  // the plan of matrices [a, b): its tables follow the previous plan's
+  auto plan = [&](GroupPlan& gp, int a, int b) -> hipError_t {
+    const int n = b - a;
+    gp.num = n;
+    gp.right = h->lay[0].right != 0;
+    gp.r = h->lay[0].r;
+    gp.st16 = (h->cfg.flags & GLR_STORE_BF16) != 0;
+    gp.topr_lds = topr_lds;
+    gp.gm = gm + a;
+    gp.first = first + h->gfirst.size();
+    for (int k = 0; k < kGrpKinds; ++k) {
+      int64_t acc = 0;
+      for (int i = a; i < b; ++i) {
+        h->gfirst.push_back((int)acc);
+        acc += blocks[(size_t)i * kGrpKinds + k];
+      }
+      if (acc > INT32_MAX) return hipErrorInvalidValue;
+      h->gfirst.push_back((int)acc);
+      gp.total[k] = (int)acc;
     }
-    if (acc > INT32_MAX) return hipErrorInvalidValue;
-    h->gfirst[(size_t)k * (num + 1) + num] = (int)acc;
-    gp.total[k] = (int)acc;
-  }
-  gp.gm = (const GroupMat*)(h->work + h->ws.off_gmats);
-  gp.first = (const int*)(h->work + h->ws.off_gfirst);
-  hipError_t e = hipMemcpyAsync((void*)gp.first, h->gfirst.data(), h->gfirst.size() * sizeof(int),
-                                hipMemcpyHostToDevice, s);
+    return hipSuccess;
+  };
+  hipError_t e = plan(h->gp, 0, nA);
+  h->gp2 = GroupPlan{};
+  if (e == hipSuccess && nA < num) e = plan(h->gp2, nA, num);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync((void*)first, h->gfirst.data(), h->gfirst.size() * sizeof(int), hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->gring, 2 * (size_t)num * sizeof(GroupMat), hipHostMallocDefault);
   for (int k = 0; e == hipSuccess && k < 2; ++k) e = hipEventCreateWithFlags(&h->gev[k], hipEventDisableTiming);
   return e;

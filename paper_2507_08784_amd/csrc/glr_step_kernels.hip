@@ -1008,14 +1008,16 @@ void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]) {
 
 template <class ST>
 static hipError_t launch_group_select_st(const GroupPlan& gp, bool check_finite, bool approx, bool bf16,
-                                         uint64_t seed, int64_t t, const OptParams& o, hipStream_t s) {
+                                         uint64_t seed, int64_t t, const OptParams& o, int part, hipStream_t s) {
   if (bf16 && !approx) return hipErrorInvalidValue;
   const int num = gp.num, r = gp.r;
   const bool right = gp.right;
   auto table = [&](int kind) { return gp.first + (int64_t)kind * (num + 1); };
   auto grid = [&](int kind) { return dim3((unsigned)gp.total[kind]); };
-  hipLaunchKernelGGL(k_g_ef_mean<ST>, grid(kGrpEfMean), dim3(kThreads), 0, s, gp.gm, table(kGrpEfMean), num,
-                     check_finite ? 1 : 0);
+  if (part != 2)
+    hipLaunchKernelGGL(k_g_ef_mean<ST>, grid(kGrpEfMean), dim3(kThreads), 0, s, gp.gm, table(kGrpEfMean), num,
+                       check_finite ? 1 : 0);
+  if (part == 1) return hipGetLastError();
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
 #define GLR_GSEL(R, A, B)                                                                                   \
@@ -1061,9 +1063,9 @@ static hipError_t launch_group_select_st(const GroupPlan& gp, bool check_finite,
   return hipGetLastError();
 }
 hipError_t launch_group_select(const GroupPlan& gp, bool check_finite, bool approx, bool bf16, uint64_t seed,
-                               int64_t t, const OptParams& o, hipStream_t s) {
-  return gp.st16 ? launch_group_select_st<bf16_t>(gp, check_finite, approx, bf16, seed, t, o, s)
-                 : launch_group_select_st<float>(gp, check_finite, approx, bf16, seed, t, o, s);
+                               int64_t t, const OptParams& o, int part, hipStream_t s) {
+  return gp.st16 ? launch_group_select_st<bf16_t>(gp, check_finite, approx, bf16, seed, t, o, part, s)
+                 : launch_group_select_st<float>(gp, check_finite, approx, bf16, seed, t, o, part, s);
 }
 
 }  // namespace glr
