@@ -275,8 +275,8 @@ WsPlan ws_plan(const glr_config* c) {
   o = align_up(o + ((uint64_t)kJointKinds * ((uint64_t)c->num_mats + 1) + (uint64_t)c->num_mats) * 4);
   p.off_gmats = o;
   o = align_up(o + (uint64_t)c->num_mats * sizeof(GroupMat));
-  p.off_gfirst = o;   // the tables of the two halves of a split grouped step
-  o = align_up(o + (uint64_t)kGrpKinds * ((uint64_t)c->num_mats + 2) * 4);
+  p.off_gfirst = o;   // the tables of the parts of a grouped selection step
+  o = align_up(o + (uint64_t)kGrpKinds * ((uint64_t)c->num_mats + kMaxLanes) * 4);
   p.bytes = o;
   p.lanes = c->num_mats < kMaxLanes ? c->num_mats : kMaxLanes;
   return p;
@@ -352,8 +352,9 @@ struct glr_handle {
   JointPlan jp;
   bool grouped = false;                // selection steps launch each kernel once for all matrices
   std::vector<int> gfirst;
-  GroupPlan gp;
-  GroupPlan gp2;                       // second half of a split grouped step (num 0: no split)
+  GroupPlan gp[kMaxLanes];             // the parts of a grouped selection step (gparts of them)
+  int gparts = 0;
+  hipEvent_t gev_mean[kMaxLanes] = {}; // end of each part's M-bar
   GroupMat* gring = nullptr;           // pinned host copies of the per-step table, two slots
   hipEvent_t gev[2] = {};              // the upload that last read each slot
   int gslot = 0;
@@ -884,27 +885,28 @@ glr_status step_grouped(glr_handle* h, float* const* X, const void* const* G, in
     g[i].v = view_of(h, i, X[i], G[i], 0);
     group_fill(g[i], blocks);
   }
-  GLR_HIP(h, hipMemcpyAsync((void*)h->gp.gm, g, (size_t)num * sizeof(GroupMat), hipMemcpyHostToDevice, s));
+  GLR_HIP(h, hipMemcpyAsync((void*)h->gp[0].gm, g, (size_t)num * sizeof(GroupMat), hipMemcpyHostToDevice, s));
   GLR_HIP(h, hipEventRecord(h->gev[slot], s));
   OptParams op{c.opt, c.lr, c.beta1, c.beta2, c.eps};
   const bool fin = (c.flags & GLR_CHECK_FINITE) != 0, approx = c.select != GLR_SELECT_EXACT,
              b16 = c.select == GLR_SELECT_APPROX_BF16;
-  if (h->gp2.num == 0) {
-    GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 0, s));
+  if (h->gparts == 1) {
+    GLR_HIP(h, launch_group_select(h->gp[0], fin, approx, b16, c.seed, t, op, 0, s));
     return GLR_OK;
   }
-  // two halves, the second on a lane stream from the end of the first half's
-  // M-bar on: each half's launches alternate between the HBM-bound (M-bar,
-  // projection, residual) and the MFMA-bound (scores) kinds, so the
-  // staggered halves overlap the two
-  hipStream_t ls = h->lane_s[1];
-  GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 1, s));
-  GLR_HIP(h, hipEventRecord(h->ev_fork, s));
-  GLR_HIP(h, hipStreamWaitEvent(ls, h->ev_fork, 0));
-  GLR_HIP(h, launch_group_select(h->gp2, fin, approx, b16, c.seed, t, op, 0, ls));
-  GLR_HIP(h, hipEventRecord(h->ev_join[1], ls));
-  GLR_HIP(h, launch_group_select(h->gp, fin, approx, b16, c.seed, t, op, 2, s));
-  GLR_HIP(h, hipStreamWaitEvent(s, h->ev_join[1], 0));
+  // parts of about equal bytes, part k > 0 on lane k from the end of part
+  // k - 1's M-bar on: each part's launches alternate between the HBM-bound
+  // (M-bar, projection, residual) and the MFMA-bound (scores) kinds, so the
+  // staggered parts overlap the two
+  for (int k = 0; k < h->gparts; ++k) {
+    hipStream_t ks = k == 0 ? s : h->lane_s[k];
+    if (k > 0) GLR_HIP(h, hipStreamWaitEvent(ks, h->gev_mean[k - 1], 0));
+    GLR_HIP(h, launch_group_select(h->gp[k], fin, approx, b16, c.seed, t, op, 1, ks));
+    if (k + 1 < h->gparts) GLR_HIP(h, hipEventRecord(h->gev_mean[k], ks));
+    GLR_HIP(h, launch_group_select(h->gp[k], fin, approx, b16, c.seed, t, op, 2, ks));
+    if (k > 0) GLR_HIP(h, hipEventRecord(h->ev_join[k], ks));
+  }
+  for (int k = 1; k < h->gparts; ++k) GLR_HIP(h, hipStreamWaitEvent(s, h->ev_join[k], 0));
   return GLR_OK;
 }
 
@@ -927,17 +929,24 @@ bool group_allowed(const glr_handle* h) {
 // block tables of the grouped launches, the pinned ring and its events
 hipError_t group_setup(glr_handle* h, hipStream_t s) {
   const int num = h->cfg.num_mats;
-  // a split into two halves of about equal bytes needs a lane stream
-  int nA = num;
-  bool split = h->lanes > 1 && num >= 4;
-  if (const char* e = getenv("GLR_GROUP_SPLIT")) split = split && atoi(e) != 0;
-  if (split) {
+  // parts of about equal bytes, one per lane stream (two unless
+  // GLR_GROUP_PARTS asks otherwise; at most one part per two matrices)
+  int parts = std::min(h->lanes, 2);
+  if (const char* e = getenv("GLR_GROUP_PARTS")) parts = std::min(h->lanes, std::max(1, atoi(e)));
+  if (const char* e = getenv("GLR_GROUP_SPLIT"))
+    if (atoi(e) == 0) parts = 1;
+  parts = std::max(1, std::min(parts, num / 2));
+  std::vector<int> cut(1, 0);
+  {
     double tot = 0.0, acc = 0.0;
     for (int i = 0; i < num; ++i) tot += (double)h->lay[(size_t)i].m * (double)h->lay[(size_t)i].n;
-    nA = 0;
-    while (nA < num - 1 && acc + 0.5 * (double)h->lay[(size_t)nA].m * (double)h->lay[(size_t)nA].n < 0.5 * tot)
-      acc += (double)h->lay[(size_t)nA].m * (double)h->lay[(size_t)nA++].n;
-    if (nA < 1) nA = 1;
+    for (int i = 0; i < num && (int)cut.size() < parts; ++i) {
+      const double sz = (double)h->lay[(size_t)i].m * (double)h->lay[(size_t)i].n;
+      // close the part before matrix i once it holds its share
+      if (i > cut.back() && acc + 0.5 * sz >= tot * (double)cut.size() / parts) cut.push_back(i);
+      acc += sz;
+    }
+    cut.push_back(num);
   }
   std::vector<int> blocks((size_t)num * kGrpKinds);
   size_t topr_lds = 0;
@@ -974,9 +983,11 @@ hipError_t group_setup(glr_handle* h, hipStream_t s) {
     }
     return hipSuccess;
   };
-  hipError_t e = plan(h->gp, 0, nA);
-  h->gp2 = GroupPlan{};
-  if (e == hipSuccess && nA < num) e = plan(h->gp2, nA, num);
+  hipError_t e = hipSuccess;
+  h->gparts = (int)cut.size() - 1;
+  for (int k = 0; e == hipSuccess && k < h->gparts; ++k) e = plan(h->gp[k], cut[(size_t)k], cut[(size_t)k + 1]);
+  for (int k = 0; e == hipSuccess && k + 1 < h->gparts; ++k)
+    e = hipEventCreateWithFlags(&h->gev_mean[k], hipEventDisableTiming);
   if (e == hipSuccess)
     e = hipMemcpyAsync((void*)first, h->gfirst.data(), h->gfirst.size() * sizeof(int), hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->gring, 2 * (size_t)num * sizeof(GroupMat), hipHostMallocDefault);
@@ -985,6 +996,10 @@ hipError_t group_setup(glr_handle* h, hipStream_t s) {
 }
 
 void release_group(glr_handle* h) {
+  for (int k = 0; k < kMaxLanes; ++k) {
+    if (h->gev_mean[k]) (void)hipEventDestroy(h->gev_mean[k]);
+    h->gev_mean[k] = nullptr;
+  }
   for (int k = 0; k < 2; ++k) {
     if (h->gev[k]) (void)hipEventSynchronize(h->gev[k]);
     if (h->gev[k]) (void)hipEventDestroy(h->gev[k]);
