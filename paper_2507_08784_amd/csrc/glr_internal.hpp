@@ -138,23 +138,33 @@ struct ProfHook {
   void end(int g) const { if (fn) fn(ctx, g, 0); }
 };
 
-// Slices of the d contraction of the projection.  Above rank 128 one tile
-// covers all r rows and accumulates 1024 terms in fp32 per slice (the slices
-// are added in fp64 by the reduction; 1024 rather than 512 halves the
-// partial products written and read back, 0.94 instead of 1.88 GB on the
-// 8192 x 28672 matrix with four workers); otherwise slices (of at least 256)
-// are only made to fill the chip, and the kernel itself adds fp32 partial
-// sums of 512 terms into fp64.
+// Slices of the d contraction of the projection.  Above rank 64 one tile
+// covers all r rows (r <= 128: 128 x 64 tiles, above: 256 x 64) and
+// accumulates 1024 terms in fp32 per slice; the slices are added in fp64 by
+// the reduction (1024 rather than 512 terms halves the partial products
+// written and read back: 0.94 instead of 1.88 GB on the 8192 x 28672 matrix
+// with four workers).  Up to rank 64 slices (of at least 256) are only made
+// to fill the chip, and the kernel itself adds fp32 partial sums of 512
+// terms into fp64.
 constexpr int kProjWideRank = 128;
-constexpr int kProjWideSlice = 1024;
+constexpr int kProjSlice = 1024;
+constexpr int kProjFlushRank = 64;
+// fp32 terms per slice of the tiers above kProjFlushRank (0: a flushing tier)
+inline int proj_slice(int r) { return r > kProjFlushRank ? kProjSlice : 0; }
 inline int proj_splits(int64_t d, int64_t D, int r, int N) {
-  if (r > kProjWideRank) return (int)((d + kProjWideSlice - 1) / kProjWideSlice);
-  const int64_t tiles = ((D + 63) / 64) * ((r + 127) / 128) * N;
+  if (const int sl = proj_slice(r)) return (int)((d + sl - 1) / sl);
+  const int64_t tiles = ((D + 63) / 64) * N;
   if (tiles >= 2048) return 1;
   int64_t sp = (2048 + tiles - 1) / tiles;
   const int64_t mx = d / 256;
   if (sp > mx) sp = mx;
   return sp < 1 ? 1 : (int)sp;
+}
+// the slice length a projection launch uses
+inline int proj_kslice(int64_t d, int64_t D, int r, int N) {
+  if (const int sl = proj_slice(r)) return sl;
+  const int sp = proj_splits(d, D, r, N);
+  return (int)(((d + sp - 1) / sp + 31) / 32 * 32);
 }
 
 // above this rank the residuals come first from a wider-tile kernel

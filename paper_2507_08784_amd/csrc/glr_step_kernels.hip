@@ -382,8 +382,7 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
   const ST* G = static_cast<const ST*>(v.G);
   const ST* E = static_cast<const ST*>(v.E);
   const int splits = proj_splits(v.d, v.D, r, v.N);
-  const int64_t kslice = r > kProjWideRank ? kProjWideSlice
-                                           : ((v.d + splits - 1) / splits + 31) / 32 * 32;
+  const int64_t kslice = proj_kslice(v.d, v.D, r, v.N);
   float* const out = splits > 1 ? v.Qpart : v.Q;
   dim3 grid;
   grid.z = (unsigned)(v.N * splits);
@@ -402,11 +401,15 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
       hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL, ST>), gr, dim3(kThreads), 0, s, G, E,  \
                          v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles);          \
   } while (0)
-  // 64 < r <= 128 takes two 64-row rank tiles (G and E read twice): the
-  // 128-row tile keeps its fp64 accumulators in scratch memory and ran at half
-  // the speed
+  // one rank tile covers all r rows, so G and E are read once.  Up to rank
+  // 64 the tile adds its fp32 sums into fp64 every 512 terms; above, the
+  // slices are 1024 terms and the reduction adds them in fp64, which keeps
+  // fp64 accumulators out of the larger tiles (a 128-row tile holding them
+  // spills).  At rank 64 the 64 x 128 tile without the fp64 sums was 10 %
+  // slower than the 64 x 64 one with them (fewer, longer blocks).
   if (r <= 32) GLR_PROJ(32, 128, 1, 4, true);
-  else if (r <= kProjWideRank) GLR_PROJ(64, 64, 2, 2, true);
+  else if (r <= kProjFlushRank) GLR_PROJ(64, 64, 2, 2, true);
+  else if (r <= kProjWideRank) GLR_PROJ(128, 64, 2, 2, false);
   else GLR_PROJ(256, 64, 4, 1, false);
 #undef GLR_PROJ
   return hipGetLastError();
@@ -913,7 +916,8 @@ __device__ __forceinline__ int dev_next_pow2(int64_t x) {
 // projection tiles of rank r: BM x BN, WM x WN waves, fp64 flush of the slices
 #define GLR_PROJ_TIERS(X)                                   \
   if (r <= 32) X(32, 128, 1, 4, true);                      \
-  else if (r <= kProjWideRank) X(64, 64, 2, 2, true);       \
+  else if (r <= kProjFlushRank) X(64, 64, 2, 2, true);      \
+  else if (r <= kProjWideRank) X(128, 64, 2, 2, false);     \
   else X(256, 64, 4, 1, false)
 
 template <class ST>
@@ -993,7 +997,7 @@ void group_fill(GroupMat& g, int (&blocks)[kGrpKinds]) {
   const MatView& v = g.v;
   const int r = v.r;
   g.splits = proj_splits(v.d, v.D, r, v.N);
-  g.kslice = r > kProjWideRank ? kProjWideSlice : (int)(((v.d + g.splits - 1) / g.splits + 31) / 32 * 32);
+  g.kslice = proj_kslice(v.d, v.D, r, v.N);
   blocks[kGrpEfMean] = grid_for(v.m * v.n, 4);
   blocks[kGrpSelScores] = (int)(((v.d + SEL_BN - 1) / SEL_BN) * ((v.D + SEL_BM - 1) / SEL_BM));
   blocks[kGrpSelFinish] = grid_for(v.d);
