@@ -621,6 +621,24 @@ k_resid_opt16(const bf16_t* __restrict__ G, bf16_t* __restrict__ E, float* __res
 // groups (MULTI), the products of the earlier groups summed in registers.
 constexpr int kNW = 4;
 constexpr int kNWTile = 64;
+// the products of one k-slice for all kNW workers of a group, with no branch
+// between the MFMAs, so that the LDS reads of the unrolled loop are issued
+// ahead of them (a branch per worker made every MFMA wait for its own operand
+// read).  The slices of workers beyond N are zero in LDS, so their products
+// are zero.
+template <bool RIGHT, int BK, int SL, int PT>
+__device__ __forceinline__ void nw_slice(const float* smem, int soff, int qoff, int kh, f32x16 (&acc)[kNW]) {
+#pragma unroll
+  for (int kk = 0; kk < BK / 2; ++kk) {
+    const int row = (2 * kk + kh) * PT;
+    const float sv = smem[row + soff];
+#pragma unroll
+    for (int w = 0; w < kNW; ++w) {
+      const float qw = smem[(1 + w) * SL + row + qoff];
+      acc[w] = RIGHT ? mfma32(qw, sv, acc[w]) : mfma32(sv, qw, acc[w]);
+    }
+  }
+}
 template <int OPT, bool RIGHT, bool MULTI, class ST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Ebar,
@@ -697,17 +715,7 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
     for (int kb = 0; kb < nk; ++kb) {
       const bool more = kb + 1 < nk;
       if (more) fetch((kb + 1) * BK);
-#pragma unroll
-      for (int kk = 0; kk < BK / 2; ++kk) {
-        const int row = (2 * kk + kh) * PT;
-        const float sv = smem[row + soff];
-#pragma unroll
-        for (int w = 0; w < kNW; ++w) {
-          if (w >= nw) break;
-          const float qw = smem[(1 + w) * SL + row + qoff];
-          acc[w] = RIGHT ? mfma32(qw, sv, acc[w]) : mfma32(sv, qw, acc[w]);
-        }
-      }
+      nw_slice<RIGHT, BK, SL, PT>(smem, soff, qoff, kh, acc);
       __syncthreads();
       if (more) {
         put();
