@@ -30,17 +30,26 @@ namespace glr {
 //   EPI 2: C = X - acc
 // A launch whose gate word is set returns at once (a section of the tau = 1
 // refresh that the device skipped: converged, or no repair to finish).
+// The grid is one-dimensional: the gy row tiles of a (column tile, slice)
+// pair run one after another on one XCD (workgroups go to the XCDs in turn,
+// so 8 launch slots apart), so that the slice of B they share is read from
+// HBM once and then from that XCD's L2.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool B_KC, int EPI>
 __global__ void __launch_bounds__(256)
 k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, int64_t ldb,
        float* __restrict__ C, int64_t ldc, int M, int N, int Kc, int kslice, int64_t cstride,
-       const float* __restrict__ X, double* __restrict__ sums, const int* __restrict__ gate) {
+       const float* __restrict__ X, double* __restrict__ sums, const int* __restrict__ gate, int gx, int gy,
+       int ngroups) {
   if (gate && *gate) return;
+  const int L = blockIdx.x, slot = L >> 3;
+  const int grp = (slot / gy) * 8 + (L & 7), bxy = slot % gy;
+  if (grp >= ngroups) return;
+  const int bxx = grp % gx, bz = grp / gx;
   using T = MfmaTile<BM, BN, WM, WN>;
   __shared__ __align__(16) float smem[T::LDS_FLOATS];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int k0 = blockIdx.z * kslice;
+  const int n0 = bxx * BN, m0 = bxy * BM;
+  const int k0 = bz * kslice;
   const int klen = (Kc - k0 < kslice) ? Kc - k0 : kslice;
   T tile;
   if (klen > 0) {
@@ -53,7 +62,7 @@ k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, in
       tile.run(la, lb, klen, smem);
     }
   }
-  float* Cz = C + (int64_t)blockIdx.z * cstride;
+  float* Cz = C + (int64_t)bz * cstride;
   double ss = 0.0;
 #pragma unroll
   for (int tm = 0; tm < T::TM; ++tm)
@@ -82,7 +91,7 @@ k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, in
     if (lane_id() == 0) red[wave_id()] = ss;
     __syncthreads();
     if (threadIdx.x == 0)
-      sums[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+      sums[(int64_t)bxy * gx + bxx] = red[0] + red[1] + red[2] + red[3];
   }
 }
 
@@ -121,13 +130,14 @@ static void gemm_launch(const float* A, int64_t lda, const float* B, int64_t ldb
                         const float* X, double* sums, hipStream_t s, const int* gate = nullptr) {
   // 64-row tiles when M is not a multiple of 128 (no half-empty last row of tiles)
   const int bm = gemm_rows(M);
-  dim3 grid((N + 127) / 128, (M + bm - 1) / bm, p.splits);
+  const int gx = (N + 127) / 128, gy = (M + bm - 1) / bm, ngroups = gx * p.splits;
+  const dim3 grid((unsigned)(((ngroups + 7) / 8) * 8 * gy));
   if (bm == 64)
     hipLaunchKernelGGL((k_gemm<64, 128, 1, 4, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate);
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate, gx, gy, ngroups);
   else
     hipLaunchKernelGGL((k_gemm<128, 128, 2, 2, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate);
+                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate, gx, gy, ngroups);
 }
 
 // out[i] = sum over splits of part[s * count + i], in a fixed order, fp64
