@@ -204,6 +204,11 @@ def test_joint_refresh_matches_the_per_matrix_sweeps(gpu_lib, monkeypatch, name,
 
 
 _RIGHT_TRIO = {"shapes": ((1100, 1012), (1030, 1016), (700, 96)), "tau": 3, "steps": 6}
+# ranks in the projection's middle tiers: 64 x 64 tiles with fp64 partial
+# sums (32 < r <= 64) and one 128 x 64 rank tile over 1024-term slices
+# (64 < r <= 128)
+_RIGHT_TRIO_R48 = {"shapes": ((1100, 1012), (1030, 1016), (700, 300)), "tau": 3, "steps": 6, "rank": 48}
+_RIGHT_TRIO_R100 = {"shapes": ((1100, 1012), (1030, 1016), (700, 300)), "tau": 3, "steps": 6, "rank": 100}
 
 
 @pytest.mark.parametrize("name,override,select,store", [
@@ -213,6 +218,8 @@ _RIGHT_TRIO = {"shapes": ((1100, 1012), (1030, 1016), (700, 96)), "tau": 3, "ste
     ("seats64_left", _RIGHT_TRIO, "approx_bf16", "fp32"),
     ("conv_50", {"tau": 3}, "approx", "bf16"),             # bf16 gradients and error buffers
     ("seats64_left", _RIGHT_TRIO, "approx", "bf16"),
+    ("seats64_left", _RIGHT_TRIO_R48, "approx", "fp32"),
+    ("seats64_left", _RIGHT_TRIO_R100, "approx", "fp32"),
 ])
 def test_grouped_selection_steps_match_the_per_matrix_launches(gpu_lib, monkeypatch, name, override, select,
                                                                store):
