@@ -53,6 +53,15 @@
  * this off.
  * While profiling is enabled the matrices run in order on `stream`.  The
  * environment variable GLR_LANES, read by glr_create, lowers the stream count.
+ * Tuning switches of the refresh, also read by glr_create (defaults in
+ * brackets; other values change the floating-point path): GLR_JAC_FLOOR=k
+ * sets the convergence measure's floor f = 2^-k max_k |w_k| [10];
+ * GLR_JAC_SORT=0|1|2 reorders the rows by descending norm never, before
+ * every sweep or before the first only [1]; GLR_JAC_INNER=1..16 sets the
+ * cyclic sweeps of each group solve [1]; GLR_SUB_ITERS sets the cap of the
+ * tau = 1 block iterations after a warm start [4].  GLR_GROUP_PARTS and
+ * GLR_GROUP_SPLIT=0 set the parts of a grouped selection step [2 when there
+ * are streams for them] (same results).
  *
  * glr_step only enqueues: it never waits for the device (refresh steps
  * included).  A refresh enqueues a budget of Jacobi sweeps; the sweeps after
