@@ -117,12 +117,13 @@ def group_work(wl, name, esz=4):
         elif name == "proj":
             w = (2.0 * esz * N * mn + 4.0 * N * r * D, 2.0 * r * d * D * N, 0, 0)
         elif name == "resid_opt":
-            # G, E read and E written per worker; Mbar read and Ebar written;
-            # X and the optimizer state read and written.  Products: P Q^(i)
-            # per worker, and Ghat = P Rbar as a product of its own up to rank
-            # 128 (above it Ghat is the mean of the workers' products)
+            # G, E read and E written per worker; Ebar written (the mean of
+            # the stored residuals, summed in registers); X and the optimizer
+            # state read and written.  Products: P Q^(i) per worker, and
+            # Ghat = P Rbar as a product of its own up to rank 128 (above it
+            # Ghat is the mean of the workers' products)
             prods = N if r > 128 else N + 1
-            w = ((3.0 * esz * N + 8 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * prods, 0, 0)
+            w = ((3.0 * esz * N + 4 + (24 if adam else 16)) * mn + 4.0 * N * r * D, 2.0 * r * d * D * prods, 0, 0)
         elif name.startswith("jac_") and not sub:
             w = jacobi_work(name[4:], d)
         elif name.startswith("rr_") and sub:

@@ -456,8 +456,10 @@ hipError_t launch_rbar(const MatView& v, hipStream_t s) {
 // S5 + S7 + S8 fused, one pass over a ROWS x 64 tile of the m x n layout:
 //   C^(i) = (P Q^(i)) in the caller's layout (rank-r MFMA product)
 //   E^(i) <- (G^(i) - C^(i)) + E^(i)
-//   Ghat  = P Rbar;  Ebar = Mbar - Ghat (the mean of the E^(i) by
-//   linearity; with bf16 storage the mean of the stored, rounded E^(i));
+//   Ghat  = P Rbar;  Ebar = the mean of the stored E^(i) (summed in
+//   registers as they are written: Mbar - Ghat equals it in real
+//   arithmetic, but when the residual is small against Mbar that difference
+//   keeps only the low bits of two nearly equal fp32 values);
 //   optimizer on X with Ghat.
 // MFMA rows are tile rows and lanes are tile columns, so that a load or
 // store of one accumulator register moves two whole 128-byte rows of 32
@@ -498,15 +500,12 @@ __device__ __forceinline__ void resid_opt_at(const ST* __restrict__ G, ST* __res
       const int64_t row = r0 + geo.row(tm, v);
       ob[tm][v] = (cok && row < m) ? (uint32_t)((row * n + cc) * 4) : kBufNone;
     }
-  // with bf16 storage Ebar is the mean of the stored residuals
-  constexpr bool B16 = sizeof(ST) == 2;
-  float esum[B16 ? TM : 1][16];
-  if (B16) {
+  // Ebar: the mean of the stored residuals
+  float esum[TM][16];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) esum[B16 ? tm : 0][v] = 0.f;
-  }
+    for (int v = 0; v < 16; ++v) esum[tm][v] = 0.f;
   for (int wk = 0; wk < N; ++wk) {
     const BufRsrc Gi = buf_rsrc_s(G + (int64_t)wk * mn, mn);
     const BufRsrc Ei = buf_rsrc_s(E + (int64_t)wk * mn, mn);
@@ -539,7 +538,7 @@ __device__ __forceinline__ void resid_opt_at(const ST* __restrict__ G, ST* __res
         // (G - P Q) + E: G and P Q nearly cancel, E is the small part
         const float e = (gv[tm][v] - tile.acc[tm][0][v]) + eo[tm][v];
         buf_ste<ST>(Ei, ob[tm][v], e);
-        if (B16) esum[B16 ? tm : 0][v] += stored<ST>(e);
+        esum[tm][v] += stored<ST>(e);
       }
   }
 
@@ -555,7 +554,6 @@ __device__ __forceinline__ void resid_opt_at(const ST* __restrict__ G, ST* __res
     tile.run(la, lb, r, smem);
   }
   const BufRsrc Xr = buf_rsrc(X, bytes), S1r = buf_rsrc(S1, bytes), Ebr = buf_rsrc(Ebar, bytes);
-  const BufRsrc Mr = buf_rsrc(Mbar, bytes);
   const BufRsrc S2r = buf_rsrc(OPT == 1 ? S2 : S1, bytes);
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
@@ -580,13 +578,15 @@ __device__ __forceinline__ void resid_opt_at(const ST* __restrict__ G, ST* __res
         }
         buf_st(S1r, o, s1);
       }
-      const float eb = B16 ? esum[B16 ? tm : 0][v] / (float)(N > 0 ? N : 1) : buf_ld(Mr, o) - gh;
+      const float eb = esum[tm][v] / (float)(N > 0 ? N : 1);
       buf_st(Ebr, o, op.ef ? eb : 0.0f);
       buf_st(Xr, o, xv);
     }
 }
+// (the stored residuals' running sum for Ebar takes 32 registers per lane
+// beside the rest, so three waves per SIMD instead of four, without spills)
 template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restrict__ Ebar,
             const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Rbar,
             const float* __restrict__ Ut,
@@ -596,8 +596,7 @@ k_resid_opt(const float* __restrict__ G, float* __restrict__ E, float* __restric
   resid_opt_at<OPT, RIGHT, ROWS, RO_COLS, float>(G, E, Ebar, Mbar, Q, Rbar, Ut, J, X, S1, S2, m, n, d, D, r, N,
                                                  op, blockIdx.x, blockIdx.y);
 }
-// the same with bf16 storage: the stored residuals' running sum (for Ebar)
-// takes 32 more registers per lane, so three waves per SIMD instead of four
+// the same with bf16 storage
 template <int OPT, bool RIGHT, int ROWS, int RO_COLS>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 k_resid_opt16(const bf16_t* __restrict__ G, bf16_t* __restrict__ E, float* __restrict__ Ebar,
@@ -616,8 +615,7 @@ k_resid_opt16(const bf16_t* __restrict__ G, bf16_t* __restrict__ E, float* __res
 // worker, so that the MFMAs run back to back over the whole rank-r
 // contraction.  Then E^(w) <- (G^(w) - P Q^(w)) + E^(w) for each worker,
 // Ghat = (1/N) sum_w P Q^(w) (= P Rbar by linearity, with no product of its
-// own), Ebar = Mbar - Ghat (with bf16 storage the mean of the stored
-// residuals) and the optimizer on X.  More than kNW workers take several
+// own), Ebar = the mean of the stored residuals and the optimizer on X.  More than kNW workers take several
 // groups (MULTI), the products of the earlier groups summed in registers.
 constexpr int kNW = 4;
 constexpr int kNWTile = 64;
@@ -667,12 +665,9 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
 #pragma unroll
     for (int v = 0; v < 16; ++v) gs[MULTI ? v : 0] = 0.f;
   }
-  constexpr bool B16 = sizeof(ST) == 2;
-  float esum[B16 ? 16 : 1];
-  if (B16) {
+  float esum[16];   // the stored residuals' sum over the workers (for Ebar)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) esum[B16 ? v : 0] = 0.f;
-  }
+  for (int v = 0; v < 16; ++v) esum[v] = 0.f;
   f32x16 acc[kNW];
   const int64_t rD = (int64_t)r * D;
   const int nk = (r + BK - 1) / BK;
@@ -742,7 +737,7 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
         // (G - P Q) + E: G and P Q nearly cancel, E is the small part
         const float e = (gv[v] - acc[w][v]) + eo[v];
         buf_ste<ST>(Ew, ob[v], e);
-        if (B16) esum[B16 ? v : 0] += stored<ST>(e);
+        esum[v] += stored<ST>(e);
         if (MULTI) gs[MULTI ? v : 0] += acc[w][v];
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -750,7 +745,6 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
   }
   const float inv_n = 1.0f / (float)N;
   const BufRsrc Xr = buf_rsrc(X, bytes), S1r = buf_rsrc(S1, bytes), Ebr = buf_rsrc(Ebar, bytes);
-  const BufRsrc Mr = buf_rsrc(Mbar, bytes);
   const BufRsrc S2r = buf_rsrc(OPT == 1 ? S2 : S1, bytes);
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -776,7 +770,7 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
       buf_st(S2r, o, s2);
     }
     buf_st(S1r, o, s1);
-    buf_st(Ebr, o, B16 ? esum[B16 ? v : 0] * inv_n : buf_ld(Mr, o) - gh);
+    buf_st(Ebr, o, esum[v] * inv_n);
     buf_st(Xr, o, xv);
     if ((v & 3) == 3) __builtin_amdgcn_sched_barrier(0);
   }
@@ -991,7 +985,7 @@ __device__ __forceinline__ void g_resid_opt_at(const GroupMat* __restrict__ gm, 
                                        local % gx, local / gx);
 }
 template <int OPT, bool RIGHT>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 k_g_resid_opt(const GroupMat* __restrict__ gm, const int* __restrict__ first, int num, OptParams op) {
   g_resid_opt_at<OPT, RIGHT, float>(gm, first, num, op);
 }

@@ -24,6 +24,17 @@ def test_trajectory_parity(gpu_lib, name):
     assert sum(1 for r in log if "t" in r) == wl.steps * len(wl.shapes)
 
 
+@pytest.mark.parametrize("name,over", [("mid_left", {"rank": 48}), ("ragged_right", {"rank": 48}),
+                                       ("mid_left", {"rank": 64})])
+def test_trajectory_parity_middle_ranks(gpu_lib, name, over):
+    # 32 < r <= 64: the projection's 64 x 64 tier with fp64 partial sums, the
+    # residual's 64-row tiles
+    _print_case(name, **over)
+    wl = get_workload(name, **over)
+    log = run_parity(gpu_lib, wl)
+    assert sum(1 for r in log if "t" in r) == wl.steps * len(wl.shapes)
+
+
 def test_many_shapes_vector_case_and_full_rank(gpu_lib):
     # d = 1 (the vector problem), r >= d, square, both orientations, ragged tiles
     _print_case("mixed_small")
@@ -165,6 +176,7 @@ def test_bf16_selection_parity(gpu_lib, name):
     ("one_256x128", {}, {}), ("ragged_right", {}, {}), ("mid_left", {}, {}), ("single_worker", {}, {}),
     ("wide_left", {}, {}), ("wide_right", {}, {"opt": "msgd", "lr": 0.01}), ("tau1_left", {}, {}),
     ("tau1_right", {}, {}), ("ragged_right", {"refresh": "full"}, {}), ("tiny_left", {"select": "exact"}, {}),
+    ("mid_left", {}, {"rank": 48}), ("two_tiles_left", {}, {}), ("two_tiles_right", {}, {}),
 ])
 def test_bf16_storage_parity(gpu_lib, name, kw, wkw):
     # G^(i) and E^(i) stored in bf16: trajectory parity with the oracle's same
