@@ -35,6 +35,19 @@ def test_trajectory_parity_middle_ranks(gpu_lib, name, over):
     assert sum(1 for r in log if "t" in r) == wl.steps * len(wl.shapes)
 
 
+@pytest.mark.parametrize("name,over", [("wide_left", {"workers": 6}),
+                                       ("wide_right", {"workers": 5, "opt": "msgd", "lr": 0.01}),
+                                       ("mid_left", {"workers": 7, "rank": 100})])
+def test_trajectory_parity_more_workers(gpu_lib, name, over):
+    # more workers than one pass of the wide residual kernel holds (its
+    # groups of four workers, the products of the earlier groups summed in
+    # registers), and the rank <= 128 path with seven workers
+    _print_case(name, **over)
+    wl = get_workload(name, **over)
+    log = run_parity(gpu_lib, wl)
+    assert sum(1 for r in log if "t" in r) == wl.steps * len(wl.shapes)
+
+
 def test_many_shapes_vector_case_and_full_rank(gpu_lib):
     # d = 1 (the vector problem), r >= d, square, both orientations, ragged tiles
     _print_case("mixed_small")
