@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace glr {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -26,6 +28,9 @@ __device__ __forceinline__ float4 load_nt4(const float* p) {
 // outside the array passes kBufNone.
 typedef __amdgpu_buffer_rsrc_t BufRsrc;
 constexpr uint32_t kBufNone = 0xFFFFFFFFu;
+// the same for a 16-byte access to an array below 2^31 bytes (no dword of
+// it wraps around to a small offset)
+constexpr uint32_t kBufNone4 = 0x80000000u;
 __device__ __forceinline__ BufRsrc buf_rsrc(const float* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)bytes, 0x00020000);
 }
@@ -156,7 +161,7 @@ struct LoadK {
 
   __device__ LoadK(const ST* b, const ST* b2, int64_t ld_, int row0, int nrows_, int K_,
                    const int* rows) : base(b), base2(b2), ld(ld_), nrows(nrows_), K(K_) {
-    vec = ((ld & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
+    vec = ((ld & 3) == 0) && ((K & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
           (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & kAl) == 0));
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
@@ -175,25 +180,38 @@ struct LoadK {
     if (FUSED) x += ld_e(base2, off);
     return x;
   }
+  // The float4 and the element-wise paths are separate loops under the
+  // wave-uniform `vec`: inside one loop the compiler merged the loads of the
+  // two paths into shared registers and then waited for every load in
+  // flight before issuing the next one.
   __device__ __forceinline__ void fetch(int k0) {
+    if (vec) {
+      // K is a multiple of 4 here, and so is k: k < K covers k + 3
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int k = k0 + 4 * kq[i];
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (roff[i] >= 0 && k < K) {
+          x = ld_e4(base, roff[i] + k);
+          if (FUSED) {
+            const float4 y = ld_e4(base2, roff[i] + k);
+            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+          }
+        }
+        v[i] = x;
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       int k = k0 + 4 * kq[i];
       float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
       if (roff[i] >= 0) {
         int64_t off = roff[i] + k;
-        if (vec && k + 3 < K) {
-          x = ld_e4(base, off);
-          if (FUSED) {
-            float4 y = ld_e4(base2, off);
-            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
-          }
-        } else {
-          if (k + 0 < K) x.x = ld1(off + 0);
-          if (k + 1 < K) x.y = ld1(off + 1);
-          if (k + 2 < K) x.z = ld1(off + 2);
-          if (k + 3 < K) x.w = ld1(off + 3);
-        }
+        if (k + 0 < K) x.x = ld1(off + 0);
+        if (k + 1 < K) x.y = ld1(off + 1);
+        if (k + 2 < K) x.z = ld1(off + 2);
+        if (k + 3 < K) x.w = ld1(off + 3);
       }
       v[i] = x;
     }
@@ -232,7 +250,7 @@ struct LoadR {
   __device__ LoadR(const ST* b, const ST* b2, int64_t ld_, int r0_, int nr_, int K_,
                    const int* rows_ = nullptr)
       : base(b), base2(b2), rows(rows_), ld(ld_), r0(r0_), nr(nr_), K(K_) {
-    vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
+    vec = ((ld & 3) == 0) && ((r0 & 3) == 0) && ((nr & 3) == 0) && ((reinterpret_cast<uintptr_t>(b) & kAl) == 0) &&
           (!FUSED || ((reinterpret_cast<uintptr_t>(b2) & kAl) == 0));
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
@@ -246,7 +264,36 @@ struct LoadR {
     if (FUSED) x += ld_e(base2, off);
     return x;
   }
+  // float4 and element-wise paths as separate loops under the wave-uniform
+  // `vec` (see LoadK::fetch)
   __device__ __forceinline__ void fetch(int k0) {
+    if (vec) {
+      // the gathered row indices first, so that one wait covers them all
+      // (unconditional loads at clamped k, the data loads below being masked:
+      // a load under a branch is widened inside the branch, which waits for it)
+      int kr[NV];
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int k = k0 + kl[i];
+        kr[i] = k;
+        if (GATHER && K > 0) kr[i] = rows[k < K ? k : K - 1];
+      }
+      // nr and r are multiples of 4 here: r < nr covers r + 3
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int k = k0 + kl[i], r = r0 + 4 * rq[i];
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (kl[i] < BK && k < K && r < nr) {
+          x = ld_e4(base, (int64_t)kr[i] * ld + r);
+          if (FUSED) {
+            const float4 y = ld_e4(base2, (int64_t)kr[i] * ld + r);
+            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+          }
+        }
+        v[i] = x;
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       int k = k0 + kl[i];
@@ -255,20 +302,67 @@ struct LoadR {
       if (kl[i] < BK && k < K) {
         const int64_t kr = GATHER ? (int64_t)rows[k] : (int64_t)k;
         int64_t off = kr * ld + r;
-        if (vec && r + 3 < nr) {
-          x = ld_e4(base, off);
-          if (FUSED) {
-            float4 y = ld_e4(base2, off);
-            x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
-          }
-        } else {
-          if (r + 0 < nr) x.x = ld1(off + 0);
-          if (r + 1 < nr) x.y = ld1(off + 1);
-          if (r + 2 < nr) x.z = ld1(off + 2);
-          if (r + 3 < nr) x.w = ld1(off + 3);
-        }
+        if (r + 0 < nr) x.x = ld1(off + 0);
+        if (r + 1 < nr) x.y = ld1(off + 1);
+        if (r + 2 < nr) x.z = ld1(off + 2);
+        if (r + 3 < nr) x.w = ld1(off + 3);
       }
       v[i] = x;
+    }
+  }
+  template <int P>
+  __device__ __forceinline__ void put(float* s) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (kl[i] >= BK) continue;
+      *reinterpret_cast<float4*>(s + kl[i] * P + 4 * rq[i]) = v[i];
+    }
+  }
+};
+
+// LoadR's float4 case on a buffer descriptor: element (r, k) of the fp32
+// operand at byte off0 + 4 (krow(k) ld + r) of the descriptor's array (below
+// 2^31 bytes; ld, r0 and nr multiples of 4).  Every load is issued
+// unconditionally, an element outside the slice or the operand reading 0
+// through an offset past the array, so a fetch is one run of loads with no
+// branch between them (under branches, the compiler's waits for loads it
+// cannot track made each load wait for the previous ones).
+template <int R, int BK, bool GATHER>
+struct LoadRB {
+  static constexpr bool kSwz = false;
+  static constexpr int RQ = R / 4;
+  static constexpr int NV = (BK * RQ + kThreads - 1) / kThreads;
+  BufRsrc rs;
+  uint32_t off0;
+  const int* rows;
+  int ld, r0, nr, K;
+  int kl[NV], rq[NV];
+  float4 v[NV];
+
+  __device__ LoadRB(BufRsrc rs_, uint32_t off0_, int ld_, int r0_, int nr_, int K_, const int* rows_ = nullptr)
+      : rs(rs_), off0(off0_), rows(rows_), ld(ld_), r0(r0_), nr(nr_), K(K_) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + kThreads * i;
+      kl[i] = idx / RQ;
+      rq[i] = idx % RQ;
+    }
+  }
+  __device__ __forceinline__ void fetch(int k0) {
+    int kr[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = k0 + kl[i];
+      kr[i] = k;
+      if (GATHER && K > 0) kr[i] = rows[k < K ? k : K - 1];   // clamped: the data load below is dropped
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = k0 + kl[i], r = r0 + 4 * rq[i];
+      const bool ok = kl[i] < BK && k < K && r < nr;
+      const uint32_t off = ok ? off0 + 4u * (uint32_t)(kr[i] * ld + r) : kBufNone4;
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0);
+      v[i] = make_float4(__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3]));
     }
   }
   template <int P>

@@ -637,7 +637,9 @@ __device__ __forceinline__ void nw_slice(const float* smem, int soff, int qoff, 
     }
   }
 }
-template <int OPT, bool RIGHT, bool MULTI, class ST>
+// VEC: the operand slices load through buffer descriptors as float4s (d and
+// D multiples of 4, U^T and every group's Q within 2^31 bytes)
+template <int OPT, bool RIGHT, bool MULTI, class ST, bool VEC>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Ebar,
            const float* __restrict__ Mbar, const float* __restrict__ Q, const float* __restrict__ Ut,
@@ -677,32 +679,35 @@ k_resid_nw(const ST* __restrict__ G, ST* __restrict__ E, float* __restrict__ Eba
     for (int w = 0; w < kNW; ++w)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[w][v] = 0.f;
-    LoadR<T, BK, false, true> ls(Ut, nullptr, d, s0, (int)d, r, J);
-    // the workers' Q slices share one geometry: loader w reads worker w0 + w
-    // (a worker beyond N reads nothing: contraction length 0)
-    LoadR<T, BK, false> lq(Q + (int64_t)w0 * rD, nullptr, D, q0, (int)D, r);
-    const bool qvec = lq.vec;   // float4 loads need every worker's slice 16-byte aligned
-    float4 qv[kNW][decltype(lq)::NV];
+    // one loader per worker slot, each loading into registers of its own, so
+    // that the loads of all slots are in flight together (one loader moved
+    // from slot to slot made each slot's loads wait for the previous slot's
+    // to land); a slot beyond N reads nothing (contraction length 0).  VEC:
+    // buffer loads through one descriptor for U^T and one for this group's Q.
+    static_assert(kNW == 4, "one loader per worker slot");
+    using LS = std::conditional_t<VEC, LoadRB<T, BK, true>, LoadR<T, BK, false, true>>;
+    using LQ = std::conditional_t<VEC, LoadRB<T, BK, false>, LoadR<T, BK, false>>;
+    const BufRsrc ur = buf_rsrc(Ut, VEC ? (uint32_t)(d * d * 4) : 0u);
+    const BufRsrc qr = buf_rsrc(Q + (int64_t)w0 * rD, VEC ? (uint32_t)(nw * rD * 4) : 0u);
+    auto make_s = [&]() {
+      if constexpr (VEC) return LS(ur, 0u, (int)d, s0, (int)d, r, J);
+      else return LS(Ut, nullptr, d, s0, (int)d, r, J);
+    };
+    auto slot = [&](int w) {
+      if constexpr (VEC) return LQ(qr, (uint32_t)((w < nw ? w : 0) * rD * 4), (int)D, q0, (int)D, w < nw ? r : 0);
+      else return LQ(Q + (int64_t)(w0 + (w < nw ? w : 0)) * rD, nullptr, D, q0, (int)D, w < nw ? r : 0);
+    };
+    LS ls = make_s();
+    LQ lq[kNW] = {slot(0), slot(1), slot(2), slot(3)};
     auto fetch = [&](int k0) {
       ls.fetch(k0);
 #pragma unroll
-      for (int w = 0; w < kNW; ++w) {
-        lq.base = Q + (int64_t)(w0 + (w < nw ? w : 0)) * rD;
-        lq.vec = qvec && ((reinterpret_cast<uintptr_t>(lq.base) & 15) == 0);
-        lq.K = w < nw ? r : 0;
-        lq.fetch(k0);
-#pragma unroll
-        for (int i = 0; i < decltype(lq)::NV; ++i) qv[w][i] = lq.v[i];
-      }
+      for (int w = 0; w < kNW; ++w) lq[w].fetch(k0);
     };
     auto put = [&]() {
       ls.template put<PT>(smem);
 #pragma unroll
-      for (int w = 0; w < kNW; ++w) {
-#pragma unroll
-        for (int i = 0; i < decltype(lq)::NV; ++i) lq.v[i] = qv[w][i];
-        lq.template put<PT>(smem + (1 + w) * SL);
-      }
+      for (int w = 0; w < kNW; ++w) lq[w].template put<PT>(smem + (1 + w) * SL);
     };
     fetch(0);
     put();
@@ -787,9 +792,20 @@ static hipError_t launch_resid_opt_st(const MatView& v, const OptParams& o, hipS
     const unsigned rt = (unsigned)((v.m + kNWTile - 1) / kNWTile), ct = (unsigned)((v.n + kNWTile - 1) / kNWTile);
     const int rows_fast = ct <= 65535u ? 1 : 0;
     dim3 gw(rows_fast ? rt : ct, rows_fast ? ct : rt);
+    // the conditions of the buffer loaders: float4 rows, and U^T and one
+    // group's Q within 2^31 bytes
+    const bool vec = v.d % 4 == 0 && v.D % 4 == 0 && (reinterpret_cast<uintptr_t>(v.Ut) & 3) == 0 &&
+                     (reinterpret_cast<uintptr_t>(v.Q) & 3) == 0 && v.d * v.d * 4 < ((int64_t)1 << 31) &&
+                     (int64_t)kNW * v.r * v.D * 4 < ((int64_t)1 << 31);
 #define GLR_RW(OPT, R, MU)                                                                                   \
-  hipLaunchKernelGGL((k_resid_nw<OPT, R, MU, ST>), gw, dim3(kThreads), 0, s, G, E, v.Ebar, v.Mbar, v.Q, v.Ut, v.J, \
-                     v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o, rows_fast)
+  do {                                                                                                       \
+    if (vec)                                                                                                 \
+      hipLaunchKernelGGL((k_resid_nw<OPT, R, MU, ST, true>), gw, dim3(kThreads), 0, s, G, E, v.Ebar, v.Mbar,  \
+                         v.Q, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o, rows_fast);       \
+    else                                                                                                     \
+      hipLaunchKernelGGL((k_resid_nw<OPT, R, MU, ST, false>), gw, dim3(kThreads), 0, s, G, E, v.Ebar, v.Mbar, \
+                         v.Q, v.Ut, v.J, v.X, v.S1, v.S2, v.m, v.n, v.d, v.D, v.r, v.N, o, rows_fast);       \
+  } while (0)
 #define GLR_RW2(OPT, R) do { if (multi) GLR_RW(OPT, R, true); else GLR_RW(OPT, R, false); } while (0)
     if (o.opt == 0)      { if (v.right) GLR_RW2(0, true); else GLR_RW2(0, false); }
     else if (o.opt == 1) { if (v.right) GLR_RW2(1, true); else GLR_RW2(1, false); }
