@@ -64,6 +64,35 @@ __device__ __forceinline__ float4 ld_e4(const bf16_t* p, int64_t i) {
   return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
                      __uint_as_float(u.y & 0xFFFF0000u));
 }
+// four elements as loaded (fp32: a float4, bf16: two dwords), widened only
+// where the value is used, so that a run of loads is not interrupted by a
+// wait for each one
+template <class ST>
+struct Raw4 {
+  float4 v;
+};
+template <>
+struct Raw4<bf16_t> {
+  uint2 v;
+};
+__device__ __forceinline__ Raw4<float> ld_raw4(const float* p, int64_t i) {
+  return {*reinterpret_cast<const float4*>(p + i)};
+}
+__device__ __forceinline__ Raw4<bf16_t> ld_raw4(const bf16_t* p, int64_t i) {
+  return {*reinterpret_cast<const uint2*>(p + i)};
+}
+__device__ __forceinline__ float4 widen4(const Raw4<float>& x) { return x.v; }
+__device__ __forceinline__ float4 widen4(const Raw4<bf16_t>& x) {
+  return make_float4(__uint_as_float(x.v.x << 16), __uint_as_float(x.v.x & 0xFFFF0000u),
+                     __uint_as_float(x.v.y << 16), __uint_as_float(x.v.y & 0xFFFF0000u));
+}
+template <class ST>
+__device__ __forceinline__ Raw4<ST> raw4_zero() {
+  Raw4<ST> z;
+  if constexpr (sizeof(ST) == 2) z.v = make_uint2(0u, 0u);
+  else z.v = make_float4(0.f, 0.f, 0.f, 0.f);
+  return z;
+}
 // the same, streaming (non-temporal)
 __device__ __forceinline__ float4 ld_nt_e4(const float* p, int64_t i) { return load_nt4(p + i); }
 __device__ __forceinline__ float4 ld_nt_e4(const bf16_t* p, int64_t i) {
@@ -143,7 +172,10 @@ __device__ __forceinline__ constexpr int lds_swz(int k) { return 4 * ((k >> 3) &
 // The transposing LDS store puts eight rows x eight float4 k-groups of a
 // half-wave in one LDS row pair; with the (R + 4)-float row pitch alone
 // those 32 stores meet in 8 banks, and the swizzle spreads them over 32.
-template <int R, int BK, bool FUSED, bool GATHER, class ST = float>
+// VEC: the caller has checked on the host that `vec` holds (then only the
+// float4 path is compiled, and its loads are widened and added in put(), so
+// that a fetch issues all its loads before any wait).
+template <int R, int BK, bool FUSED, bool GATHER, class ST = float, bool VEC = false>
 struct LoadK {
   static constexpr bool kSwz = true;
   static_assert(R % 16 == 0, "swizzle stays inside the slice");
@@ -157,7 +189,8 @@ struct LoadK {
   bool vec;
   int64_t roff[NV];
   int rl[NV], kq[NV];
-  float4 v[NV];
+  float4 v[VEC ? 1 : NV];
+  Raw4<ST> ra[VEC ? NV : 1], rb[VEC && FUSED ? NV : 1];   // VEC: the loads from base and base2
 
   __device__ LoadK(const ST* b, const ST* b2, int64_t ld_, int row0, int nrows_, int K_,
                    const int* rows) : base(b), base2(b2), ld(ld_), nrows(nrows_), K(K_) {
@@ -185,6 +218,22 @@ struct LoadK {
   // two paths into shared registers and then waited for every load in
   // flight before issuing the next one.
   __device__ __forceinline__ void fetch(int k0) {
+    if constexpr (VEC) fetch_raw(k0);
+    else fetch_rt(k0);
+  }
+  __device__ __forceinline__ void fetch_raw(int k0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = k0 + 4 * kq[i];
+      ra[i] = raw4_zero<ST>();
+      if (FUSED) rb[FUSED ? i : 0] = raw4_zero<ST>();
+      if (roff[i] >= 0 && k < K) {
+        ra[i] = ld_raw4(base, roff[i] + k);
+        if (FUSED) rb[FUSED ? i : 0] = ld_raw4(base2, roff[i] + k);
+      }
+    }
+  }
+  __device__ __forceinline__ void fetch_rt(int k0) {
     if (vec) {
       // K is a multiple of 4 here, and so is k: k < K covers k + 3
 #pragma unroll
@@ -216,23 +265,36 @@ struct LoadK {
       v[i] = x;
     }
   }
+  __device__ __forceinline__ float4 value(int i) const {
+    if constexpr (VEC) {
+      float4 x = widen4(ra[i]);
+      if (FUSED) {
+        const float4 y = widen4(rb[FUSED ? i : 0]);
+        x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+      }
+      return x;
+    } else {
+      return v[i];
+    }
+  }
   template <int P>
   __device__ __forceinline__ void put(float* s) const {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       if (rl[i] >= R) continue;
       const int k = 4 * kq[i], c = rl[i] ^ lds_swz(k);   // k .. k+3 share the swizzle
-      s[(k + 0) * P + c] = v[i].x;
-      s[(k + 1) * P + c] = v[i].y;
-      s[(k + 2) * P + c] = v[i].z;
-      s[(k + 3) * P + c] = v[i].w;
+      const float4 x = value(i);
+      s[(k + 0) * P + c] = x.x;
+      s[(k + 1) * P + c] = x.y;
+      s[(k + 2) * P + c] = x.z;
+      s[(k + 3) * P + c] = x.w;
     }
   }
 };
 
 // Element (r, k) at base[krow(k) * ld + r] (+ base2): contiguous along r;
-// krow(k) = rows[k] when GATHER, else k.  ST as for LoadK.
-template <int R, int BK, bool FUSED, bool GATHER = false, class ST = float>
+// krow(k) = rows[k] when GATHER, else k.  ST and VEC as for LoadK.
+template <int R, int BK, bool FUSED, bool GATHER = false, class ST = float, bool VEC = false>
 struct LoadR {
   static constexpr bool kSwz = false;
   static constexpr int RQ = R / 4;
@@ -245,7 +307,8 @@ struct LoadR {
   int r0, nr, K;
   bool vec;
   int kl[NV], rq[NV];
-  float4 v[NV];
+  float4 v[VEC ? 1 : NV];
+  Raw4<ST> ra[VEC ? NV : 1], rb[VEC && FUSED ? NV : 1];   // VEC: the loads from base and base2
 
   __device__ LoadR(const ST* b, const ST* b2, int64_t ld_, int r0_, int nr_, int K_,
                    const int* rows_ = nullptr)
@@ -267,17 +330,39 @@ struct LoadR {
   // float4 and element-wise paths as separate loops under the wave-uniform
   // `vec` (see LoadK::fetch)
   __device__ __forceinline__ void fetch(int k0) {
-    if (vec) {
-      // the gathered row indices first, so that one wait covers them all
-      // (unconditional loads at clamped k, the data loads below being masked:
-      // a load under a branch is widened inside the branch, which waits for it)
-      int kr[NV];
+    if constexpr (VEC) fetch_raw(k0);
+    else fetch_rt(k0);
+  }
+  // the gathered row indices first, so that one wait covers them all
+  // (unconditional loads at clamped k, the data loads being masked: a load
+  // under a branch is widened inside the branch, which waits for it)
+  __device__ __forceinline__ void row_indices(int k0, int (&kr)[NV]) const {
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        const int k = k0 + kl[i];
-        kr[i] = k;
-        if (GATHER && K > 0) kr[i] = rows[k < K ? k : K - 1];
+    for (int i = 0; i < NV; ++i) {
+      const int k = k0 + kl[i];
+      kr[i] = k;
+      if (GATHER && K > 0) kr[i] = rows[k < K ? k : K - 1];
+    }
+  }
+  __device__ __forceinline__ void fetch_raw(int k0) {
+    int kr[NV];
+    row_indices(k0, kr);
+    // nr and r are multiples of 4 here: r < nr covers r + 3
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int k = k0 + kl[i], r = r0 + 4 * rq[i];
+      ra[i] = raw4_zero<ST>();
+      if (FUSED) rb[FUSED ? i : 0] = raw4_zero<ST>();
+      if (kl[i] < BK && k < K && r < nr) {
+        ra[i] = ld_raw4(base, (int64_t)kr[i] * ld + r);
+        if (FUSED) rb[FUSED ? i : 0] = ld_raw4(base2, (int64_t)kr[i] * ld + r);
       }
+    }
+  }
+  __device__ __forceinline__ void fetch_rt(int k0) {
+    if (vec) {
+      int kr[NV];
+      row_indices(k0, kr);
       // nr and r are multiples of 4 here: r < nr covers r + 3
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
@@ -310,12 +395,24 @@ struct LoadR {
       v[i] = x;
     }
   }
+  __device__ __forceinline__ float4 value(int i) const {
+    if constexpr (VEC) {
+      float4 x = widen4(ra[i]);
+      if (FUSED) {
+        const float4 y = widen4(rb[FUSED ? i : 0]);
+        x.x += y.x; x.y += y.y; x.z += y.z; x.w += y.w;
+      }
+      return x;
+    } else {
+      return v[i];
+    }
+  }
   template <int P>
   __device__ __forceinline__ void put(float* s) const {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       if (kl[i] >= BK) continue;
-      *reinterpret_cast<float4*>(s + kl[i] * P + 4 * rq[i]) = v[i];
+      *reinterpret_cast<float4*>(s + kl[i] * P + 4 * rq[i]) = value(i);
     }
   }
 };

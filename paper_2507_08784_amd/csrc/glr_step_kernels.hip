@@ -299,9 +299,10 @@ hipError_t launch_iota_J(const MatView& v, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // S4: Q^(i) = P^T M^(i), r x D per worker (both orientations), with
 // P^T[k][a] = Ut[J[k]][a] and M^(i) = G^(i) + E^(i) fused into the load (G
-// and E in the storage type ST, widened to fp32 as they load).
+// and E in the storage type ST, widened to fp32 as they load).  VEC: every
+// operand slice loads as whole float4s (proj_vec on the host).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST, bool VEC = false>
 __device__ __forceinline__ void proj_at(const ST* __restrict__ G, const ST* __restrict__ E,
                                         const float* __restrict__ Ut, const int* __restrict__ J,
                                         float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice,
@@ -329,14 +330,14 @@ __device__ __forceinline__ void proj_at(const ST* __restrict__ G, const ST* __re
 #pragma unroll
         for (int v = 0; v < 16; ++v) dacc[FLUSH ? tm : 0][FLUSH ? tn : 0][v] = 0.0;
   }
-  LoadK<BM, 32, false, true> la(Ut + k0, nullptr, d, m0, r, klen, J);
+  LoadK<BM, 32, false, true, float, VEC> la(Ut + k0, nullptr, d, m0, r, klen, J);
   if (RIGHT) {
     // M^(i) oriented: Mo[a][b] = M[b][a], M is D x d row-major
-    LoadK<BN, 32, true, false, ST> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
+    LoadK<BN, 32, true, false, ST, VEC> lb(Gi + k0, Ei + k0, d, n0, (int)D, klen, nullptr);
     if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
     else tile.run(la, lb, klen, smem);
   } else {
-    LoadR<BN, 32, true, false, ST> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
+    LoadR<BN, 32, true, false, ST, VEC> lb(Gi + k0 * D, Ei + k0 * D, D, n0, (int)D, klen);
     if constexpr (FLUSH) tile.run(la, lb, klen, smem, dacc);
     else tile.run(la, lb, klen, smem);
   }
@@ -359,7 +360,7 @@ __device__ __forceinline__ void proj_at(const ST* __restrict__ G, const ST* __re
 // blocks apart, so they run on the same XCD at the same time and the second
 // read of those columns hits that XCD's L2 (blocks go to the XCDs in turn);
 // gy = 1: the 3-D grid (x column tiles, z worker and slice)
-template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST>
+template <int BM, int BN, int WM, int WN, bool RIGHT, bool FLUSH, class ST, bool VEC>
 __global__ void __launch_bounds__(256)
 k_proj(const ST* __restrict__ G, const ST* __restrict__ E, const float* __restrict__ Ut,
        const int* __restrict__ J, float* __restrict__ Qpart, int64_t d, int64_t D, int r, int N, int kslice,
@@ -373,7 +374,15 @@ k_proj(const ST* __restrict__ G, const ST* __restrict__ E, const float* __restri
     bx = tile % gx;
     bz = tile / gx;
   }
-  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST>(G, E, Ut, J, Qpart, d, D, r, N, kslice, bx, by, bz);
+  proj_at<BM, BN, WM, WN, RIGHT, FLUSH, ST, VEC>(G, E, Ut, J, Qpart, d, D, r, N, kslice, bx, by, bz);
+}
+// the conditions under which every loader of the projection takes its
+// float4 path: rows of U^T, G and E in whole float4s (d and D multiples of
+// 4, so every slice start and length is one), and the arrays aligned
+static bool proj_vec(const MatView& v, size_t esz) {
+  const uintptr_t al = 4 * esz - 1;
+  return v.d % 4 == 0 && v.D % 4 == 0 && (reinterpret_cast<uintptr_t>(v.Ut) & 15) == 0 &&
+         (reinterpret_cast<uintptr_t>(v.G) & al) == 0 && (reinterpret_cast<uintptr_t>(v.E) & al) == 0;
 }
 
 template <class ST>
@@ -384,8 +393,12 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
   const int splits = proj_splits(v.d, v.D, r, v.N);
   const int64_t kslice = proj_kslice(v.d, v.D, r, v.N);
   float* const out = splits > 1 ? v.Qpart : v.Q;
+  const bool vec = proj_vec(v, sizeof(ST));
   dim3 grid;
   grid.z = (unsigned)(v.N * splits);
+#define GLR_PROJ1(BM, BN, WM, WN, FL, R, VE)                                                      \
+  hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, R, FL, ST, VE>), gr, dim3(kThreads), 0, s, G, E, v.Ut, \
+                     v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles)
 #define GLR_PROJ(BM, BN, WM, WN, FL)                                                              \
   do {                                                                                            \
     const int gx = (int)((v.D + BN - 1) / BN), gy = (r + BM - 1) / BM;                            \
@@ -394,12 +407,13 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
     gr.x = (unsigned)gx;                                                                          \
     gr.y = (unsigned)gy;                                                                          \
     if (gy > 1) gr = dim3((unsigned)(((ntiles + 7) / 8) * 8 * gy));                               \
-    if (v.right)                                                                                  \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, true, FL, ST>), gr, dim3(kThreads), 0, s, G, E,   \
-                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles);          \
-    else                                                                                          \
-      hipLaunchKernelGGL((k_proj<BM, BN, WM, WN, false, FL, ST>), gr, dim3(kThreads), 0, s, G, E,  \
-                         v.Ut, v.J, out, v.d, v.D, r, v.N, (int)kslice, gx, gy, ntiles);          \
+    if (v.right) {                                                                                \
+      if (vec) GLR_PROJ1(BM, BN, WM, WN, FL, true, true);                                         \
+      else GLR_PROJ1(BM, BN, WM, WN, FL, true, false);                                            \
+    } else {                                                                                      \
+      if (vec) GLR_PROJ1(BM, BN, WM, WN, FL, false, true);                                        \
+      else GLR_PROJ1(BM, BN, WM, WN, FL, false, false);                                           \
+    }                                                                                             \
   } while (0)
   // one rank tile covers all r rows, so G and E are read once.  Up to rank
   // 64 the tile adds its fp32 sums into fp64 every 512 terms; above, the
@@ -412,6 +426,7 @@ static hipError_t launch_proj_st(const MatView& v, hipStream_t s) {
   else if (r <= kProjWideRank) GLR_PROJ(128, 64, 2, 2, false);
   else GLR_PROJ(256, 64, 4, 1, false);
 #undef GLR_PROJ
+#undef GLR_PROJ1
   return hipGetLastError();
 }
 hipError_t launch_proj(const MatView& v, hipStream_t s) {

@@ -33,9 +33,10 @@ namespace glr {
 // The grid is one-dimensional: the gy row tiles of a (column tile, slice)
 // pair run one after another on one XCD (workgroups go to the XCDs in turn,
 // so 8 launch slots apart), so that the slice of B they share is read from
-// HBM once and then from that XCD's L2.
+// HBM once and then from that XCD's L2.  VEC: every operand slice loads as
+// whole float4s (checked by gemm_launch).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool B_KC, int EPI>
+template <int BM, int BN, int WM, int WN, bool B_KC, int EPI, bool VEC>
 __global__ void __launch_bounds__(256)
 k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, int64_t ldb,
        float* __restrict__ C, int64_t ldc, int M, int N, int Kc, int kslice, int64_t cstride,
@@ -53,12 +54,12 @@ k_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ B, in
   const int klen = (Kc - k0 < kslice) ? Kc - k0 : kslice;
   T tile;
   if (klen > 0) {
-    LoadK<BM, 32, false, false> la(A + k0, nullptr, lda, m0, M, klen, nullptr);
+    LoadK<BM, 32, false, false, float, VEC> la(A + k0, nullptr, lda, m0, M, klen, nullptr);
     if (B_KC) {
-      LoadK<BN, 32, false, false> lb(B + k0, nullptr, ldb, n0, N, klen, nullptr);
+      LoadK<BN, 32, false, false, float, VEC> lb(B + k0, nullptr, ldb, n0, N, klen, nullptr);
       tile.run(la, lb, klen, smem);
     } else {
-      LoadR<BN, 32, false> lb(B + (int64_t)k0 * ldb, nullptr, ldb, n0, N, klen);
+      LoadR<BN, 32, false, false, float, VEC> lb(B + (int64_t)k0 * ldb, nullptr, ldb, n0, N, klen);
       tile.run(la, lb, klen, smem);
     }
   }
@@ -132,12 +133,22 @@ static void gemm_launch(const float* A, int64_t lda, const float* B, int64_t ldb
   const int bm = gemm_rows(M);
   const int gx = (N + 127) / 128, gy = (M + bm - 1) / bm, ngroups = gx * p.splits;
   const dim3 grid((unsigned)(((ngroups + 7) / 8) * 8 * gy));
-  if (bm == 64)
-    hipLaunchKernelGGL((k_gemm<64, 128, 1, 4, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate, gx, gy, ngroups);
-  else
-    hipLaunchKernelGGL((k_gemm<128, 128, 2, 2, B_KC, EPI>), grid, dim3(256), 0, s, A, lda, B, ldb, C,
-                       ldc, M, N, Kc, p.kslice, cstride, X, sums, gate, gx, gy, ngroups);
+  // the loaders' float4 conditions for every slice: leading dimensions and
+  // Kc (hence every slice start and length) multiples of 4, B's row length
+  // too when it is read along rows, and both operands 16-byte aligned
+  const bool vec = lda % 4 == 0 && ldb % 4 == 0 && Kc % 4 == 0 && p.kslice % 4 == 0 && (B_KC || N % 4 == 0) &&
+                   (reinterpret_cast<uintptr_t>(A) & 15) == 0 && (reinterpret_cast<uintptr_t>(B) & 15) == 0;
+#define GLR_GEMM(BM, WM, WN, VE)                                                                         \
+  hipLaunchKernelGGL((k_gemm<BM, 128, WM, WN, B_KC, EPI, VE>), grid, dim3(256), 0, s, A, lda, B, ldb, C, \
+                     ldc, M, N, Kc, p.kslice, cstride, X, sums, gate, gx, gy, ngroups)
+  if (bm == 64) {
+    if (vec) GLR_GEMM(64, 1, 4, true);
+    else GLR_GEMM(64, 1, 4, false);
+  } else {
+    if (vec) GLR_GEMM(128, 2, 2, true);
+    else GLR_GEMM(128, 2, 2, false);
+  }
+#undef GLR_GEMM
 }
 
 // out[i] = sum over splits of part[s * count + i], in a fixed order, fp64
