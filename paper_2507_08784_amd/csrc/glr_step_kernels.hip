@@ -109,7 +109,7 @@ hipError_t launch_ef_mean(const MatView& v, bool check_finite, hipStream_t s) {
 // ---------------------------------------------------------------------------
 constexpr int SEL_BM = 128, SEL_BN = 128;
 
-template <bool RIGHT, bool APPROX, bool BF16>
+template <bool RIGHT, bool APPROX, bool BF16, bool VEC = false>
 __device__ __forceinline__ void sel_scores_at(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d,
                                               int64_t D, float* __restrict__ part, uint32_t mat, uint32_t tstep,
                                               uint32_t key0, uint32_t key1, int bx, int by) {
@@ -119,14 +119,14 @@ __device__ __forceinline__ void sel_scores_at(const float* __restrict__ Mbar, co
   const int m0 = by * SEL_BM;   // rows: b in [0, D)
   const int n0 = bx * SEL_BN;   // cols: j in [0, d)
   T tile;
-  LoadK<SEL_BN, 32, false, false> lb(Ut, nullptr, d, n0, (int)d, (int)d, nullptr);
+  LoadK<SEL_BN, 32, false, false, float, VEC> lb(Ut, nullptr, d, n0, (int)d, (int)d, nullptr);
   if (RIGHT) {
     // Mo[a][b] = Mbar[b][a] : A[b][a] contiguous along a
-    LoadK<SEL_BM, 32, false, false> la(Mbar, nullptr, d, m0, (int)D, (int)d, nullptr);
+    LoadK<SEL_BM, 32, false, false, float, VEC> la(Mbar, nullptr, d, m0, (int)D, (int)d, nullptr);
     tile.template run<BF16>(la, lb, (int)d, smem);
   } else {
     // Mo[a][b] = Mbar[a][b] : A[b][a] contiguous along b
-    LoadR<SEL_BM, 32, false> la(Mbar, nullptr, D, m0, (int)D, (int)d);
+    LoadR<SEL_BM, 32, false, false, float, VEC> la(Mbar, nullptr, D, m0, (int)D, (int)d);
     tile.template run<BF16>(la, lb, (int)d, smem);
   }
   const int lane = lane_id();
@@ -166,11 +166,13 @@ __device__ __forceinline__ void sel_scores_at(const float* __restrict__ Mbar, co
     if (j < d) part[(int64_t)by * d + j] = red[0][threadIdx.x] + red[1][threadIdx.x];
   }
 }
-template <bool RIGHT, bool APPROX, bool BF16>
+// VEC: d and D multiples of 4 and both operands 16-byte aligned, so every
+// operand slice loads as whole float4s
+template <bool RIGHT, bool APPROX, bool BF16, bool VEC>
 __global__ void __launch_bounds__(256)
 k_sel_scores(const float* __restrict__ Mbar, const float* __restrict__ Ut, int64_t d, int64_t D,
              float* __restrict__ part, uint32_t mat, uint32_t tstep, uint32_t key0, uint32_t key1) {
-  sel_scores_at<RIGHT, APPROX, BF16>(Mbar, Ut, d, D, part, mat, tstep, key0, key1, blockIdx.x, blockIdx.y);
+  sel_scores_at<RIGHT, APPROX, BF16, VEC>(Mbar, Ut, d, D, part, mat, tstep, key0, key1, blockIdx.x, blockIdx.y);
 }
 
 // lambdabar / scores from the tile partials, summed in a fixed order
@@ -192,9 +194,16 @@ hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t 
   dim3 grid((unsigned)((v.d + SEL_BN - 1) / SEL_BN), (unsigned)((v.D + SEL_BM - 1) / SEL_BM));
   const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
   const uint32_t tt = (uint32_t)((uint64_t)t & 0xFFFFFFFFu);
-#define GLR_SEL(R, A, B)                                                                          \
-  hipLaunchKernelGGL((k_sel_scores<R, A, B>), grid, dim3(kThreads), 0, s, v.Mbar, v.Ut, v.d, v.D, \
+  const bool vec = v.d % 4 == 0 && v.D % 4 == 0 && (reinterpret_cast<uintptr_t>(v.Ut) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(v.Mbar) & 15) == 0;
+#define GLR_SEL1(R, A, B, VE)                                                                         \
+  hipLaunchKernelGGL((k_sel_scores<R, A, B, VE>), grid, dim3(kThreads), 0, s, v.Mbar, v.Ut, v.d, v.D, \
                      v.lam_part, (uint32_t)v.mat, tt, k0, k1)
+#define GLR_SEL(R, A, B)                       \
+  do {                                         \
+    if (vec) GLR_SEL1(R, A, B, true);          \
+    else GLR_SEL1(R, A, B, false);             \
+  } while (0)
   if (v.right) {
     if (bf16) GLR_SEL(true, true, true);
     else if (approx) GLR_SEL(true, true, false);
@@ -204,6 +213,7 @@ hipError_t launch_sel_scores(const MatView& v, bool approx, bool bf16, uint64_t 
     else if (approx) GLR_SEL(false, true, false);
     else GLR_SEL(false, false, false);
   }
+#undef GLR_SEL1
 #undef GLR_SEL
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
